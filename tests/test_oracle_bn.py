@@ -1,0 +1,199 @@
+"""Pins for the oracle's batch normalisation (Eq. 1-2 of Section 4.1, the
+0.25 multiplier of Section 4.2, local statistics of Section 5.1, and the
+ReLU that follows each BN, Section 1).
+"""
+
+from fractions import Fraction
+
+import numpy as np
+import pytest
+
+import oracle
+from exact import half_value, to_half_bits, to_single
+from paper_1911_07384_amd import synth
+
+EPS = 1e-5
+
+
+def _bn_inputs(n, c, h, w, layout, seed, grid=None):
+    shp = oracle.bn_shape(n, c, h, w, layout)
+    xs = (n, h, w, c) if layout == "NHWC" else (n, c, h, w)
+    x = synth.normal_f16(xs, 1.0, seed, 1, mean=0.3)
+    if grid is not None:  # values on a 2^-grid lattice, |x| < 4
+        x = (np.round(x.astype(np.float64) * 2 ** grid) / 2 ** grid).clip(-3.9, 3.9).astype(np.float16)
+    gamma = synth.normal_f16((c,), 0.5, seed, 2, mean=1.0)
+    beta = synth.normal_f16((c,), 0.5, seed, 3)
+    res = synth.normal_f16(xs, 1.0, seed, 4)
+    dy = synth.normal_f16(xs, 1.0, seed, 5)
+    return shp, x, gamma, beta, res, dy
+
+
+def _chan_view(a, layout):
+    """(C, M) view of an activation in either layout."""
+    if layout == "NHWC":
+        return np.moveaxis(a, -1, 0).reshape(a.shape[-1], -1)
+    return np.moveaxis(a, 1, 0).reshape(a.shape[1], -1)
+
+
+def test_worked_example():
+    # one channel, x = [1, 2, 3, 4]: mu = 2.5, var = 1.25 (biased),
+    # xhat = (x - 2.5) / sqrt(1.25 + 1e-5f) = [-1.34164, -0.44721, 0.44721, 1.34164];
+    # relu -> [0, 0, 0.44721, 1.34164]; nearest binary16: 0.447265625 (0x3728),
+    # 1.341796875 (0x3D5E); with the 0.25 multiplier: 0.11181640625 (0x2F28),
+    # 0.33544921875 (0x355E).
+    shp = oracle.bn_shape(1, 1, 1, 4, "NHWC")
+    x = np.array([1, 2, 3, 4], np.float16).reshape(1, 1, 4, 1)
+    g = np.array([1.0], np.float16)
+    b = np.array([0.0], np.float16)
+    r1 = oracle.bn_fwd(shp, x, g, b, eps=EPS, post_scale=1.0)
+    assert r1["mean"][0] == 2.5 and r1["var"][0] == 1.25
+    assert list(r1["y"].view(np.uint16).ravel()) == [0x0000, 0x0000, 0x3728, 0x3D5E]
+    r2 = oracle.bn_fwd(shp, x, g, b, eps=EPS, post_scale=0.25)
+    assert list(r2["y"].view(np.uint16).ravel()) == [0x0000, 0x0000, 0x2F28, 0x355E]
+
+
+@pytest.mark.parametrize("layout", ["NHWC", "NCHW"])
+def test_normalisation_invariants(layout):
+    shp, x, _, _, _, _ = _bn_inputs(3, 5, 4, 6, layout, 0)
+    one = np.ones(5, np.float16)
+    zero = np.zeros(5, np.float16)
+    r = oracle.bn_fwd(shp, x, one, zero, eps=EPS, relu=False)
+    xh = _chan_view(r["y64"], layout)
+    X = _chan_view(x.astype(np.float64), layout)
+    v = X.var(axis=1)
+    assert np.allclose(r["var"], v, rtol=1e-13, atol=0)
+    assert np.allclose(xh.mean(axis=1), 0.0, atol=1e-12)
+    eps = float(np.float32(EPS))
+    assert np.allclose((xh ** 2).mean(axis=1), v / (v + eps), rtol=1e-12, atol=0)
+
+
+def test_layouts_agree():
+    shp_h, x, g, b, res, _ = _bn_inputs(2, 4, 3, 5, "NHWC", 1)
+    shp_c = oracle.bn_shape(2, 4, 3, 5, "NCHW")
+    xc = np.ascontiguousarray(np.moveaxis(x, -1, 1))
+    rc = np.ascontiguousarray(np.moveaxis(res, -1, 1))
+    a = oracle.bn_fwd(shp_h, x, g, b, res, post_scale=0.25)
+    c = oracle.bn_fwd(shp_c, xc, g, b, rc, post_scale=0.25)
+    assert np.array_equal(np.moveaxis(a["y"], -1, 1).view(np.uint16), c["y"].view(np.uint16))
+
+
+def test_scale_and_residual_placement():
+    # y = relu(s * (gamma * xhat + beta) + r): with relu off, the residual
+    # enters after the multiplier and the multiplier scales gamma and beta.
+    shp, x, g, b, res, _ = _bn_inputs(2, 3, 4, 4, "NHWC", 2)
+    base = oracle.bn_fwd(shp, x, g, b, relu=False)["y64"]
+    scaled = oracle.bn_fwd(shp, x, g, b, post_scale=0.25, relu=False)["y64"]
+    withr = oracle.bn_fwd(shp, x, g, b, res, post_scale=0.25, relu=False)["y64"]
+    assert np.array_equal(scaled, 0.25 * base)  # exact: power-of-two scaling
+    assert np.allclose(withr - scaled, res.astype(np.float64), rtol=0, atol=1e-15)
+    relu = oracle.bn_fwd(shp, x, g, b, res, post_scale=0.25, relu=True)["y64"]
+    assert np.array_equal(relu, np.where(withr > 0, withr, 0.0))
+
+
+def _exact_apply(xb, gb, bb, rb, mean, rstd, s, relu):
+    """Exact-rational evaluation of the declared float32 apply sequence."""
+    F = Fraction
+    s = F(float(np.float32(s)))
+    a = to_single(to_single(s * half_value(gb)) * F(float(rstd)))
+    b = to_single(s * half_value(bb))
+    t = to_single(half_value(xb) - F(float(mean)))
+    v = to_single(t * a + b)
+    if rb is not None:
+        v = to_single(v + half_value(rb))
+    if relu and v <= 0:
+        return 0x0000
+    return to_half_bits(v)
+
+
+@pytest.mark.parametrize("with_res,relu,s", [(False, True, 1.0), (True, True, 0.25), (True, False, 0.25),
+                                            (False, False, 1.0)])
+def test_apply_f32_matches_exact(with_res, relu, s):
+    shp, x, g, b, res, _ = _bn_inputs(2, 3, 5, 4, "NHWC", 3)
+    st = oracle.bn_fwd(shp, x, g, b)
+    mean = st["mean"].astype(np.float32)
+    rstd = (1.0 / np.sqrt(st["var"] + float(np.float32(EPS)))).astype(np.float32)
+    y = oracle.bn_apply_f32(shp, x, g, b, mean, rstd, res if with_res else None, s, relu)
+    xb, yb, rb = x.view(np.uint16).reshape(-1, 3), y.view(np.uint16).reshape(-1, 3), \
+        res.view(np.uint16).reshape(-1, 3)
+    for j in range(xb.shape[0]):
+        for c in range(3):
+            want = _exact_apply(int(xb[j, c]), int(g.view(np.uint16)[c]), int(b.view(np.uint16)[c]),
+                                int(rb[j, c]) if with_res else None, mean[c], rstd[c], s, relu)
+            assert int(yb[j, c]) == want, (j, c)
+
+
+def test_apply_f32_close_to_float64_forward():
+    shp, x, g, b, res, _ = _bn_inputs(4, 8, 7, 7, "NHWC", 4)
+    st = oracle.bn_fwd(shp, x, g, b, res, post_scale=0.25)
+    mean = st["mean"].astype(np.float32)
+    rstd = (1.0 / np.sqrt(st["var"] + float(np.float32(EPS)))).astype(np.float32)
+    y = oracle.bn_apply_f32(shp, x, g, b, mean, rstd, res, 0.25, True)
+    a = st["y"].view(np.uint16).astype(np.int32)
+    c = y.view(np.uint16).astype(np.int32)
+    assert np.max(np.abs(a - c)) <= 1  # non-negative outputs: bit distance = ulp distance
+
+
+def _loss(shp, x, g, b, res, dy, s):
+    y64 = oracle.bn_fwd(shp, x, g, b, res, post_scale=s, relu=False)["y64"]
+    return float(np.sum(dy.astype(np.float64) * y64))
+
+
+@pytest.mark.parametrize("layout", ["NHWC", "NCHW"])
+def test_backward_finite_differences(layout):
+    s = 0.25
+    shp, x, g, b, res, dy = _bn_inputs(2, 3, 3, 3, layout, 6, grid=8)
+    g = (np.round(g.astype(np.float64) * 256) / 256).astype(np.float16)
+    b = (np.round(b.astype(np.float64) * 256) / 256).astype(np.float16)
+    r = oracle.bn_bwd(shp, x, None, dy, g, post_scale=s, relu=False, want_dres=True)
+    h = 2.0 ** -8
+    flat = x.reshape(-1)
+    fd = np.empty(flat.size)
+    for i in range(flat.size):
+        xp, xm = flat.copy(), flat.copy()
+        xp[i] = np.float16(float(flat[i]) + h)
+        xm[i] = np.float16(float(flat[i]) - h)
+        assert float(xp[i]) - float(flat[i]) == h and float(flat[i]) - float(xm[i]) == h
+        fd[i] = (_loss(shp, xp.reshape(x.shape), g, b, res, dy, s)
+                 - _loss(shp, xm.reshape(x.shape), g, b, res, dy, s)) / (2 * h)
+    an = r["dx64"].reshape(-1)
+    assert np.max(np.abs(fd - an)) <= 2e-4 * np.max(np.abs(an))
+    for name, arr in (("dgamma64", g), ("dbeta64", b)):
+        for c in range(3):
+            ap, am = arr.copy(), arr.copy()
+            ap[c] = np.float16(float(arr[c]) + h)
+            am[c] = np.float16(float(arr[c]) - h)
+            args_p = (ap, b) if name == "dgamma64" else (g, ap)
+            args_m = (am, b) if name == "dgamma64" else (g, am)
+            fdc = (_loss(shp, x, *args_p, res, dy, s) - _loss(shp, x, *args_m, res, dy, s)) / (2 * h)
+            assert abs(fdc - r[name][c]) <= 1e-9 * max(1.0, abs(fdc))
+    # the shortcut gradient passes dy through unchanged (relu off)
+    assert np.array_equal(r["dres"].view(np.uint16), dy.view(np.uint16))
+
+
+def test_backward_invariants():
+    shp, x, g, b, _, dy = _bn_inputs(3, 4, 5, 5, "NHWC", 7)
+    r = oracle.bn_bwd(shp, x, None, dy, g, post_scale=1.0, relu=False)
+    one = np.ones(4, np.float16)
+    xh = _chan_view(oracle.bn_fwd(shp, x, one, np.zeros(4, np.float16), relu=False)["y64"], "NHWC")
+    dx = _chan_view(r["dx64"], "NHWC")
+    scale = np.abs(dx).max()
+    assert np.allclose(dx.sum(axis=1), 0.0, atol=1e-12 * scale * dx.shape[1])
+    # sum dx * xhat = gamma * rstd * (S2 - S2 * mean(xhat^2)) = gamma * rstd * S2 * eps / (var + eps)
+    st = oracle.bn_fwd(shp, x, one, np.zeros(4, np.float16), relu=False)
+    eps = float(np.float32(EPS))
+    rstd = 1.0 / np.sqrt(st["var"] + eps)
+    want = g.astype(np.float64) * rstd * r["dgamma64"] * eps / (st["var"] + eps)
+    assert np.allclose((dx * xh).sum(axis=1), want, rtol=1e-9, atol=1e-12 * scale * dx.shape[1])
+    assert np.max(np.abs(want)) > 1e-6  # the identity is not vacuous here
+
+
+def test_backward_relu_mask_is_masked_gradient():
+    shp, x, g, b, res, dy = _bn_inputs(2, 4, 6, 5, "NHWC", 8)
+    y = oracle.bn_fwd(shp, x, g, b, res, post_scale=0.25)["y"]
+    r1 = oracle.bn_bwd(shp, x, y, dy, g, post_scale=0.25, relu=True, want_dres=True)
+    masked = np.where(y.astype(np.float64) > 0, dy, np.float16(0)).astype(np.float16)
+    r0 = oracle.bn_bwd(shp, x, None, masked, g, post_scale=0.25, relu=False, want_dres=True)
+    assert np.array_equal(r1["dx64"], r0["dx64"])
+    assert np.array_equal(r1["dgamma"].view(np.uint16), r0["dgamma"].view(np.uint16))
+    assert np.array_equal(r1["dres"].astype(np.float64), masked.astype(np.float64))
+    assert 0.2 < np.mean(y.astype(np.float64) > 0) < 0.8
