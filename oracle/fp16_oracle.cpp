@@ -430,7 +430,8 @@ void oracle_bn_apply_f32(const int32_t* shp, const uint16_t* x16, const uint16_t
 //   g = s * dy * mask  (gradient reaching z = gamma * xhat + beta);
 //   S1 = sum g;  S2 = sum g * xhat;  dbeta = S1;  dgamma = S2;
 //   dx = gamma * rstd * (g - S1 / M - xhat * S2 / M);
-//   dr = dy * mask  (gradient to the identity shortcut, if requested).
+//   dr = dy where mask is 1, +0 elsewhere (gradient to the identity shortcut,
+//        if requested; ReLU passes the gradient only where its output is positive).
 // Each output is rounded once to binary16.  The 64-bit outputs may be NULL.
 
 void oracle_bn_bwd(const int32_t* shp, const uint16_t* x16, const uint16_t* y16,
@@ -468,7 +469,7 @@ void oracle_bn_bwd(const int32_t* shp, const uint16_t* x16, const uint16_t* y16,
       const double v = gam * rstd * (g - S1 / (double)M - xhat * S2 / (double)M);
       if (dx64) dx64[i] = v;
       if (dx16) dx16[i] = round_half(v);
-      if (dres16) dres16[i] = round_half(half_to_double(dy16[i]) * mask);
+      if (dres16) dres16[i] = mask > 0.0 ? dy16[i] : (uint16_t)0x0000;
     }
     if (dgamma64) dgamma64[c] = S2;
     if (dbeta64) dbeta64[c] = S1;

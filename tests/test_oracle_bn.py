@@ -195,5 +195,6 @@ def test_backward_relu_mask_is_masked_gradient():
     r0 = oracle.bn_bwd(shp, x, None, masked, g, post_scale=0.25, relu=False, want_dres=True)
     assert np.array_equal(r1["dx64"], r0["dx64"])
     assert np.array_equal(r1["dgamma"].view(np.uint16), r0["dgamma"].view(np.uint16))
-    assert np.array_equal(r1["dres"].astype(np.float64), masked.astype(np.float64))
+    want = np.where(y.astype(np.float64) > 0, dy.view(np.uint16), np.uint16(0))
+    assert np.array_equal(r1["dres"].view(np.uint16), want)
     assert 0.2 < np.mean(y.astype(np.float64) > 0) < 0.8
