@@ -1,0 +1,176 @@
+/*
+ * fp16train: the all-FP16 training hot path of arXiv:1911.07384,
+ * "Distributed low-precision Training Without Mixed Precision", for AMD
+ * MI355X (gfx950).
+ *
+ * Every tensor that crosses this interface is IEEE binary16 (Section 5.2:
+ * activations, weights and gradients are all stored in FP16 and no master
+ * copy is kept in higher precision).  Inside a kernel, products are formed
+ * exactly and accumulated in float32 (matrix cores) and every result is
+ * rounded once to binary16, to nearest with ties to even, at its store
+ * (Section 4.2 leaves the rounding method open; this library uses the IEEE
+ * default).  Binary16 subnormals are kept (gradual underflow) and overflow
+ * rounds to +-infinity.
+ *
+ * Conventions shared by every entry point:
+ *   - Buffers are device pointers owned by the caller.  The library never
+ *     allocates or frees device memory and keeps no state between calls.
+ *     Any scratch memory a call needs is the caller's workspace, sized by
+ *     the matching *_workspace_bytes query.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL is the default
+ *     stream) and the call returns without waiting for it.
+ *   - Arguments are checked before anything is enqueued: a nonzero status
+ *     means nothing was launched.  FP16_ERR_HIP reports a failed launch.
+ *     Faults inside kernels surface at the caller's next synchronisation.
+ *   - Activation, filter, workspace and parameter pointers must be 16-byte
+ *     aligned (FP16_ERR_MISALIGNED otherwise).
+ *   - Results are deterministic: the same inputs give the same bits on
+ *     every run (no floating-point atomics).
+ *   - Layout FP16_NHWC: activations [N][H][W][C], filters [K][R][S][C].
+ *     Layout FP16_NCHW: activations [N][C][H][W], filters [K][C][R][S].
+ *     NHWC is the native layout; NCHW calls convert through the workspace.
+ */
+#ifndef FP16TRAIN_H
+#define FP16TRAIN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef uint16_t fp16_t;      /* IEEE binary16 bit pattern */
+typedef void* fp16_stream_t;  /* hipStream_t */
+
+typedef enum {
+  FP16_OK = 0,
+  FP16_ERR_NULL = 1,        /* a required pointer is NULL */
+  FP16_ERR_SHAPE = 2,       /* a dimension is out of range or inconsistent */
+  FP16_ERR_LAYOUT = 3,      /* unknown layout value */
+  FP16_ERR_MISALIGNED = 4,  /* a pointer is not 16-byte aligned */
+  FP16_ERR_ALIASING = 5,    /* an output overlaps an input it must not */
+  FP16_ERR_WORKSPACE = 6,   /* workspace missing or smaller than required */
+  FP16_ERR_UNSUPPORTED = 7, /* valid request outside what is implemented */
+  FP16_ERR_HIP = 8          /* the HIP runtime reported an error */
+} fp16_status;
+
+typedef enum { FP16_NHWC = 0, FP16_NCHW = 1 } fp16_layout;
+
+typedef enum { FP16_PASS_FWD = 0, FP16_PASS_DGRAD = 1, FP16_PASS_WGRAD = 2 } fp16_conv_pass;
+
+/* Convolution problem: input x [N,C,H,W] (logical), filter W [K,C,R,S],
+ * output y [N,K,P,Q] with P = (H + 2*pad_h - R)/stride_h + 1 and
+ * Q = (W + 2*pad_w - S)/stride_w + 1.  Cross-correlation, zero padding,
+ * no dilation, one group.  All dimensions >= 1, pads >= 0, P, Q >= 1. */
+typedef struct {
+  int32_t n, c, h, w;
+  int32_t k, r, s;
+  int32_t stride_h, stride_w;
+  int32_t pad_h, pad_w;
+  int32_t layout; /* fp16_layout */
+} fp16_conv_desc;
+
+/* Batch normalisation problem on x [N,C,H,W] (logical). */
+typedef struct {
+  int32_t n, c, h, w;
+  int32_t layout;     /* fp16_layout */
+  float eps;          /* added to the variance, held in float32 */
+  float post_scale;   /* output multiplier s: 0.25 inside residual blocks, 1 for the stem */
+  int32_t relu;       /* 1: apply ReLU to the output; 0: no ReLU */
+  int32_t use_stats;  /* 0: compute batch statistics from x and write them to `stats`;
+                         1: read mean and rstd from `stats` and only apply */
+} fp16_bn_desc;
+
+/* Output spatial size of a convolution; FP16_ERR_SHAPE if it is empty. */
+fp16_status fp16_conv_out_dims(const fp16_conv_desc* desc, int32_t* p, int32_t* q);
+
+/* Bytes of workspace a convolution pass needs (0 when it needs none).
+ * Returns 0 for an invalid descriptor as well; the pass call reports it. */
+size_t fp16_conv_workspace_bytes(const fp16_conv_desc* desc, int32_t pass);
+
+/* Forward convolution (ResNet-50's convolutions, Section 5.1):
+ *   y[n,k,p,q] = sum_{c,r,s} x[n,c, p*stride_h - pad_h + r, q*stride_w - pad_w + s] * W[k,c,r,s]
+ * with out-of-image taps reading zero.  Accumulation in float32, one
+ * rounding to binary16 per output.  y must not overlap x, w or ws. */
+fp16_status fp16_conv_fwd(const fp16_conv_desc* desc, const fp16_t* x, const fp16_t* w, fp16_t* y,
+                          void* ws, size_t ws_bytes, fp16_stream_t stream);
+
+/* Data gradient (back-propagation through the convolution; the adjoint of
+ * fp16_conv_fwd in x):
+ *   dx[n,c,h,w] = sum over (k,r,s) with h + pad_h - r = p*stride_h and
+ *                 w + pad_w - s = q*stride_w, (p,q) inside the P x Q grid, of dy[n,k,p,q] * W[k,c,r,s].
+ * Every element of dx is written (positions no tap reaches get zero).
+ * dx must not overlap dy, w or ws. */
+fp16_status fp16_conv_dgrad(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* w,
+                            fp16_t* dx, void* ws, size_t ws_bytes, fp16_stream_t stream);
+
+/* Weight gradient (the adjoint of fp16_conv_fwd in W):
+ *   dW[k,c,r,s] = sum_{n,p,q} dy[n,k,p,q] * x[n,c, p*stride_h - pad_h + r, q*stride_w - pad_w + s].
+ * Partial sums over pixel ranges stay float32 in the workspace and are
+ * added in a fixed order before the single rounding.  dw must not overlap
+ * x, dy or ws. */
+fp16_status fp16_conv_wgrad(const fp16_conv_desc* desc, const fp16_t* x, const fp16_t* dy,
+                            fp16_t* dw, void* ws, size_t ws_bytes, fp16_stream_t stream);
+
+/* Bytes of workspace the BN forward or backward call needs. */
+size_t fp16_bn_workspace_bytes(const fp16_bn_desc* desc);
+
+/* BN forward fused with the output multiplier, the identity shortcut and
+ * ReLU (Eq. 1-2 of Section 4.1; the 0.25 multiplier after each BN inside a
+ * residual block and the unchanged stem BN of Section 4.2; statistics over
+ * this GPU's batch only, Section 5.1):
+ *   mean_c, var_c over the M = N*H*W elements of channel c (biased variance);
+ *   rstd_c = 1 / sqrt(var_c + eps);
+ *   y = relu( s * (gamma_c * (x - mean_c) * rstd_c + beta_c) + r ).
+ * With use_stats = 0, mean and rstd (float32) are computed in this call and
+ * written to stats[0..C) and stats[C..2C).  With use_stats = 1 they are read
+ * from stats.  The apply step is the float32 sequence
+ *   a = fl(fl(s*gamma)*rstd); b = fl(s*beta); t = fl(x - mean);
+ *   v = fma(t, a, b); v = fl(v + r); y = round_to_binary16(relu(v)),
+ * so given statistics determine y bit for bit.  residual may be NULL.
+ * y may equal x (in place); y must not overlap gamma, beta, stats or ws. */
+fp16_status fp16_bn_relu(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t* gamma,
+                         const fp16_t* beta, const fp16_t* residual, fp16_t* y, float* stats,
+                         void* ws, size_t ws_bytes, fp16_stream_t stream);
+
+/* BN backward through the same fused forward (not one of the paper's named
+ * operations, but what training through Eq. 1-2 requires):
+ *   mask = [y > 0] (all ones without ReLU);  g = s * dy * mask;
+ *   S1_c = sum g;  S2_c = sum g * xhat,  xhat = (x - mean_c) * rstd_c;
+ *   dbeta_c = S1_c;  dgamma_c = S2_c;
+ *   dx = gamma_c * rstd_c * (g - S1_c/M - xhat * S2_c/M);
+ *   dresidual = mask ? dy : 0  (the gradient reaching the identity shortcut).
+ * stats holds the forward's mean and rstd (float32, 2C values).  y is the
+ * forward output; it may be NULL, in which case the mask is recomputed from
+ * x, gamma, beta, residual and stats by the forward's float32 apply
+ * sequence (bit-identical to what the forward stored).  dresidual may be
+ * NULL.  dx may equal dy (in place). */
+fp16_status fp16_bn_relu_bwd(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t* y,
+                             const fp16_t* dy, const fp16_t* gamma, const fp16_t* beta,
+                             const fp16_t* residual, const float* stats, fp16_t* dx,
+                             fp16_t* dgamma, fp16_t* dbeta, fp16_t* dresidual, void* ws,
+                             size_t ws_bytes, fp16_stream_t stream);
+
+/* Momentum SGD on FP16 weights and an FP16 momentum buffer, with no master
+ * copy (Section 5.1 recipe: PyTorch SGD, dampening 0, no Nesterov;
+ * Section 5.2), in place over n elements:
+ *   d = fma(weight_decay, w, g);  m = round_to_binary16(fma(momentum, m, d));
+ *   w = round_to_binary16(fma(-lr, m, w))
+ * evaluated in float32 exactly as written, so results are unique bit
+ * patterns.  BN parameters take weight_decay = 0 (Section 5.1).  g must not
+ * overlap w or m; w and m must not overlap each other.  n = 0 is a no-op. */
+fp16_status fp16_sgd_step(fp16_t* w, const fp16_t* g, fp16_t* m, size_t n, float lr,
+                          float momentum, float weight_decay, fp16_stream_t stream);
+
+/* Human-readable name of a status code (static string). */
+const char* fp16_status_string(fp16_status status);
+
+/* Library version, e.g. "fp16train 0.1". */
+const char* fp16_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FP16TRAIN_H */

@@ -1,0 +1,209 @@
+"""paper_1911_07384_amd: the all-FP16 training hot path of arXiv:1911.07384
+("Distributed low-precision Training Without Mixed Precision") on MI355X.
+
+This module is a thin ctypes binding over ``libfp16train.so``, whose C ABI is
+declared in ``include/fp16train.h``.  Functions carry the same names as the
+C entry points and only marshal arguments: torch tensors (float16, CUDA/HIP
+device, contiguous) are passed as raw device pointers, and work is enqueued
+on the current torch stream unless another stream is given.  Every step of
+the computation runs in the HIP kernels; there is no fallback path.  A
+nonzero status raises ``Fp16Error``.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfp16train.so")
+
+FP16_NHWC = 0
+FP16_NCHW = 1
+PASS_FWD, PASS_DGRAD, PASS_WGRAD = 0, 1, 2
+_LAYOUTS = {"NHWC": FP16_NHWC, "NCHW": FP16_NCHW, FP16_NHWC: FP16_NHWC, FP16_NCHW: FP16_NCHW}
+
+STATUS = {0: "FP16_OK", 1: "FP16_ERR_NULL", 2: "FP16_ERR_SHAPE", 3: "FP16_ERR_LAYOUT",
+          4: "FP16_ERR_MISALIGNED", 5: "FP16_ERR_ALIASING", 6: "FP16_ERR_WORKSPACE",
+          7: "FP16_ERR_UNSUPPORTED", 8: "FP16_ERR_HIP"}
+
+EXPORTS = ["fp16_conv_out_dims", "fp16_conv_workspace_bytes", "fp16_conv_fwd", "fp16_conv_dgrad",
+           "fp16_conv_wgrad", "fp16_bn_workspace_bytes", "fp16_bn_relu", "fp16_bn_relu_bwd",
+           "fp16_sgd_step", "fp16_status_string", "fp16_version"]
+
+
+class Fp16Error(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn}: {STATUS.get(status, status)} ({_status_string(status)})")
+
+
+class ConvDesc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("n", "c", "h", "w", "k", "r", "s", "stride_h", "stride_w", "pad_h", "pad_w",
+                 "layout")]
+
+
+class BnDesc(ctypes.Structure):
+    _fields_ = [("n", ctypes.c_int32), ("c", ctypes.c_int32), ("h", ctypes.c_int32),
+                ("w", ctypes.c_int32), ("layout", ctypes.c_int32), ("eps", ctypes.c_float),
+                ("post_scale", ctypes.c_float), ("relu", ctypes.c_int32),
+                ("use_stats", ctypes.c_int32)]
+
+
+_lib = None
+_P = ctypes.c_void_p
+_SZ = ctypes.c_size_t
+_F = ctypes.c_float
+_I32 = ctypes.c_int32
+_SIGS = {
+    "fp16_conv_out_dims": (ctypes.c_int, [_P, _P, _P]),
+    "fp16_conv_workspace_bytes": (_SZ, [_P, _I32]),
+    "fp16_conv_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _SZ, _P]),
+    "fp16_conv_dgrad": (ctypes.c_int, [_P, _P, _P, _P, _P, _SZ, _P]),
+    "fp16_conv_wgrad": (ctypes.c_int, [_P, _P, _P, _P, _P, _SZ, _P]),
+    "fp16_bn_workspace_bytes": (_SZ, [_P]),
+    "fp16_bn_relu": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "fp16_bn_relu_bwd": (ctypes.c_int, [_P] * 13 + [_SZ, _P]),
+    "fp16_sgd_step": (ctypes.c_int, [_P, _P, _P, _SZ, _F, _F, _F, _P]),
+    "fp16_status_string": (ctypes.c_char_p, [ctypes.c_int]),
+    "fp16_version": (ctypes.c_char_p, []),
+}
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded HIP library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -c 'import "
+                               f"__graft_entry__ as g; g.build()'` (no fallback path exists)")
+        l = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            f = getattr(l, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = l
+    return _lib
+
+
+def _status_string(status: int) -> str:
+    try:
+        return lib().fp16_status_string(int(status)).decode()
+    except Exception:  # pragma: no cover - only when the library cannot load
+        return "?"
+
+
+def _check(fn: str, status: int) -> None:
+    if status != 0:
+        raise Fp16Error(fn, status)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    import torch
+    if t.dtype not in (torch.float16, torch.float32, torch.uint8):
+        raise TypeError(f"expected float16/float32/uint8 tensor, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError("tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def conv_desc(n, c, h, w, k, r, s, stride=1, pad=0, layout="NHWC") -> ConvDesc:
+    sh, sw = (stride, stride) if isinstance(stride, int) else stride
+    ph, pw = (pad, pad) if isinstance(pad, int) else pad
+    return ConvDesc(n, c, h, w, k, r, s, sh, sw, ph, pw, _LAYOUTS[layout])
+
+
+def bn_desc(n, c, h, w, layout="NHWC", eps=1e-5, post_scale=1.0, relu=True, use_stats=False) -> BnDesc:
+    return BnDesc(n, c, h, w, _LAYOUTS[layout], eps, post_scale, int(bool(relu)), int(bool(use_stats)))
+
+
+# ---- C entry points, same names --------------------------------------------
+
+def fp16_version() -> str:
+    return lib().fp16_version().decode()
+
+
+def fp16_status_string(status: int) -> str:
+    return lib().fp16_status_string(int(status)).decode()
+
+
+def fp16_conv_out_dims(desc: ConvDesc):
+    p, q = ctypes.c_int32(), ctypes.c_int32()
+    _check("fp16_conv_out_dims", lib().fp16_conv_out_dims(ctypes.byref(desc), ctypes.byref(p),
+                                                          ctypes.byref(q)))
+    return p.value, q.value
+
+
+def fp16_conv_workspace_bytes(desc: ConvDesc, pass_: int) -> int:
+    return int(lib().fp16_conv_workspace_bytes(ctypes.byref(desc), int(pass_)))
+
+
+def fp16_conv_fwd(desc, x, w, y, ws=None, ws_bytes=None, stream=None) -> None:
+    _check("fp16_conv_fwd", lib().fp16_conv_fwd(ctypes.byref(desc), _ptr(x), _ptr(w), _ptr(y),
+                                                _ptr(ws), _wsb(ws, ws_bytes), _stream(stream)))
+
+
+def fp16_conv_dgrad(desc, dy, w, dx, ws=None, ws_bytes=None, stream=None) -> None:
+    _check("fp16_conv_dgrad", lib().fp16_conv_dgrad(ctypes.byref(desc), _ptr(dy), _ptr(w), _ptr(dx),
+                                                    _ptr(ws), _wsb(ws, ws_bytes), _stream(stream)))
+
+
+def fp16_conv_wgrad(desc, x, dy, dw, ws=None, ws_bytes=None, stream=None) -> None:
+    _check("fp16_conv_wgrad", lib().fp16_conv_wgrad(ctypes.byref(desc), _ptr(x), _ptr(dy), _ptr(dw),
+                                                    _ptr(ws), _wsb(ws, ws_bytes), _stream(stream)))
+
+
+def fp16_bn_workspace_bytes(desc: BnDesc) -> int:
+    return int(lib().fp16_bn_workspace_bytes(ctypes.byref(desc)))
+
+
+def fp16_bn_relu(desc, x, gamma, beta, residual, y, stats, ws=None, ws_bytes=None,
+                 stream=None) -> None:
+    _check("fp16_bn_relu", lib().fp16_bn_relu(ctypes.byref(desc), _ptr(x), _ptr(gamma), _ptr(beta),
+                                              _ptr(residual), _ptr(y), _ptr(stats), _ptr(ws),
+                                              _wsb(ws, ws_bytes), _stream(stream)))
+
+
+def fp16_bn_relu_bwd(desc, x, y, dy, gamma, beta, residual, stats, dx, dgamma, dbeta, dresidual,
+                     ws=None, ws_bytes=None, stream=None) -> None:
+    _check("fp16_bn_relu_bwd", lib().fp16_bn_relu_bwd(
+        ctypes.byref(desc), _ptr(x), _ptr(y), _ptr(dy), _ptr(gamma), _ptr(beta), _ptr(residual),
+        _ptr(stats), _ptr(dx), _ptr(dgamma), _ptr(dbeta), _ptr(dresidual), _ptr(ws),
+        _wsb(ws, ws_bytes), _stream(stream)))
+
+
+def fp16_sgd_step(w, g, m, n=None, lr=0.1, momentum=0.9, weight_decay=1e-4, stream=None) -> None:
+    if n is None:
+        n = w.numel()
+    _check("fp16_sgd_step", lib().fp16_sgd_step(_ptr(w), _ptr(g), _ptr(m), int(n), float(lr),
+                                                float(momentum), float(weight_decay),
+                                                _stream(stream)))
+
+
+def _wsb(ws, ws_bytes):
+    if ws_bytes is not None:
+        return int(ws_bytes)
+    if ws is None or isinstance(ws, int):
+        return 0
+    return ws.numel() * ws.element_size()
+
+
+# ---- conveniences that allocate outputs and workspaces with torch -----------
+
+def workspace(nbytes: int, device="cuda"):
+    import torch
+    return torch.empty(max(int(nbytes), 16), dtype=torch.uint8, device=device)

@@ -1,0 +1,404 @@
+// C ABI of fp16train: argument validation, workspace planning and dispatch
+// to the HIP kernels.  Nothing here allocates device memory; every call is
+// enqueued on the caller's stream.
+
+#include "../../include/fp16train.h"
+#include "kernels.hpp"
+
+#include <stdint.h>
+
+using namespace fp16k;
+
+namespace {
+
+constexpr int64_t kMaxElems = (int64_t)1 << 31;  // int32 indexing inside the kernels
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  const uintptr_t pa = (uintptr_t)a, pb = (uintptr_t)b;
+  return pa < pb + nb && pb < pa + na;
+}
+
+int round8(int v) { return (v + 7) / 8 * 8; }
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+struct ConvDims {
+  int N, C, H, W, K, R, S, sh, sw, ph, pw, P, Q, layout, Cp, Kp;
+  int64_t x_elems, y_elems, w_elems;
+};
+
+fp16_status check_conv(const fp16_conv_desc* d, ConvDims* o) {
+  if (!d) return FP16_ERR_NULL;
+  if (d->layout != FP16_NHWC && d->layout != FP16_NCHW) return FP16_ERR_LAYOUT;
+  if (d->n < 1 || d->c < 1 || d->h < 1 || d->w < 1 || d->k < 1 || d->r < 1 || d->s < 1 ||
+      d->stride_h < 1 || d->stride_w < 1 || d->pad_h < 0 || d->pad_w < 0)
+    return FP16_ERR_SHAPE;
+  if (d->r > 64 || d->s > 64 || d->stride_h > 64 || d->stride_w > 64 || d->pad_h > 64 ||
+      d->pad_w > 64 || d->c > 65535 || d->k > 65535 || d->h > 65535 || d->w > 65535)
+    return FP16_ERR_SHAPE;
+  if (d->h + 2 * d->pad_h < d->r || d->w + 2 * d->pad_w < d->s) return FP16_ERR_SHAPE;
+  o->N = d->n; o->C = d->c; o->H = d->h; o->W = d->w; o->K = d->k; o->R = d->r; o->S = d->s;
+  o->sh = d->stride_h; o->sw = d->stride_w; o->ph = d->pad_h; o->pw = d->pad_w;
+  o->layout = d->layout;
+  o->P = (o->H + 2 * o->ph - o->R) / o->sh + 1;
+  o->Q = (o->W + 2 * o->pw - o->S) / o->sw + 1;
+  o->Cp = round8(o->C);
+  o->Kp = round8(o->K);
+  o->x_elems = (int64_t)o->N * o->C * o->H * o->W;
+  o->y_elems = (int64_t)o->N * o->K * o->P * o->Q;
+  o->w_elems = (int64_t)o->K * o->C * o->R * o->S;
+  const int64_t xp = (int64_t)o->N * o->Cp * o->H * o->W;
+  const int64_t yp = (int64_t)o->N * o->Kp * o->P * o->Q;
+  const int64_t wp = (int64_t)o->Kp * o->Cp * o->R * o->S;
+  if (xp >= kMaxElems || yp >= kMaxElems || wp >= kMaxElems) return FP16_ERR_SHAPE;
+  return FP16_OK;
+}
+
+// Workspace regions of one convolution pass (byte offsets, 256-aligned).
+struct ConvWs {
+  size_t x = 0, w = 0, y = 0, wf = 0, part = 0, total = 0;
+  bool need_x = false, need_w = false, need_y = false;
+  int splits = 0, pps = 0;
+};
+
+ConvWs conv_ws(const ConvDims& d, int pass) {
+  ConvWs L;
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off += align256(bytes);
+    return at;
+  };
+  const bool nchw = d.layout == FP16_NCHW;
+  if (pass == FP16_PASS_FWD) {
+    if (nchw || d.Cp != d.C) {
+      L.need_x = L.need_w = true;
+      L.x = take((size_t)d.N * d.H * d.W * d.Cp * 2);
+      L.w = take((size_t)d.K * d.R * d.S * d.Cp * 2);
+    }
+    if (nchw) {
+      L.need_y = true;
+      L.y = take((size_t)d.N * d.P * d.Q * d.K * 2);
+    }
+  } else if (pass == FP16_PASS_DGRAD) {
+    if (nchw || d.Kp != d.K) {  // dy as NHWC with Kp channels
+      L.need_y = true;
+      L.y = take((size_t)d.N * d.P * d.Q * d.Kp * 2);
+    }
+    if (nchw) {  // filter KCRS -> KRSC, and dx staged as NHWC
+      L.need_w = true;
+      L.w = take((size_t)d.K * d.R * d.S * d.C * 2);
+      L.need_x = true;
+      L.x = take((size_t)d.N * d.H * d.W * d.C * 2);
+    }
+    L.wf = take((size_t)d.C * d.R * d.S * d.Kp * 2);
+  } else {
+    if (nchw || d.Cp != d.C) {
+      L.need_x = true;
+      L.x = take((size_t)d.N * d.H * d.W * d.Cp * 2);
+    }
+    if (nchw || d.Kp != d.K) {
+      L.need_y = true;
+      L.y = take((size_t)d.N * d.P * d.Q * d.Kp * 2);
+    }
+    wgrad_plan(d.Kp, d.Cp, d.R, d.S, (int64_t)d.N * d.P * d.Q, &L.splits, &L.pps);
+    L.part = take((size_t)L.splits * d.Kp * d.R * d.S * d.Cp * 4);
+  }
+  L.total = off;
+  return L;
+}
+
+fp16_status hip_status(hipError_t e) { return e == hipSuccess ? FP16_OK : FP16_ERR_HIP; }
+
+#define TRY(expr)                                  \
+  do {                                             \
+    const hipError_t e_ = (expr);                  \
+    if (e_ != hipSuccess) return FP16_ERR_HIP;     \
+  } while (0)
+
+fp16_status check_ws(const ConvWs& L, const void* ws, size_t ws_bytes) {
+  if (L.total == 0) return FP16_OK;
+  if (!ws || ws_bytes < L.total) return FP16_ERR_WORKSPACE;
+  if (!aligned16(ws)) return FP16_ERR_MISALIGNED;
+  return FP16_OK;
+}
+
+h16* wsp(void* ws, size_t off) { return reinterpret_cast<h16*>(static_cast<char*>(ws) + off); }
+
+}  // namespace
+
+extern "C" {
+
+const char* fp16_status_string(fp16_status s) {
+  switch (s) {
+    case FP16_OK: return "ok";
+    case FP16_ERR_NULL: return "null pointer";
+    case FP16_ERR_SHAPE: return "invalid shape";
+    case FP16_ERR_LAYOUT: return "invalid layout";
+    case FP16_ERR_MISALIGNED: return "pointer not 16-byte aligned";
+    case FP16_ERR_ALIASING: return "output overlaps an input";
+    case FP16_ERR_WORKSPACE: return "workspace missing or too small";
+    case FP16_ERR_UNSUPPORTED: return "unsupported";
+    case FP16_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* fp16_version(void) { return "fp16train 0.1"; }
+
+fp16_status fp16_conv_out_dims(const fp16_conv_desc* desc, int32_t* p, int32_t* q) {
+  ConvDims d;
+  const fp16_status s = check_conv(desc, &d);
+  if (s != FP16_OK) return s;
+  if (!p || !q) return FP16_ERR_NULL;
+  *p = d.P;
+  *q = d.Q;
+  return FP16_OK;
+}
+
+size_t fp16_conv_workspace_bytes(const fp16_conv_desc* desc, int32_t pass) {
+  ConvDims d;
+  if (check_conv(desc, &d) != FP16_OK) return 0;
+  if (pass < FP16_PASS_FWD || pass > FP16_PASS_WGRAD) return 0;
+  return conv_ws(d, pass).total;
+}
+
+fp16_status fp16_conv_fwd(const fp16_conv_desc* desc, const fp16_t* x, const fp16_t* w, fp16_t* y,
+                          void* ws, size_t ws_bytes, fp16_stream_t stream) {
+  ConvDims d;
+  fp16_status s = check_conv(desc, &d);
+  if (s != FP16_OK) return s;
+  if (!x || !w || !y) return FP16_ERR_NULL;
+  if (!aligned16(x) || !aligned16(w) || !aligned16(y)) return FP16_ERR_MISALIGNED;
+  const ConvWs L = conv_ws(d, FP16_PASS_FWD);
+  if ((s = check_ws(L, ws, ws_bytes)) != FP16_OK) return s;
+  const size_t yb = (size_t)d.y_elems * 2;
+  if (overlap(y, yb, x, (size_t)d.x_elems * 2) || overlap(y, yb, w, (size_t)d.w_elems * 2) ||
+      overlap(y, yb, ws, L.total))
+    return FP16_ERR_ALIASING;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const h16* xe = reinterpret_cast<const h16*>(x);
+  const h16* we = reinterpret_cast<const h16*>(w);
+  h16* ye = reinterpret_cast<h16*>(y);
+  if (d.layout == FP16_NCHW) {
+    TRY(launch_nchw_to_nhwc(xe, wsp(ws, L.x), d.N, d.C, d.H * d.W, d.Cp, st));
+    TRY(launch_nchw_to_nhwc(we, wsp(ws, L.w), d.K, d.C, d.R * d.S, d.Cp, st));
+    xe = wsp(ws, L.x);
+    we = wsp(ws, L.w);
+    ye = wsp(ws, L.y);
+  } else if (d.Cp != d.C) {
+    TRY(launch_pad_channels(xe, wsp(ws, L.x), (int64_t)d.N * d.H * d.W, d.C, d.Cp, st));
+    TRY(launch_pad_channels(we, wsp(ws, L.w), (int64_t)d.K * d.R * d.S, d.C, d.Cp, st));
+    xe = wsp(ws, L.x);
+    we = wsp(ws, L.w);
+  }
+  IgemmArgs a{};
+  a.act = xe; a.N = d.N; a.Hi = d.H; a.Wi = d.W; a.Ci = d.Cp;
+  a.stride_h = d.sh; a.stride_w = d.sw;
+  a.Co = d.K; a.out = ye; a.OH = d.P; a.OW = d.Q; a.ldo = d.K; a.os_h = 1; a.os_w = 1;
+  a.nphase = 1;
+  a.ph[0] = IgemmPhase{we, d.R * d.S * d.Cp, d.R, d.S, d.ph, d.pw, d.P, d.Q, 0, 0};
+  TRY(launch_igemm(a, st));
+  if (d.layout == FP16_NCHW) TRY(launch_nhwc_to_nchw(ye, reinterpret_cast<h16*>(y), d.N, d.K,
+                                                     d.P * d.Q, d.K, st));
+  return FP16_OK;
+}
+
+fp16_status fp16_conv_dgrad(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* w,
+                            fp16_t* dx, void* ws, size_t ws_bytes, fp16_stream_t stream) {
+  ConvDims d;
+  fp16_status s = check_conv(desc, &d);
+  if (s != FP16_OK) return s;
+  if (!dy || !w || !dx) return FP16_ERR_NULL;
+  if (!aligned16(dy) || !aligned16(w) || !aligned16(dx)) return FP16_ERR_MISALIGNED;
+  const ConvWs L = conv_ws(d, FP16_PASS_DGRAD);
+  if ((s = check_ws(L, ws, ws_bytes)) != FP16_OK) return s;
+  const size_t xb = (size_t)d.x_elems * 2;
+  if (overlap(dx, xb, dy, (size_t)d.y_elems * 2) || overlap(dx, xb, w, (size_t)d.w_elems * 2) ||
+      overlap(dx, xb, ws, L.total))
+    return FP16_ERR_ALIASING;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const h16* dye = reinterpret_cast<const h16*>(dy);
+  const h16* wk = reinterpret_cast<const h16*>(w);
+  h16* dxe = reinterpret_cast<h16*>(dx);
+  if (d.layout == FP16_NCHW) {
+    TRY(launch_nchw_to_nhwc(dye, wsp(ws, L.y), d.N, d.K, d.P * d.Q, d.Kp, st));
+    TRY(launch_nchw_to_nhwc(wk, wsp(ws, L.w), d.K, d.C, d.R * d.S, d.C, st));
+    dye = wsp(ws, L.y);
+    wk = wsp(ws, L.w);
+    dxe = wsp(ws, L.x);
+  } else if (d.Kp != d.K) {
+    TRY(launch_pad_channels(dye, wsp(ws, L.y), (int64_t)d.N * d.P * d.Q, d.K, d.Kp, st));
+    dye = wsp(ws, L.y);
+  }
+  h16* wf = wsp(ws, L.wf);
+  TRY(launch_dgrad_filter(wk, wf, d.K, d.C, d.R, d.S, d.C, d.Kp, d.sh, d.sw, d.ph, d.pw, st));
+  IgemmArgs a{};
+  a.act = dye; a.N = d.N; a.Hi = d.P; a.Wi = d.Q; a.Ci = d.Kp;
+  a.stride_h = 1; a.stride_w = 1;
+  a.Co = d.C; a.out = dxe; a.OH = d.H; a.OW = d.W; a.ldo = d.C; a.os_h = d.sh; a.os_w = d.sw;
+  a.nphase = 0;
+  int64_t off = 0;
+  for (int ph = 0; ph < d.sh; ++ph) {
+    for (int pw = 0; pw < d.sw; ++pw) {
+      const DgradPhase g = dgrad_phase(ph, pw, d.H, d.W, d.R, d.S, d.sh, d.sw, d.ph, d.pw);
+      if (g.Hph > 0 && g.Wph > 0) {
+        a.ph[a.nphase++] = IgemmPhase{wf + off, g.ntr * g.nts * d.Kp, g.ntr, g.nts, g.pad_h,
+                                      g.pad_w, g.Hph, g.Wph, ph, pw};
+        if (a.nphase == 4) {
+          TRY(launch_igemm(a, st));
+          a.nphase = 0;
+        }
+      }
+      off += (int64_t)d.C * g.ntr * g.nts * d.Kp;
+    }
+  }
+  if (a.nphase > 0) TRY(launch_igemm(a, st));
+  if (d.layout == FP16_NCHW)
+    TRY(launch_nhwc_to_nchw(dxe, reinterpret_cast<h16*>(dx), d.N, d.C, d.H * d.W, d.C, st));
+  return FP16_OK;
+}
+
+fp16_status fp16_conv_wgrad(const fp16_conv_desc* desc, const fp16_t* x, const fp16_t* dy,
+                            fp16_t* dw, void* ws, size_t ws_bytes, fp16_stream_t stream) {
+  ConvDims d;
+  fp16_status s = check_conv(desc, &d);
+  if (s != FP16_OK) return s;
+  if (!x || !dy || !dw) return FP16_ERR_NULL;
+  if (!aligned16(x) || !aligned16(dy) || !aligned16(dw)) return FP16_ERR_MISALIGNED;
+  const ConvWs L = conv_ws(d, FP16_PASS_WGRAD);
+  if ((s = check_ws(L, ws, ws_bytes)) != FP16_OK) return s;
+  const size_t wb = (size_t)d.w_elems * 2;
+  if (overlap(dw, wb, x, (size_t)d.x_elems * 2) || overlap(dw, wb, dy, (size_t)d.y_elems * 2) ||
+      overlap(dw, wb, ws, L.total))
+    return FP16_ERR_ALIASING;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const h16* xe = reinterpret_cast<const h16*>(x);
+  const h16* dye = reinterpret_cast<const h16*>(dy);
+  if (d.layout == FP16_NCHW) {
+    TRY(launch_nchw_to_nhwc(xe, wsp(ws, L.x), d.N, d.C, d.H * d.W, d.Cp, st));
+    TRY(launch_nchw_to_nhwc(dye, wsp(ws, L.y), d.N, d.K, d.P * d.Q, d.Kp, st));
+    xe = wsp(ws, L.x);
+    dye = wsp(ws, L.y);
+  } else {
+    if (d.Cp != d.C) {
+      TRY(launch_pad_channels(xe, wsp(ws, L.x), (int64_t)d.N * d.H * d.W, d.C, d.Cp, st));
+      xe = wsp(ws, L.x);
+    }
+    if (d.Kp != d.K) {
+      TRY(launch_pad_channels(dye, wsp(ws, L.y), (int64_t)d.N * d.P * d.Q, d.K, d.Kp, st));
+      dye = wsp(ws, L.y);
+    }
+  }
+  float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + L.part);
+  WgradArgs a{};
+  a.x = xe; a.dy = dye;
+  a.N = d.N; a.H = d.H; a.W = d.W; a.C = d.Cp; a.K = d.Kp; a.R = d.R; a.S = d.S;
+  a.sh = d.sh; a.sw = d.sw; a.ph = d.ph; a.pw = d.pw; a.P = d.P; a.Q = d.Q;
+  a.partial = part; a.splits = L.splits; a.pix_per_split = L.pps;
+  TRY(launch_wgrad_partial(a, st));
+  TRY(launch_wgrad_reduce(part, L.splits, d.K, d.Kp, d.R, d.S, d.C, d.Cp, d.layout,
+                          reinterpret_cast<h16*>(dw), st));
+  return FP16_OK;
+}
+
+// ---- batch normalisation ----------------------------------------------------
+
+static fp16_status check_bn(const fp16_bn_desc* d, BnArgs* a) {
+  if (!d) return FP16_ERR_NULL;
+  if (d->layout != FP16_NHWC && d->layout != FP16_NCHW) return FP16_ERR_LAYOUT;
+  if (d->n < 1 || d->c < 1 || d->h < 1 || d->w < 1 || d->c > 65535) return FP16_ERR_SHAPE;
+  if ((int64_t)d->n * d->c * d->h * d->w >= kMaxElems) return FP16_ERR_SHAPE;
+  if (!(d->eps >= 0.0f) || !(d->post_scale == d->post_scale)) return FP16_ERR_SHAPE;
+  if (d->use_stats != 0 && d->use_stats != 1) return FP16_ERR_SHAPE;
+  a->N = d->n; a->C = d->c; a->H = d->h; a->W = d->w; a->layout = d->layout;
+  a->eps = d->eps; a->post_scale = d->post_scale; a->relu = d->relu ? 1 : 0;
+  return FP16_OK;
+}
+
+size_t fp16_bn_workspace_bytes(const fp16_bn_desc* desc) {
+  BnArgs a;
+  if (check_bn(desc, &a) != FP16_OK) return 0;
+  return bn_ws_bytes(a);
+}
+
+fp16_status fp16_bn_relu(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t* gamma,
+                         const fp16_t* beta, const fp16_t* residual, fp16_t* y, float* stats,
+                         void* ws, size_t ws_bytes, fp16_stream_t stream) {
+  BnArgs a;
+  fp16_status s = check_bn(desc, &a);
+  if (s != FP16_OK) return s;
+  if (!x || !gamma || !beta || !y || !stats) return FP16_ERR_NULL;
+  if (!aligned16(x) || !aligned16(y) || (residual && !aligned16(residual)) || !aligned16(stats))
+    return FP16_ERR_MISALIGNED;
+  const size_t need = bn_ws_bytes(a);
+  if (!ws || ws_bytes < need) return FP16_ERR_WORKSPACE;
+  if (!aligned16(ws)) return FP16_ERR_MISALIGNED;
+  const size_t eb = (size_t)a.N * a.C * a.H * a.W * 2;
+  const size_t cb = (size_t)a.C * 2;
+  if ((y != x && overlap(y, eb, x, eb)) || (residual && y != residual && overlap(y, eb, residual, eb)) ||
+      overlap(y, eb, gamma, cb) || overlap(y, eb, beta, cb) || overlap(y, eb, stats, (size_t)a.C * 8) ||
+      overlap(y, eb, ws, need) || overlap(stats, (size_t)a.C * 8, ws, need))
+    return FP16_ERR_ALIASING;
+  return hip_status(launch_bn_fwd(a, reinterpret_cast<const h16*>(x),
+                                  reinterpret_cast<const h16*>(gamma),
+                                  reinterpret_cast<const h16*>(beta),
+                                  reinterpret_cast<const h16*>(residual), reinterpret_cast<h16*>(y),
+                                  stats, desc->use_stats, ws, static_cast<hipStream_t>(stream)));
+}
+
+fp16_status fp16_bn_relu_bwd(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t* y,
+                             const fp16_t* dy, const fp16_t* gamma, const fp16_t* beta,
+                             const fp16_t* residual, const float* stats, fp16_t* dx,
+                             fp16_t* dgamma, fp16_t* dbeta, fp16_t* dresidual, void* ws,
+                             size_t ws_bytes, fp16_stream_t stream) {
+  BnArgs a;
+  fp16_status s = check_bn(desc, &a);
+  if (s != FP16_OK) return s;
+  if (!x || !dy || !gamma || !beta || !stats || !dx || !dgamma || !dbeta) return FP16_ERR_NULL;
+  if (!aligned16(x) || (y && !aligned16(y)) || !aligned16(dy) || !aligned16(dx) ||
+      (residual && !aligned16(residual)) || (dresidual && !aligned16(dresidual)) ||
+      !aligned16(stats))
+    return FP16_ERR_MISALIGNED;
+  const size_t need = bn_ws_bytes(a);
+  if (!ws || ws_bytes < need) return FP16_ERR_WORKSPACE;
+  if (!aligned16(ws)) return FP16_ERR_MISALIGNED;
+  const size_t eb = (size_t)a.N * a.C * a.H * a.W * 2;
+  const size_t cb = (size_t)a.C * 2;
+  const void* ins[4] = {x, y, residual, gamma};
+  const size_t insz[4] = {eb, eb, eb, cb};
+  for (int i = 0; i < 4; ++i) {
+    if (overlap(dx, eb, ins[i], insz[i])) return FP16_ERR_ALIASING;
+    if (dresidual && overlap(dresidual, eb, ins[i], insz[i])) return FP16_ERR_ALIASING;
+  }
+  if ((dx != dy && overlap(dx, eb, dy, eb)) || (dresidual && overlap(dresidual, eb, dy, eb)) ||
+      (dresidual && overlap(dresidual, eb, dx, eb)) || overlap(dx, eb, ws, need) ||
+      overlap(dgamma, cb, dbeta, cb) || overlap(dgamma, cb, ws, need) ||
+      overlap(dbeta, cb, ws, need) || overlap(dgamma, cb, dx, eb) || overlap(dbeta, cb, dx, eb))
+    return FP16_ERR_ALIASING;
+  return hip_status(launch_bn_bwd(
+      a, reinterpret_cast<const h16*>(x), reinterpret_cast<const h16*>(y),
+      reinterpret_cast<const h16*>(dy), reinterpret_cast<const h16*>(gamma),
+      reinterpret_cast<const h16*>(beta), reinterpret_cast<const h16*>(residual), stats,
+      reinterpret_cast<h16*>(dx), reinterpret_cast<h16*>(dgamma), reinterpret_cast<h16*>(dbeta),
+      reinterpret_cast<h16*>(dresidual), ws, static_cast<hipStream_t>(stream)));
+}
+
+// ---- SGD ------------------------------------------------------------------------
+
+fp16_status fp16_sgd_step(fp16_t* w, const fp16_t* g, fp16_t* m, size_t n, float lr,
+                          float momentum, float weight_decay, fp16_stream_t stream) {
+  if (n == 0) return FP16_OK;
+  if (!w || !g || !m) return FP16_ERR_NULL;
+  if (!aligned16(w) || !aligned16(g) || !aligned16(m)) return FP16_ERR_MISALIGNED;
+  if (n >= ((size_t)1 << 40)) return FP16_ERR_SHAPE;
+  const size_t b = n * 2;
+  if (overlap(w, b, g, b) || overlap(m, b, g, b) || overlap(w, b, m, b)) return FP16_ERR_ALIASING;
+  return hip_status(launch_sgd(reinterpret_cast<h16*>(w), reinterpret_cast<const h16*>(g),
+                               reinterpret_cast<h16*>(m), n, lr, momentum, weight_decay,
+                               static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

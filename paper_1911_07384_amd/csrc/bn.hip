@@ -1,0 +1,511 @@
+// Batch normalisation fused with the 0.25 output multiplier, the identity
+// shortcut and ReLU (arXiv:1911.07384, Eq. 1-2 of Section 4.1; Section 4.2
+// for the multiplier; statistics over the local batch, Section 5.1), and
+// its backward.
+//
+// Forward = reduce (per-channel shifted sums of x and x^2), finalize (mean,
+// rstd in float64 -> float32 stats), apply (declared float32 sequence):
+//   a = fl(fl(s*gamma)*rstd); b = fl(s*beta); t = fl(x - mean);
+//   v = fma(t, a, b); v = fl(v + r); y = rne16(relu(v)).
+// Backward = reduce (S1 = sum g, S2 = sum g*xhat), finalize (dgamma,
+// dbeta, apply coefficients), apply (dx, dresidual).
+//
+// Bandwidth-bound.  The NHWC path (C a power-of-two multiple of 8, at most
+// 2048) gives each thread a fixed 8-channel chunk, so every access is a
+// 16-byte vector and per-channel coefficients are computed once per thread.
+// Other shapes and the NCHW layout use a generic per-element path.
+// Reductions are float32 within a thread, combined in a fixed order within a
+// block and in float64 across blocks: the result does not depend on timing.
+
+#include "kernels.hpp"
+
+namespace fp16k {
+namespace {
+
+constexpr int kT = 256;
+
+struct Geo {
+  int64_t M;  // elements per channel
+  int C, HW, layout;
+};
+
+// memory index of element j (0 <= j < M) of channel c
+__device__ __forceinline__ int64_t geo_at(const Geo& g, int c, int64_t j) {
+  if (g.layout == 0) return j * g.C + c;
+  const int64_t n = j / g.HW;
+  return (n * g.C + c) * g.HW + (j - n * g.HW);
+}
+// channel of memory index i
+__device__ __forceinline__ int geo_chan(const Geo& g, int64_t i) {
+  return g.layout == 0 ? (int)(i % g.C) : (int)((i / g.HW) % g.C);
+}
+
+struct Plan {
+  bool vec;
+  int CV, RB, G;
+  int64_t rpb;  // rows (or elements) per block
+};
+
+Plan make_plan(const BnArgs& a) {
+  Plan p{};
+  const int64_t M = (int64_t)a.N * a.H * a.W;
+  const int CV = a.C / 8;
+  p.vec = a.layout == 0 && a.C % 8 == 0 && CV >= 1 && CV <= kT && (kT % CV) == 0;
+  if (p.vec) {
+    p.CV = CV;
+    p.RB = kT / CV;
+    int64_t G = (M * CV + 4 * kT - 1) / (4 * kT);  // about four vectors per thread
+    if (G > 1024) G = 1024;
+    if (G < 1) G = 1;
+    int64_t rpb = (M + G - 1) / G;
+    rpb = (rpb + p.RB - 1) / p.RB * p.RB;
+    p.rpb = rpb;
+    p.G = (int)((M + rpb - 1) / rpb);
+  } else {
+    int64_t G = (M + 8 * kT - 1) / (8 * kT);
+    if (G > 64) G = 64;
+    if (G < 1) G = 1;
+    p.rpb = (M + G - 1) / G;
+    p.G = (int)((M + p.rpb - 1) / p.rpb);
+  }
+  return p;
+}
+
+// Per-channel forward coefficients of the declared float32 apply sequence.
+struct FwdCoef {
+  float mean, a, b;
+};
+__device__ __forceinline__ FwdCoef fwd_coef(const float* stats, const h16* gamma, const h16* beta,
+                                            int C, int c, float s) {
+  FwdCoef k;
+  k.mean = stats[c];
+  const float rstd = stats[C + c];
+  const float sg = s * to_f32(gamma[c]);
+  k.a = sg * rstd;
+  k.b = s * to_f32(beta[c]);
+  return k;
+}
+
+__device__ __forceinline__ float fwd_value(float x, const FwdCoef& k, bool has_r, float r,
+                                           bool relu) {
+  const float t = x - k.mean;
+  float v = __builtin_fmaf(t, k.a, k.b);
+  if (has_r) v = v + r;
+  if (relu) v = relu_keep_nan(v);
+  return v;
+}
+
+// Mask of the ReLU: from the stored output when given, else recomputed bit
+// for bit with the forward sequence.
+__device__ __forceinline__ bool relu_mask(bool relu, bool has_y, h16 y, float x, const FwdCoef& k,
+                                          bool has_r, float r) {
+  if (!relu) return true;
+  if (has_y) return to_f32(y) > 0.0f;
+  return to_f32(to_h16(fwd_value(x, k, has_r, r, true))) > 0.0f;
+}
+
+// ---- block reduction of 16 float32 partials per thread ----------------------
+// red: [16][kT] floats in LDS.  Threads t < CV sum entries t, t+CV, ... (RB of
+// them) in order and return the totals for their 8 channels.
+__device__ __forceinline__ void block_reduce_vec(float (&s1)[8], float (&s2)[8], float* red, int CV,
+                                                 int RB, float* out1, float* out2, int C) {
+  const int t = threadIdx.x;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    red[e * kT + t] = s1[e];
+    red[(8 + e) * kT + t] = s2[e];
+  }
+  __syncthreads();
+  if (t < CV) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      float a = 0.0f, b = 0.0f;
+      for (int r = 0; r < RB; ++r) {
+        a += red[e * kT + r * CV + t];
+        b += red[(8 + e) * kT + r * CV + t];
+      }
+      out1[(int64_t)blockIdx.x * C + t * 8 + e] = a;
+      out2[(int64_t)blockIdx.x * C + t * 8 + e] = b;
+    }
+  }
+}
+
+// ---- forward reduce ----------------------------------------------------------
+// Sums of (x - K_c) and (x - K_c)^2 with K_c = the channel's first element
+// (a shift that keeps the variance free of cancellation).
+
+__global__ __launch_bounds__(kT) void bn_fwd_reduce_vec(const h16* __restrict__ x, Geo g, int CV,
+                                                        int RB, int64_t rpb, float* ws1,
+                                                        float* ws2) {
+  __shared__ float red[16 * kT];
+  const int t = threadIdx.x;
+  const int j = t % CV;
+  const int64_t row0 = (int64_t)blockIdx.x * rpb;
+  int64_t row1 = row0 + rpb;
+  if (row1 > g.M) row1 = g.M;
+  const V8 kv = load16(x + j * 8);
+  float sh[8], s1[8], s2[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    sh[e] = to_f32(kv.h[e]);
+    s1[e] = 0.0f;
+    s2[e] = 0.0f;
+  }
+  for (int64_t row = row0 + t / CV; row < row1; row += RB) {
+    const V8 v = load16(x + row * g.C + j * 8);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float d = to_f32(v.h[e]) - sh[e];
+      s1[e] += d;
+      s2[e] = __builtin_fmaf(d, d, s2[e]);
+    }
+  }
+  block_reduce_vec(s1, s2, red, CV, RB, ws1, ws2, g.C);
+}
+
+__device__ __forceinline__ void block_reduce_1(float& a, float& b, float* red) {
+  const int t = threadIdx.x;
+  red[t] = a;
+  red[kT + t] = b;
+  __syncthreads();
+  for (int w = kT / 2; w > 0; w >>= 1) {
+    if (t < w) {
+      red[t] += red[t + w];
+      red[kT + t] += red[kT + t + w];
+    }
+    __syncthreads();
+  }
+  a = red[0];
+  b = red[kT];
+}
+
+__global__ __launch_bounds__(kT) void bn_fwd_reduce_gen(const h16* __restrict__ x, Geo g,
+                                                        int64_t rpb, float* ws1, float* ws2) {
+  __shared__ float red[2 * kT];
+  const int c = blockIdx.y;
+  const int64_t j0 = (int64_t)blockIdx.x * rpb;
+  int64_t j1 = j0 + rpb;
+  if (j1 > g.M) j1 = g.M;
+  const float sh = to_f32(x[geo_at(g, c, 0)]);
+  float s1 = 0.0f, s2 = 0.0f;
+  for (int64_t j = j0 + threadIdx.x; j < j1; j += kT) {
+    const float d = to_f32(x[geo_at(g, c, j)]) - sh;
+    s1 += d;
+    s2 = __builtin_fmaf(d, d, s2);
+  }
+  block_reduce_1(s1, s2, red);
+  if (threadIdx.x == 0) {
+    ws1[(int64_t)blockIdx.x * g.C + c] = s1;
+    ws2[(int64_t)blockIdx.x * g.C + c] = s2;
+  }
+}
+
+// mean = K + S1/M, var = S2/M - (S1/M)^2 (float64), rstd = 1/sqrt(var + eps).
+__global__ void bn_fwd_finalize(const h16* __restrict__ x, Geo g, int G, const float* ws1,
+                                const float* ws2, float eps, float* stats) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= g.C) return;
+  double S1 = 0.0, S2 = 0.0;
+  for (int b = 0; b < G; ++b) {
+    S1 += (double)ws1[(int64_t)b * g.C + c];
+    S2 += (double)ws2[(int64_t)b * g.C + c];
+  }
+  const double sh = (double)to_f32(x[geo_at(g, c, 0)]);
+  const double md = S1 / (double)g.M;
+  double var = S2 / (double)g.M - md * md;
+  if (var < 0.0) var = 0.0;
+  stats[c] = (float)(sh + md);
+  stats[g.C + c] = (float)(1.0 / __builtin_sqrt(var + (double)eps));
+}
+
+// ---- forward apply -------------------------------------------------------------
+
+__global__ __launch_bounds__(kT) void bn_fwd_apply_vec(const h16* x, const h16* __restrict__ gamma,
+                                                       const h16* __restrict__ beta, const h16* res,
+                                                       h16* y, const float* __restrict__ stats,
+                                                       Geo g, int CV, float s, int relu) {
+  const int64_t gt = (int64_t)blockIdx.x * kT + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * kT;  // a multiple of CV
+  const int j = (int)(gt % CV);
+  FwdCoef k[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) k[e] = fwd_coef(stats, gamma, beta, g.C, j * 8 + e, s);
+  const int64_t nvec = g.M * CV;
+  for (int64_t v = gt; v < nvec; v += stride) {
+    const V8 xv = load16(x + v * 8);
+    V8 rv;
+    if (res) rv = load16(res + v * 8);
+    V8 out;
+#pragma unroll
+    for (int e = 0; e < 8; ++e)
+      out.h[e] = to_h16(fwd_value(to_f32(xv.h[e]), k[e], res != nullptr,
+                                  res ? to_f32(rv.h[e]) : 0.0f, relu != 0));
+    store16(y + v * 8, out);
+  }
+}
+
+__global__ __launch_bounds__(kT) void bn_fwd_apply_gen(const h16* x, const h16* __restrict__ gamma,
+                                                       const h16* __restrict__ beta, const h16* res,
+                                                       h16* y, const float* __restrict__ stats,
+                                                       Geo g, float s, int relu) {
+  const int64_t total = g.M * g.C;
+  for (int64_t i = (int64_t)blockIdx.x * kT + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * kT) {
+    const int c = geo_chan(g, i);
+    const FwdCoef k = fwd_coef(stats, gamma, beta, g.C, c, s);
+    y[i] = to_h16(fwd_value(to_f32(x[i]), k, res != nullptr, res ? to_f32(res[i]) : 0.0f,
+                            relu != 0));
+  }
+}
+
+// ---- backward reduce -----------------------------------------------------------
+
+__global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ x,
+                                                        const h16* __restrict__ y,
+                                                        const h16* __restrict__ dy,
+                                                        const h16* __restrict__ gamma,
+                                                        const h16* __restrict__ beta,
+                                                        const h16* __restrict__ res,
+                                                        const float* __restrict__ stats, Geo g,
+                                                        int CV, int RB, int64_t rpb, float s,
+                                                        int relu, float* ws1, float* ws2) {
+  __shared__ float red[16 * kT];
+  const int t = threadIdx.x;
+  const int j = t % CV;
+  const int64_t row0 = (int64_t)blockIdx.x * rpb;
+  int64_t row1 = row0 + rpb;
+  if (row1 > g.M) row1 = g.M;
+  FwdCoef k[8];
+  float rstd[8], s1[8], s2[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    k[e] = fwd_coef(stats, gamma, beta, g.C, j * 8 + e, s);
+    rstd[e] = stats[g.C + j * 8 + e];
+    s1[e] = 0.0f;
+    s2[e] = 0.0f;
+  }
+  const bool has_y = y != nullptr, has_r = res != nullptr && !has_y && relu;
+  for (int64_t row = row0 + t / CV; row < row1; row += RB) {
+    const int64_t off = row * g.C + j * 8;
+    const V8 xv = load16(x + off);
+    const V8 dv = load16(dy + off);
+    V8 yv, rv;
+    if (relu && has_y) yv = load16(y + off);
+    if (has_r) rv = load16(res + off);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float xf = to_f32(xv.h[e]);
+      const bool m = relu_mask(relu != 0, has_y, has_y ? yv.h[e] : (h16)0.0f, xf, k[e], has_r,
+                               has_r ? to_f32(rv.h[e]) : 0.0f);
+      const float gg = m ? s * to_f32(dv.h[e]) : 0.0f;
+      const float xh = (xf - k[e].mean) * rstd[e];
+      s1[e] += gg;
+      s2[e] = __builtin_fmaf(gg, xh, s2[e]);
+    }
+  }
+  block_reduce_vec(s1, s2, red, CV, RB, ws1, ws2, g.C);
+}
+
+__global__ __launch_bounds__(kT) void bn_bwd_reduce_gen(const h16* __restrict__ x,
+                                                        const h16* __restrict__ y,
+                                                        const h16* __restrict__ dy,
+                                                        const h16* __restrict__ gamma,
+                                                        const h16* __restrict__ beta,
+                                                        const h16* __restrict__ res,
+                                                        const float* __restrict__ stats, Geo g,
+                                                        int64_t rpb, float s, int relu, float* ws1,
+                                                        float* ws2) {
+  __shared__ float red[2 * kT];
+  const int c = blockIdx.y;
+  const int64_t j0 = (int64_t)blockIdx.x * rpb;
+  int64_t j1 = j0 + rpb;
+  if (j1 > g.M) j1 = g.M;
+  const FwdCoef k = fwd_coef(stats, gamma, beta, g.C, c, s);
+  const float rstd = stats[g.C + c];
+  const bool has_y = y != nullptr, has_r = res != nullptr && !has_y && relu;
+  float s1 = 0.0f, s2 = 0.0f;
+  for (int64_t j = j0 + threadIdx.x; j < j1; j += kT) {
+    const int64_t i = geo_at(g, c, j);
+    const float xf = to_f32(x[i]);
+    const bool m = relu_mask(relu != 0, has_y, has_y ? y[i] : (h16)0.0f, xf, k, has_r,
+                             has_r ? to_f32(res[i]) : 0.0f);
+    const float gg = m ? s * to_f32(dy[i]) : 0.0f;
+    const float xh = (xf - k.mean) * rstd;
+    s1 += gg;
+    s2 = __builtin_fmaf(gg, xh, s2);
+  }
+  block_reduce_1(s1, s2, red);
+  if (threadIdx.x == 0) {
+    ws1[(int64_t)blockIdx.x * g.C + c] = s1;
+    ws2[(int64_t)blockIdx.x * g.C + c] = s2;
+  }
+}
+
+// dbeta = S1, dgamma = S2 (one rounding from float64); apply coefficients
+// A = gamma*rstd, B = S1/M, D = S2/M for dx = A * (g - (xhat*D + B)).
+__global__ void bn_bwd_finalize(Geo g, int G, const float* ws1, const float* ws2,
+                                const h16* __restrict__ gamma, const float* __restrict__ stats,
+                                h16* dgamma, h16* dbeta, float* coef) {
+  const int c = blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= g.C) return;
+  double S1 = 0.0, S2 = 0.0;
+  for (int b = 0; b < G; ++b) {
+    S1 += (double)ws1[(int64_t)b * g.C + c];
+    S2 += (double)ws2[(int64_t)b * g.C + c];
+  }
+  dbeta[c] = dbl_to_h16(S1);
+  dgamma[c] = dbl_to_h16(S2);
+  coef[c] = to_f32(gamma[c]) * stats[g.C + c];
+  coef[g.C + c] = (float)(S1 / (double)g.M);
+  coef[2 * g.C + c] = (float)(S2 / (double)g.M);
+}
+
+// ---- backward apply ------------------------------------------------------------
+
+__global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* y, const h16* dy,
+                                                       const h16* __restrict__ gamma,
+                                                       const h16* __restrict__ beta, const h16* res,
+                                                       const float* __restrict__ stats,
+                                                       const float* __restrict__ coef, Geo g,
+                                                       int CV, float s, int relu, h16* dx,
+                                                       h16* dres) {
+  const int64_t gt = (int64_t)blockIdx.x * kT + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * kT;
+  const int j = (int)(gt % CV);
+  FwdCoef k[8];
+  float rstd[8], A[8], B[8], D[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    const int c = j * 8 + e;
+    k[e] = fwd_coef(stats, gamma, beta, g.C, c, s);
+    rstd[e] = stats[g.C + c];
+    A[e] = coef[c];
+    B[e] = coef[g.C + c];
+    D[e] = coef[2 * g.C + c];
+  }
+  const bool has_y = y != nullptr, has_r = res != nullptr && !has_y && relu;
+  const int64_t nvec = g.M * CV;
+  for (int64_t v = gt; v < nvec; v += stride) {
+    const int64_t off = v * 8;
+    const V8 xv = load16(x + off);
+    const V8 dv = load16(dy + off);
+    V8 yv, rv, o, od;
+    if (relu && has_y) yv = load16(y + off);
+    if (has_r) rv = load16(res + off);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const float xf = to_f32(xv.h[e]);
+      const bool m = relu_mask(relu != 0, has_y, has_y ? yv.h[e] : (h16)0.0f, xf, k[e], has_r,
+                               has_r ? to_f32(rv.h[e]) : 0.0f);
+      const float gg = m ? s * to_f32(dv.h[e]) : 0.0f;
+      const float xh = (xf - k[e].mean) * rstd[e];
+      o.h[e] = to_h16(A[e] * (gg - __builtin_fmaf(xh, D[e], B[e])));
+      od.s[e] = m ? dv.s[e] : (uint16_t)0;
+    }
+    store16(dx + off, o);
+    if (dres) store16(dres + off, od);
+  }
+}
+
+__global__ __launch_bounds__(kT) void bn_bwd_apply_gen(const h16* x, const h16* y, const h16* dy,
+                                                       const h16* __restrict__ gamma,
+                                                       const h16* __restrict__ beta, const h16* res,
+                                                       const float* __restrict__ stats,
+                                                       const float* __restrict__ coef, Geo g,
+                                                       float s, int relu, h16* dx, h16* dres) {
+  const int64_t total = g.M * g.C;
+  const bool has_y = y != nullptr, has_r = res != nullptr && !has_y && relu;
+  for (int64_t i = (int64_t)blockIdx.x * kT + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * kT) {
+    const int c = geo_chan(g, i);
+    const FwdCoef k = fwd_coef(stats, gamma, beta, g.C, c, s);
+    const float xf = to_f32(x[i]);
+    const h16 dyv = dy[i];
+    const bool m = relu_mask(relu != 0, has_y, has_y ? y[i] : (h16)0.0f, xf, k, has_r,
+                             has_r ? to_f32(res[i]) : 0.0f);
+    const float gg = m ? s * to_f32(dyv) : 0.0f;
+    const float xh = (xf - k.mean) * stats[g.C + c];
+    dx[i] = to_h16(coef[c] * (gg - __builtin_fmaf(xh, coef[2 * g.C + c], coef[g.C + c])));
+    if (dres) dres[i] = m ? dyv : (h16)0.0f;
+  }
+}
+
+unsigned apply_grid(int64_t nthreads_wanted, int CV) {
+  int64_t b = (nthreads_wanted + kT - 1) / kT;
+  if (b > 16384) b = 16384;
+  if (b < 1) b = 1;
+  (void)CV;  // kT is a multiple of CV, so any grid keeps each thread on one chunk
+  return (unsigned)b;
+}
+
+Geo make_geo(const BnArgs& a) {
+  Geo g;
+  g.M = (int64_t)a.N * a.H * a.W;
+  g.C = a.C;
+  g.HW = a.H * a.W;
+  g.layout = a.layout;
+  return g;
+}
+
+size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
+
+}  // namespace
+
+size_t bn_ws_bytes(const BnArgs& a) {
+  const Plan p = make_plan(a);
+  return align256((size_t)2 * p.G * a.C * sizeof(float)) + align256((size_t)3 * a.C * sizeof(float));
+}
+
+hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const h16* beta,
+                         const h16* res, h16* y, float* stats, int use_stats, void* ws,
+                         hipStream_t st) {
+  const Plan p = make_plan(a);
+  const Geo g = make_geo(a);
+  float* ws1 = reinterpret_cast<float*>(ws);
+  float* ws2 = ws1 + (size_t)p.G * a.C;
+  if (!use_stats) {
+    if (p.vec)
+      hipLaunchKernelGGL(bn_fwd_reduce_vec, dim3(p.G), dim3(kT), 0, st, x, g, p.CV, p.RB, p.rpb,
+                         ws1, ws2);
+    else
+      hipLaunchKernelGGL(bn_fwd_reduce_gen, dim3(p.G, a.C), dim3(kT), 0, st, x, g, p.rpb, ws1, ws2);
+    hipLaunchKernelGGL(bn_fwd_finalize, dim3(ceil_div(a.C, kT)), dim3(kT), 0, st, x, g, p.G, ws1,
+                       ws2, a.eps, stats);
+  }
+  if (p.vec)
+    hipLaunchKernelGGL(bn_fwd_apply_vec, dim3(apply_grid(g.M * p.CV / 4, p.CV)), dim3(kT), 0, st,
+                       x, gamma, beta, res, y, stats, g, p.CV, a.post_scale, a.relu);
+  else
+    hipLaunchKernelGGL(bn_fwd_apply_gen, dim3(apply_grid(g.M * a.C / 4, 1)), dim3(kT), 0, st, x,
+                       gamma, beta, res, y, stats, g, a.post_scale, a.relu);
+  return hipGetLastError();
+}
+
+hipError_t launch_bn_bwd(const BnArgs& a, const h16* x, const h16* y, const h16* dy,
+                         const h16* gamma, const h16* beta, const h16* res, const float* stats,
+                         h16* dx, h16* dgamma, h16* dbeta, h16* dres, void* ws, hipStream_t st) {
+  const Plan p = make_plan(a);
+  const Geo g = make_geo(a);
+  float* ws1 = reinterpret_cast<float*>(ws);
+  float* ws2 = ws1 + (size_t)p.G * a.C;
+  float* coef = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) +
+                                         align256((size_t)2 * p.G * a.C * sizeof(float)));
+  if (p.vec)
+    hipLaunchKernelGGL(bn_bwd_reduce_vec, dim3(p.G), dim3(kT), 0, st, x, y, dy, gamma, beta, res,
+                       stats, g, p.CV, p.RB, p.rpb, a.post_scale, a.relu, ws1, ws2);
+  else
+    hipLaunchKernelGGL(bn_bwd_reduce_gen, dim3(p.G, a.C), dim3(kT), 0, st, x, y, dy, gamma, beta,
+                       res, stats, g, p.rpb, a.post_scale, a.relu, ws1, ws2);
+  hipLaunchKernelGGL(bn_bwd_finalize, dim3(ceil_div(a.C, kT)), dim3(kT), 0, st, g, p.G, ws1, ws2,
+                     gamma, stats, dgamma, dbeta, coef);
+  if (p.vec)
+    hipLaunchKernelGGL(bn_bwd_apply_vec, dim3(apply_grid(g.M * p.CV / 4, p.CV)), dim3(kT), 0, st,
+                       x, y, dy, gamma, beta, res, stats, coef, g, p.CV, a.post_scale, a.relu, dx,
+                       dres);
+  else
+    hipLaunchKernelGGL(bn_bwd_apply_gen, dim3(apply_grid(g.M * a.C / 4, 1)), dim3(kT), 0, st, x,
+                       y, dy, gamma, beta, res, stats, coef, g, a.post_scale, a.relu, dx, dres);
+  return hipGetLastError();
+}
+
+}  // namespace fp16k

@@ -1,0 +1,112 @@
+// Internal launch interface between the C ABI (api.hip) and the kernel
+// translation units.  Every launcher enqueues on `st` and returns the
+// hipError_t of the launch.  Arguments have already been validated.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <stddef.h>
+
+#include "common.hpp"
+
+namespace fp16k {
+
+// ---- SGD (sgd.hip) --------------------------------------------------------
+hipError_t launch_sgd(h16* w, const h16* g, h16* m, size_t n, float lr, float momentum,
+                      float weight_decay, hipStream_t st);
+
+// ---- layout helpers (layout.hip) -----------------------------------------
+// [N][C][HW] -> [N][HW][Cp] with channels c >= C zero-filled (Cp >= C).
+hipError_t launch_nchw_to_nhwc(const h16* src, h16* dst, int N, int C, int HW, int Cp,
+                               hipStream_t st);
+// [N][HW][Cp] -> [N][C][HW] (channels >= C dropped).
+hipError_t launch_nhwc_to_nchw(const h16* src, h16* dst, int N, int C, int HW, int Cp,
+                               hipStream_t st);
+// Repack channels of an NHWC tensor: [P][C] -> [P][Cp] zero-filled.
+hipError_t launch_pad_channels(const h16* src, h16* dst, int64_t P, int C, int Cp, hipStream_t st);
+
+// ---- convolution (conv_igemm.hip, conv_wgrad.hip) -------------------------
+// One implicit-GEMM "phase": a stride-1-or-sigma gather of the NHWC source
+// over an output grid, against a filter laid out [Co][Rt][St][Ci].
+struct IgemmPhase {
+  const h16* filt;  // [Co][Rt*St*Ci], row stride ldb
+  int ldb;
+  int Rt, St;       // taps of this phase
+  int pad_h, pad_w; // source row = i*stride_h - pad_h + r
+  int Ho, Wo;       // output grid of this phase
+  int oph, opw;     // output tensor position = (i*os_h + oph, j*os_w + opw)
+};
+
+struct IgemmArgs {
+  const h16* act;  // NHWC source [N][Hi][Wi][Ci], Ci % 8 == 0
+  int N, Hi, Wi, Ci;
+  int stride_h, stride_w;
+  int Co;          // output channels (GEMM N)
+  h16* out;        // NHWC output [N][OH][OW][ldo], writes channels [0, Co)
+  int OH, OW, ldo;
+  int os_h, os_w;
+  int nphase;
+  IgemmPhase ph[4];
+};
+
+hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st);
+
+// Geometry of one stride phase (ph, pw) of the data gradient.  Output rows
+// h = ph + sh*i (i < Hph) receive exactly the taps r = r0 + sh*t (t < ntr)
+// with r0 = (ph + pad_h) mod sh, reading dy row p = i + (ph + pad_h - r0)/sh - t.
+// With the taps stored in reverse order (t' = ntr-1-t) this is a stride-1
+// gather p = i - pad_h' + t' with pad_h' = ntr - 1 - (ph + pad_h - r0)/sh.
+// Columns likewise.  A phase with ntr or nts = 0 receives no tap (zeros).
+struct DgradPhase {
+  int r0, s0, ntr, nts, Hph, Wph, pad_h, pad_w;
+};
+inline DgradPhase dgrad_phase(int ph, int pw, int H, int W, int R, int S, int sh, int sw,
+                              int pad_h, int pad_w) {
+  DgradPhase d;
+  d.r0 = (ph + pad_h) % sh;
+  d.s0 = (pw + pad_w) % sw;
+  d.ntr = d.r0 < R ? (R - d.r0 + sh - 1) / sh : 0;
+  d.nts = d.s0 < S ? (S - d.s0 + sw - 1) / sw : 0;
+  d.Hph = ph < H ? (H - ph + sh - 1) / sh : 0;
+  d.Wph = pw < W ? (W - pw + sw - 1) / sw : 0;
+  d.pad_h = d.ntr - 1 - (ph + pad_h - d.r0) / sh;
+  d.pad_w = d.nts - 1 - (pw + pad_w - d.s0) / sw;
+  return d;
+}
+
+// Filter transform for the data gradient: W [K][R][S][Cw] (KRSC, row channel
+// stride Cw) -> per stride phase (ph, pw) a filter [C][nt_r][nt_s][Kp]
+// holding W[k][r0 + sh*(nt_r-1-t_r)][s0 + sw*(nt_s-1-t_s)][c] (zero for k >= K).
+hipError_t launch_dgrad_filter(const h16* w, h16* dst, int K, int C, int R, int S, int Cw,
+                               int Kp, int sh, int sw, int pad_h, int pad_w, hipStream_t st);
+
+struct WgradArgs {
+  const h16* x;   // NHWC [N][H][W][C], C % 8 == 0
+  const h16* dy;  // NHWC [N][P][Q][K], K % 8 == 0
+  int N, H, W, C, K, R, S, sh, sw, ph, pw, P, Q;
+  float* partial; // [splits][K][R*S*C]
+  int splits;
+  int pix_per_split;
+};
+hipError_t launch_wgrad_partial(const WgradArgs& a, hipStream_t st);
+// dw[k][r][s][c] = rne16(sum_split partial[split][k][(r*S+s)*Cp + c]) for k < K, c < C,
+// with Kp rows per split, written as KRSC (layout 0) or KCRS (layout 1).
+hipError_t launch_wgrad_reduce(const float* partial, int splits, int K, int Kp, int R, int S,
+                               int C, int Cp, int layout, h16* dw, hipStream_t st);
+void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int* splits, int* pix_per_split);
+
+// ---- batch normalisation (bn.hip) ----------------------------------------
+struct BnArgs {
+  int N, C, H, W, layout;
+  float eps, post_scale;
+  int relu;
+};
+size_t bn_ws_bytes(const BnArgs& a);
+hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const h16* beta,
+                         const h16* res, h16* y, float* stats, int use_stats, void* ws,
+                         hipStream_t st);
+hipError_t launch_bn_bwd(const BnArgs& a, const h16* x, const h16* y, const h16* dy,
+                         const h16* gamma, const h16* beta, const h16* res, const float* stats,
+                         h16* dx, h16* dgamma, h16* dbeta, h16* dres, void* ws, hipStream_t st);
+
+}  // namespace fp16k

@@ -1,0 +1,150 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every function include/fp16train.h declares, and rejects invalid arguments
+with the documented status before anything is launched.  Pointers here are
+fake addresses that validation must reject without dereferencing: every call
+here carries at least one invalid argument, so nothing is ever launched."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_1911_07384_amd as F
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "fp16train.h")
+
+OK, NULL, SHAPE, LAYOUT, MISALIGNED, ALIASING, WORKSPACE = 0, 1, 2, 3, 4, 5, 6
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fp16_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_function():
+    names = _declared()
+    assert "fp16_conv_fwd" in names and "fp16_sgd_step" in names and len(names) >= 11
+    lib = ctypes.CDLL(F.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(F.EXPORTS) == set(names)
+
+
+def test_version_and_status_strings():
+    assert F.fp16_version().startswith("fp16train")
+    for s in range(9):
+        assert F.fp16_status_string(s)
+    assert F.fp16_status_string(99) == "unknown status"
+
+
+def _conv(**kw):
+    base = dict(n=2, c=64, h=56, w=56, k=64, r=3, s=3, stride=1, pad=1, layout="NHWC")
+    base.update(kw)
+    return F.conv_desc(base["n"], base["c"], base["h"], base["w"], base["k"], base["r"], base["s"],
+                       base["stride"], base["pad"], base["layout"])
+
+
+def _call(fn, desc, a, b, c, ws=0, wsb=0):
+    return getattr(F.lib(), fn)(ctypes.byref(desc) if desc is not None else None, a, b, c, ws, wsb,
+                                None)
+
+
+A = 0x10000000  # fake, 16-byte aligned, far apart
+B = 0x20000000
+Cc = 0x30000000
+WS = 0x40000000
+
+
+@pytest.mark.parametrize("fn", ["fp16_conv_fwd", "fp16_conv_dgrad", "fp16_conv_wgrad"])
+def test_conv_validation(fn):
+    d = _conv()
+    assert _call(fn, None, A, B, Cc) == NULL
+    assert _call(fn, d, None, B, Cc) == NULL
+    assert _call(fn, d, A, B, None) == NULL
+    # NCHW is accepted; it needs staging workspace, whose absence is the error
+    assert _call(fn, _conv(layout=1), A, B, Cc) == WORKSPACE
+    bad = _conv()
+    bad.layout = 7
+    assert _call(fn, bad, A, B, Cc) == LAYOUT
+    for field, val in [("n", 0), ("c", 0), ("h", -1), ("k", 0), ("stride_h", 0), ("pad_w", -1),
+                       ("r", 100)]:
+        d2 = _conv()
+        setattr(d2, field, val)
+        assert _call(fn, d2, A, B, Cc) == SHAPE, field
+    # kernel larger than the padded image
+    assert _call(fn, _conv(h=1, w=1, pad=0), A, B, Cc) == SHAPE
+    assert _call(fn, d, A + 2, B, Cc) == MISALIGNED
+    assert _call(fn, d, A, B, Cc + 8) == MISALIGNED
+
+
+def test_conv_workspace_and_aliasing():
+    d = _conv()
+    # native NHWC forward with C % 8 == 0 needs no workspace ...
+    assert F.fp16_conv_workspace_bytes(d, F.PASS_FWD) == 0
+    # ... so overlapping output/input is the next check
+    assert _call("fp16_conv_fwd", d, A, B, A + 64) == ALIASING
+    # the data gradient needs its phase filters and the weight gradient its partials
+    for p in (F.PASS_DGRAD, F.PASS_WGRAD):
+        need = F.fp16_conv_workspace_bytes(d, p)
+        assert need > 0
+    need = F.fp16_conv_workspace_bytes(d, F.PASS_WGRAD)
+    assert _call("fp16_conv_wgrad", d, A, B, Cc, 0, 0) == WORKSPACE
+    assert _call("fp16_conv_wgrad", d, A, B, Cc, WS, need - 1) == WORKSPACE
+    assert _call("fp16_conv_wgrad", d, A, B, Cc, WS + 4, need) == MISALIGNED
+    assert _call("fp16_conv_wgrad", d, A, B, WS + 16, WS, need) == ALIASING
+    # channel padding and NCHW need staging space in the forward pass too
+    assert F.fp16_conv_workspace_bytes(_conv(c=3), F.PASS_FWD) > 0
+    assert F.fp16_conv_workspace_bytes(_conv(layout="NCHW"), F.PASS_FWD) > 0
+    assert F.fp16_conv_workspace_bytes(_conv(), 5) == 0
+
+
+@pytest.mark.parametrize("hw,r,st,pad", [(56, 3, 1, 1), (56, 1, 2, 0), (224, 7, 2, 3), (7, 3, 1, 1),
+                                         (14, 3, 2, 1), (1, 1, 1, 0), (5, 3, 2, 0)])
+def test_out_dims(hw, r, st, pad):
+    d = _conv(h=hw, w=hw, r=r, s=r, stride=st, pad=pad)
+    p, q = F.fp16_conv_out_dims(d)
+    assert p == q == (hw + 2 * pad - r) // st + 1
+
+
+def test_bn_validation():
+    lib = F.lib()
+    d = F.bn_desc(2, 64, 8, 8)
+    need = F.fp16_bn_workspace_bytes(d)
+    assert need > 0
+    args = [A, B, B + 256, None, Cc, WS + (1 << 20), WS, need, None]
+    assert lib.fp16_bn_relu(None, *args) == NULL
+    assert lib.fp16_bn_relu(ctypes.byref(d), None, *args[1:]) == NULL
+    assert lib.fp16_bn_relu(ctypes.byref(d), A, B, B + 256, None, Cc, None, WS, need, None) == NULL
+    assert lib.fp16_bn_relu(ctypes.byref(d), A, B, B + 256, None, Cc, WS + (1 << 20), WS, need - 4,
+                            None) == WORKSPACE
+    assert lib.fp16_bn_relu(ctypes.byref(d), A + 2, B, B + 256, None, Cc, WS + (1 << 20), WS, need,
+                            None) == MISALIGNED
+    # y overlapping x partially is rejected (exactly equal is allowed: in place)
+    assert lib.fp16_bn_relu(ctypes.byref(d), A, B, B + 256, None, A + 16, WS + (1 << 20), WS, need,
+                            None) == ALIASING
+    bad = F.bn_desc(2, 64, 8, 8)
+    bad.layout = 3
+    assert lib.fp16_bn_relu(ctypes.byref(bad), *args) == LAYOUT
+    bad = F.bn_desc(0, 64, 8, 8)
+    assert lib.fp16_bn_relu(ctypes.byref(bad), *args) == SHAPE
+    # backward: required pointers and the dx/dy in-place rule
+    bw = [A, None, Cc, B, B + 256, None, WS + (1 << 20), Cc + (1 << 20), B + 512, B + 768, None, WS,
+          need, None]
+    assert lib.fp16_bn_relu_bwd(ctypes.byref(d), None, *bw[1:]) == NULL
+    bw_alias = list(bw)
+    bw_alias[7] = Cc + 32  # dx partially overlapping dy
+    assert lib.fp16_bn_relu_bwd(ctypes.byref(d), *bw_alias) == ALIASING
+    bw_alias = list(bw)
+    bw_alias[7] = A  # dx == x
+    assert lib.fp16_bn_relu_bwd(ctypes.byref(d), *bw_alias) == ALIASING
+
+
+def test_sgd_validation():
+    lib = F.lib()
+    assert lib.fp16_sgd_step(None, None, None, 0, 0.1, 0.9, 1e-4, None) == OK  # n = 0: no-op
+    assert lib.fp16_sgd_step(None, B, Cc, 8, 0.1, 0.9, 1e-4, None) == NULL
+    assert lib.fp16_sgd_step(A + 2, B, Cc, 8, 0.1, 0.9, 1e-4, None) == MISALIGNED
+    assert lib.fp16_sgd_step(A, A + 16, Cc, 64, 0.1, 0.9, 1e-4, None) == ALIASING
+    assert lib.fp16_sgd_step(A, B, A + 64, 64, 0.1, 0.9, 1e-4, None) == ALIASING

@@ -1,0 +1,121 @@
+"""GPU parity of fp16_conv_fwd / fp16_conv_dgrad / fp16_conv_wgrad against the
+oracle's float64 convolutions (ResNet-50's convolutions, Section 5.1; FP16
+storage with one rounding per output, Section 5.2).
+
+Bar: max |gpu - oracle| <= 1e-2 * RMS(oracle) on every output element, at
+sizes the oracle evaluates whole; on sampled outputs for full-size layers;
+bit-exact where the sums are exact (delta filters, one-hot gradients)."""
+
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import paper_1911_07384_amd as F
+from gpu_util import ConvCase, check_close, dev, host, note, require_gpu, ulp_dist
+
+pytestmark = pytest.mark.gpu
+
+PASSES = ("fwd", "dgrad", "wgrad")
+
+# (n, c, h, w, k, r, s, stride, pad, layout)
+SHAPES = [
+    (2, 64, 56, 56, 64, 3, 3, 1, 1, "NHWC"),    # the single 3x3 layer, N = 2 (full size)
+    (2, 64, 28, 28, 64, 3, 3, 1, 1, "NHWC"),    # several M tiles and a ragged last tile
+    (2, 256, 14, 14, 64, 1, 1, 1, 0, "NHWC"),   # bottleneck-entry 1x1
+    (2, 64, 14, 14, 256, 1, 1, 1, 0, "NHWC"),   # bottleneck-exit 1x1
+    (2, 64, 15, 15, 128, 1, 1, 2, 0, "NHWC"),   # strided 1x1 shortcut, odd size
+    (2, 32, 17, 17, 48, 3, 3, 2, 1, "NHWC"),    # strided 3x3, odd size
+    (2, 3, 32, 32, 64, 7, 7, 2, 3, "NHWC"),     # the stem (3 input channels)
+    (2, 24, 9, 11, 40, 3, 3, 1, 1, "NHWC"),     # channels not a tile multiple
+    (3, 16, 6, 5, 3, 3, 3, 1, 2, "NHWC"),       # 3 output channels, pad > R/2
+    (4, 512, 1, 1, 200, 1, 1, 1, 0, "NHWC"),    # fully connected as a 1x1 on 1x1 images
+    (1, 8, 1, 1, 8, 1, 1, 1, 0, "NHWC"),        # smallest case
+    (2, 128, 7, 7, 128, 3, 3, 1, 1, "NHWC"),    # wide channels, tiny image
+    (1, 16, 9, 9, 16, 3, 3, 3, 0, "NHWC"),      # stride 3 (9 dgrad phases)
+    (2, 64, 12, 12, 64, 3, 3, 1, 1, "NCHW"),
+    (2, 3, 20, 20, 16, 7, 7, 2, 3, "NCHW"),
+    (2, 64, 15, 15, 128, 1, 1, 2, 0, "NCHW"),
+]
+
+
+def _id(s):
+    return "n{}c{}h{}w{}k{}r{}s{}st{}p{}{}".format(*s)
+
+
+@pytest.mark.parametrize("shape", SHAPES, ids=[_id(s) for s in SHAPES])
+@pytest.mark.parametrize("which", PASSES)
+def test_parity_full(shape, which):
+    require_gpu()
+    n, c, h, w, k, r, s, st, pad, lay = shape
+    case = ConvCase(n, c, h, w, k, r, s, st, pad, lay, seed=1)
+    got = case.run(which)
+    ref64, ref16 = case.oracle(which)
+    check_close(got, ref64, what=f"{which} {case.label}")
+    # nearly every element is the oracle's rounding or its neighbour
+    assert np.mean(ulp_dist(got, ref16) <= 1) > 0.99
+
+
+@pytest.mark.parametrize("which", PASSES)
+def test_deterministic(which):
+    require_gpu()
+    case = ConvCase(2, 64, 28, 28, 64, 3, 3, 1, 1, seed=2)
+    a = case.run(which)
+    b = case.run(which)
+    assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
+
+
+@pytest.mark.parametrize("layout", ["NHWC", "NCHW"])
+@pytest.mark.parametrize("r,shift", [(3, (0, 0)), (3, (1, -1)), (1, (0, 0)), (7, (-2, 3))])
+def test_delta_filter_forward_is_exact(layout, r, shift):
+    require_gpu()
+    n, c, h, w = 2, 16, 10, 9
+    pad = r // 2
+    Wk = np.zeros((c, c, r, r), np.float16)
+    for ci in range(c):
+        Wk[ci, ci, pad + shift[0], pad + shift[1]] = 1.0
+    wt = Wk if layout == "NCHW" else np.ascontiguousarray(np.transpose(Wk, (0, 2, 3, 1)))
+    case = ConvCase(n, c, h, w, c, r, r, 1, pad, layout, seed=3, wt=wt)
+    got = case.run("fwd")
+    _, ref16 = case.oracle("fwd")
+    assert np.array_equal(got.view(np.uint16), ref16.view(np.uint16))
+
+
+@pytest.mark.parametrize("r,st,pad", [(3, 1, 1), (3, 2, 1), (1, 2, 0), (7, 2, 3)])
+def test_one_hot_gradient_is_exact(r, st, pad):
+    require_gpu()
+    n, c, h, w, k = 2, 8, 11, 10, 16
+    case = ConvCase(n, c, h, w, k, r, r, st, pad, "NHWC", seed=4)
+    dy = np.zeros(case.ys, np.float16)
+    for (n0, p0, q0, k0) in [(1, case.P - 1, 0, 3), (0, case.P // 2, case.Q - 1, 15)]:
+        dy[n0, p0, q0, k0] = 1.0
+    case.dy = dy
+    for which in ("dgrad", "wgrad"):
+        got = case.run(which)
+        _, ref16 = case.oracle(which)
+        assert np.array_equal(got.astype(np.float64), ref16.astype(np.float64)), which
+
+
+# The bottleneck block of ResNet-50 stage conv2_x at the paper's per-GPU
+# batch of 32 (Section 5.2), layer by layer at full size: sampled outputs.
+BLOCK = [
+    (32, 256, 56, 56, 64, 1, 1, 1, 0),
+    (32, 64, 56, 56, 64, 3, 3, 1, 1),
+    (32, 64, 56, 56, 256, 1, 1, 1, 0),
+]
+
+
+@pytest.mark.parametrize("shape", BLOCK, ids=[_id(s + ("NHWC",)) for s in BLOCK])
+@pytest.mark.parametrize("which", PASSES)
+def test_parity_full_size_sampled(shape, which):
+    require_gpu()
+    case = ConvCase(*shape, "NHWC", seed=0, dy_std=1e-3)
+    got = case.run(which).reshape(-1)
+    rng = np.random.default_rng(7)
+    idx = np.unique(np.concatenate([rng.integers(0, got.size, 2000), [0, got.size - 1]]))
+    ref = case.oracle_at(which, idx)
+    rms = np.sqrt(np.mean(ref ** 2))
+    err = np.max(np.abs(got[idx].astype(np.float64) - ref))
+    assert err <= 1e-2 * rms, (err, rms)
+    assert np.all(np.isfinite(got.astype(np.float32)))
