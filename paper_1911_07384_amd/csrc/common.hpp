@@ -36,8 +36,15 @@ __device__ __forceinline__ V8 zero8() {
 }
 
 // float32 -> binary16, round to nearest even (v_cvt_f16_f32 in the default
-// rounding mode; binary16 subnormals are produced, not flushed).
-__device__ __forceinline__ h16 to_h16(float v) { return (h16)v; }
+// rounding mode; binary16 subnormals are produced, not flushed).  The empty
+// asm pins the float32 value in a register: without it the compiler may fold
+// a preceding fma into v_fma_mix*_f16, which rounds the exact result once to
+// binary16 instead of first to float32 -- a different result in rare cases,
+// and not the declared sequence.
+__device__ __forceinline__ h16 to_h16(float v) {
+  __asm__("" : "+v"(v));
+  return (h16)v;
+}
 __device__ __forceinline__ float to_f32(h16 v) { return (float)v; }
 
 // float64 -> binary16 with a single rounding (nearest even).  The double is
