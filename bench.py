@@ -1,0 +1,260 @@
+"""Benchmark: one all-FP16 training step of the ResNet-50 conv2_x bottleneck
+block at batch 32 (56x56, 256->64->64->256 channels) on one MI355X.
+
+A step is the whole hot path over one synthetic batch: three convolution
+forwards, three fused BN(0.25)+ReLU forwards (the last with the identity
+shortcut), their backwards, three data and three weight gradients, and the
+FP16 momentum-SGD update of every parameter.  Inputs are resident in HBM
+before timing; the step is captured once in a HIP graph and replayed.
+
+Prints one JSON line: the headline value is the convolution throughput of the
+step (fwd + dgrad + wgrad FLOPs / step time, TFLOP/s), with images/s, the
+fraction of the FP16 matrix-core peak, a per-call breakdown measured with HIP
+events, the roofline of the dominant kernel, and the CPU oracle's rate on a
+bounded sample of the same step.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_FP16_TFLOPS = 2516.6   # MI355X dense FP16 matrix cores: 256 CU x 2.4 GHz x 4096 FLOP/clk
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+METRIC = "FP16 conv TFLOP/s (fwd+dgrad+wgrad) as % MFMA peak; ResNet-50 train images/sec"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--batch", type=int, default=32)
+    ap.add_argument("--eager", action="store_true", help="no HIP graph")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="target duration of the CPU oracle sample")
+    return ap.parse_args()
+
+
+def call_work(name, s):
+    """Algorithmic work of one ABI call of the step: (flops, bytes, bound)."""
+    n, hw, c, w = s.n, s.hw, s.c, s.width
+    m = n * hw * hw
+    convs = {"conv1": (c, w, 1), "conv2": (w, w, 3), "conv3": (w, c, 1)}
+    if name.startswith("conv"):
+        ci, co, r = convs[name[:5]]
+        flops = 2 * m * co * ci * r * r
+        byts = 2 * (m * ci + m * co + co * ci * r * r)
+        if name.endswith("dgrad_add"):
+            byts += 2 * m * ci  # the shortcut gradient read in the epilogue
+        bound = "mfma" if flops / byts >= PEAK_FP16_TFLOPS / PEAK_HBM_GBS * 1e3 else "hbm"
+        return flops, byts, bound
+    if name.startswith("bn"):
+        co = {"bn1": w, "bn2": w, "bn3": c}[name[:3]]
+        e = m * co
+        if name.endswith("fwd"):
+            byts = 6 * e + (2 * e if name == "bn3_fwd" else 0)  # reduce x; apply x (+r) -> y
+        else:
+            # reduce x, dy (+r); apply x, dy (+r) -> dx (+ shortcut gradient)
+            byts = 10 * e + (6 * e if name == "bn3_bwd" else 0)
+        return 0, byts, "hbm"
+    if name == "sgd_conv":
+        return 0, 10 * sum(co * ci * r * r for ci, co, r in s.conv_shapes), "hbm"
+    if name == "sgd_bn":
+        return 0, 10 * 2 * (w + w + c), "hbm"
+    raise KeyError(name)
+
+
+KERNELS_OF_CALL = {
+    "conv_fwd": ["igemm_kernel"],
+    "conv_dgrad": ["dgrad_filter_kernel", "igemm_kernel"],
+    "conv_wgrad": ["wgrad_kernel", "wgrad_reduce_kernel"],
+    "bn_fwd": ["bn_fwd_reduce_vec", "bn_fwd_finalize", "bn_fwd_apply_vec"],
+    "bn_bwd": ["bn_bwd_reduce_vec", "bn_bwd_finalize", "bn_bwd_apply_vec"],
+    "sgd": ["sgd_kernel"],
+}
+
+
+def profile_calls(block, reps, torch):
+    """Average duration of every ABI call of the step, timed with HIP events
+    recorded on the stream the calls are enqueued on."""
+    stream = torch.cuda.current_stream()
+    calls = block.calls()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in calls]
+    tot = [0.0] * len(calls)
+    for _ in range(reps):
+        # hold the stream with a short device-side spin so the whole step is
+        # queued before it starts: calls then run back to back, as in the graph
+        torch.cuda._sleep(20_000_000)
+        for (name, fn), (a, b) in zip(calls, evs):
+            a.record(stream)
+            fn()
+            b.record(stream)
+        torch.cuda.synchronize()
+        for i, (a, b) in enumerate(evs):
+            tot[i] += a.elapsed_time(b)
+    return [(name, tot[i] / reps) for i, (name, _) in enumerate(calls)]
+
+
+def traffic_for(kernel_src: str, call: str):
+    """HBM bytes per call from the committed rocprofv3 counter summary, if it
+    was taken on the current source of the kernel (else None)."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        data = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    src = os.path.join(ROOT, "paper_1911_07384_amd", "csrc", kernel_src)
+    try:
+        digest = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    except OSError:
+        return None
+    ent = data.get(call)
+    if not ent or ent.get("source_sha256_16") != digest:
+        return None
+    return ent.get("hbm_bytes")
+
+
+def cpu_baseline(shape, target_s):
+    """The oracle's block step on a batch slice, on this host's cores."""
+    import numpy as np
+    import oracle
+    from oracle.bottleneck import block_step, block_flops
+    from paper_1911_07384_amd import synth
+
+    def run(n):
+        x = synth.normal_f16((n, shape.hw, shape.hw, shape.c), 1.0, 0, 1)
+        W = [synth.normal_f16((co, r, r, ci), synth.he_std(ci * r * r), 0, 10 + i)
+             for i, (ci, co, r) in enumerate(shape.conv_shapes)]
+        g = [np.ones(co, np.float16) for _, co, _ in shape.conv_shapes]
+        b = [np.zeros(co, np.float16) for _, co, _ in shape.conv_shapes]
+        dout = synth.normal_f16((n, shape.hw, shape.hw, shape.c), 1e-3, 0, 2)
+        t = time.perf_counter()
+        block_step(x, W, g, b, dout, shape.post_scale, shape.eps)
+        dt = time.perf_counter() - t
+        return dt, 3 * block_flops(n, shape.hw, shape.conv_shapes)
+
+    t1, _ = run(1)
+    n = max(1, min(shape.n, int(round(target_s / max(t1, 1e-3)))))
+    dt, fl = run(n)
+    return {"value": fl / dt / 1e12, "unit": "TFLOP/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"the full block step (3 conv fwd/dgrad/wgrad, 3 BN fwd/bwd, SGD) at batch "
+                      f"{n} of {shape.n}, float64 direct loops, {dt:.2f} s; TFLOP/s counts the "
+                      f"convolution FLOPs like the GPU value",
+            "seconds": dt, "batch": n}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (this build runs "
+              f"on a single GPU and has no multi-GPU path)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    import paper_1911_07384_amd as F
+    from paper_1911_07384_amd.bottleneck import Bottleneck, BlockShape
+
+    torch.cuda.set_device(0)
+    shape = BlockShape(n=args.batch)
+    block = Bottleneck(shape, seed=0)
+    torch.cuda.synchronize()
+
+    # capture the step once (every call enqueues on the capture stream)
+    graph = None
+    if not args.eager:
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            block.step()  # one eager step on the capture stream before capturing
+        torch.cuda.current_stream().wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            block.step()
+        torch.cuda.synchronize()
+    step = graph.replay if graph is not None else block.step
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for _ in range(args.steps):
+        step()
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = start.elapsed_time(end) / args.steps
+    flops = 3 * shape.conv_flops()
+    tflops = flops / (ms * 1e-3) / 1e12
+    assert torch.isfinite(block.w_arena.float()).all(), "weights left the finite range"
+
+    # per-call durations (eager, HIP events on the launch stream)
+    per_call = profile_calls(block, max(5, args.steps // 2), torch)
+    kernels = []
+    for name, t in per_call:
+        fl, by, bound = call_work(name, shape)
+        k = {"call": name, "ms": round(t, 5), "bound": bound, "bytes": by, "flops": fl}
+        if fl:
+            k["tflops"] = round(fl / (t * 1e-3) / 1e12, 2)
+            k["pct_mfma_peak"] = round(100 * fl / (t * 1e-3) / 1e12 / PEAK_FP16_TFLOPS, 2)
+        k["gbs"] = round(by / (t * 1e-3) / 1e9, 1)
+        k["pct_hbm_peak"] = round(100 * by / (t * 1e-3) / 1e9 / PEAK_HBM_GBS, 2)
+        kernels.append(k)
+    dom = max(kernels, key=lambda k: k["ms"])
+    kind = dom["call"].split("_", 1)[1] if dom["call"].startswith("conv") else dom["call"]
+    src = {"fwd": "conv_igemm.hip", "dgrad": "conv_igemm.hip", "dgrad_add": "conv_igemm.hip",
+           "wgrad": "conv_wgrad.hip"}.get(kind, "bn.hip" if dom["call"].startswith("bn") else "sgd.hip")
+    if dom["bound"] == "mfma":
+        roof = {"bound": "mfma", "achieved": dom["tflops"], "peak": PEAK_FP16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(dom["tflops"] / PEAK_FP16_TFLOPS, 4)}
+    else:
+        roof = {"bound": "hbm", "achieved": dom["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(dom["gbs"] / PEAK_HBM_GBS, 4)}
+    roof["traffic"] = traffic_for(src, dom["call"])
+    roof["kernel"] = dom["call"]
+    roof["ms"] = dom["ms"]
+
+    out = {
+        "metric": METRIC,
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": "resnet50_conv2x_bottleneck_train_step", "batch": shape.n,
+                   "hw": shape.hw, "channels": [shape.c, shape.width, shape.width, shape.c],
+                   "post_scale": shape.post_scale, "layout": "NHWC",
+                   "graph": graph is not None},
+        "images_per_sec": round(shape.n / (ms * 1e-3), 1),
+        "pct_mfma_peak": round(100 * tflops / PEAK_FP16_TFLOPS, 3),
+        "conv_gflop_per_step": round(flops / 1e9, 3),
+        "wall_s_timed": round(wall, 4),
+        "roofline": roof,
+        "kernels": kernels,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(shape, args.cpu_seconds)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -105,6 +105,18 @@ fp16_status fp16_conv_fwd(const fp16_conv_desc* desc, const fp16_t* x, const fp1
 fp16_status fp16_conv_dgrad(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* w,
                             fp16_t* dx, void* ws, size_t ws_bytes, fp16_stream_t stream);
 
+/* Data gradient plus an addend, rounded once:
+ *   dx = round_to_binary16(dgrad(dy, W) + addend)
+ * with the float32 sum of fp16_conv_dgrad and the binary16 addend added in
+ * float32 before the single rounding.  This is the input gradient of a
+ * residual block (Section 4.1: the identity shortcut carries its own
+ * gradient, which joins the branch gradient at the block input).  addend
+ * has dx's shape and layout and may equal dx (accumulate in place); it must
+ * not overlap dx otherwise.  dx must not overlap dy, w or ws. */
+fp16_status fp16_conv_dgrad_add(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* w,
+                                const fp16_t* addend, fp16_t* dx, void* ws, size_t ws_bytes,
+                                fp16_stream_t stream);
+
 /* Weight gradient (the adjoint of fp16_conv_fwd in W):
  *   dW[k,c,r,s] = sum_{n,p,q} dy[n,k,p,q] * x[n,c, p*stride_h - pad_h + r, q*stride_w - pad_w + s].
  * Partial sums over pixel ranges stay float32 in the workspace and are

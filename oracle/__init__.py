@@ -53,6 +53,7 @@ _SIGS = {
     "oracle_conv_fwd": (None, [_P, _P, _P, _P, _P]),
     "oracle_conv_dgrad": (None, [_P, _P, _P, _P, _P]),
     "oracle_conv_wgrad": (None, [_P, _P, _P, _P, _P]),
+    "oracle_conv_dgrad_add": (None, [_P, _P, _P, _P, _P, _P]),
     "oracle_conv_fwd_at": (None, [_P, _P, _P, _P, _I64, _P]),
     "oracle_conv_dgrad_at": (None, [_P, _P, _P, _P, _I64, _P]),
     "oracle_conv_wgrad_at": (None, [_P, _P, _P, _P, _I64, _P]),
@@ -159,6 +160,17 @@ def conv_dgrad(shp, dy, w):
     dx64 = np.empty(xs, np.float64)
     dx16 = np.empty(xs, np.uint16)
     lib().oracle_conv_dgrad(_ptr(shp), _ptr(dy), _ptr(w), _ptr(dx64), _ptr(dx16))
+    return dx64, dx16.view(np.float16)
+
+
+def conv_dgrad_add(shp, dy, w, addend):
+    """Data gradient plus a binary16 addend, one rounding: (dx64, dx16)."""
+    dy, w, addend = _h(dy), _h(w), _h(addend)
+    xs = _act_shape(shp, "x")
+    assert addend.shape == xs, (addend.shape, xs)
+    dx64 = np.empty(xs, np.float64)
+    dx16 = np.empty(xs, np.uint16)
+    lib().oracle_conv_dgrad_add(_ptr(shp), _ptr(dy), _ptr(w), _ptr(addend), _ptr(dx64), _ptr(dx16))
     return dx64, dx16.view(np.float16)
 
 

@@ -299,6 +299,25 @@ void oracle_conv_dgrad(const int32_t* shp, const uint16_t* dy16, const uint16_t*
   }
 }
 
+// Data gradient plus an addend with one rounding: the input gradient of a
+// residual block, where the identity shortcut's gradient (the addend) joins
+// the branch gradient (Section 4.1's residual connection).
+//   dx16 = round_half(dgrad(dy, W) + addend).
+void oracle_conv_dgrad_add(const int32_t* shp, const uint16_t* dy16, const uint16_t* w16,
+                           const uint16_t* add16, double* dx64, uint16_t* dx16) {
+  Conv d(shp);
+  std::vector<double> dy = decode(dy16, d.y_size()), w = decode(w16, d.w_size());
+  const int64_t total = d.x_size();
+#pragma omp parallel for schedule(dynamic, 64)
+  for (int64_t i = 0; i < total; ++i) {
+    int64_t n, c, h, ww;
+    d.x_coords(i, &n, &c, &h, &ww);
+    const double v = conv_dgrad_elem(d, dy.data(), w.data(), n, c, h, ww) + half_to_double(add16[i]);
+    if (dx64) dx64[i] = v;
+    if (dx16) dx16[i] = round_half(v);
+  }
+}
+
 void oracle_conv_wgrad(const int32_t* shp, const uint16_t* x16, const uint16_t* dy16,
                        double* dw64, uint16_t* dw16) {
   Conv d(shp);

@@ -28,7 +28,7 @@ STATUS = {0: "FP16_OK", 1: "FP16_ERR_NULL", 2: "FP16_ERR_SHAPE", 3: "FP16_ERR_LA
           7: "FP16_ERR_UNSUPPORTED", 8: "FP16_ERR_HIP"}
 
 EXPORTS = ["fp16_conv_out_dims", "fp16_conv_workspace_bytes", "fp16_conv_fwd", "fp16_conv_dgrad",
-           "fp16_conv_wgrad", "fp16_bn_workspace_bytes", "fp16_bn_relu", "fp16_bn_relu_bwd",
+           "fp16_conv_dgrad_add", "fp16_conv_wgrad", "fp16_bn_workspace_bytes", "fp16_bn_relu", "fp16_bn_relu_bwd",
            "fp16_sgd_step", "fp16_status_string", "fp16_version"]
 
 
@@ -61,6 +61,7 @@ _SIGS = {
     "fp16_conv_workspace_bytes": (_SZ, [_P, _I32]),
     "fp16_conv_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_conv_dgrad": (ctypes.c_int, [_P, _P, _P, _P, _P, _SZ, _P]),
+    "fp16_conv_dgrad_add": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_conv_wgrad": (ctypes.c_int, [_P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_bn_workspace_bytes": (_SZ, [_P]),
     "fp16_bn_relu": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
@@ -160,6 +161,12 @@ def fp16_conv_fwd(desc, x, w, y, ws=None, ws_bytes=None, stream=None) -> None:
 def fp16_conv_dgrad(desc, dy, w, dx, ws=None, ws_bytes=None, stream=None) -> None:
     _check("fp16_conv_dgrad", lib().fp16_conv_dgrad(ctypes.byref(desc), _ptr(dy), _ptr(w), _ptr(dx),
                                                     _ptr(ws), _wsb(ws, ws_bytes), _stream(stream)))
+
+
+def fp16_conv_dgrad_add(desc, dy, w, addend, dx, ws=None, ws_bytes=None, stream=None) -> None:
+    _check("fp16_conv_dgrad_add", lib().fp16_conv_dgrad_add(
+        ctypes.byref(desc), _ptr(dy), _ptr(w), _ptr(addend), _ptr(dx), _ptr(ws), _wsb(ws, ws_bytes),
+        _stream(stream)))
 
 
 def fp16_conv_wgrad(desc, x, dy, dw, ws=None, ws_bytes=None, stream=None) -> None:

@@ -206,18 +206,23 @@ fp16_status fp16_conv_fwd(const fp16_conv_desc* desc, const fp16_t* x, const fp1
   return FP16_OK;
 }
 
-fp16_status fp16_conv_dgrad(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* w,
-                            fp16_t* dx, void* ws, size_t ws_bytes, fp16_stream_t stream) {
+}  // extern "C"
+
+static fp16_status conv_dgrad_impl(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* w,
+                                   const fp16_t* addend, fp16_t* dx, void* ws, size_t ws_bytes,
+                                   fp16_stream_t stream) {
   ConvDims d;
   fp16_status s = check_conv(desc, &d);
   if (s != FP16_OK) return s;
   if (!dy || !w || !dx) return FP16_ERR_NULL;
-  if (!aligned16(dy) || !aligned16(w) || !aligned16(dx)) return FP16_ERR_MISALIGNED;
+  if (!aligned16(dy) || !aligned16(w) || !aligned16(dx) || (addend && !aligned16(addend)))
+    return FP16_ERR_MISALIGNED;
   const ConvWs L = conv_ws(d, FP16_PASS_DGRAD);
   if ((s = check_ws(L, ws, ws_bytes)) != FP16_OK) return s;
   const size_t xb = (size_t)d.x_elems * 2;
   if (overlap(dx, xb, dy, (size_t)d.y_elems * 2) || overlap(dx, xb, w, (size_t)d.w_elems * 2) ||
-      overlap(dx, xb, ws, L.total))
+      overlap(dx, xb, ws, L.total) || (addend && addend != dx && overlap(dx, xb, addend, xb)) ||
+      (addend && overlap(addend, xb, ws, L.total)))
     return FP16_ERR_ALIASING;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const h16* dye = reinterpret_cast<const h16*>(dy);
@@ -229,6 +234,10 @@ fp16_status fp16_conv_dgrad(const fp16_conv_desc* desc, const fp16_t* dy, const 
     dye = wsp(ws, L.y);
     wk = wsp(ws, L.w);
     dxe = wsp(ws, L.x);
+    if (addend) {  // stage the addend as NHWC in the dx buffer and accumulate in place
+      TRY(launch_nchw_to_nhwc(reinterpret_cast<const h16*>(addend), dxe, d.N, d.C, d.H * d.W, d.C,
+                              st));
+    }
   } else if (d.Kp != d.K) {
     TRY(launch_pad_channels(dye, wsp(ws, L.y), (int64_t)d.N * d.P * d.Q, d.K, d.Kp, st));
     dye = wsp(ws, L.y);
@@ -239,6 +248,7 @@ fp16_status fp16_conv_dgrad(const fp16_conv_desc* desc, const fp16_t* dy, const 
   a.act = dye; a.N = d.N; a.Hi = d.P; a.Wi = d.Q; a.Ci = d.Kp;
   a.stride_h = 1; a.stride_w = 1;
   a.Co = d.C; a.out = dxe; a.OH = d.H; a.OW = d.W; a.ldo = d.C; a.os_h = d.sh; a.os_w = d.sw;
+  a.addend = addend ? (d.layout == FP16_NCHW ? dxe : reinterpret_cast<const h16*>(addend)) : nullptr;
   a.nphase = 0;
   int64_t off = 0;
   for (int ph = 0; ph < d.sh; ++ph) {
@@ -260,6 +270,24 @@ fp16_status fp16_conv_dgrad(const fp16_conv_desc* desc, const fp16_t* dy, const 
     TRY(launch_nhwc_to_nchw(dxe, reinterpret_cast<h16*>(dx), d.N, d.C, d.H * d.W, d.C, st));
   return FP16_OK;
 }
+
+extern "C" {
+
+fp16_status fp16_conv_dgrad(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* w,
+                            fp16_t* dx, void* ws, size_t ws_bytes, fp16_stream_t stream) {
+  return conv_dgrad_impl(desc, dy, w, nullptr, dx, ws, ws_bytes, stream);
+}
+
+fp16_status fp16_conv_dgrad_add(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* w,
+                                const fp16_t* addend, fp16_t* dx, void* ws, size_t ws_bytes,
+                                fp16_stream_t stream) {
+  if (!addend) return FP16_ERR_NULL;
+  return conv_dgrad_impl(desc, dy, w, addend, dx, ws, ws_bytes, stream);
+}
+
+}  // extern "C"
+
+extern "C" {
 
 fp16_status fp16_conv_wgrad(const fp16_conv_desc* desc, const fp16_t* x, const fp16_t* dy,
                             fp16_t* dw, void* ws, size_t ws_bytes, fp16_stream_t stream) {

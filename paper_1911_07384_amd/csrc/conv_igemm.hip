@@ -15,7 +15,8 @@
 // walks k in steps of 32, staging A and B tiles through LDS (double
 // buffered, one barrier per step).  Each wave owns a (BM/WM) x (BN/WN)
 // sub-tile computed with v_mfma_f32_32x32x16_f16 (float32 accumulators).
-// The epilogue rounds each float32 sum once to binary16 (RNE).
+// The epilogue rounds each float32 sum once to binary16 (RNE), optionally
+// after adding a binary16 addend in float32.
 
 #include "kernels.hpp"
 
@@ -155,11 +156,16 @@ __global__ __launch_bounds__(256) void igemm_kernel(const IgemmArgs a) {
       const int j = rem - i * ph.Wo;
       const int oh = i * a.os_h + ph.oph;
       const int ow = j * a.os_w + ph.opw;
-      h16* orow = a.out + ((int64_t)(img * a.OH + oh) * a.OW + ow) * a.ldo;
+      const int64_t obase = ((int64_t)(img * a.OH + oh) * a.OW + ow) * a.ldo;
+      h16* orow = a.out + obase;
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) {
         const int n = n0 + wn * WTN + tn * 32 + lrow;
-        if (n < a.Co) orow[n] = to_h16(acc[tm][tn][e]);
+        if (n < a.Co) {
+          float v = acc[tm][tn][e];
+          if (a.addend) v += to_f32(a.addend[obase + n]);
+          orow[n] = to_h16(v);
+        }
       }
     }
   }

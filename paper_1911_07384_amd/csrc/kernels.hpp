@@ -43,6 +43,7 @@ struct IgemmArgs {
   int stride_h, stride_w;
   int Co;          // output channels (GEMM N)
   h16* out;        // NHWC output [N][OH][OW][ldo], writes channels [0, Co)
+  const h16* addend;  // nullable, laid out like out: out = rne16(acc + addend)
   int OH, OW, ldo;
   int os_h, os_w;
   int nphase;

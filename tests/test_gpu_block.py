@@ -1,0 +1,97 @@
+"""The bottleneck block's training step on the GPU (every call through the C
+ABI): HIP-graph replays match eager execution bit for bit, and the chained
+step agrees with the oracle's composition of the same step."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from oracle.bottleneck import block_step
+from gpu_util import host, note, require_gpu, ulp_dist
+from paper_1911_07384_amd.bottleneck import BlockShape, Bottleneck
+
+pytestmark = pytest.mark.gpu
+
+
+def _outputs(b):
+    return [host(t).copy() for t in (b.dx, b.dw_arena, b.dbn_arena, b.w_arena, b.mw_arena,
+                                     b.bn_arena, b.act[2])]
+
+
+def test_graph_replay_matches_eager():
+    require_gpu()
+    b = Bottleneck(BlockShape(n=4, hw=28), seed=3)
+    s0 = b.state()
+    note("[gpu] block eager x3")
+    eager = []
+    for _ in range(3):
+        b.step()
+        torch.cuda.synchronize()
+        eager.append(_outputs(b))
+    b.load_state(s0)
+    torch.cuda.synchronize()
+    note("[gpu] block graph capture")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        b.step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        b.step()
+    torch.cuda.synchronize()
+    b.load_state(s0)
+    torch.cuda.synchronize()
+    for i in range(3):
+        note(f"[gpu] block graph replay {i}")
+        g.replay()
+        torch.cuda.synchronize()
+        _ = torch.ones(1024, device="cuda").sum().item()  # eager work between replays
+        got = _outputs(b)
+        for a, e in zip(got, eager[i]):
+            assert np.array_equal(a.view(np.uint16) if a.dtype == np.float16 else a,
+                                  e.view(np.uint16) if e.dtype == np.float16 else e), i
+
+
+def test_block_step_matches_oracle_chain():
+    require_gpu()
+    shape = BlockShape(n=2, hw=56)
+    b = Bottleneck(shape, seed=0)
+    x = host(b.x)
+    W = [host(w).copy() for w in b.W]
+    g = [host(t).copy() for t in b.gamma]
+    be = [host(t).copy() for t in b.beta]
+    dout = host(b.dout)
+    note("[gpu] block step n=2")
+    b.step()
+    torch.cuda.synchronize()
+    ref = block_step(x, W, g, be, dout, shape.post_scale, shape.eps, b.lr, b.momentum, b.wd)
+
+    def rel_max(got, want):
+        want = want.astype(np.float64)
+        return np.max(np.abs(got.astype(np.float64) - want)) / np.sqrt(np.mean(want ** 2))
+
+    # forward: every element within the convolution bar
+    for i in range(3):
+        assert rel_max(host(b.cv[i]), ref["conv"][i]) <= 1e-2, i
+        assert rel_max(host(b.act[i]), ref["act"][i]) <= 1e-2, i
+    # backward: a 1-ulp difference in a BN input can flip a ReLU mask bit at an
+    # activation that is almost exactly zero, which changes that one gradient
+    # element by O(its size); all other elements meet the bar, and the
+    # aggregates (weight gradients, BN parameter gradients) do too
+    for got, want in [(host(b.dcv[i]), ref["dconv"][i]) for i in range(3)] + [(host(b.dx), ref["dx"])]:
+        w64 = want.astype(np.float64)
+        rms = np.sqrt(np.mean(w64 ** 2))
+        bad = np.abs(got.astype(np.float64) - w64) > 1e-2 * rms
+        assert bad.mean() <= 1e-4, bad.mean()
+    for i in range(3):
+        assert rel_max(host(b.dW[i]), ref["dW"][i]) <= 2e-2, i
+        assert rel_max(host(b.dgamma[i]), ref["dgamma"][i]) <= 2e-2, i
+        assert rel_max(host(b.dbeta[i]), ref["dbeta"][i]) <= 2e-2, i
+    assert np.array_equal(host(b.dshort).view(np.uint16) != 0, ref["dshort"].view(np.uint16) != 0) \
+        or np.mean(host(b.dshort).view(np.uint16) != ref["dshort"].view(np.uint16)) < 1e-4
+    # SGD: the updated parameters are within one binary16 ulp of the oracle's
+    assert np.max(ulp_dist(host(b.w_arena), ref["w_arena"])) <= 1
+    assert np.max(ulp_dist(host(b.bn_arena), ref["bn_arena"])) <= 1

@@ -205,3 +205,18 @@ def test_sampled_equals_full(layout):
         idx = rng.integers(0, full.size, 200)
         got = fn(shp, a, b, idx)
         assert np.array_equal(got, full.reshape(-1)[idx])
+
+
+@pytest.mark.parametrize("layout", ["NHWC", "NCHW"])
+def test_dgrad_add(layout):
+    shp = oracle.conv_shape(2, 8, 9, 7, 6, 3, 3, 2, 1, layout)
+    x, wt, dy = _inputs(shp, seed=13)
+    addend = synth.normal_f16(x.shape, 1.0, 13, 9)
+    dx64, _ = oracle.conv_dgrad(shp, dy, wt)
+    a64, a16 = oracle.conv_dgrad_add(shp, dy, wt, addend)
+    # the addend enters the float64 sum before the single rounding
+    assert np.allclose(a64, dx64 + addend.astype(np.float64), rtol=0, atol=1e-15)
+    assert np.array_equal(a16.view(np.uint16), a64.astype(np.float16).view(np.uint16))
+    # with a zero gradient the result is the addend, bit for bit (-0 + 0 aside)
+    z64, z16 = oracle.conv_dgrad_add(shp, np.zeros_like(dy), wt, addend)
+    assert np.array_equal(z16.astype(np.float64), addend.astype(np.float64))
