@@ -94,7 +94,7 @@ def profile_calls(block, reps, torch):
     for _ in range(reps):
         # hold the stream with a short device-side spin so the whole step is
         # queued before it starts: calls then run back to back, as in the graph
-        torch.cuda._sleep(20_000_000)
+        torch.cuda._sleep(5_000_000)
         for (name, fn), (a, b) in zip(calls, evs):
             a.record(stream)
             fn()

@@ -15,7 +15,8 @@
 // 16-byte vector and per-channel coefficients are computed once per thread.
 // Other shapes and the NCHW layout use a generic per-element path.
 // Reductions are float32 within a thread, combined in a fixed order within a
-// block and in float64 across blocks: the result does not depend on timing.
+// block and in float64 across blocks (channel-major partials, one wave per
+// channel): the result does not depend on timing.
 
 #include "kernels.hpp"
 
@@ -106,9 +107,10 @@ __device__ __forceinline__ bool relu_mask(bool relu, bool has_y, h16 y, float x,
 
 // ---- block reduction of 16 float32 partials per thread ----------------------
 // red: [16][kT] floats in LDS.  Threads t < CV sum entries t, t+CV, ... (RB of
-// them) in order and return the totals for their 8 channels.
+// them) in order and write the block totals of their 8 channels to the
+// channel-major partial arrays out[c * G + block].
 __device__ __forceinline__ void block_reduce_vec(float (&s1)[8], float (&s2)[8], float* red, int CV,
-                                                 int RB, float* out1, float* out2, int C) {
+                                                 int RB, float* out1, float* out2, int G) {
   const int t = threadIdx.x;
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
@@ -124,8 +126,8 @@ __device__ __forceinline__ void block_reduce_vec(float (&s1)[8], float (&s2)[8],
         a += red[e * kT + r * CV + t];
         b += red[(8 + e) * kT + r * CV + t];
       }
-      out1[(int64_t)blockIdx.x * C + t * 8 + e] = a;
-      out2[(int64_t)blockIdx.x * C + t * 8 + e] = b;
+      out1[(int64_t)(t * 8 + e) * G + blockIdx.x] = a;
+      out2[(int64_t)(t * 8 + e) * G + blockIdx.x] = b;
     }
   }
 }
@@ -160,7 +162,7 @@ __global__ __launch_bounds__(kT) void bn_fwd_reduce_vec(const h16* __restrict__ 
       s2[e] = __builtin_fmaf(d, d, s2[e]);
     }
   }
-  block_reduce_vec(s1, s2, red, CV, RB, ws1, ws2, g.C);
+  block_reduce_vec(s1, s2, red, CV, RB, ws1, ws2, (int)gridDim.x);
 }
 
 __device__ __forceinline__ void block_reduce_1(float& a, float& b, float* red) {
@@ -195,21 +197,40 @@ __global__ __launch_bounds__(kT) void bn_fwd_reduce_gen(const h16* __restrict__ 
   }
   block_reduce_1(s1, s2, red);
   if (threadIdx.x == 0) {
-    ws1[(int64_t)blockIdx.x * g.C + c] = s1;
-    ws2[(int64_t)blockIdx.x * g.C + c] = s2;
+    ws1[(int64_t)c * gridDim.x + blockIdx.x] = s1;
+    ws2[(int64_t)c * gridDim.x + blockIdx.x] = s2;
   }
 }
 
-// mean = K + S1/M, var = S2/M - (S1/M)^2 (float64), rstd = 1/sqrt(var + eps).
-__global__ void bn_fwd_finalize(const h16* __restrict__ x, Geo g, int G, const float* ws1,
-                                const float* ws2, float eps, float* stats) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= g.C) return;
-  double S1 = 0.0, S2 = 0.0;
-  for (int b = 0; b < G; ++b) {
-    S1 += (double)ws1[(int64_t)b * g.C + c];
-    S2 += (double)ws2[(int64_t)b * g.C + c];
+// Sum of the G block partials of channel c in float64: each lane of one wave
+// takes every 64th partial, then a butterfly over the wave (a fixed order, so
+// the total does not depend on timing).
+__device__ __forceinline__ void channel_sums(const float* ws1, const float* ws2, int c, int G,
+                                             double& S1, double& S2) {
+  const int t = threadIdx.x;
+  double a = 0.0, b = 0.0;
+  for (int j = t; j < G; j += 64) {
+    a += (double)ws1[(int64_t)c * G + j];
+    b += (double)ws2[(int64_t)c * G + j];
   }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    a += __shfl_xor(a, off, 64);
+    b += __shfl_xor(b, off, 64);
+  }
+  S1 = a;
+  S2 = b;
+}
+
+// mean = K + S1/M, var = S2/M - (S1/M)^2 (float64), rstd = 1/sqrt(var + eps).
+// One 64-thread block per channel.
+__global__ __launch_bounds__(64) void bn_fwd_finalize(const h16* __restrict__ x, Geo g, int G,
+                                                      const float* ws1, const float* ws2, float eps,
+                                                      float* stats) {
+  const int c = blockIdx.x;
+  double S1, S2;
+  channel_sums(ws1, ws2, c, G, S1, S2);
+  if (threadIdx.x != 0) return;
   const double sh = (double)to_f32(x[geo_at(g, c, 0)]);
   const double md = S1 / (double)g.M;
   double var = S2 / (double)g.M - md * md;
@@ -303,7 +324,7 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
       s2[e] = __builtin_fmaf(gg, xh, s2[e]);
     }
   }
-  block_reduce_vec(s1, s2, red, CV, RB, ws1, ws2, g.C);
+  block_reduce_vec(s1, s2, red, CV, RB, ws1, ws2, (int)gridDim.x);
 }
 
 __global__ __launch_bounds__(kT) void bn_bwd_reduce_gen(const h16* __restrict__ x,
@@ -336,23 +357,22 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_gen(const h16* __restrict__ 
   }
   block_reduce_1(s1, s2, red);
   if (threadIdx.x == 0) {
-    ws1[(int64_t)blockIdx.x * g.C + c] = s1;
-    ws2[(int64_t)blockIdx.x * g.C + c] = s2;
+    ws1[(int64_t)c * gridDim.x + blockIdx.x] = s1;
+    ws2[(int64_t)c * gridDim.x + blockIdx.x] = s2;
   }
 }
 
 // dbeta = S1, dgamma = S2 (one rounding from float64); apply coefficients
 // A = gamma*rstd, B = S1/M, D = S2/M for dx = A * (g - (xhat*D + B)).
-__global__ void bn_bwd_finalize(Geo g, int G, const float* ws1, const float* ws2,
-                                const h16* __restrict__ gamma, const float* __restrict__ stats,
-                                h16* dgamma, h16* dbeta, float* coef) {
-  const int c = blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= g.C) return;
-  double S1 = 0.0, S2 = 0.0;
-  for (int b = 0; b < G; ++b) {
-    S1 += (double)ws1[(int64_t)b * g.C + c];
-    S2 += (double)ws2[(int64_t)b * g.C + c];
-  }
+// One 64-thread block per channel.
+__global__ __launch_bounds__(64) void bn_bwd_finalize(Geo g, int G, const float* ws1,
+                                                      const float* ws2, const h16* __restrict__ gamma,
+                                                      const float* __restrict__ stats, h16* dgamma,
+                                                      h16* dbeta, float* coef) {
+  const int c = blockIdx.x;
+  double S1, S2;
+  channel_sums(ws1, ws2, c, G, S1, S2);
+  if (threadIdx.x != 0) return;
   dbeta[c] = dbl_to_h16(S1);
   dgamma[c] = dbl_to_h16(S2);
   coef[c] = to_f32(gamma[c]) * stats[g.C + c];
@@ -469,8 +489,8 @@ hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const 
                          ws1, ws2);
     else
       hipLaunchKernelGGL(bn_fwd_reduce_gen, dim3(p.G, a.C), dim3(kT), 0, st, x, g, p.rpb, ws1, ws2);
-    hipLaunchKernelGGL(bn_fwd_finalize, dim3(ceil_div(a.C, kT)), dim3(kT), 0, st, x, g, p.G, ws1,
-                       ws2, a.eps, stats);
+    hipLaunchKernelGGL(bn_fwd_finalize, dim3(a.C), dim3(64), 0, st, x, g, p.G, ws1, ws2, a.eps,
+                       stats);
   }
   if (p.vec)
     hipLaunchKernelGGL(bn_fwd_apply_vec, dim3(apply_grid(g.M * p.CV / 4, p.CV)), dim3(kT), 0, st,
@@ -496,8 +516,8 @@ hipError_t launch_bn_bwd(const BnArgs& a, const h16* x, const h16* y, const h16*
   else
     hipLaunchKernelGGL(bn_bwd_reduce_gen, dim3(p.G, a.C), dim3(kT), 0, st, x, y, dy, gamma, beta,
                        res, stats, g, p.rpb, a.post_scale, a.relu, ws1, ws2);
-  hipLaunchKernelGGL(bn_bwd_finalize, dim3(ceil_div(a.C, kT)), dim3(kT), 0, st, g, p.G, ws1, ws2,
-                     gamma, stats, dgamma, dbeta, coef);
+  hipLaunchKernelGGL(bn_bwd_finalize, dim3(a.C), dim3(64), 0, st, g, p.G, ws1, ws2, gamma, stats,
+                     dgamma, dbeta, coef);
   if (p.vec)
     hipLaunchKernelGGL(bn_bwd_apply_vec, dim3(apply_grid(g.M * p.CV / 4, p.CV)), dim3(kT), 0, st,
                        x, y, dy, gamma, beta, res, stats, coef, g, p.CV, a.post_scale, a.relu, dx,

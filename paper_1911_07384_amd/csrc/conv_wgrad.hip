@@ -167,26 +167,39 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
   }
 }
 
-// dw = rne16(sum over splits in order), written KRSC or KCRS with the real C.
-__global__ void wgrad_reduce_kernel(const float* __restrict__ partial, int splits, int K, int Kp,
-                                    int R, int S, int C, int Cp, int layout,
-                                    h16* __restrict__ dw) {
+// dw = rne16(sum over splits), written KRSC or KCRS with the real C.  A block
+// of 256 threads owns 64 consecutive outputs; its four waves each add every
+// fourth split (in order), and the four subtotals are added in a fixed order,
+// so the result is deterministic.
+__global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restrict__ partial,
+                                                           int splits, int K, int Kp, int R, int S,
+                                                           int C, int Cp, int layout,
+                                                           h16* __restrict__ dw) {
+  __shared__ float red[4][64];
   const int64_t Nw = (int64_t)R * S * Cp;
   const int64_t total = (int64_t)K * R * S * C;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
-       i += (int64_t)gridDim.x * blockDim.x) {
-    // i enumerates KRSC with the real C
-    const int c = (int)(i % C);
+  const int lane = threadIdx.x & 63, grp = threadIdx.x >> 6;
+  const int64_t i = (int64_t)blockIdx.x * 64 + lane;  // enumerates KRSC with the real C
+  int64_t src = 0;
+  int k = 0, r = 0, s = 0, c = 0;
+  if (i < total) {
+    c = (int)(i % C);
     int64_t t = i / C;
-    const int s = (int)(t % S);
+    s = (int)(t % S);
     t /= S;
-    const int r = (int)(t % R);
-    const int k = (int)(t / R);
-    const int64_t src = (int64_t)k * Nw + ((int64_t)r * S + s) * Cp + c;
-    float sum = 0.0f;
-    for (int sp = 0; sp < splits; ++sp) sum += partial[(int64_t)sp * Kp * Nw + src];
+    r = (int)(t % R);
+    k = (int)(t / R);
+    src = (int64_t)k * Nw + ((int64_t)r * S + s) * Cp + c;
+  }
+  float sum = 0.0f;
+  if (i < total)
+    for (int sp = grp; sp < splits; sp += 4) sum += partial[(int64_t)sp * Kp * Nw + src];
+  red[grp][lane] = sum;
+  __syncthreads();
+  if (grp == 0 && i < total) {
+    const float v = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
     const int64_t dst = layout == 0 ? i : (((int64_t)k * C + c) * R + r) * S + s;
-    dw[dst] = to_h16(sum);
+    dw[dst] = to_h16(v);
   }
 }
 
@@ -205,7 +218,7 @@ void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int* splits, int* pix
   const int Nw = R * S * Cp;
   const WCfg cfg = wgrad_cfg(K, Nw);
   const int64_t tiles = (int64_t)ceil_div(K, cfg.BM) * ceil_div(Nw, cfg.BN);
-  int64_t want = (1024 + tiles - 1) / tiles;          // about four workgroups per CU
+  int64_t want = (512 + tiles - 1) / tiles;           // about two workgroups per CU
   const int64_t max_splits = (npix + 2 * BKP - 1) / (2 * BKP);  // at least two k-steps each
   if (want > max_splits) want = max_splits;
   if (want < 1) want = 1;
@@ -232,9 +245,7 @@ hipError_t launch_wgrad_partial(const WgradArgs& a, hipStream_t st) {
 hipError_t launch_wgrad_reduce(const float* partial, int splits, int K, int Kp, int R, int S, int C,
                                int Cp, int layout, h16* dw, hipStream_t st) {
   const int64_t total = (int64_t)K * R * S * C;
-  int64_t blocks = (total + 255) / 256;
-  if (blocks > 65536) blocks = 65536;
-  if (blocks < 1) blocks = 1;
+  const int64_t blocks = (total + 63) / 64;
   hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, st, partial, splits,
                      K, Kp, R, S, C, Cp, layout, dw);
   return hipGetLastError();
