@@ -41,6 +41,10 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="target duration of the CPU oracle sample")
+    ap.add_argument("--sweep", action="store_true",
+                    help="also time all 23 ResNet-50 conv shapes (53 layers) at batch 128")
+    ap.add_argument("--no-sweep3x3", action="store_true",
+                    help="skip the batch-128 3x3-layer sweep")
     return ap.parse_args()
 
 
@@ -251,6 +255,20 @@ def main():
         "roofline": roof,
         "kernels": kernels,
     }
+    if args.sweep or not args.no_sweep3x3:
+        from paper_1911_07384_amd import resnet50
+        layers = resnet50.LAYERS if args.sweep else [l for l in resnet50.LAYERS if l.r == 3]
+        del graph
+        torch.cuda.empty_cache()
+        rows = resnet50.sweep(128, layers)
+        summ = resnet50.summarize(rows, PEAK_FP16_TFLOPS)
+        out["conv3x3_b128"] = {k: round(v, 4) for k, v in summ["3x3_16"].items()}
+        out["conv3x3_b128"]["note"] = ("the 16 ResNet-50 3x3 convolutions at batch 128, fwd + dgrad "
+                                       "+ wgrad, each pass timed separately with HIP events")
+        if args.sweep:
+            out["conv53_b128"] = {k: round(v, 4) for k, v in summ["all_53"].items()}
+            out["sweep_layers"] = [{k: (round(v, 3) if isinstance(v, float) else v)
+                                    for k, v in r.items()} for r in rows]
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, args.cpu_seconds)
     print(json.dumps(out), flush=True)

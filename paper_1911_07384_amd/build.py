@@ -56,6 +56,14 @@ def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
         objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
+    # A kernel whose host-side stub was not emitted links fine but fails to
+    # load; catch it here (nm lists such stubs as undefined, "U").
+    for obj in objs:
+        r = subprocess.run(["nm", obj], capture_output=True, text=True, check=True)
+        missing = [l.split()[-1] for l in r.stdout.splitlines()
+                   if l.split()[0] == "U" and "__device_stub__" in l]
+        if missing:
+            raise RuntimeError(f"{obj}: kernel stubs not emitted: {missing}")
     tmp = LIB + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     if verbose:

@@ -11,7 +11,7 @@ using namespace fp16k;
 
 namespace {
 
-constexpr int64_t kMaxElems = (int64_t)1 << 31;  // int32 indexing inside the kernels
+constexpr int64_t kMaxElems = (int64_t)1 << 30;  // buffer-load offsets are 32-bit byte offsets
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
