@@ -106,29 +106,48 @@ __device__ __forceinline__ bool relu_mask(bool relu, bool has_y, h16 y, float x,
 }
 
 // ---- block reduction of 16 float32 partials per thread ----------------------
-// red: [16][kT] floats in LDS.  Threads t < CV sum entries t, t+CV, ... (RB of
-// them) in order and write the block totals of their 8 channels to the
-// channel-major partial arrays out[c * G + block].
+// Thread t holds s1[8], s2[8] for the 8 channels of chunk j = t % CV.  Lanes
+// of one wave that hold the same chunk are combined by a butterfly over the
+// lane bits at or above log2(CV); the waves' totals (or, for CV > 64, the
+// threads' own values) are then summed in a fixed order from LDS and written
+// to the channel-major partial arrays out[c * G + block].  red: [16][kT].
 __device__ __forceinline__ void block_reduce_vec(float (&s1)[8], float (&s2)[8], float* red, int CV,
                                                  int RB, float* out1, float* out2, int G) {
   const int t = threadIdx.x;
+  const int lane = t & 63;
+  int groups;
+  if (CV <= 64) {
+    for (int off = CV; off < 64; off <<= 1) {
 #pragma unroll
-  for (int e = 0; e < 8; ++e) {
-    red[e * kT + t] = s1[e];
-    red[(8 + e) * kT + t] = s2[e];
-  }
-  __syncthreads();
-  if (t < CV) {
+      for (int e = 0; e < 8; ++e) {
+        s1[e] += __shfl_xor(s1[e], off, 64);
+        s2[e] += __shfl_xor(s2[e], off, 64);
+      }
+    }
+    groups = kT / 64;
+    if (lane < CV) {
+      const int slot = (t >> 6) * CV + lane;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        red[e * kT + slot] = s1[e];
+        red[(8 + e) * kT + slot] = s2[e];
+      }
+    }
+  } else {
+    groups = RB;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
-      float a = 0.0f, b = 0.0f;
-      for (int r = 0; r < RB; ++r) {
-        a += red[e * kT + r * CV + t];
-        b += red[(8 + e) * kT + r * CV + t];
-      }
-      out1[(int64_t)(t * 8 + e) * G + blockIdx.x] = a;
-      out2[(int64_t)(t * 8 + e) * G + blockIdx.x] = b;
+      red[e * kT + t] = s1[e];
+      red[(8 + e) * kT + t] = s2[e];
     }
+  }
+  __syncthreads();
+  for (int idx = t; idx < 16 * CV; idx += kT) {
+    const int v = idx / CV, j = idx - v * CV;
+    float acc = red[v * kT + j];
+    for (int gi = 1; gi < groups; ++gi) acc += red[v * kT + gi * CV + j];
+    float* out = v < 8 ? out1 : out2;
+    out[(int64_t)(j * 8 + (v & 7)) * G + blockIdx.x] = acc;
   }
 }
 
@@ -153,13 +172,22 @@ __global__ __launch_bounds__(kT) void bn_fwd_reduce_vec(const h16* __restrict__ 
     s1[e] = 0.0f;
     s2[e] = 0.0f;
   }
-  for (int64_t row = row0 + t / CV; row < row1; row += RB) {
-    const V8 v = load16(x + row * g.C + j * 8);
+  // four rows in flight per thread; the sums still run row by row
+  int64_t row = row0 + t / CV;
+  for (; row < row1; row += 4 * RB) {
+    V8 v[4];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float d = to_f32(v.h[e]) - sh[e];
-      s1[e] += d;
-      s2[e] = __builtin_fmaf(d, d, s2[e]);
+    for (int u = 0; u < 4; ++u)
+      if (row + u * RB < row1) v[u] = load16(x + (row + u * RB) * g.C + j * 8);
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (row + u * RB >= row1) break;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float d = to_f32(v[u].h[e]) - sh[e];
+        s1[e] += d;
+        s2[e] = __builtin_fmaf(d, d, s2[e]);
+      }
     }
   }
   block_reduce_vec(s1, s2, red, CV, RB, ws1, ws2, (int)gridDim.x);
@@ -209,9 +237,24 @@ __device__ __forceinline__ void channel_sums(const float* ws1, const float* ws2,
                                              double& S1, double& S2) {
   const int t = threadIdx.x;
   double a = 0.0, b = 0.0;
-  for (int j = t; j < G; j += 64) {
-    a += (double)ws1[(int64_t)c * G + j];
-    b += (double)ws2[(int64_t)c * G + j];
+  const float* p1 = ws1 + (int64_t)c * G;
+  const float* p2 = ws2 + (int64_t)c * G;
+  for (int j = t; j < G; j += 256) {
+    // four partials per lane in flight, added in index order
+    float u1[4], u2[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = j + 64 * u;
+      u1[u] = i < G ? p1[i] : 0.0f;
+      u2[u] = i < G ? p2[i] : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (j + 64 * u < G) {
+        a += (double)u1[u];
+        b += (double)u2[u];
+      }
+    }
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
@@ -241,27 +284,44 @@ __global__ __launch_bounds__(64) void bn_fwd_finalize(const h16* __restrict__ x,
 
 // ---- forward apply -------------------------------------------------------------
 
+// Each block takes runs of kApplyU * kT consecutive 16-byte vectors; a thread
+// loads its kApplyU vectors (and residual vectors) before it stores any, so
+// several loads per thread are in flight.  y may equal x: every element is
+// read and then written by the same thread.
+constexpr int kApplyU = 4;
+
 __global__ __launch_bounds__(kT) void bn_fwd_apply_vec(const h16* x, const h16* __restrict__ gamma,
                                                        const h16* __restrict__ beta, const h16* res,
                                                        h16* y, const float* __restrict__ stats,
                                                        Geo g, int CV, float s, int relu) {
-  const int64_t gt = (int64_t)blockIdx.x * kT + threadIdx.x;
-  const int64_t stride = (int64_t)gridDim.x * kT;  // a multiple of CV
-  const int j = (int)(gt % CV);
+  const int t = threadIdx.x;
+  const int j = t % CV;  // run starts and kT are multiples of CV
   FwdCoef k[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) k[e] = fwd_coef(stats, gamma, beta, g.C, j * 8 + e, s);
   const int64_t nvec = g.M * CV;
-  for (int64_t v = gt; v < nvec; v += stride) {
-    const V8 xv = load16(x + v * 8);
-    V8 rv;
-    if (res) rv = load16(res + v * 8);
-    V8 out;
+  for (int64_t base = (int64_t)blockIdx.x * (kApplyU * kT) + t; base < nvec;
+       base += (int64_t)gridDim.x * (kApplyU * kT)) {
+    V8 xv[kApplyU], rv[kApplyU];
 #pragma unroll
-    for (int e = 0; e < 8; ++e)
-      out.h[e] = to_h16(fwd_value(to_f32(xv.h[e]), k[e], res != nullptr,
-                                  res ? to_f32(rv.h[e]) : 0.0f, relu != 0));
-    store16(y + v * 8, out);
+    for (int u = 0; u < kApplyU; ++u) {
+      const int64_t v = base + u * kT;
+      if (v < nvec) {
+        xv[u] = load16(x + v * 8);
+        if (res) rv[u] = load16(res + v * 8);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kApplyU; ++u) {
+      const int64_t v = base + u * kT;
+      if (v >= nvec) break;
+      V8 out;
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        out.h[e] = to_h16(fwd_value(to_f32(xv[u].h[e]), k[e], res != nullptr,
+                                    res ? to_f32(rv[u].h[e]) : 0.0f, relu != 0));
+      store16(y + v * 8, out);
+    }
   }
 }
 
@@ -306,22 +366,32 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
     s2[e] = 0.0f;
   }
   const bool has_y = y != nullptr, has_r = res != nullptr && !has_y && relu;
-  for (int64_t row = row0 + t / CV; row < row1; row += RB) {
-    const int64_t off = row * g.C + j * 8;
-    const V8 xv = load16(x + off);
-    const V8 dv = load16(dy + off);
-    V8 yv, rv;
-    if (relu && has_y) yv = load16(y + off);
-    if (has_r) rv = load16(res + off);
+  // two rows in flight per thread; the sums still run row by row
+  for (int64_t row = row0 + t / CV; row < row1; row += 2 * RB) {
+    V8 xv[2], dv[2], yv[2], rv[2];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float xf = to_f32(xv.h[e]);
-      const bool m = relu_mask(relu != 0, has_y, has_y ? yv.h[e] : (h16)0.0f, xf, k[e], has_r,
-                               has_r ? to_f32(rv.h[e]) : 0.0f);
-      const float gg = m ? s * to_f32(dv.h[e]) : 0.0f;
-      const float xh = (xf - k[e].mean) * rstd[e];
-      s1[e] += gg;
-      s2[e] = __builtin_fmaf(gg, xh, s2[e]);
+    for (int u = 0; u < 2; ++u) {
+      if (row + u * RB < row1) {
+        const int64_t off = (row + u * RB) * g.C + j * 8;
+        xv[u] = load16(x + off);
+        dv[u] = load16(dy + off);
+        if (relu && has_y) yv[u] = load16(y + off);
+        if (has_r) rv[u] = load16(res + off);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      if (row + u * RB >= row1) break;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float xf = to_f32(xv[u].h[e]);
+        const bool m = relu_mask(relu != 0, has_y, has_y ? yv[u].h[e] : (h16)0.0f, xf, k[e],
+                                 has_r, has_r ? to_f32(rv[u].h[e]) : 0.0f);
+        const float gg = m ? s * to_f32(dv[u].h[e]) : 0.0f;
+        const float xh = (xf - k[e].mean) * rstd[e];
+        s1[e] += gg;
+        s2[e] = __builtin_fmaf(gg, xh, s2[e]);
+      }
     }
   }
   block_reduce_vec(s1, s2, red, CV, RB, ws1, ws2, (int)gridDim.x);
@@ -389,9 +459,8 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* 
                                                        const float* __restrict__ coef, Geo g,
                                                        int CV, float s, int relu, h16* dx,
                                                        h16* dres) {
-  const int64_t gt = (int64_t)blockIdx.x * kT + threadIdx.x;
-  const int64_t stride = (int64_t)gridDim.x * kT;
-  const int j = (int)(gt % CV);
+  const int t = threadIdx.x;
+  const int j = t % CV;  // run starts and kT are multiples of CV
   FwdCoef k[8];
   float rstd[8], A[8], B[8], D[8];
 #pragma unroll
@@ -405,25 +474,38 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* 
   }
   const bool has_y = y != nullptr, has_r = res != nullptr && !has_y && relu;
   const int64_t nvec = g.M * CV;
-  for (int64_t v = gt; v < nvec; v += stride) {
-    const int64_t off = v * 8;
-    const V8 xv = load16(x + off);
-    const V8 dv = load16(dy + off);
-    V8 yv, rv, o, od;
-    if (relu && has_y) yv = load16(y + off);
-    if (has_r) rv = load16(res + off);
+  constexpr int U = kApplyU / 2;  // vectors per thread and run: 2 or 3 loads each
+  for (int64_t base = (int64_t)blockIdx.x * (U * kT) + t; base < nvec;
+       base += (int64_t)gridDim.x * (U * kT)) {
+    V8 xv[U], dv[U], yv[U], rv[U];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float xf = to_f32(xv.h[e]);
-      const bool m = relu_mask(relu != 0, has_y, has_y ? yv.h[e] : (h16)0.0f, xf, k[e], has_r,
-                               has_r ? to_f32(rv.h[e]) : 0.0f);
-      const float gg = m ? s * to_f32(dv.h[e]) : 0.0f;
-      const float xh = (xf - k[e].mean) * rstd[e];
-      o.h[e] = to_h16(A[e] * (gg - __builtin_fmaf(xh, D[e], B[e])));
-      od.s[e] = m ? dv.s[e] : (uint16_t)0;
+    for (int u = 0; u < U; ++u) {
+      const int64_t v = base + u * kT;
+      if (v < nvec) {
+        xv[u] = load16(x + v * 8);
+        dv[u] = load16(dy + v * 8);
+        if (relu && has_y) yv[u] = load16(y + v * 8);
+        if (has_r) rv[u] = load16(res + v * 8);
+      }
     }
-    store16(dx + off, o);
-    if (dres) store16(dres + off, od);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int64_t v = base + u * kT;
+      if (v >= nvec) break;
+      V8 o, od;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float xf = to_f32(xv[u].h[e]);
+        const bool m = relu_mask(relu != 0, has_y, has_y ? yv[u].h[e] : (h16)0.0f, xf, k[e],
+                                 has_r, has_r ? to_f32(rv[u].h[e]) : 0.0f);
+        const float gg = m ? s * to_f32(dv[u].h[e]) : 0.0f;
+        const float xh = (xf - k[e].mean) * rstd[e];
+        o.h[e] = to_h16(A[e] * (gg - __builtin_fmaf(xh, D[e], B[e])));
+        od.s[e] = m ? dv[u].s[e] : (uint16_t)0;
+      }
+      store16(dx + v * 8, o);
+      if (dres) store16(dres + v * 8, od);
+    }
   }
 }
 
@@ -493,7 +575,8 @@ hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const 
                        stats);
   }
   if (p.vec)
-    hipLaunchKernelGGL(bn_fwd_apply_vec, dim3(apply_grid(g.M * p.CV / 4, p.CV)), dim3(kT), 0, st,
+    hipLaunchKernelGGL(bn_fwd_apply_vec, dim3(apply_grid(g.M * p.CV / kApplyU, p.CV)), dim3(kT),
+                       0, st,
                        x, gamma, beta, res, y, stats, g, p.CV, a.post_scale, a.relu);
   else
     hipLaunchKernelGGL(bn_fwd_apply_gen, dim3(apply_grid(g.M * a.C / 4, 1)), dim3(kT), 0, st, x,
@@ -519,7 +602,8 @@ hipError_t launch_bn_bwd(const BnArgs& a, const h16* x, const h16* y, const h16*
   hipLaunchKernelGGL(bn_bwd_finalize, dim3(a.C), dim3(64), 0, st, g, p.G, ws1, ws2, gamma, stats,
                      dgamma, dbeta, coef);
   if (p.vec)
-    hipLaunchKernelGGL(bn_bwd_apply_vec, dim3(apply_grid(g.M * p.CV / 4, p.CV)), dim3(kT), 0, st,
+    hipLaunchKernelGGL(bn_bwd_apply_vec, dim3(apply_grid(g.M * p.CV / (kApplyU / 2), p.CV)),
+                       dim3(kT), 0, st,
                        x, y, dy, gamma, beta, res, stats, coef, g, p.CV, a.post_scale, a.relu, dx,
                        dres);
   else
