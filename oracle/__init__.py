@@ -62,6 +62,12 @@ _SIGS = {
     "oracle_bn_bwd": (None, [_P, _P, _P, _P, _P, _F32, _F32, _INT, _P, _P, _P, _P, _P, _P, _P]),
     "oracle_sgd_f32": (None, [_P, _P, _P, _I64, _F32, _F32, _F32]),
     "oracle_sgd_f64": (None, [_P, _P, _P, _I64, _F64, _F64, _F64]),
+    "oracle_pool_out_dims": (None, [_P, _P, _P]),
+    "oracle_maxpool_fwd": (None, [_P, _P, _P, _P]),
+    "oracle_maxpool_bwd": (None, [_P, _P, _P, _P]),
+    "oracle_avgpool_fwd": (None, [_P, _P, _P, _P]),
+    "oracle_avgpool_bwd": (None, [_P, _P, _P]),
+    "oracle_softmax_ce": (None, [_I64, _I64, _P, _P, _P, _P, _P, _P, _P]),
 }
 
 
@@ -280,3 +286,80 @@ def sgd_f64(w, g, m, lr, momentum, weight_decay):
     lib().oracle_sgd_f64(_ptr(w), _ptr(g), _ptr(m), w.size, float(lr), float(momentum),
                          float(weight_decay))
     return w.view(np.float16), m.view(np.float16)
+
+
+# ---- pooling, classifier bias and loss --------------------------------------
+
+def pool_shape(n, c, h, w, r, s, stride=1, pad=0, layout="NHWC") -> np.ndarray:
+    sh, sw = (stride, stride) if np.isscalar(stride) else stride
+    ph, pw = (pad, pad) if np.isscalar(pad) else pad
+    return np.array([n, c, h, w, r, s, sh, sw, ph, pw, {"NHWC": 0, "NCHW": 1}[layout]],
+                    dtype=np.int32)
+
+
+def pool_out_dims(shp) -> tuple:
+    p = np.zeros(1, np.int32)
+    q = np.zeros(1, np.int32)
+    lib().oracle_pool_out_dims(_ptr(shp), _ptr(p), _ptr(q))
+    return int(p[0]), int(q[0])
+
+
+def _pool_y_shape(shp):
+    n, c = int(shp[0]), int(shp[1])
+    p, q = pool_out_dims(shp)
+    return (n, p, q, c) if int(shp[10]) == 0 else (n, c, p, q)
+
+
+def maxpool_fwd(shp, x):
+    """Returns (y, idx): binary16 maxima and the winning tap r*S+s (uint8)."""
+    x = _h(x)
+    ys = _pool_y_shape(shp)
+    y = np.empty(ys, np.uint16)
+    idx = np.empty(ys, np.uint8)
+    lib().oracle_maxpool_fwd(_ptr(shp), _ptr(x), _ptr(y), _ptr(idx))
+    return y.view(np.float16), idx
+
+
+def maxpool_bwd(shp, x, dy):
+    x, dy = _h(x), _h(dy)
+    dx = np.empty(x.shape, np.uint16)
+    lib().oracle_maxpool_bwd(_ptr(shp), _ptr(x), _ptr(dy), _ptr(dx))
+    return dx.view(np.float16)
+
+
+def avgpool_fwd(shp, x):
+    """Global average pool: returns (y64, y16), each [N, C]."""
+    x = _h(x)
+    n, c = int(shp[0]), int(shp[1])
+    y64 = np.empty((n, c), np.float64)
+    y16 = np.empty((n, c), np.uint16)
+    lib().oracle_avgpool_fwd(_ptr(shp), _ptr(x), _ptr(y64), _ptr(y16))
+    return y64, y16.view(np.float16)
+
+
+def avgpool_bwd(shp, dy):
+    dy = _h(dy)
+    n, c, h, w = (int(v) for v in shp[:4])
+    xs = (n, h, w, c) if int(shp[10]) == 0 else (n, c, h, w)
+    dx = np.empty(xs, np.uint16)
+    lib().oracle_avgpool_bwd(_ptr(shp), _ptr(dy), _ptr(dx))
+    return dx.view(np.float16)
+
+
+def softmax_ce(z, b, labels):
+    """Classifier bias + softmax cross-entropy, mean over the batch.
+
+    Returns dict(loss (mean), loss_rows, dz, db); dz is the gradient of the
+    mean loss with respect to z (and to the logits), db that of the bias."""
+    z, b = _h(z), _h(b)
+    n, k = z.shape
+    labels = np.ascontiguousarray(labels, dtype=np.int32)
+    assert labels.shape == (n,) and b.shape == (k,)
+    rows = np.empty(n, np.float64)
+    mean = np.empty(1, np.float64)
+    dz = np.empty((n, k), np.uint16)
+    db = np.empty(k, np.uint16)
+    lib().oracle_softmax_ce(n, k, _ptr(z), _ptr(b), _ptr(labels), _ptr(rows), _ptr(mean),
+                            _ptr(dz), _ptr(db))
+    return {"loss": float(mean[0]), "loss_rows": rows, "dz": dz.view(np.float16),
+            "db": db.view(np.float16)}

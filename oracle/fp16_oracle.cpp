@@ -19,7 +19,10 @@
 //     (N, H, W), with the 0.25 output multiplier of Section 4.2 and the ReLU
 //     that follows each BN (Section 1);
 //   * the optimiser is momentum SGD with FP16 weights and FP16 momentum
-//     (Section 5.1 recipe, Section 5.2 no master copy).
+//     (Section 5.1 recipe, Section 5.2 no master copy);
+//   * the rest of ResNet-50 (Section 5.1): 3x3 stride-2 max pooling after the
+//     stem, global average pooling, the fully connected classifier with bias,
+//     and the softmax cross-entropy loss averaged over the local batch.
 //
 // Readings where the paper is silent are listed with each function.
 //
@@ -536,6 +539,182 @@ void oracle_sgd_f64(uint16_t* w16, const uint16_t* g16, uint16_t* m16, int64_t n
     m16[i] = m1;
     w16[i] = w1;
   }
+}
+
+}  // extern "C"
+
+namespace {
+
+// ---- pooling ----------------------------------------------------------------
+// Geometry shp = {N, C, H, W, R, S, stride_h, stride_w, pad_h, pad_w, layout}
+// (layout 0: NHWC, 1: NCHW); output P = floor((H + 2 pad_h - R) / stride_h) + 1.
+//
+// Max pooling (the 3x3 stride-2 pool after ResNet-50's stem): positions in the
+// padding are not candidates.  The window is scanned in (r, s) order; a
+// later element replaces the running maximum only if it is strictly larger,
+// and the first NaN met is kept (NaN propagates; reading: ties and NaN go to
+// the earliest position, so the backward has one well-defined target).
+// idx (may be NULL) receives the winning tap r * S + s of each output.
+
+struct Pool {
+  int64_t N, C, H, W, R, S, sh, sw, ph, pw, P, Q;
+  int layout;
+  explicit Pool(const int32_t* s) {
+    N = s[0]; C = s[1]; H = s[2]; W = s[3]; R = s[4]; S = s[5];
+    sh = s[6]; sw = s[7]; ph = s[8]; pw = s[9]; layout = s[10];
+    P = (H + 2 * ph - R) / sh + 1;
+    Q = (W + 2 * pw - S) / sw + 1;
+  }
+  int64_t xi(int64_t n, int64_t c, int64_t h, int64_t w) const {
+    return layout == 0 ? ((n * H + h) * W + w) * C + c : ((n * C + c) * H + h) * W + w;
+  }
+  int64_t yi(int64_t n, int64_t c, int64_t p, int64_t q) const {
+    return layout == 0 ? ((n * P + p) * Q + q) * C + c : ((n * C + c) * P + p) * Q + q;
+  }
+  // winning tap of output (n, c, p, q), or -1 if the window has no position
+  // inside the image
+  int64_t argmax(const uint16_t* x16, int64_t n, int64_t c, int64_t p, int64_t q) const {
+    int64_t best = -1;
+    double bv = 0.0;
+    for (int64_t r = 0; r < R; ++r) {
+      const int64_t h = p * sh - ph + r;
+      if (h < 0 || h >= H) continue;
+      for (int64_t s = 0; s < S; ++s) {
+        const int64_t w = q * sw - pw + s;
+        if (w < 0 || w >= W) continue;
+        const double v = half_to_double(x16[xi(n, c, h, w)]);
+        if (best < 0 || (!std::isnan(bv) && (std::isnan(v) || v > bv))) {
+          best = r * S + s;
+          bv = v;
+        }
+      }
+    }
+    return best;
+  }
+};
+
+}  // namespace
+
+extern "C" {
+
+void oracle_pool_out_dims(const int32_t* shp, int32_t* p, int32_t* q) {
+  Pool d(shp);
+  *p = (int32_t)d.P;
+  *q = (int32_t)d.Q;
+}
+
+// y = the winning element itself (no rounding: it is already binary16).
+void oracle_maxpool_fwd(const int32_t* shp, const uint16_t* x16, uint16_t* y16, uint8_t* idx) {
+  Pool d(shp);
+#pragma omp parallel for collapse(2) schedule(static)
+  for (int64_t n = 0; n < d.N; ++n)
+    for (int64_t c = 0; c < d.C; ++c)
+      for (int64_t p = 0; p < d.P; ++p)
+        for (int64_t q = 0; q < d.Q; ++q) {
+          const int64_t t = d.argmax(x16, n, c, p, q);
+          const int64_t o = d.yi(n, c, p, q);
+          // a window with no position inside the image has no input; its
+          // output is +0 (the ABI rejects such geometries)
+          y16[o] = t < 0 ? (uint16_t)0 : x16[d.xi(n, c, p * d.sh - d.ph + t / d.S,
+                                                   q * d.sw - d.pw + t % d.S)];
+          if (idx) idx[o] = (uint8_t)(t < 0 ? 255 : t);
+        }
+}
+
+// dx[n,c,h,w] = sum of dy over the outputs whose winning position is (h, w),
+// summed in float64 (exact: at most R*S binary16 terms here) and rounded
+// once; +0 where no output selects the position.
+void oracle_maxpool_bwd(const int32_t* shp, const uint16_t* x16, const uint16_t* dy16,
+                        uint16_t* dx16) {
+  Pool d(shp);
+  const int64_t nx = d.N * d.C * d.H * d.W;
+  std::vector<double> acc((size_t)nx, 0.0);
+#pragma omp parallel for collapse(2) schedule(static)
+  for (int64_t n = 0; n < d.N; ++n)
+    for (int64_t c = 0; c < d.C; ++c)
+      for (int64_t p = 0; p < d.P; ++p)
+        for (int64_t q = 0; q < d.Q; ++q) {
+          const int64_t t = d.argmax(x16, n, c, p, q);
+          if (t < 0) continue;
+          const int64_t h = p * d.sh - d.ph + t / d.S, w = q * d.sw - d.pw + t % d.S;
+          acc[(size_t)d.xi(n, c, h, w)] += half_to_double(dy16[d.yi(n, c, p, q)]);
+        }
+  for (int64_t i = 0; i < nx; ++i) dx16[i] = round_half(acc[(size_t)i]);
+}
+
+// Global average pooling (ResNet-50's pool before the classifier), shp as for
+// pooling with R = H, S = W: y[n,c] = (sum over the H x W grid of x) / (H W),
+// with the sum exact in float64, one float64 division, one rounding.
+// y is [N, C] (the NHWC and NCHW orders coincide for a 1 x 1 grid).
+void oracle_avgpool_fwd(const int32_t* shp, const uint16_t* x16, double* y64, uint16_t* y16) {
+  Pool d(shp);
+#pragma omp parallel for collapse(2) schedule(static)
+  for (int64_t n = 0; n < d.N; ++n)
+    for (int64_t c = 0; c < d.C; ++c) {
+      double sum = 0.0;
+      for (int64_t h = 0; h < d.H; ++h)
+        for (int64_t w = 0; w < d.W; ++w) sum += half_to_double(x16[d.xi(n, c, h, w)]);
+      const double v = sum / (double)(d.H * d.W);
+      if (y64) y64[n * d.C + c] = v;
+      if (y16) y16[n * d.C + c] = round_half(v);
+    }
+}
+
+// Its adjoint: every position of the grid receives dy[n,c] / (H W), rounded once.
+void oracle_avgpool_bwd(const int32_t* shp, const uint16_t* dy16, uint16_t* dx16) {
+  Pool d(shp);
+#pragma omp parallel for collapse(2) schedule(static)
+  for (int64_t n = 0; n < d.N; ++n)
+    for (int64_t c = 0; c < d.C; ++c) {
+      const uint16_t v = round_half(half_to_double(dy16[n * d.C + c]) / (double)(d.H * d.W));
+      for (int64_t h = 0; h < d.H; ++h)
+        for (int64_t w = 0; w < d.W; ++w) dx16[d.xi(n, c, h, w)] = v;
+    }
+}
+
+// ---- classifier bias and softmax cross-entropy -------------------------------
+// z[N, K]: the classifier's matrix product (a 1x1 convolution, stored in
+// binary16); b[K]: its bias; labels[N] in [0, K).
+//   l = round_half(z + b)                     (the logits, a binary16 tensor)
+//   loss_n = log(sum_j exp(l_nj - m)) + (m - l_n,label), m = max_j l_nj (float64)
+//   mean loss = (1/N) sum_n loss_n            (average over the local batch)
+//   dl_nj = (softmax(l_n)_j - [j == label]) / N, rounded once   (= dz)
+//   db_j = sum_n dl_nj over the stored dl, exact in float64, rounded once.
+// loss_rows (may be NULL) receives loss_n; loss_mean (may be NULL) the mean.
+void oracle_softmax_ce(int64_t N, int64_t K, const uint16_t* z16, const uint16_t* b16,
+                       const int32_t* labels, double* loss_rows, double* loss_mean,
+                       uint16_t* dz16, uint16_t* db16) {
+  std::vector<double> rows((size_t)N);
+#pragma omp parallel for schedule(static)
+  for (int64_t n = 0; n < N; ++n) {
+    std::vector<double> l((size_t)K);
+    double m = -INFINITY;
+    for (int64_t j = 0; j < K; ++j) {
+      l[(size_t)j] = half_to_double(round_half(half_to_double(z16[n * K + j]) +
+                                               half_to_double(b16[j])));
+      if (l[(size_t)j] > m) m = l[(size_t)j];
+    }
+    double s = 0.0;
+    for (int64_t j = 0; j < K; ++j) s += std::exp(l[(size_t)j] - m);
+    const int64_t y = labels[n];
+    rows[(size_t)n] = std::log(s) + (m - l[(size_t)y]);  // the difference is exact
+    for (int64_t j = 0; j < K; ++j) {
+      const double pj = std::exp(l[(size_t)j] - m) / s;
+      dz16[n * K + j] = round_half((pj - (j == y ? 1.0 : 0.0)) / (double)N);
+    }
+  }
+  double tot = 0.0;
+  for (int64_t n = 0; n < N; ++n) {
+    if (loss_rows) loss_rows[n] = rows[(size_t)n];
+    tot += rows[(size_t)n];
+  }
+  if (loss_mean) *loss_mean = tot / (double)N;
+  if (db16)
+    for (int64_t j = 0; j < K; ++j) {
+      double a = 0.0;
+      for (int64_t n = 0; n < N; ++n) a += half_to_double(dz16[n * K + j]);
+      db16[j] = round_half(a);
+    }
 }
 
 }  // extern "C"
