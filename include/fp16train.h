@@ -175,6 +175,72 @@ fp16_status fp16_bn_relu_bwd(const fp16_bn_desc* desc, const fp16_t* x, const fp
 fp16_status fp16_sgd_step(fp16_t* w, const fp16_t* g, fp16_t* m, size_t n, float lr,
                           float momentum, float weight_decay, fp16_stream_t stream);
 
+/* ---- the rest of ResNet-50 around the residual blocks (Section 5.1) ---- */
+
+/* Pooling problem on x [N,C,H,W] (logical) with an R x S window:
+ * output [N,C,P,Q], P = (H + 2*pad_h - R)/stride_h + 1 (likewise Q).
+ * Layouts as for activations above. */
+typedef struct {
+  int32_t n, c, h, w;
+  int32_t r, s;
+  int32_t stride_h, stride_w;
+  int32_t pad_h, pad_w;
+  int32_t layout; /* fp16_layout */
+} fp16_pool_desc;
+
+/* Output spatial size of a pooling window; FP16_ERR_SHAPE if invalid.
+ * Valid: all sizes >= 1, 1 <= r, s <= 15, 1 <= strides <= 16,
+ * 0 <= pad_h < r, 0 <= pad_w < s (every window meets the image). */
+fp16_status fp16_pool_out_dims(const fp16_pool_desc* desc, int32_t* p, int32_t* q);
+
+/* Max pooling (the 3x3 stride-2 pool after ResNet-50's stem).  Positions in
+ * the padding are not candidates.  Each window is scanned in (r, s) order; a
+ * later element replaces the running maximum only if it is strictly larger,
+ * and the first NaN met is kept.  y[n,c,p,q] is the winning element (no
+ * rounding), idx[n,c,p,q] its tap r*S + s (one byte per output, laid out
+ * like y).  y and idx must not overlap x or each other; idx is 16-byte
+ * aligned like every buffer. */
+fp16_status fp16_maxpool_fwd(const fp16_pool_desc* desc, const fp16_t* x, fp16_t* y,
+                             uint8_t* idx, fp16_stream_t stream);
+
+/* Max-pooling backward from the forward's idx:
+ *   dx[n,c,h,w] = sum of dy[n,c,p,q] over the outputs whose winning position
+ *                 is (h, w), added in float64 (exact) and rounded once;
+ *                 +0 where no output selects the position.
+ * Every element of dx is written.  dx must not overlap dy or idx. */
+fp16_status fp16_maxpool_bwd(const fp16_pool_desc* desc, const uint8_t* idx, const fp16_t* dy,
+                             fp16_t* dx, fp16_stream_t stream);
+
+/* Global average pooling (before ResNet-50's classifier): the window must be
+ * the whole image (r = h, s = w, pads 0; FP16_ERR_UNSUPPORTED otherwise).
+ *   y[n,c] = (sum over the H x W grid of x[n,c,.,.]) / (H*W)
+ * with the sum exact in float64, one float64 division and one rounding.
+ * y is [N,C] in both layouts.  y must not overlap x. */
+fp16_status fp16_avgpool_fwd(const fp16_pool_desc* desc, const fp16_t* x, fp16_t* y,
+                             fp16_stream_t stream);
+
+/* Its adjoint: dx[n,c,h,w] = round_to_binary16(dy[n,c] / (H*W)) (float64
+ * division).  dy is [N,C]; dx has x's shape and layout and must not overlap dy. */
+fp16_status fp16_avgpool_bwd(const fp16_pool_desc* desc, const fp16_t* dy, fp16_t* dx,
+                             fp16_stream_t stream);
+
+/* Classifier bias and softmax cross-entropy averaged over the batch.
+ * z [N,K] is the classifier's product (a 1x1 convolution), bias [K],
+ * labels [N] int32 in [0, K):
+ *   l = round_to_binary16(z + bias)                       (the logits)
+ *   loss[n] = log(sum_j exp(l_nj - m_n)) + (m_n - l_n,label),  m_n = max_j l_nj
+ *   dz[n,j] = round_to_binary16((softmax(l_n)_j - [j == label_n]) / N)
+ *   dbias[j] = round_to_binary16(sum_n dz[n,j])           (exact float64 sum)
+ * computed in float64; loss (float32, N values) is per sample, its mean is
+ * the batch loss; dz is the gradient of that mean with respect to z and the
+ * logits (no loss scaling: entries near 1/(N*K) are binary16 subnormals and
+ * are kept).  A label outside [0, K) gives a NaN loss for its row and no
+ * one-hot term.  dz may equal z; otherwise no output overlaps an input or
+ * another output.  1 <= K <= 65535. */
+fp16_status fp16_softmax_ce(int32_t n, int32_t k, const fp16_t* z, const fp16_t* bias,
+                            const int32_t* labels, float* loss, fp16_t* dz, fp16_t* dbias,
+                            fp16_stream_t stream);
+
 /* Human-readable name of a status code (static string). */
 const char* fp16_status_string(fp16_status status);
 

@@ -29,7 +29,9 @@ STATUS = {0: "FP16_OK", 1: "FP16_ERR_NULL", 2: "FP16_ERR_SHAPE", 3: "FP16_ERR_LA
 
 EXPORTS = ["fp16_conv_out_dims", "fp16_conv_workspace_bytes", "fp16_conv_fwd", "fp16_conv_dgrad",
            "fp16_conv_dgrad_add", "fp16_conv_wgrad", "fp16_bn_workspace_bytes", "fp16_bn_relu", "fp16_bn_relu_bwd",
-           "fp16_sgd_step", "fp16_status_string", "fp16_version"]
+           "fp16_sgd_step", "fp16_pool_out_dims", "fp16_maxpool_fwd", "fp16_maxpool_bwd",
+           "fp16_avgpool_fwd", "fp16_avgpool_bwd", "fp16_softmax_ce", "fp16_status_string",
+           "fp16_version"]
 
 
 class Fp16Error(RuntimeError):
@@ -51,6 +53,11 @@ class BnDesc(ctypes.Structure):
                 ("use_stats", ctypes.c_int32)]
 
 
+class PoolDesc(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("n", "c", "h", "w", "r", "s", "stride_h", "stride_w", "pad_h", "pad_w", "layout")]
+
+
 _lib = None
 _P = ctypes.c_void_p
 _SZ = ctypes.c_size_t
@@ -67,6 +74,12 @@ _SIGS = {
     "fp16_bn_relu": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_bn_relu_bwd": (ctypes.c_int, [_P] * 13 + [_SZ, _P]),
     "fp16_sgd_step": (ctypes.c_int, [_P, _P, _P, _SZ, _F, _F, _F, _P]),
+    "fp16_pool_out_dims": (ctypes.c_int, [_P, _P, _P]),
+    "fp16_maxpool_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P]),
+    "fp16_maxpool_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P]),
+    "fp16_avgpool_fwd": (ctypes.c_int, [_P, _P, _P, _P]),
+    "fp16_avgpool_bwd": (ctypes.c_int, [_P, _P, _P, _P]),
+    "fp16_softmax_ce": (ctypes.c_int, [_I32, _I32, _P, _P, _P, _P, _P, _P, _P]),
     "fp16_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "fp16_version": (ctypes.c_char_p, []),
 }
@@ -106,8 +119,8 @@ def _ptr(t):
     if isinstance(t, int):
         return t
     import torch
-    if t.dtype not in (torch.float16, torch.float32, torch.uint8):
-        raise TypeError(f"expected float16/float32/uint8 tensor, got {t.dtype}")
+    if t.dtype not in (torch.float16, torch.float32, torch.uint8, torch.int32):
+        raise TypeError(f"expected float16/float32/uint8/int32 tensor, got {t.dtype}")
     if not t.is_contiguous():
         raise ValueError("tensor must be contiguous")
     return t.data_ptr()
@@ -199,6 +212,45 @@ def fp16_sgd_step(w, g, m, n=None, lr=0.1, momentum=0.9, weight_decay=1e-4, stre
     _check("fp16_sgd_step", lib().fp16_sgd_step(_ptr(w), _ptr(g), _ptr(m), int(n), float(lr),
                                                 float(momentum), float(weight_decay),
                                                 _stream(stream)))
+
+
+def pool_desc(n, c, h, w, r, s, stride=1, pad=0, layout="NHWC") -> PoolDesc:
+    sh, sw = (stride, stride) if isinstance(stride, int) else stride
+    ph, pw = (pad, pad) if isinstance(pad, int) else pad
+    return PoolDesc(n, c, h, w, r, s, sh, sw, ph, pw, _LAYOUTS[layout])
+
+
+def fp16_pool_out_dims(desc: PoolDesc):
+    p, q = ctypes.c_int32(), ctypes.c_int32()
+    _check("fp16_pool_out_dims", lib().fp16_pool_out_dims(ctypes.byref(desc), ctypes.byref(p),
+                                                          ctypes.byref(q)))
+    return p.value, q.value
+
+
+def fp16_maxpool_fwd(desc, x, y, idx, stream=None) -> None:
+    _check("fp16_maxpool_fwd", lib().fp16_maxpool_fwd(ctypes.byref(desc), _ptr(x), _ptr(y),
+                                                      _ptr(idx), _stream(stream)))
+
+
+def fp16_maxpool_bwd(desc, idx, dy, dx, stream=None) -> None:
+    _check("fp16_maxpool_bwd", lib().fp16_maxpool_bwd(ctypes.byref(desc), _ptr(idx), _ptr(dy),
+                                                      _ptr(dx), _stream(stream)))
+
+
+def fp16_avgpool_fwd(desc, x, y, stream=None) -> None:
+    _check("fp16_avgpool_fwd", lib().fp16_avgpool_fwd(ctypes.byref(desc), _ptr(x), _ptr(y),
+                                                      _stream(stream)))
+
+
+def fp16_avgpool_bwd(desc, dy, dx, stream=None) -> None:
+    _check("fp16_avgpool_bwd", lib().fp16_avgpool_bwd(ctypes.byref(desc), _ptr(dy), _ptr(dx),
+                                                      _stream(stream)))
+
+
+def fp16_softmax_ce(n, k, z, bias, labels, loss, dz, dbias, stream=None) -> None:
+    _check("fp16_softmax_ce", lib().fp16_softmax_ce(int(n), int(k), _ptr(z), _ptr(bias),
+                                                    _ptr(labels), _ptr(loss), _ptr(dz),
+                                                    _ptr(dbias), _stream(stream)))
 
 
 def _wsb(ws, ws_bytes):

@@ -429,4 +429,128 @@ fp16_status fp16_sgd_step(fp16_t* w, const fp16_t* g, fp16_t* m, size_t n, float
                                static_cast<hipStream_t>(stream)));
 }
 
+// ---- pooling --------------------------------------------------------------------
+
+static fp16_status check_pool(const fp16_pool_desc* d, PoolArgs* a) {
+  if (!d) return FP16_ERR_NULL;
+  if (d->layout != FP16_NHWC && d->layout != FP16_NCHW) return FP16_ERR_LAYOUT;
+  if (d->n < 1 || d->c < 1 || d->h < 1 || d->w < 1 || d->r < 1 || d->s < 1 || d->r > 15 ||
+      d->s > 15 || d->stride_h < 1 || d->stride_w < 1 || d->stride_h > 16 || d->stride_w > 16 ||
+      d->pad_h < 0 || d->pad_w < 0 || d->pad_h >= d->r || d->pad_w >= d->s ||
+      d->c > 65535 || d->h > 65535 || d->w > 65535)
+    return FP16_ERR_SHAPE;
+  if (d->h + 2 * d->pad_h < d->r || d->w + 2 * d->pad_w < d->s) return FP16_ERR_SHAPE;
+  if ((int64_t)d->n * d->c * d->h * d->w >= kMaxElems) return FP16_ERR_SHAPE;
+  a->N = d->n; a->C = d->c; a->H = d->h; a->W = d->w; a->R = d->r; a->S = d->s;
+  a->sh = d->stride_h; a->sw = d->stride_w; a->ph = d->pad_h; a->pw = d->pad_w;
+  a->layout = d->layout;
+  a->P = (a->H + 2 * a->ph - a->R) / a->sh + 1;
+  a->Q = (a->W + 2 * a->pw - a->S) / a->sw + 1;
+  return FP16_OK;
+}
+
+fp16_status fp16_pool_out_dims(const fp16_pool_desc* desc, int32_t* p, int32_t* q) {
+  PoolArgs a;
+  const fp16_status s = check_pool(desc, &a);
+  if (s != FP16_OK) return s;
+  if (!p || !q) return FP16_ERR_NULL;
+  *p = a.P;
+  *q = a.Q;
+  return FP16_OK;
+}
+
+fp16_status fp16_maxpool_fwd(const fp16_pool_desc* desc, const fp16_t* x, fp16_t* y,
+                             uint8_t* idx, fp16_stream_t stream) {
+  PoolArgs a;
+  const fp16_status s = check_pool(desc, &a);
+  if (s != FP16_OK) return s;
+  if (!x || !y || !idx) return FP16_ERR_NULL;
+  if (!aligned16(x) || !aligned16(y) || !aligned16(idx)) return FP16_ERR_MISALIGNED;
+  const size_t xb = (size_t)a.N * a.C * a.H * a.W * 2;
+  const size_t yn = (size_t)a.N * a.C * a.P * a.Q;
+  if (overlap(y, yn * 2, x, xb) || overlap(idx, yn, x, xb) || overlap(y, yn * 2, idx, yn))
+    return FP16_ERR_ALIASING;
+  return hip_status(launch_maxpool_fwd(a, reinterpret_cast<const h16*>(x),
+                                       reinterpret_cast<h16*>(y), idx,
+                                       static_cast<hipStream_t>(stream)));
+}
+
+fp16_status fp16_maxpool_bwd(const fp16_pool_desc* desc, const uint8_t* idx, const fp16_t* dy,
+                             fp16_t* dx, fp16_stream_t stream) {
+  PoolArgs a;
+  const fp16_status s = check_pool(desc, &a);
+  if (s != FP16_OK) return s;
+  if (!idx || !dy || !dx) return FP16_ERR_NULL;
+  if (!aligned16(idx) || !aligned16(dy) || !aligned16(dx)) return FP16_ERR_MISALIGNED;
+  const size_t xb = (size_t)a.N * a.C * a.H * a.W * 2;
+  const size_t yn = (size_t)a.N * a.C * a.P * a.Q;
+  if (overlap(dx, xb, dy, yn * 2) || overlap(dx, xb, idx, yn)) return FP16_ERR_ALIASING;
+  return hip_status(launch_maxpool_bwd(a, idx, reinterpret_cast<const h16*>(dy),
+                                       reinterpret_cast<h16*>(dx),
+                                       static_cast<hipStream_t>(stream)));
+}
+
+// The global window only.  With r, s <= 15 the window holds at most 225
+// binary16 terms, so every float64 sum of them is exact (|sum| < 2^24 in
+// units of 2^-24 fits in 53 bits).
+static fp16_status check_global_pool(const fp16_pool_desc* desc, PoolArgs* a) {
+  const fp16_status s = check_pool(desc, a);
+  if (s != FP16_OK) return s;
+  if (a->R != a->H || a->S != a->W || a->ph != 0 || a->pw != 0) return FP16_ERR_UNSUPPORTED;
+  return FP16_OK;
+}
+
+fp16_status fp16_avgpool_fwd(const fp16_pool_desc* desc, const fp16_t* x, fp16_t* y,
+                             fp16_stream_t stream) {
+  PoolArgs a;
+  const fp16_status s = check_global_pool(desc, &a);
+  if (s != FP16_OK) return s;
+  if (!x || !y) return FP16_ERR_NULL;
+  if (!aligned16(x) || !aligned16(y)) return FP16_ERR_MISALIGNED;
+  if (overlap(y, (size_t)a.N * a.C * 2, x, (size_t)a.N * a.C * a.H * a.W * 2))
+    return FP16_ERR_ALIASING;
+  return hip_status(launch_avgpool_fwd(a, reinterpret_cast<const h16*>(x),
+                                       reinterpret_cast<h16*>(y),
+                                       static_cast<hipStream_t>(stream)));
+}
+
+fp16_status fp16_avgpool_bwd(const fp16_pool_desc* desc, const fp16_t* dy, fp16_t* dx,
+                             fp16_stream_t stream) {
+  PoolArgs a;
+  const fp16_status s = check_global_pool(desc, &a);
+  if (s != FP16_OK) return s;
+  if (!dy || !dx) return FP16_ERR_NULL;
+  if (!aligned16(dy) || !aligned16(dx)) return FP16_ERR_MISALIGNED;
+  if (overlap(dx, (size_t)a.N * a.C * a.H * a.W * 2, dy, (size_t)a.N * a.C * 2))
+    return FP16_ERR_ALIASING;
+  return hip_status(launch_avgpool_bwd(a, reinterpret_cast<const h16*>(dy),
+                                       reinterpret_cast<h16*>(dx),
+                                       static_cast<hipStream_t>(stream)));
+}
+
+// ---- classifier bias and softmax cross-entropy ------------------------------------
+
+fp16_status fp16_softmax_ce(int32_t n, int32_t k, const fp16_t* z, const fp16_t* bias,
+                            const int32_t* labels, float* loss, fp16_t* dz, fp16_t* dbias,
+                            fp16_stream_t stream) {
+  // n <= 2^24 keeps the float64 batch sum of the bias gradient exact
+  if (n < 1 || k < 1 || k > 65535 || n > (1 << 24)) return FP16_ERR_SHAPE;
+  if ((int64_t)n * k >= kMaxElems) return FP16_ERR_SHAPE;
+  if (!z || !bias || !labels || !loss || !dz || !dbias) return FP16_ERR_NULL;
+  if (!aligned16(z) || !aligned16(bias) || !aligned16(labels) || !aligned16(loss) ||
+      !aligned16(dz) || !aligned16(dbias))
+    return FP16_ERR_MISALIGNED;
+  const size_t zb = (size_t)n * k * 2, kb = (size_t)k * 2, nb = (size_t)n * 4;
+  if ((dz != z && overlap(dz, zb, z, zb)) || overlap(dz, zb, bias, kb) ||
+      overlap(dz, zb, labels, nb) || overlap(dz, zb, loss, nb) || overlap(dz, zb, dbias, kb) ||
+      overlap(dbias, kb, z, zb) || overlap(dbias, kb, bias, kb) || overlap(dbias, kb, labels, nb) ||
+      overlap(dbias, kb, loss, nb) || overlap(loss, nb, z, zb) || overlap(loss, nb, bias, kb) ||
+      overlap(loss, nb, labels, nb))
+    return FP16_ERR_ALIASING;
+  return hip_status(launch_softmax_ce(n, k, reinterpret_cast<const h16*>(z),
+                                      reinterpret_cast<const h16*>(bias), labels, loss,
+                                      reinterpret_cast<h16*>(dz), reinterpret_cast<h16*>(dbias),
+                                      static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

@@ -110,4 +110,19 @@ hipError_t launch_bn_bwd(const BnArgs& a, const h16* x, const h16* y, const h16*
                          const h16* gamma, const h16* beta, const h16* res, const float* stats,
                          h16* dx, h16* dgamma, h16* dbeta, h16* dres, void* ws, hipStream_t st);
 
+// ---- pooling (pool.hip) ----------------------------------------------------
+struct PoolArgs {
+  int N, C, H, W, R, S, sh, sw, ph, pw, P, Q, layout;
+};
+hipError_t launch_maxpool_fwd(const PoolArgs& a, const h16* x, h16* y, uint8_t* idx,
+                              hipStream_t st);
+hipError_t launch_maxpool_bwd(const PoolArgs& a, const uint8_t* idx, const h16* dy, h16* dx,
+                              hipStream_t st);
+hipError_t launch_avgpool_fwd(const PoolArgs& a, const h16* x, h16* y, hipStream_t st);
+hipError_t launch_avgpool_bwd(const PoolArgs& a, const h16* dy, h16* dx, hipStream_t st);
+
+// ---- classifier bias and loss (loss.hip) -------------------------------------
+hipError_t launch_softmax_ce(int N, int K, const h16* z, const h16* bias, const int32_t* labels,
+                             float* loss, h16* dz, h16* dbias, hipStream_t st);
+
 }  // namespace fp16k

@@ -148,3 +148,63 @@ def test_sgd_validation():
     assert lib.fp16_sgd_step(A + 2, B, Cc, 8, 0.1, 0.9, 1e-4, None) == MISALIGNED
     assert lib.fp16_sgd_step(A, A + 16, Cc, 64, 0.1, 0.9, 1e-4, None) == ALIASING
     assert lib.fp16_sgd_step(A, B, A + 64, 64, 0.1, 0.9, 1e-4, None) == ALIASING
+
+
+# ---- pooling and loss: every call below is invalid, nothing is launched ---------
+
+UNSUPPORTED = 7
+
+
+def _pool(**kw):
+    base = dict(n=2, c=64, h=112, w=112, r=3, s=3, stride=2, pad=1, layout="NHWC")
+    base.update(kw)
+    return F.pool_desc(base["n"], base["c"], base["h"], base["w"], base["r"], base["s"],
+                       base["stride"], base["pad"], base["layout"])
+
+
+def test_pool_out_dims():
+    assert F.fp16_pool_out_dims(_pool()) == (56, 56)
+    assert F.fp16_pool_out_dims(_pool(h=7, w=7, r=7, s=7, stride=1, pad=0)) == (1, 1)
+    for kw in [dict(pad=3), dict(r=16), dict(stride=0), dict(n=0), dict(h=1, w=1, pad=0),
+               dict(layout=2)]:
+        d = _pool(**{k: v for k, v in kw.items() if k != "layout"})
+        if "layout" in kw:
+            d.layout = kw["layout"]
+        with pytest.raises(F.Fp16Error):
+            F.fp16_pool_out_dims(d)
+
+
+def test_maxpool_validation():
+    l = F.lib()
+    d = _pool()
+    assert l.fp16_maxpool_fwd(None, A, B, Cc, None) == NULL
+    assert l.fp16_maxpool_fwd(ctypes.byref(d), A, B, None, None) == NULL
+    assert l.fp16_maxpool_fwd(ctypes.byref(d), A, B, Cc + 8, None) == MISALIGNED
+    assert l.fp16_maxpool_fwd(ctypes.byref(d), A, A + 16, Cc, None) == ALIASING
+    assert l.fp16_maxpool_fwd(ctypes.byref(_pool(pad=3)), A, B, Cc, None) == SHAPE
+    assert l.fp16_maxpool_bwd(ctypes.byref(d), None, B, Cc, None) == NULL
+    assert l.fp16_maxpool_bwd(ctypes.byref(d), A, B, B + 32, None) == ALIASING
+    assert l.fp16_maxpool_bwd(ctypes.byref(d), A + 4, B, Cc, None) == MISALIGNED
+
+
+def test_avgpool_validation():
+    l = F.lib()
+    g = _pool(h=7, w=7, r=7, s=7, stride=1, pad=0, c=2048)
+    assert l.fp16_avgpool_fwd(ctypes.byref(_pool()), A, B, None) == UNSUPPORTED
+    assert l.fp16_avgpool_fwd(ctypes.byref(g), None, B, None) == NULL
+    assert l.fp16_avgpool_fwd(ctypes.byref(g), A, A + 64, None) == ALIASING
+    assert l.fp16_avgpool_bwd(ctypes.byref(g), A, B + 2, None) == MISALIGNED
+    assert l.fp16_avgpool_bwd(ctypes.byref(_pool(h=7, w=7, r=7, s=7, pad=1)), A, B, None) == \
+        UNSUPPORTED
+
+
+def test_softmax_ce_validation():
+    l = F.lib()
+    D, E, G = 0x50000000, 0x60000000, 0x70000000
+    assert l.fp16_softmax_ce(0, 1000, A, B, Cc, D, E, G, None) == SHAPE
+    assert l.fp16_softmax_ce(128, 0, A, B, Cc, D, E, G, None) == SHAPE
+    assert l.fp16_softmax_ce(128, 70000, A, B, Cc, D, E, G, None) == SHAPE
+    assert l.fp16_softmax_ce(128, 1000, A, B, None, D, E, G, None) == NULL
+    assert l.fp16_softmax_ce(128, 1000, A, B, Cc, D + 4, E, G, None) == MISALIGNED
+    assert l.fp16_softmax_ce(128, 1000, A, B, Cc, D, A + 16, G, None) == ALIASING
+    assert l.fp16_softmax_ce(128, 1000, A, B, Cc, D, E, B, None) == ALIASING
