@@ -1,0 +1,364 @@
+"""ResNet-50 trained all in FP16 through the C ABI: one training step of the
+whole network on one GPU's batch (Section 5.1 of arXiv:1911.07384).
+
+The network is torchvision's ResNet-50 v1.5 (stride on the 3x3 convolution
+of each downsampling bottleneck): a 7x7 stride-2 stem convolution with BN and
+ReLU, a 3x3 stride-2 max pool, four stages of 3, 4, 6 and 3 bottleneck
+blocks, global average pooling and a 2048->1000 classifier with bias,
+trained with the softmax cross-entropy averaged over the batch.  Every BN
+inside a residual block is followed by the 0.25 multiplier (Section 4.2),
+including the BN of a downsampling shortcut; the stem BN is not.  All
+tensors are binary16 (no master copy, no loss scaling, Section 5.2); the SGD
+step runs over two flat parameter arenas (weight decay on the convolution
+and classifier weights and the classifier bias, none on BN parameters,
+Section 5.1).
+
+The step is an explicit program: a list of ``Op`` records, each one ABI call
+with named device buffers.  Running the list in order is one training step;
+it enqueues on the current stream only and can be captured in a HIP graph.
+The records also let tests replay any call's inputs through the oracle.
+"""
+
+from __future__ import annotations
+
+from dataclasses import dataclass, field
+
+import numpy as np
+import torch
+
+import paper_1911_07384_amd as F
+from paper_1911_07384_amd import synth
+
+STAGES = ((3, 64, 256, 1), (4, 128, 512, 2), (6, 256, 1024, 2), (3, 512, 2048, 2))
+
+
+@dataclass
+class Op:
+    kind: str
+    name: str
+    a: dict = field(default_factory=dict)
+
+
+class ResNet50:
+    """Device state and the ABI program of one ResNet-50 training step."""
+
+    def __init__(self, n: int = 128, image: int = 224, classes: int = 1000, seed: int = 0,
+                 lr: float = 0.1, momentum: float = 0.9, weight_decay: float = 1e-4,
+                 post_scale: float = 0.25, eps: float = 1e-5, stages=STAGES, device="cuda"):
+        self.n, self.image, self.classes = n, image, classes
+        self.lr, self.momentum, self.wd = lr, momentum, weight_decay
+        self.post_scale, self.eps = post_scale, eps
+        self.seed = seed
+        self.dev = torch.device(device)
+        self._stream_id = 100
+        self.convs = []    # (name, desc, W view, dW view)
+        self.bns = []      # (name, channels)
+        self._wspecs = []  # (name, shape, std) of every weight-decay parameter
+        self._bnspecs = []
+        self.fwd, self.bwd, self.upd = [], [], []
+        self.buffers = {}
+        self._ws_need = 0
+        self._plan(stages)
+        self._allocate_params()
+        self.ws = F.workspace(self._ws_need, self.dev)
+
+    # ---- buffers -------------------------------------------------------------
+
+    def _buf(self, name, shape, dtype=torch.float16):
+        t = torch.empty(shape, dtype=dtype, device=self.dev)
+        self.buffers[name] = t
+        return t
+
+    def _next_stream(self):
+        self._stream_id += 1
+        return self._stream_id
+
+    # ---- planning: shapes, buffers and the op lists -------------------------------
+
+    def _conv(self, name, x, xname, ci, co, r, stride, pad):
+        n, h = x.shape[0], x.shape[1]
+        d = F.conv_desc(n, ci, h, h, co, r, r, stride, pad)
+        p, q = F.fp16_conv_out_dims(d)
+        for ps in (F.PASS_FWD, F.PASS_DGRAD, F.PASS_WGRAD):
+            self._ws_need = max(self._ws_need, F.fp16_conv_workspace_bytes(d, ps))
+        y = self._buf(name + ".y", (n, p, q, co))
+        self._wspecs.append((name, (co, r, r, ci), synth.he_std(ci * r * r)))
+        self.convs.append({"name": name, "desc": d, "x": xname, "y": name + ".y"})
+        self.fwd.append(Op("conv_fwd", name, {"desc": d, "x": xname, "w": name, "y": name + ".y"}))
+        return y
+
+    def _bn(self, name, x, xname, relu, post_scale, res=None):
+        n, h, w, c = x.shape
+        d = F.bn_desc(n, c, h, w, "NHWC", self.eps, post_scale, relu)
+        self._ws_need = max(self._ws_need, F.fp16_bn_workspace_bytes(d))
+        y = self._buf(name + ".y", x.shape)
+        self._buf(name + ".stats", (2 * c,), torch.float32)
+        self._bnspecs.append((name, c))
+        self.fwd.append(Op("bn_fwd", name, {"desc": d, "x": xname, "res": res, "y": name + ".y",
+                                            "stats": name + ".stats"}))
+        return y
+
+    def _plan(self, stages):
+        n, s = self.n, self.post_scale
+        img = self._buf("image", (n, self.image, self.image, 3))
+        self._buf("labels", (n,), torch.int32)
+        # stem: conv 7x7/2, BN (multiplier 1) + ReLU, max pool 3x3/2
+        y = self._conv("stem", img, "image", 3, 64, 7, 2, 3)
+        a = self._bn("stem.bn", y, "stem.y", True, 1.0)
+        pd = F.pool_desc(n, 64, a.shape[1], a.shape[2], 3, 3, 2, 1)
+        p, q = F.fp16_pool_out_dims(pd)
+        self._buf("pool.y", (n, p, q, 64))
+        self._buf("pool.idx", (n, p, q, 64), torch.uint8)
+        self.fwd.append(Op("maxpool_fwd", "pool", {"desc": pd, "x": "stem.bn.y", "y": "pool.y",
+                                                   "idx": "pool.idx"}))
+        x, xname, cin = self.buffers["pool.y"], "pool.y", 64
+        self.blocks = []
+        for si, (nb, width, cout, stride) in enumerate(stages):
+            for bi in range(nb):
+                nm = f"l{si + 1}.{bi}"
+                st = stride if bi == 0 else 1
+                blk = {"name": nm, "x": xname, "ds": bi == 0}
+                y1 = self._conv(nm + ".c1", x, xname, cin, width, 1, 1, 0)
+                a1 = self._bn(nm + ".bn1", y1, nm + ".c1.y", True, s)
+                y2 = self._conv(nm + ".c2", a1, nm + ".bn1.y", width, width, 3, st, 1)
+                a2 = self._bn(nm + ".bn2", y2, nm + ".c2.y", True, s)
+                y3 = self._conv(nm + ".c3", a2, nm + ".bn2.y", width, cout, 1, 1, 0)
+                if bi == 0:
+                    yd = self._conv(nm + ".ds", x, xname, cin, cout, 1, st, 0)
+                    self._bn(nm + ".bnd", yd, nm + ".ds.y", False, s)
+                    res = nm + ".bnd.y"
+                else:
+                    res = xname
+                blk["res"] = res
+                out = self._bn(nm + ".bn3", y3, nm + ".c3.y", True, s, res=res)
+                self.blocks.append(blk)
+                x, xname, cin = out, nm + ".bn3.y", cout
+        # global average pool to [N, 1, 1, C], classifier as a 1x1 convolution
+        h = x.shape[1]
+        gd = F.pool_desc(n, cin, h, h, h, h, 1, 0)
+        self._buf("gap.y", (n, 1, 1, cin))
+        self.fwd.append(Op("avgpool_fwd", "gap", {"desc": gd, "x": xname, "y": "gap.y"}))
+        self._conv("fc", self.buffers["gap.y"], "gap.y", cin, self.classes, 1, 1, 0)
+        self._buf("loss", (n,), torch.float32)
+        self._buf("fc.dy", (n, 1, 1, self.classes))
+        self.fwd.append(Op("softmax_ce", "loss", {"n": n, "k": self.classes, "z": "fc.y",
+                                                  "bias": "fc.bias", "labels": "labels",
+                                                  "loss": "loss", "dz": "fc.dy",
+                                                  "dbias": "fc.dbias"}))
+        self._last = xname
+        self._plan_backward(gd, pd)
+
+    def _grad(self, name):
+        """Gradient buffer shaped like buffer `name`, registered as d:<name>."""
+        key = "d:" + name
+        if key not in self.buffers:
+            src = self.buffers[name]
+            self.buffers[key] = torch.empty(src.shape, dtype=src.dtype, device=self.dev)
+        return key
+
+    def _conv_op(self, name):
+        return next(c for c in self.convs if c["name"] == name)
+
+    def _bn_op(self, name):
+        return next(o for o in self.fwd if o.kind == "bn_fwd" and o.name == name)
+
+    def _bn_bwd(self, name, dy, want_dres):
+        f = self._bn_op(name).a
+        dx = self._grad(f["x"])
+        a = {"desc": f["desc"], "x": f["x"], "y": None, "dy": dy, "res": f["res"],
+             "stats": f["stats"], "dx": dx, "dgamma": name + ".dgamma", "dbeta": name + ".dbeta",
+             "dres": None}
+        if want_dres:
+            a["dres"] = self._grad(f["res"]) if f["res"] is not None else None
+        self.bwd.append(Op("bn_bwd", name, a))
+        return dx
+
+    def _conv_bwd(self, name, dy, dx_needed=True, addend=None, dx_name=None):
+        c = self._conv_op(name)
+        if dx_needed:
+            dx = dx_name or self._grad(c["x"])
+            if addend is None:
+                self.bwd.append(Op("conv_dgrad", name, {"desc": c["desc"], "dy": dy, "w": name,
+                                                        "dx": dx}))
+            else:
+                self.bwd.append(Op("conv_dgrad_add", name, {"desc": c["desc"], "dy": dy,
+                                                            "w": name, "addend": addend,
+                                                            "dx": dx}))
+        self.bwd.append(Op("conv_wgrad", name, {"desc": c["desc"], "x": c["x"], "dy": dy,
+                                                "dw": "d:" + name}))
+
+    def _plan_backward(self, gd, pd):
+        # classifier: the loss kernel wrote fc.dy and the bias gradient
+        self._conv_bwd("fc", "fc.dy")
+        dgap = self._grad("gap.y")
+        dlast = self._grad(self._last)
+        self.bwd.append(Op("avgpool_bwd", "gap", {"desc": gd, "dy": dgap, "dx": dlast}))
+        dout = dlast
+        for blk in reversed(self.blocks):
+            nm = blk["name"]
+            dc3 = self._bn_bwd(nm + ".bn3", dout, want_dres=True)
+            dres = self._bn_op(nm + ".bn3").a["res"]
+            dres = "d:" + dres
+            self._conv_bwd(nm + ".c3", dc3)
+            dc2 = self._bn_bwd(nm + ".bn2", "d:" + nm + ".bn2.y", want_dres=False)
+            self._conv_bwd(nm + ".c2", dc2)
+            dc1 = self._bn_bwd(nm + ".bn1", "d:" + nm + ".bn1.y", want_dres=False)
+            # block input gradient = branch gradient + shortcut gradient, one rounding
+            dxb = "dx:" + nm
+            self.buffers[dxb] = torch.empty(self.buffers[blk["x"]].shape, dtype=torch.float16,
+                                            device=self.dev)
+            if blk["ds"]:
+                dcd = self._bn_bwd(nm + ".bnd", dres, want_dres=False)
+                dsx = "dds:" + nm
+                self.buffers[dsx] = torch.empty_like(self.buffers[dxb])
+                self._conv_bwd(nm + ".ds", dcd, dx_name=dsx)
+                self._conv_bwd(nm + ".c1", dc1, addend=dsx, dx_name=dxb)
+            else:
+                self._conv_bwd(nm + ".c1", dc1, addend=dres, dx_name=dxb)
+            dout = dxb
+        # max pool, stem BN (mask from its stored output), stem weights (the
+        # image gradient is not needed)
+        dstem = self._grad("stem.bn.y")
+        self.bwd.append(Op("maxpool_bwd", "pool", {"desc": pd, "idx": "pool.idx", "dy": dout,
+                                                   "dx": dstem}))
+        dc = self._bn_bwd("stem.bn", dstem, want_dres=False)
+        self.bwd[-1].a["y"] = "stem.bn.y"
+        self._conv_bwd("stem", dc, dx_needed=False)
+
+    # ---- parameters ----------------------------------------------------------------
+
+    def _allocate_params(self):
+        f16 = dict(dtype=torch.float16, device=self.dev)
+        sizes = [int(np.prod(sh)) for _, sh, _ in self._wspecs]
+        nw = sum(sizes) + self.classes  # + classifier bias
+        self.w_arena = torch.empty(nw, **f16)
+        self.dw_arena = torch.zeros(nw, **f16)
+        self.mw_arena = torch.zeros(nw, **f16)
+        off = 0
+        for (name, sh, std), sz in zip(self._wspecs, sizes):
+            w = synth.normal_f16(sh, std, self.seed, self._next_stream())
+            self.w_arena[off:off + sz].copy_(torch.from_numpy(w.reshape(-1)).to(self.dev))
+            self.buffers[name] = self.w_arena[off:off + sz].view(sh)
+            self.buffers["d:" + name] = self.dw_arena[off:off + sz].view(sh)
+            off += sz
+        self.w_arena[off:].zero_()
+        self.buffers["fc.bias"] = self.w_arena[off:]
+        self.buffers["fc.dbias"] = self.dw_arena[off:]
+        nb = 2 * sum(c for _, c in self._bnspecs)
+        self.bn_arena = torch.empty(nb, **f16)
+        self.dbn_arena = torch.zeros(nb, **f16)
+        self.mbn_arena = torch.zeros(nb, **f16)
+        off = 0
+        for name, c in self._bnspecs:
+            self.bn_arena[off:off + c].fill_(1.0)
+            self.buffers[name + ".gamma"] = self.bn_arena[off:off + c]
+            self.buffers[name + ".dgamma"] = self.dbn_arena[off:off + c]
+            off += c
+            self.bn_arena[off:off + c].fill_(0.0)
+            self.buffers[name + ".beta"] = self.bn_arena[off:off + c]
+            self.buffers[name + ".dbeta"] = self.dbn_arena[off:off + c]
+            off += c
+        self.upd = [
+            Op("sgd", "sgd_weights", {"w": self.w_arena, "g": self.dw_arena, "m": self.mw_arena,
+                                      "wd": self.wd}),
+            Op("sgd", "sgd_bn", {"w": self.bn_arena, "g": self.dbn_arena, "m": self.mbn_arena,
+                                 "wd": 0.0}),
+        ]
+        self.n_weights, self.n_bn = nw, nb
+
+    def load_batch(self, seed: int = 0):
+        """Synthetic images ~ N(0, 1) and uniform labels (the ImageNet shapes)."""
+        img = synth.normal_f16((self.n, self.image, self.image, 3), 1.0, seed, 1)
+        lab = synth.labels(self.n, self.classes, seed, 2)
+        self.buffers["image"].copy_(torch.from_numpy(img).to(self.dev))
+        self.buffers["labels"].copy_(torch.from_numpy(lab).to(self.dev))
+
+    # ---- execution -------------------------------------------------------------------
+
+    def _t(self, key):
+        return None if key is None else self.buffers[key]
+
+    def run(self, op: Op) -> None:
+        a, t, ws = op.a, self._t, self.ws
+        k = op.kind
+        if k == "conv_fwd":
+            F.fp16_conv_fwd(a["desc"], t(a["x"]), t(a["w"]), t(a["y"]), ws)
+        elif k == "conv_dgrad":
+            F.fp16_conv_dgrad(a["desc"], t(a["dy"]), t(a["w"]), t(a["dx"]), ws)
+        elif k == "conv_dgrad_add":
+            F.fp16_conv_dgrad_add(a["desc"], t(a["dy"]), t(a["w"]), t(a["addend"]), t(a["dx"]), ws)
+        elif k == "conv_wgrad":
+            F.fp16_conv_wgrad(a["desc"], t(a["x"]), t(a["dy"]), t(a["dw"]), ws)
+        elif k == "bn_fwd":
+            nm = op.name
+            F.fp16_bn_relu(a["desc"], t(a["x"]), t(nm + ".gamma"), t(nm + ".beta"), t(a["res"]),
+                           t(a["y"]), t(a["stats"]), ws)
+        elif k == "bn_bwd":
+            nm = op.name
+            F.fp16_bn_relu_bwd(a["desc"], t(a["x"]), t(a["y"]), t(a["dy"]), t(nm + ".gamma"),
+                               t(nm + ".beta"), t(a["res"]), t(a["stats"]), t(a["dx"]),
+                               t(a["dgamma"]), t(a["dbeta"]), t(a["dres"]), ws)
+        elif k == "maxpool_fwd":
+            F.fp16_maxpool_fwd(a["desc"], t(a["x"]), t(a["y"]), t(a["idx"]))
+        elif k == "maxpool_bwd":
+            F.fp16_maxpool_bwd(a["desc"], t(a["idx"]), t(a["dy"]), t(a["dx"]))
+        elif k == "avgpool_fwd":
+            F.fp16_avgpool_fwd(a["desc"], t(a["x"]), t(a["y"]))
+        elif k == "avgpool_bwd":
+            F.fp16_avgpool_bwd(a["desc"], t(a["dy"]), t(a["dx"]))
+        elif k == "softmax_ce":
+            F.fp16_softmax_ce(a["n"], a["k"], t(a["z"]), t(a["bias"]), t(a["labels"]),
+                              t(a["loss"]), t(a["dz"]), t(a["dbias"]))
+        elif k == "sgd":
+            F.fp16_sgd_step(a["w"], a["g"], a["m"], a["w"].numel(), self.lr, self.momentum,
+                            a["wd"])
+        else:
+            raise ValueError(k)
+
+    def program(self):
+        return self.fwd + self.bwd + self.upd
+
+    def forward(self):
+        for op in self.fwd:
+            self.run(op)
+
+    def backward(self):
+        for op in self.bwd:
+            self.run(op)
+
+    def update(self):
+        for op in self.upd:
+            self.run(op)
+
+    def step(self):
+        for op in self.program():
+            self.run(op)
+
+    def calls(self):
+        """(name, thunk) for every ABI call of one step, in order."""
+        return [(f"{op.name}:{op.kind}", (lambda o=op: self.run(o))) for op in self.program()]
+
+    # ---- accounting -----------------------------------------------------------------
+
+    def conv_flops(self) -> int:
+        """Algorithmic FLOPs of one forward pass over every convolution (the
+        classifier included); a training step does three such passes, less the
+        stem's data gradient, which is not computed."""
+        tot = 0
+        for c in self.convs:
+            d = c["desc"]
+            p, q = F.fp16_conv_out_dims(d)
+            tot += 2 * d.n * p * q * d.k * d.c * d.r * d.s
+        return tot
+
+    def step_flops(self) -> int:
+        stem = next(c for c in self.convs if c["name"] == "stem")["desc"]
+        p, q = F.fp16_conv_out_dims(stem)
+        return 3 * self.conv_flops() - 2 * stem.n * p * q * stem.k * stem.c * stem.r * stem.s
+
+    def state(self):
+        return [t.clone() for t in (self.w_arena, self.mw_arena, self.bn_arena, self.mbn_arena)]
+
+    def load_state(self, st):
+        for t, v in zip((self.w_arena, self.mw_arena, self.bn_arena, self.mbn_arena), st):
+            t.copy_(v)

@@ -1,0 +1,67 @@
+"""The ResNet-50 step program, planned on the host (no kernels run): the
+network has ResNet-50's layer count and parameter count (Section 5.1), every
+buffer a call reads is written earlier in the step, and no buffer is written
+twice."""
+
+import numpy as np
+import pytest
+
+from paper_1911_07384_amd.network import ResNet50
+
+
+@pytest.fixture(scope="module")
+def net():
+    return ResNet50(n=1, image=224, device="cpu")
+
+
+def test_layer_and_parameter_counts(net):
+    convs = [o for o in net.fwd if o.kind == "conv_fwd"]
+    assert len(convs) == 54                      # 53 convolutions + the classifier
+    assert len([o for o in net.fwd if o.kind == "bn_fwd"]) == 53
+    conv_w = sum(int(np.prod(net.buffers[c["name"]].shape)) for c in net.convs if c["name"] != "fc")
+    assert conv_w == 23_454_912
+    assert net.n_weights == 23_454_912 + 2_048_000 + 1000
+    assert net.n_bn == 53_120
+    assert net.n_weights + net.n_bn == 25_557_032  # ResNet-50's parameter count
+
+
+def test_conv_flops_at_batch_128(net):
+    # FLOPs scale with the batch; at 128 the forward convolutions + classifier
+    # are 1.0468 TFLOP (the classifier is 2*128*2048*1000)
+    f = 128 * net.conv_flops()
+    assert abs(f - 1.0468e12) < 0.0005e12
+    assert net.step_flops() == 3 * net.conv_flops() - 2 * 112 * 112 * 64 * 3 * 49
+
+
+OUTPUTS = {"conv_fwd": ["y"], "conv_dgrad": ["dx"], "conv_dgrad_add": ["dx"],
+           "conv_wgrad": ["dw"], "bn_fwd": ["y", "stats"],
+           "bn_bwd": ["dx", "dgamma", "dbeta", "dres"], "maxpool_fwd": ["y", "idx"],
+           "maxpool_bwd": ["dx"], "avgpool_fwd": ["y"], "avgpool_bwd": ["dx"],
+           "softmax_ce": ["loss", "dz", "dbias"]}
+
+
+def test_dataflow(net):
+    # every buffer a call reads is an input, a parameter, or written earlier in
+    # the step; every output is written exactly once
+    params = {c["name"] for c in net.convs} | {"fc.bias"}
+    for name, _ in net._bnspecs:
+        params |= {name + ".gamma", name + ".beta"}
+    written = {"image", "labels"} | params
+    seen = set()
+    for op in net.fwd + net.bwd:
+        outs = [k for k in OUTPUTS[op.kind] if op.a.get(k) is not None]
+        reads = [v for k, v in op.a.items() if isinstance(v, str) and k not in outs]
+        if op.kind in ("bn_fwd", "bn_bwd"):
+            reads += [op.name + ".gamma", op.name + ".beta"]
+        for v in reads:
+            assert v in net.buffers and v in written, (op.name, op.kind, v)
+        for k in outs:
+            v = op.a[k]
+            assert v in net.buffers and v not in seen, (op.name, k, v)
+            seen.add(v)
+            written.add(v)
+    # every weight and BN parameter receives a gradient
+    grads = {op.a["dw"] for op in net.bwd if op.kind == "conv_wgrad"}
+    assert grads == {"d:" + c["name"] for c in net.convs}
+    bn_grads = {op.a["dgamma"] for op in net.bwd if op.kind == "bn_bwd"}
+    assert bn_grads == {name + ".dgamma" for name, _ in net._bnspecs}
