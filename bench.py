@@ -45,6 +45,12 @@ def parse():
                     help="also time all 23 ResNet-50 conv shapes (53 layers) at batch 128")
     ap.add_argument("--no-sweep3x3", action="store_true",
                     help="skip the batch-128 3x3-layer sweep")
+    ap.add_argument("--no-resnet50", action="store_true",
+                    help="skip the full ResNet-50 training step at batch 128")
+    ap.add_argument("--resnet50-steps", type=int, default=10)
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="first run three device-to-device copies of MIB MiB (a plain copy of "
+                         "known size, the yardstick for the HBM byte counters)")
     return ap.parse_args()
 
 
@@ -128,6 +134,66 @@ def traffic_for(kernel_src: str, call: str):
     return ent.get("hbm_bytes")
 
 
+def resnet50_leg(torch, steps: int, warmup: int = 3, batch: int = 128):
+    """The whole ResNet-50 training step (forward, softmax cross-entropy,
+    backward, FP16 SGD over every parameter) at batch 128 on 224x224 synthetic
+    images, captured once in a HIP graph; images/s over `steps` replays, and
+    the time per kind of call from one eager pass timed call by call."""
+    from paper_1911_07384_amd.network import ResNet50
+    net = ResNet50(n=batch, image=224, seed=0)
+    net.load_batch(0)
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        net.step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        net.step()
+    torch.cuda.synchronize()
+    for _ in range(warmup):
+        graph.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(steps):
+        graph.replay()
+    b.record()
+    torch.cuda.synchronize()
+    ms = a.elapsed_time(b) / steps
+    loss = float(net.buffers["loss"].float().mean().item())
+    finite = bool(torch.isfinite(net.w_arena.float()).all().item())
+    # per-kind time: each call between two events on the launch stream
+    stream = torch.cuda.current_stream()
+    calls = net.calls()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in calls]
+    torch.cuda._sleep(200_000_000)  # covers the host enqueue of all 274 calls
+    for (_, fn), (e0, e1) in zip(calls, evs):
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+    torch.cuda.synchronize()
+    kinds = {}
+    for (name, _), (e0, e1) in zip(calls, evs):
+        kind = name.split(":")[1]
+        kinds[kind] = kinds.get(kind, 0.0) + e0.elapsed_time(e1)
+    fl = net.step_flops()
+    del graph, net
+    torch.cuda.empty_cache()
+    return {"images_per_sec": round(batch / (ms * 1e-3), 1), "ms_per_step": round(ms, 4),
+            "batch": batch, "image": 224, "steps": steps, "graph": True,
+            "conv_tflop_per_step": round(fl / 1e12, 4),
+            "conv_tflops_effective": round(fl / (ms * 1e-3) / 1e12, 2),
+            "loss_after": round(loss, 4), "weights_finite": finite,
+            "eager_ms_by_kind": {k: round(v, 3) for k, v in sorted(kinds.items(),
+                                                                    key=lambda kv: -kv[1])},
+            "note": "one HIP graph per step: 274 ABI calls (54 conv fwd, 53 wgrad, 52 dgrad, "
+                    "53 BN fwd/bwd, pools, loss, 2 SGD); images ~N(0,1), uniform labels"}
+
+
 def cpu_baseline(shape, target_s):
     """The oracle's block step on a batch slice, on this host's cores."""
     import numpy as np
@@ -169,6 +235,13 @@ def main():
     from paper_1911_07384_amd.bottleneck import Bottleneck, BlockShape
 
     torch.cuda.set_device(0)
+    if args.calibrate_copy:
+        src = torch.empty(args.calibrate_copy << 20, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     shape = BlockShape(n=args.batch)
     block = Bottleneck(shape, seed=0)
     torch.cuda.synchronize()
@@ -269,6 +342,8 @@ def main():
             out["conv53_b128"] = {k: round(v, 4) for k, v in summ["all_53"].items()}
             out["sweep_layers"] = [{k: (round(v, 3) if isinstance(v, float) else v)
                                     for k, v in r.items()} for r in rows]
+    if not args.no_resnet50:
+        out["resnet50_train_b128"] = resnet50_leg(torch, args.resnet50_steps)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, args.cpu_seconds)
     print(json.dumps(out), flush=True)
