@@ -57,9 +57,10 @@ _SIGS = {
     "oracle_conv_fwd_at": (None, [_P, _P, _P, _P, _I64, _P]),
     "oracle_conv_dgrad_at": (None, [_P, _P, _P, _P, _I64, _P]),
     "oracle_conv_wgrad_at": (None, [_P, _P, _P, _P, _I64, _P]),
-    "oracle_bn_fwd": (None, [_P, _P, _P, _P, _P, _F32, _F32, _INT, _P, _P, _P, _P]),
-    "oracle_bn_apply_f32": (None, [_P, _P, _P, _P, _P, _P, _P, _F32, _INT, _P]),
-    "oracle_bn_bwd": (None, [_P, _P, _P, _P, _P, _F32, _F32, _INT, _P, _P, _P, _P, _P, _P, _P]),
+    "oracle_bn_fwd": (None, [_P, _P, _P, _P, _P, _F32, _F32, _INT, _P, _P, _P, _P, _INT]),
+    "oracle_bn_apply_f32": (None, [_P, _P, _P, _P, _P, _P, _P, _F32, _INT, _P, _INT]),
+    "oracle_bn_bwd": (None, [_P, _P, _P, _P, _P, _F32, _F32, _INT, _P, _P, _P, _P, _P, _P, _P,
+                             _INT, _P]),
     "oracle_sgd_f32": (None, [_P, _P, _P, _I64, _F32, _F32, _F32]),
     "oracle_sgd_f64": (None, [_P, _P, _P, _I64, _F64, _F64, _F64]),
     "oracle_pool_out_dims": (None, [_P, _P, _P]),
@@ -216,10 +217,13 @@ def bn_shape(n, c, h, w, layout="NHWC") -> np.ndarray:
     return np.array([n, c, h, w, {"NHWC": 0, "NCHW": 1}[layout]], dtype=np.int32)
 
 
-def bn_fwd(shp, x, gamma, beta, residual=None, eps=1e-5, post_scale=1.0, relu=True):
-    """Returns dict(mean, var, y64, y) with y binary16."""
+def bn_fwd(shp, x, gamma, beta, residual=None, eps=1e-5, post_scale=1.0, relu=True, swap=False):
+    """Returns dict(mean, var, y64, y) with y binary16.  swap: the BN swap
+    (the shortcut joins before gamma; needs the residual)."""
     x, gamma, beta = _h(x), _h(gamma), _h(beta)
     res = None if residual is None else _h(residual)
+    if swap and res is None:
+        raise ValueError("the BN swap needs the residual")
     C = int(shp[1])
     mean = np.empty(C, np.float64)
     var = np.empty(C, np.float64)
@@ -227,27 +231,35 @@ def bn_fwd(shp, x, gamma, beta, residual=None, eps=1e-5, post_scale=1.0, relu=Tr
     y16 = np.empty(x.shape, np.uint16)
     lib().oracle_bn_fwd(_ptr(shp), _ptr(x), _ptr(gamma), _ptr(beta), _ptr(res),
                         float(eps), float(post_scale), int(bool(relu)),
-                        _ptr(mean), _ptr(var), _ptr(y64), _ptr(y16))
+                        _ptr(mean), _ptr(var), _ptr(y64), _ptr(y16), int(bool(swap)))
     return {"mean": mean, "var": var, "y64": y64, "y": y16.view(np.float16)}
 
 
-def bn_apply_f32(shp, x, gamma, beta, mean, rstd, residual=None, post_scale=1.0, relu=True):
+def bn_apply_f32(shp, x, gamma, beta, mean, rstd, residual=None, post_scale=1.0, relu=True,
+                 swap=False):
     """Declared float32 apply with given float32 statistics; binary16 result."""
     x, gamma, beta = _h(x), _h(gamma), _h(beta)
     res = None if residual is None else _h(residual)
+    if swap and res is None:
+        raise ValueError("the BN swap needs the residual")
     mean = np.ascontiguousarray(mean, dtype=np.float32)
     rstd = np.ascontiguousarray(rstd, dtype=np.float32)
     y16 = np.empty(x.shape, np.uint16)
     lib().oracle_bn_apply_f32(_ptr(shp), _ptr(x), _ptr(gamma), _ptr(beta), _ptr(res),
                               _ptr(mean), _ptr(rstd), float(post_scale), int(bool(relu)),
-                              _ptr(y16))
+                              _ptr(y16), int(bool(swap)))
     return y16.view(np.float16)
 
 
-def bn_bwd(shp, x, y, dy, gamma, eps=1e-5, post_scale=1.0, relu=True, want_dres=False):
-    """Returns dict(dx, dgamma, dbeta, dres, dx64, dgamma64, dbeta64)."""
+def bn_bwd(shp, x, y, dy, gamma, eps=1e-5, post_scale=1.0, relu=True, want_dres=False,
+           swap=False, residual=None):
+    """Returns dict(dx, dgamma, dbeta, dres, dx64, dgamma64, dbeta64).  With
+    swap the residual is needed (dgamma includes sum g*r)."""
     x, dy, gamma = _h(x), _h(dy), _h(gamma)
     y = None if y is None else _h(y)
+    res = None if residual is None else _h(residual)
+    if swap and res is None:
+        raise ValueError("the BN swap needs the residual")
     if relu and y is None:
         raise ValueError("the ReLU mask needs the forward output y")
     C = int(shp[1])
@@ -260,7 +272,8 @@ def bn_bwd(shp, x, y, dy, gamma, eps=1e-5, post_scale=1.0, relu=True, want_dres=
     dres = np.empty(x.shape, np.uint16) if want_dres else None
     lib().oracle_bn_bwd(_ptr(shp), _ptr(x), _ptr(y), _ptr(dy), _ptr(gamma), float(eps),
                         float(post_scale), int(bool(relu)), _ptr(dx), _ptr(dg), _ptr(db),
-                        _ptr(dres), _ptr(dx64), _ptr(dg64), _ptr(db64))
+                        _ptr(dres), _ptr(dx64), _ptr(dg64), _ptr(db64), int(bool(swap)),
+                        _ptr(res))
     return {"dx": dx.view(np.float16), "dgamma": dg.view(np.float16),
             "dbeta": db.view(np.float16),
             "dres": None if dres is None else dres.view(np.float16),

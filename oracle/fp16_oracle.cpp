@@ -386,10 +386,16 @@ void oracle_conv_wgrad_at(const int32_t* shp, const uint16_t* x16, const uint16_
 // 1 for the stem BN); r is the identity shortcut (block-last BN only, may
 // be NULL); relu may be switched off.  eps is held as the float32 value the
 // caller passes.  y64 (may be NULL) is u or relu(u) before rounding.
+//
+// swap = 1 is the BN swap of Section 4.1: the shortcut joins before gamma,
+//   u = s * (gamma * (xhat + r) + beta)
+// (reading: the positions of the residual addition and of gamma exchange;
+// the multiplier stays on the BN output).  It needs r.
 
 void oracle_bn_fwd(const int32_t* shp, const uint16_t* x16, const uint16_t* gamma16,
                    const uint16_t* beta16, const uint16_t* res16, float eps, float post_scale,
-                   int relu, double* mean_out, double* var_out, double* y64, uint16_t* y16) {
+                   int relu, double* mean_out, double* var_out, double* y64, uint16_t* y16,
+                   int swap) {
   BN d(shp);
   const int64_t M = d.M();
 #pragma omp parallel for schedule(dynamic, 1)
@@ -408,8 +414,13 @@ void oracle_bn_fwd(const int32_t* shp, const uint16_t* x16, const uint16_t* gamm
     for (int64_t j = 0; j < M; ++j) {
       const int64_t i = d.at(c, j);
       const double xhat = (half_to_double(x16[i]) - mu) * rstd;
-      double u = (double)post_scale * (g * xhat + b);
-      if (res16) u += half_to_double(res16[i]);
+      double u;
+      if (swap)
+        u = (double)post_scale * (g * (xhat + half_to_double(res16[i])) + b);
+      else {
+        u = (double)post_scale * (g * xhat + b);
+        if (res16) u += half_to_double(res16[i]);
+      }
       if (relu) u = relu_d(u);
       if (y64) y64[i] = u;
       if (y16) y16[i] = round_half(u);
@@ -424,11 +435,15 @@ void oracle_bn_fwd(const int32_t* shp, const uint16_t* x16, const uint16_t* gamm
 // reading this library fixes; every step is one IEEE float32 operation):
 //   a = fl(fl(s * gamma) * rstd);  b = fl(s * beta);  t = fl(x - mean);
 //   v = fma(t, a, b);  v = fl(v + r);  y = round_half(relu(v)).
+// With swap (u = s*gamma*(xhat + r) + s*beta) the shortcut enters the
+// offset instead:  sg = fl(s * gamma);  a = fl(sg * rstd);  b = fl(s * beta);
+//   t = fl(x - mean);  w = fma(sg, r, b);  v = fma(t, a, w);  y = round_half(relu(v)).
 // The result is the unique binary16 pattern of that sequence.
 
 void oracle_bn_apply_f32(const int32_t* shp, const uint16_t* x16, const uint16_t* gamma16,
                          const uint16_t* beta16, const uint16_t* res16, const float* mean,
-                         const float* rstd, float post_scale, int relu, uint16_t* y16) {
+                         const float* rstd, float post_scale, int relu, uint16_t* y16,
+                         int swap) {
   BN d(shp);
   const int64_t M = d.M();
 #pragma omp parallel for schedule(dynamic, 1)
@@ -439,8 +454,13 @@ void oracle_bn_apply_f32(const int32_t* shp, const uint16_t* x16, const uint16_t
     for (int64_t j = 0; j < M; ++j) {
       const int64_t i = d.at(c, j);
       const float t = half_to_float(x16[i]) - mean[c];
-      float v = std::fmaf(t, a, b);
-      if (res16) v = v + half_to_float(res16[i]);
+      float v;
+      if (swap) {
+        v = std::fmaf(t, a, std::fmaf(sg, half_to_float(res16[i]), b));
+      } else {
+        v = std::fmaf(t, a, b);
+        if (res16) v = v + half_to_float(res16[i]);
+      }
       if (relu) v = relu_f(v);
       y16[i] = round_half((double)v);
     }
@@ -449,17 +469,23 @@ void oracle_bn_apply_f32(const int32_t* shp, const uint16_t* x16, const uint16_t
 
 // Backward of the forward above in float64, statistics recomputed from x:
 //   mask = [y > 0] from the given forward output y (all ones when relu is off);
-//   g = s * dy * mask  (gradient reaching z = gamma * xhat + beta);
+//   g = s * dy where mask is 1, +0 where it is 0 (the gradient reaching
+//       z = gamma * xhat + beta; the ReLU's derivative is zero there, and
+//       the zero is +0 like the ReLU's own output);
 //   S1 = sum g;  S2 = sum g * xhat;  dbeta = S1;  dgamma = S2;
 //   dx = gamma * rstd * (g - S1 / M - xhat * S2 / M);
 //   dr = dy where mask is 1, +0 elsewhere (gradient to the identity shortcut,
 //        if requested; ReLU passes the gradient only where its output is positive).
+// With swap (u = s * (gamma * (xhat + r) + beta)): g as above;
+//   dbeta = S1;  dgamma = S2 + S3 with S3 = sum g * r;  dx as above (xhat is
+//   the only path from x);  dr = gamma * g (the shortcut now passes gamma).
 // Each output is rounded once to binary16.  The 64-bit outputs may be NULL.
 
 void oracle_bn_bwd(const int32_t* shp, const uint16_t* x16, const uint16_t* y16,
                    const uint16_t* dy16, const uint16_t* gamma16, float eps, float post_scale,
                    int relu, uint16_t* dx16, uint16_t* dgamma16, uint16_t* dbeta16,
-                   uint16_t* dres16, double* dx64, double* dgamma64, double* dbeta64) {
+                   uint16_t* dres16, double* dx64, double* dgamma64, double* dbeta64, int swap,
+                   const uint16_t* res16) {
   BN d(shp);
   const int64_t M = d.M();
 #pragma omp parallel for schedule(dynamic, 1)
@@ -473,29 +499,35 @@ void oracle_bn_bwd(const int32_t* shp, const uint16_t* x16, const uint16_t* y16,
       ss += t * t;
     }
     const double rstd = 1.0 / std::sqrt(ss / (double)M + (double)eps);
-    double S1 = 0.0, S2 = 0.0;
+    double S1 = 0.0, S2 = 0.0, S3 = 0.0;
     for (int64_t j = 0; j < M; ++j) {
       const int64_t i = d.at(c, j);
       const double mask = (!relu || half_to_double(y16[i]) > 0.0) ? 1.0 : 0.0;
-      const double g = (double)post_scale * half_to_double(dy16[i]) * mask;
+      const double g = mask > 0.0 ? (double)post_scale * half_to_double(dy16[i]) : 0.0;
       const double xhat = (half_to_double(x16[i]) - mu) * rstd;
       S1 += g;
       S2 += g * xhat;
+      if (swap) S3 += g * half_to_double(res16[i]);
     }
     const double gam = half_to_double(gamma16[c]);
     for (int64_t j = 0; j < M; ++j) {
       const int64_t i = d.at(c, j);
       const double mask = (!relu || half_to_double(y16[i]) > 0.0) ? 1.0 : 0.0;
-      const double g = (double)post_scale * half_to_double(dy16[i]) * mask;
+      const double g = mask > 0.0 ? (double)post_scale * half_to_double(dy16[i]) : 0.0;
       const double xhat = (half_to_double(x16[i]) - mu) * rstd;
       const double v = gam * rstd * (g - S1 / (double)M - xhat * S2 / (double)M);
       if (dx64) dx64[i] = v;
       if (dx16) dx16[i] = round_half(v);
-      if (dres16) dres16[i] = mask > 0.0 ? dy16[i] : (uint16_t)0x0000;
+      if (dres16) {
+        if (swap)
+          dres16[i] = round_half(gam * g);
+        else
+          dres16[i] = mask > 0.0 ? dy16[i] : (uint16_t)0x0000;
+      }
     }
-    if (dgamma64) dgamma64[c] = S2;
+    if (dgamma64) dgamma64[c] = S2 + S3;
     if (dbeta64) dbeta64[c] = S1;
-    if (dgamma16) dgamma16[c] = round_half(S2);
+    if (dgamma16) dgamma16[c] = round_half(S2 + S3);
     if (dbeta16) dbeta16[c] = round_half(S1);
   }
 }
