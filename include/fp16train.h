@@ -80,6 +80,9 @@ typedef struct {
   int32_t relu;       /* 1: apply ReLU to the output; 0: no ReLU */
   int32_t use_stats;  /* 0: compute batch statistics from x and write them to `stats`;
                          1: read mean and rstd from `stats` and only apply */
+  int32_t swap;       /* 0: y = relu(s*(gamma*xhat + beta) + r);
+                         1: the BN swap of Section 4.1, the shortcut joining before gamma:
+                            y = relu(s*(gamma*(xhat + r) + beta)); needs the residual */
 } fp16_bn_desc;
 
 /* Output spatial size of a convolution; FP16_ERR_SHAPE if it is empty. */
@@ -146,6 +149,11 @@ fp16_status fp16_bn_relu(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t
                          const fp16_t* beta, const fp16_t* residual, fp16_t* y, float* stats,
                          void* ws, size_t ws_bytes, fp16_stream_t stream);
 
+/* With desc->swap = 1 (BN swap) the apply step is instead
+ *   sg = fl(s*gamma); a = fl(sg*rstd); b = fl(s*beta); t = fl(x - mean);
+ *   w = fma(sg, r, b); v = fma(t, a, w); y = round_to_binary16(relu(v)),
+ * and residual must not be NULL (FP16_ERR_NULL). */
+
 /* BN backward through the same fused forward (not one of the paper's named
  * operations, but what training through Eq. 1-2 requires):
  *   mask = [y > 0] (all ones without ReLU);  g = s * dy * mask;
@@ -153,6 +161,9 @@ fp16_status fp16_bn_relu(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t
  *   dbeta_c = S1_c;  dgamma_c = S2_c;
  *   dx = gamma_c * rstd_c * (g - S1_c/M - xhat * S2_c/M);
  *   dresidual = mask ? dy : 0  (the gradient reaching the identity shortcut).
+ * With desc->swap = 1: dgamma_c = S2_c + S3_c with S3_c = sum g * r, dx as
+ * above, and dresidual = round_to_binary16(gamma_c * g); residual must not
+ * be NULL.
  * stats holds the forward's mean and rstd (float32, 2C values).  y is the
  * forward output; it may be NULL, in which case the mask is recomputed from
  * x, gamma, beta, residual and stats by the forward's float32 apply

@@ -50,7 +50,7 @@ class BnDesc(ctypes.Structure):
     _fields_ = [("n", ctypes.c_int32), ("c", ctypes.c_int32), ("h", ctypes.c_int32),
                 ("w", ctypes.c_int32), ("layout", ctypes.c_int32), ("eps", ctypes.c_float),
                 ("post_scale", ctypes.c_float), ("relu", ctypes.c_int32),
-                ("use_stats", ctypes.c_int32)]
+                ("use_stats", ctypes.c_int32), ("swap", ctypes.c_int32)]
 
 
 class PoolDesc(ctypes.Structure):
@@ -141,8 +141,10 @@ def conv_desc(n, c, h, w, k, r, s, stride=1, pad=0, layout="NHWC") -> ConvDesc:
     return ConvDesc(n, c, h, w, k, r, s, sh, sw, ph, pw, _LAYOUTS[layout])
 
 
-def bn_desc(n, c, h, w, layout="NHWC", eps=1e-5, post_scale=1.0, relu=True, use_stats=False) -> BnDesc:
-    return BnDesc(n, c, h, w, _LAYOUTS[layout], eps, post_scale, int(bool(relu)), int(bool(use_stats)))
+def bn_desc(n, c, h, w, layout="NHWC", eps=1e-5, post_scale=1.0, relu=True, use_stats=False,
+            swap=False) -> BnDesc:
+    return BnDesc(n, c, h, w, _LAYOUTS[layout], eps, post_scale, int(bool(relu)),
+                  int(bool(use_stats)), int(bool(swap)))
 
 
 # ---- C entry points, same names --------------------------------------------

@@ -341,8 +341,10 @@ static fp16_status check_bn(const fp16_bn_desc* d, BnArgs* a) {
   if ((int64_t)d->n * d->c * d->h * d->w >= kMaxElems) return FP16_ERR_SHAPE;
   if (!(d->eps >= 0.0f) || !(d->post_scale == d->post_scale)) return FP16_ERR_SHAPE;
   if (d->use_stats != 0 && d->use_stats != 1) return FP16_ERR_SHAPE;
+  if (d->swap != 0 && d->swap != 1) return FP16_ERR_SHAPE;
   a->N = d->n; a->C = d->c; a->H = d->h; a->W = d->w; a->layout = d->layout;
   a->eps = d->eps; a->post_scale = d->post_scale; a->relu = d->relu ? 1 : 0;
+  a->swap = d->swap;
   return FP16_OK;
 }
 
@@ -359,6 +361,7 @@ fp16_status fp16_bn_relu(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t
   fp16_status s = check_bn(desc, &a);
   if (s != FP16_OK) return s;
   if (!x || !gamma || !beta || !y || !stats) return FP16_ERR_NULL;
+  if (a.swap && !residual) return FP16_ERR_NULL;
   if (!aligned16(x) || !aligned16(y) || (residual && !aligned16(residual)) || !aligned16(stats))
     return FP16_ERR_MISALIGNED;
   const size_t need = bn_ws_bytes(a);
@@ -386,6 +389,7 @@ fp16_status fp16_bn_relu_bwd(const fp16_bn_desc* desc, const fp16_t* x, const fp
   fp16_status s = check_bn(desc, &a);
   if (s != FP16_OK) return s;
   if (!x || !dy || !gamma || !beta || !stats || !dx || !dgamma || !dbeta) return FP16_ERR_NULL;
+  if (a.swap && !residual) return FP16_ERR_NULL;
   if (!aligned16(x) || (y && !aligned16(y)) || !aligned16(dy) || !aligned16(dx) ||
       (residual && !aligned16(residual)) || (dresidual && !aligned16(dresidual)) ||
       !aligned16(stats))

@@ -10,6 +10,12 @@
 // Backward = reduce (S1 = sum g, S2 = sum g*xhat), finalize (dgamma,
 // dbeta, apply coefficients), apply (dx, dresidual).
 //
+// BN swap (Section 4.1; Geo::swap = 1): the shortcut joins before gamma,
+//   u = s * (gamma * (xhat + r) + beta), applied as
+//   sg = fl(s*gamma); w = fma(sg, r, b); v = fma(t, a, w); y = rne16(relu(v)),
+// and the backward adds S3 = sum g*r to dgamma and sends gamma*g (rounded
+// once) to the shortcut.
+//
 // Bandwidth-bound.  The NHWC path (C a power-of-two multiple of 8, at most
 // 2048) gives each thread a fixed 8-channel chunk, so every access is a
 // 16-byte vector and per-channel coefficients are computed once per thread.
@@ -28,6 +34,7 @@ constexpr int kT = 256;
 struct Geo {
   int64_t M;  // elements per channel
   int C, HW, layout;
+  int swap;   // 1: the shortcut joins before gamma (BN swap)
 };
 
 // memory index of element j (0 <= j < M) of channel c
@@ -74,7 +81,7 @@ Plan make_plan(const BnArgs& a) {
 
 // Per-channel forward coefficients of the declared float32 apply sequence.
 struct FwdCoef {
-  float mean, a, b;
+  float mean, a, b, sg;
 };
 __device__ __forceinline__ FwdCoef fwd_coef(const float* stats, const h16* gamma, const h16* beta,
                                             int C, int c, float s) {
@@ -84,14 +91,20 @@ __device__ __forceinline__ FwdCoef fwd_coef(const float* stats, const h16* gamma
   const float sg = s * to_f32(gamma[c]);
   k.a = sg * rstd;
   k.b = s * to_f32(beta[c]);
+  k.sg = sg;
   return k;
 }
 
 __device__ __forceinline__ float fwd_value(float x, const FwdCoef& k, bool has_r, float r,
-                                           bool relu) {
+                                           bool relu, bool swap) {
   const float t = x - k.mean;
-  float v = __builtin_fmaf(t, k.a, k.b);
-  if (has_r) v = v + r;
+  float v;
+  if (swap) {
+    v = __builtin_fmaf(t, k.a, __builtin_fmaf(k.sg, r, k.b));
+  } else {
+    v = __builtin_fmaf(t, k.a, k.b);
+    if (has_r) v = v + r;
+  }
   if (relu) v = relu_keep_nan(v);
   return v;
 }
@@ -99,55 +112,55 @@ __device__ __forceinline__ float fwd_value(float x, const FwdCoef& k, bool has_r
 // Mask of the ReLU: from the stored output when given, else recomputed bit
 // for bit with the forward sequence.
 __device__ __forceinline__ bool relu_mask(bool relu, bool has_y, h16 y, float x, const FwdCoef& k,
-                                          bool has_r, float r) {
+                                          bool has_r, float r, bool swap) {
   if (!relu) return true;
   if (has_y) return to_f32(y) > 0.0f;
-  return to_f32(to_h16(fwd_value(x, k, has_r, r, true))) > 0.0f;
+  return to_f32(to_h16(fwd_value(x, k, has_r, r, true, swap))) > 0.0f;
 }
 
-// ---- block reduction of 16 float32 partials per thread ----------------------
-// Thread t holds s1[8], s2[8] for the 8 channels of chunk j = t % CV.  Lanes
-// of one wave that hold the same chunk are combined by a butterfly over the
-// lane bits at or above log2(CV); the waves' totals (or, for CV > 64, the
-// threads' own values) are then summed in a fixed order from LDS and written
-// to the channel-major partial arrays out[c * G + block].  red: [16][kT].
-__device__ __forceinline__ void block_reduce_vec(float (&s1)[8], float (&s2)[8], float* red, int CV,
-                                                 int RB, float* out1, float* out2, int G) {
+// ---- block reduction of NS x 8 float32 partials per thread -------------------
+// Thread t holds sums[v][8] (v < NS) for the 8 channels of chunk j = t % CV.
+// Lanes of one wave that hold the same chunk are combined by a butterfly
+// over the lane bits at or above log2(CV); the waves' totals (or, for
+// CV > 64, the threads' own values) are then summed in a fixed order from
+// LDS and written to the channel-major partial arrays
+// out[(v * C + c) * G + block].  red: [8 * NS][kT].
+template <int NS>
+__device__ __forceinline__ void block_reduce_vec(float (&sums)[NS][8], float* red, int CV, int RB,
+                                                 float* out, int G) {
   const int t = threadIdx.x;
   const int lane = t & 63;
   int groups;
   if (CV <= 64) {
     for (int off = CV; off < 64; off <<= 1) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        s1[e] += __shfl_xor(s1[e], off, 64);
-        s2[e] += __shfl_xor(s2[e], off, 64);
-      }
+      for (int v = 0; v < NS; ++v)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sums[v][e] += __shfl_xor(sums[v][e], off, 64);
     }
     groups = kT / 64;
     if (lane < CV) {
       const int slot = (t >> 6) * CV + lane;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        red[e * kT + slot] = s1[e];
-        red[(8 + e) * kT + slot] = s2[e];
-      }
+      for (int v = 0; v < NS; ++v)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) red[(v * 8 + e) * kT + slot] = sums[v][e];
     }
   } else {
     groups = RB;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      red[e * kT + t] = s1[e];
-      red[(8 + e) * kT + t] = s2[e];
-    }
+    for (int v = 0; v < NS; ++v)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) red[(v * 8 + e) * kT + t] = sums[v][e];
   }
   __syncthreads();
-  for (int idx = t; idx < 16 * CV; idx += kT) {
-    const int v = idx / CV, j = idx - v * CV;
-    float acc = red[v * kT + j];
-    for (int gi = 1; gi < groups; ++gi) acc += red[v * kT + gi * CV + j];
-    float* out = v < 8 ? out1 : out2;
-    out[(int64_t)(j * 8 + (v & 7)) * G + blockIdx.x] = acc;
+  const int C = CV * 8;
+  for (int idx = t; idx < 8 * NS * CV; idx += kT) {
+    const int ve = idx / CV, j = idx - ve * CV;
+    float acc = red[ve * kT + j];
+    for (int gi = 1; gi < groups; ++gi) acc += red[ve * kT + gi * CV + j];
+    const int v = ve >> 3, e = ve & 7;
+    out[((int64_t)v * C + j * 8 + e) * G + blockIdx.x] = acc;
   }
 }
 
@@ -156,8 +169,7 @@ __device__ __forceinline__ void block_reduce_vec(float (&s1)[8], float (&s2)[8],
 // (a shift that keeps the variance free of cancellation).
 
 __global__ __launch_bounds__(kT) void bn_fwd_reduce_vec(const h16* __restrict__ x, Geo g, int CV,
-                                                        int RB, int64_t rpb, float* ws1,
-                                                        float* ws2) {
+                                                        int RB, int64_t rpb, float* ws) {
   __shared__ float red[16 * kT];
   const int t = threadIdx.x;
   const int j = t % CV;
@@ -165,12 +177,12 @@ __global__ __launch_bounds__(kT) void bn_fwd_reduce_vec(const h16* __restrict__ 
   int64_t row1 = row0 + rpb;
   if (row1 > g.M) row1 = g.M;
   const V8 kv = load16(x + j * 8);
-  float sh[8], s1[8], s2[8];
+  float sh[8], sums[2][8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     sh[e] = to_f32(kv.h[e]);
-    s1[e] = 0.0f;
-    s2[e] = 0.0f;
+    sums[0][e] = 0.0f;
+    sums[1][e] = 0.0f;
   }
   // four rows in flight per thread; the sums still run row by row
   int64_t row = row0 + t / CV;
@@ -185,32 +197,37 @@ __global__ __launch_bounds__(kT) void bn_fwd_reduce_vec(const h16* __restrict__ 
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float d = to_f32(v[u].h[e]) - sh[e];
-        s1[e] += d;
-        s2[e] = __builtin_fmaf(d, d, s2[e]);
+        sums[0][e] += d;
+        sums[1][e] = __builtin_fmaf(d, d, sums[1][e]);
       }
     }
   }
-  block_reduce_vec(s1, s2, red, CV, RB, ws1, ws2, (int)gridDim.x);
+  block_reduce_vec<2>(sums, red, CV, RB, ws, (int)gridDim.x);
 }
 
-__device__ __forceinline__ void block_reduce_1(float& a, float& b, float* red) {
+// Tree reduction of NS values per thread over the block (fixed order).
+// red: [NS][kT].
+template <int NS>
+__device__ __forceinline__ void block_reduce_1(float (&v)[NS], float* red) {
   const int t = threadIdx.x;
-  red[t] = a;
-  red[kT + t] = b;
+#pragma unroll
+  for (int i = 0; i < NS; ++i) red[i * kT + t] = v[i];
   __syncthreads();
   for (int w = kT / 2; w > 0; w >>= 1) {
     if (t < w) {
-      red[t] += red[t + w];
-      red[kT + t] += red[kT + t + w];
+#pragma unroll
+      for (int i = 0; i < NS; ++i) red[i * kT + t] += red[i * kT + t + w];
     }
     __syncthreads();
   }
-  a = red[0];
-  b = red[kT];
+#pragma unroll
+  for (int i = 0; i < NS; ++i) v[i] = red[i * kT];
 }
 
 __global__ __launch_bounds__(kT) void bn_fwd_reduce_gen(const h16* __restrict__ x, Geo g,
-                                                        int64_t rpb, float* ws1, float* ws2) {
+                                                        int64_t rpb, float* ws) {
+  float* ws1 = ws;
+  float* ws2 = ws + (int64_t)g.C * gridDim.x;
   __shared__ float red[2 * kT];
   const int c = blockIdx.y;
   const int64_t j0 = (int64_t)blockIdx.x * rpb;
@@ -223,10 +240,11 @@ __global__ __launch_bounds__(kT) void bn_fwd_reduce_gen(const h16* __restrict__ 
     s1 += d;
     s2 = __builtin_fmaf(d, d, s2);
   }
-  block_reduce_1(s1, s2, red);
+  float v[2] = {s1, s2};
+  block_reduce_1<2>(v, red);
   if (threadIdx.x == 0) {
-    ws1[(int64_t)c * gridDim.x + blockIdx.x] = s1;
-    ws2[(int64_t)c * gridDim.x + blockIdx.x] = s2;
+    ws1[(int64_t)c * gridDim.x + blockIdx.x] = v[0];
+    ws2[(int64_t)c * gridDim.x + blockIdx.x] = v[1];
   }
 }
 
@@ -268,11 +286,10 @@ __device__ __forceinline__ void channel_sums(const float* ws1, const float* ws2,
 // mean = K + S1/M, var = S2/M - (S1/M)^2 (float64), rstd = 1/sqrt(var + eps).
 // One 64-thread block per channel.
 __global__ __launch_bounds__(64) void bn_fwd_finalize(const h16* __restrict__ x, Geo g, int G,
-                                                      const float* ws1, const float* ws2, float eps,
-                                                      float* stats) {
+                                                      const float* ws, float eps, float* stats) {
   const int c = blockIdx.x;
   double S1, S2;
-  channel_sums(ws1, ws2, c, G, S1, S2);
+  channel_sums(ws, ws + (int64_t)g.C * G, c, G, S1, S2);
   if (threadIdx.x != 0) return;
   const double sh = (double)to_f32(x[geo_at(g, c, 0)]);
   const double md = S1 / (double)g.M;
@@ -319,7 +336,7 @@ __global__ __launch_bounds__(kT) void bn_fwd_apply_vec(const h16* x, const h16* 
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         out.h[e] = to_h16(fwd_value(to_f32(xv[u].h[e]), k[e], res != nullptr,
-                                    res ? to_f32(rv[u].h[e]) : 0.0f, relu != 0));
+                                    res ? to_f32(rv[u].h[e]) : 0.0f, relu != 0, g.swap != 0));
       store16(y + v * 8, out);
     }
   }
@@ -335,12 +352,14 @@ __global__ __launch_bounds__(kT) void bn_fwd_apply_gen(const h16* x, const h16* 
     const int c = geo_chan(g, i);
     const FwdCoef k = fwd_coef(stats, gamma, beta, g.C, c, s);
     y[i] = to_h16(fwd_value(to_f32(x[i]), k, res != nullptr, res ? to_f32(res[i]) : 0.0f,
-                            relu != 0));
+                            relu != 0, g.swap != 0));
   }
 }
 
 // ---- backward reduce -----------------------------------------------------------
 
+// NS = 2: S1 = sum g, S2 = sum g*xhat; NS = 3 (BN swap) adds S3 = sum g*r.
+template <int NS>
 __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ x,
                                                         const h16* __restrict__ y,
                                                         const h16* __restrict__ dy,
@@ -349,23 +368,25 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
                                                         const h16* __restrict__ res,
                                                         const float* __restrict__ stats, Geo g,
                                                         int CV, int RB, int64_t rpb, float s,
-                                                        int relu, float* ws1, float* ws2) {
-  __shared__ float red[16 * kT];
+                                                        int relu, float* ws) {
+  constexpr bool SWAP = NS == 3;
+  __shared__ float red[8 * NS * kT];
   const int t = threadIdx.x;
   const int j = t % CV;
   const int64_t row0 = (int64_t)blockIdx.x * rpb;
   int64_t row1 = row0 + rpb;
   if (row1 > g.M) row1 = g.M;
   FwdCoef k[8];
-  float rstd[8], s1[8], s2[8];
+  float rstd[8], sums[NS][8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     k[e] = fwd_coef(stats, gamma, beta, g.C, j * 8 + e, s);
     rstd[e] = stats[g.C + j * 8 + e];
-    s1[e] = 0.0f;
-    s2[e] = 0.0f;
+#pragma unroll
+    for (int v = 0; v < NS; ++v) sums[v][e] = 0.0f;
   }
   const bool has_y = y != nullptr, has_r = res != nullptr && !has_y && relu;
+  const bool load_r = has_r || SWAP;
   // two rows in flight per thread; the sums still run row by row
   for (int64_t row = row0 + t / CV; row < row1; row += 2 * RB) {
     V8 xv[2], dv[2], yv[2], rv[2];
@@ -376,7 +397,7 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
         xv[u] = load16(x + off);
         dv[u] = load16(dy + off);
         if (relu && has_y) yv[u] = load16(y + off);
-        if (has_r) rv[u] = load16(res + off);
+        if (load_r) rv[u] = load16(res + off);
       }
     }
 #pragma unroll
@@ -385,16 +406,18 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float xf = to_f32(xv[u].h[e]);
+        const float rf = load_r ? to_f32(rv[u].h[e]) : 0.0f;
         const bool m = relu_mask(relu != 0, has_y, has_y ? yv[u].h[e] : (h16)0.0f, xf, k[e],
-                                 has_r, has_r ? to_f32(rv[u].h[e]) : 0.0f);
+                                 has_r, rf, SWAP);
         const float gg = m ? s * to_f32(dv[u].h[e]) : 0.0f;
         const float xh = (xf - k[e].mean) * rstd[e];
-        s1[e] += gg;
-        s2[e] = __builtin_fmaf(gg, xh, s2[e]);
+        sums[0][e] += gg;
+        sums[1][e] = __builtin_fmaf(gg, xh, sums[1][e]);
+        if (SWAP) sums[NS - 1][e] = __builtin_fmaf(gg, rf, sums[NS - 1][e]);
       }
     }
   }
-  block_reduce_vec(s1, s2, red, CV, RB, ws1, ws2, (int)gridDim.x);
+  block_reduce_vec<NS>(sums, red, CV, RB, ws, (int)gridDim.x);
 }
 
 __global__ __launch_bounds__(kT) void bn_bwd_reduce_gen(const h16* __restrict__ x,
@@ -404,47 +427,51 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_gen(const h16* __restrict__ 
                                                         const h16* __restrict__ beta,
                                                         const h16* __restrict__ res,
                                                         const float* __restrict__ stats, Geo g,
-                                                        int64_t rpb, float s, int relu, float* ws1,
-                                                        float* ws2) {
-  __shared__ float red[2 * kT];
+                                                        int64_t rpb, float s, int relu, float* ws) {
+  __shared__ float red[3 * kT];
   const int c = blockIdx.y;
   const int64_t j0 = (int64_t)blockIdx.x * rpb;
   int64_t j1 = j0 + rpb;
   if (j1 > g.M) j1 = g.M;
   const FwdCoef k = fwd_coef(stats, gamma, beta, g.C, c, s);
   const float rstd = stats[g.C + c];
+  const bool swap = g.swap != 0;
   const bool has_y = y != nullptr, has_r = res != nullptr && !has_y && relu;
-  float s1 = 0.0f, s2 = 0.0f;
+  const bool load_r = has_r || swap;
+  float v[3] = {0.0f, 0.0f, 0.0f};
   for (int64_t j = j0 + threadIdx.x; j < j1; j += kT) {
     const int64_t i = geo_at(g, c, j);
     const float xf = to_f32(x[i]);
-    const bool m = relu_mask(relu != 0, has_y, has_y ? y[i] : (h16)0.0f, xf, k, has_r,
-                             has_r ? to_f32(res[i]) : 0.0f);
+    const float rf = load_r ? to_f32(res[i]) : 0.0f;
+    const bool m = relu_mask(relu != 0, has_y, has_y ? y[i] : (h16)0.0f, xf, k, has_r, rf, swap);
     const float gg = m ? s * to_f32(dy[i]) : 0.0f;
     const float xh = (xf - k.mean) * rstd;
-    s1 += gg;
-    s2 = __builtin_fmaf(gg, xh, s2);
+    v[0] += gg;
+    v[1] = __builtin_fmaf(gg, xh, v[1]);
+    v[2] = __builtin_fmaf(gg, rf, v[2]);
   }
-  block_reduce_1(s1, s2, red);
+  block_reduce_1<3>(v, red);
   if (threadIdx.x == 0) {
-    ws1[(int64_t)c * gridDim.x + blockIdx.x] = s1;
-    ws2[(int64_t)c * gridDim.x + blockIdx.x] = s2;
+    const int64_t G = gridDim.x;
+    for (int q = 0; q < (swap ? 3 : 2); ++q) ws[((int64_t)q * g.C + c) * G + blockIdx.x] = v[q];
   }
 }
 
-// dbeta = S1, dgamma = S2 (one rounding from float64); apply coefficients
-// A = gamma*rstd, B = S1/M, D = S2/M for dx = A * (g - (xhat*D + B)).
-// One 64-thread block per channel.
-__global__ __launch_bounds__(64) void bn_bwd_finalize(Geo g, int G, const float* ws1,
-                                                      const float* ws2, const h16* __restrict__ gamma,
+// dbeta = S1, dgamma = S2 (+ S3 with the BN swap), one rounding from float64;
+// apply coefficients A = gamma*rstd, B = S1/M, D = S2/M for
+// dx = A * (g - (xhat*D + B)).  One 64-thread block per channel.
+__global__ __launch_bounds__(64) void bn_bwd_finalize(Geo g, int G, const float* ws,
+                                                      const h16* __restrict__ gamma,
                                                       const float* __restrict__ stats, h16* dgamma,
                                                       h16* dbeta, float* coef) {
   const int c = blockIdx.x;
-  double S1, S2;
-  channel_sums(ws1, ws2, c, G, S1, S2);
+  const int64_t CG = (int64_t)g.C * G;
+  double S1, S2, S3 = 0.0, unused;
+  channel_sums(ws, ws + CG, c, G, S1, S2);
+  if (g.swap) channel_sums(ws + 2 * CG, ws + 2 * CG, c, G, S3, unused);
   if (threadIdx.x != 0) return;
   dbeta[c] = dbl_to_h16(S1);
-  dgamma[c] = dbl_to_h16(S2);
+  dgamma[c] = dbl_to_h16(S2 + S3);
   coef[c] = to_f32(gamma[c]) * stats[g.C + c];
   coef[g.C + c] = (float)(S1 / (double)g.M);
   coef[2 * g.C + c] = (float)(S2 / (double)g.M);
@@ -462,7 +489,7 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* 
   const int t = threadIdx.x;
   const int j = t % CV;  // run starts and kT are multiples of CV
   FwdCoef k[8];
-  float rstd[8], A[8], B[8], D[8];
+  float rstd[8], A[8], B[8], D[8], gam[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const int c = j * 8 + e;
@@ -471,7 +498,9 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* 
     A[e] = coef[c];
     B[e] = coef[g.C + c];
     D[e] = coef[2 * g.C + c];
+    gam[e] = to_f32(gamma[c]);
   }
+  const bool swap = g.swap != 0;
   const bool has_y = y != nullptr, has_r = res != nullptr && !has_y && relu;
   const int64_t nvec = g.M * CV;
   constexpr int U = kApplyU / 2;  // vectors per thread and run: 2 or 3 loads each
@@ -497,11 +526,14 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* 
       for (int e = 0; e < 8; ++e) {
         const float xf = to_f32(xv[u].h[e]);
         const bool m = relu_mask(relu != 0, has_y, has_y ? yv[u].h[e] : (h16)0.0f, xf, k[e],
-                                 has_r, has_r ? to_f32(rv[u].h[e]) : 0.0f);
+                                 has_r, has_r ? to_f32(rv[u].h[e]) : 0.0f, swap);
         const float gg = m ? s * to_f32(dv[u].h[e]) : 0.0f;
         const float xh = (xf - k[e].mean) * rstd[e];
         o.h[e] = to_h16(A[e] * (gg - __builtin_fmaf(xh, D[e], B[e])));
-        od.s[e] = m ? dv[u].s[e] : (uint16_t)0;
+        if (swap)
+          od.h[e] = to_h16(gam[e] * gg);
+        else
+          od.s[e] = m ? dv[u].s[e] : (uint16_t)0;
       }
       store16(dx + v * 8, o);
       if (dres) store16(dres + v * 8, od);
@@ -516,6 +548,7 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_gen(const h16* x, const h16* 
                                                        const float* __restrict__ coef, Geo g,
                                                        float s, int relu, h16* dx, h16* dres) {
   const int64_t total = g.M * g.C;
+  const bool swap = g.swap != 0;
   const bool has_y = y != nullptr, has_r = res != nullptr && !has_y && relu;
   for (int64_t i = (int64_t)blockIdx.x * kT + threadIdx.x; i < total;
        i += (int64_t)gridDim.x * kT) {
@@ -524,11 +557,11 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_gen(const h16* x, const h16* 
     const float xf = to_f32(x[i]);
     const h16 dyv = dy[i];
     const bool m = relu_mask(relu != 0, has_y, has_y ? y[i] : (h16)0.0f, xf, k, has_r,
-                             has_r ? to_f32(res[i]) : 0.0f);
+                             has_r ? to_f32(res[i]) : 0.0f, swap);
     const float gg = m ? s * to_f32(dyv) : 0.0f;
     const float xh = (xf - k.mean) * stats[g.C + c];
     dx[i] = to_h16(coef[c] * (gg - __builtin_fmaf(xh, coef[2 * g.C + c], coef[g.C + c])));
-    if (dres) dres[i] = m ? dyv : (h16)0.0f;
+    if (dres) dres[i] = swap ? to_h16(to_f32(gamma[c]) * gg) : (m ? dyv : (h16)0.0f);
   }
 }
 
@@ -546,16 +579,21 @@ Geo make_geo(const BnArgs& a) {
   g.C = a.C;
   g.HW = a.H * a.W;
   g.layout = a.layout;
+  g.swap = a.swap;
   return g;
 }
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
+// Workspace: up to three channel-major partial arrays [3][C][G] (float32),
+// then the backward's apply coefficients [3][C].
+size_t partial_bytes(const Plan& p, int C) { return align256((size_t)3 * p.G * C * sizeof(float)); }
+
 }  // namespace
 
 size_t bn_ws_bytes(const BnArgs& a) {
   const Plan p = make_plan(a);
-  return align256((size_t)2 * p.G * a.C * sizeof(float)) + align256((size_t)3 * a.C * sizeof(float));
+  return partial_bytes(p, a.C) + align256((size_t)3 * a.C * sizeof(float));
 }
 
 hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const h16* beta,
@@ -563,21 +601,19 @@ hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const 
                          hipStream_t st) {
   const Plan p = make_plan(a);
   const Geo g = make_geo(a);
-  float* ws1 = reinterpret_cast<float*>(ws);
-  float* ws2 = ws1 + (size_t)p.G * a.C;
+  float* part = reinterpret_cast<float*>(ws);
   if (!use_stats) {
     if (p.vec)
       hipLaunchKernelGGL(bn_fwd_reduce_vec, dim3(p.G), dim3(kT), 0, st, x, g, p.CV, p.RB, p.rpb,
-                         ws1, ws2);
+                         part);
     else
-      hipLaunchKernelGGL(bn_fwd_reduce_gen, dim3(p.G, a.C), dim3(kT), 0, st, x, g, p.rpb, ws1, ws2);
-    hipLaunchKernelGGL(bn_fwd_finalize, dim3(a.C), dim3(64), 0, st, x, g, p.G, ws1, ws2, a.eps,
+      hipLaunchKernelGGL(bn_fwd_reduce_gen, dim3(p.G, a.C), dim3(kT), 0, st, x, g, p.rpb, part);
+    hipLaunchKernelGGL(bn_fwd_finalize, dim3(a.C), dim3(64), 0, st, x, g, p.G, part, a.eps,
                        stats);
   }
   if (p.vec)
     hipLaunchKernelGGL(bn_fwd_apply_vec, dim3(apply_grid(g.M * p.CV / kApplyU, p.CV)), dim3(kT),
-                       0, st,
-                       x, gamma, beta, res, y, stats, g, p.CV, a.post_scale, a.relu);
+                       0, st, x, gamma, beta, res, y, stats, g, p.CV, a.post_scale, a.relu);
   else
     hipLaunchKernelGGL(bn_fwd_apply_gen, dim3(apply_grid(g.M * a.C / 4, 1)), dim3(kT), 0, st, x,
                        gamma, beta, res, y, stats, g, a.post_scale, a.relu);
@@ -589,23 +625,25 @@ hipError_t launch_bn_bwd(const BnArgs& a, const h16* x, const h16* y, const h16*
                          h16* dx, h16* dgamma, h16* dbeta, h16* dres, void* ws, hipStream_t st) {
   const Plan p = make_plan(a);
   const Geo g = make_geo(a);
-  float* ws1 = reinterpret_cast<float*>(ws);
-  float* ws2 = ws1 + (size_t)p.G * a.C;
-  float* coef = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) +
-                                         align256((size_t)2 * p.G * a.C * sizeof(float)));
-  if (p.vec)
-    hipLaunchKernelGGL(bn_bwd_reduce_vec, dim3(p.G), dim3(kT), 0, st, x, y, dy, gamma, beta, res,
-                       stats, g, p.CV, p.RB, p.rpb, a.post_scale, a.relu, ws1, ws2);
-  else
+  float* part = reinterpret_cast<float*>(ws);
+  float* coef = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + partial_bytes(p, a.C));
+  if (p.vec) {
+    if (a.swap)
+      hipLaunchKernelGGL(bn_bwd_reduce_vec<3>, dim3(p.G), dim3(kT), 0, st, x, y, dy, gamma, beta,
+                         res, stats, g, p.CV, p.RB, p.rpb, a.post_scale, a.relu, part);
+    else
+      hipLaunchKernelGGL(bn_bwd_reduce_vec<2>, dim3(p.G), dim3(kT), 0, st, x, y, dy, gamma, beta,
+                         res, stats, g, p.CV, p.RB, p.rpb, a.post_scale, a.relu, part);
+  } else {
     hipLaunchKernelGGL(bn_bwd_reduce_gen, dim3(p.G, a.C), dim3(kT), 0, st, x, y, dy, gamma, beta,
-                       res, stats, g, p.rpb, a.post_scale, a.relu, ws1, ws2);
-  hipLaunchKernelGGL(bn_bwd_finalize, dim3(a.C), dim3(64), 0, st, g, p.G, ws1, ws2, gamma, stats,
+                       res, stats, g, p.rpb, a.post_scale, a.relu, part);
+  }
+  hipLaunchKernelGGL(bn_bwd_finalize, dim3(a.C), dim3(64), 0, st, g, p.G, part, gamma, stats,
                      dgamma, dbeta, coef);
   if (p.vec)
     hipLaunchKernelGGL(bn_bwd_apply_vec, dim3(apply_grid(g.M * p.CV / (kApplyU / 2), p.CV)),
-                       dim3(kT), 0, st,
-                       x, y, dy, gamma, beta, res, stats, coef, g, p.CV, a.post_scale, a.relu, dx,
-                       dres);
+                       dim3(kT), 0, st, x, y, dy, gamma, beta, res, stats, coef, g, p.CV,
+                       a.post_scale, a.relu, dx, dres);
   else
     hipLaunchKernelGGL(bn_bwd_apply_gen, dim3(apply_grid(g.M * a.C / 4, 1)), dim3(kT), 0, st, x,
                        y, dy, gamma, beta, res, stats, coef, g, a.post_scale, a.relu, dx, dres);

@@ -101,6 +101,7 @@ struct BnArgs {
   int N, C, H, W, layout;
   float eps, post_scale;
   int relu;
+  int swap;  // BN swap: the shortcut joins before gamma
 };
 size_t bn_ws_bytes(const BnArgs& a);
 hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const h16* beta,

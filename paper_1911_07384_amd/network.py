@@ -13,6 +13,11 @@ step runs over two flat parameter arenas (weight decay on the convolution
 and classifier weights and the classifier bias, none on BN parameters,
 Section 5.1).
 
+Options: ``bn_swap`` makes every block-last BN the BN swap of Section 4.1
+(the shortcut joins before gamma); ``zero_gamma_last`` starts every
+block-last gamma at 0 (the initialisation of Section 5.1; with the swap it
+also zeroes the shortcut's contribution at the start).
+
 The step is an explicit program: a list of ``Op`` records, each one ABI call
 with named device buffers.  Running the list in order is one training step;
 it enqueues on the current stream only and can be captured in a HIP graph.
@@ -44,10 +49,12 @@ class ResNet50:
 
     def __init__(self, n: int = 128, image: int = 224, classes: int = 1000, seed: int = 0,
                  lr: float = 0.1, momentum: float = 0.9, weight_decay: float = 1e-4,
-                 post_scale: float = 0.25, eps: float = 1e-5, stages=STAGES, device="cuda"):
+                 post_scale: float = 0.25, eps: float = 1e-5, stages=STAGES, device="cuda",
+                 bn_swap: bool = False, zero_gamma_last: bool = False):
         self.n, self.image, self.classes = n, image, classes
         self.lr, self.momentum, self.wd = lr, momentum, weight_decay
         self.post_scale, self.eps = post_scale, eps
+        self.bn_swap, self.zero_gamma_last = bn_swap, zero_gamma_last
         self.seed = seed
         self.dev = torch.device(device)
         self._stream_id = 100
@@ -87,9 +94,9 @@ class ResNet50:
         self.fwd.append(Op("conv_fwd", name, {"desc": d, "x": xname, "w": name, "y": name + ".y"}))
         return y
 
-    def _bn(self, name, x, xname, relu, post_scale, res=None):
+    def _bn(self, name, x, xname, relu, post_scale, res=None, swap=False):
         n, h, w, c = x.shape
-        d = F.bn_desc(n, c, h, w, "NHWC", self.eps, post_scale, relu)
+        d = F.bn_desc(n, c, h, w, "NHWC", self.eps, post_scale, relu, swap=swap)
         self._ws_need = max(self._ws_need, F.fp16_bn_workspace_bytes(d))
         y = self._buf(name + ".y", x.shape)
         self._buf(name + ".stats", (2 * c,), torch.float32)
@@ -130,7 +137,8 @@ class ResNet50:
                 else:
                     res = xname
                 blk["res"] = res
-                out = self._bn(nm + ".bn3", y3, nm + ".c3.y", True, s, res=res)
+                out = self._bn(nm + ".bn3", y3, nm + ".c3.y", True, s, res=res,
+                               swap=self.bn_swap)
                 self.blocks.append(blk)
                 x, xname, cin = out, nm + ".bn3.y", cout
         # global average pool to [N, 1, 1, C], classifier as a 1x1 convolution
@@ -250,7 +258,8 @@ class ResNet50:
         self.mbn_arena = torch.zeros(nb, **f16)
         off = 0
         for name, c in self._bnspecs:
-            self.bn_arena[off:off + c].fill_(1.0)
+            last = name.endswith(".bn3") and self.zero_gamma_last
+            self.bn_arena[off:off + c].fill_(0.0 if last else 1.0)
             self.buffers[name + ".gamma"] = self.bn_arena[off:off + c]
             self.buffers[name + ".dgamma"] = self.dbn_arena[off:off + c]
             off += c

@@ -208,3 +208,16 @@ def test_softmax_ce_validation():
     assert l.fp16_softmax_ce(128, 1000, A, B, Cc, D + 4, E, G, None) == MISALIGNED
     assert l.fp16_softmax_ce(128, 1000, A, B, Cc, D, A + 16, G, None) == ALIASING
     assert l.fp16_softmax_ce(128, 1000, A, B, Cc, D, E, B, None) == ALIASING
+
+
+def test_bn_swap_needs_residual_and_valid_flag():
+    l = F.lib()
+    d = F.bn_desc(2, 64, 8, 8, "NHWC", 1e-5, 0.25, True, swap=True)
+    WSB = 1 << 20
+    # residual NULL with swap: FP16_ERR_NULL before anything else is checked
+    assert l.fp16_bn_relu(ctypes.byref(d), A, B, B + 256, None, Cc, WS, WS + 4096, WSB, None) == NULL
+    assert l.fp16_bn_relu_bwd(ctypes.byref(d), A, None, B, Cc, Cc + 256, None, WS, A + 4096,
+                              Cc + 512, Cc + 768, None, WS + 8192, WSB, None) == NULL
+    d.swap = 2
+    assert l.fp16_bn_relu(ctypes.byref(d), A, B, B + 256, A + 64, Cc, WS, WS + 4096, WSB,
+                          None) == SHAPE

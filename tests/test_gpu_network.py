@@ -28,8 +28,8 @@ from paper_1911_07384_amd.network import ResNet50
 pytestmark = pytest.mark.gpu
 
 
-def _net(n=2, image=64, seed=1):
-    net = ResNet50(n=n, image=image, seed=seed)
+def _net(n=2, image=64, seed=1, **kw):
+    net = ResNet50(n=n, image=image, seed=seed, **kw)
     net.load_batch(seed)
     torch.cuda.synchronize()
     return net
@@ -90,14 +90,16 @@ def _check_op(net, op, H):
         shp = oracle.bn_shape(d.n, d.c, d.h, d.w)
         ref = oracle.bn_fwd(shp, H[a["x"]], H[op.name + ".gamma"], H[op.name + ".beta"],
                             None if a["res"] is None else H[a["res"]], d.eps, d.post_scale,
-                            bool(d.relu))
+                            bool(d.relu), swap=bool(d.swap))
         assert ulp_dist(H[a["y"]], ref["y"]).max() <= 1, what
     elif k == "bn_bwd":
         d = a["desc"]
         shp = oracle.bn_shape(d.n, d.c, d.h, d.w)
         y = H[op.name + ".y"]  # the forward output: the mask the GPU recomputed
         ref = oracle.bn_bwd(shp, H[a["x"]], y, H[a["dy"]], H[op.name + ".gamma"], d.eps,
-                            d.post_scale, bool(d.relu), want_dres=a["dres"] is not None)
+                            d.post_scale, bool(d.relu), want_dres=a["dres"] is not None,
+                            swap=bool(d.swap),
+                            residual=None if a["res"] is None else H[a["res"]])
         _close(H[a["dx"]], ref["dx64"], what)
         _small_ok(H[a["dgamma"]], ref["dgamma"], ref["dgamma64"], what + " dgamma")
         _small_ok(H[a["dbeta"]], ref["dbeta"], ref["dbeta64"], what + " dbeta")
@@ -131,9 +133,10 @@ def _check_op(net, op, H):
         raise AssertionError(k)
 
 
-def test_every_call_matches_the_oracle_on_its_own_inputs():
+@pytest.mark.parametrize("variant", ["plain", "bn_swap"])
+def test_every_call_matches_the_oracle_on_its_own_inputs(variant):
     require_gpu()
-    net = _net()
+    net = _net(bn_swap=variant == "bn_swap")
     note("[gpu] resnet50 n=2 64x64 forward+backward")
     net.forward()
     net.backward()

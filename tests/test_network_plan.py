@@ -65,3 +65,13 @@ def test_dataflow(net):
     assert grads == {"d:" + c["name"] for c in net.convs}
     bn_grads = {op.a["dgamma"] for op in net.bwd if op.kind == "bn_bwd"}
     assert bn_grads == {name + ".dgamma" for name, _ in net._bnspecs}
+
+
+def test_bn_swap_and_zero_gamma_options():
+    net = ResNet50(n=1, image=64, device="cpu", bn_swap=True, zero_gamma_last=True)
+    last = [o for o in net.fwd if o.kind == "bn_fwd" and o.name.endswith(".bn3")]
+    assert len(last) == 16 and all(o.a["desc"].swap == 1 for o in last)
+    others = [o for o in net.fwd if o.kind == "bn_fwd" and not o.name.endswith(".bn3")]
+    assert all(o.a["desc"].swap == 0 for o in others)
+    assert all(float(net.buffers[o.name + ".gamma"].abs().max()) == 0.0 for o in last)
+    assert all(float(net.buffers[o.name + ".gamma"].min()) == 1.0 for o in others)
