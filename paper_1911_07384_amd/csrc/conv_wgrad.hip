@@ -191,9 +191,22 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restri
     k = (int)(t / R);
     src = (int64_t)k * Nw + ((int64_t)r * S + s) * Cp + c;
   }
+  // splits grp, grp+4, grp+8, ... added in that order; eight loads are
+  // issued before their adds so the loop is not a chain of load latencies
   float sum = 0.0f;
-  if (i < total)
-    for (int sp = grp; sp < splits; sp += 4) sum += partial[(int64_t)sp * Kp * Nw + src];
+  if (i < total) {
+    const int64_t stride = (int64_t)Kp * Nw;
+    const float* p = partial + src;
+    int sp = grp;
+    for (; sp + 28 < splits; sp += 32) {
+      float v[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) v[u] = p[(int64_t)(sp + 4 * u) * stride];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) sum += v[u];
+    }
+    for (; sp < splits; sp += 4) sum += p[(int64_t)sp * stride];
+  }
   red[grp][lane] = sum;
   __syncthreads();
   if (grp == 0 && i < total) {
@@ -207,8 +220,15 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restri
 struct WCfg {
   int BM, BN;
 };
+// Larger tiles re-read less: a wider N tile reuses the dy tile over more
+// filter columns (three 3x3 taps at once for 64 output channels), a taller M
+// tile reuses the x tile over more output channels.  Each configuration has
+// at most one 8x8 load block per thread (BM + BN <= 256).
 inline WCfg wgrad_cfg(int K, int Nw) {
   if (K >= 128 && Nw >= 128) return {128, 128};
+  if (K >= 128) return {128, 64};
+  if (Nw >= 192 && Nw % 192 == 0) return {64, 192};
+  if (Nw >= 128) return {64, 128};
   return {64, 64};
 }
 
@@ -235,8 +255,14 @@ hipError_t launch_wgrad_partial(const WgradArgs& a, hipStream_t st) {
   const WCfg cfg = wgrad_cfg(a.K, Nw);
   const int tiles = ceil_div(a.K, cfg.BM) * ceil_div(Nw, cfg.BN);
   dim3 grid(tiles, a.splits);
-  if (cfg.BM == 128)
+  if (cfg.BM == 128 && cfg.BN == 128)
     hipLaunchKernelGGL((wgrad_kernel<128, 128, 2, 2>), grid, dim3(256), 0, st, a);
+  else if (cfg.BM == 128)
+    hipLaunchKernelGGL((wgrad_kernel<128, 64, 2, 2>), grid, dim3(256), 0, st, a);
+  else if (cfg.BN == 192)
+    hipLaunchKernelGGL((wgrad_kernel<64, 192, 2, 2>), grid, dim3(256), 0, st, a);
+  else if (cfg.BN == 128)
+    hipLaunchKernelGGL((wgrad_kernel<64, 128, 2, 2>), grid, dim3(256), 0, st, a);
   else
     hipLaunchKernelGGL((wgrad_kernel<64, 64, 2, 2>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
