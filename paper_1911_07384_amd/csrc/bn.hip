@@ -307,6 +307,7 @@ __global__ __launch_bounds__(64) void bn_fwd_finalize(const h16* __restrict__ x,
 // read and then written by the same thread.
 constexpr int kApplyU = 4;
 
+template <bool SWAP>
 __global__ __launch_bounds__(kT) void bn_fwd_apply_vec(const h16* x, const h16* __restrict__ gamma,
                                                        const h16* __restrict__ beta, const h16* res,
                                                        h16* y, const float* __restrict__ stats,
@@ -336,7 +337,7 @@ __global__ __launch_bounds__(kT) void bn_fwd_apply_vec(const h16* x, const h16* 
 #pragma unroll
       for (int e = 0; e < 8; ++e)
         out.h[e] = to_h16(fwd_value(to_f32(xv[u].h[e]), k[e], res != nullptr,
-                                    res ? to_f32(rv[u].h[e]) : 0.0f, relu != 0, g.swap != 0));
+                                    res ? to_f32(rv[u].h[e]) : 0.0f, relu != 0, SWAP));
       store16(y + v * 8, out);
     }
   }
@@ -479,6 +480,7 @@ __global__ __launch_bounds__(64) void bn_bwd_finalize(Geo g, int G, const float*
 
 // ---- backward apply ------------------------------------------------------------
 
+template <bool SWAP>
 __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* y, const h16* dy,
                                                        const h16* __restrict__ gamma,
                                                        const h16* __restrict__ beta, const h16* res,
@@ -500,7 +502,7 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* 
     D[e] = coef[2 * g.C + c];
     gam[e] = to_f32(gamma[c]);
   }
-  const bool swap = g.swap != 0;
+  constexpr bool swap = SWAP;
   const bool has_y = y != nullptr, has_r = res != nullptr && !has_y && relu;
   const int64_t nvec = g.M * CV;
   constexpr int U = kApplyU / 2;  // vectors per thread and run: 2 or 3 loads each
@@ -611,9 +613,14 @@ hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const 
     hipLaunchKernelGGL(bn_fwd_finalize, dim3(a.C), dim3(64), 0, st, x, g, p.G, part, a.eps,
                        stats);
   }
-  if (p.vec)
-    hipLaunchKernelGGL(bn_fwd_apply_vec, dim3(apply_grid(g.M * p.CV / kApplyU, p.CV)), dim3(kT),
-                       0, st, x, gamma, beta, res, y, stats, g, p.CV, a.post_scale, a.relu);
+  if (p.vec && a.swap)
+    hipLaunchKernelGGL(bn_fwd_apply_vec<true>, dim3(apply_grid(g.M * p.CV / kApplyU, p.CV)),
+                       dim3(kT), 0, st, x, gamma, beta, res, y, stats, g, p.CV, a.post_scale,
+                       a.relu);
+  else if (p.vec)
+    hipLaunchKernelGGL(bn_fwd_apply_vec<false>, dim3(apply_grid(g.M * p.CV / kApplyU, p.CV)),
+                       dim3(kT), 0, st, x, gamma, beta, res, y, stats, g, p.CV, a.post_scale,
+                       a.relu);
   else
     hipLaunchKernelGGL(bn_fwd_apply_gen, dim3(apply_grid(g.M * a.C / 4, 1)), dim3(kT), 0, st, x,
                        gamma, beta, res, y, stats, g, a.post_scale, a.relu);
@@ -640,8 +647,12 @@ hipError_t launch_bn_bwd(const BnArgs& a, const h16* x, const h16* y, const h16*
   }
   hipLaunchKernelGGL(bn_bwd_finalize, dim3(a.C), dim3(64), 0, st, g, p.G, part, gamma, stats,
                      dgamma, dbeta, coef);
-  if (p.vec)
-    hipLaunchKernelGGL(bn_bwd_apply_vec, dim3(apply_grid(g.M * p.CV / (kApplyU / 2), p.CV)),
+  if (p.vec && a.swap)
+    hipLaunchKernelGGL(bn_bwd_apply_vec<true>, dim3(apply_grid(g.M * p.CV / (kApplyU / 2), p.CV)),
+                       dim3(kT), 0, st, x, y, dy, gamma, beta, res, stats, coef, g, p.CV,
+                       a.post_scale, a.relu, dx, dres);
+  else if (p.vec)
+    hipLaunchKernelGGL(bn_bwd_apply_vec<false>, dim3(apply_grid(g.M * p.CV / (kApplyU / 2), p.CV)),
                        dim3(kT), 0, st, x, y, dy, gamma, beta, res, stats, coef, g, p.CV,
                        a.post_scale, a.relu, dx, dres);
   else
