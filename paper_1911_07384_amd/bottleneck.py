@@ -11,8 +11,13 @@ convolution weights, none on the BN parameters, Section 5.1).
 Every tensor is binary16 in device memory (no master copy, Section 5.2); the
 per-channel BN statistics are float32 buffers between forward and backward.
 Parameters, gradients and momenta each live in one flat arena per
-weight-decay group, so each SGD update is a single launch.  All work is
-enqueued on the current stream and can be captured in a HIP graph.
+weight-decay group, so each SGD update is a single launch.  The weight
+gradients are off the backward's critical path (nothing reads them before
+the update), so they run on a second stream with their own workspace, each
+after the BN backward that produces its input, and overlap the chain of
+data gradients; the update waits for both streams.  Everything is enqueued
+from the current stream (forked and joined with events), so a step can be
+captured in a HIP graph.
 """
 
 from __future__ import annotations
@@ -111,6 +116,8 @@ class Bottleneck:
         for d in self.bn_desc:
             need = max(need, F.fp16_bn_workspace_bytes(d))
         self.ws = F.workspace(need, dev)
+        self.ws_side = F.workspace(need, dev)  # the weight-gradient stream's own workspace
+        self.side = torch.cuda.Stream(device=dev) if dev.type == "cuda" else None
 
     # ---- the step, one ABI call per line -------------------------------------
 
@@ -127,23 +134,34 @@ class Bottleneck:
                        self.stats[2], ws)
 
     def backward(self):
-        d, ws = self.conv_desc, self.ws
+        d, ws, wss = self.conv_desc, self.ws, self.ws_side
+        main, side = torch.cuda.current_stream(), self.side
+
+        def wgrad_after(i, x, dy):
+            # the weight gradient of conv i on the side stream, once dy exists
+            ev = torch.cuda.Event()
+            ev.record(main)
+            side.wait_event(ev)
+            with torch.cuda.stream(side):
+                F.fp16_conv_wgrad(d[i], x, dy, self.dW[i], wss)
+
         # ReLU masks are recomputed from the conv outputs and statistics (y = None)
         F.fp16_bn_relu_bwd(self.bn_desc[2], self.cv[2], None, self.dout, self.gamma[2], self.beta[2],
                            self.x, self.stats[2], self.dcv[2], self.dgamma[2], self.dbeta[2],
                            self.dshort, ws)
+        wgrad_after(2, self.act[1], self.dcv[2])
         F.fp16_conv_dgrad(d[2], self.dcv[2], self.W[2], self.dact[1], ws)
-        F.fp16_conv_wgrad(d[2], self.act[1], self.dcv[2], self.dW[2], ws)
         F.fp16_bn_relu_bwd(self.bn_desc[1], self.cv[1], None, self.dact[1], self.gamma[1],
                            self.beta[1], None, self.stats[1], self.dcv[1], self.dgamma[1],
                            self.dbeta[1], None, ws)
+        wgrad_after(1, self.act[0], self.dcv[1])
         F.fp16_conv_dgrad(d[1], self.dcv[1], self.W[1], self.dact[0], ws)
-        F.fp16_conv_wgrad(d[1], self.act[0], self.dcv[1], self.dW[1], ws)
         F.fp16_bn_relu_bwd(self.bn_desc[0], self.cv[0], None, self.dact[0], self.gamma[0],
                            self.beta[0], None, self.stats[0], self.dcv[0], self.dgamma[0],
                            self.dbeta[0], None, ws)
+        wgrad_after(0, self.x, self.dcv[0])
         F.fp16_conv_dgrad_add(d[0], self.dcv[0], self.W[0], self.dshort, self.dx, ws)
-        F.fp16_conv_wgrad(d[0], self.x, self.dcv[0], self.dW[0], ws)
+        main.wait_stream(side)  # the update reads every weight gradient
 
     def update(self):
         F.fp16_sgd_step(self.w_arena, self.dw_arena, self.mw_arena, self.w_arena.numel(), self.lr,

@@ -19,9 +19,13 @@ block-last gamma at 0 (the initialisation of Section 5.1; with the swap it
 also zeroes the shortcut's contribution at the start).
 
 The step is an explicit program: a list of ``Op`` records, each one ABI call
-with named device buffers.  Running the list in order is one training step;
-it enqueues on the current stream only and can be captured in a HIP graph.
-The records also let tests replay any call's inputs through the oracle.
+with named device buffers.  Running the list in order is one training step.
+The weight gradients are off the backward's critical path, so ``backward``
+runs them on a second stream with their own workspace, each after an event
+from the call that produced its input gradient, and joins the streams before
+the update; everything else runs in order on the current stream.  The step
+can be captured in a HIP graph.  The records also let tests replay any
+call's inputs through the oracle.
 """
 
 from __future__ import annotations
@@ -68,6 +72,9 @@ class ResNet50:
         self._plan(stages)
         self._allocate_params()
         self.ws = F.workspace(self._ws_need, self.dev)
+        self.ws_side = F.workspace(self._ws_need, self.dev)  # the weight-gradient stream's
+        self.side = torch.cuda.Stream(device=self.dev) if self.dev.type == "cuda" else None
+        self._schedule()
 
     # ---- buffers -------------------------------------------------------------
 
@@ -287,8 +294,9 @@ class ResNet50:
     def _t(self, key):
         return None if key is None else self.buffers[key]
 
-    def run(self, op: Op) -> None:
-        a, t, ws = op.a, self._t, self.ws
+    def run(self, op: Op, ws=None) -> None:
+        a, t = op.a, self._t
+        ws = self.ws if ws is None else ws
         k = op.kind
         if k == "conv_fwd":
             F.fp16_conv_fwd(a["desc"], t(a["x"]), t(a["w"]), t(a["y"]), ws)
@@ -327,21 +335,65 @@ class ResNet50:
     def program(self):
         return self.fwd + self.bwd + self.upd
 
+    _OUTPUTS = {"conv_fwd": ("y",), "conv_dgrad": ("dx",), "conv_dgrad_add": ("dx",),
+                "conv_wgrad": ("dw",), "bn_fwd": ("y", "stats"),
+                "bn_bwd": ("dx", "dgamma", "dbeta", "dres"), "maxpool_fwd": ("y", "idx"),
+                "maxpool_bwd": ("dx",), "avgpool_fwd": ("y",), "avgpool_bwd": ("dx",),
+                "softmax_ce": ("loss", "dz", "dbias")}
+
+    def _schedule(self):
+        """For each weight gradient of the backward, the index (in bwd) of the
+        call that writes its input gradient, or -1 when that happens before the
+        backward starts."""
+        writer = {}
+        self._dep = {}
+        self._mark = set()
+        for i, op in enumerate(self.bwd):
+            if op.kind == "conv_wgrad":
+                dep = writer.get(op.a["dy"], -1)
+                self._dep[i] = dep
+                if dep >= 0:
+                    self._mark.add(dep)
+            else:
+                for k in self._OUTPUTS[op.kind]:
+                    if op.a.get(k) is not None:
+                        writer[op.a[k]] = i
+
     def forward(self):
         for op in self.fwd:
             self.run(op)
 
     def backward(self):
-        for op in self.bwd:
-            self.run(op)
+        if self.side is None:
+            for op in self.bwd:
+                self.run(op)
+            return
+        main, side = torch.cuda.current_stream(), self.side
+        start = torch.cuda.Event()
+        start.record(main)
+        events = {}
+        for i, op in enumerate(self.bwd):
+            if op.kind == "conv_wgrad":
+                dep = self._dep[i]
+                side.wait_event(events[dep] if dep >= 0 else start)
+                with torch.cuda.stream(side):
+                    self.run(op, ws=self.ws_side)
+            else:
+                self.run(op)
+                if i in self._mark:
+                    ev = torch.cuda.Event()
+                    ev.record(main)
+                    events[i] = ev
+        main.wait_stream(side)  # the update reads every weight gradient
 
     def update(self):
         for op in self.upd:
             self.run(op)
 
     def step(self):
-        for op in self.program():
-            self.run(op)
+        self.forward()
+        self.backward()
+        self.update()
 
     def calls(self):
         """(name, thunk) for every ABI call of one step, in order."""
