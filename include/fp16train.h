@@ -186,6 +186,37 @@ fp16_status fp16_bn_relu_bwd(const fp16_bn_desc* desc, const fp16_t* x, const fp
 fp16_status fp16_sgd_step(fp16_t* w, const fp16_t* g, fp16_t* m, size_t n, float lr,
                           float momentum, float weight_decay, fp16_stream_t stream);
 
+/* ---- a convolution fused with the statistics of the BN that follows ---- */
+
+/* Workspace bytes of fp16_conv_bn_relu_fwd; 0 for invalid descriptors. */
+size_t fp16_conv_bn_workspace_bytes(const fp16_conv_desc* conv, const fp16_bn_desc* bn);
+
+/* Convolution forward followed by its BN (+ multiplier, shortcut, ReLU), the
+ * BN statistics taken in the convolution's epilogue instead of a second pass
+ * over y (a fusion of the network's conv -> BN pairs, ResNet-50, Section 5.1;
+ * Eq. 1-2 of Section 4.1):
+ *   y = fp16_conv_fwd(conv, x, w)              (bit-identical to that call)
+ *   mean, rstd of y per channel                 (written to stats[0..2C))
+ *   z = the BN apply of fp16_bn_relu on y with those statistics.
+ * The epilogue keeps, per 128-row tile of y and channel, a shift K (the
+ * tile's first value) and float32 sums of (y - K) and (y - K)^2 over its
+ * rounded values; the tiles are combined in float64.  (Shapes that the
+ * register-direct convolution kernel does not take run the convolution and
+ * the BN's own statistics pass instead, with the same results as the two
+ * separate calls.)  The statistics may differ from fp16_bn_relu's in the last
+ * bits (another summation grouping); z is bit-exact against the declared
+ * apply with the statistics written.
+ * Requires NHWC, conv->k a multiple of 8, a BN descriptor of y's shape
+ * (n = n, c = k, h = p, w = q) with use_stats = 0 (FP16_ERR_UNSUPPORTED /
+ * FP16_ERR_SHAPE otherwise).  z may equal y (then only the BN output
+ * remains) or the residual; y must not overlap x, w, the residual or any
+ * other argument. */
+fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc* bn,
+                                  const fp16_t* x, const fp16_t* w, const fp16_t* gamma,
+                                  const fp16_t* beta, const fp16_t* residual, fp16_t* y,
+                                  fp16_t* z, float* stats, void* ws, size_t ws_bytes,
+                                  fp16_stream_t stream);
+
 /* ---- the rest of ResNet-50 around the residual blocks (Section 5.1) ---- */
 
 /* Pooling problem on x [N,C,H,W] (logical) with an R x S window:

@@ -31,7 +31,7 @@ EXPORTS = ["fp16_conv_out_dims", "fp16_conv_workspace_bytes", "fp16_conv_fwd", "
            "fp16_conv_dgrad_add", "fp16_conv_wgrad", "fp16_bn_workspace_bytes", "fp16_bn_relu", "fp16_bn_relu_bwd",
            "fp16_sgd_step", "fp16_pool_out_dims", "fp16_maxpool_fwd", "fp16_maxpool_bwd",
            "fp16_avgpool_fwd", "fp16_avgpool_bwd", "fp16_softmax_ce", "fp16_status_string",
-           "fp16_version"]
+           "fp16_version", "fp16_conv_bn_workspace_bytes", "fp16_conv_bn_relu_fwd"]
 
 
 class Fp16Error(RuntimeError):
@@ -80,6 +80,8 @@ _SIGS = {
     "fp16_avgpool_fwd": (ctypes.c_int, [_P, _P, _P, _P]),
     "fp16_avgpool_bwd": (ctypes.c_int, [_P, _P, _P, _P]),
     "fp16_softmax_ce": (ctypes.c_int, [_I32, _I32, _P, _P, _P, _P, _P, _P, _P]),
+    "fp16_conv_bn_workspace_bytes": (_SZ, [_P, _P]),
+    "fp16_conv_bn_relu_fwd": (ctypes.c_int, [_P] * 11 + [_SZ, _P]),
     "fp16_status_string": (ctypes.c_char_p, [ctypes.c_int]),
     "fp16_version": (ctypes.c_char_p, []),
 }
@@ -253,6 +255,18 @@ def fp16_softmax_ce(n, k, z, bias, labels, loss, dz, dbias, stream=None) -> None
     _check("fp16_softmax_ce", lib().fp16_softmax_ce(int(n), int(k), _ptr(z), _ptr(bias),
                                                     _ptr(labels), _ptr(loss), _ptr(dz),
                                                     _ptr(dbias), _stream(stream)))
+
+
+def fp16_conv_bn_workspace_bytes(conv: ConvDesc, bn: BnDesc) -> int:
+    return int(lib().fp16_conv_bn_workspace_bytes(ctypes.byref(conv), ctypes.byref(bn)))
+
+
+def fp16_conv_bn_relu_fwd(conv, bn, x, w, gamma, beta, residual, y, z, stats, ws=None,
+                          ws_bytes=None, stream=None) -> None:
+    _check("fp16_conv_bn_relu_fwd", lib().fp16_conv_bn_relu_fwd(
+        ctypes.byref(conv), ctypes.byref(bn), _ptr(x), _ptr(w), _ptr(gamma), _ptr(beta),
+        _ptr(residual), _ptr(y), _ptr(z), _ptr(stats), _ptr(ws), _wsb(ws, ws_bytes),
+        _stream(stream)))
 
 
 def _wsb(ws, ws_bytes):

@@ -55,8 +55,10 @@ class Bottleneck:
     """Device state and the ABI call sequence of one training step."""
 
     def __init__(self, shape: BlockShape = BlockShape(), seed: int = 0, device="cuda",
-                 lr=0.1, momentum=0.9, weight_decay=1e-4, dy_std=1e-3):
+                 lr=0.1, momentum=0.9, weight_decay=1e-4, dy_std=1e-3, fuse_bn_stats=True):
         self.s = s = shape
+        # each conv -> BN pair as one fused call (statistics in the conv epilogue)
+        self.fuse = fuse_bn_stats
         self.lr, self.momentum, self.wd = lr, momentum, weight_decay
         n, hw, c, wdt = s.n, s.hw, s.c, s.width
         dev = torch.device(device)
@@ -115,6 +117,8 @@ class Bottleneck:
                 need = max(need, F.fp16_conv_workspace_bytes(d, p))
         for d in self.bn_desc:
             need = max(need, F.fp16_bn_workspace_bytes(d))
+        for cd, bd in zip(self.conv_desc, self.bn_desc):
+            need = max(need, F.fp16_conv_bn_workspace_bytes(cd, bd))
         self.ws = F.workspace(need, dev)
         self.ws_side = F.workspace(need, dev)  # the weight-gradient stream's own workspace
         self.side = torch.cuda.Stream(device=dev) if dev.type == "cuda" else None
@@ -123,6 +127,13 @@ class Bottleneck:
 
     def forward(self):
         d, ws = self.conv_desc, self.ws
+        if self.fuse:
+            ins, res = [self.x, self.act[0], self.act[1]], [None, None, self.x]
+            for i in range(3):
+                F.fp16_conv_bn_relu_fwd(d[i], self.bn_desc[i], ins[i], self.W[i], self.gamma[i],
+                                        self.beta[i], res[i], self.cv[i], self.act[i],
+                                        self.stats[i], ws)
+            return
         F.fp16_conv_fwd(d[0], self.x, self.W[0], self.cv[0], ws)
         F.fp16_bn_relu(self.bn_desc[0], self.cv[0], self.gamma[0], self.beta[0], None, self.act[0],
                        self.stats[0], ws)
@@ -180,15 +191,24 @@ class Bottleneck:
         """(name, thunk) for every ABI call of one step, in order."""
         d, ws, bd = self.conv_desc, self.ws, self.bn_desc
         c = []
-        c.append(("conv1_fwd", lambda: F.fp16_conv_fwd(d[0], self.x, self.W[0], self.cv[0], ws)))
-        c.append(("bn1_fwd", lambda: F.fp16_bn_relu(bd[0], self.cv[0], self.gamma[0], self.beta[0],
-                                                    None, self.act[0], self.stats[0], ws)))
-        c.append(("conv2_fwd", lambda: F.fp16_conv_fwd(d[1], self.act[0], self.W[1], self.cv[1], ws)))
-        c.append(("bn2_fwd", lambda: F.fp16_bn_relu(bd[1], self.cv[1], self.gamma[1], self.beta[1],
-                                                    None, self.act[1], self.stats[1], ws)))
-        c.append(("conv3_fwd", lambda: F.fp16_conv_fwd(d[2], self.act[1], self.W[2], self.cv[2], ws)))
-        c.append(("bn3_fwd", lambda: F.fp16_bn_relu(bd[2], self.cv[2], self.gamma[2], self.beta[2],
-                                                    self.x, self.act[2], self.stats[2], ws)))
+        if self.fuse:
+            ins, res = [self.x, self.act[0], self.act[1]], [None, None, self.x]
+            for i in range(3):
+                c.append((f"conv{i + 1}_bn{i + 1}_fwd",
+                          lambda i=i: F.fp16_conv_bn_relu_fwd(d[i], bd[i], ins[i], self.W[i],
+                                                              self.gamma[i], self.beta[i], res[i],
+                                                              self.cv[i], self.act[i],
+                                                              self.stats[i], ws)))
+        else:
+            c.append(("conv1_fwd", lambda: F.fp16_conv_fwd(d[0], self.x, self.W[0], self.cv[0], ws)))
+            c.append(("bn1_fwd", lambda: F.fp16_bn_relu(bd[0], self.cv[0], self.gamma[0], self.beta[0],
+                                                        None, self.act[0], self.stats[0], ws)))
+            c.append(("conv2_fwd", lambda: F.fp16_conv_fwd(d[1], self.act[0], self.W[1], self.cv[1], ws)))
+            c.append(("bn2_fwd", lambda: F.fp16_bn_relu(bd[1], self.cv[1], self.gamma[1], self.beta[1],
+                                                        None, self.act[1], self.stats[1], ws)))
+            c.append(("conv3_fwd", lambda: F.fp16_conv_fwd(d[2], self.act[1], self.W[2], self.cv[2], ws)))
+            c.append(("bn3_fwd", lambda: F.fp16_bn_relu(bd[2], self.cv[2], self.gamma[2], self.beta[2],
+                                                        self.x, self.act[2], self.stats[2], ws)))
         c.append(("bn3_bwd", lambda: F.fp16_bn_relu_bwd(
             bd[2], self.cv[2], None, self.dout, self.gamma[2], self.beta[2], self.x, self.stats[2],
             self.dcv[2], self.dgamma[2], self.dbeta[2], self.dshort, ws)))

@@ -557,4 +557,97 @@ fp16_status fp16_softmax_ce(int32_t n, int32_t k, const fp16_t* z, const fp16_t*
                                       static_cast<hipStream_t>(stream)));
 }
 
+// ---- convolution fused with the statistics of the BN that follows ---------------
+
+static fp16_status check_conv_bn(const fp16_conv_desc* cd, const fp16_bn_desc* bd, ConvDims* d,
+                                 BnArgs* b) {
+  fp16_status s = check_conv(cd, d);
+  if (s != FP16_OK) return s;
+  if ((s = check_bn(bd, b)) != FP16_OK) return s;
+  if (d->layout != FP16_NHWC || b->layout != FP16_NHWC || d->K % 8 != 0)
+    return FP16_ERR_UNSUPPORTED;
+  if (b->N != d->N || b->C != d->K || b->H != d->P || b->W != d->Q || bd->use_stats != 0)
+    return FP16_ERR_SHAPE;
+  return FP16_OK;
+}
+
+// Tile records ([nb][3][K] float32, 128 rows each) after the convolution's
+// own workspace; when the convolution does not run on the register-direct
+// kernel, the BN's own workspace takes that place instead.
+static size_t conv_bn_band_off(const ConvDims& d) { return conv_ws(d, FP16_PASS_FWD).total; }
+static int conv_bn_nb(const ConvDims& d) { return (int)(((int64_t)d.N * d.P * d.Q + 127) / 128); }
+
+size_t fp16_conv_bn_workspace_bytes(const fp16_conv_desc* conv, const fp16_bn_desc* bn) {
+  ConvDims d;
+  BnArgs b;
+  if (check_conv_bn(conv, bn, &d, &b) != FP16_OK) return 0;
+  const size_t rec = align256((size_t)3 * d.K * conv_bn_nb(d) * sizeof(float));
+  const size_t bnw = bn_ws_bytes(b);
+  return conv_bn_band_off(d) + (rec > bnw ? rec : bnw);
+}
+
+fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc* bn,
+                                  const fp16_t* x, const fp16_t* w, const fp16_t* gamma,
+                                  const fp16_t* beta, const fp16_t* residual, fp16_t* y,
+                                  fp16_t* z, float* stats, void* ws, size_t ws_bytes,
+                                  fp16_stream_t stream) {
+  ConvDims d;
+  BnArgs b;
+  fp16_status s = check_conv_bn(conv, bn, &d, &b);
+  if (s != FP16_OK) return s;
+  if (!x || !w || !gamma || !beta || !y || !z || !stats) return FP16_ERR_NULL;
+  if (b.swap && !residual) return FP16_ERR_NULL;
+  if (!aligned16(x) || !aligned16(w) || !aligned16(y) || !aligned16(z) || !aligned16(stats) ||
+      (residual && !aligned16(residual)))
+    return FP16_ERR_MISALIGNED;
+  const size_t need = fp16_conv_bn_workspace_bytes(conv, bn);
+  if (!ws || ws_bytes < need) return FP16_ERR_WORKSPACE;
+  if (!aligned16(ws)) return FP16_ERR_MISALIGNED;
+  const size_t yb = (size_t)d.y_elems * 2, xb = (size_t)d.x_elems * 2,
+               wb = (size_t)d.w_elems * 2, cb = (size_t)d.K * 2, sb = (size_t)d.K * 8;
+  if (overlap(y, yb, x, xb) || overlap(y, yb, w, wb) || overlap(y, yb, ws, need) ||
+      overlap(y, yb, gamma, cb) || overlap(y, yb, beta, cb) || overlap(y, yb, stats, sb) ||
+      (z != y && overlap(z, yb, y, yb)) || overlap(z, yb, x, xb) || overlap(z, yb, w, wb) ||
+      overlap(z, yb, ws, need) || overlap(z, yb, gamma, cb) || overlap(z, yb, beta, cb) ||
+      overlap(z, yb, stats, sb) || (residual && z != residual && overlap(z, yb, residual, yb)) ||
+      (residual && overlap(y, yb, residual, yb)) || overlap(stats, sb, ws, need))
+    return FP16_ERR_ALIASING;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const ConvWs L = conv_ws(d, FP16_PASS_FWD);
+  const h16* xe = reinterpret_cast<const h16*>(x);
+  const h16* we = reinterpret_cast<const h16*>(w);
+  if (d.Cp != d.C) {
+    TRY(launch_pad_channels(xe, wsp(ws, L.x), (int64_t)d.N * d.H * d.W, d.C, d.Cp, st));
+    TRY(launch_pad_channels(we, wsp(ws, L.w), (int64_t)d.K * d.R * d.S, d.C, d.Cp, st));
+    xe = wsp(ws, L.x);
+    we = wsp(ws, L.w);
+  }
+  float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + conv_bn_band_off(d));
+  IgemmArgs a{};
+  a.act = xe; a.N = d.N; a.Hi = d.H; a.Wi = d.W; a.Ci = d.Cp;
+  a.stride_h = d.sh; a.stride_w = d.sw;
+  a.Co = d.K; a.out = reinterpret_cast<h16*>(y); a.OH = d.P; a.OW = d.Q; a.ldo = d.K;
+  a.os_h = 1; a.os_w = 1;
+  a.nphase = 1;
+  a.ph[0] = IgemmPhase{we, d.R * d.S * d.Cp, d.R, d.S, d.ph, d.pw, d.P, d.Q, 0, 0};
+  const h16* gp = reinterpret_cast<const h16*>(gamma);
+  const h16* bp = reinterpret_cast<const h16*>(beta);
+  const h16* rp = reinterpret_cast<const h16*>(residual);
+  if (!igemm_direct(a)) {
+    // the statistics need the register-direct kernel's epilogue: run the
+    // convolution and the BN as separate kernels (same results as the two calls)
+    TRY(launch_igemm(a, st));
+    return hip_status(launch_bn_fwd(b, reinterpret_cast<const h16*>(y), gp, bp, rp,
+                                    reinterpret_cast<h16*>(z), stats, 0, part, st));
+  }
+  a.stat = part;
+  a.stat_nb = conv_bn_nb(d);
+  TRY(launch_igemm(a, st));
+  return hip_status(launch_bn_fwd_bands(b, part, a.stat_nb, reinterpret_cast<const h16*>(y),
+                                        reinterpret_cast<const h16*>(gamma),
+                                        reinterpret_cast<const h16*>(beta),
+                                        reinterpret_cast<const h16*>(residual),
+                                        reinterpret_cast<h16*>(z), stats, st));
+}
+
 }  // extern "C"

@@ -299,6 +299,42 @@ __global__ __launch_bounds__(64) void bn_fwd_finalize(const h16* __restrict__ x,
   stats[g.C + c] = (float)(1.0 / __builtin_sqrt(var + (double)eps));
 }
 
+// Statistics from the records a convolution's epilogue wrote ([nb][3][C]:
+// per 128-row tile b and channel c a shift K_b (its first value) and the sums
+// of (y - K_b) and (y - K_b)^2 over its n_b rows).  About K_0:
+//   S1 = sum_b s1_b + n_b d_b,  S2 = sum_b s2_b + 2 d_b s1_b + n_b d_b^2,
+// d_b = K_b - K_0, in float64 (each lane takes every 64th record in order,
+// then a butterfly: a fixed order); then as bn_fwd_finalize.  One 64-thread
+// block per channel.
+__global__ __launch_bounds__(64) void bn_band_finalize(const float* __restrict__ part, int nb,
+                                                       Geo g, float eps, float* stats) {
+  const int c = blockIdx.x;
+  const int t = threadIdx.x;
+  const int64_t C3 = (int64_t)3 * g.C;
+  const double K0 = (double)part[c];
+  double a = 0.0, b = 0.0;
+  for (int j = t; j < nb; j += 64) {
+    const float* rec = part + j * C3 + c;
+    const int64_t rows = g.M - (int64_t)j * 128;
+    const double n = (double)(rows < 128 ? rows : 128);
+    const double d = (double)rec[0] - K0;
+    const double s1 = (double)rec[g.C];
+    a += s1 + n * d;
+    b += (double)rec[2 * g.C] + 2.0 * d * s1 + n * d * d;
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    a += __shfl_xor(a, off, 64);
+    b += __shfl_xor(b, off, 64);
+  }
+  if (t != 0) return;
+  const double md = a / (double)g.M;
+  double var = b / (double)g.M - md * md;
+  if (var < 0.0) var = 0.0;
+  stats[c] = (float)(K0 + md);
+  stats[g.C + c] = (float)(1.0 / __builtin_sqrt(var + (double)eps));
+}
+
 // ---- forward apply -------------------------------------------------------------
 
 // Each block takes runs of kApplyU * kT consecutive 16-byte vectors; a thread
@@ -613,6 +649,26 @@ hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const 
     hipLaunchKernelGGL(bn_fwd_finalize, dim3(a.C), dim3(64), 0, st, x, g, p.G, part, a.eps,
                        stats);
   }
+  if (p.vec && a.swap)
+    hipLaunchKernelGGL(bn_fwd_apply_vec<true>, dim3(apply_grid(g.M * p.CV / kApplyU, p.CV)),
+                       dim3(kT), 0, st, x, gamma, beta, res, y, stats, g, p.CV, a.post_scale,
+                       a.relu);
+  else if (p.vec)
+    hipLaunchKernelGGL(bn_fwd_apply_vec<false>, dim3(apply_grid(g.M * p.CV / kApplyU, p.CV)),
+                       dim3(kT), 0, st, x, gamma, beta, res, y, stats, g, p.CV, a.post_scale,
+                       a.relu);
+  else
+    hipLaunchKernelGGL(bn_fwd_apply_gen, dim3(apply_grid(g.M * a.C / 4, 1)), dim3(kT), 0, st, x,
+                       gamma, beta, res, y, stats, g, a.post_scale, a.relu);
+  return hipGetLastError();
+}
+
+hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, const h16* x,
+                               const h16* gamma, const h16* beta, const h16* res, h16* y,
+                               float* stats, hipStream_t st) {
+  const Plan p = make_plan(a);
+  const Geo g = make_geo(a);
+  hipLaunchKernelGGL(bn_band_finalize, dim3(a.C), dim3(64), 0, st, part, nb, g, a.eps, stats);
   if (p.vec && a.swap)
     hipLaunchKernelGGL(bn_fwd_apply_vec<true>, dim3(apply_grid(g.M * p.CV / kApplyU, p.CV)),
                        dim3(kT), 0, st, x, gamma, beta, res, y, stats, g, p.CV, a.post_scale,

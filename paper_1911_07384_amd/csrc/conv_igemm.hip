@@ -29,7 +29,9 @@
 // Epilogue (both): each wave stages a 32-row band of its float32 tile in LDS
 // and writes whole output rows with 16-byte stores.  Every value is rounded
 // once to binary16 (RNE), optionally after adding a binary16 addend in
-// float32.
+// float32.  igemm4_kernel can also take the statistics of a BN that follows
+// the convolution, without a second pass over the output: per 128-row tile
+// and channel, shifted sums of the rounded values (IgemmArgs::stat).
 
 #include "kernels.hpp"
 
@@ -420,6 +422,11 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
   float* stg = reinterpret_cast<float*>(wave == 0 ? lds0 : wave == 1 ? lds1 : wave == 2 ? lds2 : lds3);
   const int cc = lane & 7;
   const int rr = lane >> 3;
+  // BN statistics: per wave band (32 rows) and channel, the band's first
+  // value K and sums of (y - K), (y - K)^2 over its rounded values; the four
+  // bands of a 128-row tile are then combined (wave order) into one record
+  __shared__ float bst[4][3][64];
+  __shared__ int bcnt[4];
 #pragma unroll
   for (int tm = 0; tm < TM; ++tm) {
 #pragma unroll
@@ -432,6 +439,19 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
       __syncthreads();
       const int n = n0 + nc * 64 + cc * 8;
       const bool vec_ok = (a.ldo % 8) == 0 && n + 8 <= a.Co;
+      const int band_m0 = m0 + wave * 32 * TM + tm * 32;
+      // statistics only for one 32-row band per wave (TM = 1): the four
+      // waves' bands then form one 128-row tile
+      const bool stats = TM == 1 && a.stat != nullptr;
+      float K[8], s1[8], s2[8];
+      if (stats) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          K[e] = to_f32(to_h16(stg[cc * 8 + e]));  // the band's first row, as stored
+          s1[e] = 0.0f;
+          s2[e] = 0.0f;
+        }
+      }
 #pragma unroll
       for (int pass = 0; pass < 4; ++pass) {
         const int r = pass * 8 + rr;
@@ -458,6 +478,14 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
 #pragma unroll
             for (int e = 0; e < 8; ++e) o.h[e] = to_h16(v[e]);
             store16(a.out + off, o);
+            if (stats) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) {
+                const float d = to_f32(o.h[e]) - K[e];
+                s1[e] += d;
+                s2[e] = __builtin_fmaf(d, d, s2[e]);
+              }
+            }
           } else {
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
@@ -469,6 +497,52 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
             }
           }
         }
+      }
+      if (stats) {
+        // lanes with the same 8 channels (lane bits 3-5) combine; lanes 0-7
+        // hold the band's sums
+#pragma unroll
+        for (int sh = 8; sh < 64; sh <<= 1) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            s1[e] += __shfl_xor(s1[e], sh, 64);
+            s2[e] += __shfl_xor(s2[e], sh, 64);
+          }
+        }
+        if (lane < 8) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            bst[wave][0][cc * 8 + e] = K[e];
+            bst[wave][1][cc * 8 + e] = s1[e];
+            bst[wave][2][cc * 8 + e] = s2[e];
+          }
+        }
+        if (lane == 0) {
+          const int rows = M - band_m0;
+          bcnt[wave] = rows <= 0 ? 0 : (rows < 32 ? rows : 32);
+        }
+      }
+      if (stats) __syncthreads();
+      if (stats && wave == 0 && bcnt[0] > 0 && n0 + nc * 64 + lane < a.Co) {
+        // one record per 128-row tile: the bands re-based on the first
+        // band's K (differences of two samples: no cancellation), wave order
+        const int c = lane;
+        const float K0 = bst[0][0][c];
+        float S1 = 0.0f, S2 = 0.0f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const float nw = (float)bcnt[w];
+          if (bcnt[w] == 0) break;
+          const float d = bst[w][0][c] - K0;
+          const float t1 = bst[w][1][c];
+          S1 += __builtin_fmaf(nw, d, t1);
+          S2 += __builtin_fmaf(nw * d, d, __builtin_fmaf(2.0f * d, t1, bst[w][2][c]));
+        }
+        const int tile = m0 / 128;
+        float* rec = a.stat + (int64_t)tile * 3 * a.Co + n0 + nc * 64 + c;
+        rec[0] = K0;
+        rec[a.Co] = S1;
+        rec[2 * a.Co] = S2;
       }
       __syncthreads();
     }
@@ -504,6 +578,17 @@ hipError_t launch_cfg(const IgemmArgs& a, hipStream_t st) {
 
 }  // namespace
 
+bool igemm_direct(const IgemmArgs& a) {
+  int maxM = 0, maxK = 0;
+  for (int p = 0; p < a.nphase; ++p) {
+    const int m = a.N * a.ph[p].Ho * a.ph[p].Wo;
+    const int k = a.ph[p].Rt * a.ph[p].St * a.Ci;
+    if (m > maxM) maxM = m;
+    if (k > maxK) maxK = k;
+  }
+  return (a.Ci % 32 == 0) && (maxK <= 512 || maxM <= 8192);
+}
+
 // Kernel choice per problem (measured on MI355X over the ResNet-50 shapes):
 // the register-direct kernel is faster for short reductions and small M; the
 // LDS-staged one for long reductions over large M.  Results are identical.
@@ -515,7 +600,7 @@ hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st) {
     if (m > maxM) maxM = m;
     if (k > maxK) maxK = k;
   }
-  const bool direct = (a.Ci % 32 == 0) && (maxK <= 512 || maxM <= 8192);
+  const bool direct = igemm_direct(a);
   if (a.Co <= 64) return direct ? launch_cfg4<1, 2>(a, st) : launch_cfg<128, 64, 4, 1, 64>(a, st);
   return direct ? launch_cfg4<1, 4>(a, st) : launch_cfg<128, 128, 2, 2, 64>(a, st);
 }

@@ -48,9 +48,19 @@ struct IgemmArgs {
   int os_h, os_w;
   int nphase;
   IgemmPhase ph[4];
+  // Optional statistics of the rounded output for a following BN (single
+  // phase, Co % 8 == 0, no addend, register-direct kernel only, see
+  // igemm_direct): per 128-row tile b of the output rows and channel c, a
+  // shift K (the tile's first value) and the sums of (y - K) and (y - K)^2
+  // over its rows, at stat[(b * 3 + q) * Co + c], q = 0, 1, 2.
+  float* stat;
+  int stat_nb;
 };
 
 hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st);
+// Whether launch_igemm runs the register-direct kernel for this problem (the
+// one that can take BN statistics in its epilogue).
+bool igemm_direct(const IgemmArgs& a);
 
 // Geometry of one stride phase (ph, pw) of the data gradient.  Output rows
 // h = ph + sh*i (i < Hph) receive exactly the taps r = r0 + sh*t (t < ntr)
@@ -107,6 +117,11 @@ size_t bn_ws_bytes(const BnArgs& a);
 hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const h16* beta,
                          const h16* res, h16* y, float* stats, int use_stats, void* ws,
                          hipStream_t st);
+// Forward from the band records of a convolution epilogue (IgemmArgs::stat):
+// statistics, then the apply.  part: [nb][3][C] float32, 128 rows per record.
+hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, const h16* x,
+                               const h16* gamma, const h16* beta, const h16* res, h16* y,
+                               float* stats, hipStream_t st);
 hipError_t launch_bn_bwd(const BnArgs& a, const h16* x, const h16* y, const h16* dy,
                          const h16* gamma, const h16* beta, const h16* res, const float* stats,
                          h16* dx, h16* dgamma, h16* dbeta, h16* dres, void* ws, hipStream_t st);

@@ -54,11 +54,13 @@ class ResNet50:
     def __init__(self, n: int = 128, image: int = 224, classes: int = 1000, seed: int = 0,
                  lr: float = 0.1, momentum: float = 0.9, weight_decay: float = 1e-4,
                  post_scale: float = 0.25, eps: float = 1e-5, stages=STAGES, device="cuda",
-                 bn_swap: bool = False, zero_gamma_last: bool = False):
+                 bn_swap: bool = False, zero_gamma_last: bool = False,
+                 fuse_bn_stats: bool = True):
         self.n, self.image, self.classes = n, image, classes
         self.lr, self.momentum, self.wd = lr, momentum, weight_decay
         self.post_scale, self.eps = post_scale, eps
         self.bn_swap, self.zero_gamma_last = bn_swap, zero_gamma_last
+        self.fuse = fuse_bn_stats
         self.seed = seed
         self.dev = torch.device(device)
         self._stream_id = 100
@@ -136,13 +138,13 @@ class ResNet50:
                 a1 = self._bn(nm + ".bn1", y1, nm + ".c1.y", True, s)
                 y2 = self._conv(nm + ".c2", a1, nm + ".bn1.y", width, width, 3, st, 1)
                 a2 = self._bn(nm + ".bn2", y2, nm + ".c2.y", True, s)
-                y3 = self._conv(nm + ".c3", a2, nm + ".bn2.y", width, cout, 1, 1, 0)
-                if bi == 0:
+                if bi == 0:  # the shortcut first, so that c3 is followed by its BN
                     yd = self._conv(nm + ".ds", x, xname, cin, cout, 1, st, 0)
                     self._bn(nm + ".bnd", yd, nm + ".ds.y", False, s)
                     res = nm + ".bnd.y"
                 else:
                     res = xname
+                y3 = self._conv(nm + ".c3", a2, nm + ".bn2.y", width, cout, 1, 1, 0)
                 blk["res"] = res
                 out = self._bn(nm + ".bn3", y3, nm + ".c3.y", True, s, res=res,
                                swap=self.bn_swap)
@@ -162,6 +164,30 @@ class ResNet50:
                                                   "dbias": "fc.dbias"}))
         self._last = xname
         self._plan_backward(gd, pd)
+        if self.fuse:
+            self._fuse_conv_bn()
+
+    def _fuse_conv_bn(self):
+        """Each conv whose next forward call is the BN of its output becomes
+        one fp16_conv_bn_relu_fwd call (statistics in the conv epilogue)."""
+        out, i = [], 0
+        while i < len(self.fwd):
+            op = self.fwd[i]
+            nxt = self.fwd[i + 1] if i + 1 < len(self.fwd) else None
+            if (op.kind == "conv_fwd" and nxt is not None and nxt.kind == "bn_fwd"
+                    and nxt.a["x"] == op.a["y"] and op.a["desc"].k % 8 == 0):
+                self._ws_need = max(self._ws_need,
+                                    F.fp16_conv_bn_workspace_bytes(op.a["desc"], nxt.a["desc"]))
+                out.append(Op("conv_bn_fwd", nxt.name,
+                              {"desc": op.a["desc"], "bn": nxt.a["desc"], "x": op.a["x"],
+                               "w": op.a["w"], "y": op.a["y"], "z": nxt.a["y"],
+                               "res": nxt.a["res"], "stats": nxt.a["stats"],
+                               "conv": op.name}))
+                i += 2
+            else:
+                out.append(op)
+                i += 1
+        self.fwd = out
 
     def _grad(self, name):
         """Gradient buffer shaped like buffer `name`, registered as d:<name>."""
@@ -306,6 +332,11 @@ class ResNet50:
             F.fp16_conv_dgrad_add(a["desc"], t(a["dy"]), t(a["w"]), t(a["addend"]), t(a["dx"]), ws)
         elif k == "conv_wgrad":
             F.fp16_conv_wgrad(a["desc"], t(a["x"]), t(a["dy"]), t(a["dw"]), ws)
+        elif k == "conv_bn_fwd":
+            nm = op.name
+            F.fp16_conv_bn_relu_fwd(a["desc"], a["bn"], t(a["x"]), t(a["w"]), t(nm + ".gamma"),
+                                    t(nm + ".beta"), t(a["res"]), t(a["y"]), t(a["z"]),
+                                    t(a["stats"]), ws)
         elif k == "bn_fwd":
             nm = op.name
             F.fp16_bn_relu(a["desc"], t(a["x"]), t(nm + ".gamma"), t(nm + ".beta"), t(a["res"]),
@@ -335,7 +366,8 @@ class ResNet50:
     def program(self):
         return self.fwd + self.bwd + self.upd
 
-    _OUTPUTS = {"conv_fwd": ("y",), "conv_dgrad": ("dx",), "conv_dgrad_add": ("dx",),
+    _OUTPUTS = {"conv_fwd": ("y",), "conv_bn_fwd": ("y", "z", "stats"), "conv_dgrad": ("dx",),
+                "conv_dgrad_add": ("dx",),
                 "conv_wgrad": ("dw",), "bn_fwd": ("y", "stats"),
                 "bn_bwd": ("dx", "dgamma", "dbeta", "dres"), "maxpool_fwd": ("y", "idx"),
                 "maxpool_bwd": ("dx",), "avgpool_fwd": ("y",), "avgpool_bwd": ("dx",),

@@ -221,3 +221,34 @@ def test_bn_swap_needs_residual_and_valid_flag():
     d.swap = 2
     assert l.fp16_bn_relu(ctypes.byref(d), A, B, B + 256, A + 64, Cc, WS, WS + 4096, WSB,
                           None) == SHAPE
+
+
+def test_conv_bn_validation():
+    l = F.lib()
+    cd = F.conv_desc(2, 64, 14, 14, 64, 3, 3, 1, 1)
+    bd = F.bn_desc(2, 64, 14, 14, "NHWC", 1e-5, 0.25, True)
+    assert F.fp16_conv_bn_workspace_bytes(cd, bd) > 0
+    D = 0x50000000
+    args = [A, B, Cc, Cc + 256, None, D, D + (1 << 22), WS, WS + (1 << 22), 1 << 20, None]
+    # a BN descriptor of another shape
+    bad = F.bn_desc(2, 64, 7, 7, "NHWC", 1e-5, 0.25, True)
+    assert l.fp16_conv_bn_relu_fwd(ctypes.byref(cd), ctypes.byref(bad), *args) == SHAPE
+    # given statistics are not what the fused call computes
+    gs = F.bn_desc(2, 64, 14, 14, "NHWC", 1e-5, 0.25, True, use_stats=True)
+    assert l.fp16_conv_bn_relu_fwd(ctypes.byref(cd), ctypes.byref(gs), *args) == SHAPE
+    # NCHW and channel counts that are not multiples of 8 are not fused
+    nchw = F.conv_desc(2, 64, 14, 14, 64, 3, 3, 1, 1, "NCHW")
+    assert l.fp16_conv_bn_relu_fwd(ctypes.byref(nchw), ctypes.byref(bd), *args) == UNSUPPORTED
+    odd = F.conv_desc(2, 64, 14, 14, 60, 3, 3, 1, 1)
+    bodd = F.bn_desc(2, 60, 14, 14, "NHWC", 1e-5, 0.25, True)
+    assert l.fp16_conv_bn_relu_fwd(ctypes.byref(odd), ctypes.byref(bodd), *args) == UNSUPPORTED
+    # workspace too small, missing pointers, overlapping outputs
+    small = list(args)
+    small[9] = 16
+    assert l.fp16_conv_bn_relu_fwd(ctypes.byref(cd), ctypes.byref(bd), *small) == WORKSPACE
+    nul = list(args)
+    nul[6] = None
+    assert l.fp16_conv_bn_relu_fwd(ctypes.byref(cd), ctypes.byref(bd), *nul) == NULL
+    ov = list(args)
+    ov[6] = D + 64  # z overlaps y without being y
+    assert l.fp16_conv_bn_relu_fwd(ctypes.byref(cd), ctypes.byref(bd), *ov) == ALIASING

@@ -1,0 +1,94 @@
+"""GPU parity of fp16_conv_bn_relu_fwd: a convolution whose epilogue also
+takes the statistics of the BN that follows (ResNet-50's conv -> BN pairs,
+Section 5.1; Eq. 1-2 of Section 4.1).
+
+Bars: y bit-identical to fp16_conv_fwd; the statistics within float32
+rounding of the oracle's on that y; z bit-exact against the declared float32
+apply with the written statistics, and within 1 ulp of the oracle's BN."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_1911_07384_amd as F
+from gpu_util import dev, host, note, require_gpu, ulp_dist
+from paper_1911_07384_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+EPS = 1e-5
+
+# n, c, h, k, r, stride, pad, post_scale, residual, relu, swap
+CASES = [
+    (2, 256, 56, 64, 1, 1, 0, 0.25, False, True, False),   # block conv1 + bn1 (register-direct kernel)
+    (4, 64, 56, 64, 3, 1, 1, 0.25, False, True, False),    # 3x3, M > 8192: LDS-staged kernel
+    (2, 64, 28, 256, 1, 1, 0, 0.25, True, True, False),    # block conv3 + bn3 with the shortcut
+    (3, 64, 7, 128, 3, 1, 1, 0.25, False, True, False),    # M = 147: ragged last band
+    (2, 3, 32, 64, 7, 2, 3, 1.0, False, True, False),      # the stem (3 channels staged), s = 1
+    (2, 64, 14, 256, 1, 1, 0, 0.25, True, True, True),     # BN swap on the block-last BN
+    (2, 128, 15, 64, 3, 2, 1, 0.25, False, False, False),  # strided, no ReLU
+    (32, 256, 56, 64, 1, 1, 0, 0.25, False, True, False),  # the conv2_x block's conv1 at batch 32
+]
+
+
+def _ids(c):
+    return "n{}c{}h{}k{}r{}st{}{}{}{}".format(c[0], c[1], c[2], c[3], c[4], c[5],
+                                             "res" if c[8] else "", "relu" if c[9] else "",
+                                             "swap" if c[10] else "")
+
+
+@pytest.mark.parametrize("case", CASES, ids=[_ids(c) for c in CASES])
+def test_conv_bn_fused(case):
+    require_gpu()
+    n, c, h, k, r, st, pad, s, with_res, relu, swap = case
+    cd = F.conv_desc(n, c, h, h, k, r, r, st, pad)
+    p, q = F.fp16_conv_out_dims(cd)
+    bd = F.bn_desc(n, k, p, q, "NHWC", EPS, s, relu, swap=swap)
+    x = synth.normal_f16((n, h, h, c), 1.0, 60 + h, 1)
+    w = synth.normal_f16((k, r, r, c), synth.he_std(c * r * r), 60 + h, 2)
+    gamma = synth.normal_f16((k,), 0.3, 60 + h, 3, mean=1.0)
+    beta = synth.normal_f16((k,), 0.3, 60 + h, 4)
+    res = synth.normal_f16((n, p, q, k), 1.0, 60 + h, 5) if with_res else None
+    X, W, G, B = dev(x), dev(w), dev(gamma), dev(beta)
+    R = dev(res) if with_res else None
+    Y = torch.empty((n, p, q, k), dtype=torch.float16, device="cuda")
+    Z = torch.empty_like(Y)
+    S = torch.empty(2 * k, dtype=torch.float32, device="cuda")
+    ws = F.workspace(F.fp16_conv_bn_workspace_bytes(cd, bd))
+    note(f"[gpu] conv_bn {case}")
+    F.fp16_conv_bn_relu_fwd(cd, bd, X, W, G, B, R, Y, Z, S, ws)
+    Y2 = torch.empty_like(Y)
+    F.fp16_conv_fwd(cd, X, W, Y2, F.workspace(F.fp16_conv_workspace_bytes(cd, F.PASS_FWD)))
+    torch.cuda.synchronize()
+    y, z, st_ = host(Y), host(Z), host(S)
+    assert np.array_equal(y.view(np.uint16), host(Y2).view(np.uint16))
+    shp = oracle.bn_shape(n, k, p, q)
+    ref = oracle.bn_fwd(shp, y, gamma, beta, res, EPS, s, relu, swap=swap)
+    rstd = 1.0 / np.sqrt(ref["var"] + float(np.float32(EPS)))
+    assert np.allclose(st_[:k], ref["mean"], rtol=0, atol=2e-6 * (1 + np.abs(ref["mean"])).max())
+    assert np.allclose(st_[k:], rstd, rtol=4e-6, atol=0)
+    want = oracle.bn_apply_f32(shp, y, gamma, beta, st_[:k], st_[k:], res, s, relu, swap=swap)
+    assert np.array_equal(z.view(np.uint16), want.view(np.uint16))
+    assert ulp_dist(z, ref["y"]).max() <= 1
+
+
+def test_conv_bn_in_place_output():
+    # z may equal y: the convolution output is then replaced by the BN output
+    require_gpu()
+    n, c, h, k = 2, 64, 14, 64
+    cd = F.conv_desc(n, c, h, h, k, 3, 3, 1, 1)
+    bd = F.bn_desc(n, k, h, h, "NHWC", EPS, 0.25, True)
+    x = synth.normal_f16((n, h, h, c), 1.0, 70, 1)
+    w = synth.normal_f16((k, 3, 3, c), synth.he_std(c * 9), 70, 2)
+    g = np.ones(k, np.float16)
+    b = np.zeros(k, np.float16)
+    ws = F.workspace(F.fp16_conv_bn_workspace_bytes(cd, bd))
+    Y = torch.empty((n, h, h, k), dtype=torch.float16, device="cuda")
+    Z = torch.empty_like(Y)
+    S = torch.empty(2 * k, dtype=torch.float32, device="cuda")
+    F.fp16_conv_bn_relu_fwd(cd, bd, dev(x), dev(w), dev(g), dev(b), None, Y, Z, S, ws)
+    Y2 = torch.empty_like(Y)
+    F.fp16_conv_bn_relu_fwd(cd, bd, dev(x), dev(w), dev(g), dev(b), None, Y2, Y2, S, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(Y2.view(torch.int16), Z.view(torch.int16))

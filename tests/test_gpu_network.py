@@ -85,6 +85,20 @@ def _check_op(net, op, H):
         else:
             ref = oracle.conv_wgrad(shp, H[a["x"]], H[a["dy"]])
             _close(H[a["dw"]], ref[0], what, ref[1])
+    elif k == "conv_bn_fwd":
+        ref = oracle.conv_fwd(_conv_shape(a["desc"]), H[a["x"]], H[a["w"]])
+        _close(H[a["y"]], ref[0], what, ref[1])
+        d = a["bn"]
+        shp = oracle.bn_shape(d.n, d.c, d.h, d.w)
+        res = None if a["res"] is None else H[a["res"]]
+        ref = oracle.bn_fwd(shp, H[a["y"]], H[op.name + ".gamma"], H[op.name + ".beta"], res,
+                            d.eps, d.post_scale, bool(d.relu), swap=bool(d.swap))
+        assert ulp_dist(H[a["z"]], ref["y"]).max() <= 1, what
+        st = H[a["stats"]]
+        want = oracle.bn_apply_f32(shp, H[a["y"]], H[op.name + ".gamma"], H[op.name + ".beta"],
+                                   st[:d.c], st[d.c:], res, d.post_scale, bool(d.relu),
+                                   swap=bool(d.swap))
+        assert np.array_equal(H[a["z"]].view(np.uint16), want.view(np.uint16)), what
     elif k == "bn_fwd":
         d = a["desc"]
         shp = oracle.bn_shape(d.n, d.c, d.h, d.w)
@@ -133,10 +147,10 @@ def _check_op(net, op, H):
         raise AssertionError(k)
 
 
-@pytest.mark.parametrize("variant", ["plain", "bn_swap"])
+@pytest.mark.parametrize("variant", ["plain", "bn_swap", "unfused"])
 def test_every_call_matches_the_oracle_on_its_own_inputs(variant):
     require_gpu()
-    net = _net(bn_swap=variant == "bn_swap")
+    net = _net(bn_swap=variant == "bn_swap", fuse_bn_stats=variant != "unfused")
     note("[gpu] resnet50 n=2 64x64 forward+backward")
     net.forward()
     net.backward()
@@ -146,10 +160,11 @@ def test_every_call_matches_the_oracle_on_its_own_inputs(variant):
     for op in net.fwd + net.bwd:
         _check_op(net, op, H)
         kinds.add(op.kind)
-    assert kinds == {"conv_fwd", "conv_dgrad", "conv_dgrad_add", "conv_wgrad", "bn_fwd",
-                     "bn_bwd", "maxpool_fwd", "maxpool_bwd", "avgpool_fwd", "avgpool_bwd",
-                     "softmax_ce"}
-    assert len([o for o in net.fwd if o.kind == "conv_fwd"]) == 54  # 53 convs + classifier
+    fused = {"conv_bn_fwd"} if net.fuse else {"bn_fwd"}
+    assert kinds == {"conv_fwd", "conv_dgrad", "conv_dgrad_add", "conv_wgrad", "bn_bwd",
+                     "maxpool_fwd", "maxpool_bwd", "avgpool_fwd", "avgpool_bwd",
+                     "softmax_ce"} | fused
+    assert len([o for o in net.fwd if o.kind in ("conv_fwd", "conv_bn_fwd")]) == 54
     # the update, bit-exact against the declared float32 sequence
     w0, m0 = host(net.w_arena).copy(), host(net.mw_arena).copy()
     b0, mb0 = host(net.bn_arena).copy(), host(net.mbn_arena).copy()

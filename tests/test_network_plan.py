@@ -15,9 +15,14 @@ def net():
 
 
 def test_layer_and_parameter_counts(net):
-    convs = [o for o in net.fwd if o.kind == "conv_fwd"]
-    assert len(convs) == 54                      # 53 convolutions + the classifier
-    assert len([o for o in net.fwd if o.kind == "bn_fwd"]) == 53
+    kinds = [o.kind for o in net.fwd]
+    # 53 convolutions + the classifier; 53 BNs, each fused with the conv before it
+    assert kinds.count("conv_fwd") + kinds.count("conv_bn_fwd") == 54
+    assert kinds.count("bn_fwd") + kinds.count("conv_bn_fwd") == 53
+    assert kinds.count("conv_bn_fwd") == 53 and kinds.count("conv_fwd") == 1
+    unfused = ResNet50(n=1, image=64, device="cpu", fuse_bn_stats=False)
+    uk = [o.kind for o in unfused.fwd]
+    assert uk.count("conv_fwd") == 54 and uk.count("bn_fwd") == 53
     conv_w = sum(int(np.prod(net.buffers[c["name"]].shape)) for c in net.convs if c["name"] != "fc")
     assert conv_w == 23_454_912
     assert net.n_weights == 23_454_912 + 2_048_000 + 1000
@@ -33,7 +38,8 @@ def test_conv_flops_at_batch_128(net):
     assert net.step_flops() == 3 * net.conv_flops() - 2 * 112 * 112 * 64 * 3 * 49
 
 
-OUTPUTS = {"conv_fwd": ["y"], "conv_dgrad": ["dx"], "conv_dgrad_add": ["dx"],
+OUTPUTS = {"conv_fwd": ["y"], "conv_bn_fwd": ["y", "z", "stats"], "conv_dgrad": ["dx"],
+           "conv_dgrad_add": ["dx"],
            "conv_wgrad": ["dw"], "bn_fwd": ["y", "stats"],
            "bn_bwd": ["dx", "dgamma", "dbeta", "dres"], "maxpool_fwd": ["y", "idx"],
            "maxpool_bwd": ["dx"], "avgpool_fwd": ["y"], "avgpool_bwd": ["dx"],
@@ -51,7 +57,7 @@ def test_dataflow(net):
     for op in net.fwd + net.bwd:
         outs = [k for k in OUTPUTS[op.kind] if op.a.get(k) is not None]
         reads = [v for k, v in op.a.items() if isinstance(v, str) and k not in outs]
-        if op.kind in ("bn_fwd", "bn_bwd"):
+        if op.kind in ("bn_fwd", "bn_bwd", "conv_bn_fwd"):
             reads += [op.name + ".gamma", op.name + ".beta"]
         for v in reads:
             assert v in net.buffers and v in written, (op.name, op.kind, v)
@@ -69,9 +75,11 @@ def test_dataflow(net):
 
 def test_bn_swap_and_zero_gamma_options():
     net = ResNet50(n=1, image=64, device="cpu", bn_swap=True, zero_gamma_last=True)
-    last = [o for o in net.fwd if o.kind == "bn_fwd" and o.name.endswith(".bn3")]
-    assert len(last) == 16 and all(o.a["desc"].swap == 1 for o in last)
-    others = [o for o in net.fwd if o.kind == "bn_fwd" and not o.name.endswith(".bn3")]
-    assert all(o.a["desc"].swap == 0 for o in others)
+    bns = [(o, o.a["bn"] if o.kind == "conv_bn_fwd" else o.a["desc"]) for o in net.fwd
+           if o.kind in ("bn_fwd", "conv_bn_fwd")]
+    last = [o for o, _ in bns if o.name.endswith(".bn3")]
+    assert len(last) == 16 and all(d.swap == 1 for o, d in bns if o.name.endswith(".bn3"))
+    others = [o for o, d in bns if not o.name.endswith(".bn3")]
+    assert all(d.swap == 0 for o, d in bns if not o.name.endswith(".bn3"))
     assert all(float(net.buffers[o.name + ".gamma"].abs().max()) == 0.0 for o in last)
     assert all(float(net.buffers[o.name + ".gamma"].min()) == 1.0 for o in others)
