@@ -200,10 +200,13 @@ size_t fp16_conv_bn_workspace_bytes(const fp16_conv_desc* conv, const fp16_bn_de
  *   z = the BN apply of fp16_bn_relu on y with those statistics.
  * The epilogue keeps, per 128-row tile of y and channel, a shift K (the
  * tile's first value) and float32 sums of (y - K) and (y - K)^2 over its
- * rounded values; the tiles are combined in float64.  (Shapes that the
- * register-direct convolution kernel does not take run the convolution and
- * the BN's own statistics pass instead, with the same results as the two
- * separate calls.)  The statistics may differ from fp16_bn_relu's in the last
+ * rounded values; the tiles are combined in float64.  (Shapes whose
+ * convolution kernel does not take the statistics -- the LDS-staged one,
+ * used for channel counts that are not a multiple of 32 and for long
+ * reductions over large outputs with fewer than 64-multiple channels -- run
+ * the convolution and the BN's own statistics pass instead, with the same
+ * results as the two separate calls.)  The statistics may differ from
+ * fp16_bn_relu's in the last
  * bits (another summation grouping); z is bit-exact against the declared
  * apply with the statistics written.
  * Requires NHWC, conv->k a multiple of 8, a BN descriptor of y's shape

@@ -633,8 +633,8 @@ fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc
   const h16* gp = reinterpret_cast<const h16*>(gamma);
   const h16* bp = reinterpret_cast<const h16*>(beta);
   const h16* rp = reinterpret_cast<const h16*>(residual);
-  if (!igemm_direct(a)) {
-    // the statistics need the register-direct kernel's epilogue: run the
+  if (!igemm_takes_stats(a)) {
+    // the kernel picked for this shape does not take the statistics: run the
     // convolution and the BN as separate kernels (same results as the two calls)
     TRY(launch_igemm(a, st));
     return hip_status(launch_bn_fwd(b, reinterpret_cast<const h16*>(y), gp, bp, rp,

@@ -14,7 +14,7 @@
 // image (or a row past the end) gets an out-of-range offset and reads zeros,
 // with no branch.
 //
-// Two kernels, both v_mfma_f32_32x32x16_f16 with float32 accumulators and
+// Three kernels, all v_mfma_f32_32x32x16_f16 with float32 accumulators and
 // the same k order (so they give identical bits):
 //   igemm_kernel  -- 4 waves in a 2x2 or 4x1 grid; A and B tiles staged in
 //                    LDS through registers, k-step 64, double buffered.
@@ -25,13 +25,21 @@
 //                    four stage buffers with XOR-swizzled rows.  Needs
 //                    Ci % 32 == 0.  Less LDS traffic per MFMA; wins on short
 //                    reductions and small M.
+//   igemm7_kernel -- both operands DMA'd straight from global memory into a
+//                    ring of LDS stages, k-step 64 so that each operand row
+//                    of a stage is one whole 128-byte line, per-row tap masks
+//                    precomputed so a DMA costs a few ALU operations, and the
+//                    MFMA operands read one k sub-step ahead.  Needs
+//                    Ci % 64 == 0; wins on the long reductions (every 3x3
+//                    layer).
 //
-// Epilogue (both): each wave stages a 32-row band of its float32 tile in LDS
+// Epilogue (all): each wave stages a 32-row band of its float32 tile in LDS
 // and writes whole output rows with 16-byte stores.  Every value is rounded
 // once to binary16 (RNE), optionally after adding a binary16 addend in
-// float32.  igemm4_kernel can also take the statistics of a BN that follows
-// the convolution, without a second pass over the output: per 128-row tile
-// and channel, shifted sums of the rounded values (IgemmArgs::stat).
+// float32.  igemm4_kernel and igemm7_kernel can also take the statistics of a
+// BN that follows the convolution, without a second pass over the output:
+// per 128-row tile and channel, shifted sums of the rounded values
+// (IgemmArgs::stat).
 
 #include "kernels.hpp"
 
@@ -549,6 +557,326 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
   }
 }
 
+// ---- k-step 64, whole 128-byte operand rows, fragment reads one sub-step ahead
+// As igemm6, with a k-step of 64 channels: every operand row of a stage is one
+// whole 128-byte line (8 lanes x 16 bytes per row, 8 rows per 1 KB DMA
+// instruction), and each wave does 4 x TM x TN MFMAs per barrier.  The
+// fragments of k sub-step ks+1 are read from LDS while the MFMAs of sub-step
+// ks run; the first sub-step of the next stage is read right after the
+// barrier that publishes it, before the last MFMAs of the current stage.
+// S stages: the stage refilled at the end of step kt is needed at the end of
+// step kt+S-1.  Needs Ci % 64 == 0, at most 32 filter taps per phase, and
+// operands below 1 GiB (the out-of-range offsets used for padding).
+// One 16-byte-per-lane DMA from a buffer resource into LDS (1 KB per wave).
+// (Called through this function: the builtin written directly in the
+// igemm7 lambda made the host pass drop that kernel's launch stubs.)
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t rs, char* lds_dst, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds_dst, 16,
+                                           voff, 0, 0, 0);
+}
+template <int TM, int TN, int WM, int WN, int S>
+struct Cfg7 {
+  static constexpr int BM = 32 * TM * WM, BN = 32 * TN * WN;
+  static constexpr int IA = BM / 32, IB = BN / 32;  // DMA instructions per wave per stage
+  static constexpr int Q = IA + IB;
+  static constexpr int STAGE = (BM + BN) * 128;     // bytes
+  static constexpr int SP = 32 * TN + 4;            // epilogue staging pitch (floats)
+  static constexpr int EPI = 4 * 32 * SP * 4;
+  // BN statistics of the epilogue: [WN][4 bands][3][32*TN] floats + 4 row
+  // counts, after the staging area
+  static constexpr int STAT = WN * 4 * 3 * 32 * TN * 4 + 16;
+  static constexpr int LDS = S * STAGE > EPI + STAT ? S * STAGE : EPI + STAT;
+};
+
+template <int TM, int TN, int WM, int WN, int S, bool STATS>
+__global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
+  using K = Cfg7<TM, TN, WM, WN, S>;
+  constexpr int BM = K::BM, BN = K::BN, IA = K::IA, IB = K::IB;
+  static_assert(WM * WN == 4 && IA >= 1 && IB >= 1 && S >= 2, "tile shape");
+  static_assert(K::Q * (S - 1) < 64, "vmcnt range");
+  __shared__ __attribute__((aligned(1024))) char lds[K::LDS];
+
+  const IgemmPhase ph = a.ph[blockIdx.z];
+  const int HoWo = ph.Ho * ph.Wo;
+  const int M = a.N * HoWo;
+  const int m0 = blockIdx.x * BM;
+  if (m0 >= M) return;
+  const int n0 = blockIdx.y * BN;
+  const int Ci = a.Ci;
+  const int Kg = ph.Rt * ph.St * Ci;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const int act_bytes = (int)((int64_t)a.N * a.Hi * a.Wi * Ci * 2);
+  const int filt_bytes = (int)((int64_t)a.Co * ph.ldb * 2);
+  constexpr uint32_t OOB = 0x80000000u;
+
+  // DMA lane roles: row (wave*I + q)*8 + lane/8 of the tile, physical chunk
+  // lane%8 holding logical chunk (lane%8) ^ ((row/2)%8).  Per A row: the byte
+  // offset of its tap-(0,0) pixel (wrapping below zero in the padding) and a
+  // bit mask of the taps that fall inside the image, so that a k-step costs
+  // one add, one mask test and one select per DMA.
+  uint32_t a_pix[IA], a_vm[IA];
+  uint32_t b_off[IB];
+#pragma unroll
+  for (int q = 0; q < IA; ++q) {
+    const int row = (wave * IA + q) * 8 + (lane >> 3);
+    const int lc = (lane & 7) ^ ((row >> 1) & 7);
+    const int m = m0 + row;
+    a_pix[q] = 0;
+    a_vm[q] = 0;
+    if (m < M) {
+      const int img = m / HoWo;
+      const int rem = m - img * HoWo;
+      const int i = rem / ph.Wo;
+      const int j = rem - i * ph.Wo;
+      const int ih0 = i * a.stride_h - ph.pad_h;
+      const int iw0 = j * a.stride_w - ph.pad_w;
+      a_pix[q] = (uint32_t)((int64_t)img * a.Hi * a.Wi * Ci * 2) +
+                 (uint32_t)(((int64_t)ih0 * a.Wi + iw0) * Ci * 2) + (uint32_t)lc * 16u;
+      for (int r = 0; r < ph.Rt; ++r)
+        for (int t = 0; t < ph.St; ++t)
+          if ((unsigned)(ih0 + r) < (unsigned)a.Hi && (unsigned)(iw0 + t) < (unsigned)a.Wi)
+            a_vm[q] |= 1u << (r * ph.St + t);
+    }
+  }
+#pragma unroll
+  for (int q = 0; q < IB; ++q) {
+    const int row = (wave * IB + q) * 8 + (lane >> 3);
+    const int lc = (lane & 7) ^ ((row >> 1) & 7);
+    const int n = n0 + row;
+    b_off[q] = n < a.Co ? (uint32_t)n * (uint32_t)ph.ldb * 2u + (uint32_t)lc * 16u : 0x40000000u;
+  }
+
+  // k-step state (uniform): channel base, tap, byte offset of the tap's pixel
+  int k0 = 0, cb = 0, tap = 0, ts = 0;
+  uint32_t tap_off = 0;
+  const uint32_t row_bytes = (uint32_t)a.Wi * (uint32_t)Ci * 2u;
+  auto issue = [&](char* buf) {
+    const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<h16*>(a.act), (short)0, act_bytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rs_b = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<h16*>(ph.filt), (short)0, filt_bytes, 0x00020000);
+    const bool kval = k0 < Kg;
+    const uint32_t bit = kval ? 1u << tap : 0u;
+    const uint32_t aoff = tap_off + (uint32_t)cb * 2u;
+#pragma unroll
+    for (int q = 0; q < IA; ++q) {
+      const uint32_t addr = pin_v(a_pix[q] + aoff);
+      dma16(rs_a, buf + (wave * IA + q) * 1024, (a_vm[q] & bit) ? addr : OOB);
+    }
+    const uint32_t boff = kval ? (uint32_t)k0 * 2u : 0x40000000u;
+#pragma unroll
+    for (int q = 0; q < IB; ++q) {
+      dma16(rs_b, buf + BM * 128 + (wave * IB + q) * 1024, b_off[q] + boff);
+    }
+    k0 += 64;
+    cb += 64;
+    if (cb == Ci) {
+      cb = 0;
+      ++tap;
+      if (++ts == ph.St) {
+        ts = 0;
+        tap_off += row_bytes - (uint32_t)(ph.St - 1) * (uint32_t)Ci * 2u;
+      } else {
+        tap_off += (uint32_t)Ci * 2u;
+      }
+    }
+  };
+
+  const int wm = wave / WN, wn = wave % WN;
+  const int lrow = lane & 31, lhi = lane >> 5;
+  const int swz = (lrow >> 1) & 7;
+  floatx16 acc[TM][TN];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[tm][tn][e] = 0.0f;
+
+  half8 af[2][TM], bf[2][TN];
+  auto fetch = [&](const char* buf, int ks, half8 (&fa)[TM], half8 (&fb)[TN]) {
+    const int pos = ((ks * 2 + lhi) ^ swz) * 16;
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+      fa[tm] = *reinterpret_cast<const half8*>(buf + (wm * 32 * TM + tm * 32 + lrow) * 128 + pos);
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn)
+      fb[tn] = *reinterpret_cast<const half8*>(buf + BM * 128 + (wn * 32 * TN + tn * 32 + lrow) * 128 + pos);
+  };
+  auto mma = [&](const half8 (&fa)[TM], const half8 (&fb)[TN]) {
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = mfma32x32x16(fa[tm], fb[tn], acc[tm][tn]);
+  };
+
+  const int KT = (Kg + 63) / 64;
+#pragma unroll
+  for (int s = 0; s < S; ++s) issue(lds + s * K::STAGE);
+  constexpr int ALLOW0 = K::Q * (S - 1);  // prologue: stages 1 .. S-1 stay in flight
+  constexpr int WAIT0 = (0x0 << 8) | (0x7 << 4) | (ALLOW0 & 0xF) | ((ALLOW0 >> 4) << 14);
+  constexpr int ALLOW = K::Q * (S - 2);   // steady state: stages kt+2 .. kt+S-1
+  constexpr int WAIT = (0x0 << 8) | (0x7 << 4) | (ALLOW & 0xF) | ((ALLOW >> 4) << 14);
+  __builtin_amdgcn_s_waitcnt(WAIT0);
+  bare_barrier();
+  fetch(lds, 0, af[0], bf[0]);
+  int rd = 0;
+  for (int kt = 0; kt < KT; ++kt) {
+    const char* cur = lds + rd * K::STAGE;
+    fetch(cur, 1, af[1], bf[1]);
+    mma(af[0], bf[0]);
+    fetch(cur, 2, af[0], bf[0]);
+    mma(af[1], bf[1]);
+    fetch(cur, 3, af[1], bf[1]);
+    mma(af[0], bf[0]);
+    // publish stage kt+1, refill this stage's buffer with stage kt+S, and
+    // read the next stage's first sub-step before the last MFMAs of this one
+    __builtin_amdgcn_s_waitcnt(WAIT);
+    bare_barrier();
+    issue(lds + rd * K::STAGE);
+    rd = rd + 1 == S ? 0 : rd + 1;
+    fetch(lds + rd * K::STAGE, 0, af[0], bf[0]);
+    mma(af[1], bf[1]);
+  }
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  float* stg = reinterpret_cast<float*>(lds) + wave * 32 * K::SP;
+  constexpr int CPR = 32 * TN / 8;  // lanes per row
+  constexpr int RPP = 64 / CPR;     // rows per pass
+  const int cc = lane % CPR;
+  const int rr = lane / CPR;
+  const int n = n0 + wn * 32 * TN + cc * 8;
+  const bool vec_ok = (a.ldo % 8) == 0 && n + 8 <= a.Co;
+  // BN statistics of the rounded output (BM == 128: one record per tile):
+  // per 32-row band and channel the band's first value K and the sums of
+  // (y - K), (y - K)^2, taken column by column from the staged band (one lane
+  // per column, rows in order); the four bands are combined in row order below
+  // (kept inside the one LDS array: a second __shared__ object makes the
+  // compiler wait for every LDS DMA in flight before each LDS read)
+  constexpr int NB = 4, CW = 32 * TN;
+  constexpr int RH = 32 * CW / 64;  // rows per lane
+  static_assert(!STATS || BM == 128, "statistics records cover 128 rows");
+  float (*bst)[NB][3][CW] = reinterpret_cast<float (*)[NB][3][CW]>(lds + K::EPI);
+  int* bcnt = reinterpret_cast<int*>(lds + K::EPI + K::STAT - 16);
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+      for (int e = 0; e < 16; ++e)
+        stg[(8 * (e >> 2) + 4 * lhi + (e & 3)) * K::SP + tn * 32 + lrow] = acc[tm][tn][e];
+    __syncthreads();
+    const int band = wm * TM + tm;
+    const int band_m0 = m0 + band * 32;
+#pragma unroll
+    for (int pass = 0; pass < 32 / RPP; ++pass) {
+      const int r = pass * RPP + rr;
+      const int m = band_m0 + r;
+      if (m < M && n < a.Co) {
+        const int img = m / HoWo;
+        const int rem = m - img * HoWo;
+        const int i = rem / ph.Wo;
+        const int j = rem - i * ph.Wo;
+        const int oh = i * a.os_h + ph.oph;
+        const int ow = j * a.os_w + ph.opw;
+        const int64_t off = ((int64_t)(img * a.OH + oh) * a.OW + ow) * a.ldo + n;
+        const float* src = stg + r * K::SP + cc * 8;
+        float v[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[e] = src[e];
+        if (vec_ok) {
+          if (a.addend) {
+            const V8 ad = load16(a.addend + off);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] += to_f32(ad.h[e]);
+          }
+          V8 o;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o.h[e] = to_h16(v[e]);
+          store16(a.out + off, o);
+        } else {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            if (n + e < a.Co) {
+              float x = v[e];
+              if (a.addend) x += to_f32(a.addend[off + e]);
+              a.out[off + e] = to_h16(x);
+            }
+          }
+        }
+      }
+    }
+    if (STATS) {
+      const int rows = M - band_m0 <= 0 ? 0 : (M - band_m0 < 32 ? M - band_m0 : 32);
+      const int c = lane % CW, h = lane / CW;
+      const float Kc = to_f32(to_h16(stg[c]));  // the band's first row, as stored
+      float s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+      for (int q = 0; q < RH; ++q) {
+        const int r = h * RH + q;
+        if (r < rows) {
+          const float d = to_f32(to_h16(stg[r * K::SP + c])) - Kc;
+          s1 += d;
+          s2 = __builtin_fmaf(d, d, s2);
+        }
+      }
+      if (CW < 64) {  // two lanes per column: rows 0-15 and 16-31
+        s1 += __shfl_xor(s1, 32, 64);
+        s2 += __shfl_xor(s2, 32, 64);
+      }
+      if (lane < CW) {
+        bst[wn][band][0][c] = Kc;
+        bst[wn][band][1][c] = s1;
+        bst[wn][band][2][c] = s2;
+      }
+      if (lane == 0 && wn == 0) bcnt[band] = rows;
+    }
+    __syncthreads();
+  }
+  if (STATS && tid < WN * CW && bcnt[0] > 0) {
+    // one record per 128-row tile: the bands re-based on the first band's K
+    // (differences of two samples: no cancellation), in row order
+    const int h = tid / CW, c = tid % CW;
+    const int col = n0 + h * CW + c;
+    if (col < a.Co) {
+      const float K0 = bst[h][0][0][c];
+      float S1 = 0.0f, S2 = 0.0f;
+#pragma unroll
+      for (int w = 0; w < NB; ++w) {
+        if (bcnt[w] == 0) break;
+        const float nw = (float)bcnt[w];
+        const float d = bst[h][w][0][c] - K0;
+        const float t1 = bst[h][w][1][c];
+        S1 += __builtin_fmaf(nw, d, t1);
+        S2 += __builtin_fmaf(nw * d, d, __builtin_fmaf(2.0f * d, t1, bst[h][w][2][c]));
+      }
+      float* rec = a.stat + (int64_t)(m0 / 128) * 3 * a.Co + col;
+      rec[0] = K0;
+      rec[a.Co] = S1;
+      rec[2 * a.Co] = S2;
+    }
+  }
+}
+
+template <int TM, int TN, int WM, int WN, int S>
+hipError_t launch_cfg7(const IgemmArgs& a, hipStream_t st) {
+  using K = Cfg7<TM, TN, WM, WN, S>;
+  int maxM = 0;
+  for (int p = 0; p < a.nphase; ++p) {
+    const int m = a.N * a.ph[p].Ho * a.ph[p].Wo;
+    if (m > maxM) maxM = m;
+  }
+  if (maxM == 0 || a.nphase == 0) return hipSuccess;
+  dim3 grid(ceil_div(maxM, K::BM), ceil_div(a.Co, K::BN), a.nphase);
+  if (a.stat)
+    hipLaunchKernelGGL((igemm7_kernel<TM, TN, WM, WN, S, true>), grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((igemm7_kernel<TM, TN, WM, WN, S, false>), grid, dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
 template <int TM, int TN>
 hipError_t launch_cfg4(const IgemmArgs& a, hipStream_t st) {
   using K = Cfg4<TM, TN>;
@@ -578,31 +906,56 @@ hipError_t launch_cfg(const IgemmArgs& a, hipStream_t st) {
 
 }  // namespace
 
-bool igemm_direct(const IgemmArgs& a) {
-  int maxM = 0, maxK = 0;
+namespace {
+
+enum class IgemmKind { kLds, kDirect, kDma };
+
+// Kernel choice per problem (measured on MI355X over the ResNet-50 shapes at
+// batch 32 and 128): the DMA-staged kernel for reductions of 576 and more
+// (every 3x3 layer, the 1x1 layers with 1024+ input channels); below that
+// the register-direct kernel for short reductions or small M, else the
+// LDS-staged one.  All three give identical bits.
+IgemmKind igemm_kind(const IgemmArgs& a) {
+  int maxM = 0, maxK = 0, maxT = 0;
+  int64_t maxF = 0;
   for (int p = 0; p < a.nphase; ++p) {
     const int m = a.N * a.ph[p].Ho * a.ph[p].Wo;
-    const int k = a.ph[p].Rt * a.ph[p].St * a.Ci;
+    const int t = a.ph[p].Rt * a.ph[p].St;
+    const int64_t f = (int64_t)a.Co * a.ph[p].ldb * 2;
     if (m > maxM) maxM = m;
-    if (k > maxK) maxK = k;
+    if (t * a.Ci > maxK) maxK = t * a.Ci;
+    if (t > maxT) maxT = t;
+    if (f > maxF) maxF = f;
   }
-  return (a.Ci % 32 == 0) && (maxK <= 512 || maxM <= 8192);
+  const int64_t act = (int64_t)a.N * a.Hi * a.Wi * a.Ci * 2;
+  if (a.Ci % 64 == 0 && maxK >= 576 && maxT <= 32 && act < ((int64_t)1 << 31) &&
+      maxF <= ((int64_t)1 << 30))
+    return IgemmKind::kDma;
+  if (a.Ci % 32 == 0 && (maxK <= 512 || maxM <= 8192)) return IgemmKind::kDirect;
+  return IgemmKind::kLds;
 }
 
-// Kernel choice per problem (measured on MI355X over the ResNet-50 shapes):
-// the register-direct kernel is faster for short reductions and small M; the
-// LDS-staged one for long reductions over large M.  Results are identical.
+}  // namespace
+
+bool igemm_takes_stats(const IgemmArgs& a) { return igemm_kind(a) != IgemmKind::kLds; }
+
 hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st) {
-  int maxM = 0, maxK = 0;
-  for (int p = 0; p < a.nphase; ++p) {
-    const int m = a.N * a.ph[p].Ho * a.ph[p].Wo;
-    const int k = a.ph[p].Rt * a.ph[p].St * a.Ci;
-    if (m > maxM) maxM = m;
-    if (k > maxK) maxK = k;
+  switch (igemm_kind(a)) {
+    case IgemmKind::kDma: {
+      // two stages (two workgroups per CU) unless the grid fits the 256 CUs
+      // once, where a third stage of prefetch costs no occupancy
+      int maxM = 0;
+      for (int p = 0; p < a.nphase; ++p) maxM = max(maxM, a.N * a.ph[p].Ho * a.ph[p].Wo);
+      const bool narrow = a.Co <= 64;
+      const int64_t wgs = (int64_t)ceil_div(maxM, 128) * ceil_div(a.Co, narrow ? 64 : 128) * a.nphase;
+      if (narrow) return wgs <= 256 ? launch_cfg7<2, 1, 2, 2, 3>(a, st) : launch_cfg7<2, 1, 2, 2, 2>(a, st);
+      return wgs <= 256 ? launch_cfg7<2, 2, 2, 2, 3>(a, st) : launch_cfg7<2, 2, 2, 2, 2>(a, st);
+    }
+    case IgemmKind::kDirect:
+      return a.Co <= 64 ? launch_cfg4<1, 2>(a, st) : launch_cfg4<1, 4>(a, st);
+    default:
+      return a.Co <= 64 ? launch_cfg<128, 64, 4, 1, 64>(a, st) : launch_cfg<128, 128, 2, 2, 64>(a, st);
   }
-  const bool direct = igemm_direct(a);
-  if (a.Co <= 64) return direct ? launch_cfg4<1, 2>(a, st) : launch_cfg<128, 64, 4, 1, 64>(a, st);
-  return direct ? launch_cfg4<1, 4>(a, st) : launch_cfg<128, 128, 2, 2, 64>(a, st);
 }
 
 }  // namespace fp16k

@@ -49,8 +49,8 @@ struct IgemmArgs {
   int nphase;
   IgemmPhase ph[4];
   // Optional statistics of the rounded output for a following BN (single
-  // phase, Co % 8 == 0, no addend, register-direct kernel only, see
-  // igemm_direct): per 128-row tile b of the output rows and channel c, a
+  // phase, Co % 8 == 0, no addend, and a kernel that takes them, see
+  // igemm_takes_stats): per 128-row tile b of the output rows and channel c, a
   // shift K (the tile's first value) and the sums of (y - K) and (y - K)^2
   // over its rows, at stat[(b * 3 + q) * Co + c], q = 0, 1, 2.
   float* stat;
@@ -58,9 +58,9 @@ struct IgemmArgs {
 };
 
 hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st);
-// Whether launch_igemm runs the register-direct kernel for this problem (the
-// one that can take BN statistics in its epilogue).
-bool igemm_direct(const IgemmArgs& a);
+// Whether the kernel launch_igemm picks for this problem can take the BN
+// statistics (IgemmArgs::stat) in its epilogue.
+bool igemm_takes_stats(const IgemmArgs& a);
 
 // Geometry of one stride phase (ph, pw) of the data gradient.  Output rows
 // h = ph + sh*i (i < Hph) receive exactly the taps r = r0 + sh*t (t < ntr)

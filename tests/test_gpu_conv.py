@@ -37,6 +37,9 @@ SHAPES = [
     (2, 64, 12, 12, 64, 3, 3, 1, 1, "NCHW"),
     (2, 3, 20, 20, 16, 7, 7, 2, 3, "NCHW"),
     (2, 64, 15, 15, 128, 1, 1, 2, 0, "NCHW"),
+    (2, 64, 15, 15, 64, 3, 3, 2, 1, "NHWC"),    # strided 3x3 on the DMA-staged kernel (fwd)
+    (2, 256, 9, 9, 192, 3, 3, 2, 1, "NHWC"),    # dgrad phases of up to 4 taps x 192: DMA-staged; ragged N
+    (2, 1024, 5, 5, 96, 1, 1, 1, 0, "NHWC"),    # 1x1 with a 1024-long reduction: DMA-staged
 ]
 
 
