@@ -167,6 +167,226 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
   }
 }
 
+// ---- DMA-staged variant: no register transposes ------------------------------
+// For channel counts that are multiples of 64.  Each stage covers 64 pixels:
+// the dy rows (BM channels) and the x patch rows (BN filter columns, 64 per
+// tap and channel block) are DMA'd pixel-major straight into LDS, in 8 KB
+// sub-tiles of 64 pixel rows x 128 bytes (16-byte chunks XOR-swizzled by
+// pixel row).  The MFMA operands, which need 8 consecutive pixels per lane,
+// come from the transposing LDS read of gfx950 (ds_read_b64_tr_b16: within
+// each 16-lane group, lane b*4+a receives element a of the 8-byte rows that
+// lanes b, b+4, b+8 and b+12 address), two reads per operand.  S stages in a
+// ring, operand reads one k sub-step ahead, as in the implicit-GEMM kernel.
+// The k order (pixels) and the split plan are those of wgrad_kernel, so the
+// partial sums are the same.
+
+typedef short short4v __attribute__((ext_vector_type(4)));
+
+// One 16-byte-per-lane DMA from a buffer resource into LDS (1 KB per wave).
+__device__ __forceinline__ void wdma16(__amdgpu_buffer_rsrc_t rs, char* lds_dst, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (__attribute__((address_space(3))) void*)lds_dst, 16,
+                                           voff, 0, 0, 0);
+}
+
+// Four binary16 values from the transposing LDS read.
+__device__ __forceinline__ short4v ldtr(const char* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) short4v*)(const_cast<char*>(p)));
+}
+
+__device__ __forceinline__ void wbarrier() { __asm__ volatile("s_barrier" ::: "memory"); }
+
+template <int BM, int BN, int WM, int WN, int S>
+struct WCfg7 {
+  static constexpr int SA = BM / 64, SB = BN / 64;  // 64-channel sub-tiles
+  static constexpr int NI = (SA + SB) * 8;          // DMA instructions per stage
+  static constexpr int IW = NI / 4;                 // per wave
+  static constexpr int STAGE = (SA + SB) * 8192;    // bytes
+  static constexpr int WTM = BM / WM, WTN = BN / WN;
+  static constexpr int TM = WTM / 32, TN = WTN / 32;
+};
+
+template <int BM, int BN, int WM, int WN, int S>
+__global__ __launch_bounds__(256) void wgrad7_kernel(const WgradArgs a) {
+  using K = WCfg7<BM, BN, WM, WN, S>;
+  constexpr int SA = K::SA, IW = K::IW, TM = K::TM, TN = K::TN, WTM = K::WTM, WTN = K::WTN;
+  static_assert(WM * WN == 4 && TM >= 1 && TN >= 1 && S >= 2, "tile shape");
+  static_assert(IW * (S - 1) < 64, "vmcnt range");
+  __shared__ __attribute__((aligned(1024))) char lds[S * K::STAGE];
+
+  const int Nw = a.R * a.S * a.C;
+  const int tiles_n = (Nw + BN - 1) / BN;
+  const int m0 = (blockIdx.x / tiles_n) * BM;
+  const int n0 = (blockIdx.x % tiles_n) * BN;
+  const int split = blockIdx.y;
+  const int64_t npix = (int64_t)a.N * a.P * a.Q;
+  const int64_t pbeg = (int64_t)split * a.pix_per_split;
+  int64_t pend = pbeg + a.pix_per_split;
+  if (pend > npix) pend = npix;
+  const int KT = pend > pbeg ? (int)((pend - pbeg + 63) / 64) : 0;
+
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  constexpr uint32_t OOB = 0x80000000u;
+  const int dy_bytes = (int)(npix * a.K * 2);
+  const int x_bytes = (int)((int64_t)a.N * a.H * a.W * a.C * 2);
+
+  // DMA roles: instruction i of this wave fills sub-tile i/2, pixel rows
+  // rb*8 .. rb*8+7 with rb = 4*(i%2) + wave; a lane covers pixel row
+  // rb*8 + lane/8 and physical chunk lane%8, holding logical chunk
+  // (lane%8) ^ swz(row), swz(row) = 2*((row/2)%4)
+  int prow[2], img[2], pp[2], qq[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    prow[h] = (4 * h + wave) * 8 + (lane >> 3);
+    const int64_t pix = pbeg + prow[h];
+    const int64_t PQ = (int64_t)a.P * a.Q;
+    img[h] = (int)(pix / PQ);
+    const int rem = (int)(pix - (int64_t)img[h] * PQ);
+    pp[h] = rem / a.Q;
+    qq[h] = rem - pp[h] * a.Q;
+  }
+  const int dq = 64 % a.Q, dp = (64 / a.Q) % a.P, dimg = 64 / (a.P * a.Q);
+  int lc[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) lc[h] = (lane & 7) ^ (((prow[h] >> 1) & 3) << 1);
+
+  int64_t pstage = pbeg;  // first pixel of the next stage to issue
+  auto issue = [&](char* buf) {
+    const __amdgpu_buffer_rsrc_t rs_dy = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<h16*>(a.dy), (short)0, dy_bytes, 0x00020000);
+    const __amdgpu_buffer_rsrc_t rs_x = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<h16*>(a.x), (short)0, x_bytes, 0x00020000);
+#pragma unroll
+    for (int i = 0; i < IW; ++i) {
+      const int h = i & 1;
+      const int sub = i >> 1;
+      const int rb = 4 * h + wave;
+      char* dst = buf + sub * 8192 + rb * 1024;
+      const int64_t pix = pstage + prow[h];
+      const bool pv = pix < pend;
+      if (sub < SA) {
+        const int m = m0 + sub * 64;
+        const uint32_t off = (uint32_t)((pix * a.K + m + lc[h] * 8) * 2);
+        wdma16(rs_dy, dst, (pv && m < a.K) ? off : OOB);
+      } else {
+        const int cb = n0 + (sub - SA) * 64;
+        const int tap = cb / a.C;
+        const int c0 = cb - tap * a.C;
+        const int r = tap / a.S, t = tap - r * a.S;
+        const int ih = pp[h] * a.sh - a.ph + r, iw = qq[h] * a.sw - a.pw + t;
+        const bool v = pv && cb < Nw && (unsigned)ih < (unsigned)a.H && (unsigned)iw < (unsigned)a.W;
+        const uint32_t off =
+            (uint32_t)(((((int64_t)img[h] * a.H + ih) * a.W + iw) * a.C + c0 + lc[h] * 8) * 2);
+        wdma16(rs_x, dst, v ? off : OOB);
+      }
+    }
+    // advance the two pixel rows by 64
+    pstage += 64;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      qq[h] += dq;
+      const int c1 = qq[h] >= a.Q;
+      qq[h] -= c1 ? a.Q : 0;
+      pp[h] += dp + c1;
+      const int c2 = pp[h] >= a.P;
+      pp[h] -= c2 ? a.P : 0;
+      img[h] += dimg + c2;
+    }
+  };
+
+  const int wm = wave / WN, wn = wave % WN;
+  const int g = lane >> 4, j = lane & 15;
+  // transposing-read address pieces of this lane: pixel row within a k16
+  // sub-step, and channel quad within a 32-row operand
+  const int kr_l = 8 * (g >> 1) + (j >> 2);
+  const int ch_l = 16 * (g & 1) + 4 * (j & 3);
+  floatx16 acc[TM][TN];
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[tm][tn][e] = 0.0f;
+
+  // operand of 32 channels starting at channel `c` of a 64-channel region
+  // (sub-tile base `sb`), pixels ks*16 .. ks*16+15 of the stage
+  auto operand = [&](const char* sb, int c, int ks) {
+    const int ch = c + ch_l;
+    const int lcn = ch >> 3, hf = (ch >> 2) & 1;
+    const int kr0 = ks * 16 + kr_l, kr1 = kr0 + 4;
+    const short4v v0 = ldtr(sb + kr0 * 128 + ((lcn ^ (((kr0 >> 1) & 3) << 1)) << 4) + hf * 8);
+    const short4v v1 = ldtr(sb + kr1 * 128 + ((lcn ^ (((kr1 >> 1) & 3) << 1)) << 4) + hf * 8);
+    // (one shuffle and one bit cast: element-wise insertion of the two
+    // halves was miscompiled into a broadcast of the first element)
+    return __builtin_bit_cast(half8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
+  half8 af[2][TM], bf[2][TN];
+  auto fetch = [&](const char* buf, int ks, half8 (&fa)[TM], half8 (&fb)[TN]) {
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) {
+      const int c = wm * WTM + tm * 32;
+      fa[tm] = operand(buf + (c >> 6) * 8192, c & 63, ks);
+    }
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      const int c = wn * WTN + tn * 32;
+      fb[tn] = operand(buf + (SA + (c >> 6)) * 8192, c & 63, ks);
+    }
+  };
+  auto mma = [&](const half8 (&fa)[TM], const half8 (&fb)[TN]) {
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm)
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = mfma32x32x16(fa[tm], fb[tn], acc[tm][tn]);
+  };
+
+  if (KT > 0) {
+#pragma unroll
+    for (int s = 0; s < S; ++s) issue(lds + s * K::STAGE);
+    constexpr int ALLOW0 = IW * (S - 1);
+    constexpr int WAIT0 = (0x0 << 8) | (0x7 << 4) | (ALLOW0 & 0xF) | ((ALLOW0 >> 4) << 14);
+    constexpr int ALLOW = IW * (S - 2);
+    constexpr int WAIT = (0x0 << 8) | (0x7 << 4) | (ALLOW & 0xF) | ((ALLOW >> 4) << 14);
+    __builtin_amdgcn_s_waitcnt(WAIT0);
+    wbarrier();
+    fetch(lds, 0, af[0], bf[0]);
+    int rd = 0;
+    for (int kt = 0; kt < KT; ++kt) {
+      const char* cur = lds + rd * K::STAGE;
+      fetch(cur, 1, af[1], bf[1]);
+      mma(af[0], bf[0]);
+      fetch(cur, 2, af[0], bf[0]);
+      mma(af[1], bf[1]);
+      fetch(cur, 3, af[1], bf[1]);
+      mma(af[0], bf[0]);
+      __builtin_amdgcn_s_waitcnt(WAIT);
+      wbarrier();
+      issue(lds + rd * K::STAGE);
+      rd = rd + 1 == S ? 0 : rd + 1;
+      fetch(lds + rd * K::STAGE, 0, af[0], bf[0]);
+      mma(af[1], bf[1]);
+    }
+    __builtin_amdgcn_s_waitcnt(0);
+  }
+
+  // float32 partial tile of this split
+  float* out = a.partial + (int64_t)split * a.K * Nw;
+#pragma unroll
+  for (int tm = 0; tm < TM; ++tm) {
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int m = m0 + wm * WTM + tm * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+      if (m >= a.K) continue;
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        const int n = n0 + wn * WTN + tn * 32 + (lane & 31);
+        if (n < Nw) out[(int64_t)m * Nw + n] = acc[tm][tn][e];
+      }
+    }
+  }
+}
+
 // dw = rne16(sum over splits), written KRSC or KCRS with the real C.  A block
 // of 256 threads owns 64 consecutive outputs; its four waves each add every
 // fourth split (in order), and the four subtotals are added in a fixed order,
@@ -231,12 +451,24 @@ inline WCfg wgrad_cfg(int K, int Nw) {
   if (Nw >= 128) return {64, 128};
   return {64, 64};
 }
+// The DMA-staged kernel (channel counts multiples of 64) and its tiles.
+inline bool wgrad_dma(int K, int C) { return K % 64 == 0 && C % 64 == 0; }
+inline WCfg wgrad7_cfg(int K, int Nw) {
+  if (K >= 128 && Nw >= 128) return {128, 128};
+  if (K >= 128) return {128, 64};
+  if (Nw >= 256) return {64, 256};
+  if (Nw >= 128) return {64, 128};
+  return {64, 64};
+}
+inline WCfg wgrad_choice(int K, int C, int Nw) {
+  return wgrad_dma(K, C) ? wgrad7_cfg(K, Nw) : wgrad_cfg(K, Nw);
+}
 
 }  // namespace
 
 void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int* splits, int* pix_per_split) {
   const int Nw = R * S * Cp;
-  const WCfg cfg = wgrad_cfg(K, Nw);
+  const WCfg cfg = wgrad_choice(K, Cp, Nw);
   const int64_t tiles = (int64_t)ceil_div(K, cfg.BM) * ceil_div(Nw, cfg.BN);
   int64_t want = (512 + tiles - 1) / tiles;           // about two workgroups per CU
   const int64_t max_splits = (npix + 2 * BKP - 1) / (2 * BKP);  // at least two k-steps each
@@ -252,9 +484,22 @@ void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int* splits, int* pix
 
 hipError_t launch_wgrad_partial(const WgradArgs& a, hipStream_t st) {
   const int Nw = a.R * a.S * a.C;
-  const WCfg cfg = wgrad_cfg(a.K, Nw);
+  const WCfg cfg = wgrad_choice(a.K, a.C, Nw);
   const int tiles = ceil_div(a.K, cfg.BM) * ceil_div(Nw, cfg.BN);
   dim3 grid(tiles, a.splits);
+  if (wgrad_dma(a.K, a.C)) {
+    if (cfg.BM == 128 && cfg.BN == 128)
+      hipLaunchKernelGGL((wgrad7_kernel<128, 128, 2, 2, 2>), grid, dim3(256), 0, st, a);
+    else if (cfg.BM == 128)
+      hipLaunchKernelGGL((wgrad7_kernel<128, 64, 2, 2, 2>), grid, dim3(256), 0, st, a);
+    else if (cfg.BN == 256)
+      hipLaunchKernelGGL((wgrad7_kernel<64, 256, 1, 4, 2>), grid, dim3(256), 0, st, a);
+    else if (cfg.BN == 128)
+      hipLaunchKernelGGL((wgrad7_kernel<64, 128, 2, 2, 2>), grid, dim3(256), 0, st, a);
+    else
+      hipLaunchKernelGGL((wgrad7_kernel<64, 64, 2, 2, 2>), grid, dim3(256), 0, st, a);
+    return hipGetLastError();
+  }
   if (cfg.BM == 128 && cfg.BN == 128)
     hipLaunchKernelGGL((wgrad_kernel<128, 128, 2, 2>), grid, dim3(256), 0, st, a);
   else if (cfg.BM == 128)
