@@ -436,6 +436,36 @@ __global__ __launch_bounds__(256) void wgrad_reduce_kernel(const float* __restri
   }
 }
 
+// Few splits, KRSC output with unpadded channels (the partial rows are then
+// the output rows): each thread adds four consecutive outputs over all splits
+// in split order (16-byte loads, four splits in flight), and rounds once.
+__global__ __launch_bounds__(256) void wgrad_reduce_vec_kernel(const float* __restrict__ partial,
+                                                               int splits, int64_t total,
+                                                               int64_t stride, h16* __restrict__ dw) {
+  const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  if (i >= total) return;
+  const floatx4* p = reinterpret_cast<const floatx4*>(partial + i);
+  const int64_t st4 = stride / 4;
+  floatx4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+  int sp = 0;
+  for (; sp + 4 <= splits; sp += 4) {
+    const floatx4 v0 = p[(sp + 0) * st4], v1 = p[(sp + 1) * st4];
+    const floatx4 v2 = p[(sp + 2) * st4], v3 = p[(sp + 3) * st4];
+    acc += v0;
+    acc += v1;
+    acc += v2;
+    acc += v3;
+  }
+  for (; sp < splits; ++sp) acc += p[sp * st4];
+  union {
+    h16 h[4];
+    uint2 u;
+  } o;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) o.h[e] = to_h16(acc[e]);
+  *reinterpret_cast<uint2*>(dw + i) = o.u;
+}
+
 // Tile configuration shared by the plan and the launch.
 struct WCfg {
   int BM, BN;
@@ -453,8 +483,9 @@ inline WCfg wgrad_cfg(int K, int Nw) {
 }
 // The DMA-staged kernel (channel counts multiples of 64) and its tiles.
 inline bool wgrad_dma(int K, int C) { return K % 64 == 0 && C % 64 == 0; }
+// (measured on the ResNet-50 shapes at batch 128: narrower tiles at higher
+// occupancy beat 128 x 128 once K >= 128)
 inline WCfg wgrad7_cfg(int K, int Nw) {
-  if (K >= 128 && Nw >= 128) return {128, 128};
   if (K >= 128) return {128, 64};
   if (Nw >= 256) return {64, 256};
   if (Nw >= 128) return {64, 128};
@@ -516,6 +547,12 @@ hipError_t launch_wgrad_partial(const WgradArgs& a, hipStream_t st) {
 hipError_t launch_wgrad_reduce(const float* partial, int splits, int K, int Kp, int R, int S, int C,
                                int Cp, int layout, h16* dw, hipStream_t st) {
   const int64_t total = (int64_t)K * R * S * C;
+  if (layout == 0 && C == Cp && splits <= 32) {
+    const int64_t threads = total / 4;  // C % 8 == 0 here
+    hipLaunchKernelGGL(wgrad_reduce_vec_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0,
+                       st, partial, splits, total, (int64_t)Kp * R * S * Cp, dw);
+    return hipGetLastError();
+  }
   const int64_t blocks = (total + 63) / 64;
   hipLaunchKernelGGL(wgrad_reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, st, partial, splits,
                      K, Kp, R, S, C, Cp, layout, dw);
