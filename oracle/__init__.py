@@ -69,6 +69,12 @@ _SIGS = {
     "oracle_avgpool_fwd": (None, [_P, _P, _P, _P]),
     "oracle_avgpool_bwd": (None, [_P, _P, _P]),
     "oracle_softmax_ce": (None, [_I64, _I64, _P, _P, _P, _P, _P, _P, _P]),
+    "oracle_fma16": (ctypes.c_uint16, [ctypes.c_uint16, ctypes.c_uint16, ctypes.c_uint16]),
+    "oracle_fma16_array": (None, [_P, _P, _P, _P, _I64]),
+    "oracle_sgd_f16": (None, [_P, _P, _P, _I64, _F32, _F32, _F32]),
+    "oracle_conv_fwd_f16acc": (None, [_P, _P, _P, _P]),
+    "oracle_conv_dgrad_f16acc": (None, [_P, _P, _P, _P]),
+    "oracle_conv_wgrad_f16acc": (None, [_P, _P, _P, _P]),
 }
 
 
@@ -299,6 +305,51 @@ def sgd_f64(w, g, m, lr, momentum, weight_decay):
     lib().oracle_sgd_f64(_ptr(w), _ptr(g), _ptr(m), w.size, float(lr), float(momentum),
                          float(weight_decay))
     return w.view(np.float16), m.view(np.float16)
+
+
+# ---- strict binary16 arithmetic (all operations in FP16) --------------------
+
+def fma16(a, b, c):
+    """Elementwise binary16 fused multiply-add, one rounding (arrays)."""
+    a, b, c = (_h(np.asarray(v, dtype=np.float16) if np.asarray(v).dtype != np.uint16 else v)
+               for v in (a, b, c))
+    a, b, c = np.broadcast_arrays(a, b, c)
+    a, b, c = (np.ascontiguousarray(v) for v in (a, b, c))
+    out = np.empty(a.shape, np.uint16)
+    lib().oracle_fma16_array(_ptr(a), _ptr(b), _ptr(c), _ptr(out), a.size)
+    return out.view(np.float16)
+
+
+def sgd_f16(w, g, m, lr, momentum, weight_decay):
+    """SGD with every operation a binary16 fma; the scalars are the binary16
+    roundings of the float32 arguments."""
+    w = _h(w).copy()
+    m = _h(m).copy()
+    g = _h(g)
+    lib().oracle_sgd_f16(_ptr(w), _ptr(g), _ptr(m), w.size, float(lr), float(momentum),
+                         float(weight_decay))
+    return w.view(np.float16), m.view(np.float16)
+
+
+def _f16acc(fn, shp, a, b, which):
+    assert int(shp[11]) == 0, "binary16 accumulation is defined for NHWC / KRSC"
+    a, b = _h(a), _h(b)
+    out = np.empty(_act_shape(shp, which), np.uint16)
+    fn(_ptr(shp), _ptr(a), _ptr(b), _ptr(out))
+    return out.view(np.float16)
+
+
+def conv_fwd_f16acc(shp, x, w):
+    """Forward convolution with a binary16 accumulator rounded per 16 terms."""
+    return _f16acc(lib().oracle_conv_fwd_f16acc, shp, x, w, "y")
+
+
+def conv_dgrad_f16acc(shp, dy, w):
+    return _f16acc(lib().oracle_conv_dgrad_f16acc, shp, dy, w, "x")
+
+
+def conv_wgrad_f16acc(shp, x, dy):
+    return _f16acc(lib().oracle_conv_wgrad_f16acc, shp, x, dy, "w")
 
 
 # ---- pooling, classifier bias and loss --------------------------------------

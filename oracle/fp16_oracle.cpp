@@ -750,3 +750,190 @@ void oracle_softmax_ce(int64_t N, int64_t K, const uint16_t* z16, const uint16_t
 }
 
 }  // extern "C"
+
+// ===========================================================================
+// Strict binary16 arithmetic (the literal reading of Section 5.2: all
+// arithmetic in FP16, not only storage).  Used to measure what the float32
+// accumulators of the default path buy; not the product's default.
+// ===========================================================================
+
+namespace {
+
+// binary16 round-to-nearest-even of the exact value s + err, where s is a
+// double and err the exact error of the double addition that produced s
+// (TwoSum).  |err| is far below half a binary16 ulp, so it only decides the
+// result when s lies exactly halfway between two binary16 values.
+uint16_t round_half_exact(double s, double err) {
+  const uint16_t r = round_half(s);
+  if (err == 0.0 || std::isnan(s) || std::isinf(s)) return r;
+  const bool neg = std::signbit(s);
+  const double a = std::fabs(s);
+  const double e = neg ? -err : err;
+  const uint16_t ra = (uint16_t)(r & 0x7FFF);
+  const double v = half_to_double(ra);
+  if (v == a) return r;
+  double lo, hi;
+  uint16_t lob, hib;
+  if (v < a) {
+    lob = ra; lo = v;
+    hib = (uint16_t)(ra + 1);
+    hi = ra == 0x7BFF ? 65536.0 : half_to_double(hib);  // past the largest finite: the overflow midpoint
+  } else {
+    hib = ra; hi = std::isinf(v) ? 65536.0 : v;
+    lob = (uint16_t)(ra - 1); lo = half_to_double(lob);
+  }
+  if (a - lo != hi - a) return r;  // not a midpoint: the double already decides
+  const uint16_t pick = e > 0 ? hib : lob;
+  return (uint16_t)(pick | (neg ? 0x8000 : 0));
+}
+
+// One binary16 fused multiply-add: round(a * b + c) with a single rounding.
+// The product of two binary16 values is exact in double; the sum's exact
+// error comes from TwoSum (Knuth).
+uint16_t fma_half(uint16_t a16, uint16_t b16, uint16_t c16) {
+  const double a = half_to_double(a16), b = half_to_double(b16), c = half_to_double(c16);
+  const double p = a * b;
+  const double s = p + c;
+  if (std::isnan(s) || std::isinf(s) || std::isinf(p)) return round_half(s);
+  const double bb = s - p;
+  const double err = (p - (s - bb)) + (c - bb);
+  return round_half_exact(s, err);
+}
+
+// Convolution reductions in the strict mode: the accumulator is a binary16
+// value, updated once per block of 16 consecutive terms of the reduction
+// order (the matrix-core granularity): acc = round(acc + sum of the block),
+// the block sum taken in double.
+struct Acc16 {
+  double acc = 0.0, block = 0.0;
+  int64_t in_block = 0;
+  void add(double t) {
+    block += t;
+    if (++in_block == 16) flush();
+  }
+  void flush() {
+    if (in_block == 0) return;
+    acc = half_to_double(round_half(acc + block));
+    block = 0.0;
+    in_block = 0;
+  }
+};
+
+inline int64_t round8(int64_t v) { return (v + 7) / 8 * 8; }
+
+}  // namespace
+
+extern "C" {
+
+uint16_t oracle_fma16(uint16_t a, uint16_t b, uint16_t c) { return fma_half(a, b, c); }
+
+void oracle_fma16_array(const uint16_t* a, const uint16_t* b, const uint16_t* c, uint16_t* out,
+                        int64_t n) {
+  for (int64_t i = 0; i < n; ++i) out[i] = fma_half(a[i], b[i], c[i]);
+}
+
+// SGD with every operation in binary16: the scalars are the binary16
+// roundings of the float32 weight decay, momentum and -lr, and
+//   d = fma16(wd, w, g);  m' = fma16(mu, m, d);  w' = fma16(-lr, m', w).
+void oracle_sgd_f16(uint16_t* w16, const uint16_t* g16, uint16_t* m16, int64_t n, float lr,
+                    float momentum, float weight_decay) {
+  const uint16_t lam = round_half((double)weight_decay), mu = round_half((double)momentum),
+                 nlr = round_half(-(double)lr);
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < n; ++i) {
+    const uint16_t d = fma_half(lam, w16[i], g16[i]);
+    const uint16_t m1 = fma_half(mu, m16[i], d);
+    const uint16_t w1 = fma_half(nlr, m1, w16[i]);
+    m16[i] = m1;
+    w16[i] = w1;
+  }
+}
+
+// Forward convolution with binary16 accumulation (NHWC / KRSC).  Reduction
+// order: taps (r, s) row-major, channels c fastest over Cp = C rounded up
+// to a multiple of 8 (channels >= C, and taps outside the image, are zero
+// terms that still take their place in the blocks of 16).
+void oracle_conv_fwd_f16acc(const int32_t* shp, const uint16_t* x16, const uint16_t* w16,
+                            uint16_t* y16) {
+  const Conv d(shp);
+  const int64_t Cp = round8(d.C);
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < d.y_size(); ++i) {
+    int64_t n, k, p, q;
+    d.y_coords(i, &n, &k, &p, &q);
+    Acc16 a;
+    for (int64_t r = 0; r < d.R; ++r)
+      for (int64_t s = 0; s < d.S; ++s) {
+        const int64_t h = p * d.sh - d.ph + r, ww = q * d.sw - d.pw + s;
+        const bool in = h >= 0 && h < d.H && ww >= 0 && ww < d.W;
+        for (int64_t c = 0; c < Cp; ++c)
+          a.add(in && c < d.C ? half_to_double(x16[d.xi(n, c, h, ww)]) *
+                                    half_to_double(w16[d.wi(k, c, r, s)])
+                              : 0.0);
+      }
+    a.flush();
+    y16[i] = round_half(a.acc);
+  }
+}
+
+// Data gradient with binary16 accumulation (NHWC / KRSC).  For the output
+// position (h, w) the reduction runs over the taps that reach it, in
+// decreasing r, then decreasing s (those with r = (h + pad_h) mod stride_h,
+// and likewise s, up the filter), and within a tap over the output channels
+// k < Kp (K rounded up to a multiple of 8); a tap whose source position lies
+// outside the P x Q grid contributes zero terms in its place.
+void oracle_conv_dgrad_f16acc(const int32_t* shp, const uint16_t* dy16, const uint16_t* w16,
+                              uint16_t* dx16) {
+  const Conv d(shp);
+  const int64_t Kp = round8(d.K);
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < d.x_size(); ++i) {
+    int64_t n, c, h, ww;
+    d.x_coords(i, &n, &c, &h, &ww);
+    const int64_t r0 = (h + d.ph) % d.sh, s0 = (ww + d.pw) % d.sw;
+    Acc16 a;
+    int64_t rtop = r0;
+    while (rtop + d.sh < d.R) rtop += d.sh;
+    int64_t stop = s0;
+    while (stop + d.sw < d.S) stop += d.sw;
+    if (r0 < d.R && s0 < d.S) {
+      for (int64_t r = rtop; r >= r0; r -= d.sh)
+        for (int64_t s = stop; s >= s0; s -= d.sw) {
+          const int64_t p = (h + d.ph - r) / d.sh, q = (ww + d.pw - s) / d.sw;
+          const bool in = h + d.ph - r >= 0 && ww + d.pw - s >= 0 && p < d.P && q < d.Q;
+          for (int64_t k = 0; k < Kp; ++k)
+            a.add(in && k < d.K ? half_to_double(dy16[d.yi(n, k, p, q)]) *
+                                      half_to_double(w16[d.wi(k, c, r, s)])
+                                : 0.0);
+        }
+    }
+    a.flush();
+    dx16[i] = round_half(a.acc);
+  }
+}
+
+// Weight gradient with binary16 accumulation (NHWC / KRSC): the reduction
+// runs over the output pixels (n, p, q) in order, every pixel taking its
+// place in the blocks of 16 (a tap outside the image gives a zero term).
+void oracle_conv_wgrad_f16acc(const int32_t* shp, const uint16_t* x16, const uint16_t* dy16,
+                              uint16_t* dw16) {
+  const Conv d(shp);
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < d.w_size(); ++i) {
+    int64_t k, c, r, s;
+    d.w_coords(i, &k, &c, &r, &s);
+    Acc16 a;
+    for (int64_t n = 0; n < d.N; ++n)
+      for (int64_t p = 0; p < d.P; ++p)
+        for (int64_t q = 0; q < d.Q; ++q) {
+          const int64_t h = p * d.sh - d.ph + r, ww = q * d.sw - d.pw + s;
+          const bool in = h >= 0 && h < d.H && ww >= 0 && ww < d.W;
+          a.add(in ? half_to_double(dy16[d.yi(n, k, p, q)]) * half_to_double(x16[d.xi(n, c, h, ww)])
+                   : 0.0);
+        }
+    a.flush();
+    dw16[i] = round_half(a.acc);
+  }
+}
+
+}  // extern "C"
