@@ -48,6 +48,8 @@ def parse():
     ap.add_argument("--no-resnet50", action="store_true",
                     help="skip the full ResNet-50 training step at batch 128")
     ap.add_argument("--resnet50-steps", type=int, default=10)
+    ap.add_argument("--no-f16-arith", action="store_true",
+                    help="skip the strict binary16-arithmetic timing leg")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="first run three device-to-device copies of MIB MiB (a plain copy of "
                          "known size, the yardstick for the HBM byte counters)")
@@ -204,6 +206,61 @@ def resnet50_leg(torch, steps: int, warmup: int = 3, batch: int = 128):
                     "call; weight gradients on a second stream; images ~N(0,1), uniform labels"}
 
 
+def f16_arith_leg(torch, reps: int = 10):
+    """Timing of the strict binary16-arithmetic mode next to the default:
+    the SGD update over the ResNet-50 parameter count, and the three passes
+    of the conv4_x 3x3 layer (256 -> 256, 14x14, batch 128) with binary16
+    accumulation (accum = 1) and with float32 accumulators."""
+    import paper_1911_07384_amd as F
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(5)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(1_000_000)
+        a.record()
+        for _ in range(reps):
+            fn()
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / reps
+
+    out = {}
+    n = 25_557_032
+    w = (torch.randn(n, generator=gen, device="cuda") * 0.05).half()
+    g = (torch.randn(n, generator=gen, device="cuda") * 1e-3).half()
+    m = torch.zeros(n, dtype=torch.float16, device="cuda")
+    for name, fn in (("sgd_f32_sequence", F.fp16_sgd_step), ("sgd_binary16", F.fp16_sgd_step_f16)):
+        ms = timed(lambda: fn(w, g, m, lr=0.1, momentum=0.9, weight_decay=1e-4))
+        out[name] = {"ms": round(ms, 5), "gb_per_s": round(10 * n / (ms * 1e-3) / 1e9, 1)}
+    del w, g, m
+    N, C, H, K = 128, 256, 14, 256
+    x = torch.randn((N, H, H, C), generator=gen, device="cuda").half()
+    wt = (torch.randn((K, 3, 3, C), generator=gen, device="cuda") * (2.0 / (9 * C)) ** 0.5).half()
+    dy = (torch.randn((N, H, H, K), generator=gen, device="cuda") * 1e-3).half()
+    y = torch.empty_like(dy)
+    dx = torch.empty_like(x)
+    dw = torch.empty_like(wt)
+    flop = 2.0 * N * H * H * K * C * 9
+    for accum in (0, 1):
+        d = F.conv_desc(N, C, H, H, K, 3, 3, 1, 1, accum=accum)
+        ws = F.workspace(max(F.fp16_conv_workspace_bytes(d, q) for q in (0, 1, 2)))
+        row = {}
+        for pname, fn in (("fwd", lambda: F.fp16_conv_fwd(d, x, wt, y, ws)),
+                          ("dgrad", lambda: F.fp16_conv_dgrad(d, dy, wt, dx, ws)),
+                          ("wgrad", lambda: F.fp16_conv_wgrad(d, x, dy, dw, ws))):
+            ms = timed(fn)
+            row[pname] = {"us": round(ms * 1e3, 2), "tflops": round(flop / (ms * 1e-3) / 1e12, 1)}
+        out["conv4x_3x3_b128_" + ("binary16_acc" if accum else "float32_acc")] = row
+    out["note"] = ("strict binary16 arithmetic (accum = 1 convolutions: the accumulator rounded to "
+                   "binary16 after every 16 terms, weight gradient unsplit; fp16_sgd_step_f16: three "
+                   "binary16 fmas) next to the default float32 accumulators / float32 sequence")
+    return out
+
+
 def cpu_baseline(shape, target_s):
     """The oracle's block step on a batch slice, on this host's cores."""
     import numpy as np
@@ -356,6 +413,8 @@ def main():
                                     for k, v in r.items()} for r in rows]
     if not args.no_resnet50:
         out["resnet50_train_b128"] = resnet50_leg(torch, args.resnet50_steps)
+    if not args.no_f16_arith:
+        out["f16_arith"] = f16_arith_leg(torch)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(shape, args.cpu_seconds)
     print(json.dumps(out), flush=True)

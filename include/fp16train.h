@@ -69,6 +69,15 @@ typedef struct {
   int32_t stride_h, stride_w;
   int32_t pad_h, pad_w;
   int32_t layout; /* fp16_layout */
+  int32_t accum;  /* 0: float32 accumulators (default);
+                     1: binary16 accumulation -- the strict reading of "all arithmetic
+                        in FP16" (Section 5.2), to measure what float32 accumulators buy:
+                        the accumulator is rounded to binary16 after every 16 terms of the
+                        reduction.  Reduction orders: forward (r, s, c) with c over C
+                        rounded up to a multiple of 8; data gradient the taps reaching the
+                        output in decreasing (r, s), then k over K rounded up to 8; weight
+                        gradient the output pixels (n, p, q) in order, unsplit.  NHWC only
+                        (FP16_ERR_UNSUPPORTED otherwise); slower than the default. */
 } fp16_conv_desc;
 
 /* Batch normalisation problem on x [N,C,H,W] (logical). */
@@ -185,6 +194,17 @@ fp16_status fp16_bn_relu_bwd(const fp16_bn_desc* desc, const fp16_t* x, const fp
  * overlap w or m; w and m must not overlap each other.  n = 0 is a no-op. */
 fp16_status fp16_sgd_step(fp16_t* w, const fp16_t* g, fp16_t* m, size_t n, float lr,
                           float momentum, float weight_decay, fp16_stream_t stream);
+
+/* The same update with every operation in binary16 arithmetic (the strict
+ * reading of "all arithmetic in FP16", Section 5.2), for measuring what the
+ * float32 sequence of fp16_sgd_step buys:
+ *   d = fma16(wd, w, g);  m = fma16(mu, m, d);  w = fma16(nlr, m, w)
+ * where fma16 rounds a*b + c once to binary16 (nearest even) and wd, mu and
+ * nlr are the binary16 roundings of the float32 arguments weight_decay,
+ * momentum and -lr.  Same aliasing rules and error behaviour as
+ * fp16_sgd_step. */
+fp16_status fp16_sgd_step_f16(fp16_t* w, const fp16_t* g, fp16_t* m, size_t n, float lr,
+                              float momentum, float weight_decay, fp16_stream_t stream);
 
 /* ---- a convolution fused with the statistics of the BN that follows ---- */
 

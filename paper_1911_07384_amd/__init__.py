@@ -31,7 +31,8 @@ EXPORTS = ["fp16_conv_out_dims", "fp16_conv_workspace_bytes", "fp16_conv_fwd", "
            "fp16_conv_dgrad_add", "fp16_conv_wgrad", "fp16_bn_workspace_bytes", "fp16_bn_relu", "fp16_bn_relu_bwd",
            "fp16_sgd_step", "fp16_pool_out_dims", "fp16_maxpool_fwd", "fp16_maxpool_bwd",
            "fp16_avgpool_fwd", "fp16_avgpool_bwd", "fp16_softmax_ce", "fp16_status_string",
-           "fp16_version", "fp16_conv_bn_workspace_bytes", "fp16_conv_bn_relu_fwd"]
+           "fp16_version", "fp16_conv_bn_workspace_bytes", "fp16_conv_bn_relu_fwd",
+           "fp16_sgd_step_f16"]
 
 
 class Fp16Error(RuntimeError):
@@ -43,7 +44,7 @@ class Fp16Error(RuntimeError):
 class ConvDesc(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int32) for n in
                 ("n", "c", "h", "w", "k", "r", "s", "stride_h", "stride_w", "pad_h", "pad_w",
-                 "layout")]
+                 "layout", "accum")]
 
 
 class BnDesc(ctypes.Structure):
@@ -74,6 +75,7 @@ _SIGS = {
     "fp16_bn_relu": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_bn_relu_bwd": (ctypes.c_int, [_P] * 13 + [_SZ, _P]),
     "fp16_sgd_step": (ctypes.c_int, [_P, _P, _P, _SZ, _F, _F, _F, _P]),
+    "fp16_sgd_step_f16": (ctypes.c_int, [_P, _P, _P, _SZ, _F, _F, _F, _P]),
     "fp16_pool_out_dims": (ctypes.c_int, [_P, _P, _P]),
     "fp16_maxpool_fwd": (ctypes.c_int, [_P, _P, _P, _P, _P]),
     "fp16_maxpool_bwd": (ctypes.c_int, [_P, _P, _P, _P, _P]),
@@ -137,10 +139,11 @@ def _stream(stream):
     return stream.cuda_stream
 
 
-def conv_desc(n, c, h, w, k, r, s, stride=1, pad=0, layout="NHWC") -> ConvDesc:
+def conv_desc(n, c, h, w, k, r, s, stride=1, pad=0, layout="NHWC", accum=0) -> ConvDesc:
+    """accum = 1 selects binary16 accumulation (see fp16_conv_desc.accum)."""
     sh, sw = (stride, stride) if isinstance(stride, int) else stride
     ph, pw = (pad, pad) if isinstance(pad, int) else pad
-    return ConvDesc(n, c, h, w, k, r, s, sh, sw, ph, pw, _LAYOUTS[layout])
+    return ConvDesc(n, c, h, w, k, r, s, sh, sw, ph, pw, _LAYOUTS[layout], int(accum))
 
 
 def bn_desc(n, c, h, w, layout="NHWC", eps=1e-5, post_scale=1.0, relu=True, use_stats=False,
@@ -216,6 +219,15 @@ def fp16_sgd_step(w, g, m, n=None, lr=0.1, momentum=0.9, weight_decay=1e-4, stre
     _check("fp16_sgd_step", lib().fp16_sgd_step(_ptr(w), _ptr(g), _ptr(m), int(n), float(lr),
                                                 float(momentum), float(weight_decay),
                                                 _stream(stream)))
+
+
+def fp16_sgd_step_f16(w, g, m, n=None, lr=0.1, momentum=0.9, weight_decay=1e-4,
+                      stream=None) -> None:
+    if n is None:
+        n = w.numel()
+    _check("fp16_sgd_step_f16", lib().fp16_sgd_step_f16(_ptr(w), _ptr(g), _ptr(m), int(n),
+                                                        float(lr), float(momentum),
+                                                        float(weight_decay), _stream(stream)))
 
 
 def pool_desc(n, c, h, w, r, s, stride=1, pad=0, layout="NHWC") -> PoolDesc:

@@ -25,7 +25,7 @@ int round8(int v) { return (v + 7) / 8 * 8; }
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
 struct ConvDims {
-  int N, C, H, W, K, R, S, sh, sw, ph, pw, P, Q, layout, Cp, Kp;
+  int N, C, H, W, K, R, S, sh, sw, ph, pw, P, Q, layout, Cp, Kp, accum;
   int64_t x_elems, y_elems, w_elems;
 };
 
@@ -39,6 +39,9 @@ fp16_status check_conv(const fp16_conv_desc* d, ConvDims* o) {
       d->pad_w > 64 || d->c > 65535 || d->k > 65535 || d->h > 65535 || d->w > 65535)
     return FP16_ERR_SHAPE;
   if (d->h + 2 * d->pad_h < d->r || d->w + 2 * d->pad_w < d->s) return FP16_ERR_SHAPE;
+  if (d->accum != 0 && d->accum != 1) return FP16_ERR_UNSUPPORTED;
+  if (d->accum == 1 && d->layout != FP16_NHWC) return FP16_ERR_UNSUPPORTED;
+  o->accum = d->accum;
   o->N = d->n; o->C = d->c; o->H = d->h; o->W = d->w; o->K = d->k; o->R = d->r; o->S = d->s;
   o->sh = d->stride_h; o->sw = d->stride_w; o->ph = d->pad_h; o->pw = d->pad_w;
   o->layout = d->layout;
@@ -103,7 +106,7 @@ ConvWs conv_ws(const ConvDims& d, int pass) {
       L.need_y = true;
       L.y = take((size_t)d.N * d.P * d.Q * d.Kp * 2);
     }
-    wgrad_plan(d.Kp, d.Cp, d.R, d.S, (int64_t)d.N * d.P * d.Q, &L.splits, &L.pps);
+    wgrad_plan(d.Kp, d.Cp, d.R, d.S, (int64_t)d.N * d.P * d.Q, d.accum, &L.splits, &L.pps);
     L.part = take((size_t)L.splits * d.Kp * d.R * d.S * d.Cp * 4);
   }
   L.total = off;
@@ -199,6 +202,7 @@ fp16_status fp16_conv_fwd(const fp16_conv_desc* desc, const fp16_t* x, const fp1
   a.stride_h = d.sh; a.stride_w = d.sw;
   a.Co = d.K; a.out = ye; a.OH = d.P; a.OW = d.Q; a.ldo = d.K; a.os_h = 1; a.os_w = 1;
   a.nphase = 1;
+  a.f16acc = d.accum;
   a.ph[0] = IgemmPhase{we, d.R * d.S * d.Cp, d.R, d.S, d.ph, d.pw, d.P, d.Q, 0, 0};
   TRY(launch_igemm(a, st));
   if (d.layout == FP16_NCHW) TRY(launch_nhwc_to_nchw(ye, reinterpret_cast<h16*>(y), d.N, d.K,
@@ -250,6 +254,7 @@ static fp16_status conv_dgrad_impl(const fp16_conv_desc* desc, const fp16_t* dy,
   a.Co = d.C; a.out = dxe; a.OH = d.H; a.OW = d.W; a.ldo = d.C; a.os_h = d.sh; a.os_w = d.sw;
   a.addend = addend ? (d.layout == FP16_NCHW ? dxe : reinterpret_cast<const h16*>(addend)) : nullptr;
   a.nphase = 0;
+  a.f16acc = d.accum;
   int64_t off = 0;
   for (int ph = 0; ph < d.sh; ++ph) {
     for (int pw = 0; pw < d.sw; ++pw) {
@@ -325,7 +330,7 @@ fp16_status fp16_conv_wgrad(const fp16_conv_desc* desc, const fp16_t* x, const f
   a.x = xe; a.dy = dye;
   a.N = d.N; a.H = d.H; a.W = d.W; a.C = d.Cp; a.K = d.Kp; a.R = d.R; a.S = d.S;
   a.sh = d.sh; a.sw = d.sw; a.ph = d.ph; a.pw = d.pw; a.P = d.P; a.Q = d.Q;
-  a.partial = part; a.splits = L.splits; a.pix_per_split = L.pps;
+  a.partial = part; a.splits = L.splits; a.pix_per_split = L.pps; a.f16acc = d.accum;
   TRY(launch_wgrad_partial(a, st));
   TRY(launch_wgrad_reduce(part, L.splits, d.K, d.Kp, d.R, d.S, d.C, d.Cp, d.layout,
                           reinterpret_cast<h16*>(dw), st));
@@ -431,6 +436,19 @@ fp16_status fp16_sgd_step(fp16_t* w, const fp16_t* g, fp16_t* m, size_t n, float
   return hip_status(launch_sgd(reinterpret_cast<h16*>(w), reinterpret_cast<const h16*>(g),
                                reinterpret_cast<h16*>(m), n, lr, momentum, weight_decay,
                                static_cast<hipStream_t>(stream)));
+}
+
+fp16_status fp16_sgd_step_f16(fp16_t* w, const fp16_t* g, fp16_t* m, size_t n, float lr,
+                              float momentum, float weight_decay, fp16_stream_t stream) {
+  if (n == 0) return FP16_OK;
+  if (!w || !g || !m) return FP16_ERR_NULL;
+  if (!aligned16(w) || !aligned16(g) || !aligned16(m)) return FP16_ERR_MISALIGNED;
+  if (n >= ((size_t)1 << 40)) return FP16_ERR_SHAPE;
+  const size_t b = n * 2;
+  if (overlap(w, b, g, b) || overlap(m, b, g, b) || overlap(w, b, m, b)) return FP16_ERR_ALIASING;
+  return hip_status(launch_sgd_f16(reinterpret_cast<h16*>(w), reinterpret_cast<const h16*>(g),
+                                   reinterpret_cast<h16*>(m), n, lr, momentum, weight_decay,
+                                   static_cast<hipStream_t>(stream)));
 }
 
 // ---- pooling --------------------------------------------------------------------
@@ -629,6 +647,7 @@ fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc
   a.Co = d.K; a.out = reinterpret_cast<h16*>(y); a.OH = d.P; a.OW = d.Q; a.ldo = d.K;
   a.os_h = 1; a.os_w = 1;
   a.nphase = 1;
+  a.f16acc = d.accum;
   a.ph[0] = IgemmPhase{we, d.R * d.S * d.Cp, d.R, d.S, d.ph, d.pw, d.P, d.Q, 0, 0};
   const h16* gp = reinterpret_cast<const h16*>(gamma);
   const h16* bp = reinterpret_cast<const h16*>(beta);

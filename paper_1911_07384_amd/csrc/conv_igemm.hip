@@ -18,6 +18,9 @@
 // the same k order (so they give identical bits):
 //   igemm_kernel  -- 4 waves in a 2x2 or 4x1 grid; A and B tiles staged in
 //                    LDS through registers, k-step 64, double buffered.
+//                    Also the strict binary16-accumulation variant (the
+//                    accumulator rounded to binary16 after every MFMA, i.e.
+//                    every 16 terms of the k order).
 //   igemm4_kernel -- 4 waves split M only, so no A element is shared: each
 //                    lane loads its own MFMA operand rows from global memory
 //                    into registers three k-steps ahead, and only the filter
@@ -68,7 +71,7 @@ struct Cfg {
   static constexpr int LDS_BYTES = MAIN_BYTES > STAGE_BYTES ? MAIN_BYTES : STAGE_BYTES;
 };
 
-template <int BM, int BN, int WM, int WN, int BK>
+template <int BM, int BN, int WM, int WN, int BK, bool F16ACC>
 __global__ __launch_bounds__(256) void igemm_kernel(const IgemmArgs a) {
   using K = Cfg<BM, BN, WM, WN, BK>;
   constexpr int LDK = K::LDK, KC = K::KC, RSTEP = K::RSTEP;
@@ -182,7 +185,13 @@ __global__ __launch_bounds__(256) void igemm_kernel(const IgemmArgs a) {
 #pragma unroll
       for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-        for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = mfma32x32x16(af[tm], bf[tn], acc[tm][tn]);
+        for (int tn = 0; tn < TN; ++tn) {
+          acc[tm][tn] = mfma32x32x16(af[tm], bf[tn], acc[tm][tn]);
+          if (F16ACC) {  // binary16 accumulator: one rounding per 16 terms
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[tm][tn][e] = to_f32(to_h16(acc[tm][tn][e]));
+          }
+        }
     }
   };
 
@@ -891,7 +900,7 @@ hipError_t launch_cfg4(const IgemmArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN, int BK>
+template <int BM, int BN, int WM, int WN, int BK, bool F16ACC = false>
 hipError_t launch_cfg(const IgemmArgs& a, hipStream_t st) {
   int maxM = 0;
   for (int p = 0; p < a.nphase; ++p) {
@@ -900,7 +909,7 @@ hipError_t launch_cfg(const IgemmArgs& a, hipStream_t st) {
   }
   if (maxM == 0 || a.nphase == 0) return hipSuccess;
   dim3 grid(ceil_div(maxM, BM), ceil_div(a.Co, BN), a.nphase);
-  hipLaunchKernelGGL((igemm_kernel<BM, BN, WM, WN, BK>), grid, dim3(256), 0, st, a);
+  hipLaunchKernelGGL((igemm_kernel<BM, BN, WM, WN, BK, F16ACC>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
@@ -916,6 +925,7 @@ enum class IgemmKind { kLds, kDirect, kDma };
 // the register-direct kernel for short reductions or small M, else the
 // LDS-staged one.  All three give identical bits.
 IgemmKind igemm_kind(const IgemmArgs& a) {
+  if (a.f16acc) return IgemmKind::kLds;
   int maxM = 0, maxK = 0, maxT = 0;
   int64_t maxF = 0;
   for (int p = 0; p < a.nphase; ++p) {
@@ -940,6 +950,9 @@ IgemmKind igemm_kind(const IgemmArgs& a) {
 bool igemm_takes_stats(const IgemmArgs& a) { return igemm_kind(a) != IgemmKind::kLds; }
 
 hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st) {
+  if (a.f16acc)
+    return a.Co <= 64 ? launch_cfg<128, 64, 4, 1, 64, true>(a, st)
+                      : launch_cfg<128, 128, 2, 2, 64, true>(a, st);
   switch (igemm_kind(a)) {
     case IgemmKind::kDma: {
       // two stages (two workgroups per CU) unless the grid fits the 256 CUs

@@ -14,6 +14,9 @@ namespace fp16k {
 // ---- SGD (sgd.hip) --------------------------------------------------------
 hipError_t launch_sgd(h16* w, const h16* g, h16* m, size_t n, float lr, float momentum,
                       float weight_decay, hipStream_t st);
+// The same update with every operation a binary16 fma (binary16 scalars).
+hipError_t launch_sgd_f16(h16* w, const h16* g, h16* m, size_t n, float lr, float momentum,
+                          float weight_decay, hipStream_t st);
 
 // ---- layout helpers (layout.hip) -----------------------------------------
 // [N][C][HW] -> [N][HW][Cp] with channels c >= C zero-filled (Cp >= C).
@@ -55,6 +58,9 @@ struct IgemmArgs {
   // over its rows, at stat[(b * 3 + q) * Co + c], q = 0, 1, 2.
   float* stat;
   int stat_nb;
+  // 1: binary16 accumulation, the accumulator rounded to binary16 after every
+  // 16 terms of the k order (LDS-staged kernel only; no statistics)
+  int f16acc;
 };
 
 hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st);
@@ -98,13 +104,16 @@ struct WgradArgs {
   float* partial; // [splits][K][R*S*C]
   int splits;
   int pix_per_split;
+  int f16acc;     // 1: binary16 accumulation per 16 pixels (one split, register-transpose kernel)
 };
 hipError_t launch_wgrad_partial(const WgradArgs& a, hipStream_t st);
 // dw[k][r][s][c] = rne16(sum_split partial[split][k][(r*S+s)*Cp + c]) for k < K, c < C,
 // with Kp rows per split, written as KRSC (layout 0) or KCRS (layout 1).
 hipError_t launch_wgrad_reduce(const float* partial, int splits, int K, int Kp, int R, int S,
                                int C, int Cp, int layout, h16* dw, hipStream_t st);
-void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int* splits, int* pix_per_split);
+// Split-K plan of the weight gradient; with f16acc one split over all pixels.
+void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int f16acc, int* splits,
+                int* pix_per_split);
 
 // ---- batch normalisation (bn.hip) ----------------------------------------
 struct BnArgs {

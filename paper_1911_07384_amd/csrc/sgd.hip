@@ -7,6 +7,7 @@
 //   w' = rne16(fma(-lr, m', w))
 // Bandwidth-bound: 10 bytes per element (read w, g, m; write w, m).  Each
 // thread moves 16-byte vectors; the grid strides over the arrays.
+// launch_sgd_f16 runs the same update with every operation in binary16.
 
 #include "kernels.hpp"
 
@@ -22,9 +23,28 @@ __device__ __forceinline__ void sgd_one(h16& w, h16 g, h16& m, float lr, float m
   w = w1;
 }
 
+// Strict binary16 arithmetic: three binary16 fused multiply-adds (one
+// rounding each, v_fma_f16) with binary16 scalars.
+__device__ __forceinline__ void sgd_one_f16(h16& w, h16 g, h16& m, h16 nlr, h16 mu, h16 wd) {
+  const h16 d = __builtin_fmaf16(wd, w, g);
+  const h16 m1 = __builtin_fmaf16(mu, m, d);
+  const h16 w1 = __builtin_fmaf16(nlr, m1, w);
+  m = m1;
+  w = w1;
+}
+
+struct SgdF32 {
+  float lr, mu, wd;
+  __device__ void operator()(h16& w, h16 g, h16& m) const { sgd_one(w, g, m, lr, mu, wd); }
+};
+struct SgdF16 {
+  h16 nlr, mu, wd;
+  __device__ void operator()(h16& w, h16 g, h16& m) const { sgd_one_f16(w, g, m, nlr, mu, wd); }
+};
+
+template <class Op>
 __global__ __launch_bounds__(256) void sgd_kernel(h16* __restrict__ w, const h16* __restrict__ g,
-                                                  h16* __restrict__ m, size_t n, float lr,
-                                                  float mu, float wd) {
+                                                  h16* __restrict__ m, size_t n, Op op) {
   const size_t nvec = n / 8;
   const size_t stride = (size_t)gridDim.x * blockDim.x;
   size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -35,7 +55,7 @@ __global__ __launch_bounds__(256) void sgd_kernel(h16* __restrict__ w, const h16
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       h16 we = wv.h[e], me = mv.h[e];
-      sgd_one(we, gv.h[e], me, lr, mu, wd);
+      op(we, gv.h[e], me);
       wv.h[e] = we;
       mv.h[e] = me;
     }
@@ -47,7 +67,7 @@ __global__ __launch_bounds__(256) void sgd_kernel(h16* __restrict__ w, const h16
   const size_t j = nvec * 8 + t;
   if (j < n) {
     h16 wv = w[j], mv = m[j];
-    sgd_one(wv, g[j], mv, lr, mu, wd);
+    op(wv, g[j], mv);
     m[j] = mv;
     w[j] = wv;
   }
@@ -55,17 +75,29 @@ __global__ __launch_bounds__(256) void sgd_kernel(h16* __restrict__ w, const h16
 
 }  // namespace
 
-hipError_t launch_sgd(h16* w, const h16* g, h16* m, size_t n, float lr, float momentum,
-                      float weight_decay, hipStream_t st) {
+namespace {
+template <class Op>
+hipError_t launch_sgd_op(h16* w, const h16* g, h16* m, size_t n, Op op, hipStream_t st) {
   if (n == 0) return hipSuccess;
   const size_t nvec = n / 8;
   size_t blocks = (nvec + 255) / 256;
   if (blocks < 1) blocks = 1;
   // one vector per thread up to a grid of 64k blocks, grid-stride beyond
   if (blocks > 65536) blocks = 65536;
-  hipLaunchKernelGGL(sgd_kernel, dim3((unsigned)blocks), dim3(256), 0, st, w, g, m, n, lr,
-                     momentum, weight_decay);
+  hipLaunchKernelGGL(sgd_kernel<Op>, dim3((unsigned)blocks), dim3(256), 0, st, w, g, m, n, op);
   return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_sgd(h16* w, const h16* g, h16* m, size_t n, float lr, float momentum,
+                      float weight_decay, hipStream_t st) {
+  return launch_sgd_op(w, g, m, n, SgdF32{lr, momentum, weight_decay}, st);
+}
+
+hipError_t launch_sgd_f16(h16* w, const h16* g, h16* m, size_t n, float lr, float momentum,
+                          float weight_decay, hipStream_t st) {
+  // binary16 roundings (nearest even) of the float32 scalars
+  return launch_sgd_op(w, g, m, n, SgdF16{(h16)(-lr), (h16)momentum, (h16)weight_decay}, st);
 }
 
 }  // namespace fp16k

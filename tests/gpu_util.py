@@ -50,9 +50,9 @@ class ConvCase:
     dy ~ N(0, dy_std^2)) and the three passes on the GPU."""
 
     def __init__(self, n, c, h, w, k, r, s, stride=1, pad=0, layout="NHWC", seed=0,
-                 dy_std=1e-2, x=None, wt=None, dy=None):
+                 dy_std=1e-2, x=None, wt=None, dy=None, accum=0):
         self.shp = oracle.conv_shape(n, c, h, w, k, r, s, stride, pad, layout)
-        self.desc = F.conv_desc(n, c, h, w, k, r, s, stride, pad, layout)
+        self.desc = F.conv_desc(n, c, h, w, k, r, s, stride, pad, layout, accum=accum)
         self.P, self.Q = F.fp16_conv_out_dims(self.desc)
         assert (self.P, self.Q) == oracle.conv_out_dims(self.shp)
         if layout == "NHWC":

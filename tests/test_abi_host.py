@@ -141,13 +141,36 @@ def test_bn_validation():
     assert lib.fp16_bn_relu_bwd(ctypes.byref(d), *bw_alias) == ALIASING
 
 
-def test_sgd_validation():
-    lib = F.lib()
-    assert lib.fp16_sgd_step(None, None, None, 0, 0.1, 0.9, 1e-4, None) == OK  # n = 0: no-op
-    assert lib.fp16_sgd_step(None, B, Cc, 8, 0.1, 0.9, 1e-4, None) == NULL
-    assert lib.fp16_sgd_step(A + 2, B, Cc, 8, 0.1, 0.9, 1e-4, None) == MISALIGNED
-    assert lib.fp16_sgd_step(A, A + 16, Cc, 64, 0.1, 0.9, 1e-4, None) == ALIASING
-    assert lib.fp16_sgd_step(A, B, A + 64, 64, 0.1, 0.9, 1e-4, None) == ALIASING
+@pytest.mark.parametrize("fn", ["fp16_sgd_step", "fp16_sgd_step_f16"])
+def test_sgd_validation(fn):
+    f = getattr(F.lib(), fn)
+    assert f(None, None, None, 0, 0.1, 0.9, 1e-4, None) == OK  # n = 0: no-op
+    assert f(None, B, Cc, 8, 0.1, 0.9, 1e-4, None) == NULL
+    assert f(A + 2, B, Cc, 8, 0.1, 0.9, 1e-4, None) == MISALIGNED
+    assert f(A, A + 16, Cc, 64, 0.1, 0.9, 1e-4, None) == ALIASING
+    assert f(A, B, A + 64, 64, 0.1, 0.9, 1e-4, None) == ALIASING
+
+
+@pytest.mark.parametrize("fn", ["fp16_conv_fwd", "fp16_conv_dgrad", "fp16_conv_wgrad"])
+def test_conv_accum_validation(fn):
+    # binary16 accumulation: only 0 / 1, and only NHWC
+    d = _conv()
+    d.accum = 2
+    assert _call(fn, d, A, B, Cc) == 7
+    d = _conv(layout="NCHW")
+    d.accum = 1
+    assert _call(fn, d, A, B, Cc) == 7
+    assert F.fp16_conv_workspace_bytes(d, F.PASS_FWD) == 0  # invalid descriptor
+
+
+def test_conv_accum_wgrad_runs_one_split():
+    # the binary16 accumulator runs over all pixels: the partial workspace
+    # holds exactly one float32 tile (K x R*S*C), 256-aligned
+    d = _conv()
+    d.accum = 1
+    need = F.fp16_conv_workspace_bytes(d, F.PASS_WGRAD)
+    assert need == (64 * 9 * 64 * 4 + 255) // 256 * 256
+    assert need < F.fp16_conv_workspace_bytes(_conv(), F.PASS_WGRAD)
 
 
 # ---- pooling and loss: every call below is invalid, nothing is launched ---------
