@@ -424,35 +424,41 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
   }
   const bool has_y = y != nullptr, has_r = res != nullptr && !has_y && relu;
   const bool load_r = has_r || SWAP;
-  // two rows in flight per thread; the sums still run row by row
-  for (int64_t row = row0 + t / CV; row < row1; row += 2 * RB) {
-    V8 xv[2], dv[2], yv[2], rv[2];
+  // one row per step, the next row loaded before this one is summed
+  // (software pipelined, two rows in flight); the sums run row by row
+  struct Row {
+    V8 x, d, y, r;
+  };
+  auto load_row = [&](Row& b, int64_t row) {
+    const int64_t off = row * g.C + j * 8;
+    b.x = load16(x + off);
+    b.d = load16(dy + off);
+    if (relu && has_y) b.y = load16(y + off);
+    if (load_r) b.r = load16(res + off);
+  };
+  auto sum_row = [&](const Row& b) {
 #pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      if (row + u * RB < row1) {
-        const int64_t off = (row + u * RB) * g.C + j * 8;
-        xv[u] = load16(x + off);
-        dv[u] = load16(dy + off);
-        if (relu && has_y) yv[u] = load16(y + off);
-        if (load_r) rv[u] = load16(res + off);
-      }
+    for (int e = 0; e < 8; ++e) {
+      const float xf = to_f32(b.x.h[e]);
+      const float rf = load_r ? to_f32(b.r.h[e]) : 0.0f;
+      const bool m = relu_mask(relu != 0, has_y, has_y ? b.y.h[e] : (h16)0.0f, xf, k[e], has_r, rf,
+                               SWAP);
+      const float gg = m ? s * to_f32(b.d.h[e]) : 0.0f;
+      const float xh = (xf - k[e].mean) * rstd[e];
+      sums[0][e] += gg;
+      sums[1][e] = __builtin_fmaf(gg, xh, sums[1][e]);
+      if (SWAP) sums[NS - 1][e] = __builtin_fmaf(gg, rf, sums[NS - 1][e]);
     }
-#pragma unroll
-    for (int u = 0; u < 2; ++u) {
-      if (row + u * RB >= row1) break;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float xf = to_f32(xv[u].h[e]);
-        const float rf = load_r ? to_f32(rv[u].h[e]) : 0.0f;
-        const bool m = relu_mask(relu != 0, has_y, has_y ? yv[u].h[e] : (h16)0.0f, xf, k[e],
-                                 has_r, rf, SWAP);
-        const float gg = m ? s * to_f32(dv[u].h[e]) : 0.0f;
-        const float xh = (xf - k[e].mean) * rstd[e];
-        sums[0][e] += gg;
-        sums[1][e] = __builtin_fmaf(gg, xh, sums[1][e]);
-        if (SWAP) sums[NS - 1][e] = __builtin_fmaf(gg, rf, sums[NS - 1][e]);
-      }
-    }
+  };
+  Row ra, rb;
+  int64_t row = row0 + t / CV;
+  if (row < row1) load_row(ra, row);
+  for (; row < row1; row += 2 * RB) {
+    if (row + RB < row1) load_row(rb, row + RB);
+    sum_row(ra);
+    if (row + RB >= row1) break;
+    if (row + 2 * RB < row1) load_row(ra, row + 2 * RB);
+    sum_row(rb);
   }
   block_reduce_vec<NS>(sums, red, CV, RB, ws, (int)gridDim.x);
 }
