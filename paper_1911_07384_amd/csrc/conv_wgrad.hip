@@ -175,7 +175,9 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
 }
 
 // ---- DMA-staged variant: no register transposes ------------------------------
-// For channel counts that are multiples of 64.  Each stage covers 64 pixels:
+// For K a multiple of 64 and C a multiple of 8 (when C is not a multiple of
+// 64 -- the padded 3-channel stem -- each lane's 8-channel chunk carries its
+// own filter tap).  Each stage covers 64 pixels:
 // the dy rows (BM channels) and the x patch rows (BN filter columns, 64 per
 // tap and channel block) are DMA'd pixel-major straight into LDS, in 8 KB
 // sub-tiles of 64 pixel rows x 128 bytes (16-byte chunks XOR-swizzled by
@@ -213,10 +215,11 @@ struct WCfg7 {
   static constexpr int TM = WTM / 32, TN = WTN / 32;
 };
 
-template <int BM, int BN, int WM, int WN, int S>
+template <int BM, int BN, int WM, int WN, int S, bool CGEN = false>
 __global__ __launch_bounds__(256) void wgrad7_kernel(const WgradArgs a) {
   using K = WCfg7<BM, BN, WM, WN, S>;
-  constexpr int SA = K::SA, IW = K::IW, TM = K::TM, TN = K::TN, WTM = K::WTM, WTN = K::WTN;
+  constexpr int SA = K::SA, SB = K::SB, IW = K::IW, TM = K::TM, TN = K::TN, WTM = K::WTM,
+                WTN = K::WTN;
   static_assert(WM * WN == 4 && TM >= 1 && TN >= 1 && S >= 2, "tile shape");
   static_assert(IW * (S - 1) < 64, "vmcnt range");
   __shared__ __attribute__((aligned(1024))) char lds[S * K::STAGE];
@@ -257,6 +260,22 @@ __global__ __launch_bounds__(256) void wgrad7_kernel(const WgradArgs a) {
   int lc[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) lc[h] = (lane & 7) ^ (((prow[h] >> 1) & 3) << 1);
+  // CGEN (C a multiple of 8 but not of 64): a 64-column block of the x patch
+  // spans several filter taps, so each lane's 8-channel chunk has a tap of its
+  // own; precomputed here (tap row, tap column, channel offset; -1 past Nw)
+  int gr[2][CGEN ? SB : 1], gt[2][CGEN ? SB : 1], gc[2][CGEN ? SB : 1];
+  if (CGEN) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int b = 0; b < SB; ++b) {
+        const int col = n0 + b * 64 + lc[h] * 8;
+        const int tap = col / a.C;
+        gc[h][b] = col < Nw ? col - tap * a.C : -1;
+        gr[h][b] = tap / a.S;
+        gt[h][b] = tap - gr[h][b] * a.S;
+      }
+  }
 
   int64_t pstage = pbeg;  // first pixel of the next stage to issue
   auto issue = [&](char* buf) {
@@ -276,6 +295,14 @@ __global__ __launch_bounds__(256) void wgrad7_kernel(const WgradArgs a) {
         const int m = m0 + sub * 64;
         const uint32_t off = (uint32_t)((pix * a.K + m + lc[h] * 8) * 2);
         wdma16(rs_dy, dst, (pv && m < a.K) ? off : OOB);
+      } else if (CGEN) {
+        const int b = sub - SA;
+        const int ih = pp[h] * a.sh - a.ph + gr[h][b], iw = qq[h] * a.sw - a.pw + gt[h][b];
+        const bool v = pv && gc[h][b] >= 0 && (unsigned)ih < (unsigned)a.H &&
+                       (unsigned)iw < (unsigned)a.W;
+        const uint32_t off =
+            (uint32_t)(((((int64_t)img[h] * a.H + ih) * a.W + iw) * a.C + gc[h][b]) * 2);
+        wdma16(rs_x, dst, v ? off : OOB);
       } else {
         const int cb = n0 + (sub - SA) * 64;
         const int tap = cb / a.C;
@@ -489,7 +516,7 @@ inline WCfg wgrad_cfg(int K, int Nw) {
   return {64, 64};
 }
 // The DMA-staged kernel (channel counts multiples of 64) and its tiles.
-inline bool wgrad_dma(int K, int C) { return K % 64 == 0 && C % 64 == 0; }
+inline bool wgrad_dma(int K, int C) { return K % 64 == 0 && C % 8 == 0; }
 // (measured on the ResNet-50 shapes at batch 128: narrower tiles at higher
 // occupancy beat 128 x 128 once K >= 128)
 inline WCfg wgrad7_cfg(int K, int Nw) {
@@ -547,10 +574,20 @@ hipError_t launch_wgrad_partial(const WgradArgs& a, hipStream_t st) {
       hipLaunchKernelGGL((wgrad_kernel<64, 64, 2, 2, true>), g2, dim3(256), 0, st, a);
     return hipGetLastError();
   }
+  if (wgrad_dma(a.K, a.C) && a.C % 64 != 0) {
+    // channel counts that are multiples of 8 only (the 3-channel stem, padded)
+    if (cfg.BM == 128)
+      hipLaunchKernelGGL((wgrad7_kernel<128, 64, 2, 2, 2, true>), grid, dim3(256), 0, st, a);
+    else if (cfg.BN == 256)
+      hipLaunchKernelGGL((wgrad7_kernel<64, 256, 1, 4, 2, true>), grid, dim3(256), 0, st, a);
+    else if (cfg.BN == 128)
+      hipLaunchKernelGGL((wgrad7_kernel<64, 128, 2, 2, 2, true>), grid, dim3(256), 0, st, a);
+    else
+      hipLaunchKernelGGL((wgrad7_kernel<64, 64, 2, 2, 2, true>), grid, dim3(256), 0, st, a);
+    return hipGetLastError();
+  }
   if (wgrad_dma(a.K, a.C)) {
-    if (cfg.BM == 128 && cfg.BN == 128)
-      hipLaunchKernelGGL((wgrad7_kernel<128, 128, 2, 2, 2>), grid, dim3(256), 0, st, a);
-    else if (cfg.BM == 128)
+    if (cfg.BM == 128)
       hipLaunchKernelGGL((wgrad7_kernel<128, 64, 2, 2, 2>), grid, dim3(256), 0, st, a);
     else if (cfg.BN == 256)
       hipLaunchKernelGGL((wgrad7_kernel<64, 256, 1, 4, 2>), grid, dim3(256), 0, st, a);
