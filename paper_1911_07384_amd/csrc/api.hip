@@ -589,9 +589,10 @@ static fp16_status check_conv_bn(const fp16_conv_desc* cd, const fp16_bn_desc* b
   return FP16_OK;
 }
 
-// Tile records ([nb][3][K] float32, 128 rows each) after the convolution's
-// own workspace; when the convolution does not run on the register-direct
-// kernel, the BN's own workspace takes that place instead.
+// Tile records ([nb][3][K] float32, 128 rows each) and the statistics'
+// per-slice sums after the convolution's own workspace; when the kernel picked
+// for the convolution does not take the statistics, the BN's own workspace
+// takes that place instead.
 static size_t conv_bn_band_off(const ConvDims& d) { return conv_ws(d, FP16_PASS_FWD).total; }
 static int conv_bn_nb(const ConvDims& d) { return (int)(((int64_t)d.N * d.P * d.Q + 127) / 128); }
 
@@ -599,7 +600,8 @@ size_t fp16_conv_bn_workspace_bytes(const fp16_conv_desc* conv, const fp16_bn_de
   ConvDims d;
   BnArgs b;
   if (check_conv_bn(conv, bn, &d, &b) != FP16_OK) return 0;
-  const size_t rec = align256((size_t)3 * d.K * conv_bn_nb(d) * sizeof(float));
+  const size_t rec = align256((size_t)3 * d.K * conv_bn_nb(d) * sizeof(float)) +
+                     bn_band_ws_bytes(d.K, conv_bn_nb(d));
   const size_t bnw = bn_ws_bytes(b);
   return conv_bn_band_off(d) + (rec > bnw ? rec : bnw);
 }
@@ -662,7 +664,10 @@ fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc
   a.stat = part;
   a.stat_nb = conv_bn_nb(d);
   TRY(launch_igemm(a, st));
-  return hip_status(launch_bn_fwd_bands(b, part, a.stat_nb, reinterpret_cast<const h16*>(y),
+  void* band_ws = reinterpret_cast<char*>(part) +
+                  align256((size_t)3 * d.K * a.stat_nb * sizeof(float));
+  return hip_status(launch_bn_fwd_bands(b, part, a.stat_nb, band_ws,
+                                        reinterpret_cast<const h16*>(y),
                                         reinterpret_cast<const h16*>(gamma),
                                         reinterpret_cast<const h16*>(beta),
                                         reinterpret_cast<const h16*>(residual),

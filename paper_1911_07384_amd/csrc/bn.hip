@@ -249,29 +249,34 @@ __global__ __launch_bounds__(kT) void bn_fwd_reduce_gen(const h16* __restrict__ 
 }
 
 // Sum of the G block partials of channel c in float64: each lane of one wave
-// takes every 64th partial, then a butterfly over the wave (a fixed order, so
-// the total does not depend on timing).
+// takes every 64th partial, in index order, then a butterfly over the wave (a
+// fixed order, so the total does not depend on timing).  The partials of a
+// lane are loaded 16 at a time before any is added, so one memory round trip
+// covers up to 1,024 partials.
 __device__ __forceinline__ void channel_sums(const float* ws1, const float* ws2, int c, int G,
                                              double& S1, double& S2) {
   const int t = threadIdx.x;
   double a = 0.0, b = 0.0;
   const float* p1 = ws1 + (int64_t)c * G;
   const float* p2 = ws2 + (int64_t)c * G;
-  for (int j = t; j < G; j += 256) {
-    // four partials per lane in flight, added in index order
-    float u1[4], u2[4];
+  constexpr int U = 16;
+  for (int j = t; j < G; j += 64 * U) {
+    float u1[U], u2[U];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int i = j + 64 * u;
-      u1[u] = i < G ? p1[i] : 0.0f;
-      u2[u] = i < G ? p2[i] : 0.0f;
+    for (int u = 0; u < U; ++u) {
+      // unconditional loads from a clamped index (a load under a lane
+      // condition would be waited for before the next one is issued)
+      const int i = j + 64 * u < G ? j + 64 * u : G - 1;
+      u1[u] = p1[i];
+      u2[u] = p2[i];
     }
+    // adding zero for the lanes past G keeps every load unconditional (a
+    // load used only under a condition would be moved behind it)
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      if (j + 64 * u < G) {
-        a += (double)u1[u];
-        b += (double)u2[u];
-      }
+    for (int u = 0; u < U; ++u) {
+      const bool ok = j + 64 * u < G;
+      a += ok ? (double)u1[u] : 0.0;
+      b += ok ? (double)u2[u] : 0.0;
     }
   }
 #pragma unroll
@@ -283,8 +288,6 @@ __device__ __forceinline__ void channel_sums(const float* ws1, const float* ws2,
   S2 = b;
 }
 
-// mean = K + S1/M, var = S2/M - (S1/M)^2 (float64), rstd = 1/sqrt(var + eps).
-// One 64-thread block per channel.
 __global__ __launch_bounds__(64) void bn_fwd_finalize(const h16* __restrict__ x, Geo g, int G,
                                                       const float* ws, float eps, float* stats) {
   const int c = blockIdx.x;
@@ -303,24 +306,140 @@ __global__ __launch_bounds__(64) void bn_fwd_finalize(const h16* __restrict__ x,
 // per 128-row tile b and channel c a shift K_b (its first value) and the sums
 // of (y - K_b) and (y - K_b)^2 over its n_b rows).  About K_0:
 //   S1 = sum_b s1_b + n_b d_b,  S2 = sum_b s2_b + 2 d_b s1_b + n_b d_b^2,
-// d_b = K_b - K_0, in float64 (each lane takes every 64th record in order,
-// then a butterfly: a fixed order); then as bn_fwd_finalize.  One 64-thread
-// block per channel.
-__global__ __launch_bounds__(64) void bn_band_finalize(const float* __restrict__ part, int nb,
-                                                       Geo g, float eps, float* stats) {
+// d_b = K_b - K_0, in float64.  Up to kBandOne records: bn_band_finalize, one
+// 256-thread block per channel; thread t takes records t, t + 256, ... in
+// order (the loads of four of them in flight), then the block's fixed-order
+// reduction.  More records, in two kernels:
+//  - bn_band_slices: block (channel group of 64, slice s) sums the records
+//    [s*kBandRps, (s+1)*kBandRps) of its 64 channels (one lane per channel, so
+//    every record row is read with 256-byte coalesced loads; wave w takes every
+//    4th record from the w-th, all of them in flight; the waves then in order)
+//    and writes the slice sums channel-major, [2][C][nslice] float64;
+//  - bn_band_combine: one wave per channel adds its slices (lane t takes every
+//    64th in order, then a butterfly) and writes mean and 1/sqrt(var + eps).
+// Every sum has a fixed order, so the statistics do not depend on timing.
+constexpr int kBandOne = 2048;
+constexpr int kBandRps = 32;  // records per slice: 8 per wave
+
+// One record's terms; a record past the last adds exact zeros, so that its
+// (clamped, in-bounds) loads stay unconditional and in flight together.
+__device__ __forceinline__ void band_term_if(bool ok, int64_t rows, float k, double K0, float s1,
+                                             float s2, double& a, double& b) {
+  const double n = ok ? (double)(rows < 128 ? rows : 128) : 0.0;
+  const double d = ok ? (double)k - K0 : 0.0;
+  const double t1 = ok ? (double)s1 : 0.0, t2 = ok ? (double)s2 : 0.0;
+  a += t1 + n * d;
+  b += t2 + 2.0 * d * t1 + n * d * d;
+}
+
+__device__ __forceinline__ void band_stats(double a, double b, double K0, Geo g, float eps,
+                                           int c, float* stats) {
+  const double md = a / (double)g.M;
+  double var = b / (double)g.M - md * md;
+  if (var < 0.0) var = 0.0;
+  stats[c] = (float)(K0 + md);
+  stats[g.C + c] = (float)(1.0 / __builtin_sqrt(var + (double)eps));
+}
+
+__global__ __launch_bounds__(256) void bn_band_finalize(const float* __restrict__ part, int nb,
+                                                        Geo g, float eps, float* stats) {
+  __shared__ double red[2][4];
   const int c = blockIdx.x;
   const int t = threadIdx.x;
   const int64_t C3 = (int64_t)3 * g.C;
   const double K0 = (double)part[c];
   double a = 0.0, b = 0.0;
-  for (int j = t; j < nb; j += 64) {
-    const float* rec = part + j * C3 + c;
-    const int64_t rows = g.M - (int64_t)j * 128;
-    const double n = (double)(rows < 128 ? rows : 128);
-    const double d = (double)rec[0] - K0;
-    const double s1 = (double)rec[g.C];
-    a += s1 + n * d;
-    b += (double)rec[2 * g.C] + 2.0 * d * s1 + n * d * d;
+  constexpr int U = 4;
+  for (int j0 = t; j0 < nb; j0 += 256 * U) {
+    float k[U], s1[U], s2[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + 256 * u;
+      const float* rec = part + (int64_t)(j < nb ? j : nb - 1) * C3 + c;
+      k[u] = rec[0];
+      s1[u] = rec[g.C];
+      s2[u] = rec[2 * g.C];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + 256 * u;
+      band_term_if(j < nb, g.M - (int64_t)j * 128, k[u], K0, s1[u], s2[u], a, b);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    a += __shfl_xor(a, off, 64);
+    b += __shfl_xor(b, off, 64);
+  }
+  if ((t & 63) == 0) {
+    red[0][t >> 6] = a;
+    red[1][t >> 6] = b;
+  }
+  __syncthreads();
+  if (t != 0) return;
+  band_stats(((red[0][0] + red[0][1]) + red[0][2]) + red[0][3],
+             ((red[1][0] + red[1][1]) + red[1][2]) + red[1][3], K0, g, eps, c, stats);
+}
+
+__global__ __launch_bounds__(256) void bn_band_slices(const float* __restrict__ part, int nb,
+                                                      Geo g, double* __restrict__ sl, int ns) {
+  __shared__ double red[2][4][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int c = blockIdx.x * 64 + lane;
+  const int s = blockIdx.y;
+  const int64_t C3 = (int64_t)3 * g.C;
+  double a = 0.0, b = 0.0;
+  if (c < g.C) {
+    const double K0 = (double)part[c];
+    constexpr int U = kBandRps / 4;
+    float k[U], s1[U], s2[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = s * kBandRps + w + 4 * u;
+      const float* rec = part + (int64_t)(j < nb ? j : nb - 1) * C3 + c;
+      k[u] = rec[0];
+      s1[u] = rec[g.C];
+      s2[u] = rec[2 * g.C];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = s * kBandRps + w + 4 * u;
+      band_term_if(j < nb, g.M - (int64_t)j * 128, k[u], K0, s1[u], s2[u], a, b);
+    }
+  }
+  red[0][w][lane] = a;
+  red[1][w][lane] = b;
+  __syncthreads();
+  if (w != 0 || c >= g.C) return;
+  const double A = ((red[0][0][lane] + red[0][1][lane]) + red[0][2][lane]) + red[0][3][lane];
+  const double B = ((red[1][0][lane] + red[1][1][lane]) + red[1][2][lane]) + red[1][3][lane];
+  sl[(int64_t)c * ns + s] = A;
+  sl[((int64_t)g.C + c) * ns + s] = B;
+}
+
+__global__ __launch_bounds__(64) void bn_band_combine(const float* __restrict__ part,
+                                                      const double* __restrict__ sl, int ns,
+                                                      Geo g, float eps, float* stats) {
+  const int c = blockIdx.x;
+  const int t = threadIdx.x;
+  const double* pa = sl + (int64_t)c * ns;
+  const double* pb = sl + ((int64_t)g.C + c) * ns;
+  constexpr int U = 8;
+  double a = 0.0, b = 0.0;
+  for (int j = t; j < ns; j += 64 * U) {
+    double ua[U], ub[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = j + 64 * u < ns ? j + 64 * u : ns - 1;
+      ua[u] = pa[i];
+      ub[u] = pb[i];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool ok = j + 64 * u < ns;
+      a += ok ? ua[u] : 0.0;
+      b += ok ? ub[u] : 0.0;
+    }
   }
 #pragma unroll
   for (int off = 32; off > 0; off >>= 1) {
@@ -328,11 +447,7 @@ __global__ __launch_bounds__(64) void bn_band_finalize(const float* __restrict__
     b += __shfl_xor(b, off, 64);
   }
   if (t != 0) return;
-  const double md = a / (double)g.M;
-  double var = b / (double)g.M - md * md;
-  if (var < 0.0) var = 0.0;
-  stats[c] = (float)(K0 + md);
-  stats[g.C + c] = (float)(1.0 / __builtin_sqrt(var + (double)eps));
+  band_stats(a, b, (double)part[c], g, eps, c, stats);
 }
 
 // ---- forward apply -------------------------------------------------------------
@@ -669,12 +784,26 @@ hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const 
   return hipGetLastError();
 }
 
-hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, const h16* x,
-                               const h16* gamma, const h16* beta, const h16* res, h16* y,
-                               float* stats, hipStream_t st) {
+size_t bn_band_ws_bytes(int C, int nb) {
+  const int64_t ns = ((int64_t)nb + kBandRps - 1) / kBandRps;
+  return align256((size_t)2 * C * ns * sizeof(double));
+}
+
+hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, void* band_ws,
+                               const h16* x, const h16* gamma, const h16* beta, const h16* res,
+                               h16* y, float* stats, hipStream_t st) {
   const Plan p = make_plan(a);
   const Geo g = make_geo(a);
-  hipLaunchKernelGGL(bn_band_finalize, dim3(a.C), dim3(64), 0, st, part, nb, g, a.eps, stats);
+  if (nb <= kBandOne) {
+    hipLaunchKernelGGL(bn_band_finalize, dim3(a.C), dim3(256), 0, st, part, nb, g, a.eps, stats);
+  } else {
+    const int ns = (nb + kBandRps - 1) / kBandRps;
+    double* sl = reinterpret_cast<double*>(band_ws);
+    hipLaunchKernelGGL(bn_band_slices, dim3((a.C + 63) / 64, ns), dim3(256), 0, st, part, nb, g,
+                       sl, ns);
+    hipLaunchKernelGGL(bn_band_combine, dim3(a.C), dim3(64), 0, st, part, sl, ns, g, a.eps,
+                       stats);
+  }
   if (p.vec && a.swap)
     hipLaunchKernelGGL(bn_fwd_apply_vec<true>, dim3(apply_grid(g.M * p.CV / kApplyU, p.CV)),
                        dim3(kT), 0, st, x, gamma, beta, res, y, stats, g, p.CV, a.post_scale,

@@ -127,10 +127,12 @@ hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const 
                          const h16* res, h16* y, float* stats, int use_stats, void* ws,
                          hipStream_t st);
 // Forward from the band records of a convolution epilogue (IgemmArgs::stat):
-// statistics, then the apply.  part: [nb][3][C] float32, 128 rows per record.
-hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, const h16* x,
-                               const h16* gamma, const h16* beta, const h16* res, h16* y,
-                               float* stats, hipStream_t st);
+// statistics, then the apply.  part: [nb][3][C] float32, 128 rows per record;
+// band_ws: bn_band_ws_bytes(C, nb) bytes of scratch for the per-slice sums.
+size_t bn_band_ws_bytes(int C, int nb);
+hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, void* band_ws,
+                               const h16* x, const h16* gamma, const h16* beta, const h16* res,
+                               h16* y, float* stats, hipStream_t st);
 hipError_t launch_bn_bwd(const BnArgs& a, const h16* x, const h16* y, const h16* dy,
                          const h16* gamma, const h16* beta, const h16* res, const float* stats,
                          h16* dx, h16* dgamma, h16* dbeta, h16* dres, void* ws, hipStream_t st);
