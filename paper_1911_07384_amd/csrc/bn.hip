@@ -184,19 +184,25 @@ __global__ __launch_bounds__(kT) void bn_fwd_reduce_vec(const h16* __restrict__ 
     sums[0][e] = 0.0f;
     sums[1][e] = 0.0f;
   }
-  // four rows in flight per thread; the sums still run row by row
-  int64_t row = row0 + t / CV;
-  for (; row < row1; row += 4 * RB) {
+  // four rows in flight per thread, the sums row by row; the step count is
+  // the block's, and a row past the block's last is loaded clamped (in
+  // bounds) and adds exact zeros, so no load waits behind a condition
+  const int64_t rt = row0 + t / CV;
+  const int64_t nsteps = (row1 - row0 + RB - 1) / RB;
+  for (int64_t i = 0; i < nsteps; i += 4) {
     V8 v[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u)
-      if (row + u * RB < row1) v[u] = load16(x + (row + u * RB) * g.C + j * 8);
+    for (int u = 0; u < 4; ++u) {
+      const int64_t row = rt + (i + u) * RB;
+      v[u] = load16(x + (row < row1 ? row : row1 - 1) * g.C + j * 8);
+    }
+    __builtin_amdgcn_sched_barrier(0);  // every load issued before the first use
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      if (row + u * RB >= row1) break;
+      const bool ok = rt + (i + u) * RB < row1;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const float d = to_f32(v[u].h[e]) - sh[e];
+        const float d = ok ? to_f32(v[u].h[e]) - sh[e] : 0.0f;
         sums[0][e] += d;
         sums[1][e] = __builtin_fmaf(d, d, sums[1][e]);
       }
@@ -452,44 +458,56 @@ __global__ __launch_bounds__(64) void bn_band_combine(const float* __restrict__ 
 
 // ---- forward apply -------------------------------------------------------------
 
+// Variants of the vectorised kernels are template bits, so that every load
+// of a step is issued without a condition: a load behind a branch (on a lane
+// or on a runtime flag) made the compiler wait for all loads in flight before
+// the next one.
+//   kSwap: BN swap; kRelu: ReLU; kMaskY: the backward takes the ReLU mask from
+//   the stored output y; kLoadR: the shortcut r is read; kDres: the backward
+//   writes the shortcut gradient.
+constexpr int kSwap = 1, kRelu = 2, kMaskY = 4, kLoadR = 8, kDres = 16;
+
 // Each block takes runs of kApplyU * kT consecutive 16-byte vectors; a thread
 // loads its kApplyU vectors (and residual vectors) before it stores any, so
-// several loads per thread are in flight.  y may equal x: every element is
-// read and then written by the same thread.
+// several loads per thread are in flight.  The run loop is the block's; a
+// vector past the end is loaded clamped (in bounds) and not stored.  y may
+// equal x: every element is read and then written by the same thread (a
+// clamped load may read an element another lane rewrites; its value is
+// discarded).
 constexpr int kApplyU = 4;
 
-template <bool SWAP>
+template <int MODE>
 __global__ __launch_bounds__(kT) void bn_fwd_apply_vec(const h16* x, const h16* __restrict__ gamma,
                                                        const h16* __restrict__ beta, const h16* res,
                                                        h16* y, const float* __restrict__ stats,
-                                                       Geo g, int CV, float s, int relu) {
+                                                       Geo g, int CV, float s) {
+  constexpr bool SWAP = MODE & kSwap, RELU = MODE & kRelu, HAS_R = MODE & kLoadR;
   const int t = threadIdx.x;
   const int j = t % CV;  // run starts and kT are multiples of CV
   FwdCoef k[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) k[e] = fwd_coef(stats, gamma, beta, g.C, j * 8 + e, s);
   const int64_t nvec = g.M * CV;
-  for (int64_t base = (int64_t)blockIdx.x * (kApplyU * kT) + t; base < nvec;
-       base += (int64_t)gridDim.x * (kApplyU * kT)) {
+  constexpr int64_t RUN = (int64_t)kApplyU * kT;
+  for (int64_t run = (int64_t)blockIdx.x * RUN; run < nvec; run += (int64_t)gridDim.x * RUN) {
     V8 xv[kApplyU], rv[kApplyU];
 #pragma unroll
     for (int u = 0; u < kApplyU; ++u) {
-      const int64_t v = base + u * kT;
-      if (v < nvec) {
-        xv[u] = load16(x + v * 8);
-        if (res) rv[u] = load16(res + v * 8);
-      }
+      const int64_t v = run + t + u * kT;
+      const int64_t vc = v < nvec ? v : nvec - 1;
+      xv[u] = load16(x + vc * 8);
+      if (HAS_R) rv[u] = load16(res + vc * 8);
     }
+    __builtin_amdgcn_sched_barrier(0);  // every load issued before the first use
 #pragma unroll
     for (int u = 0; u < kApplyU; ++u) {
-      const int64_t v = base + u * kT;
-      if (v >= nvec) break;
+      const int64_t v = run + t + u * kT;
       V8 out;
 #pragma unroll
       for (int e = 0; e < 8; ++e)
-        out.h[e] = to_h16(fwd_value(to_f32(xv[u].h[e]), k[e], res != nullptr,
-                                    res ? to_f32(rv[u].h[e]) : 0.0f, relu != 0, SWAP));
-      store16(y + v * 8, out);
+        out.h[e] = to_h16(fwd_value(to_f32(xv[u].h[e]), k[e], HAS_R,
+                                    HAS_R ? to_f32(rv[u].h[e]) : 0.0f, RELU, SWAP));
+      if (v < nvec) store16(y + v * 8, out);
     }
   }
 }
@@ -510,8 +528,8 @@ __global__ __launch_bounds__(kT) void bn_fwd_apply_gen(const h16* x, const h16* 
 
 // ---- backward reduce -----------------------------------------------------------
 
-// NS = 2: S1 = sum g, S2 = sum g*xhat; NS = 3 (BN swap) adds S3 = sum g*r.
-template <int NS>
+// S1 = sum g, S2 = sum g*xhat; with the BN swap also S3 = sum g*r.
+template <int MODE>
 __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ x,
                                                         const h16* __restrict__ y,
                                                         const h16* __restrict__ dy,
@@ -520,8 +538,10 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
                                                         const h16* __restrict__ res,
                                                         const float* __restrict__ stats, Geo g,
                                                         int CV, int RB, int64_t rpb, float s,
-                                                        int relu, float* ws) {
-  constexpr bool SWAP = NS == 3;
+                                                        float* ws) {
+  constexpr bool SWAP = MODE & kSwap, RELU = MODE & kRelu, MASK_Y = MODE & kMaskY,
+                 LOAD_R = MODE & kLoadR;
+  constexpr int NS = SWAP ? 3 : 2;
   __shared__ float red[8 * NS * kT];
   const int t = threadIdx.x;
   const int j = t % CV;
@@ -537,43 +557,47 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
 #pragma unroll
     for (int v = 0; v < NS; ++v) sums[v][e] = 0.0f;
   }
-  const bool has_y = y != nullptr, has_r = res != nullptr && !has_y && relu;
-  const bool load_r = has_r || SWAP;
-  // one row per step, the next row loaded before this one is summed
-  // (software pipelined, two rows in flight); the sums run row by row
+  // one row per step, the next row loaded before this one is summed (two rows
+  // in flight); the step count is the block's, and a row past the block's
+  // last is loaded clamped (in bounds) and adds exact zeros
   struct Row {
     V8 x, d, y, r;
   };
-  auto load_row = [&](Row& b, int64_t row) {
+  const int64_t rt = row0 + t / CV;
+  const int64_t nsteps = (row1 - row0 + RB - 1) / RB;
+  auto load_row = [&](Row& b, int64_t i) {
+    int64_t row = rt + i * RB;
+    if (row >= row1) row = row1 - 1;
     const int64_t off = row * g.C + j * 8;
     b.x = load16(x + off);
     b.d = load16(dy + off);
-    if (relu && has_y) b.y = load16(y + off);
-    if (load_r) b.r = load16(res + off);
+    if (MASK_Y) b.y = load16(y + off);
+    if (LOAD_R) b.r = load16(res + off);
   };
-  auto sum_row = [&](const Row& b) {
+  auto sum_row = [&](const Row& b, int64_t i) {
+    const bool ok = rt + i * RB < row1;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float xf = to_f32(b.x.h[e]);
-      const float rf = load_r ? to_f32(b.r.h[e]) : 0.0f;
-      const bool m = relu_mask(relu != 0, has_y, has_y ? b.y.h[e] : (h16)0.0f, xf, k[e], has_r, rf,
+      const float rf = LOAD_R ? to_f32(b.r.h[e]) : 0.0f;
+      const bool m = relu_mask(RELU, MASK_Y, MASK_Y ? b.y.h[e] : (h16)0.0f, xf, k[e], LOAD_R, rf,
                                SWAP);
-      const float gg = m ? s * to_f32(b.d.h[e]) : 0.0f;
-      const float xh = (xf - k[e].mean) * rstd[e];
+      const float gg = ok && m ? s * to_f32(b.d.h[e]) : 0.0f;
+      const float xh = ok ? (xf - k[e].mean) * rstd[e] : 0.0f;
       sums[0][e] += gg;
       sums[1][e] = __builtin_fmaf(gg, xh, sums[1][e]);
-      if (SWAP) sums[NS - 1][e] = __builtin_fmaf(gg, rf, sums[NS - 1][e]);
+      if (SWAP) sums[NS - 1][e] = __builtin_fmaf(gg, ok ? rf : 0.0f, sums[NS - 1][e]);
     }
   };
   Row ra, rb;
-  int64_t row = row0 + t / CV;
-  if (row < row1) load_row(ra, row);
-  for (; row < row1; row += 2 * RB) {
-    if (row + RB < row1) load_row(rb, row + RB);
-    sum_row(ra);
-    if (row + RB >= row1) break;
-    if (row + 2 * RB < row1) load_row(ra, row + 2 * RB);
-    sum_row(rb);
+  load_row(ra, 0);
+  for (int64_t i = 0; i < nsteps; i += 2) {
+    load_row(rb, i + 1);
+    __builtin_amdgcn_sched_barrier(0);  // the next row's loads ahead of this row's sums
+    sum_row(ra, i);
+    load_row(ra, i + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    sum_row(rb, i + 1);
   }
   block_reduce_vec<NS>(sums, red, CV, RB, ws, (int)gridDim.x);
 }
@@ -637,14 +661,17 @@ __global__ __launch_bounds__(64) void bn_bwd_finalize(Geo g, int G, const float*
 
 // ---- backward apply ------------------------------------------------------------
 
-template <bool SWAP>
+template <int MODE>
 __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* y, const h16* dy,
                                                        const h16* __restrict__ gamma,
                                                        const h16* __restrict__ beta, const h16* res,
                                                        const float* __restrict__ stats,
                                                        const float* __restrict__ coef, Geo g,
-                                                       int CV, float s, int relu, h16* dx,
-                                                       h16* dres) {
+                                                       int CV, float s, h16* dx, h16* dres) {
+  constexpr bool SWAP = MODE & kSwap, RELU = MODE & kRelu, MASK_Y = MODE & kMaskY,
+                 DRES = MODE & kDres;
+  // the shortcut is read here only for the ReLU mask recomputed from x
+  constexpr bool NEED_R = (MODE & kLoadR) && RELU && !MASK_Y;
   const int t = threadIdx.x;
   const int j = t % CV;  // run starts and kT are multiples of CV
   FwdCoef k[8];
@@ -659,43 +686,42 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* 
     D[e] = coef[2 * g.C + c];
     gam[e] = to_f32(gamma[c]);
   }
-  constexpr bool swap = SWAP;
-  const bool has_y = y != nullptr, has_r = res != nullptr && !has_y && relu;
   const int64_t nvec = g.M * CV;
-  constexpr int U = kApplyU / 2;  // vectors per thread and run: 2 or 3 loads each
-  for (int64_t base = (int64_t)blockIdx.x * (U * kT) + t; base < nvec;
-       base += (int64_t)gridDim.x * (U * kT)) {
+  constexpr int U = kApplyU / 2;  // vectors per thread and run: 2 to 4 loads each
+  constexpr int64_t RUN = (int64_t)U * kT;
+  for (int64_t run = (int64_t)blockIdx.x * RUN; run < nvec; run += (int64_t)gridDim.x * RUN) {
     V8 xv[U], dv[U], yv[U], rv[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t v = base + u * kT;
-      if (v < nvec) {
-        xv[u] = load16(x + v * 8);
-        dv[u] = load16(dy + v * 8);
-        if (relu && has_y) yv[u] = load16(y + v * 8);
-        if (has_r) rv[u] = load16(res + v * 8);
-      }
+      const int64_t v = run + t + u * kT;
+      const int64_t vc = v < nvec ? v : nvec - 1;
+      xv[u] = load16(x + vc * 8);
+      dv[u] = load16(dy + vc * 8);
+      if (MASK_Y) yv[u] = load16(y + vc * 8);
+      if (NEED_R) rv[u] = load16(res + vc * 8);
     }
+    __builtin_amdgcn_sched_barrier(0);  // every load issued before the first use
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int64_t v = base + u * kT;
-      if (v >= nvec) break;
+      const int64_t v = run + t + u * kT;
       V8 o, od;
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float xf = to_f32(xv[u].h[e]);
-        const bool m = relu_mask(relu != 0, has_y, has_y ? yv[u].h[e] : (h16)0.0f, xf, k[e],
-                                 has_r, has_r ? to_f32(rv[u].h[e]) : 0.0f, swap);
+        const bool m = relu_mask(RELU, MASK_Y, MASK_Y ? yv[u].h[e] : (h16)0.0f, xf, k[e], NEED_R,
+                                 NEED_R ? to_f32(rv[u].h[e]) : 0.0f, SWAP);
         const float gg = m ? s * to_f32(dv[u].h[e]) : 0.0f;
         const float xh = (xf - k[e].mean) * rstd[e];
         o.h[e] = to_h16(A[e] * (gg - __builtin_fmaf(xh, D[e], B[e])));
-        if (swap)
+        if (SWAP)
           od.h[e] = to_h16(gam[e] * gg);
         else
           od.s[e] = m ? dv[u].s[e] : (uint16_t)0;
       }
-      store16(dx + v * 8, o);
-      if (dres) store16(dres + v * 8, od);
+      if (v < nvec) {
+        store16(dx + v * 8, o);
+        if (DRES) store16(dres + v * 8, od);
+      }
     }
   }
 }
@@ -730,6 +756,41 @@ unsigned apply_grid(int64_t nthreads_wanted, int CV) {
   if (b < 1) b = 1;
   (void)CV;  // kT is a multiple of CV, so any grid keeps each thread on one chunk
   return (unsigned)b;
+}
+
+// Template variant of the vectorised kernels for these arguments.
+int fwd_mode(const BnArgs& a, const h16* res) {
+  return (a.swap ? kSwap : 0) | (a.relu ? kRelu : 0) | (res ? kLoadR : 0);
+}
+int bwd_mode(const BnArgs& a, const h16* y, const h16* res, const h16* dres) {
+  const bool relu = a.relu != 0, mask_y = relu && y != nullptr;
+  const bool load_r = a.swap || (relu && !mask_y && res != nullptr);
+  return (a.swap ? kSwap : 0) | (relu ? kRelu : 0) | (mask_y ? kMaskY : 0) |
+         (load_r ? kLoadR : 0) | (dres ? kDres : 0);
+}
+
+// The valid variants (the BN swap always reads the shortcut).
+#define FP16K_BN_FWD_MODES(X) X(0) X(2) X(8) X(10) X(9) X(11)
+#define FP16K_BN_BWD_MODES(X) X(0) X(6) X(2) X(10) X(9) X(15) X(11)
+#define FP16K_BN_BWD_APPLY_MODES(X) \
+  FP16K_BN_BWD_MODES(X) X(16) X(22) X(18) X(26) X(25) X(31) X(27)
+
+hipError_t launch_fwd_apply_vec(int mode, const Plan& p, const Geo& g, const h16* x,
+                                const h16* gamma, const h16* beta, const h16* res, h16* y,
+                                const float* stats, float s, hipStream_t st) {
+  const dim3 grid(apply_grid(g.M * p.CV / kApplyU, p.CV));
+  switch (mode) {
+#define FP16K_CASE(m)                                                                          \
+  case m:                                                                                      \
+    hipLaunchKernelGGL(bn_fwd_apply_vec<m>, grid, dim3(kT), 0, st, x, gamma, beta, res, y,     \
+                       stats, g, p.CV, s);                                                      \
+    break;
+    FP16K_BN_FWD_MODES(FP16K_CASE)
+#undef FP16K_CASE
+    default:
+      return hipErrorInvalidValue;
+  }
+  return hipSuccess;
 }
 
 Geo make_geo(const BnArgs& a) {
@@ -770,17 +831,14 @@ hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const 
     hipLaunchKernelGGL(bn_fwd_finalize, dim3(a.C), dim3(64), 0, st, x, g, p.G, part, a.eps,
                        stats);
   }
-  if (p.vec && a.swap)
-    hipLaunchKernelGGL(bn_fwd_apply_vec<true>, dim3(apply_grid(g.M * p.CV / kApplyU, p.CV)),
-                       dim3(kT), 0, st, x, gamma, beta, res, y, stats, g, p.CV, a.post_scale,
-                       a.relu);
-  else if (p.vec)
-    hipLaunchKernelGGL(bn_fwd_apply_vec<false>, dim3(apply_grid(g.M * p.CV / kApplyU, p.CV)),
-                       dim3(kT), 0, st, x, gamma, beta, res, y, stats, g, p.CV, a.post_scale,
-                       a.relu);
-  else
+  if (p.vec) {
+    const hipError_t e =
+        launch_fwd_apply_vec(fwd_mode(a, res), p, g, x, gamma, beta, res, y, stats, a.post_scale, st);
+    if (e != hipSuccess) return e;
+  } else {
     hipLaunchKernelGGL(bn_fwd_apply_gen, dim3(apply_grid(g.M * a.C / 4, 1)), dim3(kT), 0, st, x,
                        gamma, beta, res, y, stats, g, a.post_scale, a.relu);
+  }
   return hipGetLastError();
 }
 
@@ -804,17 +862,14 @@ hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, void*
     hipLaunchKernelGGL(bn_band_combine, dim3(a.C), dim3(64), 0, st, part, sl, ns, g, a.eps,
                        stats);
   }
-  if (p.vec && a.swap)
-    hipLaunchKernelGGL(bn_fwd_apply_vec<true>, dim3(apply_grid(g.M * p.CV / kApplyU, p.CV)),
-                       dim3(kT), 0, st, x, gamma, beta, res, y, stats, g, p.CV, a.post_scale,
-                       a.relu);
-  else if (p.vec)
-    hipLaunchKernelGGL(bn_fwd_apply_vec<false>, dim3(apply_grid(g.M * p.CV / kApplyU, p.CV)),
-                       dim3(kT), 0, st, x, gamma, beta, res, y, stats, g, p.CV, a.post_scale,
-                       a.relu);
-  else
+  if (p.vec) {
+    const hipError_t e =
+        launch_fwd_apply_vec(fwd_mode(a, res), p, g, x, gamma, beta, res, y, stats, a.post_scale, st);
+    if (e != hipSuccess) return e;
+  } else {
     hipLaunchKernelGGL(bn_fwd_apply_gen, dim3(apply_grid(g.M * a.C / 4, 1)), dim3(kT), 0, st, x,
                        gamma, beta, res, y, stats, g, a.post_scale, a.relu);
+  }
   return hipGetLastError();
 }
 
@@ -825,30 +880,42 @@ hipError_t launch_bn_bwd(const BnArgs& a, const h16* x, const h16* y, const h16*
   const Geo g = make_geo(a);
   float* part = reinterpret_cast<float*>(ws);
   float* coef = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + partial_bytes(p, a.C));
+  const int mode = bwd_mode(a, y, res, dres);
   if (p.vec) {
-    if (a.swap)
-      hipLaunchKernelGGL(bn_bwd_reduce_vec<3>, dim3(p.G), dim3(kT), 0, st, x, y, dy, gamma, beta,
-                         res, stats, g, p.CV, p.RB, p.rpb, a.post_scale, a.relu, part);
-    else
-      hipLaunchKernelGGL(bn_bwd_reduce_vec<2>, dim3(p.G), dim3(kT), 0, st, x, y, dy, gamma, beta,
-                         res, stats, g, p.CV, p.RB, p.rpb, a.post_scale, a.relu, part);
+    switch (mode & ~kDres) {
+#define FP16K_CASE(m)                                                                          \
+  case m:                                                                                      \
+    hipLaunchKernelGGL(bn_bwd_reduce_vec<m>, dim3(p.G), dim3(kT), 0, st, x, y, dy, gamma, beta, \
+                       res, stats, g, p.CV, p.RB, p.rpb, a.post_scale, part);                    \
+    break;
+      FP16K_BN_BWD_MODES(FP16K_CASE)
+#undef FP16K_CASE
+      default:
+        return hipErrorInvalidValue;
+    }
   } else {
     hipLaunchKernelGGL(bn_bwd_reduce_gen, dim3(p.G, a.C), dim3(kT), 0, st, x, y, dy, gamma, beta,
                        res, stats, g, p.rpb, a.post_scale, a.relu, part);
   }
   hipLaunchKernelGGL(bn_bwd_finalize, dim3(a.C), dim3(64), 0, st, g, p.G, part, gamma, stats,
                      dgamma, dbeta, coef);
-  if (p.vec && a.swap)
-    hipLaunchKernelGGL(bn_bwd_apply_vec<true>, dim3(apply_grid(g.M * p.CV / (kApplyU / 2), p.CV)),
-                       dim3(kT), 0, st, x, y, dy, gamma, beta, res, stats, coef, g, p.CV,
-                       a.post_scale, a.relu, dx, dres);
-  else if (p.vec)
-    hipLaunchKernelGGL(bn_bwd_apply_vec<false>, dim3(apply_grid(g.M * p.CV / (kApplyU / 2), p.CV)),
-                       dim3(kT), 0, st, x, y, dy, gamma, beta, res, stats, coef, g, p.CV,
-                       a.post_scale, a.relu, dx, dres);
-  else
+  if (p.vec) {
+    const dim3 grid(apply_grid(g.M * p.CV / (kApplyU / 2), p.CV));
+    switch (mode) {
+#define FP16K_CASE(m)                                                                          \
+  case m:                                                                                      \
+    hipLaunchKernelGGL(bn_bwd_apply_vec<m>, grid, dim3(kT), 0, st, x, y, dy, gamma, beta, res, \
+                       stats, coef, g, p.CV, a.post_scale, dx, dres);                           \
+    break;
+      FP16K_BN_BWD_APPLY_MODES(FP16K_CASE)
+#undef FP16K_CASE
+      default:
+        return hipErrorInvalidValue;
+    }
+  } else {
     hipLaunchKernelGGL(bn_bwd_apply_gen, dim3(apply_grid(g.M * a.C / 4, 1)), dim3(kT), 0, st, x,
                        y, dy, gamma, beta, res, stats, coef, g, a.post_scale, a.relu, dx, dres);
+  }
   return hipGetLastError();
 }
 

@@ -35,9 +35,17 @@
 //                    MFMA operands read one k sub-step ahead.  Needs
 //                    Ci % 64 == 0; wins on the long reductions (every 3x3
 //                    layer).
+//   pw_kernel     -- 1x1 filters with 64 or 128 input channels and a dense
+//                    output of 128+ channels (bound by the output's bytes):
+//                    the filter tile stays in LDS, each workgroup walks over
+//                    128-row tiles, and the MFMA operands are swapped so that
+//                    the accumulators hold the transposed tile; lane-pair
+//                    swaps (v_permlane32_swap) then give each lane 8
+//                    consecutive channels of one output pixel, written
+//                    straight from registers.
 //
-// Epilogue (all): each wave stages a 32-row band of its float32 tile in LDS
-// and writes whole output rows with 16-byte stores.  Every value is rounded
+// Epilogue (the first three): each wave stages a 32-row band of its float32
+// tile in LDS and writes whole output rows with 16-byte stores.  Every value is rounded
 // once to binary16 (RNE), optionally after adding a binary16 addend in
 // float32.  igemm4_kernel and igemm7_kernel can also take the statistics of a
 // BN that follows the convolution, without a second pass over the output:
@@ -566,6 +574,219 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
   }
 }
 
+// ---- pointwise (1x1) convolutions bound by the output's bytes ------------------
+// For a 1x1 filter over CI = 64 or 128 input channels with 128+ output
+// channels, writing y costs 2-4x more bytes than reading x, and staging the
+// accumulators through LDS for the stores (as the kernels above do) held these
+// layers at 2-2.5 TB/s.  Here:
+//  - the BN x CI filter tile is loaded into LDS once (16-byte chunks XOR-
+//    swizzled by row, so fragment reads are conflict free) and each workgroup
+//    walks over 128-row tiles of the output, grid-stride; every lane loads its
+//    own pixel row's operand fragments one tile ahead;
+//  - the MFMA runs with the operands swapped, D = W x X^T, so a lane's
+//    accumulators hold one output pixel (lane % 32) and channels
+//    8*(e/4) + 4*(lane/32) + e%4 of each 32-channel tile.  Swapping the upper
+//    lane half of channel group 2g with the lower lane half of group 2g+1
+//    (v_permlane32_swap, four register pairs per group pair) leaves each lane
+//    with 8 consecutive channels twice, which go out as 16-byte stores;
+//  - with BN statistics the plain product D = X x W is computed too (the
+//    MFMAs are cheap here), whose layout gives each lane one channel and 16
+//    rows: the band sums are taken in the lane, and the four waves' bands of a
+//    tile are combined into one 128-row record as in igemm4_kernel.
+// Each output element is the same k-ordered sum of exact products in both
+// MFMA forms, so the values equal the other kernels' bit for bit.
+template <int CI, int BN, bool STATS>
+struct CfgPw {
+  static constexpr int KS = CI / 16;          // k sub-steps of 16 channels
+  static constexpr int TN = BN / 32;          // 32-channel tiles
+  static constexpr int BBYTES = BN * CI * 2;  // resident filter tile
+  static constexpr int BST = STATS ? 4 * 3 * BN * 4 : 0;  // [wave][K, s1, s2][BN]
+  static constexpr int LDS = BBYTES + BST + 16;
+};
+
+__device__ __forceinline__ void lane_half_swap(float& x, float& y) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__builtin_bit_cast(unsigned, x),
+                                                  __builtin_bit_cast(unsigned, y), false, false);
+  x = __builtin_bit_cast(float, (unsigned)r[0]);
+  y = __builtin_bit_cast(float, (unsigned)r[1]);
+}
+
+template <int CI, int BN, bool STATS, bool ADD>
+__global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) {
+  using K = CfgPw<CI, BN, STATS>;
+  constexpr int KS = K::KS, TN = K::TN;
+  static_assert(CI == 64 || CI == 128, "input channels");
+  static_assert(!(STATS && ADD), "statistics are taken without an addend");
+  __shared__ __attribute__((aligned(1024))) char lds[K::LDS];
+  char* bt = lds;
+  float* bst = reinterpret_cast<float*>(lds + K::BBYTES);
+  int* bcnt = reinterpret_cast<int*>(lds + K::BBYTES + K::BST);
+
+  const IgemmPhase ph = a.ph[0];
+  const int HoWo = ph.Ho * ph.Wo;
+  const int M = a.N * HoWo;
+  const int n0 = blockIdx.y * BN;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const int lrow = lane & 31, lhi = lane >> 5;
+  constexpr uint32_t OOB = 0x80000000u;
+  const int act_bytes = (int)((int64_t)a.N * a.Hi * a.Wi * CI * 2);
+  const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<h16*>(a.act), (short)0, act_bytes, 0x00020000);
+
+  // filter tile: row n (channel n0 + n), chunk c stored at chunk c ^ (n % 8)
+  for (int i = tid; i < BN * (CI / 8); i += 256) {
+    const int n = i / (CI / 8), c = i - n * (CI / 8);
+    V8 v;
+    if (n0 + n < a.Co) {
+      v = load16(ph.filt + (int64_t)(n0 + n) * ph.ldb + c * 8);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v.s[e] = 0;
+    }
+    *reinterpret_cast<V8*>(bt + (n * (CI / 8) + (c ^ (n & 7))) * 16) = v;
+  }
+
+  // this lane's source pixel row in a tile (out of range: reads zeros)
+  auto row_off = [&](int tile) -> uint32_t {
+    const int m = tile * 128 + wave * 32 + lrow;
+    if (tile >= ntiles || m >= M) return OOB;
+    const int img = m / HoWo;
+    const int rem = m - img * HoWo;
+    const int i = rem / ph.Wo;
+    const int j = rem - i * ph.Wo;
+    const int pix = (img * a.Hi + i * a.stride_h) * a.Wi + j * a.stride_w;
+    return (uint32_t)pix * (uint32_t)(CI * 2) + (uint32_t)lhi * 16u;
+  };
+  auto load_a = [&](half8 (&A)[KS], uint32_t o) {
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      A[ks] = __builtin_bit_cast(half8, __builtin_amdgcn_raw_buffer_load_b128(
+                                            rs_a, o == OOB ? OOB : o + ks * 32, 0, 0));
+  };
+  half8 Acur[KS], Anext[KS];
+  int tile = blockIdx.x;
+  load_a(Acur, row_off(tile));
+  __syncthreads();
+  const int swz = lrow & 7;
+  for (; tile < ntiles; tile += gridDim.x) {
+    const int band_m0 = tile * 128 + wave * 32;
+    const int mp = band_m0 + lrow;  // this lane's output pixel in the transposed tile
+    const bool mp_ok = mp < M;
+    V8 adv[ADD ? TN : 1][2];
+    if (ADD) {
+      // the tile's addend, loaded before the MFMAs (pixel clamped into range)
+      const int64_t mrow = (int64_t)(mp_ok ? mp : M - 1) * a.ldo;
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int n = n0 + tn * 32 + h * 16 + lhi * 8;
+          adv[tn][h] = load16(a.addend + mrow + (n < a.Co ? n : 0));
+        }
+    }
+    load_a(Anext, row_off(tile + gridDim.x));
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) {
+      floatx16 at, an;
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        at[e] = 0.0f;
+        an[e] = 0.0f;
+      }
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int pos = ((ks * 2 + lhi) ^ swz) * 16;
+        const half8 bf = *reinterpret_cast<const half8*>(bt + (tn * 32 + lrow) * (CI * 2) + pos);
+        at = mfma32x32x16(bf, Acur[ks], at);
+        if (STATS) an = mfma32x32x16(Acur[ks], bf, an);
+      }
+      float v[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) v[e] = at[e];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        lane_half_swap(v[q], v[4 + q]);
+        lane_half_swap(v[8 + q], v[12 + q]);
+      }
+      // v[8h .. 8h+7] = channels tn*32 + 16h + 8*lhi + 0..7 of pixel mp
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int n = n0 + tn * 32 + h * 16 + lhi * 8;
+        if (mp_ok && n < a.Co) {
+          const int64_t off = (int64_t)mp * a.ldo + n;
+          float w[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) w[e] = v[h * 8 + e];
+          if (ADD) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) w[e] += to_f32(adv[tn][h].h[e]);
+          }
+          V8 o;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o.h[e] = to_h16(w[e]);
+          store16(a.out + off, o);
+        }
+      }
+      if (STATS) {
+        // plain layout: lane holds channel tn*32 + lane % 32 and band rows
+        // 8*(e/4) + 4*(lane/32) + e%4; the shift is the band's first row
+        float y[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) y[e] = to_f32(to_h16(an[e]));
+        const float K0 = __shfl(y[0], lrow, 64);
+        float s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          const int r = 8 * (e >> 2) + 4 * lhi + (e & 3);
+          const float d = band_m0 + r < M ? y[e] - K0 : 0.0f;
+          s1 += d;
+          s2 = __builtin_fmaf(d, d, s2);
+        }
+        s1 += __shfl_xor(s1, 32, 64);
+        s2 += __shfl_xor(s2, 32, 64);
+        if (lhi == 0) {
+          bst[(wave * 3 + 0) * BN + tn * 32 + lrow] = K0;
+          bst[(wave * 3 + 1) * BN + tn * 32 + lrow] = s1;
+          bst[(wave * 3 + 2) * BN + tn * 32 + lrow] = s2;
+        }
+      }
+    }
+    if (STATS) {
+      if (lane == 0) {
+        const int rows = M - band_m0;
+        bcnt[wave] = rows <= 0 ? 0 : (rows < 32 ? rows : 32);
+      }
+      __syncthreads();
+      // one record per 128-row tile: the bands re-based on the first band's
+      // shift, in wave order
+      for (int c = tid; c < BN; c += 256) {
+        if (bcnt[0] > 0 && n0 + c < a.Co) {
+          const float K0 = bst[c];
+          float S1 = 0.0f, S2 = 0.0f;
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            const float nw = (float)bcnt[w];
+            if (bcnt[w] == 0) break;
+            const float d = bst[(w * 3) * BN + c] - K0;
+            const float t1 = bst[(w * 3 + 1) * BN + c];
+            S1 += __builtin_fmaf(nw, d, t1);
+            S2 += __builtin_fmaf(nw * d, d,
+                                 __builtin_fmaf(2.0f * d, t1, bst[(w * 3 + 2) * BN + c]));
+          }
+          float* rec = a.stat + (int64_t)tile * 3 * a.Co + n0 + c;
+          rec[0] = K0;
+          rec[a.Co] = S1;
+          rec[2 * a.Co] = S2;
+        }
+      }
+      __syncthreads();
+    }
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) Acur[ks] = Anext[ks];
+  }
+}
+
 // ---- k-step 64, whole 128-byte operand rows, fragment reads one sub-step ahead
 // As igemm6, with a k-step of 64 channels: every operand row of a stage is one
 // whole 128-byte line (8 lanes x 16 bytes per row, 8 rows per 1 KB DMA
@@ -900,6 +1121,22 @@ hipError_t launch_cfg4(const IgemmArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <int CI, int BN>
+hipError_t launch_pw(const IgemmArgs& a, hipStream_t st) {
+  const int M = a.N * a.ph[0].Ho * a.ph[0].Wo;
+  if (M == 0) return hipSuccess;
+  const int ntiles = ceil_div(M, 128);
+  // two to three workgroups per CU walk the tiles
+  dim3 grid(ntiles < 512 ? ntiles : 512, ceil_div(a.Co, BN));
+  if (a.stat)
+    hipLaunchKernelGGL((pw_kernel<CI, BN, true, false>), grid, dim3(256), 0, st, a, ntiles);
+  else if (a.addend)
+    hipLaunchKernelGGL((pw_kernel<CI, BN, false, true>), grid, dim3(256), 0, st, a, ntiles);
+  else
+    hipLaunchKernelGGL((pw_kernel<CI, BN, false, false>), grid, dim3(256), 0, st, a, ntiles);
+  return hipGetLastError();
+}
+
 template <int BM, int BN, int WM, int WN, int BK, bool F16ACC = false>
 hipError_t launch_cfg(const IgemmArgs& a, hipStream_t st) {
   int maxM = 0;
@@ -917,15 +1154,27 @@ hipError_t launch_cfg(const IgemmArgs& a, hipStream_t st) {
 
 namespace {
 
-enum class IgemmKind { kLds, kDirect, kDma };
+enum class IgemmKind { kLds, kDirect, kDma, kPointwise };
 
 // Kernel choice per problem (measured on MI355X over the ResNet-50 shapes at
-// batch 32 and 128): the DMA-staged kernel for reductions of 576 and more
-// (every 3x3 layer, the 1x1 layers with 1024+ input channels); below that
-// the register-direct kernel for short reductions or small M, else the
-// LDS-staged one.  All three give identical bits.
+// batch 32 and 128): the pointwise kernel for 1x1 filters over 64 or 128
+// channels with 128+ output channels; the DMA-staged kernel for reductions of
+// 576 and more (every 3x3 layer, the 1x1 layers with 1024+ input channels);
+// below that the register-direct kernel for short reductions or small M,
+// else the LDS-staged one.  All four give identical bits.
 IgemmKind igemm_kind(const IgemmArgs& a) {
   if (a.f16acc) return IgemmKind::kLds;
+  {
+    // a 1x1 filter over 64 or 128 channels with a dense output of 128+
+    // channels: the pointwise kernel
+    const IgemmPhase& p = a.ph[0];
+    const int64_t act = (int64_t)a.N * a.Hi * a.Wi * a.Ci * 2;
+    if (a.nphase == 1 && p.Rt == 1 && p.St == 1 && p.pad_h == 0 && p.pad_w == 0 &&
+        p.oph == 0 && p.opw == 0 && a.os_h == 1 && a.os_w == 1 && a.OH == p.Ho &&
+        a.OW == p.Wo && (a.Ci == 64 || a.Ci == 128) && p.ldb == a.Ci && a.Co >= 128 &&
+        a.Co % 8 == 0 && a.ldo % 8 == 0 && act < ((int64_t)1 << 31))
+      return IgemmKind::kPointwise;
+  }
   int maxM = 0, maxK = 0, maxT = 0;
   int64_t maxF = 0;
   for (int p = 0; p < a.nphase; ++p) {
@@ -966,6 +1215,9 @@ hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st) {
     }
     case IgemmKind::kDirect:
       return a.Co <= 64 ? launch_cfg4<1, 2>(a, st) : launch_cfg4<1, 4>(a, st);
+    case IgemmKind::kPointwise:
+      if (a.Ci == 64) return a.Co >= 256 ? launch_pw<64, 256>(a, st) : launch_pw<64, 128>(a, st);
+      return launch_pw<128, 256>(a, st);
     default:
       return a.Co <= 64 ? launch_cfg<128, 64, 4, 1, 64>(a, st) : launch_cfg<128, 128, 2, 2, 64>(a, st);
   }

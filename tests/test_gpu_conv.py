@@ -42,6 +42,11 @@ SHAPES = [
     (2, 1024, 5, 5, 96, 1, 1, 1, 0, "NHWC"),    # 1x1 with a 1024-long reduction: DMA-staged
     (2, 24, 9, 9, 64, 3, 3, 1, 1, "NHWC"),      # wgrad: 8-channel chunks of one 64-column block span taps
     (2, 8, 12, 12, 128, 1, 1, 2, 0, "NHWC"),    # wgrad: 8 channels, K = 128
+    (2, 64, 20, 20, 192, 1, 1, 1, 0, "NHWC"),   # pointwise fwd: 64 -> 192, second channel tile partial
+    (3, 128, 9, 9, 384, 1, 1, 1, 0, "NHWC"),    # pointwise fwd over 128 channels, M = 243 (ragged)
+    (3, 136, 9, 9, 64, 1, 1, 1, 0, "NHWC"),     # pointwise dgrad: 64 -> 136 channels (one 8-wide chunk
+                                                # in the second channel tile)
+    (5, 64, 56, 56, 256, 1, 1, 1, 0, "NHWC"),   # pointwise fwd / dgrad over many tiles per workgroup
 ]
 
 
@@ -124,3 +129,27 @@ def test_parity_full_size_sampled(shape, which):
     err = np.max(np.abs(got[idx].astype(np.float64) - ref))
     assert err <= 1e-2 * rms, (err, rms)
     assert np.all(np.isfinite(got.astype(np.float32)))
+
+
+# (n, c, h, k): 1x1 stride-1 data gradients plus an addend (the bottleneck's
+# first convolution, whose input gradient joins the shortcut's)
+ADD_SHAPES = [(2, 256, 14, 64), (3, 136, 9, 64), (2, 64, 28, 64), (4, 256, 56, 64)]
+
+
+@pytest.mark.parametrize("shape", ADD_SHAPES, ids=["n{}c{}h{}k{}".format(*s) for s in ADD_SHAPES])
+def test_dgrad_add_parity(shape):
+    require_gpu()
+    import oracle
+    from paper_1911_07384_amd import synth
+    n, c, h, k = shape
+    case = ConvCase(n, c, h, h, k, 1, 1, 1, 0, seed=4)
+    addend = synth.normal_f16(case.xs, 1e-2, 4, 9)
+    ws = F.workspace(F.fp16_conv_workspace_bytes(case.desc, F.PASS_DGRAD))
+    out = torch.empty(case.xs, dtype=torch.float16, device="cuda")
+    note(f"[gpu] dgrad_add {case.label}")
+    F.fp16_conv_dgrad_add(case.desc, dev(case.dy), dev(case.w), dev(addend), out, ws)
+    torch.cuda.synchronize()
+    got = host(out)
+    ref64, ref16 = oracle.conv_dgrad_add(case.shp, case.dy, case.w, addend)
+    check_close(got, ref64, what=f"dgrad_add {case.label}")
+    assert np.mean(ulp_dist(got, ref16) <= 1) > 0.99

@@ -31,6 +31,9 @@ CASES = [
     (2, 64, 14, 256, 1, 1, 0, 0.25, True, True, True),     # BN swap on the block-last BN
     (2, 128, 15, 64, 3, 2, 1, 0.25, False, False, False),  # strided, no ReLU
     (32, 256, 56, 64, 1, 1, 0, 0.25, False, True, False),  # the conv2_x block's conv1 at batch 32
+    (3, 128, 9, 384, 1, 1, 0, 0.25, False, True, False),   # pointwise kernel over 128 channels,
+                                                           # ragged rows and channel tiles
+    (5, 64, 56, 256, 1, 1, 0, 0.25, True, True, False),    # pointwise, many tiles per workgroup
     (6, 64, 212, 64, 1, 1, 0, 0.25, False, True, False),   # 2,107 tile records (ragged): the
                                                            # statistics take the sliced two-kernel path
 ]
