@@ -7,8 +7,9 @@
 // rstd in float64 -> float32 stats), apply (declared float32 sequence):
 //   a = fl(fl(s*gamma)*rstd); b = fl(s*beta); t = fl(x - mean);
 //   v = fma(t, a, b); v = fl(v + r); y = rne16(relu(v)).
-// Backward = reduce (S1 = sum g, S2 = sum g*xhat), finalize (dgamma,
-// dbeta, apply coefficients), apply (dx, dresidual).
+// Backward = reduce (S1 = sum g, T = sum g*(x - mean)), finalize (S2 =
+// rstd*T = sum g*xhat, dgamma, dbeta, apply coefficients), apply (dx,
+// dresidual).
 //
 // BN swap (Section 4.1; Geo::swap = 1): the shortcut joins before gamma,
 //   u = s * (gamma * (xhat + r) + beta), applied as
@@ -110,12 +111,15 @@ __device__ __forceinline__ float fwd_value(float x, const FwdCoef& k, bool has_r
 }
 
 // Mask of the ReLU: from the stored output when given, else recomputed bit
-// for bit with the forward sequence.
+// for bit with the forward sequence.  The stored rne16(relu(v)) is positive
+// exactly when v > 2^-25 (smaller positive values round to +0, 2^-25 itself
+// ties to the even +0; a NaN compares false either way), so the recomputed
+// mask is one float32 comparison.
 __device__ __forceinline__ bool relu_mask(bool relu, bool has_y, h16 y, float x, const FwdCoef& k,
                                           bool has_r, float r, bool swap) {
   if (!relu) return true;
   if (has_y) return to_f32(y) > 0.0f;
-  return to_f32(to_h16(fwd_value(x, k, has_r, r, true, swap))) > 0.0f;
+  return fwd_value(x, k, has_r, r, false, swap) > 0x1p-25f;
 }
 
 // ---- block reduction of NS x 8 float32 partials per thread -------------------
@@ -528,7 +532,7 @@ __global__ __launch_bounds__(kT) void bn_fwd_apply_gen(const h16* x, const h16* 
 
 // ---- backward reduce -----------------------------------------------------------
 
-// S1 = sum g, S2 = sum g*xhat; with the BN swap also S3 = sum g*r.
+// S1 = sum g, T = sum g*(x - mean); with the BN swap also S3 = sum g*r.
 template <int MODE>
 __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ x,
                                                         const h16* __restrict__ y,
@@ -549,11 +553,10 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
   int64_t row1 = row0 + rpb;
   if (row1 > g.M) row1 = g.M;
   FwdCoef k[8];
-  float rstd[8], sums[NS][8];
+  float sums[NS][8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     k[e] = fwd_coef(stats, gamma, beta, g.C, j * 8 + e, s);
-    rstd[e] = stats[g.C + j * 8 + e];
 #pragma unroll
     for (int v = 0; v < NS; ++v) sums[v][e] = 0.0f;
   }
@@ -583,9 +586,9 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
       const bool m = relu_mask(RELU, MASK_Y, MASK_Y ? b.y.h[e] : (h16)0.0f, xf, k[e], LOAD_R, rf,
                                SWAP);
       const float gg = ok && m ? s * to_f32(b.d.h[e]) : 0.0f;
-      const float xh = ok ? (xf - k[e].mean) * rstd[e] : 0.0f;
+      const float xt = ok ? xf - k[e].mean : 0.0f;
       sums[0][e] += gg;
-      sums[1][e] = __builtin_fmaf(gg, xh, sums[1][e]);
+      sums[1][e] = __builtin_fmaf(gg, xt, sums[1][e]);
       if (SWAP) sums[NS - 1][e] = __builtin_fmaf(gg, ok ? rf : 0.0f, sums[NS - 1][e]);
     }
   };
@@ -616,7 +619,6 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_gen(const h16* __restrict__ 
   int64_t j1 = j0 + rpb;
   if (j1 > g.M) j1 = g.M;
   const FwdCoef k = fwd_coef(stats, gamma, beta, g.C, c, s);
-  const float rstd = stats[g.C + c];
   const bool swap = g.swap != 0;
   const bool has_y = y != nullptr, has_r = res != nullptr && !has_y && relu;
   const bool load_r = has_r || swap;
@@ -627,9 +629,9 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_gen(const h16* __restrict__ 
     const float rf = load_r ? to_f32(res[i]) : 0.0f;
     const bool m = relu_mask(relu != 0, has_y, has_y ? y[i] : (h16)0.0f, xf, k, has_r, rf, swap);
     const float gg = m ? s * to_f32(dy[i]) : 0.0f;
-    const float xh = (xf - k.mean) * rstd;
+    const float xt = xf - k.mean;
     v[0] += gg;
-    v[1] = __builtin_fmaf(gg, xh, v[1]);
+    v[1] = __builtin_fmaf(gg, xt, v[1]);
     v[2] = __builtin_fmaf(gg, rf, v[2]);
   }
   block_reduce_1<3>(v, red);
@@ -639,24 +641,27 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_gen(const h16* __restrict__ 
   }
 }
 
-// dbeta = S1, dgamma = S2 (+ S3 with the BN swap), one rounding from float64;
-// apply coefficients A = gamma*rstd, B = S1/M, D = S2/M for
-// dx = A * (g - (xhat*D + B)).  One 64-thread block per channel.
+// S2 = rstd*T = sum g*xhat; dbeta = S1, dgamma = S2 (+ S3 with the BN swap),
+// one rounding from float64; apply coefficients A = gamma*rstd, B = S1/M and
+// D = rstd*S2/M for dx = A * (g - ((x - mean)*D + B)), which is
+// A * (g - (xhat*S2/M + S1/M)).  One 64-thread block per channel.
 __global__ __launch_bounds__(64) void bn_bwd_finalize(Geo g, int G, const float* ws,
                                                       const h16* __restrict__ gamma,
                                                       const float* __restrict__ stats, h16* dgamma,
                                                       h16* dbeta, float* coef) {
   const int c = blockIdx.x;
   const int64_t CG = (int64_t)g.C * G;
-  double S1, S2, S3 = 0.0, unused;
-  channel_sums(ws, ws + CG, c, G, S1, S2);
+  double S1, T, S3 = 0.0, unused;
+  channel_sums(ws, ws + CG, c, G, S1, T);
   if (g.swap) channel_sums(ws + 2 * CG, ws + 2 * CG, c, G, S3, unused);
   if (threadIdx.x != 0) return;
+  const double rstd = (double)stats[g.C + c];
+  const double S2 = rstd * T;
   dbeta[c] = dbl_to_h16(S1);
   dgamma[c] = dbl_to_h16(S2 + S3);
   coef[c] = to_f32(gamma[c]) * stats[g.C + c];
   coef[g.C + c] = (float)(S1 / (double)g.M);
-  coef[2 * g.C + c] = (float)(S2 / (double)g.M);
+  coef[2 * g.C + c] = (float)(rstd * S2 / (double)g.M);
 }
 
 // ---- backward apply ------------------------------------------------------------
@@ -675,12 +680,11 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* 
   const int t = threadIdx.x;
   const int j = t % CV;  // run starts and kT are multiples of CV
   FwdCoef k[8];
-  float rstd[8], A[8], B[8], D[8], gam[8];
+  float A[8], B[8], D[8], gam[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) {
     const int c = j * 8 + e;
     k[e] = fwd_coef(stats, gamma, beta, g.C, c, s);
-    rstd[e] = stats[g.C + c];
     A[e] = coef[c];
     B[e] = coef[g.C + c];
     D[e] = coef[2 * g.C + c];
@@ -711,8 +715,7 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* 
         const bool m = relu_mask(RELU, MASK_Y, MASK_Y ? yv[u].h[e] : (h16)0.0f, xf, k[e], NEED_R,
                                  NEED_R ? to_f32(rv[u].h[e]) : 0.0f, SWAP);
         const float gg = m ? s * to_f32(dv[u].h[e]) : 0.0f;
-        const float xh = (xf - k[e].mean) * rstd[e];
-        o.h[e] = to_h16(A[e] * (gg - __builtin_fmaf(xh, D[e], B[e])));
+        o.h[e] = to_h16(A[e] * (gg - __builtin_fmaf(xf - k[e].mean, D[e], B[e])));
         if (SWAP)
           od.h[e] = to_h16(gam[e] * gg);
         else
@@ -744,8 +747,7 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_gen(const h16* x, const h16* 
     const bool m = relu_mask(relu != 0, has_y, has_y ? y[i] : (h16)0.0f, xf, k, has_r,
                              has_r ? to_f32(res[i]) : 0.0f, swap);
     const float gg = m ? s * to_f32(dyv) : 0.0f;
-    const float xh = (xf - k.mean) * stats[g.C + c];
-    dx[i] = to_h16(coef[c] * (gg - __builtin_fmaf(xh, coef[2 * g.C + c], coef[g.C + c])));
+    dx[i] = to_h16(coef[c] * (gg - __builtin_fmaf(xf - k.mean, coef[2 * g.C + c], coef[g.C + c])));
     if (dres) dres[i] = swap ? to_h16(to_f32(gamma[c]) * gg) : (m ? dyv : (h16)0.0f);
   }
 }
