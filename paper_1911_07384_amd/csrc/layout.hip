@@ -76,6 +76,78 @@ __global__ void dgrad_filter_kernel(const h16* __restrict__ w, h16* __restrict__
   }
 }
 
+// All stride phases of the data-gradient filter in one launch, as 64 x 64
+// (channel x filter) tile transposes through LDS: block (c tile, k tile, tap)
+// reads 64 rows of 64 consecutive channels of W (one filter k each, 16-byte
+// loads when the channel count allows) and writes 64 rows of 64 consecutive
+// k of dst (one channel each, 16-byte stores).
+// The tap table maps each source tap (r, s) to its phase filter and its
+// position (tr, ts) there.
+constexpr int kMaxTaps = 64;
+struct DgradTaps {
+  int64_t off[kMaxTaps];  // element offset of the tap's phase filter in dst
+  int ntr[kMaxTaps], nts[kMaxTaps], tr[kMaxTaps], ts[kMaxTaps], r[kMaxTaps], s[kMaxTaps];
+};
+
+__global__ __launch_bounds__(256) void dgrad_filter_tiled(const h16* __restrict__ w,
+                                                          h16* __restrict__ dst, int K, int C,
+                                                          int R, int S, int Cw, int Kp,
+                                                          const DgradTaps taps) {
+  __shared__ h16 tile[64][66];  // [channel][k]
+  const int q = blockIdx.z;
+  const int c0 = blockIdx.x * 64, k0 = blockIdx.y * 64;
+  const int t = threadIdx.x;
+  const int r = taps.r[q], s = taps.s[q];
+  if (Cw % 8 == 0) {
+    // 16-byte loads, both of a thread's in flight together
+    V8 v[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int ci = t + 256 * q, kk = ci >> 3, c = c0 + (ci & 7) * 8;
+      const int k = k0 + kk;
+      if (k < K && c < C) {
+        v[q] = load16(w + (((int64_t)k * R + r) * S + s) * Cw + c);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) v[q].s[e] = 0;
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int ci = t + 256 * q, kk = ci >> 3, cc = (ci & 7) * 8;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) tile[cc + e][kk] = v[q].h[e];
+    }
+  } else {
+    const int cc = t & 63;
+    const int c = c0 + cc;
+    h16 v[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int k = k0 + (t >> 6) + 4 * i;
+      v[i] = (k < K && c < C) ? w[(((int64_t)k * R + r) * S + s) * Cw + c] : (h16)0.0f;
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) tile[cc][(t >> 6) + 4 * i] = v[i];
+  }
+  __syncthreads();
+  const int cc = t >> 2, kq = (t & 3) * 16;
+  const int c = c0 + cc;
+  if (c >= C) return;
+  h16* row = dst + taps.off[q] +
+             (((int64_t)c * taps.ntr[q] + taps.tr[q]) * taps.nts[q] + taps.ts[q]) * Kp;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const int k = k0 + kq + h * 8;
+    if (k < Kp) {  // Kp % 8 == 0: the 8 values stay inside the row
+      V8 v;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v.h[e] = tile[cc][kq + h * 8 + e];
+      store16(row + k, v);
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_nchw_to_nhwc(const h16* src, h16* dst, int N, int C, int HW, int Cp,
@@ -101,6 +173,33 @@ hipError_t launch_pad_channels(const h16* src, h16* dst, int64_t P, int C, int C
 hipError_t launch_dgrad_filter(const h16* w, h16* dst, int K, int C, int R, int S, int Cw, int Kp,
                                int sh, int sw, int pad_h, int pad_w, hipStream_t st) {
   // phases in (ph, pw) row-major order, each filter packed after the previous
+  if (R * S <= kMaxTaps && Kp % 8 == 0) {
+    DgradTaps taps;
+    int n = 0;
+    int64_t off = 0;
+    for (int ph = 0; ph < sh; ++ph) {
+      for (int pw = 0; pw < sw; ++pw) {
+        const DgradPhase d = dgrad_phase(ph, pw, 1, 1, R, S, sh, sw, pad_h, pad_w);
+        for (int tr = 0; tr < d.ntr; ++tr) {
+          for (int ts = 0; ts < d.nts; ++ts) {
+            taps.off[n] = off;
+            taps.ntr[n] = d.ntr;
+            taps.nts[n] = d.nts;
+            taps.tr[n] = tr;
+            taps.ts[n] = ts;
+            taps.r[n] = d.r0 + sh * (d.ntr - 1 - tr);
+            taps.s[n] = d.s0 + sw * (d.nts - 1 - ts);
+            ++n;
+          }
+        }
+        off += (int64_t)C * d.ntr * d.nts * Kp;
+      }
+    }
+    if (n == 0) return hipSuccess;
+    hipLaunchKernelGGL(dgrad_filter_tiled, dim3((C + 63) / 64, (Kp + 63) / 64, n), dim3(256), 0, st,
+                       w, dst, K, C, R, S, Cw, Kp, taps);
+    return hipGetLastError();
+  }
   int64_t off = 0;
   for (int ph = 0; ph < sh; ++ph) {
     for (int pw = 0; pw < sw; ++pw) {
