@@ -818,9 +818,13 @@ struct Cfg7 {
   static constexpr int LDS = S * STAGE > EPI + STAT ? S * STAGE : EPI + STAT;
 };
 
-template <int TM, int TN, int WM, int WN, int S, bool STATS>
+// TRANS (without statistics): the MFMA operands are swapped so that the
+// accumulators hold the transposed tile, and the epilogue writes straight from
+// registers after lane-half swaps, as pw_kernel does (no LDS staging).
+template <int TM, int TN, int WM, int WN, int S, bool STATS, bool TRANS = !STATS>
 __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
   using K = Cfg7<TM, TN, WM, WN, S>;
+  static_assert(!(STATS && TRANS), "statistics are taken from the staged tile");
   constexpr int BM = K::BM, BN = K::BN, IA = K::IA, IB = K::IB;
   static_assert(WM * WN == 4 && IA >= 1 && IB >= 1 && S >= 2, "tile shape");
   static_assert(K::Q * (S - 1) < 64, "vmcnt range");
@@ -938,7 +942,9 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
 #pragma unroll
-      for (int tn = 0; tn < TN; ++tn) acc[tm][tn] = mfma32x32x16(fa[tm], fb[tn], acc[tm][tn]);
+      for (int tn = 0; tn < TN; ++tn)
+        acc[tm][tn] = TRANS ? mfma32x32x16(fb[tn], fa[tm], acc[tm][tn])
+                            : mfma32x32x16(fa[tm], fb[tn], acc[tm][tn]);
   };
 
   const int KT = (Kg + 63) / 64;
@@ -970,6 +976,73 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
     mma(af[1], bf[1]);
   }
   __builtin_amdgcn_s_waitcnt(0);
+  if (TRANS) {
+    // lane: output pixel m (lane % 32 of each 32-row tile) and, after the
+    // swaps, channels 16h + 8*(lane/32) + 0..7 of each 32-channel tile
+    V8 adv[TM][TN][2];
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) {
+      const int m = m0 + wm * 32 * TM + tm * 32 + lrow;
+      int64_t base = 0;
+      if (m < M) {
+        const int img = m / HoWo;
+        const int rem = m - img * HoWo;
+        const int i = rem / ph.Wo;
+        const int j = rem - i * ph.Wo;
+        base = ((int64_t)(img * a.OH + i * a.os_h + ph.oph) * a.OW + j * a.os_w + ph.opw) * a.ldo;
+      }
+      if (a.addend && (a.ldo % 8) == 0) {
+        // the addend first, so its loads overlap the swaps and conversions
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int n = n0 + wn * 32 * TN + tn * 32 + h * 16 + lhi * 8;
+            if (m < M && n + 8 <= a.Co) adv[tm][tn][h] = load16(a.addend + base + n);
+          }
+      }
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        float v[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) v[e] = acc[tm][tn][e];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          lane_half_swap(v[q], v[4 + q]);
+          lane_half_swap(v[8 + q], v[12 + q]);
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int n = n0 + wn * 32 * TN + tn * 32 + h * 16 + lhi * 8;
+          if (m >= M || n >= a.Co) continue;
+          const int64_t off = base + n;
+          if ((a.ldo % 8) == 0 && n + 8 <= a.Co) {
+            float w[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) w[e] = v[h * 8 + e];
+            if (a.addend) {
+#pragma unroll
+              for (int e = 0; e < 8; ++e) w[e] += to_f32(adv[tm][tn][h].h[e]);
+            }
+            V8 o;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o.h[e] = to_h16(w[e]);
+            store16(a.out + off, o);
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              if (n + e < a.Co) {
+                float x = v[h * 8 + e];
+                if (a.addend) x += to_f32(a.addend[off + e]);
+                a.out[off + e] = to_h16(x);
+              }
+            }
+          }
+        }
+      }
+    }
+    return;
+  }
   __syncthreads();
 
   float* stg = reinterpret_cast<float*>(lds) + wave * 32 * K::SP;
