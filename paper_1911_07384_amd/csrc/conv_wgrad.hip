@@ -244,7 +244,11 @@ __global__ __launch_bounds__(256) void wgrad7_kernel(const WgradArgs a) {
   // DMA roles: instruction i of this wave fills sub-tile i/2, pixel rows
   // rb*8 .. rb*8+7 with rb = 4*(i%2) + wave; a lane covers pixel row
   // rb*8 + lane/8 and physical chunk lane%8, holding logical chunk
-  // (lane%8) ^ swz(row), swz(row) = 2*((row/2)%4)
+  // (lane%8) ^ swz(row), swz(row) = 2*(row%4).  A transposing read takes
+  // 32 bytes (chunks 2i, 2i+1) from each of 4 consecutive rows per 16-lane
+  // group; with this swizzle the 4 rows' pairs land on distinct chunk
+  // positions, and the two groups served together (the other channel
+  // half) on the rest, so the reads are bank-conflict free.
   int prow[2], img[2], pp[2], qq[2];
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
@@ -259,7 +263,7 @@ __global__ __launch_bounds__(256) void wgrad7_kernel(const WgradArgs a) {
   const int dq = 64 % a.Q, dp = (64 / a.Q) % a.P, dimg = 64 / (a.P * a.Q);
   int lc[2];
 #pragma unroll
-  for (int h = 0; h < 2; ++h) lc[h] = (lane & 7) ^ (((prow[h] >> 1) & 3) << 1);
+  for (int h = 0; h < 2; ++h) lc[h] = (lane & 7) ^ ((prow[h] & 3) << 1);
   // CGEN (C a multiple of 8 but not of 64): a 64-column block of the x patch
   // spans several filter taps, so each lane's 8-channel chunk has a tap of its
   // own; precomputed here (tap row, tap column, channel offset; -1 past Nw)
@@ -349,8 +353,8 @@ __global__ __launch_bounds__(256) void wgrad7_kernel(const WgradArgs a) {
     const int ch = c + ch_l;
     const int lcn = ch >> 3, hf = (ch >> 2) & 1;
     const int kr0 = ks * 16 + kr_l, kr1 = kr0 + 4;
-    const short4v v0 = ldtr(sb + kr0 * 128 + ((lcn ^ (((kr0 >> 1) & 3) << 1)) << 4) + hf * 8);
-    const short4v v1 = ldtr(sb + kr1 * 128 + ((lcn ^ (((kr1 >> 1) & 3) << 1)) << 4) + hf * 8);
+    const short4v v0 = ldtr(sb + kr0 * 128 + ((lcn ^ ((kr0 & 3) << 1)) << 4) + hf * 8);
+    const short4v v1 = ldtr(sb + kr1 * 128 + ((lcn ^ ((kr1 & 3) << 1)) << 4) + hf * 8);
     // (one shuffle and one bit cast: element-wise insertion of the two
     // halves was miscompiled into a broadcast of the first element)
     return __builtin_bit_cast(half8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
