@@ -787,6 +787,188 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
   }
 }
 
+// ---- 3x3 stride-1 convolutions over 64 channels ---------------------------------
+// A 3x3 layer with 64 input and 64 output channels (ResNet-50's conv2_x, and
+// its data gradient) has a reduction of only 576, and the implicit-GEMM
+// kernels above fetch every input pixel once per tap from L2 (9x) for a
+// 64-wide output: they keep the matrix cores 14-17% busy.  Here:
+//  - the whole 64 x 576 filter (72 KB) stays in LDS (16-byte chunks XOR-
+//    swizzled by row/2 within each tap) and each workgroup (one per CU, eight
+//    waves) walks over tiles of 256 consecutive output pixels of one image;
+//  - a tile's input rows with their one-pixel halo (zeros outside the image)
+//    are staged in LDS once, pixel-major, 128 bytes per pixel with chunks
+//    XOR-swizzled by pixel/2; the nine taps read shifted windows of it.
+//    (The 16 lanes an LDS cycle serves read 16 consecutive pixels or filter
+//    rows: 128-byte rows fall into two 128-byte bank halves by parity, and
+//    the swizzle by row/2 spreads each half's 8 rows over its 8 chunks.  A
+//    swizzle by the row itself left 2-way conflicts on every read);
+//  - the next tile's rows are loaded into registers while the current tile
+//    is computed, and written to LDS after it;
+//  - each wave computes 32 pixels x 64 channels with the operands swapped
+//    (D = W x X^T), reading the fragments of step i+2 while the MFMAs of step
+//    i run, and writes from registers after lane-half swaps, as pw_kernel
+//    does.
+// Same k order (tap, then channel) and the same exact products as the other
+// kernels, so the values are bit-identical.
+constexpr int kC3Tile = 256;                      // output pixels per tile
+constexpr int kC3Thr = 512;                       // threads per workgroup
+constexpr int kC3Filt = 64 * 576 * 2;             // resident filter, bytes
+constexpr int kC3HaloPix = 684;                   // staged input pixels (W <= 112)
+constexpr int kC3Pref = (kC3HaloPix * 8 + kC3Thr - 1) / kC3Thr;  // chunks per thread
+
+struct C3Geo {
+  int img, p0, oh0, rows;  // tile: image, first pixel, first output row, staged input rows
+};
+__device__ __forceinline__ C3Geo c3_geo(int tile, int tpi, int H, int W) {
+  C3Geo g;
+  g.img = tile / tpi;
+  g.p0 = (tile - g.img * tpi) * kC3Tile;
+  const int HW = H * W;
+  const int last = g.p0 + kC3Tile - 1 < HW ? g.p0 + kC3Tile - 1 : HW - 1;
+  g.oh0 = g.p0 / W;
+  g.rows = last / W - g.oh0 + 3;
+  return g;
+}
+
+__global__ __launch_bounds__(kC3Thr) void c3_kernel(const IgemmArgs a, int tpi, int ntiles) {
+  __shared__ __attribute__((aligned(1024))) char lds[kC3Filt + kC3HaloPix * 128];
+  char* filt = lds;
+  char* halo = lds + kC3Filt;
+  const IgemmPhase ph = a.ph[0];
+  const int H = a.Hi, W = a.Wi, HW = H * W, W2 = W + 2;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const int lrow = lane & 31, lhi = lane >> 5;
+  constexpr uint32_t OOB = 0x80000000u;
+  const int act_bytes = (int)((int64_t)a.N * HW * 64 * 2);
+  const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<h16*>(a.act), (short)0, act_bytes, 0x00020000);
+
+  // filter: row n, chunk c (of 72: tap*8 + channel chunk) at
+  // (c & ~7) | ((c ^ (n >> 1)) & 7)
+  for (int i = tid; i < 64 * 72; i += kC3Thr) {
+    const int n = i / 72, c = i - n * 72;
+    const V8 v = load16(ph.filt + (int64_t)n * ph.ldb + c * 8);
+    *reinterpret_cast<V8*>(filt + (n * 72 + ((c & ~7) | ((c ^ (n >> 1)) & 7))) * 16) = v;
+  }
+
+  // a tile's staged input: pixel q = row*(W+2) + col of input rows oh0-1 ..,
+  // columns -1 .. W; chunk j of it at (q*8 + (j ^ ((q >> 1) & 7)))*16
+  V8 pf[kC3Pref];
+  auto prefetch = [&](int tile) {
+    const C3Geo g = c3_geo(tile < ntiles ? tile : 0, tpi, H, W);
+    const int total = g.rows * W2 * 8;
+#pragma unroll
+    for (int i = 0; i < kC3Pref; ++i) {
+      const int q = tid + kC3Thr * i;
+      const int pix = q >> 3, j = q & 7;
+      const int hr = pix / W2, hc = pix - hr * W2;
+      const int ir = g.oh0 - 1 + hr, ic = hc - 1;
+      const bool v = tile < ntiles && q < total && (unsigned)ir < (unsigned)H &&
+                     (unsigned)ic < (unsigned)W;
+      const uint32_t off = (uint32_t)((((g.img * H + ir) * W + ic) * 64 + j * 8) * 2);
+      pf[i].u = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rs_a, v ? off : OOB, 0, 0));
+    }
+  };
+  auto stage = [&](int tile) {
+    const C3Geo g = c3_geo(tile, tpi, H, W);
+    const int total = g.rows * W2 * 8;
+#pragma unroll
+    for (int i = 0; i < kC3Pref; ++i) {
+      const int q = tid + kC3Thr * i;
+      if (q < total) {
+        const int pix = q >> 3, j = q & 7;
+        *reinterpret_cast<V8*>(halo + (pix * 8 + (j ^ ((pix >> 1) & 7))) * 16) = pf[i];
+      }
+    }
+  };
+
+  int tile = blockIdx.x;
+  prefetch(tile);
+  stage(tile);
+  __syncthreads();
+  for (; tile < ntiles; tile += gridDim.x) {
+    const C3Geo g = c3_geo(tile, tpi, H, W);
+    prefetch(tile + gridDim.x);
+    // this lane's pixel, clamped into the image for the addresses (a pixel
+    // past the end is not stored)
+    const int m = g.p0 + wave * 32 + lrow;
+    int hp0;
+    {
+      const int mc = m < HW ? m : HW - 1;
+      const int oh = mc / W, ow = mc - oh * W;
+      hp0 = (oh - g.oh0) * W2 + ow;
+    }
+    floatx16 acc[2];
+#pragma unroll
+    for (int tn = 0; tn < 2; ++tn)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) acc[tn][e] = 0.0f;
+    // step i = tap*4 + ks: the pixel fragment and the two filter fragments
+    half8 xa[3], fb[3][2];
+    auto fetch = [&](int i, int buf) {
+      const int tap = i >> 2, ks = i & 3;
+      const int j = ks * 2 + lhi;
+      const int hp = hp0 + (tap / 3) * W2 + tap % 3;
+      xa[buf] = *reinterpret_cast<const half8*>(halo + (hp * 8 + (j ^ ((hp >> 1) & 7))) * 16);
+#pragma unroll
+      for (int tn = 0; tn < 2; ++tn) {
+        const int n = tn * 32 + lrow;
+        fb[buf][tn] =
+            *reinterpret_cast<const half8*>(filt + (n * 72 + tap * 8 + ((j ^ (n >> 1)) & 7)) * 16);
+      }
+    };
+    fetch(0, 0);
+    fetch(1, 1);
+#pragma unroll
+    for (int i = 0; i < 36; ++i) {
+      if (i + 2 < 36) fetch(i + 2, (i + 2) % 3);
+#pragma unroll
+      for (int tn = 0; tn < 2; ++tn) acc[tn] = mfma32x32x16(fb[i % 3][tn], xa[i % 3], acc[tn]);
+    }
+    __syncthreads();  // every wave is done with this tile's staged rows
+    // lane: pixel m, channels 16h + 8*(lane/32) + 0..7 of each 32-channel tile
+#pragma unroll
+    for (int tn = 0; tn < 2; ++tn) {
+      float v[16];
+#pragma unroll
+      for (int e = 0; e < 16; ++e) v[e] = acc[tn][e];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        lane_half_swap(v[q], v[4 + q]);
+        lane_half_swap(v[8 + q], v[12 + q]);
+      }
+      if (m < HW) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          V8 o;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o.h[e] = to_h16(v[h * 8 + e]);
+          store16(a.out + ((int64_t)g.img * HW + m) * a.ldo + tn * 32 + h * 16 + lhi * 8, o);
+        }
+      }
+    }
+    if (tile + gridDim.x < ntiles) stage(tile + gridDim.x);
+    __syncthreads();
+  }
+}
+
+// Whether the 3x3 kernel takes this problem; tiles per image if so.
+int c3_tiles_per_image(const IgemmArgs& a) {
+  const IgemmPhase& p = a.ph[0];
+  if (a.f16acc || a.stat || a.addend || a.nphase != 1 || p.Rt != 3 || p.St != 3 ||
+      a.stride_h != 1 || a.stride_w != 1 || p.pad_h != 1 || p.pad_w != 1 || a.Ci != 64 ||
+      a.Co != 64 || p.ldb != 576 || p.Ho != a.Hi || p.Wo != a.Wi || a.OH != p.Ho ||
+      a.OW != p.Wo || a.os_h != 1 || a.os_w != 1 || p.oph != 0 || p.opw != 0 || a.ldo != 64)
+    return 0;
+  const int W = a.Wi;
+  if (W < 1 || a.Hi < 1) return 0;
+  const int rows = 1 + (W + kC3Tile - 2) / W + 2;  // most input rows a tile stages
+  if ((int64_t)rows * (W + 2) > kC3HaloPix) return 0;
+  if ((int64_t)a.N * a.Hi * a.Wi * 64 * 2 >= ((int64_t)1 << 31)) return 0;
+  return (a.Hi * a.Wi + kC3Tile - 1) / kC3Tile;
+}
+
 // ---- k-step 64, whole 128-byte operand rows, fragment reads one sub-step ahead
 // As igemm6, with a k-step of 64 channels: every operand row of a stage is one
 // whole 128-byte line (8 lanes x 16 bytes per row, 8 rows per 1 KB DMA
@@ -1194,6 +1376,14 @@ hipError_t launch_cfg4(const IgemmArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+hipError_t launch_c3(const IgemmArgs& a, int tpi, hipStream_t st) {
+  const int ntiles = a.N * tpi;
+  if (ntiles == 0) return hipSuccess;
+  hipLaunchKernelGGL(c3_kernel, dim3(ntiles < 256 ? ntiles : 256), dim3(kC3Thr), 0, st, a, tpi,
+                     ntiles);
+  return hipGetLastError();
+}
+
 template <int CI, int BN>
 hipError_t launch_pw(const IgemmArgs& a, hipStream_t st) {
   const int M = a.N * a.ph[0].Ho * a.ph[0].Wo;
@@ -1227,7 +1417,7 @@ hipError_t launch_cfg(const IgemmArgs& a, hipStream_t st) {
 
 namespace {
 
-enum class IgemmKind { kLds, kDirect, kDma, kPointwise };
+enum class IgemmKind { kLds, kDirect, kDma, kPointwise, k3x3 };
 
 // Kernel choice per problem (measured on MI355X over the ResNet-50 shapes at
 // batch 32 and 128): the pointwise kernel for 1x1 filters over 64 or 128
@@ -1237,6 +1427,7 @@ enum class IgemmKind { kLds, kDirect, kDma, kPointwise };
 // else the LDS-staged one.  All four give identical bits.
 IgemmKind igemm_kind(const IgemmArgs& a) {
   if (a.f16acc) return IgemmKind::kLds;
+  if (c3_tiles_per_image(a) > 0) return IgemmKind::k3x3;
   {
     // a 1x1 filter over 64 or 128 channels with a dense output of 128+
     // channels: the pointwise kernel
@@ -1269,7 +1460,13 @@ IgemmKind igemm_kind(const IgemmArgs& a) {
 
 }  // namespace
 
-bool igemm_takes_stats(const IgemmArgs& a) { return igemm_kind(a) != IgemmKind::kLds; }
+bool igemm_takes_stats(const IgemmArgs& a) {
+  // the kernel that would run with statistics requested (the 3x3 kernel
+  // leaves them to the DMA-staged one)
+  IgemmArgs b = a;
+  b.stat = reinterpret_cast<float*>(1);
+  return igemm_kind(b) != IgemmKind::kLds;
+}
 
 hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st) {
   if (a.f16acc)
@@ -1288,6 +1485,8 @@ hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st) {
     }
     case IgemmKind::kDirect:
       return a.Co <= 64 ? launch_cfg4<1, 2>(a, st) : launch_cfg4<1, 4>(a, st);
+    case IgemmKind::k3x3:
+      return launch_c3(a, c3_tiles_per_image(a), st);
     case IgemmKind::kPointwise:
       if (a.Ci == 64) return a.Co >= 256 ? launch_pw<64, 256>(a, st) : launch_pw<64, 128>(a, st);
       return launch_pw<128, 256>(a, st);
