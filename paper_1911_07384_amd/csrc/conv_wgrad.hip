@@ -17,6 +17,8 @@
 
 #include "kernels.hpp"
 
+#include <type_traits>
+
 namespace fp16k {
 namespace {
 
@@ -197,13 +199,32 @@ __device__ __forceinline__ void wdma16(__amdgpu_buffer_rsrc_t rs, char* lds_dst,
                                            voff, 0, 0, 0);
 }
 
-// Four binary16 values from the transposing LDS read.
-__device__ __forceinline__ short4v ldtr(const char* p) {
-  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-      (__attribute__((address_space(3))) short4v*)(const_cast<char*>(p)));
-}
-
 __device__ __forceinline__ void wbarrier() { __asm__ volatile("s_barrier" ::: "memory"); }
+
+// The transposing read, issued from inline assembly at an LDS byte address
+// plus a constant offset.  Through the compiler's builtin, every such read
+// waits for all LDS DMAs in flight (the compiler cannot tell the buffers
+// apart), so the stage just issued had to land before the next stage could be
+// read; from assembly the ring keeps its stages in flight (5-15 % faster on
+// the ResNet-50 shapes, bit-identical partials).  The compiler then neither
+// orders the read after the DMAs nor waits for its result: the loop orders
+// the DMAs by its own vmcnt wait and barrier, and each result by lds_ready()
+// before the MFMAs that use it.  Nothing may read the destination registers
+// before that wait (not even a register copy); a host-side test checks the
+// built code for it.
+template <int OFF>
+__device__ __forceinline__ short4v ldtr_asm(uint32_t addr) {
+  short4v r;
+  __asm__ volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+// Waits until at most N LDS reads of this wave are in flight; the fragment is
+// tied to the wait so that no use of it is scheduled before.
+template <int N>
+__device__ __forceinline__ void lds_ready(half8& v) {
+  __asm__ volatile("s_waitcnt lgkmcnt(%1)" : "+v"(v) : "i"(N));
+}
+__device__ __forceinline__ void lds_tie(half8& v) { __asm__ volatile("" : "+v"(v)); }
 
 template <int BM, int BN, int WM, int WN, int S>
 struct WCfg7 {
@@ -226,9 +247,21 @@ __global__ __launch_bounds__(256) void wgrad7_kernel(const WgradArgs a) {
 
   const int Nw = a.R * a.S * a.C;
   const int tiles_n = (Nw + BN - 1) / BN;
-  const int m0 = (blockIdx.x / tiles_n) * BM;
-  const int n0 = (blockIdx.x % tiles_n) * BN;
-  const int split = blockIdx.y;
+  // Workgroups are dealt to the 8 XCDs round-robin in launch order.  Each
+  // XCD gets a contiguous run of the split-major order instead, so the tiles
+  // that share a pixel range (and so its dy and x rows) share one L2: the
+  // layers with 28x28 and larger grids at batch 128 went 1.1-1.9x faster.
+  int tile, split;
+  {
+    const int total = gridDim.x * gridDim.y;
+    const int L = blockIdx.y * gridDim.x + blockIdx.x;
+    const int q = total >> 3, r = total & 7, xcd = L & 7;
+    const int Lg = xcd * q + (xcd < r ? xcd : r) + (L >> 3);
+    tile = Lg % gridDim.x;
+    split = Lg / gridDim.x;
+  }
+  const int m0 = (tile / tiles_n) * BM;
+  const int n0 = (tile % tiles_n) * BN;
   const int64_t npix = (int64_t)a.N * a.P * a.Q;
   const int64_t pbeg = (int64_t)split * a.pix_per_split;
   int64_t pend = pbeg + a.pix_per_split;
@@ -347,31 +380,7 @@ __global__ __launch_bounds__(256) void wgrad7_kernel(const WgradArgs a) {
 #pragma unroll
       for (int e = 0; e < 16; ++e) acc[tm][tn][e] = 0.0f;
 
-  // operand of 32 channels starting at channel `c` of a 64-channel region
-  // (sub-tile base `sb`), pixels ks*16 .. ks*16+15 of the stage
-  auto operand = [&](const char* sb, int c, int ks) {
-    const int ch = c + ch_l;
-    const int lcn = ch >> 3, hf = (ch >> 2) & 1;
-    const int kr0 = ks * 16 + kr_l, kr1 = kr0 + 4;
-    const short4v v0 = ldtr(sb + kr0 * 128 + ((lcn ^ ((kr0 & 3) << 1)) << 4) + hf * 8);
-    const short4v v1 = ldtr(sb + kr1 * 128 + ((lcn ^ ((kr1 & 3) << 1)) << 4) + hf * 8);
-    // (one shuffle and one bit cast: element-wise insertion of the two
-    // halves was miscompiled into a broadcast of the first element)
-    return __builtin_bit_cast(half8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
-  };
   half8 af[2][TM], bf[2][TN];
-  auto fetch = [&](const char* buf, int ks, half8 (&fa)[TM], half8 (&fb)[TN]) {
-#pragma unroll
-    for (int tm = 0; tm < TM; ++tm) {
-      const int c = wm * WTM + tm * 32;
-      fa[tm] = operand(buf + (c >> 6) * 8192, c & 63, ks);
-    }
-#pragma unroll
-    for (int tn = 0; tn < TN; ++tn) {
-      const int c = wn * WTN + tn * 32;
-      fb[tn] = operand(buf + (SA + (c >> 6)) * 8192, c & 63, ks);
-    }
-  };
   auto mma = [&](const half8 (&fa)[TM], const half8 (&fb)[TN]) {
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm)
@@ -380,6 +389,47 @@ __global__ __launch_bounds__(256) void wgrad7_kernel(const WgradArgs a) {
   };
 
   if (KT > 0) {
+    // lane part of each operand's read address (the swizzle depends on the
+    // pixel row mod 4, which k sub-steps of 16 rows and the +4 row of the
+    // second read leave unchanged): sub-step ks of a stage is at +2048*ks,
+    // the second read at +512
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)lds;
+    uint32_t oa[TM], ob[TN];
+    auto lane_part = [&](int c) {
+      const int ch = (c & 63) + ch_l;
+      return (uint32_t)((c >> 6) * 8192 + kr_l * 128 + (((ch >> 3) ^ ((kr_l & 3) << 1)) << 4) +
+                        ((ch >> 2) & 1) * 8);
+    };
+#pragma unroll
+    for (int tm = 0; tm < TM; ++tm) oa[tm] = lds0 + lane_part(wm * WTM + tm * 32);
+#pragma unroll
+    for (int tn = 0; tn < TN; ++tn) ob[tn] = lds0 + SA * 8192 + lane_part(wn * WTN + tn * 32);
+    constexpr int NR = 2 * (TM + TN);  // reads per sub-step
+    static_assert(NR <= 15, "lgkmcnt range");
+    auto afetch = [&](auto ks, uint32_t sbase, half8(&fa)[TM], half8(&fb)[TN]) {
+      constexpr int KS = decltype(ks)::value;
+#pragma unroll
+      for (int tm = 0; tm < TM; ++tm) {
+        const short4v v0 = ldtr_asm<KS * 2048>(oa[tm] + sbase);
+        const short4v v1 = ldtr_asm<KS * 2048 + 512>(oa[tm] + sbase);
+        fa[tm] = __builtin_bit_cast(half8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) {
+        const short4v v0 = ldtr_asm<KS * 2048>(ob[tn] + sbase);
+        const short4v v1 = ldtr_asm<KS * 2048 + 512>(ob[tn] + sbase);
+        fb[tn] = __builtin_bit_cast(half8, __builtin_shufflevector(v0, v1, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+    };
+    // the fragments of one sub-step are complete once at most NR reads (those
+    // of the next sub-step, issued after them) are in flight
+    auto ready = [&](half8(&fa)[TM], half8(&fb)[TN]) {
+      lds_ready<NR>(fa[0]);
+#pragma unroll
+      for (int tm = 1; tm < TM; ++tm) lds_tie(fa[tm]);
+#pragma unroll
+      for (int tn = 0; tn < TN; ++tn) lds_tie(fb[tn]);
+    };
 #pragma unroll
     for (int s = 0; s < S; ++s) issue(lds + s * K::STAGE);
     constexpr int ALLOW0 = IW * (S - 1);
@@ -388,21 +438,27 @@ __global__ __launch_bounds__(256) void wgrad7_kernel(const WgradArgs a) {
     constexpr int WAIT = (0x0 << 8) | (0x7 << 4) | (ALLOW & 0xF) | ((ALLOW >> 4) << 14);
     __builtin_amdgcn_s_waitcnt(WAIT0);
     wbarrier();
-    fetch(lds, 0, af[0], bf[0]);
+    afetch(std::integral_constant<int, 0>(), 0u, af[0], bf[0]);
     int rd = 0;
     for (int kt = 0; kt < KT; ++kt) {
-      const char* cur = lds + rd * K::STAGE;
-      fetch(cur, 1, af[1], bf[1]);
+      const uint32_t cur = (uint32_t)(rd * K::STAGE);
+      afetch(std::integral_constant<int, 1>(), cur, af[1], bf[1]);
+      ready(af[0], bf[0]);
       mma(af[0], bf[0]);
-      fetch(cur, 2, af[0], bf[0]);
+      afetch(std::integral_constant<int, 2>(), cur, af[0], bf[0]);
+      ready(af[1], bf[1]);
       mma(af[1], bf[1]);
-      fetch(cur, 3, af[1], bf[1]);
+      afetch(std::integral_constant<int, 3>(), cur, af[1], bf[1]);
+      ready(af[0], bf[0]);
       mma(af[0], bf[0]);
+      // every read of this stage is complete (lgkmcnt 0) and stage kt+1 has
+      // landed (vmcnt) in every wave before the buffer is refilled
       __builtin_amdgcn_s_waitcnt(WAIT);
       wbarrier();
       issue(lds + rd * K::STAGE);
       rd = rd + 1 == S ? 0 : rd + 1;
-      fetch(lds + rd * K::STAGE, 0, af[0], bf[0]);
+      afetch(std::integral_constant<int, 0>(), (uint32_t)(rd * K::STAGE), af[0], bf[0]);
+      ready(af[1], bf[1]);
       mma(af[1], bf[1]);
     }
     __builtin_amdgcn_s_waitcnt(0);
@@ -507,6 +563,7 @@ __global__ __launch_bounds__(256) void wgrad_reduce_vec_kernel(const float* __re
 // Tile configuration shared by the plan and the launch.
 struct WCfg {
   int BM, BN;
+  int S = 2;  // stages of the DMA ring (DMA-staged kernel)
 };
 // Larger tiles re-read less: a wider N tile reuses the dy tile over more
 // filter columns (three 3x3 taps at once for 64 output channels), a taller M
@@ -521,16 +578,35 @@ inline WCfg wgrad_cfg(int K, int Nw) {
 }
 // The DMA-staged kernel (channel counts multiples of 64) and its tiles.
 inline bool wgrad_dma(int K, int C) { return K % 64 == 0 && C % 8 == 0; }
-// (measured on the ResNet-50 shapes at batch 128: narrower tiles at higher
-// occupancy beat 128 x 128 once K >= 128)
-inline WCfg wgrad7_cfg(int K, int Nw) {
+// (measured on the ResNet-50 shapes at batch 128: 128 x 128 tiles pay once
+// the pixel count is large enough to split them over the CUs, 128 x 64 below;
+// a third ring stage pays only for the single 64-column tile)
+inline WCfg wgrad7_cfg(int K, int Nw, int64_t npix) {
+  if (K >= 128 && Nw >= 128 && npix >= 65536) return {128, 128};
+  if (K >= 128 && Nw <= 64) return {128, 64, 3};
   if (K >= 128) return {128, 64};
   if (Nw >= 256) return {64, 256};
   if (Nw >= 128) return {64, 128};
   return {64, 64};
 }
-inline WCfg wgrad_choice(int K, int C, int Nw) {
-  return wgrad_dma(K, C) ? wgrad7_cfg(K, Nw) : wgrad_cfg(K, Nw);
+inline WCfg wgrad_choice(int K, int C, int Nw, int64_t npix) {
+  return wgrad_dma(K, C) ? wgrad7_cfg(K, Nw, npix) : wgrad_cfg(K, Nw);
+}
+
+template <bool CGEN>
+void launch_wgrad7(const WCfg& cfg, dim3 grid, hipStream_t st, const WgradArgs& a) {
+  if (cfg.BM == 128 && cfg.BN == 128)
+    hipLaunchKernelGGL((wgrad7_kernel<128, 128, 2, 2, 2, CGEN>), grid, dim3(256), 0, st, a);
+  else if (cfg.BM == 128 && cfg.S == 3)
+    hipLaunchKernelGGL((wgrad7_kernel<128, 64, 2, 2, 3, CGEN>), grid, dim3(256), 0, st, a);
+  else if (cfg.BM == 128)
+    hipLaunchKernelGGL((wgrad7_kernel<128, 64, 2, 2, 2, CGEN>), grid, dim3(256), 0, st, a);
+  else if (cfg.BN == 256)
+    hipLaunchKernelGGL((wgrad7_kernel<64, 256, 1, 4, 2, CGEN>), grid, dim3(256), 0, st, a);
+  else if (cfg.BN == 128)
+    hipLaunchKernelGGL((wgrad7_kernel<64, 128, 2, 2, 2, CGEN>), grid, dim3(256), 0, st, a);
+  else
+    hipLaunchKernelGGL((wgrad7_kernel<64, 64, 2, 2, 2, CGEN>), grid, dim3(256), 0, st, a);
 }
 
 }  // namespace
@@ -544,7 +620,7 @@ void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int f16acc, int* spli
     return;
   }
   const int Nw = R * S * Cp;
-  const WCfg cfg = wgrad_choice(K, Cp, Nw);
+  const WCfg cfg = wgrad_choice(K, Cp, Nw, npix);
   const int64_t tiles = (int64_t)ceil_div(K, cfg.BM) * ceil_div(Nw, cfg.BN);
   int64_t want = (512 + tiles - 1) / tiles;           // about two workgroups per CU
   const int64_t max_splits = (npix + 2 * BKP - 1) / (2 * BKP);  // at least two k-steps each
@@ -560,7 +636,8 @@ void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int f16acc, int* spli
 
 hipError_t launch_wgrad_partial(const WgradArgs& a, hipStream_t st) {
   const int Nw = a.R * a.S * a.C;
-  const WCfg cfg = wgrad_choice(a.K, a.C, Nw);
+  const int64_t npix = (int64_t)a.N * a.P * a.Q;
+  const WCfg cfg = wgrad_choice(a.K, a.C, Nw, npix);
   const int tiles = ceil_div(a.K, cfg.BM) * ceil_div(Nw, cfg.BN);
   dim3 grid(tiles, a.splits);
   if (a.f16acc) {
@@ -578,27 +655,13 @@ hipError_t launch_wgrad_partial(const WgradArgs& a, hipStream_t st) {
       hipLaunchKernelGGL((wgrad_kernel<64, 64, 2, 2, true>), g2, dim3(256), 0, st, a);
     return hipGetLastError();
   }
-  if (wgrad_dma(a.K, a.C) && a.C % 64 != 0) {
-    // channel counts that are multiples of 8 only (the 3-channel stem, padded)
-    if (cfg.BM == 128)
-      hipLaunchKernelGGL((wgrad7_kernel<128, 64, 2, 2, 2, true>), grid, dim3(256), 0, st, a);
-    else if (cfg.BN == 256)
-      hipLaunchKernelGGL((wgrad7_kernel<64, 256, 1, 4, 2, true>), grid, dim3(256), 0, st, a);
-    else if (cfg.BN == 128)
-      hipLaunchKernelGGL((wgrad7_kernel<64, 128, 2, 2, 2, true>), grid, dim3(256), 0, st, a);
-    else
-      hipLaunchKernelGGL((wgrad7_kernel<64, 64, 2, 2, 2, true>), grid, dim3(256), 0, st, a);
-    return hipGetLastError();
-  }
   if (wgrad_dma(a.K, a.C)) {
-    if (cfg.BM == 128)
-      hipLaunchKernelGGL((wgrad7_kernel<128, 64, 2, 2, 2>), grid, dim3(256), 0, st, a);
-    else if (cfg.BN == 256)
-      hipLaunchKernelGGL((wgrad7_kernel<64, 256, 1, 4, 2>), grid, dim3(256), 0, st, a);
-    else if (cfg.BN == 128)
-      hipLaunchKernelGGL((wgrad7_kernel<64, 128, 2, 2, 2>), grid, dim3(256), 0, st, a);
+    // channel counts that are multiples of 8 only (the 3-channel stem, padded)
+    // take per-lane filter taps
+    if (a.C % 64 != 0)
+      launch_wgrad7<true>(cfg, grid, st, a);
     else
-      hipLaunchKernelGGL((wgrad7_kernel<64, 64, 2, 2, 2>), grid, dim3(256), 0, st, a);
+      launch_wgrad7<false>(cfg, grid, st, a);
     return hipGetLastError();
   }
   if (cfg.BM == 128 && cfg.BN == 128)
