@@ -56,6 +56,27 @@ __global__ void pad_channels_kernel(const h16* __restrict__ src, h16* __restrict
   }
 }
 
+// Cp a multiple of 8: one thread per pixel, 16-byte stores.  Every load is
+// unconditional (channel min(c, C - 1), then zero past C), so a thread's
+// loads are in flight together.
+__global__ void pad_channels_vec(const h16* __restrict__ src, h16* __restrict__ dst, int64_t P,
+                                 int C, int Cp) {
+  for (int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; p < P;
+       p += (int64_t)gridDim.x * blockDim.x) {
+    const h16* s = src + p * C;
+    for (int c0 = 0; c0 < Cp; c0 += 8) {
+      V8 v;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int c = c0 + e;
+        const h16 x = s[c < C ? c : C - 1];
+        v.h[e] = c < C ? x : (h16)0.0f;
+      }
+      store16(dst + p * Cp + c0, v);
+    }
+  }
+}
+
 // One stride phase of the data-gradient filter:
 // dst[c][tr][ts][k] = k < K ? W[k][r0 + sh*(ntr-1-tr)][s0 + sw*(nts-1-ts)][c] : 0.
 __global__ void dgrad_filter_kernel(const h16* __restrict__ w, h16* __restrict__ dst, int K, int C,
@@ -165,8 +186,12 @@ hipError_t launch_nhwc_to_nchw(const h16* src, h16* dst, int N, int C, int HW, i
 }
 
 hipError_t launch_pad_channels(const h16* src, h16* dst, int64_t P, int C, int Cp, hipStream_t st) {
-  hipLaunchKernelGGL(pad_channels_kernel, dim3(grid_for(P * Cp)), dim3(kThreads), 0, st, src, dst,
-                     P, C, Cp);
+  if (Cp % 8 == 0)
+    hipLaunchKernelGGL(pad_channels_vec, dim3(grid_for(P)), dim3(kThreads), 0, st, src, dst, P, C,
+                       Cp);
+  else
+    hipLaunchKernelGGL(pad_channels_kernel, dim3(grid_for(P * Cp)), dim3(kThreads), 0, st, src,
+                       dst, P, C, Cp);
   return hipGetLastError();
 }
 

@@ -180,6 +180,73 @@ __global__ __launch_bounds__(kPT) void maxpool_bwd_vec(const uint8_t* __restrict
   }
 }
 
+// The 3x3 stride-2 pad-1 pool (the ResNet stem's): a thread owns a 2x2 block
+// of input positions (rows 2a, 2a+1, columns 2b, 2b+1) and 8 channels.  The
+// windows containing them are (p, q) in {a, a+1} x {b, b+1}; each window's
+// taps and gradients are loaded once, all four before any is used (a window
+// past the last row or column is loaded clamped and contributes nothing).
+// Position (2a + i, 2b + j) receives from window (a + u, b + v) when u <= i
+// and v <= j, at tap (1 + i - 2u) * 3 + (1 + j - 2v).  At most four binary16
+// terms are added in float64, which is exact in any order.
+__global__ __launch_bounds__(kPT) void maxpool_bwd_s2(const uint8_t* __restrict__ idx,
+                                                      const h16* __restrict__ dy,
+                                                      h16* __restrict__ dx, PoolArgs a) {
+  const int CV = a.C / 8;
+  const int HB = (a.H + 1) / 2, WB = (a.W + 1) / 2;
+  const int64_t total = (int64_t)a.N * HB * WB * CV;
+  for (int64_t v = (int64_t)blockIdx.x * kPT + threadIdx.x; v < total;
+       v += (int64_t)gridDim.x * kPT) {
+    const int j = (int)(v % CV);
+    int64_t r = v / CV;
+    const int b = (int)(r % WB);
+    r /= WB;
+    const int ab = (int)(r % HB);
+    const int n = (int)(r / HB);
+    uint64_t taps[2][2];
+    V8 g[2][2];
+    bool ok[2][2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+#pragma unroll
+      for (int w = 0; w < 2; ++w) {
+        const int p = ab + u, q = b + w;
+        ok[u][w] = p < a.P && q < a.Q;
+        const int pc = p < a.P ? p : a.P - 1, qc = q < a.Q ? q : a.Q - 1;
+        const int64_t ov = (((int64_t)n * a.P + pc) * a.Q + qc) * CV + j;
+        taps[u][w] = *reinterpret_cast<const uint64_t*>(idx + ov * 8);
+        g[u][w] = load16(dy + ov * 8);
+      }
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int h = 2 * ab + i;
+#pragma unroll
+      for (int jj = 0; jj < 2; ++jj) {
+        const int wc = 2 * b + jj;
+        double acc[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+#pragma unroll
+        for (int u = 0; u <= i; ++u)
+#pragma unroll
+          for (int w = 0; w <= jj; ++w) {
+            const int t = (1 + i - 2 * u) * 3 + (1 + jj - 2 * w);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const bool hit = ok[u][w] && (int)((taps[u][w] >> (8 * e)) & 0xFF) == t;
+              acc[e] += hit ? (double)to_f32(g[u][w].h[e]) : 0.0;
+            }
+          }
+        if (h < a.H && wc < a.W) {
+          V8 o;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o.h[e] = dbl_to_h16(acc[e]);
+          store16(dx + ((((int64_t)n * a.H + h) * a.W + wc) * CV + j) * 8, o);
+        }
+      }
+    }
+  }
+}
+
 __global__ __launch_bounds__(kPT) void maxpool_bwd_gen(const uint8_t* __restrict__ idx,
                                                        const h16* __restrict__ dy,
                                                        h16* __restrict__ dx, PoolArgs a) {
@@ -311,7 +378,11 @@ hipError_t launch_maxpool_fwd(const PoolArgs& a, const h16* x, h16* y, uint8_t* 
 
 hipError_t launch_maxpool_bwd(const PoolArgs& a, const uint8_t* idx, const h16* dy, h16* dx,
                               hipStream_t st) {
-  if (vec_ok(a))
+  if (vec_ok(a) && a.R == 3 && a.S == 3 && a.sh == 2 && a.sw == 2 && a.ph == 1 && a.pw == 1)
+    hipLaunchKernelGGL(maxpool_bwd_s2,
+                       dim3(grid_for((int64_t)a.N * ((a.H + 1) / 2) * ((a.W + 1) / 2) * (a.C / 8))),
+                       dim3(kPT), 0, st, idx, dy, dx, a);
+  else if (vec_ok(a))
     hipLaunchKernelGGL(maxpool_bwd_vec, dim3(grid_for((int64_t)a.N * a.H * a.W * (a.C / 8))),
                        dim3(kPT), 0, st, idx, dy, dx, a);
   else

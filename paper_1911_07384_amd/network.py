@@ -257,13 +257,14 @@ class ResNet50:
             else:
                 self._conv_bwd(nm + ".c1", dc1, addend=dres, dx_name=dxb)
             dout = dxb
-        # max pool, stem BN (mask from its stored output), stem weights (the
-        # image gradient is not needed)
+        # max pool, stem BN (its ReLU mask recomputed from the conv output and
+        # the statistics, as for every other BN: reading the stored output
+        # instead would add 2 bytes per element to both backward passes), stem
+        # weights (the image gradient is not needed)
         dstem = self._grad("stem.bn.y")
         self.bwd.append(Op("maxpool_bwd", "pool", {"desc": pd, "idx": "pool.idx", "dy": dout,
                                                    "dx": dstem}))
         dc = self._bn_bwd("stem.bn", dstem, want_dres=False)
-        self.bwd[-1].a["y"] = "stem.bn.y"
         self._conv_bwd("stem", dc, dx_needed=False)
 
     # ---- parameters ----------------------------------------------------------------

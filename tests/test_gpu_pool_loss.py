@@ -36,6 +36,7 @@ def _maxpool_input(shape, seed, special=False):
 MAXPOOL = [  # n, c, h, w, r, stride, pad, layout, special
     (2, 64, 112, 112, 3, 2, 1, "NHWC", True),   # the ResNet-50 stem pool, batch 2
     (3, 16, 17, 13, 3, 2, 1, "NHWC", True),     # ragged sizes
+    (2, 8, 8, 10, 3, 2, 1, "NHWC", True),       # even sizes: the last block's second windows are past the edge
     (2, 3, 9, 10, 3, 2, 1, "NHWC", True),       # C not a multiple of 8
     (2, 5, 11, 9, 3, 2, 1, "NCHW", True),
     (1, 8, 6, 6, 2, 2, 0, "NHWC", False),
