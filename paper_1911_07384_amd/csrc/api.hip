@@ -113,6 +113,18 @@ ConvWs conv_ws(const ConvDims& d, int pass) {
   return L;
 }
 
+// Arguments of the stem kernel: the unpadded NHWC input and KRSC filter.
+IgemmArgs stem_args(const ConvDims& d, const h16* x, const h16* w, h16* y) {
+  IgemmArgs a{};
+  a.act = x; a.N = d.N; a.Hi = d.H; a.Wi = d.W; a.Ci = d.C;
+  a.stride_h = d.sh; a.stride_w = d.sw;
+  a.Co = d.K; a.out = y; a.OH = d.P; a.OW = d.Q; a.ldo = d.K; a.os_h = 1; a.os_w = 1;
+  a.nphase = 1;
+  a.f16acc = d.accum;
+  a.ph[0] = IgemmPhase{w, d.R * d.S * d.C, d.R, d.S, d.ph, d.pw, d.P, d.Q, 0, 0};
+  return a;
+}
+
 fp16_status hip_status(hipError_t e) { return e == hipSuccess ? FP16_OK : FP16_ERR_HIP; }
 
 #define TRY(expr)                                  \
@@ -185,6 +197,11 @@ fp16_status fp16_conv_fwd(const fp16_conv_desc* desc, const fp16_t* x, const fp1
   const h16* xe = reinterpret_cast<const h16*>(x);
   const h16* we = reinterpret_cast<const h16*>(w);
   h16* ye = reinterpret_cast<h16*>(y);
+  if (d.layout == FP16_NHWC) {
+    // the ResNet stem reads the unpadded image on its own kernel
+    const IgemmArgs sa = stem_args(d, xe, we, ye);
+    if (stem_conv_ok(sa)) return hip_status(launch_stem(sa, st));
+  }
   if (d.layout == FP16_NCHW) {
     TRY(launch_nchw_to_nhwc(xe, wsp(ws, L.x), d.N, d.C, d.H * d.W, d.Cp, st));
     TRY(launch_nchw_to_nhwc(we, wsp(ws, L.w), d.K, d.C, d.R * d.S, d.Cp, st));
@@ -636,13 +653,30 @@ fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc
   const ConvWs L = conv_ws(d, FP16_PASS_FWD);
   const h16* xe = reinterpret_cast<const h16*>(x);
   const h16* we = reinterpret_cast<const h16*>(w);
+  float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + conv_bn_band_off(d));
+  {
+    // the ResNet stem: its own kernel, on the unpadded image
+    IgemmArgs sa = stem_args(d, xe, we, reinterpret_cast<h16*>(y));
+    sa.stat = part;
+    sa.stat_nb = conv_bn_nb(d);
+    if (stem_conv_ok(sa)) {
+      TRY(launch_stem(sa, st));
+      void* band_ws = reinterpret_cast<char*>(part) +
+                      align256((size_t)3 * d.K * sa.stat_nb * sizeof(float));
+      return hip_status(launch_bn_fwd_bands(b, part, sa.stat_nb, band_ws,
+                                            reinterpret_cast<const h16*>(y),
+                                            reinterpret_cast<const h16*>(gamma),
+                                            reinterpret_cast<const h16*>(beta),
+                                            reinterpret_cast<const h16*>(residual),
+                                            reinterpret_cast<h16*>(z), stats, st));
+    }
+  }
   if (d.Cp != d.C) {
     TRY(launch_pad_channels(xe, wsp(ws, L.x), (int64_t)d.N * d.H * d.W, d.C, d.Cp, st));
     TRY(launch_pad_channels(we, wsp(ws, L.w), (int64_t)d.K * d.R * d.S, d.C, d.Cp, st));
     xe = wsp(ws, L.x);
     we = wsp(ws, L.w);
   }
-  float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + conv_bn_band_off(d));
   IgemmArgs a{};
   a.act = xe; a.N = d.N; a.Hi = d.H; a.Wi = d.W; a.Ci = d.Cp;
   a.stride_h = d.sh; a.stride_w = d.sw;

@@ -1413,6 +1413,214 @@ hipError_t launch_cfg(const IgemmArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// ---- the ResNet stem: 7x7 stride-2 convolution of 3-channel images -------------
+// The stem (Section 5.1's ResNet-50: 3 -> 64 channels, 7x7, stride 2, pad 3)
+// has a reduction of only 147, and padding its channels to 8 for the
+// implicit-GEMM kernels wastes 62 % of the matrix-core work on zeros and a
+// copy of the image.  Here:
+//  - the k order is (filter row r, window pixel s' = 0..7, channel c' = 0..3)
+//    with s' = 7 and c' = 3 zero in the filter: 7 x 32 = 224 (14 k-steps of
+//    16); the whole 64 x 224 filter stays in registers as MFMA B fragments;
+//  - a workgroup (one wave per 128 output pixels of an 8-row tile, Q/16
+//    waves) walks over tiles of 8 output rows of one image; the tile's 21
+//    input rows are staged in LDS once with 4 channels (8 bytes) per pixel
+//    and 3 zero pixels of padding on the left, so the 8-pixel window of
+//    output column q starts at pixel 2q of the staged row and each lane's
+//    two window pixels are one aligned 16-byte read;
+//  - the next tile's rows are loaded into registers (12 bytes = 2 pixels
+//    per load) while the current tile is computed, and written to LDS after;
+//  - each wave computes its 128 pixels as 4 blocks of 32 x 64 with the
+//    operands swapped (D = W X^T: a lane holds one pixel) and stores from
+//    registers after lane-half swaps, 16 bytes at a time, as pw_kernel does;
+//  - with statistics, the plain product (D = X W^T: a lane holds one channel
+//    of 16 pixels) is computed alongside, and the wave's 128 pixels are one
+//    record: shift K = the first pixel's value, sums of (y - K) and (y - K)^2
+//    in-lane over the 4 blocks, then the two lane halves.
+constexpr int kStemTR = 8;                      // output rows per tile
+constexpr int kStemIR = 2 * kStemTR + 5;        // staged input rows
+constexpr int kStemMaxQ = 128;                  // output columns (16 .. 128)
+constexpr int kStemLds = kStemIR * (2 * kStemMaxQ + 6) * 8;
+constexpr int kStemPairs = 6;                   // staged pixel pairs per thread
+
+template <bool STATS>
+__global__ __launch_bounds__(512) void stem_kernel(const IgemmArgs a, int ntiles) {
+  __shared__ __attribute__((aligned(16))) char lds[kStemLds];
+  const int Q = a.OW, P = a.OH, H = a.Hi, W = a.Wi;
+  const int RS = (2 * Q + 6) * 8;  // staged row, bytes
+  const int nthr = Q * 4;          // Q / 16 waves
+  const int tpi = (P + kStemTR - 1) / kStemTR;
+  const int tid = threadIdx.x;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
+  const int lrow = lane & 31, lhi = lane >> 5;
+  constexpr uint32_t OOB = 0x80000000u;
+  const int x_bytes = (int)((int64_t)a.N * H * W * 6);
+  const __amdgpu_buffer_rsrc_t rs_x = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<h16*>(a.act), (short)0, x_bytes, 0x00020000);
+
+  // the padding pixels (left 3, right past the image) stay zero throughout
+  for (int i = tid; i < kStemIR * RS / 16; i += nthr) {
+    V8 z;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) z.s[e] = 0;
+    *reinterpret_cast<V8*>(lds + i * 16) = z;
+  }
+
+  // filter fragments: lane holds channel nb*32 + lane%32 and, for k-step ks,
+  // filter row ks/2, window pixels 4*(ks%2) + 2*lhi + {0, 1}, channels 0..3
+  half8 bfr[2][14];
+  {
+    const h16* f = a.ph[0].filt;
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int ks = 0; ks < 14; ++ks) {
+        V8 v;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int sp = 4 * (ks & 1) + 2 * lhi + (e >> 2), c = e & 3;
+          const bool ok = sp < 7 && c < 3;
+          const h16 w = f[(int64_t)(nb * 32 + lrow) * 147 + ((ks >> 1) * 7 + (ok ? sp : 0)) * 3 +
+                          (ok ? c : 0)];
+          v.h[e] = ok ? w : (h16)0.0f;
+        }
+        bfr[nb][ks] = v.h;
+      }
+  }
+
+  // staging: pixel pair j = tid + i*nthr (i < kStemPairs) of the tile's
+  // 21 rows x Q pairs (W = 2Q): row j / Q, input columns 2(j % Q) + {0, 1}
+  uint32_t pf[kStemPairs][3];
+  auto prefetch = [&](int tile) {
+    const int n = tile / tpi, ih0 = 2 * (tile - n * tpi) * kStemTR - 3;
+#pragma unroll
+    for (int i = 0; i < kStemPairs; ++i) {
+      const int j = tid + i * nthr;
+      const int row = j / Q, k = j - row * Q;
+      const int ih = ih0 + row;
+      const bool ok = tile < ntiles && row < kStemIR && (unsigned)ih < (unsigned)H;
+      const uint32_t off = ok ? (uint32_t)((((int64_t)n * H + ih) * W + 2 * k) * 6) : OOB;
+      const auto v = __builtin_amdgcn_raw_buffer_load_b96(rs_x, off, 0, 0);
+      pf[i][0] = v[0];
+      pf[i][1] = v[1];
+      pf[i][2] = v[2];
+    }
+  };
+  auto stage = [&]() {
+#pragma unroll
+    for (int i = 0; i < kStemPairs; ++i) {
+      const int j = tid + i * nthr;
+      const int row = j / Q, k = j - row * Q;
+      if (row < kStemIR) {
+        // (c0 c1)(c2 c0')(c1' c2') -> (c0 c1)(c2 0) and (c0' c1')(c2' 0)
+        uint2 p0, p1;
+        p0.x = pf[i][0];
+        p0.y = pf[i][1] & 0xFFFFu;
+        p1.x = (pf[i][1] >> 16) | (pf[i][2] << 16);
+        p1.y = pf[i][2] >> 16;
+        char* dst = lds + row * RS + (2 * k + 3) * 8;
+        *reinterpret_cast<uint2*>(dst) = p0;
+        *reinterpret_cast<uint2*>(dst + 8) = p1;
+      }
+    }
+  };
+
+  int tile = blockIdx.x;
+  prefetch(tile);
+  __syncthreads();
+  stage();
+  __syncthreads();
+  for (; tile < ntiles; tile += gridDim.x) {
+    prefetch(tile + gridDim.x);
+    const int n = tile / tpi, oh0 = (tile - n * tpi) * kStemTR;
+    const int64_t M0 = ((int64_t)n * P + oh0) * Q;  // first output pixel of the tile
+    float K[2] = {0.0f, 0.0f}, s1[2] = {0.0f, 0.0f}, s2[2] = {0.0f, 0.0f};
+#pragma unroll 1
+    for (int blk = 0; blk < 4; ++blk) {
+      const int mb = wave * 128 + blk * 32;  // first pixel of the block in the tile
+      const int m = mb + lrow;
+      const int ohl = m / Q, ow = m - ohl * Q;
+      const char* base = lds + 2 * ohl * RS + 16 * (ow + lhi);
+      // at: D = W X^T (a lane holds one pixel: the stores); an: D = X W^T (a
+      // lane holds one channel of 16 pixels: the statistics)
+      floatx16 at[2], an[2];
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+          at[nb][e] = 0.0f;
+          an[nb][e] = 0.0f;
+        }
+      half8 xa[3];
+      xa[0] = *reinterpret_cast<const half8*>(base);
+      xa[1] = *reinterpret_cast<const half8*>(base + 32);
+#pragma unroll
+      for (int ks = 0; ks < 14; ++ks) {
+        if (ks + 2 < 14)
+          xa[(ks + 2) % 3] =
+              *reinterpret_cast<const half8*>(base + ((ks + 2) >> 1) * RS + 32 * ((ks + 2) & 1));
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+          at[nb] = mfma32x32x16(bfr[nb][ks], xa[ks % 3], at[nb]);
+          if (STATS) an[nb] = mfma32x32x16(xa[ks % 3], bfr[nb][ks], an[nb]);
+        }
+      }
+      // stores: after the lane-half swaps v[8h .. 8h+7] are channels
+      // nb*32 + 16h + 8*lhi + 0..7 of pixel mb + lane%32
+      const bool in_img = oh0 + ohl < P;
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        float v[16];
+#pragma unroll
+        for (int e = 0; e < 16; ++e) v[e] = at[nb][e];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          lane_half_swap(v[q], v[4 + q]);
+          lane_half_swap(v[8 + q], v[12 + q]);
+        }
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          V8 o;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o.h[e] = to_h16(v[h * 8 + e]);
+          if (in_img) store16(a.out + (M0 + m) * 64 + nb * 32 + h * 16 + lhi * 8, o);
+        }
+      }
+      if (STATS) {
+        // plain layout: channel nb*32 + lane%32 of pixels mb + 8*(e/4) +
+        // 4*lhi + e%4; the record's shift is its first pixel's value
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const float y = to_f32(to_h16(an[nb][e]));
+            if (blk == 0 && e == 0) K[nb] = __shfl(y, lrow, 64);
+            const float d = y - K[nb];
+            s1[nb] += d;
+            s2[nb] = __builtin_fmaf(d, d, s2[nb]);
+          }
+        }
+      }
+    }
+    if (STATS) {
+      // the tile's rows are all in the image here (P % 8 == 0)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        s1[nb] += __shfl_xor(s1[nb], 32, 64);
+        s2[nb] += __shfl_xor(s2[nb], 32, 64);
+        if (lhi == 0) {
+          float* rec = a.stat + (M0 / 128 + wave) * 3 * 64 + nb * 32 + lrow;
+          rec[0] = K[nb];
+          rec[64] = s1[nb];
+          rec[128] = s2[nb];
+        }
+      }
+    }
+    __syncthreads();
+    stage();
+    __syncthreads();
+  }
+}
+
 }  // namespace
 
 namespace {
@@ -1493,6 +1701,35 @@ hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st) {
     default:
       return a.Co <= 64 ? launch_cfg<128, 64, 4, 1, 64>(a, st) : launch_cfg<128, 128, 2, 2, 64>(a, st);
   }
+}
+
+// The stem kernel's problem: 3 input channels (unpadded NHWC, W a multiple
+// of 8), 7x7 filter (KRSC, 147 per output channel), stride 2, pad 3, 64 dense
+// output channels, 16 .. 128 output columns in steps of 16; with statistics
+// also whole 8-row tiles (P a multiple of 8), so that each wave's 128 pixels
+// are one 128-row record.
+bool stem_conv_ok(const IgemmArgs& a) {
+  const IgemmPhase& p = a.ph[0];
+  const bool shape = a.Ci == 3 && a.nphase == 1 && p.Rt == 7 && p.St == 7 && p.ldb == 147 &&
+                     p.pad_h == 3 && p.pad_w == 3 && a.stride_h == 2 && a.stride_w == 2 &&
+                     p.oph == 0 && p.opw == 0 && a.os_h == 1 && a.os_w == 1 && a.Co == 64 &&
+                     a.ldo == 64 && !a.addend && !a.f16acc && a.Wi % 8 == 0 &&
+                     a.Wi == 2 * a.OW && a.OH == p.Ho && a.OW == p.Wo &&
+                     a.OW % 16 == 0 && a.OW >= 16 && a.OW <= kStemMaxQ &&
+                     (int64_t)a.N * a.Hi * a.Wi * 6 < ((int64_t)1 << 31);
+  return shape && (!a.stat || a.OH % kStemTR == 0);
+}
+
+hipError_t launch_stem(const IgemmArgs& a, hipStream_t st) {
+  const int tpi = ceil_div(a.OH, kStemTR);
+  const int ntiles = a.N * tpi;
+  const int grid = ntiles < 256 ? ntiles : 256;
+  const dim3 block(a.OW * 4);
+  if (a.stat)
+    hipLaunchKernelGGL(stem_kernel<true>, dim3(grid), block, 0, st, a, ntiles);
+  else
+    hipLaunchKernelGGL(stem_kernel<false>, dim3(grid), block, 0, st, a, ntiles);
+  return hipGetLastError();
 }
 
 }  // namespace fp16k

@@ -64,6 +64,12 @@ struct IgemmArgs {
 };
 
 hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st);
+// The ResNet stem convolution (3 channels, 7x7, stride 2, pad 3, 64 outputs)
+// on its own kernel: act is the unpadded 3-channel image (Ci = 3) and the
+// filter KRSC with ldb = 147.  stem_conv_ok says whether launch_stem takes the
+// problem (with statistics when a.stat is set).
+bool stem_conv_ok(const IgemmArgs& a);
+hipError_t launch_stem(const IgemmArgs& a, hipStream_t st);
 // Whether the kernel launch_igemm picks for this problem can take the BN
 // statistics (IgemmArgs::stat) in its epilogue.
 bool igemm_takes_stats(const IgemmArgs& a);

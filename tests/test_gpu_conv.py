@@ -27,7 +27,9 @@ SHAPES = [
     (2, 64, 14, 14, 256, 1, 1, 1, 0, "NHWC"),   # bottleneck-exit 1x1
     (2, 64, 15, 15, 128, 1, 1, 2, 0, "NHWC"),   # strided 1x1 shortcut, odd size
     (2, 32, 17, 17, 48, 3, 3, 2, 1, "NHWC"),    # strided 3x3, odd size
-    (2, 3, 32, 32, 64, 7, 7, 2, 3, "NHWC"),     # the stem (3 input channels)
+    (2, 3, 32, 32, 64, 7, 7, 2, 3, "NHWC"),     # the stem (3 input channels): stem kernel, one wave
+    (1, 3, 224, 224, 64, 7, 7, 2, 3, "NHWC"),   # the ResNet-50 stem at full size: 7 waves per tile
+    (2, 3, 40, 32, 64, 7, 7, 2, 3, "NHWC"),     # stem kernel, 20 output rows: a partial last tile
     (2, 24, 9, 11, 40, 3, 3, 1, 1, "NHWC"),     # channels not a tile multiple
     (3, 16, 6, 5, 3, 3, 3, 1, 2, "NHWC"),       # 3 output channels, pad > R/2
     (4, 512, 1, 1, 200, 1, 1, 1, 0, "NHWC"),    # fully connected as a 1x1 on 1x1 images

@@ -26,8 +26,9 @@ CASES = [
     (2, 64, 28, 256, 1, 1, 0, 0.25, True, True, False),    # block conv3 + bn3 with the shortcut
     (3, 64, 7, 128, 3, 1, 1, 0.25, False, True, False),    # M = 147: ragged last band
     (3, 64, 9, 64, 3, 1, 1, 0.25, False, True, False),     # M = 243, 64 channels: ragged band, narrow tile
-    (2, 3, 32, 64, 7, 2, 3, 1.0, False, True, False),      # the stem (3 channels staged), s = 1:
-                                                           # LDS-staged kernel, separate statistics
+    (2, 3, 32, 64, 7, 2, 3, 1.0, False, True, False),      # the stem, s = 1: stem kernel, records
+                                                           # from one wave per 128 pixels
+    (1, 3, 224, 64, 7, 2, 3, 1.0, False, True, False),     # the ResNet-50 stem at full size
     (2, 64, 14, 256, 1, 1, 0, 0.25, True, True, True),     # BN swap on the block-last BN
     (2, 128, 15, 64, 3, 2, 1, 0.25, False, False, False),  # strided, no ReLU
     (32, 256, 56, 64, 1, 1, 0, 0.25, False, True, False),  # the conv2_x block's conv1 at batch 32
