@@ -129,6 +129,28 @@ fp16_status fp16_conv_dgrad_add(const fp16_conv_desc* desc, const fp16_t* dy, co
                                 const fp16_t* addend, fp16_t* dx, void* ws, size_t ws_bytes,
                                 fp16_stream_t stream);
 
+/* The data gradient in two steps, so that the filter rearrangement (which
+ * depends only on W) can run ahead of time, off the critical path, e.g. on
+ * a second stream during the forward pass:
+ *   fp16_conv_dgrad_filter writes W rearranged for the data gradient into wf
+ *   (per stride phase, its taps flipped, rows = input channels, reduction
+ *   over (tap, output channel) with the output channels padded to a multiple
+ *   of 8; fp16_conv_dgrad_filter_bytes bytes, 16-byte aligned, not
+ *   overlapping w);
+ *   fp16_conv_dgrad_wf computes fp16_conv_dgrad (addend NULL) or
+ *   fp16_conv_dgrad_add (addend given, same rules) from wf instead of w,
+ *   with identical results.
+ * NHWC only (FP16_ERR_UNSUPPORTED for NCHW).  The workspace is the one
+ * fp16_conv_workspace_bytes(desc, FP16_PASS_DGRAD) sizes.  wf must hold the
+ * rearrangement of the filter the data gradient is meant for: it is not
+ * checked. */
+size_t fp16_conv_dgrad_filter_bytes(const fp16_conv_desc* desc);
+fp16_status fp16_conv_dgrad_filter(const fp16_conv_desc* desc, const fp16_t* w, fp16_t* wf,
+                                   fp16_stream_t stream);
+fp16_status fp16_conv_dgrad_wf(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* wf,
+                               const fp16_t* addend, fp16_t* dx, void* ws, size_t ws_bytes,
+                               fp16_stream_t stream);
+
 /* Weight gradient (the adjoint of fp16_conv_fwd in W):
  *   dW[k,c,r,s] = sum_{n,p,q} dy[n,k,p,q] * x[n,c, p*stride_h - pad_h + r, q*stride_w - pad_w + s].
  * Partial sums over pixel ranges stay float32 in the workspace and are

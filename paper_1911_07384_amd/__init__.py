@@ -32,7 +32,8 @@ EXPORTS = ["fp16_conv_out_dims", "fp16_conv_workspace_bytes", "fp16_conv_fwd", "
            "fp16_sgd_step", "fp16_pool_out_dims", "fp16_maxpool_fwd", "fp16_maxpool_bwd",
            "fp16_avgpool_fwd", "fp16_avgpool_bwd", "fp16_softmax_ce", "fp16_status_string",
            "fp16_version", "fp16_conv_bn_workspace_bytes", "fp16_conv_bn_relu_fwd",
-           "fp16_sgd_step_f16"]
+           "fp16_sgd_step_f16", "fp16_conv_dgrad_filter_bytes", "fp16_conv_dgrad_filter",
+           "fp16_conv_dgrad_wf"]
 
 
 class Fp16Error(RuntimeError):
@@ -71,6 +72,9 @@ _SIGS = {
     "fp16_conv_dgrad": (ctypes.c_int, [_P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_conv_dgrad_add": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_conv_wgrad": (ctypes.c_int, [_P, _P, _P, _P, _P, _SZ, _P]),
+    "fp16_conv_dgrad_filter_bytes": (_SZ, [_P]),
+    "fp16_conv_dgrad_filter": (ctypes.c_int, [_P, _P, _P, _P]),
+    "fp16_conv_dgrad_wf": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_bn_workspace_bytes": (_SZ, [_P]),
     "fp16_bn_relu": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_bn_relu_bwd": (ctypes.c_int, [_P] * 13 + [_SZ, _P]),
@@ -187,6 +191,21 @@ def fp16_conv_dgrad_add(desc, dy, w, addend, dx, ws=None, ws_bytes=None, stream=
     _check("fp16_conv_dgrad_add", lib().fp16_conv_dgrad_add(
         ctypes.byref(desc), _ptr(dy), _ptr(w), _ptr(addend), _ptr(dx), _ptr(ws), _wsb(ws, ws_bytes),
         _stream(stream)))
+
+
+def fp16_conv_dgrad_filter_bytes(desc: ConvDesc) -> int:
+    return int(lib().fp16_conv_dgrad_filter_bytes(ctypes.byref(desc)))
+
+
+def fp16_conv_dgrad_filter(desc, w, wf, stream=None) -> None:
+    _check("fp16_conv_dgrad_filter", lib().fp16_conv_dgrad_filter(ctypes.byref(desc), _ptr(w),
+                                                                  _ptr(wf), _stream(stream)))
+
+
+def fp16_conv_dgrad_wf(desc, dy, wf, addend, dx, ws=None, ws_bytes=None, stream=None) -> None:
+    _check("fp16_conv_dgrad_wf", lib().fp16_conv_dgrad_wf(
+        ctypes.byref(desc), _ptr(dy), _ptr(wf), _ptr(addend), _ptr(dx), _ptr(ws),
+        _wsb(ws, ws_bytes), _stream(stream)))
 
 
 def fp16_conv_wgrad(desc, x, dy, dw, ws=None, ws_bytes=None, stream=None) -> None:

@@ -229,19 +229,27 @@ fp16_status fp16_conv_fwd(const fp16_conv_desc* desc, const fp16_t* x, const fp1
 
 }  // extern "C"
 
+// Bytes of the rearranged data-gradient filter (every stride phase's taps
+// together cover the R x S taps once).
+static size_t dgrad_filter_bytes(const ConvDims& d) { return (size_t)d.C * d.R * d.S * d.Kp * 2; }
+
+// Data gradient; with wf_given the filter is already rearranged (w is then
+// the rearranged filter, fp16_conv_dgrad_filter_bytes long, NHWC only).
 static fp16_status conv_dgrad_impl(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* w,
                                    const fp16_t* addend, fp16_t* dx, void* ws, size_t ws_bytes,
-                                   fp16_stream_t stream) {
+                                   fp16_stream_t stream, bool wf_given = false) {
   ConvDims d;
   fp16_status s = check_conv(desc, &d);
   if (s != FP16_OK) return s;
   if (!dy || !w || !dx) return FP16_ERR_NULL;
+  if (wf_given && d.layout != FP16_NHWC) return FP16_ERR_UNSUPPORTED;
   if (!aligned16(dy) || !aligned16(w) || !aligned16(dx) || (addend && !aligned16(addend)))
     return FP16_ERR_MISALIGNED;
   const ConvWs L = conv_ws(d, FP16_PASS_DGRAD);
   if ((s = check_ws(L, ws, ws_bytes)) != FP16_OK) return s;
   const size_t xb = (size_t)d.x_elems * 2;
-  if (overlap(dx, xb, dy, (size_t)d.y_elems * 2) || overlap(dx, xb, w, (size_t)d.w_elems * 2) ||
+  const size_t wb = wf_given ? dgrad_filter_bytes(d) : (size_t)d.w_elems * 2;
+  if (overlap(dx, xb, dy, (size_t)d.y_elems * 2) || overlap(dx, xb, w, wb) ||
       overlap(dx, xb, ws, L.total) || (addend && addend != dx && overlap(dx, xb, addend, xb)) ||
       (addend && overlap(addend, xb, ws, L.total)))
     return FP16_ERR_ALIASING;
@@ -263,8 +271,12 @@ static fp16_status conv_dgrad_impl(const fp16_conv_desc* desc, const fp16_t* dy,
     TRY(launch_pad_channels(dye, wsp(ws, L.y), (int64_t)d.N * d.P * d.Q, d.K, d.Kp, st));
     dye = wsp(ws, L.y);
   }
-  h16* wf = wsp(ws, L.wf);
-  TRY(launch_dgrad_filter(wk, wf, d.K, d.C, d.R, d.S, d.C, d.Kp, d.sh, d.sw, d.ph, d.pw, st));
+  const h16* wf = wk;
+  if (!wf_given) {
+    h16* wt = wsp(ws, L.wf);
+    TRY(launch_dgrad_filter(wk, wt, d.K, d.C, d.R, d.S, d.C, d.Kp, d.sh, d.sw, d.ph, d.pw, st));
+    wf = wt;
+  }
   IgemmArgs a{};
   a.act = dye; a.N = d.N; a.Hi = d.P; a.Wi = d.Q; a.Ci = d.Kp;
   a.stride_h = 1; a.stride_w = 1;
@@ -305,6 +317,32 @@ fp16_status fp16_conv_dgrad_add(const fp16_conv_desc* desc, const fp16_t* dy, co
                                 fp16_stream_t stream) {
   if (!addend) return FP16_ERR_NULL;
   return conv_dgrad_impl(desc, dy, w, addend, dx, ws, ws_bytes, stream);
+}
+
+size_t fp16_conv_dgrad_filter_bytes(const fp16_conv_desc* desc) {
+  ConvDims d;
+  if (check_conv(desc, &d) != FP16_OK || d.layout != FP16_NHWC) return 0;
+  return dgrad_filter_bytes(d);
+}
+
+fp16_status fp16_conv_dgrad_filter(const fp16_conv_desc* desc, const fp16_t* w, fp16_t* wf,
+                                   fp16_stream_t stream) {
+  ConvDims d;
+  fp16_status s = check_conv(desc, &d);
+  if (s != FP16_OK) return s;
+  if (d.layout != FP16_NHWC) return FP16_ERR_UNSUPPORTED;
+  if (!w || !wf) return FP16_ERR_NULL;
+  if (!aligned16(w) || !aligned16(wf)) return FP16_ERR_MISALIGNED;
+  if (overlap(wf, dgrad_filter_bytes(d), w, (size_t)d.w_elems * 2)) return FP16_ERR_ALIASING;
+  return hip_status(launch_dgrad_filter(reinterpret_cast<const h16*>(w), reinterpret_cast<h16*>(wf),
+                                        d.K, d.C, d.R, d.S, d.C, d.Kp, d.sh, d.sw, d.ph, d.pw,
+                                        static_cast<hipStream_t>(stream)));
+}
+
+fp16_status fp16_conv_dgrad_wf(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* wf,
+                               const fp16_t* addend, fp16_t* dx, void* ws, size_t ws_bytes,
+                               fp16_stream_t stream) {
+  return conv_dgrad_impl(desc, dy, wf, addend, dx, ws, ws_bytes, stream, true);
 }
 
 }  // extern "C"

@@ -69,6 +69,7 @@ class ResNet50:
         self._wspecs = []  # (name, shape, std) of every weight-decay parameter
         self._bnspecs = []
         self.fwd, self.bwd, self.upd = [], [], []
+        self.prep = []     # data-gradient filter rearrangements, run during the forward
         self.buffers = {}
         self._ws_need = 0
         self._plan(stages)
@@ -218,13 +219,19 @@ class ResNet50:
         c = self._conv_op(name)
         if dx_needed:
             dx = dx_name or self._grad(c["x"])
+            # the filter is rearranged for the data gradient during the forward
+            # (on the side stream, off the critical path); the data gradient
+            # reads the rearranged copy
+            wf = name + ".wf"
+            self._buf(wf, (F.fp16_conv_dgrad_filter_bytes(c["desc"]) // 2,))
+            self.prep.append(Op("dgrad_filter", name, {"desc": c["desc"], "w": name, "wf": wf}))
             if addend is None:
                 self.bwd.append(Op("conv_dgrad", name, {"desc": c["desc"], "dy": dy, "w": name,
-                                                        "dx": dx}))
+                                                        "wf": wf, "dx": dx}))
             else:
                 self.bwd.append(Op("conv_dgrad_add", name, {"desc": c["desc"], "dy": dy,
-                                                            "w": name, "addend": addend,
-                                                            "dx": dx}))
+                                                            "w": name, "wf": wf,
+                                                            "addend": addend, "dx": dx}))
         self.bwd.append(Op("conv_wgrad", name, {"desc": c["desc"], "x": c["x"], "dy": dy,
                                                 "dw": "d:" + name}))
 
@@ -328,9 +335,11 @@ class ResNet50:
         if k == "conv_fwd":
             F.fp16_conv_fwd(a["desc"], t(a["x"]), t(a["w"]), t(a["y"]), ws)
         elif k == "conv_dgrad":
-            F.fp16_conv_dgrad(a["desc"], t(a["dy"]), t(a["w"]), t(a["dx"]), ws)
+            F.fp16_conv_dgrad_wf(a["desc"], t(a["dy"]), t(a["wf"]), None, t(a["dx"]), ws)
         elif k == "conv_dgrad_add":
-            F.fp16_conv_dgrad_add(a["desc"], t(a["dy"]), t(a["w"]), t(a["addend"]), t(a["dx"]), ws)
+            F.fp16_conv_dgrad_wf(a["desc"], t(a["dy"]), t(a["wf"]), t(a["addend"]), t(a["dx"]), ws)
+        elif k == "dgrad_filter":
+            F.fp16_conv_dgrad_filter(a["desc"], t(a["w"]), t(a["wf"]))
         elif k == "conv_wgrad":
             F.fp16_conv_wgrad(a["desc"], t(a["x"]), t(a["dy"]), t(a["dw"]), ws)
         elif k == "conv_bn_fwd":
@@ -365,14 +374,14 @@ class ResNet50:
             raise ValueError(k)
 
     def program(self):
-        return self.fwd + self.bwd + self.upd
+        return self.prep + self.fwd + self.bwd + self.upd
 
     _OUTPUTS = {"conv_fwd": ("y",), "conv_bn_fwd": ("y", "z", "stats"), "conv_dgrad": ("dx",),
                 "conv_dgrad_add": ("dx",),
                 "conv_wgrad": ("dw",), "bn_fwd": ("y", "stats"),
                 "bn_bwd": ("dx", "dgamma", "dbeta", "dres"), "maxpool_fwd": ("y", "idx"),
                 "maxpool_bwd": ("dx",), "avgpool_fwd": ("y",), "avgpool_bwd": ("dx",),
-                "softmax_ce": ("loss", "dz", "dbias")}
+                "softmax_ce": ("loss", "dz", "dbias"), "dgrad_filter": ("wf",)}
 
     def _schedule(self):
         """For each weight gradient of the backward, the index (in bwd) of the
@@ -393,6 +402,21 @@ class ResNet50:
                         writer[op.a[k]] = i
 
     def forward(self):
+        # the data-gradient filters of this step's weights, on the side stream
+        # while the forward runs (the backward waits for them)
+        if self.side is None:
+            for op in self.prep:
+                self.run(op)
+        else:
+            main = torch.cuda.current_stream()
+            start = torch.cuda.Event()
+            start.record(main)
+            self.side.wait_event(start)
+            with torch.cuda.stream(self.side):
+                for op in self.prep:
+                    self.run(op, ws=self.ws_side)
+            self._wf_ready = torch.cuda.Event()
+            self._wf_ready.record(self.side)
         for op in self.fwd:
             self.run(op)
 
@@ -402,6 +426,7 @@ class ResNet50:
                 self.run(op)
             return
         main, side = torch.cuda.current_stream(), self.side
+        main.wait_event(self._wf_ready)  # the rearranged data-gradient filters
         start = torch.cuda.Event()
         start.record(main)
         events = {}

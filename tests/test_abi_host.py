@@ -100,6 +100,31 @@ def test_conv_workspace_and_aliasing():
     assert F.fp16_conv_workspace_bytes(_conv(), 5) == 0
 
 
+def test_dgrad_filter_validation():
+    d = _conv()
+    lib = F.lib()
+    # bytes: C x R x S x K (K padded to 8); NCHW is not offered
+    assert F.fp16_conv_dgrad_filter_bytes(d) == 64 * 3 * 3 * 64 * 2
+    assert F.fp16_conv_dgrad_filter_bytes(_conv(k=3)) == 64 * 3 * 3 * 8 * 2
+    assert F.fp16_conv_dgrad_filter_bytes(_conv(layout="NCHW")) == 0
+    f = lib.fp16_conv_dgrad_filter
+    assert f(None, A, B, None) == NULL
+    assert f(ctypes.byref(d), None, B, None) == NULL
+    assert f(ctypes.byref(d), A, None, None) == NULL
+    assert f(ctypes.byref(_conv(layout="NCHW")), A, B, None) == UNSUPPORTED
+    assert f(ctypes.byref(d), A + 2, B, None) == MISALIGNED
+    assert f(ctypes.byref(d), A, A + 64, None) == ALIASING
+    g = lib.fp16_conv_dgrad_wf
+    need = F.fp16_conv_workspace_bytes(d, F.PASS_DGRAD)
+    assert g(ctypes.byref(d), None, B, None, Cc, WS, need, None) == NULL
+    assert g(ctypes.byref(d), A, None, None, Cc, WS, need, None) == NULL
+    assert g(ctypes.byref(_conv(layout="NCHW")), A, B, None, Cc, WS, 1 << 30, None) == UNSUPPORTED
+    assert g(ctypes.byref(d), A, B, None, Cc, WS + 4, need, None) == MISALIGNED
+    assert g(ctypes.byref(d), A, B, None, Cc, 0, 0, None) == WORKSPACE
+    # dx over the rearranged filter
+    assert g(ctypes.byref(d), A, B, None, B + 64, WS, need, None) == ALIASING
+
+
 @pytest.mark.parametrize("hw,r,st,pad", [(56, 3, 1, 1), (56, 1, 2, 0), (224, 7, 2, 3), (7, 3, 1, 1),
                                          (14, 3, 2, 1), (1, 1, 1, 0), (5, 3, 2, 0)])
 def test_out_dims(hw, r, st, pad):

@@ -155,3 +155,38 @@ def test_dgrad_add_parity(shape):
     ref64, ref16 = oracle.conv_dgrad_add(case.shp, case.dy, case.w, addend)
     check_close(got, ref64, what=f"dgrad_add {case.label}")
     assert np.mean(ulp_dist(got, ref16) <= 1) > 0.99
+
+
+# the data gradient from a filter rearranged ahead of time equals the one-call
+# data gradient bit for bit (with and without the addend)
+WF_SHAPES = [  # (n, c, h, w, k, r, stride, pad)
+    (2, 64, 28, 28, 64, 3, 1, 1),     # the 64-channel 3x3 kernel
+    (2, 128, 14, 14, 128, 3, 1, 1),   # DMA-staged kernel
+    (2, 64, 15, 15, 128, 1, 2, 0),    # strided 1x1: four phases, three of them empty
+    (2, 32, 17, 17, 48, 3, 2, 1),     # strided 3x3: four phases of 1-4 taps
+    (3, 16, 6, 5, 3, 3, 1, 2),        # 3 output channels, padded to 8 in the filter
+    (2, 64, 14, 14, 256, 1, 1, 0),    # pointwise kernel (64 -> 256 data gradient)
+]
+
+
+@pytest.mark.parametrize("shape", WF_SHAPES, ids=[str(s) for s in WF_SHAPES])
+@pytest.mark.parametrize("with_addend", [False, True])
+def test_dgrad_from_rearranged_filter_is_identical(shape, with_addend):
+    require_gpu()
+    from paper_1911_07384_amd import synth
+    n, c, h, w, k, r, st, pad = shape
+    case = ConvCase(n, c, h, w, k, r, r, st, pad, seed=5)
+    ws = F.workspace(F.fp16_conv_workspace_bytes(case.desc, F.PASS_DGRAD))
+    wf = F.workspace(F.fp16_conv_dgrad_filter_bytes(case.desc))
+    addend = dev(synth.normal_f16(case.xs, 1e-2, 5, 9)) if with_addend else None
+    a = torch.empty(case.xs, dtype=torch.float16, device="cuda")
+    b = torch.empty_like(a)
+    note(f"[gpu] dgrad_wf {case.label} addend={with_addend}")
+    if with_addend:
+        F.fp16_conv_dgrad_add(case.desc, dev(case.dy), dev(case.w), addend, a, ws)
+    else:
+        F.fp16_conv_dgrad(case.desc, dev(case.dy), dev(case.w), a, ws)
+    F.fp16_conv_dgrad_filter(case.desc, dev(case.w), wf)
+    F.fp16_conv_dgrad_wf(case.desc, dev(case.dy), wf, addend, b, ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(a).view(np.uint16), host(b).view(np.uint16))

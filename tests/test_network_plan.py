@@ -43,7 +43,7 @@ OUTPUTS = {"conv_fwd": ["y"], "conv_bn_fwd": ["y", "z", "stats"], "conv_dgrad": 
            "conv_wgrad": ["dw"], "bn_fwd": ["y", "stats"],
            "bn_bwd": ["dx", "dgamma", "dbeta", "dres"], "maxpool_fwd": ["y", "idx"],
            "maxpool_bwd": ["dx"], "avgpool_fwd": ["y"], "avgpool_bwd": ["dx"],
-           "softmax_ce": ["loss", "dz", "dbias"]}
+           "softmax_ce": ["loss", "dz", "dbias"], "dgrad_filter": ["wf"]}
 
 
 def test_dataflow(net):
@@ -54,7 +54,9 @@ def test_dataflow(net):
         params |= {name + ".gamma", name + ".beta"}
     written = {"image", "labels"} | params
     seen = set()
-    for op in net.fwd + net.bwd:
+    # (the data-gradient filters are rearranged from the weights before the
+    # forward, on the side stream)
+    for op in net.prep + net.fwd + net.bwd:
         outs = [k for k in OUTPUTS[op.kind] if op.a.get(k) is not None]
         reads = [v for k, v in op.a.items() if isinstance(v, str) and k not in outs]
         if op.kind in ("bn_fwd", "bn_bwd", "conv_bn_fwd"):
@@ -71,6 +73,11 @@ def test_dataflow(net):
     assert grads == {"d:" + c["name"] for c in net.convs}
     bn_grads = {op.a["dgamma"] for op in net.bwd if op.kind == "bn_bwd"}
     assert bn_grads == {name + ".dgamma" for name, _ in net._bnspecs}
+    # every data gradient reads a rearranged filter made from its own weights
+    prep = {op.a["wf"]: op.a["w"] for op in net.prep}
+    for op in net.bwd:
+        if op.kind in ("conv_dgrad", "conv_dgrad_add"):
+            assert prep[op.a["wf"]] == op.a["w"] == op.name
 
 
 def test_bn_swap_and_zero_gamma_options():
