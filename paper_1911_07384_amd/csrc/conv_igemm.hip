@@ -1630,7 +1630,7 @@ enum class IgemmKind { kLds, kDirect, kDma, kPointwise, k3x3 };
 // Kernel choice per problem (measured on MI355X over the ResNet-50 shapes at
 // batch 32 and 128): the pointwise kernel for 1x1 filters over 64 or 128
 // channels with 128+ output channels; the DMA-staged kernel for reductions of
-// 576 and more (every 3x3 layer, the 1x1 layers with 1024+ input channels);
+// 512 and more (every 3x3 layer, the 1x1 layers with 512+ input channels);
 // below that the register-direct kernel for short reductions or small M,
 // else the LDS-staged one.  All four give identical bits.
 IgemmKind igemm_kind(const IgemmArgs& a) {
@@ -1659,7 +1659,10 @@ IgemmKind igemm_kind(const IgemmArgs& a) {
     if (f > maxF) maxF = f;
   }
   const int64_t act = (int64_t)a.N * a.Hi * a.Wi * a.Ci * 2;
-  if (a.Ci % 64 == 0 && maxK >= 576 && maxT <= 32 && act < ((int64_t)1 << 31) &&
+  // (a 512-long 1x1 reduction is faster on it too, except in a strided data
+  // gradient, whose empty phases favour the register-direct kernel)
+  const int kmin = a.nphase > 1 ? 576 : 512;
+  if (a.Ci % 64 == 0 && maxK >= kmin && maxT <= 32 && act < ((int64_t)1 << 31) &&
       maxF <= ((int64_t)1 << 30))
     return IgemmKind::kDma;
   if (a.Ci % 32 == 0 && (maxK <= 512 || maxM <= 8192)) return IgemmKind::kDirect;

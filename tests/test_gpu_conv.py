@@ -42,6 +42,8 @@ SHAPES = [
     (2, 64, 15, 15, 64, 3, 3, 2, 1, "NHWC"),    # strided 3x3 on the DMA-staged kernel (fwd)
     (2, 256, 9, 9, 192, 3, 3, 2, 1, "NHWC"),    # dgrad phases of up to 4 taps x 192: DMA-staged; ragged N
     (2, 1024, 5, 5, 96, 1, 1, 1, 0, "NHWC"),    # 1x1 with a 1024-long reduction: DMA-staged
+    (2, 512, 7, 7, 128, 1, 1, 1, 0, "NHWC"),    # 1x1 with a 512-long reduction: DMA-staged fwd
+    (2, 128, 7, 9, 512, 1, 1, 1, 0, "NHWC"),    # ... and DMA-staged data gradient
     (2, 24, 9, 9, 64, 3, 3, 1, 1, "NHWC"),      # wgrad: 8-channel chunks of one 64-column block span taps
     (2, 8, 12, 12, 128, 1, 1, 2, 0, "NHWC"),    # wgrad: 8 channels, K = 128
     (2, 64, 20, 20, 192, 1, 1, 1, 0, "NHWC"),   # pointwise fwd: 64 -> 192, second channel tile partial
