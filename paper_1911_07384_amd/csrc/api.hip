@@ -59,6 +59,16 @@ fp16_status check_conv(const fp16_conv_desc* d, ConvDims* o) {
   return FP16_OK;
 }
 
+// The ResNet stem's weight gradient (3 channels, 7x7, stride 2, pad 3, even
+// image sides) runs as a 4x4 stride-1 convolution over the 2x2 space-to-depth
+// image: 16 channels instead of 3 padded to 8, and one 256-column filter tile
+// instead of two for 392 columns (half the matrix-core work).
+bool stem_s2d(const ConvDims& d) {
+  return d.layout == FP16_NHWC && d.C == 3 && d.R == 7 && d.S == 7 && d.sh == 2 && d.sw == 2 &&
+         d.ph == 3 && d.pw == 3 && d.H % 2 == 0 && d.W % 2 == 0 && d.P == d.H / 2 &&
+         d.Q == d.W / 2 && !d.accum && d.K % 64 == 0 && d.Kp == d.K;
+}
+
 // Workspace regions of one convolution pass (byte offsets, 256-aligned).
 struct ConvWs {
   size_t x = 0, w = 0, y = 0, wf = 0, part = 0, total = 0;
@@ -97,6 +107,11 @@ ConvWs conv_ws(const ConvDims& d, int pass) {
       L.x = take((size_t)d.N * d.H * d.W * d.C * 2);
     }
     L.wf = take((size_t)d.C * d.R * d.S * d.Kp * 2);
+  } else if (stem_s2d(d)) {
+    L.need_x = true;
+    L.x = take((size_t)d.N * d.P * d.Q * 16 * 2);
+    wgrad_plan(d.Kp, 16, 4, 4, (int64_t)d.N * d.P * d.Q, 0, &L.splits, &L.pps);
+    L.part = take((size_t)L.splits * d.Kp * 256 * 4);
   } else {
     if (nchw || d.Cp != d.C) {
       L.need_x = true;
@@ -365,6 +380,20 @@ fp16_status fp16_conv_wgrad(const fp16_conv_desc* desc, const fp16_t* x, const f
   hipStream_t st = static_cast<hipStream_t>(stream);
   const h16* xe = reinterpret_cast<const h16*>(x);
   const h16* dye = reinterpret_cast<const h16*>(dy);
+  if (stem_s2d(d)) {
+    // 4x4 stride-1 convolution over the space-to-depth image, pad 2 before
+    // and 1 after: s2d pixel p + r' - 2 holds original rows 2(p + r') - 4 + dh
+    h16* xs = wsp(ws, L.x);
+    TRY(launch_s2d3(xe, xs, d.N, d.H, d.W, st));
+    float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + L.part);
+    WgradArgs a{};
+    a.x = xs; a.dy = dye;
+    a.N = d.N; a.H = d.P; a.W = d.Q; a.C = 16; a.K = d.Kp; a.R = 4; a.S = 4;
+    a.sh = 1; a.sw = 1; a.ph = 2; a.pw = 2; a.P = d.P; a.Q = d.Q;
+    a.partial = part; a.splits = L.splits; a.pix_per_split = L.pps; a.f16acc = 0;
+    TRY(launch_wgrad_partial(a, st));
+    return hip_status(launch_wgrad_reduce_s2d3(part, L.splits, d.K, reinterpret_cast<h16*>(dw), st));
+  }
   if (d.layout == FP16_NCHW) {
     TRY(launch_nchw_to_nhwc(xe, wsp(ws, L.x), d.N, d.C, d.H * d.W, d.Cp, st));
     TRY(launch_nchw_to_nhwc(dye, wsp(ws, L.y), d.N, d.K, d.P * d.Q, d.Kp, st));

@@ -677,6 +677,43 @@ hipError_t launch_wgrad_partial(const WgradArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// The stem's weight gradient computed as a 4x4 stride-1 convolution over the
+// 2x2 space-to-depth image (16 channels, (dh*2 + dw)*3 + c): original tap
+// (r, s, c) is s2d tap ((r+1)/2, (s+1)/2) at channel (((r+1)%2)*2 + (s+1)%2)*3
+// + c.  dw[k][r][s][c] (KRSC, 7x7x3) = rne16(sum over splits, in order, of
+// partial[split][k][(r'*4 + s')*16 + ch]).
+__global__ __launch_bounds__(256) void wgrad_reduce_s2d3_kernel(const float* __restrict__ partial,
+                                                                 int splits, int K,
+                                                                 h16* __restrict__ dw) {
+  const int i = blockIdx.x * 256 + threadIdx.x;  // enumerates k, r, s, c
+  if (i >= K * 147) return;
+  const int c = i % 3, rs = (i / 3) % 49, k = i / 147;
+  const int r = rs / 7, s = rs % 7;
+  const int rp = (r + 1) >> 1, sp = (s + 1) >> 1;
+  const int ch = (((r + 1) & 1) * 2 + ((s + 1) & 1)) * 3 + c;
+  const float* p = partial + (int64_t)k * 256 + (rp * 4 + sp) * 16 + ch;
+  const int64_t stride = (int64_t)K * 256;
+  float acc = 0.0f;
+  int sp2 = 0;
+  for (; sp2 + 4 <= splits; sp2 += 4) {
+    const float v0 = p[(sp2 + 0) * stride], v1 = p[(sp2 + 1) * stride];
+    const float v2 = p[(sp2 + 2) * stride], v3 = p[(sp2 + 3) * stride];
+    acc += v0;
+    acc += v1;
+    acc += v2;
+    acc += v3;
+  }
+  for (; sp2 < splits; ++sp2) acc += p[sp2 * stride];
+  dw[i] = to_h16(acc);
+}
+
+hipError_t launch_wgrad_reduce_s2d3(const float* partial, int splits, int K, h16* dw,
+                                    hipStream_t st) {
+  hipLaunchKernelGGL(wgrad_reduce_s2d3_kernel, dim3((K * 147 + 255) / 256), dim3(256), 0, st,
+                     partial, splits, K, dw);
+  return hipGetLastError();
+}
+
 hipError_t launch_wgrad_reduce(const float* partial, int splits, int K, int Kp, int R, int S, int C,
                                int Cp, int layout, h16* dw, hipStream_t st) {
   const int64_t total = (int64_t)K * R * S * C;

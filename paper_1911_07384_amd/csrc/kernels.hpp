@@ -117,6 +117,12 @@ hipError_t launch_wgrad_partial(const WgradArgs& a, hipStream_t st);
 // with Kp rows per split, written as KRSC (layout 0) or KCRS (layout 1).
 hipError_t launch_wgrad_reduce(const float* partial, int splits, int K, int Kp, int R, int S,
                                int C, int Cp, int layout, h16* dw, hipStream_t st);
+// The stem's weight gradient through a 2x2 space-to-depth view (layout.hip,
+// conv_wgrad.hip): the 3-channel image as 16 channels at half resolution, and
+// the 4x4 x 16 partial sums gathered back into the 7x7x3 filter.
+hipError_t launch_s2d3(const h16* src, h16* dst, int N, int H, int W, hipStream_t st);
+hipError_t launch_wgrad_reduce_s2d3(const float* partial, int splits, int K, h16* dw,
+                                    hipStream_t st);
 // Split-K plan of the weight gradient; with f16acc one split over all pixels.
 void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int f16acc, int* splits,
                 int* pix_per_split);

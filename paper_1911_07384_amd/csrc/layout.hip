@@ -185,6 +185,43 @@ hipError_t launch_nhwc_to_nchw(const h16* src, h16* dst, int N, int C, int HW, i
   return hipGetLastError();
 }
 
+// 2x2 space-to-depth of a 3-channel NHWC image (H, W even):
+// dst[n][a][b][(dh*2 + dw)*3 + c] = src[n][2a + dh][2b + dw][c], channels
+// 12..15 zero.  One thread per destination pixel: 12 loads of 2 bytes (all
+// in flight), two 16-byte stores.
+__global__ void s2d3_kernel(const h16* __restrict__ src, h16* __restrict__ dst, int N, int H,
+                            int W) {
+  const int H2 = H / 2, W2 = W / 2;
+  const int64_t total = (int64_t)N * H2 * W2;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < total;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    const int b = (int)(i % W2);
+    const int64_t t = i / W2;
+    const int a = (int)(t % H2);
+    const int n = (int)(t / H2);
+    const h16* s0 = src + (((int64_t)n * H + 2 * a) * W + 2 * b) * 3;
+    const h16* s1 = s0 + (int64_t)W * 3;
+    V8 lo, hi;
+#pragma unroll
+    for (int c = 0; c < 6; ++c) lo.h[c] = s0[c];      // (dh 0, dw 0), (0, 1)
+    lo.h[6] = s1[0];
+    lo.h[7] = s1[1];
+    hi.h[0] = s1[2];                                 // (1, 0) last channel
+#pragma unroll
+    for (int c = 0; c < 3; ++c) hi.h[1 + c] = s1[3 + c];  // (1, 1)
+#pragma unroll
+    for (int c = 4; c < 8; ++c) hi.h[c] = (h16)0.0f;
+    store16(dst + i * 16, lo);
+    store16(dst + i * 16 + 8, hi);
+  }
+}
+
+hipError_t launch_s2d3(const h16* src, h16* dst, int N, int H, int W, hipStream_t st) {
+  hipLaunchKernelGGL(s2d3_kernel, dim3(grid_for((int64_t)N * (H / 2) * (W / 2))), dim3(kThreads),
+                     0, st, src, dst, N, H, W);
+  return hipGetLastError();
+}
+
 hipError_t launch_pad_channels(const h16* src, h16* dst, int64_t P, int C, int Cp, hipStream_t st) {
   if (Cp % 8 == 0)
     hipLaunchKernelGGL(pad_channels_vec, dim3(grid_for(P)), dim3(kThreads), 0, st, src, dst, P, C,
