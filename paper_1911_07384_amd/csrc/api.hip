@@ -722,20 +722,16 @@ fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc
   const h16* we = reinterpret_cast<const h16*>(w);
   float* part = reinterpret_cast<float*>(static_cast<char*>(ws) + conv_bn_band_off(d));
   {
-    // the ResNet stem: its own kernel, on the unpadded image
-    IgemmArgs sa = stem_args(d, xe, we, reinterpret_cast<h16*>(y));
-    sa.stat = part;
-    sa.stat_nb = conv_bn_nb(d);
+    // the ResNet stem: its own kernel on the unpadded image, then the BN with
+    // its own statistics pass
+    const IgemmArgs sa = stem_args(d, xe, we, reinterpret_cast<h16*>(y));
     if (stem_conv_ok(sa)) {
       TRY(launch_stem(sa, st));
-      void* band_ws = reinterpret_cast<char*>(part) +
-                      align256((size_t)3 * d.K * sa.stat_nb * sizeof(float));
-      return hip_status(launch_bn_fwd_bands(b, part, sa.stat_nb, band_ws,
-                                            reinterpret_cast<const h16*>(y),
-                                            reinterpret_cast<const h16*>(gamma),
-                                            reinterpret_cast<const h16*>(beta),
-                                            reinterpret_cast<const h16*>(residual),
-                                            reinterpret_cast<h16*>(z), stats, st));
+      return hip_status(launch_bn_fwd(b, reinterpret_cast<const h16*>(y),
+                                      reinterpret_cast<const h16*>(gamma),
+                                      reinterpret_cast<const h16*>(beta),
+                                      reinterpret_cast<const h16*>(residual),
+                                      reinterpret_cast<h16*>(z), stats, 0, part, st));
     }
   }
   if (d.Cp != d.C) {
@@ -755,9 +751,10 @@ fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc
   const h16* gp = reinterpret_cast<const h16*>(gamma);
   const h16* bp = reinterpret_cast<const h16*>(beta);
   const h16* rp = reinterpret_cast<const h16*>(residual);
-  if (!igemm_takes_stats(a)) {
-    // the kernel picked for this shape does not take the statistics: run the
-    // convolution and the BN as separate kernels (same results as the two calls)
+  if (!igemm_stats_pay(a)) {
+    // the kernel picked for this shape does not take the statistics, or is
+    // faster without them: run the convolution and the BN as separate kernels
+    // (same results as the two calls)
     TRY(launch_igemm(a, st));
     return hip_status(launch_bn_fwd(b, reinterpret_cast<const h16*>(y), gp, bp, rp,
                                     reinterpret_cast<h16*>(z), stats, 0, part, st));

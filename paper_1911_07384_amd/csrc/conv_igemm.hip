@@ -1432,17 +1432,16 @@ hipError_t launch_cfg(const IgemmArgs& a, hipStream_t st) {
 //  - each wave computes its 128 pixels as 4 blocks of 32 x 64 with the
 //    operands swapped (D = W X^T: a lane holds one pixel) and stores from
 //    registers after lane-half swaps, 16 bytes at a time, as pw_kernel does;
-//  - with statistics, the plain product (D = X W^T: a lane holds one channel
-//    of 16 pixels) is computed alongside, and the wave's 128 pixels are one
-//    record: shift K = the first pixel's value, sums of (y - K) and (y - K)^2
-//    in-lane over the 4 blocks, then the two lane halves.
+//  - the BN statistics are not taken here: computing the plain product
+//    alongside for them (one channel of 16 pixels per lane) made the fused
+//    call 22 us slower at batch 128 than this kernel plus the BN's own
+//    statistics pass.
 constexpr int kStemTR = 8;                      // output rows per tile
 constexpr int kStemIR = 2 * kStemTR + 5;        // staged input rows
 constexpr int kStemMaxQ = 128;                  // output columns (16 .. 128)
 constexpr int kStemLds = kStemIR * (2 * kStemMaxQ + 6) * 8;
 constexpr int kStemPairs = 6;                   // staged pixel pairs per thread
 
-template <bool STATS>
 __global__ __launch_bounds__(512) void stem_kernel(const IgemmArgs a, int ntiles) {
   __shared__ __attribute__((aligned(16))) char lds[kStemLds];
   const int Q = a.OW, P = a.OH, H = a.Hi, W = a.Wi;
@@ -1533,23 +1532,18 @@ __global__ __launch_bounds__(512) void stem_kernel(const IgemmArgs a, int ntiles
     prefetch(tile + gridDim.x);
     const int n = tile / tpi, oh0 = (tile - n * tpi) * kStemTR;
     const int64_t M0 = ((int64_t)n * P + oh0) * Q;  // first output pixel of the tile
-    float K[2] = {0.0f, 0.0f}, s1[2] = {0.0f, 0.0f}, s2[2] = {0.0f, 0.0f};
 #pragma unroll 1
     for (int blk = 0; blk < 4; ++blk) {
       const int mb = wave * 128 + blk * 32;  // first pixel of the block in the tile
       const int m = mb + lrow;
       const int ohl = m / Q, ow = m - ohl * Q;
       const char* base = lds + 2 * ohl * RS + 16 * (ow + lhi);
-      // at: D = W X^T (a lane holds one pixel: the stores); an: D = X W^T (a
-      // lane holds one channel of 16 pixels: the statistics)
-      floatx16 at[2], an[2];
+      // D = W X^T: a lane holds one pixel
+      floatx16 at[2];
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          at[nb][e] = 0.0f;
-          an[nb][e] = 0.0f;
-        }
+        for (int e = 0; e < 16; ++e) at[nb][e] = 0.0f;
       half8 xa[3];
       xa[0] = *reinterpret_cast<const half8*>(base);
       xa[1] = *reinterpret_cast<const half8*>(base + 32);
@@ -1561,7 +1555,6 @@ __global__ __launch_bounds__(512) void stem_kernel(const IgemmArgs a, int ntiles
 #pragma unroll
         for (int nb = 0; nb < 2; ++nb) {
           at[nb] = mfma32x32x16(bfr[nb][ks], xa[ks % 3], at[nb]);
-          if (STATS) an[nb] = mfma32x32x16(xa[ks % 3], bfr[nb][ks], an[nb]);
         }
       }
       // stores: after the lane-half swaps v[8h .. 8h+7] are channels
@@ -1583,35 +1576,6 @@ __global__ __launch_bounds__(512) void stem_kernel(const IgemmArgs a, int ntiles
 #pragma unroll
           for (int e = 0; e < 8; ++e) o.h[e] = to_h16(v[h * 8 + e]);
           if (in_img) store16(a.out + (M0 + m) * 64 + nb * 32 + h * 16 + lhi * 8, o);
-        }
-      }
-      if (STATS) {
-        // plain layout: channel nb*32 + lane%32 of pixels mb + 8*(e/4) +
-        // 4*lhi + e%4; the record's shift is its first pixel's value
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const float y = to_f32(to_h16(an[nb][e]));
-            if (blk == 0 && e == 0) K[nb] = __shfl(y, lrow, 64);
-            const float d = y - K[nb];
-            s1[nb] += d;
-            s2[nb] = __builtin_fmaf(d, d, s2[nb]);
-          }
-        }
-      }
-    }
-    if (STATS) {
-      // the tile's rows are all in the image here (P % 8 == 0)
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb) {
-        s1[nb] += __shfl_xor(s1[nb], 32, 64);
-        s2[nb] += __shfl_xor(s2[nb], 32, 64);
-        if (lhi == 0) {
-          float* rec = a.stat + (M0 / 128 + wave) * 3 * 64 + nb * 32 + lrow;
-          rec[0] = K[nb];
-          rec[64] = s1[nb];
-          rec[128] = s2[nb];
         }
       }
     }
@@ -1671,6 +1635,21 @@ IgemmKind igemm_kind(const IgemmArgs& a) {
 
 }  // namespace
 
+bool igemm_stats_pay(const IgemmArgs& a) {
+  // Measured on every ResNet-50 conv -> BN shape at batch 128 (fused call vs
+  // convolution + the BN's own statistics pass): the 3x3 64-channel kernel
+  // without statistics beats the DMA-staged kernel with them by more than the
+  // statistics pass costs (97.7 vs 78.6 us), and so does the DMA-staged
+  // kernel's statistics-free form from 100,352 output rows on (the 28x28
+  // layers, 2-5 us); below that, and on the other kernels, fusing pays.
+  if (!igemm_takes_stats(a)) return false;
+  IgemmArgs b = a;
+  b.stat = nullptr;
+  if (igemm_kind(b) == IgemmKind::k3x3) return false;
+  b.stat = reinterpret_cast<float*>(1);
+  return !(igemm_kind(b) == IgemmKind::kDma && (int64_t)a.N * a.OH * a.OW >= 100352);
+}
+
 bool igemm_takes_stats(const IgemmArgs& a) {
   // the kernel that would run with statistics requested (the 3x3 kernel
   // leaves them to the DMA-staged one)
@@ -1714,9 +1693,7 @@ hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st) {
 
 // The stem kernel's problem: 3 input channels (unpadded NHWC, W a multiple
 // of 8), 7x7 filter (KRSC, 147 per output channel), stride 2, pad 3, 64 dense
-// output channels, 16 .. 128 output columns in steps of 16; with statistics
-// also whole 8-row tiles (P a multiple of 8), so that each wave's 128 pixels
-// are one 128-row record.
+// output channels, 16 .. 128 output columns in steps of 16, no statistics.
 bool stem_conv_ok(const IgemmArgs& a) {
   const IgemmPhase& p = a.ph[0];
   const bool shape = a.Ci == 3 && a.nphase == 1 && p.Rt == 7 && p.St == 7 && p.ldb == 147 &&
@@ -1726,7 +1703,7 @@ bool stem_conv_ok(const IgemmArgs& a) {
                      a.Wi == 2 * a.OW && a.OH == p.Ho && a.OW == p.Wo &&
                      a.OW % 16 == 0 && a.OW >= 16 && a.OW <= kStemMaxQ &&
                      (int64_t)a.N * a.Hi * a.Wi * 6 < ((int64_t)1 << 31);
-  return shape && (!a.stat || a.OH % kStemTR == 0);
+  return shape && !a.stat;
 }
 
 hipError_t launch_stem(const IgemmArgs& a, hipStream_t st) {
@@ -1734,10 +1711,7 @@ hipError_t launch_stem(const IgemmArgs& a, hipStream_t st) {
   const int ntiles = a.N * tpi;
   const int grid = ntiles < 256 ? ntiles : 256;
   const dim3 block(a.OW * 4);
-  if (a.stat)
-    hipLaunchKernelGGL(stem_kernel<true>, dim3(grid), block, 0, st, a, ntiles);
-  else
-    hipLaunchKernelGGL(stem_kernel<false>, dim3(grid), block, 0, st, a, ntiles);
+  hipLaunchKernelGGL(stem_kernel, dim3(grid), block, 0, st, a, ntiles);
   return hipGetLastError();
 }
 

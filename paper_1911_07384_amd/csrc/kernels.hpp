@@ -64,6 +64,10 @@ struct IgemmArgs {
 };
 
 hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st);
+// Whether taking the BN statistics in the convolution's epilogue is faster
+// than the convolution without them plus a separate statistics pass (false
+// where the kernel takes none).
+bool igemm_stats_pay(const IgemmArgs& a);
 // The ResNet stem convolution (3 channels, 7x7, stride 2, pad 3, 64 outputs)
 // on its own kernel: act is the unpadded 3-channel image (Ci = 3) and the
 // filter KRSC with ldb = 147.  stem_conv_ok says whether launch_stem takes the

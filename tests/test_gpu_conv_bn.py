@@ -22,12 +22,15 @@ EPS = 1e-5
 # n, c, h, k, r, stride, pad, post_scale, residual, relu, swap
 CASES = [
     (2, 256, 56, 64, 1, 1, 0, 0.25, False, True, False),   # block conv1 + bn1 (register-direct kernel)
-    (4, 64, 56, 64, 3, 1, 1, 0.25, False, True, False),    # 3x3, M > 8192: DMA-staged kernel
+    (4, 64, 56, 64, 3, 1, 1, 0.25, False, True, False),    # 3x3 64-channel: its own kernel, then
+                                                           # the BN's statistics pass
+    (2, 128, 28, 128, 3, 1, 1, 0.25, False, True, False),  # 3x3 128-channel: DMA-staged kernel
+                                                           # with the statistics epilogue
     (2, 64, 28, 256, 1, 1, 0, 0.25, True, True, False),    # block conv3 + bn3 with the shortcut
     (3, 64, 7, 128, 3, 1, 1, 0.25, False, True, False),    # M = 147: ragged last band
     (3, 64, 9, 64, 3, 1, 1, 0.25, False, True, False),     # M = 243, 64 channels: ragged band, narrow tile
-    (2, 3, 32, 64, 7, 2, 3, 1.0, False, True, False),      # the stem, s = 1: stem kernel, records
-                                                           # from one wave per 128 pixels
+    (2, 3, 32, 64, 7, 2, 3, 1.0, False, True, False),      # the stem, s = 1: stem kernel, then the
+                                                           # BN with its own statistics pass
     (1, 3, 224, 64, 7, 2, 3, 1.0, False, True, False),     # the ResNet-50 stem at full size
     (2, 64, 14, 256, 1, 1, 0, 0.25, True, True, True),     # BN swap on the block-last BN
     (2, 128, 15, 64, 3, 2, 1, 0.25, False, False, False),  # strided, no ReLU
