@@ -83,8 +83,10 @@ def call_work(name, s):
         if name.endswith("fwd"):
             byts = 6 * e + (2 * e if name == "bn3_fwd" else 0)  # reduce x; apply x (+r) -> y
         else:
-            # reduce x, dy (+r); apply x, dy (+r) -> dx (+ shortcut gradient)
-            byts = 10 * e + (6 * e if name == "bn3_bwd" else 0)
+            # reduce x, dy (+r); apply x, dy -> dx (+ shortcut gradient); the
+            # ReLU mask the reduce recomputes from r is kept at one bit per
+            # element, which is not counted
+            byts = 10 * e + (4 * e if name == "bn3_bwd" else 0)
         return 0, byts, "hbm"
     if name == "sgd_conv":
         return 0, 10 * sum(co * ci * r * r for ci, co, r in s.conv_shapes), "hbm"

@@ -545,9 +545,13 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
                                                         const h16* __restrict__ res,
                                                         const float* __restrict__ stats, Geo g,
                                                         int CV, int RB, int64_t rpb, float s,
-                                                        float* ws) {
+                                                        float* ws, uint8_t* __restrict__ mbits) {
   constexpr bool SWAP = MODE & kSwap, RELU = MODE & kRelu, MASK_Y = MODE & kMaskY,
                  LOAD_R = MODE & kLoadR;
+  // a mask recomputed from the shortcut is kept, one bit per element and one
+  // byte per 16-byte vector (its index in x), so the apply reads that byte
+  // instead of the shortcut's 16 bytes
+  constexpr bool KEEP_M = LOAD_R && RELU && !MASK_Y;
   constexpr int NS = SWAP ? 3 : 2;
   __shared__ float red[8 * NS * kT];
   const int t = threadIdx.x;
@@ -582,18 +586,21 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
   };
   auto sum_row = [&](const Row& b, int64_t i) {
     const bool ok = rt + i * RB < row1;
+    uint32_t bits = 0;
 #pragma unroll
     for (int e = 0; e < 8; ++e) {
       const float xf = to_f32(b.x.h[e]);
       const float rf = LOAD_R ? to_f32(b.r.h[e]) : 0.0f;
       const bool m = relu_mask(RELU, MASK_Y, MASK_Y ? b.y.h[e] : (h16)0.0f, xf, k[e], LOAD_R, rf,
                                SWAP);
+      bits |= (uint32_t)m << e;
       const float gg = ok && m ? s * to_f32(b.d.h[e]) : 0.0f;
       const float xt = ok ? xf - k[e].mean : 0.0f;
       sums[0][e] += gg;
       sums[1][e] = __builtin_fmaf(gg, xt, sums[1][e]);
       if (SWAP) sums[NS - 1][e] = __builtin_fmaf(gg, ok ? rf : 0.0f, sums[NS - 1][e]);
     }
+    if (KEEP_M && ok) mbits[(rt + i * RB) * CV + j] = (uint8_t)bits;
   };
   Row ra, rb;
   load_row(ra, 0);
@@ -675,10 +682,13 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* 
                                                        const h16* __restrict__ beta, const h16* res,
                                                        const float* __restrict__ stats,
                                                        const float* __restrict__ coef, Geo g,
-                                                       int CV, float s, h16* dx, h16* dres) {
+                                                       int CV, float s,
+                                                       const uint8_t* __restrict__ mbits, h16* dx,
+                                                       h16* dres) {
   constexpr bool SWAP = MODE & kSwap, RELU = MODE & kRelu, MASK_Y = MODE & kMaskY,
                  DRES = MODE & kDres;
-  // the shortcut is read here only for the ReLU mask recomputed from x
+  // the ReLU mask recomputed from x and the shortcut was kept by the reduce:
+  // one byte per vector instead of the shortcut's 16
   constexpr bool NEED_R = (MODE & kLoadR) && RELU && !MASK_Y;
   const int t = threadIdx.x;
   const int j = t % CV;  // run starts and kT are multiples of CV
@@ -697,7 +707,8 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* 
   constexpr int U = kApplyU / 2;  // vectors per thread and run: 2 to 4 loads each
   constexpr int64_t RUN = (int64_t)U * kT;
   for (int64_t run = (int64_t)blockIdx.x * RUN; run < nvec; run += (int64_t)gridDim.x * RUN) {
-    V8 xv[U], dv[U], yv[U], rv[U];
+    V8 xv[U], dv[U], yv[U];
+    uint32_t mb[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int64_t v = run + t + u * kT;
@@ -705,7 +716,7 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* 
       xv[u] = load16(x + vc * 8);
       dv[u] = load16(dy + vc * 8);
       if (MASK_Y) yv[u] = load16(y + vc * 8);
-      if (NEED_R) rv[u] = load16(res + vc * 8);
+      if (NEED_R) mb[u] = mbits[vc];
     }
     __builtin_amdgcn_sched_barrier(0);  // every load issued before the first use
 #pragma unroll
@@ -715,8 +726,9 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* 
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const float xf = to_f32(xv[u].h[e]);
-        const bool m = relu_mask(RELU, MASK_Y, MASK_Y ? yv[u].h[e] : (h16)0.0f, xf, k[e], NEED_R,
-                                 NEED_R ? to_f32(rv[u].h[e]) : 0.0f, SWAP);
+        const bool m = NEED_R ? ((mb[u] >> e) & 1u) != 0
+                              : relu_mask(RELU, MASK_Y, MASK_Y ? yv[u].h[e] : (h16)0.0f, xf, k[e],
+                                          false, 0.0f, SWAP);
         const float gg = m ? s * to_f32(dv[u].h[e]) : 0.0f;
         o.h[e] = to_h16(A[e] * (gg - __builtin_fmaf(xf - k[e].mean, D[e], B[e])));
         if (SWAP)
@@ -816,9 +828,18 @@ size_t partial_bytes(const Plan& p, int C) { return align256((size_t)3 * p.G * C
 
 }  // namespace
 
+// the backward's coefficients, after the partials
+size_t coef_bytes(int C) { return align256((size_t)3 * C * sizeof(float)); }
+
+// the backward's kept ReLU mask, after the coefficients: one byte per 16-byte
+// vector of x
+size_t mask_bytes(const Plan& p, const BnArgs& a) {
+  return p.vec && a.relu ? align256((size_t)((int64_t)a.N * a.H * a.W * p.CV)) : 0;
+}
+
 size_t bn_ws_bytes(const BnArgs& a) {
   const Plan p = make_plan(a);
-  return partial_bytes(p, a.C) + align256((size_t)3 * a.C * sizeof(float));
+  return partial_bytes(p, a.C) + coef_bytes(a.C) + mask_bytes(p, a);
 }
 
 hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const h16* beta,
@@ -885,13 +906,14 @@ hipError_t launch_bn_bwd(const BnArgs& a, const h16* x, const h16* y, const h16*
   const Geo g = make_geo(a);
   float* part = reinterpret_cast<float*>(ws);
   float* coef = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + partial_bytes(p, a.C));
+  uint8_t* mbits = reinterpret_cast<uint8_t*>(ws) + partial_bytes(p, a.C) + coef_bytes(a.C);
   const int mode = bwd_mode(a, y, res, dres);
   if (p.vec) {
     switch (mode & ~kDres) {
 #define FP16K_CASE(m)                                                                          \
   case m:                                                                                      \
     hipLaunchKernelGGL(bn_bwd_reduce_vec<m>, dim3(p.G), dim3(kT), 0, st, x, y, dy, gamma, beta, \
-                       res, stats, g, p.CV, p.RB, p.rpb, a.post_scale, part);                    \
+                       res, stats, g, p.CV, p.RB, p.rpb, a.post_scale, part, mbits);             \
     break;
       FP16K_BN_BWD_MODES(FP16K_CASE)
 #undef FP16K_CASE
@@ -910,7 +932,7 @@ hipError_t launch_bn_bwd(const BnArgs& a, const h16* x, const h16* y, const h16*
 #define FP16K_CASE(m)                                                                          \
   case m:                                                                                      \
     hipLaunchKernelGGL(bn_bwd_apply_vec<m>, grid, dim3(kT), 0, st, x, y, dy, gamma, beta, res, \
-                       stats, coef, g, p.CV, a.post_scale, dx, dres);                           \
+                       stats, coef, g, p.CV, a.post_scale, mbits, dx, dres);                    \
     break;
       FP16K_BN_BWD_APPLY_MODES(FP16K_CASE)
 #undef FP16K_CASE
