@@ -332,7 +332,6 @@ def sgd_f16(w, g, m, lr, momentum, weight_decay):
 
 
 def _f16acc(fn, shp, a, b, which):
-    assert int(shp[11]) == 0, "binary16 accumulation is defined for NHWC / KRSC"
     a, b = _h(a), _h(b)
     out = np.empty(_act_shape(shp, which), np.uint16)
     fn(_ptr(shp), _ptr(a), _ptr(b), _ptr(out))
@@ -340,15 +339,21 @@ def _f16acc(fn, shp, a, b, which):
 
 
 def conv_fwd_f16acc(shp, x, w):
-    """Forward convolution with a binary16 accumulator rounded per 16 terms."""
+    """Forward convolution with every operation in binary16: each output is
+    a chain of binary16 fmas from +0 over its in-image terms, taps (r, s)
+    row-major, channels ascending within a tap."""
     return _f16acc(lib().oracle_conv_fwd_f16acc, shp, x, w, "y")
 
 
 def conv_dgrad_f16acc(shp, dy, w):
+    """Data gradient as a binary16 fma chain: taps (r, s) row-major that
+    reach the position from the output grid, output channels ascending."""
     return _f16acc(lib().oracle_conv_dgrad_f16acc, shp, dy, w, "x")
 
 
 def conv_wgrad_f16acc(shp, x, dy):
+    """Weight gradient as a binary16 fma chain over the output pixels
+    (n, p, q) in order, in-image taps only."""
     return _f16acc(lib().oracle_conv_wgrad_f16acc, shp, x, dy, "w")
 
 

@@ -800,27 +800,6 @@ uint16_t fma_half(uint16_t a16, uint16_t b16, uint16_t c16) {
   return round_half_exact(s, err);
 }
 
-// Convolution reductions in the strict mode: the accumulator is a binary16
-// value, updated once per block of 16 consecutive terms of the reduction
-// order (the matrix-core granularity): acc = round(acc + sum of the block),
-// the block sum taken in double.
-struct Acc16 {
-  double acc = 0.0, block = 0.0;
-  int64_t in_block = 0;
-  void add(double t) {
-    block += t;
-    if (++in_block == 16) flush();
-  }
-  void flush() {
-    if (in_block == 0) return;
-    acc = half_to_double(round_half(acc + block));
-    block = 0.0;
-    in_block = 0;
-  }
-};
-
-inline int64_t round8(int64_t v) { return (v + 7) / 8 * 8; }
-
 }  // namespace
 
 extern "C" {
@@ -849,72 +828,60 @@ void oracle_sgd_f16(uint16_t* w16, const uint16_t* g16, uint16_t* m16, int64_t n
   }
 }
 
-// Forward convolution with binary16 accumulation (NHWC / KRSC).  Reduction
-// order: taps (r, s) row-major, channels c fastest over Cp = C rounded up
-// to a multiple of 8 (channels >= C, and taps outside the image, are zero
-// terms that still take their place in the blocks of 16).
+// Convolutions with every operation in binary16 (Section 5.2 read
+// literally: all arithmetic in FP16).  Each output is a binary16
+// accumulator that starts at +0 and takes its terms one at a time, each as
+// one binary16 fused multiply-add, acc = round(a * b + acc) (one rounding of
+// the exact value).  The reduction order is declared per pass below, in the
+// logical indices of the convolution's definition; a tap whose position lies
+// outside the input image (forward, weight gradient) or outside the output
+// grid (data gradient) is not a term.  Any layout.
+
+// y[n,k,p,q]: taps (r, s) in row-major order, channels c ascending within a tap.
 void oracle_conv_fwd_f16acc(const int32_t* shp, const uint16_t* x16, const uint16_t* w16,
                             uint16_t* y16) {
   const Conv d(shp);
-  const int64_t Cp = round8(d.C);
 #pragma omp parallel for schedule(static)
   for (int64_t i = 0; i < d.y_size(); ++i) {
     int64_t n, k, p, q;
     d.y_coords(i, &n, &k, &p, &q);
-    Acc16 a;
+    uint16_t acc = 0x0000;
     for (int64_t r = 0; r < d.R; ++r)
       for (int64_t s = 0; s < d.S; ++s) {
         const int64_t h = p * d.sh - d.ph + r, ww = q * d.sw - d.pw + s;
-        const bool in = h >= 0 && h < d.H && ww >= 0 && ww < d.W;
-        for (int64_t c = 0; c < Cp; ++c)
-          a.add(in && c < d.C ? half_to_double(x16[d.xi(n, c, h, ww)]) *
-                                    half_to_double(w16[d.wi(k, c, r, s)])
-                              : 0.0);
+        if (h < 0 || h >= d.H || ww < 0 || ww >= d.W) continue;
+        for (int64_t c = 0; c < d.C; ++c)
+          acc = fma_half(x16[d.xi(n, c, h, ww)], w16[d.wi(k, c, r, s)], acc);
       }
-    a.flush();
-    y16[i] = round_half(a.acc);
+    y16[i] = acc;
   }
 }
 
-// Data gradient with binary16 accumulation (NHWC / KRSC).  For the output
-// position (h, w) the reduction runs over the taps that reach it, in
-// decreasing r, then decreasing s (those with r = (h + pad_h) mod stride_h,
-// and likewise s, up the filter), and within a tap over the output channels
-// k < Kp (K rounded up to a multiple of 8); a tap whose source position lies
-// outside the P x Q grid contributes zero terms in its place.
+// dx[n,c,h,w]: the taps (r, s) in row-major order whose output position
+// p = (h + pad_h - r) / stride_h, q = (w + pad_w - s) / stride_w is a whole
+// grid point inside P x Q, and within a tap the output channels k ascending.
 void oracle_conv_dgrad_f16acc(const int32_t* shp, const uint16_t* dy16, const uint16_t* w16,
                               uint16_t* dx16) {
   const Conv d(shp);
-  const int64_t Kp = round8(d.K);
 #pragma omp parallel for schedule(static)
   for (int64_t i = 0; i < d.x_size(); ++i) {
     int64_t n, c, h, ww;
     d.x_coords(i, &n, &c, &h, &ww);
-    const int64_t r0 = (h + d.ph) % d.sh, s0 = (ww + d.pw) % d.sw;
-    Acc16 a;
-    int64_t rtop = r0;
-    while (rtop + d.sh < d.R) rtop += d.sh;
-    int64_t stop = s0;
-    while (stop + d.sw < d.S) stop += d.sw;
-    if (r0 < d.R && s0 < d.S) {
-      for (int64_t r = rtop; r >= r0; r -= d.sh)
-        for (int64_t s = stop; s >= s0; s -= d.sw) {
-          const int64_t p = (h + d.ph - r) / d.sh, q = (ww + d.pw - s) / d.sw;
-          const bool in = h + d.ph - r >= 0 && ww + d.pw - s >= 0 && p < d.P && q < d.Q;
-          for (int64_t k = 0; k < Kp; ++k)
-            a.add(in && k < d.K ? half_to_double(dy16[d.yi(n, k, p, q)]) *
-                                      half_to_double(w16[d.wi(k, c, r, s)])
-                                : 0.0);
-        }
-    }
-    a.flush();
-    dx16[i] = round_half(a.acc);
+    uint16_t acc = 0x0000;
+    for (int64_t r = 0; r < d.R; ++r)
+      for (int64_t s = 0; s < d.S; ++s) {
+        const int64_t ph = h + d.ph - r, pw = ww + d.pw - s;
+        if (ph < 0 || pw < 0 || ph % d.sh != 0 || pw % d.sw != 0) continue;
+        const int64_t p = ph / d.sh, q = pw / d.sw;
+        if (p >= d.P || q >= d.Q) continue;
+        for (int64_t k = 0; k < d.K; ++k)
+          acc = fma_half(dy16[d.yi(n, k, p, q)], w16[d.wi(k, c, r, s)], acc);
+      }
+    dx16[i] = acc;
   }
 }
 
-// Weight gradient with binary16 accumulation (NHWC / KRSC): the reduction
-// runs over the output pixels (n, p, q) in order, every pixel taking its
-// place in the blocks of 16 (a tap outside the image gives a zero term).
+// dW[k,c,r,s]: the output pixels (n, p, q) in order (n slowest, q fastest).
 void oracle_conv_wgrad_f16acc(const int32_t* shp, const uint16_t* x16, const uint16_t* dy16,
                               uint16_t* dw16) {
   const Conv d(shp);
@@ -922,17 +889,15 @@ void oracle_conv_wgrad_f16acc(const int32_t* shp, const uint16_t* x16, const uin
   for (int64_t i = 0; i < d.w_size(); ++i) {
     int64_t k, c, r, s;
     d.w_coords(i, &k, &c, &r, &s);
-    Acc16 a;
+    uint16_t acc = 0x0000;
     for (int64_t n = 0; n < d.N; ++n)
       for (int64_t p = 0; p < d.P; ++p)
         for (int64_t q = 0; q < d.Q; ++q) {
           const int64_t h = p * d.sh - d.ph + r, ww = q * d.sw - d.pw + s;
-          const bool in = h >= 0 && h < d.H && ww >= 0 && ww < d.W;
-          a.add(in ? half_to_double(dy16[d.yi(n, k, p, q)]) * half_to_double(x16[d.xi(n, c, h, ww)])
-                   : 0.0);
+          if (h < 0 || h >= d.H || ww < 0 || ww >= d.W) continue;
+          acc = fma_half(dy16[d.yi(n, k, p, q)], x16[d.xi(n, c, h, ww)], acc);
         }
-    a.flush();
-    dw16[i] = round_half(a.acc);
+    dw16[i] = acc;
   }
 }
 

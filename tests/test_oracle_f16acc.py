@@ -8,16 +8,19 @@ accumulators of the default path buy.
 - SGD with binary16 arithmetic: exact rational evaluation of the three
   fused multiply-adds with binary16 scalars; one hand-derived example where
   the extra rounding of d changes the momentum by one ulp.
-- Convolutions with a binary16 accumulator rounded once per 16 terms:
-  (a) with at most 16 terms there is one rounding, so the result equals the
+- Convolutions as chains of binary16 fmas (one rounding per term, in a
+  declared order, padding taps not terms):
+  (a) a reduction of one term is one rounding of one product, equal to the
       (separately pinned) single rounding of the exact sum;
   (b) on small-integer data every partial sum is a binary16 integer, so the
       result is exact;
-  (c) an independent brute force on tiny shapes -- the reduction written
-      out as an explicit im2col row for the forward and the weight gradient,
-      and for the data gradient as the list of forward contributions that
-      reach the position, sorted by the declared key -- accumulated in exact
-      rationals with one binary16 rounding per block of 16.
+  (c) hand-derived values: 4,096 terms of 1.0 stagnate at 2048 (2048 + 1 is
+      a tie and rounds to even), and 1 + 2^-11 + 2^-11 taken in channel
+      order stays 1 while the exact sum 1 + 2^-10 is representable;
+  (d) an independent brute force on tiny shapes: the terms of each output
+      enumerated from the index formulas of Section 5.1's convolutions,
+      sorted by the declared key, and chained in exact rational arithmetic
+      with one binary16 rounding per term (signed zeros by the IEEE rules).
 """
 
 from fractions import Fraction
@@ -141,18 +144,89 @@ def _inputs(shp, seed, grid=None, scale=1.0):
     return x, wt, dy
 
 
-@pytest.mark.parametrize("c,k", [(8, 4), (16, 16), (3, 5)])
-def test_single_block_equals_one_rounding(c, k):
-    # 1x1: the forward reduction has Cp <= 16 terms, the data gradient Kp <= 16,
-    # the weight gradient N*P*Q <= 16 pixels
-    shp = oracle.conv_shape(1, c, 4, 4, k, 1, 1)
-    x, w, dy = _inputs(shp, 11)
-    assert np.array_equal(oracle.conv_fwd_f16acc(shp, x, w).view(np.uint16),
-                          oracle.conv_fwd(shp, x, w)[1].view(np.uint16))
-    assert np.array_equal(oracle.conv_dgrad_f16acc(shp, dy, w).view(np.uint16),
-                          oracle.conv_dgrad(shp, dy, w)[1].view(np.uint16))
-    assert np.array_equal(oracle.conv_wgrad_f16acc(shp, x, dy).view(np.uint16),
-                          oracle.conv_wgrad(shp, x, dy)[1].view(np.uint16))
+def _fma_bits(a, b, c):
+    """binary16 bits of round(a*b + c) from exact rationals, with the IEEE
+    sign of an exact zero (+0 unless the product and c are both -0)."""
+    q = half_value(a) * half_value(b) + half_value(c)
+    if q == 0:
+        prod_neg = (a ^ b) & 0x8000
+        return 0x8000 if (prod_neg and (c & 0x8000) and half_value(c) == 0) else 0
+    return to_half_bits(q)
+
+
+def _chain(pairs):
+    acc = 0x0000
+    for a, b in pairs:
+        acc = _fma_bits(a, b, acc)
+    return acc
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 4, 4, 1, 1, 1, 1, 0), (1, 1, 5, 5, 1, 1, 1, 2, 0)])
+def test_one_term_is_one_rounding(shape):
+    # C = K = R = S = N*P*Q... = 1 term per output: fma16(a, b, +0) = RNE16(a*b)
+    n, c, h, w, k, r, s, st, pad = shape
+    shp = oracle.conv_shape(n, c, h, w, k, r, s, st, pad)
+    x, wt, dy = _inputs(shp, 11)
+    assert np.array_equal(oracle.conv_fwd_f16acc(shp, x, wt).view(np.uint16),
+                          oracle.conv_fwd(shp, x, wt)[1].view(np.uint16))
+    assert np.array_equal(oracle.conv_dgrad_f16acc(shp, dy, wt).view(np.uint16),
+                          oracle.conv_dgrad(shp, dy, wt)[1].view(np.uint16))
+    shp1 = oracle.conv_shape(1, 3, 1, 1, 2, 1, 1)
+    x1, _, dy1 = _inputs(shp1, 12)
+    assert np.array_equal(oracle.conv_wgrad_f16acc(shp1, x1, dy1).view(np.uint16),
+                          oracle.conv_wgrad(shp1, x1, dy1)[1].view(np.uint16))
+
+
+def test_stagnation_worked_example():
+    # 4,096 channels of x = 1, w = 1: the chain reaches 2048, where the
+    # binary16 spacing is 2, so 2048 + 1 is a tie that rounds to even (2048)
+    # and every further term is lost.  One rounding of the exact sum gives
+    # 4096.  (A 16-term block accumulator would reach 4096 exactly.)
+    shp = oracle.conv_shape(1, 4096, 1, 1, 1, 1, 1)
+    x = np.ones((1, 1, 1, 4096), np.float16)
+    w = np.ones((1, 1, 1, 4096), np.float16)
+    assert int(oracle.conv_fwd_f16acc(shp, x, w).view(np.uint16)[0, 0, 0, 0]) == 0x6800
+    assert float(oracle.conv_fwd(shp, x, w)[1][0, 0, 0, 0]) == 4096.0
+    # the same through the weight gradient: 4,096 pixels of dy = x = 1
+    shpw = oracle.conv_shape(1, 1, 64, 64, 1, 1, 1)
+    ones = np.ones((1, 64, 64, 1), np.float16)
+    assert int(oracle.conv_wgrad_f16acc(shpw, ones, ones).view(np.uint16).reshape(-1)[0]) == 0x6800
+    # and the data gradient: 4,096 output channels
+    shpd = oracle.conv_shape(1, 1, 1, 1, 4096, 1, 1)
+    assert int(oracle.conv_dgrad_f16acc(shpd, np.ones((1, 1, 1, 4096), np.float16),
+                                        np.ones((4096, 1, 1, 1), np.float16))
+               .view(np.uint16).reshape(-1)[0]) == 0x6800
+
+
+def test_order_worked_example():
+    # channels (1, 2^-11, 2^-11) against w = 1: 1 + 2^-11 is a tie between 1
+    # and 1 + 2^-10 and rounds to even (1), twice; the exact sum 1 + 2^-10
+    # (0x3C01) is what one rounding gives.  With the channels in the other
+    # order the chain reaches it too: the order is part of the definition.
+    shp = oracle.conv_shape(1, 3, 1, 1, 1, 1, 1)
+    w = np.ones((1, 1, 1, 3), np.float16)
+    x = np.array([1.0, 2.0 ** -11, 2.0 ** -11], np.float16).reshape(1, 1, 1, 3)
+    assert int(oracle.conv_fwd_f16acc(shp, x, w).view(np.uint16).reshape(-1)[0]) == 0x3C00
+    assert int(oracle.conv_fwd(shp, x, w)[1].view(np.uint16).reshape(-1)[0]) == 0x3C01
+    xr = x[..., ::-1].copy()
+    assert int(oracle.conv_fwd_f16acc(shp, xr, w).view(np.uint16).reshape(-1)[0]) == 0x3C01
+
+
+def test_signed_zero_and_padding_are_not_terms():
+    # a single tiny negative product rounds to -0; a padding tap after it is
+    # not a term, so -0 stays (a +0 term would turn it into +0)
+    shp = oracle.conv_shape(1, 1, 1, 2, 1, 1, 3, 1, (0, 1))   # W = 2, S = 3, pad 1 along w
+    x = np.array([2.0 ** -24, 0.0], np.float16).reshape(1, 1, 2, 1)
+    w = np.array([0.0, -0.25, 0.0], np.float16).reshape(1, 1, 3, 1)
+    y = oracle.conv_fwd_f16acc(shp, x, w).view(np.uint16).reshape(-1)
+    # q = 0: taps s = 1 (x[0] * -0.25 = -2^-26 -> -0), s = 2 (x[1] = 0 times +0 = +0: -0 + +0 = +0)
+    assert int(y[0]) == 0x0000
+    # q = 1: taps s = 0 (x[0] * +0 = +0), s = 1 (x[1] = +0 * -0.25 = -0: +0 + -0 = +0), s = 2 padding
+    assert int(y[1]) == 0x0000
+    x2 = np.array([0.0, 2.0 ** -24], np.float16).reshape(1, 1, 2, 1)
+    # q = 1: s = 0: +0*+0 = +0; s = 1: 2^-24 * -0.25 -> -0: +0 + -2^-26 rounds to -0;
+    # s = 2 lies in the padding and is not a term, so -0 remains
+    assert int(oracle.conv_fwd_f16acc(shp, x2, w).view(np.uint16).reshape(-1)[1]) == 0x8000
 
 
 @pytest.mark.parametrize("shape", [(2, 24, 7, 6, 10, 3, 3, 1, 1), (2, 16, 9, 9, 8, 3, 3, 2, 1),
@@ -168,76 +242,79 @@ def test_integer_grid_is_exact(shape):
         assert np.array_equal(strict.astype(np.float64), ref64)
 
 
-def _blocks16(terms):
-    """Binary16 accumulator updated once per block of 16 exact terms."""
-    acc = Fraction(0)
-    for i in range(0, len(terms), 16):
-        acc = half_value(to_half_bits(acc + sum(terms[i:i + 16], Fraction(0))))
-    return to_half_bits(acc)
-
-
-def _hv(a):
-    return [half_value(int(b)) for b in np.ascontiguousarray(a).view(np.uint16).reshape(-1)]
+def _bits(a):
+    return np.ascontiguousarray(a).view(np.uint16)
 
 
 @pytest.mark.parametrize("shape", [(1, 3, 5, 5, 4, 3, 3, 1, 1), (2, 8, 6, 5, 3, 3, 3, 2, 1),
-                                   (1, 5, 7, 7, 2, 3, 3, 2, 0), (1, 16, 4, 4, 8, 1, 1, 2, 0)])
-def test_brute_force_block_order(shape):
+                                   (1, 5, 7, 7, 2, 3, 3, 2, 0), (1, 16, 4, 4, 8, 1, 1, 2, 0),
+                                   (1, 2, 9, 9, 3, 7, 7, 2, 3)])
+def test_brute_force_chain_order(shape):
     n, c, h, w, k, r, s, st, pad = shape
     shp = oracle.conv_shape(n, c, h, w, k, r, s, st, pad)
     p, q = oracle.conv_out_dims(shp)
     x, wt, dy = _inputs(shp, 13, scale=3.0)
-    X = np.array(_hv(x), dtype=object).reshape(n, h, w, c)
-    Wt = np.array(_hv(wt), dtype=object).reshape(k, r, s, c)
-    DY = np.array(_hv(dy), dtype=object).reshape(n, p, q, k)
-    cp, kp = (c + 7) // 8 * 8, (k + 7) // 8 * 8
+    X, Wt, DY = _bits(x), _bits(wt), _bits(dy)
 
-    def xat(b, i, j, ch):
-        return X[b, i, j, ch] if 0 <= i < h and 0 <= j < w and ch < c else Fraction(0)
-
-    # forward: the im2col row of (b, i, j) against filter row kk, columns (r, s, c < Cp)
-    got = oracle.conv_fwd_f16acc(shp, x, wt).view(np.uint16)
+    # forward: every (r, s, c) whose position lies in the image, keyed (r, s, c)
+    got = _bits(oracle.conv_fwd_f16acc(shp, x, wt))
     for b in range(n):
         for i in range(p):
             for j in range(q):
-                col = [xat(b, i * st - pad + rr, j * st - pad + ss, ch)
-                       for rr in range(r) for ss in range(s) for ch in range(cp)]
                 for kk in range(k):
-                    wrow = [Wt[kk, rr, ss, ch] if ch < c else Fraction(0)
-                            for rr in range(r) for ss in range(s) for ch in range(cp)]
-                    want = _blocks16([a * bb for a, bb in zip(col, wrow)])
+                    terms = []
+                    for rr in range(r):
+                        for ss in range(s):
+                            hi, wj = i * st - pad + rr, j * st - pad + ss
+                            if 0 <= hi < h and 0 <= wj < w:
+                                terms += [((rr, ss, ch), int(X[b, hi, wj, ch]), int(Wt[kk, rr, ss, ch]))
+                                          for ch in range(c)]
+                    terms.sort(key=lambda t: t[0])
+                    want = _chain([(a_, b_) for _, a_, b_ in terms])
                     assert int(got[b, i, j, kk]) == want, ("fwd", b, i, j, kk)
 
-    # data gradient: enumerate every forward term x[b, hh, ww, cc] * W[kk, rr, ss, cc]
-    # that touches (hh, ww); the declared order is taps by decreasing (r, s)
-    # among those that reach the position (whether or not their source lies on
-    # the output grid), then output channels k < Kp
-    got = oracle.conv_dgrad_f16acc(shp, dy, wt).view(np.uint16)
+    # data gradient: every forward term x[b, hh, ww, cc] * W[kk, rr, ss, cc] that
+    # lands on an output grid point, keyed (r, s, k)
+    got = _bits(oracle.conv_dgrad_f16acc(shp, dy, wt))
     for b in range(n):
         for hh in range(h):
             for ww in range(w):
-                taps = [(rr, ss) for rr in range(r) for ss in range(s)
-                        if (hh + pad - rr) % st == 0 and (ww + pad - ss) % st == 0]
-                taps.sort(reverse=True)
                 for cc in range(c):
                     terms = []
-                    for rr, ss in taps:
-                        pi, qj = (hh + pad - rr) // st, (ww + pad - ss) // st
-                        on = 0 <= pi < p and 0 <= qj < q and hh + pad - rr >= 0 and ww + pad - ss >= 0
-                        for kk in range(kp):
-                            terms.append(DY[b, pi, qj, kk] * Wt[kk, rr, ss, cc]
-                                         if on and kk < k else Fraction(0))
-                    assert int(got[b, hh, ww, cc]) == _blocks16(terms), ("dgrad", b, hh, ww, cc)
+                    for i in range(p):
+                        for j in range(q):
+                            rr, ss = hh - (i * st - pad), ww - (j * st - pad)
+                            if 0 <= rr < r and 0 <= ss < s:
+                                terms += [((rr, ss, kk), int(DY[b, i, j, kk]), int(Wt[kk, rr, ss, cc]))
+                                          for kk in range(k)]
+                    terms.sort(key=lambda t: t[0])
+                    want = _chain([(a_, b_) for _, a_, b_ in terms])
+                    assert int(got[b, hh, ww, cc]) == want, ("dgrad", b, hh, ww, cc)
 
-    # weight gradient: pixels (b, i, j) in order
-    got = oracle.conv_wgrad_f16acc(shp, x, dy).view(np.uint16)
+    # weight gradient: output pixels (b, i, j) in order, in-image taps only
+    got = _bits(oracle.conv_wgrad_f16acc(shp, x, dy))
     for kk in range(k):
         for rr in range(r):
             for ss in range(s):
                 for cc in range(c):
-                    terms = [DY[b, i, j, kk] * xat(b, i * st - pad + rr, j * st - pad + ss, cc)
-                             for b in range(n) for i in range(p) for j in range(q)]
-                    assert int(got[kk, rr, ss, cc]) == _blocks16(terms), ("wgrad", kk, rr, ss, cc)
+                    pairs = [(int(DY[b, i, j, kk]), int(X[b, i * st - pad + rr, j * st - pad + ss, cc]))
+                             for b in range(n) for i in range(p) for j in range(q)
+                             if 0 <= i * st - pad + rr < h and 0 <= j * st - pad + ss < w]
+                    assert int(got[kk, rr, ss, cc]) == _chain(pairs), ("wgrad", kk, rr, ss, cc)
+
+
+def test_any_layout_same_values():
+    # the order is declared in logical indices, so NCHW gives the same values
+    shp = oracle.conv_shape(2, 6, 5, 5, 4, 3, 3, 2, 1)
+    shq = oracle.conv_shape(2, 6, 5, 5, 4, 3, 3, 2, 1, layout="NCHW")
+    x, wt, dy = _inputs(shp, 15)
+    xn, wn, dyn = x.transpose(0, 3, 1, 2).copy(), wt.transpose(0, 3, 1, 2).copy(), dy.transpose(0, 3, 1, 2).copy()
+    assert np.array_equal(_bits(oracle.conv_fwd_f16acc(shp, x, wt)).transpose(0, 3, 1, 2),
+                          _bits(oracle.conv_fwd_f16acc(shq, xn, wn)))
+    assert np.array_equal(_bits(oracle.conv_dgrad_f16acc(shp, dy, wt)).transpose(0, 3, 1, 2),
+                          _bits(oracle.conv_dgrad_f16acc(shq, dyn, wn)))
+    assert np.array_equal(_bits(oracle.conv_wgrad_f16acc(shp, x, dy)).transpose(0, 3, 1, 2),
+                          _bits(oracle.conv_wgrad_f16acc(shq, xn, dyn)))
 
 
 def test_binary16_accumulation_costs_accuracy():
