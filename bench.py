@@ -211,8 +211,8 @@ def resnet50_leg(torch, steps: int, warmup: int = 3, batch: int = 128):
 def f16_arith_leg(torch, reps: int = 10):
     """Timing of the strict binary16-arithmetic mode next to the default:
     the SGD update over the ResNet-50 parameter count, and the three passes
-    of the conv4_x 3x3 layer (256 -> 256, 14x14, batch 128) with binary16
-    accumulation (accum = 1) and with float32 accumulators."""
+    of the conv4_x 3x3 layer (256 -> 256, 14x14, batch 128) as chains of
+    binary16 fmas (accum = 1) and with float32 accumulators."""
     import paper_1911_07384_amd as F
     gen = torch.Generator(device="cuda")
     gen.manual_seed(5)
@@ -257,9 +257,10 @@ def f16_arith_leg(torch, reps: int = 10):
             ms = timed(fn)
             row[pname] = {"us": round(ms * 1e3, 2), "tflops": round(flop / (ms * 1e-3) / 1e12, 1)}
         out["conv4x_3x3_b128_" + ("binary16_acc" if accum else "float32_acc")] = row
-    out["note"] = ("strict binary16 arithmetic (accum = 1 convolutions: the accumulator rounded to "
-                   "binary16 after every 16 terms, weight gradient unsplit; fp16_sgd_step_f16: three "
-                   "binary16 fmas) next to the default float32 accumulators / float32 sequence")
+    out["note"] = ("strict binary16 arithmetic (accum = 1 convolutions: every output a chain of "
+                   "binary16 fmas, one rounding per term, on the vector ALUs; fp16_sgd_step_f16: "
+                   "three binary16 fmas) next to the default float32 accumulators / float32 "
+                   "sequence")
     return out
 
 

@@ -75,6 +75,9 @@ _SIGS = {
     "oracle_conv_fwd_f16acc": (None, [_P, _P, _P, _P]),
     "oracle_conv_dgrad_f16acc": (None, [_P, _P, _P, _P]),
     "oracle_conv_wgrad_f16acc": (None, [_P, _P, _P, _P]),
+    "oracle_conv_fwd_f16acc_at": (None, [_P, _P, _P, _P, _I64, _P]),
+    "oracle_conv_dgrad_f16acc_at": (None, [_P, _P, _P, _P, _I64, _P]),
+    "oracle_conv_wgrad_f16acc_at": (None, [_P, _P, _P, _P, _I64, _P]),
 }
 
 
@@ -355,6 +358,27 @@ def conv_wgrad_f16acc(shp, x, dy):
     """Weight gradient as a binary16 fma chain over the output pixels
     (n, p, q) in order, in-image taps only."""
     return _f16acc(lib().oracle_conv_wgrad_f16acc, shp, x, dy, "w")
+
+
+def _f16acc_at(fn, shp, a, b, idx):
+    a, b = _h(a), _h(b)
+    idx = np.ascontiguousarray(idx, dtype=np.int64)
+    out = np.empty(idx.size, np.uint16)
+    fn(_ptr(shp), _ptr(a), _ptr(b), _ptr(idx), idx.size, _ptr(out))
+    return out.view(np.float16)
+
+
+def conv_fwd_f16acc_at(shp, x, w, idx):
+    """conv_fwd_f16acc at the flat output indices idx only."""
+    return _f16acc_at(lib().oracle_conv_fwd_f16acc_at, shp, x, w, idx)
+
+
+def conv_dgrad_f16acc_at(shp, dy, w, idx):
+    return _f16acc_at(lib().oracle_conv_dgrad_f16acc_at, shp, dy, w, idx)
+
+
+def conv_wgrad_f16acc_at(shp, x, dy, idx):
+    return _f16acc_at(lib().oracle_conv_wgrad_f16acc_at, shp, x, dy, idx)
 
 
 # ---- pooling, classifier bias and loss --------------------------------------

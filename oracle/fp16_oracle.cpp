@@ -837,68 +837,104 @@ void oracle_sgd_f16(uint16_t* w16, const uint16_t* g16, uint16_t* m16, int64_t n
 // outside the input image (forward, weight gradient) or outside the output
 // grid (data gradient) is not a term.  Any layout.
 
+}  // extern "C"
+
+namespace {
+
 // y[n,k,p,q]: taps (r, s) in row-major order, channels c ascending within a tap.
-void oracle_conv_fwd_f16acc(const int32_t* shp, const uint16_t* x16, const uint16_t* w16,
-                            uint16_t* y16) {
-  const Conv d(shp);
-#pragma omp parallel for schedule(static)
-  for (int64_t i = 0; i < d.y_size(); ++i) {
-    int64_t n, k, p, q;
-    d.y_coords(i, &n, &k, &p, &q);
-    uint16_t acc = 0x0000;
-    for (int64_t r = 0; r < d.R; ++r)
-      for (int64_t s = 0; s < d.S; ++s) {
-        const int64_t h = p * d.sh - d.ph + r, ww = q * d.sw - d.pw + s;
-        if (h < 0 || h >= d.H || ww < 0 || ww >= d.W) continue;
-        for (int64_t c = 0; c < d.C; ++c)
-          acc = fma_half(x16[d.xi(n, c, h, ww)], w16[d.wi(k, c, r, s)], acc);
-      }
-    y16[i] = acc;
-  }
+uint16_t fwd_chain(const Conv& d, const uint16_t* x16, const uint16_t* w16, int64_t i) {
+  int64_t n, k, p, q;
+  d.y_coords(i, &n, &k, &p, &q);
+  uint16_t acc = 0x0000;
+  for (int64_t r = 0; r < d.R; ++r)
+    for (int64_t s = 0; s < d.S; ++s) {
+      const int64_t h = p * d.sh - d.ph + r, ww = q * d.sw - d.pw + s;
+      if (h < 0 || h >= d.H || ww < 0 || ww >= d.W) continue;
+      for (int64_t c = 0; c < d.C; ++c)
+        acc = fma_half(x16[d.xi(n, c, h, ww)], w16[d.wi(k, c, r, s)], acc);
+    }
+  return acc;
 }
 
 // dx[n,c,h,w]: the taps (r, s) in row-major order whose output position
 // p = (h + pad_h - r) / stride_h, q = (w + pad_w - s) / stride_w is a whole
 // grid point inside P x Q, and within a tap the output channels k ascending.
+uint16_t dgrad_chain(const Conv& d, const uint16_t* dy16, const uint16_t* w16, int64_t i) {
+  int64_t n, c, h, ww;
+  d.x_coords(i, &n, &c, &h, &ww);
+  uint16_t acc = 0x0000;
+  for (int64_t r = 0; r < d.R; ++r)
+    for (int64_t s = 0; s < d.S; ++s) {
+      const int64_t ph = h + d.ph - r, pw = ww + d.pw - s;
+      if (ph < 0 || pw < 0 || ph % d.sh != 0 || pw % d.sw != 0) continue;
+      const int64_t p = ph / d.sh, q = pw / d.sw;
+      if (p >= d.P || q >= d.Q) continue;
+      for (int64_t k = 0; k < d.K; ++k)
+        acc = fma_half(dy16[d.yi(n, k, p, q)], w16[d.wi(k, c, r, s)], acc);
+    }
+  return acc;
+}
+
+// dW[k,c,r,s]: the output pixels (n, p, q) in order (n slowest, q fastest).
+uint16_t wgrad_chain(const Conv& d, const uint16_t* x16, const uint16_t* dy16, int64_t i) {
+  int64_t k, c, r, s;
+  d.w_coords(i, &k, &c, &r, &s);
+  uint16_t acc = 0x0000;
+  for (int64_t n = 0; n < d.N; ++n)
+    for (int64_t p = 0; p < d.P; ++p)
+      for (int64_t q = 0; q < d.Q; ++q) {
+        const int64_t h = p * d.sh - d.ph + r, ww = q * d.sw - d.pw + s;
+        if (h < 0 || h >= d.H || ww < 0 || ww >= d.W) continue;
+        acc = fma_half(dy16[d.yi(n, k, p, q)], x16[d.xi(n, c, h, ww)], acc);
+      }
+  return acc;
+}
+
+}  // namespace
+
+extern "C" {
+
+void oracle_conv_fwd_f16acc(const int32_t* shp, const uint16_t* x16, const uint16_t* w16,
+                            uint16_t* y16) {
+  const Conv d(shp);
+#pragma omp parallel for schedule(static)
+  for (int64_t i = 0; i < d.y_size(); ++i) y16[i] = fwd_chain(d, x16, w16, i);
+}
+
 void oracle_conv_dgrad_f16acc(const int32_t* shp, const uint16_t* dy16, const uint16_t* w16,
                               uint16_t* dx16) {
   const Conv d(shp);
 #pragma omp parallel for schedule(static)
-  for (int64_t i = 0; i < d.x_size(); ++i) {
-    int64_t n, c, h, ww;
-    d.x_coords(i, &n, &c, &h, &ww);
-    uint16_t acc = 0x0000;
-    for (int64_t r = 0; r < d.R; ++r)
-      for (int64_t s = 0; s < d.S; ++s) {
-        const int64_t ph = h + d.ph - r, pw = ww + d.pw - s;
-        if (ph < 0 || pw < 0 || ph % d.sh != 0 || pw % d.sw != 0) continue;
-        const int64_t p = ph / d.sh, q = pw / d.sw;
-        if (p >= d.P || q >= d.Q) continue;
-        for (int64_t k = 0; k < d.K; ++k)
-          acc = fma_half(dy16[d.yi(n, k, p, q)], w16[d.wi(k, c, r, s)], acc);
-      }
-    dx16[i] = acc;
-  }
+  for (int64_t i = 0; i < d.x_size(); ++i) dx16[i] = dgrad_chain(d, dy16, w16, i);
 }
 
-// dW[k,c,r,s]: the output pixels (n, p, q) in order (n slowest, q fastest).
 void oracle_conv_wgrad_f16acc(const int32_t* shp, const uint16_t* x16, const uint16_t* dy16,
                               uint16_t* dw16) {
   const Conv d(shp);
 #pragma omp parallel for schedule(static)
-  for (int64_t i = 0; i < d.w_size(); ++i) {
-    int64_t k, c, r, s;
-    d.w_coords(i, &k, &c, &r, &s);
-    uint16_t acc = 0x0000;
-    for (int64_t n = 0; n < d.N; ++n)
-      for (int64_t p = 0; p < d.P; ++p)
-        for (int64_t q = 0; q < d.Q; ++q) {
-          const int64_t h = p * d.sh - d.ph + r, ww = q * d.sw - d.pw + s;
-          if (h < 0 || h >= d.H || ww < 0 || ww >= d.W) continue;
-          acc = fma_half(dy16[d.yi(n, k, p, q)], x16[d.xi(n, c, h, ww)], acc);
-        }
-    dw16[i] = acc;
-  }
+  for (int64_t i = 0; i < d.w_size(); ++i) dw16[i] = wgrad_chain(d, x16, dy16, i);
+}
+
+// The same chains at chosen flat output indices only (out[j] for idx[j]).
+void oracle_conv_fwd_f16acc_at(const int32_t* shp, const uint16_t* x16, const uint16_t* w16,
+                               const int64_t* idx, int64_t n, uint16_t* out) {
+  const Conv d(shp);
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t j = 0; j < n; ++j) out[j] = fwd_chain(d, x16, w16, idx[j]);
+}
+
+void oracle_conv_dgrad_f16acc_at(const int32_t* shp, const uint16_t* dy16, const uint16_t* w16,
+                                 const int64_t* idx, int64_t n, uint16_t* out) {
+  const Conv d(shp);
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t j = 0; j < n; ++j) out[j] = dgrad_chain(d, dy16, w16, idx[j]);
+}
+
+void oracle_conv_wgrad_f16acc_at(const int32_t* shp, const uint16_t* x16, const uint16_t* dy16,
+                                 const int64_t* idx, int64_t n, uint16_t* out) {
+  const Conv d(shp);
+#pragma omp parallel for schedule(dynamic, 1)
+  for (int64_t j = 0; j < n; ++j) out[j] = wgrad_chain(d, x16, dy16, idx[j]);
 }
 
 }  // extern "C"

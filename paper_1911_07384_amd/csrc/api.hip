@@ -78,6 +78,7 @@ struct ConvWs {
 
 ConvWs conv_ws(const ConvDims& d, int pass) {
   ConvWs L;
+  if (d.accum) return L;  // the binary16 chains read and write the caller's tensors only
   size_t off = 0;
   auto take = [&](size_t bytes) {
     const size_t at = off;
@@ -110,7 +111,7 @@ ConvWs conv_ws(const ConvDims& d, int pass) {
   } else if (stem_s2d(d)) {
     L.need_x = true;
     L.x = take((size_t)d.N * d.P * d.Q * 16 * 2);
-    wgrad_plan(d.Kp, 16, 4, 4, (int64_t)d.N * d.P * d.Q, 0, &L.splits, &L.pps);
+    wgrad_plan(d.Kp, 16, 4, 4, (int64_t)d.N * d.P * d.Q, &L.splits, &L.pps);
     L.part = take((size_t)L.splits * d.Kp * 256 * 4);
   } else {
     if (nchw || d.Cp != d.C) {
@@ -121,7 +122,7 @@ ConvWs conv_ws(const ConvDims& d, int pass) {
       L.need_y = true;
       L.y = take((size_t)d.N * d.P * d.Q * d.Kp * 2);
     }
-    wgrad_plan(d.Kp, d.Cp, d.R, d.S, (int64_t)d.N * d.P * d.Q, d.accum, &L.splits, &L.pps);
+    wgrad_plan(d.Kp, d.Cp, d.R, d.S, (int64_t)d.N * d.P * d.Q, &L.splits, &L.pps);
     L.part = take((size_t)L.splits * d.Kp * d.R * d.S * d.Cp * 4);
   }
   L.total = off;
@@ -135,9 +136,12 @@ IgemmArgs stem_args(const ConvDims& d, const h16* x, const h16* w, h16* y) {
   a.stride_h = d.sh; a.stride_w = d.sw;
   a.Co = d.K; a.out = y; a.OH = d.P; a.OW = d.Q; a.ldo = d.K; a.os_h = 1; a.os_w = 1;
   a.nphase = 1;
-  a.f16acc = d.accum;
   a.ph[0] = IgemmPhase{w, d.R * d.S * d.C, d.R, d.S, d.ph, d.pw, d.P, d.Q, 0, 0};
   return a;
+}
+
+ConvChainArgs chain_args(const ConvDims& d) {
+  return ConvChainArgs{d.N, d.C, d.H, d.W, d.K, d.R, d.S, d.sh, d.sw, d.ph, d.pw, d.P, d.Q};
 }
 
 fp16_status hip_status(hipError_t e) { return e == hipSuccess ? FP16_OK : FP16_ERR_HIP; }
@@ -212,6 +216,7 @@ fp16_status fp16_conv_fwd(const fp16_conv_desc* desc, const fp16_t* x, const fp1
   const h16* xe = reinterpret_cast<const h16*>(x);
   const h16* we = reinterpret_cast<const h16*>(w);
   h16* ye = reinterpret_cast<h16*>(y);
+  if (d.accum) return hip_status(launch_conv_chain(chain_args(d), 0, xe, we, ye, st));
   if (d.layout == FP16_NHWC) {
     // the ResNet stem reads the unpadded image on its own kernel
     const IgemmArgs sa = stem_args(d, xe, we, ye);
@@ -234,7 +239,6 @@ fp16_status fp16_conv_fwd(const fp16_conv_desc* desc, const fp16_t* x, const fp1
   a.stride_h = d.sh; a.stride_w = d.sw;
   a.Co = d.K; a.out = ye; a.OH = d.P; a.OW = d.Q; a.ldo = d.K; a.os_h = 1; a.os_w = 1;
   a.nphase = 1;
-  a.f16acc = d.accum;
   a.ph[0] = IgemmPhase{we, d.R * d.S * d.Cp, d.R, d.S, d.ph, d.pw, d.P, d.Q, 0, 0};
   TRY(launch_igemm(a, st));
   if (d.layout == FP16_NCHW) TRY(launch_nhwc_to_nchw(ye, reinterpret_cast<h16*>(y), d.N, d.K,
@@ -258,6 +262,8 @@ static fp16_status conv_dgrad_impl(const fp16_conv_desc* desc, const fp16_t* dy,
   if (s != FP16_OK) return s;
   if (!dy || !w || !dx) return FP16_ERR_NULL;
   if (wf_given && d.layout != FP16_NHWC) return FP16_ERR_UNSUPPORTED;
+  // the binary16 chains: the plain data gradient from the filter only
+  if (d.accum && (wf_given || addend)) return FP16_ERR_UNSUPPORTED;
   if (!aligned16(dy) || !aligned16(w) || !aligned16(dx) || (addend && !aligned16(addend)))
     return FP16_ERR_MISALIGNED;
   const ConvWs L = conv_ws(d, FP16_PASS_DGRAD);
@@ -272,6 +278,7 @@ static fp16_status conv_dgrad_impl(const fp16_conv_desc* desc, const fp16_t* dy,
   const h16* dye = reinterpret_cast<const h16*>(dy);
   const h16* wk = reinterpret_cast<const h16*>(w);
   h16* dxe = reinterpret_cast<h16*>(dx);
+  if (d.accum) return hip_status(launch_conv_chain(chain_args(d), 1, dye, wk, dxe, st));
   if (d.layout == FP16_NCHW) {
     TRY(launch_nchw_to_nhwc(dye, wsp(ws, L.y), d.N, d.K, d.P * d.Q, d.Kp, st));
     TRY(launch_nchw_to_nhwc(wk, wsp(ws, L.w), d.K, d.C, d.R * d.S, d.C, st));
@@ -298,7 +305,6 @@ static fp16_status conv_dgrad_impl(const fp16_conv_desc* desc, const fp16_t* dy,
   a.Co = d.C; a.out = dxe; a.OH = d.H; a.OW = d.W; a.ldo = d.C; a.os_h = d.sh; a.os_w = d.sw;
   a.addend = addend ? (d.layout == FP16_NCHW ? dxe : reinterpret_cast<const h16*>(addend)) : nullptr;
   a.nphase = 0;
-  a.f16acc = d.accum;
   int64_t off = 0;
   for (int ph = 0; ph < d.sh; ++ph) {
     for (int pw = 0; pw < d.sw; ++pw) {
@@ -380,6 +386,8 @@ fp16_status fp16_conv_wgrad(const fp16_conv_desc* desc, const fp16_t* x, const f
   hipStream_t st = static_cast<hipStream_t>(stream);
   const h16* xe = reinterpret_cast<const h16*>(x);
   const h16* dye = reinterpret_cast<const h16*>(dy);
+  if (d.accum)
+    return hip_status(launch_conv_chain(chain_args(d), 2, xe, dye, reinterpret_cast<h16*>(dw), st));
   if (stem_s2d(d)) {
     // 4x4 stride-1 convolution over the space-to-depth image, pad 2 before
     // and 1 after: s2d pixel p + r' - 2 holds original rows 2(p + r') - 4 + dh
@@ -390,7 +398,7 @@ fp16_status fp16_conv_wgrad(const fp16_conv_desc* desc, const fp16_t* x, const f
     a.x = xs; a.dy = dye;
     a.N = d.N; a.H = d.P; a.W = d.Q; a.C = 16; a.K = d.Kp; a.R = 4; a.S = 4;
     a.sh = 1; a.sw = 1; a.ph = 2; a.pw = 2; a.P = d.P; a.Q = d.Q;
-    a.partial = part; a.splits = L.splits; a.pix_per_split = L.pps; a.f16acc = 0;
+    a.partial = part; a.splits = L.splits; a.pix_per_split = L.pps;
     TRY(launch_wgrad_partial(a, st));
     return hip_status(launch_wgrad_reduce_s2d3(part, L.splits, d.K, reinterpret_cast<h16*>(dw), st));
   }
@@ -414,7 +422,7 @@ fp16_status fp16_conv_wgrad(const fp16_conv_desc* desc, const fp16_t* x, const f
   a.x = xe; a.dy = dye;
   a.N = d.N; a.H = d.H; a.W = d.W; a.C = d.Cp; a.K = d.Kp; a.R = d.R; a.S = d.S;
   a.sh = d.sh; a.sw = d.sw; a.ph = d.ph; a.pw = d.pw; a.P = d.P; a.Q = d.Q;
-  a.partial = part; a.splits = L.splits; a.pix_per_split = L.pps; a.f16acc = d.accum;
+  a.partial = part; a.splits = L.splits; a.pix_per_split = L.pps;
   TRY(launch_wgrad_partial(a, st));
   TRY(launch_wgrad_reduce(part, L.splits, d.K, d.Kp, d.R, d.S, d.C, d.Cp, d.layout,
                           reinterpret_cast<h16*>(dw), st));
@@ -666,7 +674,7 @@ static fp16_status check_conv_bn(const fp16_conv_desc* cd, const fp16_bn_desc* b
   fp16_status s = check_conv(cd, d);
   if (s != FP16_OK) return s;
   if ((s = check_bn(bd, b)) != FP16_OK) return s;
-  if (d->layout != FP16_NHWC || b->layout != FP16_NHWC || d->K % 8 != 0)
+  if (d->layout != FP16_NHWC || b->layout != FP16_NHWC || d->K % 8 != 0 || d->accum)
     return FP16_ERR_UNSUPPORTED;
   if (b->N != d->N || b->C != d->K || b->H != d->P || b->W != d->Q || bd->use_stats != 0)
     return FP16_ERR_SHAPE;
@@ -746,7 +754,6 @@ fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc
   a.Co = d.K; a.out = reinterpret_cast<h16*>(y); a.OH = d.P; a.OW = d.Q; a.ldo = d.K;
   a.os_h = 1; a.os_w = 1;
   a.nphase = 1;
-  a.f16acc = d.accum;
   a.ph[0] = IgemmPhase{we, d.R * d.S * d.Cp, d.R, d.S, d.ph, d.pw, d.P, d.Q, 0, 0};
   const h16* gp = reinterpret_cast<const h16*>(gamma);
   const h16* bp = reinterpret_cast<const h16*>(beta);

@@ -18,9 +18,6 @@
 // the same k order (so they give identical bits):
 //   igemm_kernel  -- 4 waves in a 2x2 or 4x1 grid; A and B tiles staged in
 //                    LDS through registers, k-step 64, double buffered.
-//                    Also the strict binary16-accumulation variant (the
-//                    accumulator rounded to binary16 after every MFMA, i.e.
-//                    every 16 terms of the k order).
 //   igemm4_kernel -- 4 waves split M only, so no A element is shared: each
 //                    lane loads its own MFMA operand rows from global memory
 //                    into registers three k-steps ahead, and only the filter
@@ -79,7 +76,7 @@ struct Cfg {
   static constexpr int LDS_BYTES = MAIN_BYTES > STAGE_BYTES ? MAIN_BYTES : STAGE_BYTES;
 };
 
-template <int BM, int BN, int WM, int WN, int BK, bool F16ACC>
+template <int BM, int BN, int WM, int WN, int BK>
 __global__ __launch_bounds__(256) void igemm_kernel(const IgemmArgs a) {
   using K = Cfg<BM, BN, WM, WN, BK>;
   constexpr int LDK = K::LDK, KC = K::KC, RSTEP = K::RSTEP;
@@ -195,10 +192,6 @@ __global__ __launch_bounds__(256) void igemm_kernel(const IgemmArgs a) {
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) {
           acc[tm][tn] = mfma32x32x16(af[tm], bf[tn], acc[tm][tn]);
-          if (F16ACC) {  // binary16 accumulator: one rounding per 16 terms
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[tm][tn][e] = to_f32(to_h16(acc[tm][tn][e]));
-          }
         }
     }
   };
@@ -956,7 +949,7 @@ __global__ __launch_bounds__(kC3Thr) void c3_kernel(const IgemmArgs a, int tpi, 
 // Whether the 3x3 kernel takes this problem; tiles per image if so.
 int c3_tiles_per_image(const IgemmArgs& a) {
   const IgemmPhase& p = a.ph[0];
-  if (a.f16acc || a.stat || a.addend || a.nphase != 1 || p.Rt != 3 || p.St != 3 ||
+  if (a.stat || a.addend || a.nphase != 1 || p.Rt != 3 || p.St != 3 ||
       a.stride_h != 1 || a.stride_w != 1 || p.pad_h != 1 || p.pad_w != 1 || a.Ci != 64 ||
       a.Co != 64 || p.ldb != 576 || p.Ho != a.Hi || p.Wo != a.Wi || a.OH != p.Ho ||
       a.OW != p.Wo || a.os_h != 1 || a.os_w != 1 || p.oph != 0 || p.opw != 0 || a.ldo != 64)
@@ -1400,7 +1393,7 @@ hipError_t launch_pw(const IgemmArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <int BM, int BN, int WM, int WN, int BK, bool F16ACC = false>
+template <int BM, int BN, int WM, int WN, int BK>
 hipError_t launch_cfg(const IgemmArgs& a, hipStream_t st) {
   int maxM = 0;
   for (int p = 0; p < a.nphase; ++p) {
@@ -1409,7 +1402,7 @@ hipError_t launch_cfg(const IgemmArgs& a, hipStream_t st) {
   }
   if (maxM == 0 || a.nphase == 0) return hipSuccess;
   dim3 grid(ceil_div(maxM, BM), ceil_div(a.Co, BN), a.nphase);
-  hipLaunchKernelGGL((igemm_kernel<BM, BN, WM, WN, BK, F16ACC>), grid, dim3(256), 0, st, a);
+  hipLaunchKernelGGL((igemm_kernel<BM, BN, WM, WN, BK>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
 
@@ -1598,7 +1591,6 @@ enum class IgemmKind { kLds, kDirect, kDma, kPointwise, k3x3 };
 // below that the register-direct kernel for short reductions or small M,
 // else the LDS-staged one.  All four give identical bits.
 IgemmKind igemm_kind(const IgemmArgs& a) {
-  if (a.f16acc) return IgemmKind::kLds;
   if (c3_tiles_per_image(a) > 0) return IgemmKind::k3x3;
   {
     // a 1x1 filter over 64 or 128 channels with a dense output of 128+
@@ -1659,9 +1651,6 @@ bool igemm_takes_stats(const IgemmArgs& a) {
 }
 
 hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st) {
-  if (a.f16acc)
-    return a.Co <= 64 ? launch_cfg<128, 64, 4, 1, 64, true>(a, st)
-                      : launch_cfg<128, 128, 2, 2, 64, true>(a, st);
   switch (igemm_kind(a)) {
     case IgemmKind::kDma: {
       // two stages (two workgroups per CU) unless the grid fits the 256 CUs
@@ -1699,7 +1688,7 @@ bool stem_conv_ok(const IgemmArgs& a) {
   const bool shape = a.Ci == 3 && a.nphase == 1 && p.Rt == 7 && p.St == 7 && p.ldb == 147 &&
                      p.pad_h == 3 && p.pad_w == 3 && a.stride_h == 2 && a.stride_w == 2 &&
                      p.oph == 0 && p.opw == 0 && a.os_h == 1 && a.os_w == 1 && a.Co == 64 &&
-                     a.ldo == 64 && !a.addend && !a.f16acc && a.Wi % 8 == 0 &&
+                     a.ldo == 64 && !a.addend && a.Wi % 8 == 0 &&
                      a.Wi == 2 * a.OW && a.OH == p.Ho && a.OW == p.Wo &&
                      a.OW % 16 == 0 && a.OW >= 16 && a.OW <= kStemMaxQ &&
                      (int64_t)a.N * a.Hi * a.Wi * 6 < ((int64_t)1 << 31);

@@ -12,8 +12,7 @@
 // The pixel range is split across workgroups (split-K).  Each split writes
 // its float32 partial tile to the workspace; a second kernel adds the splits
 // in a fixed order and rounds once to binary16, so the result is
-// deterministic.  The strict binary16-accumulation variant runs one split
-// and rounds the accumulator to binary16 after every 16 pixels.
+// deterministic.
 
 #include "kernels.hpp"
 
@@ -25,7 +24,7 @@ namespace {
 constexpr int BKP = 64;         // pixels per k-step
 constexpr int LDP = BKP + 8;    // LDS row pitch (halves)
 
-template <int BM, int BN, int WM, int WN, bool F16ACC = false>
+template <int BM, int BN, int WM, int WN>
 __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
   constexpr int WTM = BM / WM, WTN = BN / WN;
   constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -149,10 +148,6 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
 #pragma unroll
         for (int tn = 0; tn < TN; ++tn) {
           acc[tm][tn] = mfma32x32x16(af[tm], bf[tn], acc[tm][tn]);
-          if (F16ACC) {  // binary16 accumulator: one rounding per 16 pixels
-#pragma unroll
-            for (int e = 0; e < 16; ++e) acc[tm][tn][e] = to_f32(to_h16(acc[tm][tn][e]));
-          }
         }
     }
     if (kt + 1 < KT) store_tile(buf ^ 1);
@@ -611,14 +606,7 @@ void launch_wgrad7(const WCfg& cfg, dim3 grid, hipStream_t st, const WgradArgs& 
 
 }  // namespace
 
-void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int f16acc, int* splits,
-                int* pix_per_split) {
-  if (f16acc) {  // one split: the binary16 accumulator runs over every pixel in order
-    int64_t pps = (npix + BKP - 1) / BKP * BKP;
-    *pix_per_split = (int)pps;
-    *splits = 1;
-    return;
-  }
+void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int* splits, int* pix_per_split) {
   const int Nw = R * S * Cp;
   const WCfg cfg = wgrad_choice(K, Cp, Nw, npix);
   const int64_t tiles = (int64_t)ceil_div(K, cfg.BM) * ceil_div(Nw, cfg.BN);
@@ -640,21 +628,6 @@ hipError_t launch_wgrad_partial(const WgradArgs& a, hipStream_t st) {
   const WCfg cfg = wgrad_choice(a.K, a.C, Nw, npix);
   const int tiles = ceil_div(a.K, cfg.BM) * ceil_div(Nw, cfg.BN);
   dim3 grid(tiles, a.splits);
-  if (a.f16acc) {
-    const WCfg oc = wgrad_cfg(a.K, Nw);
-    dim3 g2(ceil_div(a.K, oc.BM) * ceil_div(Nw, oc.BN), a.splits);
-    if (oc.BM == 128 && oc.BN == 128)
-      hipLaunchKernelGGL((wgrad_kernel<128, 128, 2, 2, true>), g2, dim3(256), 0, st, a);
-    else if (oc.BM == 128)
-      hipLaunchKernelGGL((wgrad_kernel<128, 64, 2, 2, true>), g2, dim3(256), 0, st, a);
-    else if (oc.BN == 192)
-      hipLaunchKernelGGL((wgrad_kernel<64, 192, 2, 2, true>), g2, dim3(256), 0, st, a);
-    else if (oc.BN == 128)
-      hipLaunchKernelGGL((wgrad_kernel<64, 128, 2, 2, true>), g2, dim3(256), 0, st, a);
-    else
-      hipLaunchKernelGGL((wgrad_kernel<64, 64, 2, 2, true>), g2, dim3(256), 0, st, a);
-    return hipGetLastError();
-  }
   if (wgrad_dma(a.K, a.C)) {
     // channel counts that are multiples of 8 only (the 3-channel stem, padded)
     // take per-lane filter taps

@@ -58,9 +58,6 @@ struct IgemmArgs {
   // over its rows, at stat[(b * 3 + q) * Co + c], q = 0, 1, 2.
   float* stat;
   int stat_nb;
-  // 1: binary16 accumulation, the accumulator rounded to binary16 after every
-  // 16 terms of the k order (LDS-staged kernel only; no statistics)
-  int f16acc;
 };
 
 hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st);
@@ -114,7 +111,6 @@ struct WgradArgs {
   float* partial; // [splits][K][R*S*C]
   int splits;
   int pix_per_split;
-  int f16acc;     // 1: binary16 accumulation per 16 pixels (one split, register-transpose kernel)
 };
 hipError_t launch_wgrad_partial(const WgradArgs& a, hipStream_t st);
 // dw[k][r][s][c] = rne16(sum_split partial[split][k][(r*S+s)*Cp + c]) for k < K, c < C,
@@ -127,9 +123,18 @@ hipError_t launch_wgrad_reduce(const float* partial, int splits, int K, int Kp, 
 hipError_t launch_s2d3(const h16* src, h16* dst, int N, int H, int W, hipStream_t st);
 hipError_t launch_wgrad_reduce_s2d3(const float* partial, int splits, int K, h16* dw,
                                     hipStream_t st);
-// Split-K plan of the weight gradient; with f16acc one split over all pixels.
-void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int f16acc, int* splits,
-                int* pix_per_split);
+// Split-K plan of the weight gradient.
+void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int* splits, int* pix_per_split);
+
+// Convolutions with every operation in binary16 (conv_f16chain.hip): each
+// output a chain of binary16 fmas from +0 in the declared order.  NHWC
+// activations, KRSC filter, any C and K.  pass 0: in0 = x, in1 = w, out = y;
+// pass 1: in0 = dy, in1 = w, out = dx; pass 2: in0 = x, in1 = dy, out = dW.
+struct ConvChainArgs {
+  int N, C, H, W, K, R, S, sh, sw, ph, pw, P, Q;
+};
+hipError_t launch_conv_chain(const ConvChainArgs& a, int pass, const h16* in0, const h16* in1,
+                             h16* out, hipStream_t st);
 
 // ---- batch normalisation (bn.hip) ----------------------------------------
 struct BnArgs {

@@ -188,14 +188,25 @@ def test_conv_accum_validation(fn):
     assert F.fp16_conv_workspace_bytes(d, F.PASS_FWD) == 0  # invalid descriptor
 
 
-def test_conv_accum_wgrad_runs_one_split():
-    # the binary16 accumulator runs over all pixels: the partial workspace
-    # holds exactly one float32 tile (K x R*S*C), 256-aligned
+def test_conv_accum_needs_no_workspace():
+    # the binary16 chains read and write the caller's tensors only
     d = _conv()
     d.accum = 1
-    need = F.fp16_conv_workspace_bytes(d, F.PASS_WGRAD)
-    assert need == (64 * 9 * 64 * 4 + 255) // 256 * 256
-    assert need < F.fp16_conv_workspace_bytes(_conv(), F.PASS_WGRAD)
+    for pass_ in (F.PASS_FWD, F.PASS_DGRAD, F.PASS_WGRAD):
+        assert F.fp16_conv_workspace_bytes(d, pass_) == 0
+    assert F.fp16_conv_workspace_bytes(_conv(), F.PASS_WGRAD) > 0
+
+
+def test_conv_accum_rejects_fused_forms():
+    # the strict mode is the plain data gradient only: no addend, no
+    # rearranged filter, no fused BN (FP16_ERR_UNSUPPORTED, nothing launched)
+    d = _conv()
+    d.accum = 1
+    l = F.lib()
+    assert l.fp16_conv_dgrad_add(ctypes.byref(d), A, B, Cc, Cc + (1 << 20), None, 0, None) == 7
+    assert l.fp16_conv_dgrad_wf(ctypes.byref(d), A, B, None, Cc, None, 0, None) == 7
+    bd = F.bn_desc(d.n, d.k, d.h, d.w)
+    assert F.fp16_conv_bn_workspace_bytes(d, bd) == 0
 
 
 # ---- pooling and loss: every call below is invalid, nothing is launched ---------

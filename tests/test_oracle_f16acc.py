@@ -327,3 +327,14 @@ def test_binary16_accumulation_costs_accuracy():
     e_def = np.sqrt(np.mean((y16.astype(np.float64) - y64) ** 2))
     e_str = np.sqrt(np.mean((ys - y64) ** 2))
     assert e_str > 2 * e_def
+
+
+def test_sampled_entry_points_equal_full():
+    shp = oracle.conv_shape(2, 12, 7, 7, 10, 3, 3, 2, 1)
+    x, wt, dy = _inputs(shp, 16)
+    for full, at, a, b in ((oracle.conv_fwd_f16acc, oracle.conv_fwd_f16acc_at, x, wt),
+                           (oracle.conv_dgrad_f16acc, oracle.conv_dgrad_f16acc_at, dy, wt),
+                           (oracle.conv_wgrad_f16acc, oracle.conv_wgrad_f16acc_at, x, dy)):
+        f = _bits(full(shp, a, b)).reshape(-1)
+        idx = np.arange(0, f.size, 3, dtype=np.int64)
+        assert np.array_equal(_bits(at(shp, a, b, idx)), f[idx])
