@@ -70,14 +70,20 @@ typedef struct {
   int32_t pad_h, pad_w;
   int32_t layout; /* fp16_layout */
   int32_t accum;  /* 0: float32 accumulators (default);
-                     1: binary16 accumulation -- the strict reading of "all arithmetic
-                        in FP16" (Section 5.2), to measure what float32 accumulators buy:
-                        the accumulator is rounded to binary16 after every 16 terms of the
-                        reduction.  Reduction orders: forward (r, s, c) with c over C
-                        rounded up to a multiple of 8; data gradient the taps reaching the
-                        output in decreasing (r, s), then k over K rounded up to 8; weight
-                        gradient the output pixels (n, p, q) in order, unsplit.  NHWC only
-                        (FP16_ERR_UNSUPPORTED otherwise); slower than the default. */
+                     1: every operation in binary16 -- the strict reading of "all
+                        arithmetic in FP16" (Section 5.2), to measure what float32
+                        accumulators buy: each output is a binary16 accumulator that
+                        starts at +0 and takes its terms one at a time as binary16 fused
+                        multiply-adds (one rounding of the exact a*b + acc per term).
+                        Reduction orders: forward, taps (r, s) row-major and channels c
+                        ascending within a tap; data gradient, the taps (r, s) row-major
+                        that reach the position from a point of the P x Q grid, output
+                        channels k ascending within a tap; weight gradient, the output
+                        pixels (n, p, q) in order.  Taps outside the image (or the grid)
+                        are not terms.  NHWC only, plain fwd / dgrad / wgrad only
+                        (FP16_ERR_UNSUPPORTED for NCHW, fp16_conv_dgrad_add,
+                        fp16_conv_dgrad_wf and fp16_conv_bn_relu_fwd); needs no
+                        workspace; runs on the vector ALUs, far slower than the default. */
 } fp16_conv_desc;
 
 /* Batch normalisation problem on x [N,C,H,W] (logical). */
@@ -108,8 +114,9 @@ size_t fp16_conv_workspace_bytes(const fp16_conv_desc* desc, int32_t pass);
 fp16_status fp16_conv_fwd(const fp16_conv_desc* desc, const fp16_t* x, const fp16_t* w, fp16_t* y,
                           void* ws, size_t ws_bytes, fp16_stream_t stream);
 
-/* Data gradient (back-propagation through the convolution; the adjoint of
- * fp16_conv_fwd in x):
+/* Data gradient: the gradient with respect to the input of ResNet-50's
+ * convolutions (Section 5.1), stored in binary16 like every gradient of the
+ * method (Section 5.2); the adjoint of fp16_conv_fwd in x:
  *   dx[n,c,h,w] = sum over (k,r,s) with h + pad_h - r = p*stride_h and
  *                 w + pad_w - s = q*stride_w, (p,q) inside the P x Q grid, of dy[n,k,p,q] * W[k,c,r,s].
  * Every element of dx is written (positions no tap reaches get zero).
@@ -151,7 +158,9 @@ fp16_status fp16_conv_dgrad_wf(const fp16_conv_desc* desc, const fp16_t* dy, con
                                const fp16_t* addend, fp16_t* dx, void* ws, size_t ws_bytes,
                                fp16_stream_t stream);
 
-/* Weight gradient (the adjoint of fp16_conv_fwd in W):
+/* Weight gradient: the gradient with respect to the filter that the
+ * momentum-SGD update of Section 5.1 consumes, stored in binary16 with no
+ * higher-precision copy (Section 5.2); the adjoint of fp16_conv_fwd in W:
  *   dW[k,c,r,s] = sum_{n,p,q} dy[n,k,p,q] * x[n,c, p*stride_h - pad_h + r, q*stride_w - pad_w + s].
  * Partial sums over pixel ranges stay float32 in the workspace and are
  * added in a fixed order before the single rounding.  dw must not overlap

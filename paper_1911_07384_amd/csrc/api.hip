@@ -470,6 +470,10 @@ fp16_status fp16_bn_relu(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t
       overlap(y, eb, gamma, cb) || overlap(y, eb, beta, cb) || overlap(y, eb, stats, (size_t)a.C * 8) ||
       overlap(y, eb, ws, need) || overlap(stats, (size_t)a.C * 8, ws, need))
     return FP16_ERR_ALIASING;
+  // the workspace is written while the inputs are still being read
+  if (overlap(ws, need, x, eb) || overlap(ws, need, residual, eb) || overlap(ws, need, gamma, cb) ||
+      overlap(ws, need, beta, cb))
+    return FP16_ERR_ALIASING;
   return hip_status(launch_bn_fwd(a, reinterpret_cast<const h16*>(x),
                                   reinterpret_cast<const h16*>(gamma),
                                   reinterpret_cast<const h16*>(beta),
@@ -506,6 +510,12 @@ fp16_status fp16_bn_relu_bwd(const fp16_bn_desc* desc, const fp16_t* x, const fp
       (dresidual && overlap(dresidual, eb, dx, eb)) || overlap(dx, eb, ws, need) ||
       overlap(dgamma, cb, dbeta, cb) || overlap(dgamma, cb, ws, need) ||
       overlap(dbeta, cb, ws, need) || overlap(dgamma, cb, dx, eb) || overlap(dbeta, cb, dx, eb))
+    return FP16_ERR_ALIASING;
+  // the workspace (partial sums, the kept ReLU mask) is written while the
+  // inputs are still being read
+  if (overlap(ws, need, x, eb) || overlap(ws, need, y, eb) || overlap(ws, need, dy, eb) ||
+      overlap(ws, need, residual, eb) || overlap(ws, need, gamma, cb) ||
+      overlap(ws, need, beta, cb) || overlap(ws, need, stats, (size_t)a.C * 8))
     return FP16_ERR_ALIASING;
   return hip_status(launch_bn_bwd(
       a, reinterpret_cast<const h16*>(x), reinterpret_cast<const h16*>(y),
@@ -723,6 +733,9 @@ fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc
       overlap(z, yb, ws, need) || overlap(z, yb, gamma, cb) || overlap(z, yb, beta, cb) ||
       overlap(z, yb, stats, sb) || (residual && z != residual && overlap(z, yb, residual, yb)) ||
       (residual && overlap(y, yb, residual, yb)) || overlap(stats, sb, ws, need))
+    return FP16_ERR_ALIASING;
+  if (overlap(ws, need, x, xb) || overlap(ws, need, w, wb) || overlap(ws, need, gamma, cb) ||
+      overlap(ws, need, beta, cb) || overlap(ws, need, residual, yb))
     return FP16_ERR_ALIASING;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const ConvWs L = conv_ws(d, FP16_PASS_FWD);

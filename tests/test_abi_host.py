@@ -166,6 +166,43 @@ def test_bn_validation():
     assert lib.fp16_bn_relu_bwd(ctypes.byref(d), *bw_alias) == ALIASING
 
 
+def test_bn_workspace_must_not_overlap_inputs():
+    # the workspace (partial sums, the kept ReLU mask) is written while the
+    # inputs are read: any overlap with them is rejected
+    lib = F.lib()
+    d = F.bn_desc(2, 64, 8, 8)
+    need = F.fp16_bn_workspace_bytes(d)
+    ok = [A, B, B + 256, Cc + (2 << 20), Cc, WS + (1 << 20), WS, need, None]
+    assert lib.fp16_bn_relu(ctypes.byref(d), *ok[:6], A + 4096, need, None) == ALIASING  # x
+    bad = list(ok)
+    bad[3] = WS + 256  # residual inside the workspace
+    assert lib.fp16_bn_relu(ctypes.byref(d), *bad) == ALIASING
+    bad = list(ok)
+    bad[6] = B  # workspace over gamma and beta
+    assert lib.fp16_bn_relu(ctypes.byref(d), *bad) == ALIASING
+    # backward: x, y, dy, residual, gamma, beta, stats
+    bw = [A, Cc + (2 << 20), Cc, B, B + 256, Cc + (3 << 20), WS + (1 << 20), Cc + (1 << 20),
+          B + 512, B + 768, None, WS, need, None]
+    for i, at in ((0, A), (1, Cc + (2 << 20)), (2, Cc), (5, Cc + (3 << 20)), (3, B),
+                  (6, WS + (1 << 20))):
+        bad = list(bw)
+        bad[11] = at  # the workspace placed on input i
+        if i == 6:
+            bad[6] = WS + 64  # stats inside the workspace
+            bad[11] = WS
+        assert lib.fp16_bn_relu_bwd(ctypes.byref(d), *bad) == ALIASING, i
+    # the fused convolution + BN forward: workspace over x or the filter
+    cd = _conv()
+    bd = F.bn_desc(cd.n, cd.k, cd.h, cd.w)
+    need = F.fp16_conv_bn_workspace_bytes(cd, bd)
+    assert need > 0
+    args = [A, B, B + (1 << 20), B + (1 << 20) + 256, None, Cc, Cc + (4 << 20), WS + (8 << 20)]
+    assert lib.fp16_conv_bn_relu_fwd(ctypes.byref(cd), ctypes.byref(bd), *args, A, need,
+                                     None) == ALIASING
+    assert lib.fp16_conv_bn_relu_fwd(ctypes.byref(cd), ctypes.byref(bd), *args, B, need,
+                                     None) == ALIASING
+
+
 @pytest.mark.parametrize("fn", ["fp16_sgd_step", "fp16_sgd_step_f16"])
 def test_sgd_validation(fn):
     f = getattr(F.lib(), fn)
