@@ -16,7 +16,8 @@
  *   - Buffers are device pointers owned by the caller.  The library never
  *     allocates or frees device memory and keeps no state between calls.
  *     Any scratch memory a call needs is the caller's workspace, sized by
- *     the matching *_workspace_bytes query.
+ *     the matching *_workspace_bytes query -- except fp16_conv_wgrad_noalloc,
+ *     whose scratch is a fixed device array of the library (see there).
  *   - Work is enqueued on `stream` (a hipStream_t; NULL is the default
  *     stream) and the call returns without waiting for it.
  *   - Arguments are checked before anything is enqueued: a nonzero status
@@ -167,6 +168,24 @@ fp16_status fp16_conv_dgrad_wf(const fp16_conv_desc* desc, const fp16_t* dy, con
  * x, dy or ws. */
 fp16_status fp16_conv_wgrad(const fp16_conv_desc* desc, const fp16_t* x, const fp16_t* dy,
                             fp16_t* dw, void* ws, size_t ws_bytes, fp16_stream_t stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the
+ * weight gradient of fp16_conv_wgrad, bit-identical to it, with no workspace
+ * argument.  Its scratch (the float32 split-K partial sums, and for the
+ * ResNet stem the space-to-depth image) lives in a library-owned device
+ * array of fp16_noalloc_scratch_bytes() = 32 MiB on each GPU the library
+ * runs on, held from its first use on that GPU until the process ends; the
+ * call itself allocates nothing.  A problem whose fp16_conv_workspace_bytes
+ * (desc, FP16_PASS_WGRAD) exceeds that size returns FP16_ERR_WORKSPACE (every
+ * ResNet-50 layer at batch 128 fits except the stem).  The work goes on
+ * `stream`'s device (the current device for the NULL stream).  Calls that
+ * overlap in time on one GPU share the array and race: order them on one
+ * stream or synchronise between them.  Other arguments and errors as for
+ * fp16_conv_wgrad. */
+size_t fp16_noalloc_scratch_bytes(void);
+fp16_status fp16_conv_wgrad_noalloc(const fp16_conv_desc* desc, const fp16_t* x, const fp16_t* dy,
+                                    fp16_t* dw, fp16_stream_t stream);
 
 /* Bytes of workspace the BN forward or backward call needs. */
 size_t fp16_bn_workspace_bytes(const fp16_bn_desc* desc);

@@ -33,7 +33,7 @@ EXPORTS = ["fp16_conv_out_dims", "fp16_conv_workspace_bytes", "fp16_conv_fwd", "
            "fp16_avgpool_fwd", "fp16_avgpool_bwd", "fp16_softmax_ce", "fp16_status_string",
            "fp16_version", "fp16_conv_bn_workspace_bytes", "fp16_conv_bn_relu_fwd",
            "fp16_sgd_step_f16", "fp16_conv_dgrad_filter_bytes", "fp16_conv_dgrad_filter",
-           "fp16_conv_dgrad_wf"]
+           "fp16_conv_dgrad_wf", "fp16_noalloc_scratch_bytes", "fp16_conv_wgrad_noalloc"]
 
 
 class Fp16Error(RuntimeError):
@@ -73,6 +73,8 @@ _SIGS = {
     "fp16_conv_dgrad_add": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_conv_wgrad": (ctypes.c_int, [_P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_conv_dgrad_filter_bytes": (_SZ, [_P]),
+    "fp16_noalloc_scratch_bytes": (_SZ, []),
+    "fp16_conv_wgrad_noalloc": (ctypes.c_int, [_P, _P, _P, _P, _P]),
     "fp16_conv_dgrad_filter": (ctypes.c_int, [_P, _P, _P, _P]),
     "fp16_conv_dgrad_wf": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_bn_workspace_bytes": (_SZ, [_P]),
@@ -211,6 +213,15 @@ def fp16_conv_dgrad_wf(desc, dy, wf, addend, dx, ws=None, ws_bytes=None, stream=
 def fp16_conv_wgrad(desc, x, dy, dw, ws=None, ws_bytes=None, stream=None) -> None:
     _check("fp16_conv_wgrad", lib().fp16_conv_wgrad(ctypes.byref(desc), _ptr(x), _ptr(dy), _ptr(dw),
                                                     _ptr(ws), _wsb(ws, ws_bytes), _stream(stream)))
+
+
+def fp16_noalloc_scratch_bytes() -> int:
+    return int(lib().fp16_noalloc_scratch_bytes())
+
+
+def fp16_conv_wgrad_noalloc(desc, x, dy, dw, stream=None) -> None:
+    _check("fp16_conv_wgrad_noalloc", lib().fp16_conv_wgrad_noalloc(
+        ctypes.byref(desc), _ptr(x), _ptr(dy), _ptr(dw), _stream(stream)))
 
 
 def fp16_bn_workspace_bytes(desc: BnDesc) -> int:

@@ -18,7 +18,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libfp16train.so")
 
 SOURCES = ["api.hip", "sgd.hip", "bn.hip", "conv_igemm.hip", "conv_wgrad.hip", "conv_f16chain.hip", "layout.hip",
-           "pool.hip", "loss.hip"]
+           "pool.hip", "loss.hip", "noalloc.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

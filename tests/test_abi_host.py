@@ -246,6 +246,20 @@ def test_conv_accum_rejects_fused_forms():
     assert F.fp16_conv_bn_workspace_bytes(d, bd) == 0
 
 
+def test_wgrad_noalloc_validates_before_touching_the_device():
+    # no GPU here: every refusal happens before any HIP call
+    lib = F.lib()
+    assert lib.fp16_noalloc_scratch_bytes() == 32 << 20
+    big = F.conv_desc(128, 3, 224, 224, 64, 7, 7, 2, 3)  # the stem at batch 128: 81 MiB
+    assert F.fp16_conv_workspace_bytes(big, F.PASS_WGRAD) > lib.fp16_noalloc_scratch_bytes()
+    assert lib.fp16_conv_wgrad_noalloc(ctypes.byref(big), A, B, Cc, None) == WORKSPACE
+    bad = _conv()
+    bad.n = 0
+    assert lib.fp16_conv_wgrad_noalloc(ctypes.byref(bad), A, B, Cc, None) == SHAPE
+    assert lib.fp16_conv_wgrad_noalloc(None, A, B, Cc, None) == NULL
+    assert lib.fp16_conv_wgrad_noalloc(ctypes.byref(_conv()), A, None, Cc, None) == NULL
+
+
 # ---- pooling and loss: every call below is invalid, nothing is launched ---------
 
 UNSUPPORTED = 7
