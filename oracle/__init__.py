@@ -49,6 +49,7 @@ _SIGS = {
     "oracle_rne16_array": (None, [_P, _P, _I64]),
     "oracle_rne16_f32_array": (None, [_P, _P, _I64]),
     "oracle_num_threads": (_INT, []),
+    "oracle_set_num_threads": (None, [_INT]),
     "oracle_conv_out_dims": (None, [_P, _P, _P]),
     "oracle_conv_fwd": (None, [_P, _P, _P, _P, _P]),
     "oracle_conv_dgrad": (None, [_P, _P, _P, _P, _P]),
@@ -110,6 +111,11 @@ def _h(a) -> np.ndarray:
 
 def num_threads() -> int:
     return lib().oracle_num_threads()
+
+
+def set_num_threads(n: int) -> None:
+    """OpenMP threads of the following oracle calls (for single-core timing)."""
+    lib().oracle_set_num_threads(int(n))
 
 
 # ---- codec ----------------------------------------------------------------

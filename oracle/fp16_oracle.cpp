@@ -262,6 +262,15 @@ int oracle_num_threads(void) {
 #endif
 }
 
+// Threads for the following calls (timing on one core); n < 1 is ignored.
+void oracle_set_num_threads(int n) {
+#ifdef _OPENMP
+  if (n >= 1) omp_set_num_threads(n);
+#else
+  (void)n;
+#endif
+}
+
 // ---- convolution ----------------------------------------------------------
 // Each pass returns the float64 sum before rounding (y64, may be NULL) and
 // its binary16 rounding (y16, may be NULL): one rounding at the store.

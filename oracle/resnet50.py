@@ -73,3 +73,116 @@ def forward(image, labels, P, post_scale=0.25, stages=STAGES):
     T["fc.dy"] = out["dz"].reshape(T["fc.y"].shape)
     T["fc.dbias"] = out["db"]
     return out["loss"], out["loss_rows"], T
+
+
+def _bwd_bn(T, P, name, xname, dy, scale, relu, res=None, want_dres=False, eps=1e-5):
+    x = T[xname]
+    n, h, w, c = x.shape
+    shp = oracle.bn_shape(n, c, h, w)
+    return oracle.bn_bwd(shp, x, T[name + ".y"], dy, P[name + ".gamma"], eps, scale, relu,
+                         want_dres=want_dres, residual=res)
+
+
+def _bwd_conv(T, P, G, name, xname, dy, stride, pad, want_dx=True, addend=None):
+    x, w = T[xname], P[name]
+    n, h, wd, c = x.shape
+    k, r, s, _ = w.shape
+    shp = oracle.conv_shape(n, c, h, wd, k, r, s, stride, pad, "NHWC")
+    G[name] = oracle.conv_wgrad(shp, x, dy)[1]
+    if not want_dx:
+        return None
+    if addend is None:
+        return oracle.conv_dgrad(shp, dy, w)[1]
+    return oracle.conv_dgrad_add(shp, dy, w, addend)[1]
+
+
+def train_step(image, labels, P, M=None, lr=0.1, momentum=0.9, weight_decay=1e-4,
+               post_scale=0.25, stages=STAGES):
+    """One whole training step: the forward above, the backward through every
+    layer (the gradient of a block input is the branch's data gradient plus
+    the shortcut's, rounded once), and momentum SGD on every parameter in
+    binary16 (weight decay on filters, classifier weights and bias; none on
+    BN parameters, Section 5.1).  M holds the momentum buffers by parameter
+    name (zeros when absent).  Returns (mean loss, gradients, new parameters,
+    new momenta)."""
+    loss, _, T = forward(image, labels, P, post_scale, stages)
+    G = {"fc.bias": T["fc.dbias"]}
+    n = image.shape[0]
+    dgap = _bwd_conv(T, P, G, "fc", "gap.y", T["fc.dy"], 1, 0)
+    last = f"l{len(stages)}.{stages[-1][0] - 1}.bn3.y"
+    x = T[last]
+    gshp = oracle.pool_shape(n, x.shape[3], x.shape[1], x.shape[2], x.shape[1], x.shape[2], 1, 0,
+                             "NHWC")
+    dout = oracle.avgpool_bwd(gshp, dgap.reshape(n, -1))
+    blocks = [(si, bi) for si, (nb, _, _, _) in enumerate(stages) for bi in range(nb)]
+    for si, bi in reversed(blocks):
+        nm = f"l{si + 1}.{bi}"
+        st = stages[si][3] if bi == 0 else 1
+        xin = "pool.y" if (si, bi) == (0, 0) else (f"l{si + 1}.{bi - 1}.bn3.y" if bi > 0 else
+                                                   f"l{si}.{stages[si - 1][0] - 1}.bn3.y")
+        res = T[nm + ".bnd.y"] if bi == 0 else T[xin]
+        r3 = _bwd_bn(T, P, nm + ".bn3", nm + ".c3.y", dout, post_scale, True, res, True)
+        G[nm + ".bn3.gamma"], G[nm + ".bn3.beta"] = r3["dgamma"], r3["dbeta"]
+        d2 = _bwd_conv(T, P, G, nm + ".c3", nm + ".bn2.y", r3["dx"], 1, 0)
+        r2 = _bwd_bn(T, P, nm + ".bn2", nm + ".c2.y", d2, post_scale, True)
+        G[nm + ".bn2.gamma"], G[nm + ".bn2.beta"] = r2["dgamma"], r2["dbeta"]
+        d1 = _bwd_conv(T, P, G, nm + ".c2", nm + ".bn1.y", r2["dx"], st, 1)
+        r1 = _bwd_bn(T, P, nm + ".bn1", nm + ".c1.y", d1, post_scale, True)
+        G[nm + ".bn1.gamma"], G[nm + ".bn1.beta"] = r1["dgamma"], r1["dbeta"]
+        shortcut = r3["dres"]
+        if bi == 0:
+            rd = _bwd_bn(T, P, nm + ".bnd", nm + ".ds.y", shortcut, post_scale, False)
+            G[nm + ".bnd.gamma"], G[nm + ".bnd.beta"] = rd["dgamma"], rd["dbeta"]
+            shortcut = _bwd_conv(T, P, G, nm + ".ds", xin, rd["dx"], st, 0)
+        dout = _bwd_conv(T, P, G, nm + ".c1", xin, r1["dx"], 1, 0, addend=shortcut)
+    s = T["stem.bn.y"]
+    pshp = oracle.pool_shape(n, s.shape[3], s.shape[1], s.shape[2], 3, 3, 2, 1, "NHWC")
+    dstem = oracle.maxpool_bwd(pshp, s, dout)
+    rs = _bwd_bn(T, P, "stem.bn", "stem.y", dstem, 1.0, True)
+    G["stem.bn.gamma"], G["stem.bn.beta"] = rs["dgamma"], rs["dbeta"]
+    T["image"] = image
+    _bwd_conv(T, P, G, "stem", "image", rs["dx"], 2, 3, want_dx=False)
+    newP, newM = {}, {}
+    M = {} if M is None else M
+    for name, g in G.items():
+        w = P[name]
+        m = M.get(name, np.zeros_like(w))
+        wd = 0.0 if (".gamma" in name or ".beta" in name) else weight_decay
+        w1, m1 = oracle.sgd_f32(w.reshape(-1), g.reshape(-1), m.reshape(-1), lr, momentum, wd)
+        newP[name], newM[name] = w1.reshape(w.shape), m1.reshape(w.shape)
+    return loss, G, newP, newM
+
+
+def init_params(stages=STAGES, classes=1000, seed=0):
+    """He-normal filters (KRSC, std sqrt(2 / fan_in)), gamma 1, beta 0, zero
+    classifier bias, from the seeded generator shared with the HIP path."""
+    from paper_1911_07384_amd import synth
+    P, sid = {}, [1000]
+
+    def filt(name, k, r, c):
+        sid[0] += 1
+        P[name] = synth.normal_f16((k, r, r, c), synth.he_std(c * r * r), seed, sid[0])
+
+    def bn(name, c):
+        P[name + ".gamma"] = np.ones(c, np.float16)
+        P[name + ".beta"] = np.zeros(c, np.float16)
+
+    filt("stem", 64, 7, 3)
+    bn("stem.bn", 64)
+    cin = 64
+    for si, (nb, width, cout, _) in enumerate(stages):
+        for bi in range(nb):
+            nm = f"l{si + 1}.{bi}"
+            filt(nm + ".c1", width, 1, cin)
+            bn(nm + ".bn1", width)
+            filt(nm + ".c2", width, 3, width)
+            bn(nm + ".bn2", width)
+            filt(nm + ".c3", cout, 1, width)
+            bn(nm + ".bn3", cout)
+            if bi == 0:
+                filt(nm + ".ds", cout, 1, cin)
+                bn(nm + ".bnd", cout)
+            cin = cout
+    filt("fc", classes, 1, cin)
+    P["fc.bias"] = np.zeros(classes, np.float16)
+    return P

@@ -69,24 +69,29 @@ LAYERS = [
 assert sum(l.mult for l in LAYERS) == 53
 
 
-def sweep(n: int = 128, layers=None, reps: int = 10, seed: int = 0, passes=("fwd", "dgrad", "wgrad")):
+def sweep(n: int = 128, layers=None, reps: int = 10, seed: int = 0, passes=("fwd", "dgrad", "wgrad"),
+          layout: str = "NHWC"):
     """Time each convolution pass of each layer shape at batch n.
 
-    Inputs are seeded device tensors (x ~ N(0,1), He-normal W, dy ~ N(0, 1e-3^2)).
-    Each pass is timed over `reps` back-to-back calls between two HIP events on
-    the launch stream, after one untimed call.  Returns a list of dicts."""
+    Inputs are seeded device tensors (x ~ N(0,1), He-normal W, dy ~ N(0, 1e-3^2)),
+    NHWC/KRSC or NCHW/KCRS.  Each pass is timed over `reps` back-to-back calls
+    between two HIP events on the launch stream, after one untimed call.
+    Returns a list of dicts."""
     layers = LAYERS if layers is None else layers
     gen = torch.Generator(device="cuda")
     gen.manual_seed(seed)
     out = []
     for L in layers:
         p = L.out_hw
-        d = F.conv_desc(n, L.c, L.hw, L.hw, L.k, L.r, L.r, L.stride, L.pad)
-        x = torch.randn((n, L.hw, L.hw, L.c), generator=gen, device="cuda").half()
-        w = (torch.randn((L.k, L.r, L.r, L.c), generator=gen, device="cuda")
-             * (2.0 / (L.c * L.r * L.r)) ** 0.5).half()
-        dy = (torch.randn((n, p, p, L.k), generator=gen, device="cuda") * 1e-3).half()
-        y = torch.empty((n, p, p, L.k), dtype=torch.float16, device="cuda")
+        d = F.conv_desc(n, L.c, L.hw, L.hw, L.k, L.r, L.r, L.stride, L.pad, layout)
+        if layout == "NHWC":
+            xs, ws_, ys = (n, L.hw, L.hw, L.c), (L.k, L.r, L.r, L.c), (n, p, p, L.k)
+        else:
+            xs, ws_, ys = (n, L.c, L.hw, L.hw), (L.k, L.c, L.r, L.r), (n, L.k, p, p)
+        x = torch.randn(xs, generator=gen, device="cuda").half()
+        w = (torch.randn(ws_, generator=gen, device="cuda") * (2.0 / (L.c * L.r * L.r)) ** 0.5).half()
+        dy = (torch.randn(ys, generator=gen, device="cuda") * 1e-3).half()
+        y = torch.empty(ys, dtype=torch.float16, device="cuda")
         dx = torch.empty_like(x)
         dw = torch.empty_like(w)
         ws = F.workspace(max(F.fp16_conv_workspace_bytes(d, q) for q in (0, 1, 2)))
