@@ -367,7 +367,7 @@ def cold_hbm_leg(torch, reps=5):
     gen.manual_seed(11)
 
     flush.fill_(1)
-    sink = torch.empty(1, dtype=torch.int64, device="cuda")
+    words = flush.view(torch.int64)
 
     def timed_cold(fn):
         out = []
@@ -375,7 +375,7 @@ def cold_hbm_leg(torch, reps=5):
             # read (not write) 1 GiB: the Infinity Cache then holds only clean
             # lines of this buffer, so the timed call neither hits on its own
             # inputs nor pays for writing back someone else's dirty lines
-            torch.sum(flush, dtype=torch.int64, out=sink)
+            words.sum()
             torch.cuda.synchronize()
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
