@@ -22,8 +22,7 @@
 // 16-byte vector and per-channel coefficients are computed once per thread.
 // Other shapes and the NCHW layout use a generic per-element path.
 // Reductions are float32 within a thread, combined in a fixed order within a
-// block and in float64 across blocks (channel-major partials, one wave per
-// channel): the result does not depend on timing.
+// block and in float64 across blocks: the result does not depend on timing.
 
 #include "kernels.hpp"
 
@@ -31,6 +30,10 @@ namespace fp16k {
 namespace {
 
 constexpr int kT = 256;
+// from this many channels on the vectorised reduces write block-major
+// partials and the finalize takes 64 channels per block (else channel-major
+// partials and one block per channel)
+constexpr int kBmC = 256;
 
 struct Geo {
   int64_t M;  // elements per channel
@@ -130,11 +133,13 @@ __device__ __forceinline__ bool relu_mask(bool relu, bool has_y, h16 y, float x,
 // Lanes of one wave that hold the same chunk are combined by a butterfly
 // over the lane bits at or above log2(CV); the waves' totals (or, for
 // CV > 64, the threads' own values) are then summed in a fixed order from
-// LDS and written to the channel-major partial arrays
-// out[(v * C + c) * G + block].  red: [8 * NS][kT].
+// LDS and written either block-major, out[(block * NS + v) * C + c] (bm:
+// each block writes its sums as one contiguous run; from 256 channels on),
+// or channel-major, out[(v * C + c) * G + block] (fewer channels: the
+// finalize then spreads over one block per channel).  red: [8 * NS][kT].
 template <int NS>
 __device__ __forceinline__ void block_reduce_vec(float (&sums)[NS][8], float* red, int CV, int RB,
-                                                 float* out, int G) {
+                                                 float* out, bool bm) {
   const int t = threadIdx.x;
   const int lane = t & 63;
   int groups;
@@ -167,7 +172,10 @@ __device__ __forceinline__ void block_reduce_vec(float (&sums)[NS][8], float* re
     float acc = red[ve * kT + j];
     for (int gi = 1; gi < groups; ++gi) acc += red[ve * kT + gi * CV + j];
     const int v = ve >> 3, e = ve & 7;
-    out[((int64_t)v * C + j * 8 + e) * G + blockIdx.x] = acc;
+    if (bm)
+      out[((int64_t)blockIdx.x * NS + v) * C + j * 8 + e] = acc;
+    else
+      out[((int64_t)v * C + j * 8 + e) * gridDim.x + blockIdx.x] = acc;
   }
 }
 
@@ -215,7 +223,7 @@ __global__ __launch_bounds__(kT) void bn_fwd_reduce_vec(const h16* __restrict__ 
       }
     }
   }
-  block_reduce_vec<2>(sums, red, CV, RB, ws, (int)gridDim.x);
+  block_reduce_vec<2>(sums, red, CV, RB, ws, g.C >= kBmC);
 }
 
 // Tree reduction of NS values per thread over the block (fixed order).
@@ -239,8 +247,6 @@ __device__ __forceinline__ void block_reduce_1(float (&v)[NS], float* red) {
 
 __global__ __launch_bounds__(kT) void bn_fwd_reduce_gen(const h16* __restrict__ x, Geo g,
                                                         int64_t rpb, float* ws) {
-  float* ws1 = ws;
-  float* ws2 = ws + (int64_t)g.C * gridDim.x;
   __shared__ float red[2 * kT];
   const int c = blockIdx.y;
   const int64_t j0 = (int64_t)blockIdx.x * rpb;
@@ -256,16 +262,16 @@ __global__ __launch_bounds__(kT) void bn_fwd_reduce_gen(const h16* __restrict__ 
   float v[2] = {s1, s2};
   block_reduce_1<2>(v, red);
   if (threadIdx.x == 0) {
-    ws1[(int64_t)c * gridDim.x + blockIdx.x] = v[0];
-    ws2[(int64_t)c * gridDim.x + blockIdx.x] = v[1];
+    ws[(int64_t)c * gridDim.x + blockIdx.x] = v[0];
+    ws[((int64_t)g.C + c) * gridDim.x + blockIdx.x] = v[1];
   }
 }
 
-// Sum of the G block partials of channel c in float64: each lane of one wave
-// takes every 64th partial, in index order, then a butterfly over the wave (a
-// fixed order, so the total does not depend on timing).  The partials of a
-// lane are loaded 16 at a time before any is added, so one memory round trip
-// covers up to 1,024 partials.
+// Sum of the G channel-major partials of channel c in float64: each lane of
+// one wave takes every 64th partial, in index order, then a butterfly over
+// the wave (a fixed order, so the total does not depend on timing).  The
+// partials of a lane are loaded 16 at a time before any is added, so one
+// memory round trip covers up to 1,024 partials.
 __device__ __forceinline__ void channel_sums(const float* ws1, const float* ws2, int c, int G,
                                              double& S1, double& S2) {
   const int t = threadIdx.x;
@@ -283,8 +289,6 @@ __device__ __forceinline__ void channel_sums(const float* ws1, const float* ws2,
       u1[u] = p1[i];
       u2[u] = p2[i];
     }
-    // adding zero for the lanes past G keeps every load unconditional (a
-    // load used only under a condition would be moved behind it)
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const bool ok = j + 64 * u < G;
@@ -301,18 +305,79 @@ __device__ __forceinline__ void channel_sums(const float* ws1, const float* ws2,
   S2 = b;
 }
 
-__global__ __launch_bounds__(64) void bn_fwd_finalize(const h16* __restrict__ x, Geo g, int G,
-                                                      const float* ws, float eps, float* stats) {
-  const int c = blockIdx.x;
-  double S1, S2;
-  channel_sums(ws, ws + (int64_t)g.C * G, c, G, S1, S2);
-  if (threadIdx.x != 0) return;
+// Sums over the G blocks of the block-major partials part[(b * NS + v) * C + c]
+// in float64, for the 64 channels of this block (lane = channel): wave w
+// takes the blocks w, w + kFinW, w + 2 kFinW, ... in order (kFinU loads of
+// each value in flight, clamped in bounds, so every row read is 256
+// contiguous bytes), then the first wave adds the kFinW wave sums in order.
+// A fixed order, so the result does not depend on timing.
+constexpr int kFinW = 16, kFinU = 8;
+
+template <int NS>
+__device__ __forceinline__ void group_sums(const float* part, int C, int G, int c, bool live,
+                                           double (&S)[NS]) {
+  __shared__ double red[NS][kFinW][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int cc = live ? c : 0;
+  double acc[NS];
+#pragma unroll
+  for (int v = 0; v < NS; ++v) acc[v] = 0.0;
+  for (int b0 = w; b0 < G; b0 += kFinW * kFinU) {
+    float u[kFinU][NS];
+#pragma unroll
+    for (int k = 0; k < kFinU; ++k) {
+      const int b = b0 + kFinW * k < G ? b0 + kFinW * k : G - 1;
+#pragma unroll
+      for (int v = 0; v < NS; ++v) u[k][v] = part[((int64_t)b * NS + v) * C + cc];
+    }
+#pragma unroll
+    for (int k = 0; k < kFinU; ++k) {
+      const bool ok = b0 + kFinW * k < G;
+#pragma unroll
+      for (int v = 0; v < NS; ++v) acc[v] += ok ? (double)u[k][v] : 0.0;
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < NS; ++v) red[v][w][lane] = acc[v];
+  __syncthreads();
+#pragma unroll
+  for (int v = 0; v < NS; ++v) {
+    double t = 0.0;
+    for (int i = 0; i < kFinW; ++i) t += red[v][i][lane];
+    S[v] = t;
+  }
+}
+
+__device__ __forceinline__ void fwd_stats(const h16* x, Geo g, int c, double S1, double S2,
+                                          float eps, float* stats) {
   const double sh = (double)to_f32(x[geo_at(g, c, 0)]);
   const double md = S1 / (double)g.M;
   double var = S2 / (double)g.M - md * md;
   if (var < 0.0) var = 0.0;
   stats[c] = (float)(sh + md);
   stats[g.C + c] = (float)(1.0 / __builtin_sqrt(var + (double)eps));
+}
+
+// channel-major partials: one 64-thread block per channel
+__global__ __launch_bounds__(64) void bn_fwd_finalize(const h16* __restrict__ x, Geo g, int G,
+                                                      const float* ws, float eps, float* stats) {
+  const int c = blockIdx.x;
+  double S1, S2;
+  channel_sums(ws, ws + (int64_t)g.C * G, c, G, S1, S2);
+  if (threadIdx.x != 0) return;
+  fwd_stats(x, g, c, S1, S2, eps, stats);
+}
+
+// block-major partials: one block per 64 channels
+__global__ __launch_bounds__(64 * kFinW) void bn_fwd_finalize_bm(const h16* __restrict__ x, Geo g,
+                                                                 int G, const float* ws, float eps,
+                                                                 float* stats) {
+  const int c = blockIdx.x * 64 + (threadIdx.x & 63);
+  const bool live = c < g.C;
+  double S[2];
+  group_sums<2>(ws, g.C, G, c, live, S);
+  if (threadIdx.x >= 64 || !live) return;
+  fwd_stats(x, g, c, S[0], S[1], eps, stats);
 }
 
 // Statistics from the records a convolution's epilogue wrote ([nb][3][C]:
@@ -612,7 +677,7 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
     __builtin_amdgcn_sched_barrier(0);
     sum_row(rb, i + 1);
   }
-  block_reduce_vec<NS>(sums, red, CV, RB, ws, (int)gridDim.x);
+  block_reduce_vec<NS>(sums, red, CV, RB, ws, g.C >= kBmC);
 }
 
 __global__ __launch_bounds__(kT) void bn_bwd_reduce_gen(const h16* __restrict__ x,
@@ -654,7 +719,21 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_gen(const h16* __restrict__ 
 // S2 = rstd*T = sum g*xhat; dbeta = S1, dgamma = S2 (+ S3 with the BN swap),
 // one rounding from float64; apply coefficients A = gamma*rstd, B = S1/M and
 // D = rstd*S2/M for dx = A * (g - ((x - mean)*D + B)), which is
-// A * (g - (xhat*S2/M + S1/M)).  One 64-thread block per channel.
+// A * (g - (xhat*S2/M + S1/M)).  One block per 64 channels (NS = 3 partial
+// sums with the BN swap, else 2).
+__device__ __forceinline__ void bwd_coef(Geo g, int c, double S1, double T, double S3,
+                                         const h16* gamma, const float* stats, h16* dgamma,
+                                         h16* dbeta, float* coef) {
+  const double rstd = (double)stats[g.C + c];
+  const double S2 = rstd * T;
+  dbeta[c] = dbl_to_h16(S1);
+  dgamma[c] = dbl_to_h16(S2 + S3);
+  coef[c] = to_f32(gamma[c]) * stats[g.C + c];
+  coef[g.C + c] = (float)(S1 / (double)g.M);
+  coef[2 * g.C + c] = (float)(rstd * S2 / (double)g.M);
+}
+
+// channel-major partials: one 64-thread block per channel
 __global__ __launch_bounds__(64) void bn_bwd_finalize(Geo g, int G, const float* ws,
                                                       const h16* __restrict__ gamma,
                                                       const float* __restrict__ stats, h16* dgamma,
@@ -665,13 +744,23 @@ __global__ __launch_bounds__(64) void bn_bwd_finalize(Geo g, int G, const float*
   channel_sums(ws, ws + CG, c, G, S1, T);
   if (g.swap) channel_sums(ws + 2 * CG, ws + 2 * CG, c, G, S3, unused);
   if (threadIdx.x != 0) return;
-  const double rstd = (double)stats[g.C + c];
-  const double S2 = rstd * T;
-  dbeta[c] = dbl_to_h16(S1);
-  dgamma[c] = dbl_to_h16(S2 + S3);
-  coef[c] = to_f32(gamma[c]) * stats[g.C + c];
-  coef[g.C + c] = (float)(S1 / (double)g.M);
-  coef[2 * g.C + c] = (float)(rstd * S2 / (double)g.M);
+  bwd_coef(g, c, S1, T, S3, gamma, stats, dgamma, dbeta, coef);
+}
+
+// block-major partials (NS = 3 with the BN swap, else 2): one block per 64
+// channels
+template <int NS>
+__global__ __launch_bounds__(64 * kFinW) void bn_bwd_finalize_bm(Geo g, int G, const float* ws,
+                                                                 const h16* __restrict__ gamma,
+                                                                 const float* __restrict__ stats,
+                                                                 h16* dgamma, h16* dbeta,
+                                                                 float* coef) {
+  const int c = blockIdx.x * 64 + (threadIdx.x & 63);
+  const bool live = c < g.C;
+  double S[NS];
+  group_sums<NS>(ws, g.C, G, c, live, S);
+  if (threadIdx.x >= 64 || !live) return;
+  bwd_coef(g, c, S[0], S[1], NS == 3 ? S[NS - 1] : 0.0, gamma, stats, dgamma, dbeta, coef);
 }
 
 // ---- backward apply ------------------------------------------------------------
@@ -822,8 +911,9 @@ Geo make_geo(const BnArgs& a) {
 
 size_t align256(size_t v) { return (v + 255) & ~(size_t)255; }
 
-// Workspace: up to three channel-major partial arrays [3][C][G] (float32),
-// then the backward's apply coefficients [3][C].
+// Workspace: the partial sums, block-major [G][NS][C] from kBmC channels on,
+// else channel-major [NS][C][G] (float32, NS <= 3), then the backward's apply
+// coefficients [3][C].
 size_t partial_bytes(const Plan& p, int C) { return align256((size_t)3 * p.G * C * sizeof(float)); }
 
 }  // namespace
@@ -854,8 +944,12 @@ hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const 
                          part);
     else
       hipLaunchKernelGGL(bn_fwd_reduce_gen, dim3(p.G, a.C), dim3(kT), 0, st, x, g, p.rpb, part);
-    hipLaunchKernelGGL(bn_fwd_finalize, dim3(a.C), dim3(64), 0, st, x, g, p.G, part, a.eps,
-                       stats);
+    if (p.vec && a.C >= kBmC)
+      hipLaunchKernelGGL(bn_fwd_finalize_bm, dim3((a.C + 63) / 64), dim3(64 * kFinW), 0, st, x, g,
+                         p.G, part, a.eps, stats);
+    else
+      hipLaunchKernelGGL(bn_fwd_finalize, dim3(a.C), dim3(64), 0, st, x, g, p.G, part, a.eps,
+                         stats);
   }
   if (p.vec) {
     const hipError_t e =
@@ -924,8 +1018,15 @@ hipError_t launch_bn_bwd(const BnArgs& a, const h16* x, const h16* y, const h16*
     hipLaunchKernelGGL(bn_bwd_reduce_gen, dim3(p.G, a.C), dim3(kT), 0, st, x, y, dy, gamma, beta,
                        res, stats, g, p.rpb, a.post_scale, a.relu, part);
   }
-  hipLaunchKernelGGL(bn_bwd_finalize, dim3(a.C), dim3(64), 0, st, g, p.G, part, gamma, stats,
-                     dgamma, dbeta, coef);
+  if (!(p.vec && a.C >= kBmC))
+    hipLaunchKernelGGL(bn_bwd_finalize, dim3(a.C), dim3(64), 0, st, g, p.G, part, gamma, stats,
+                       dgamma, dbeta, coef);
+  else if (a.swap)
+    hipLaunchKernelGGL(bn_bwd_finalize_bm<3>, dim3((a.C + 63) / 64), dim3(64 * kFinW), 0, st, g,
+                       p.G, part, gamma, stats, dgamma, dbeta, coef);
+  else
+    hipLaunchKernelGGL(bn_bwd_finalize_bm<2>, dim3((a.C + 63) / 64), dim3(64 * kFinW), 0, st, g,
+                       p.G, part, gamma, stats, dgamma, dbeta, coef);
   if (p.vec) {
     const dim3 grid(apply_grid(g.M * p.CV / (kApplyU / 2), p.CV));
     switch (mode) {
