@@ -101,8 +101,10 @@ def bn_elems(d):
 def op_work(op, net):
     """(flops, bytes, bound) of one call of the network's program (the
     per-unit figures of the design: BN forward 6 B/element + 2 with the
-    shortcut, 4 + 2 when its statistics come from the convolution; BN
-    backward 10 B/element + 4 with the shortcut; SGD 10 B/element)."""
+    shortcut, 4 + 2 when its statistics come from the convolution, + 1/8 for
+    a kept ReLU mask; BN backward 10 B/element + 4 with the shortcut
+    recomputing the mask, + 2 (the shortcut gradient) + 1/4 (the mask, read
+    twice) with a kept mask; SGD 10 B/element)."""
     a, k = op.a, op.kind
     if k in ("conv_fwd", "conv_dgrad", "conv_dgrad_add", "conv_wgrad"):
         fl, by = conv_work(a["desc"], {"conv_fwd": "fwd", "conv_wgrad": "wgrad"}.get(k, "dgrad"))
@@ -112,13 +114,15 @@ def op_work(op, net):
     if k == "conv_bn_fwd":
         fl, by = conv_work(a["desc"], "fwd")
         e = bn_elems(a["bn"])
-        by += 4 * e + (2 * e if a["res"] is not None else 0)
+        by += 4 * e + (2 * e if a["res"] is not None else 0) + (e // 8 if a["mask"] else 0)
         return fl, by, "mfma" if fl / by >= RIDGE else "hbm"
     if k == "bn_fwd":
         e = bn_elems(a["desc"])
-        return 0, 6 * e + (2 * e if a["res"] is not None else 0), "hbm"
+        return 0, 6 * e + (2 * e if a["res"] is not None else 0) + (e // 8 if a["mask"] else 0), "hbm"
     if k == "bn_bwd":
         e = bn_elems(a["desc"])
+        if a["mask"]:
+            return 0, 10 * e + (2 * e if a["dres"] is not None else 0) + e // 4, "hbm"
         return 0, 10 * e + (4 * e if a["dres"] is not None else 0), "hbm"
     if k == "dgrad_filter":
         d = a["desc"]
@@ -398,6 +402,19 @@ def cold_hbm_leg(torch, reps=5):
         return a.elapsed_time(b) / n
 
     res = {}
+    # what plain streams reach on this chip with the cache cold: a 1 GiB read
+    # (sum), write (fill) and copy, the ceilings the fractions below sit under
+    buf = torch.empty(1 << 27, dtype=torch.int64, device="cuda")
+    dst = torch.empty(1 << 26, dtype=torch.int64, device="cuda")
+    ref = {}
+    for name, fn, byts in (("read_1GiB", lambda: buf.sum(), 1 << 30),
+                           ("write_1GiB", lambda: buf.fill_(3), 1 << 30),
+                           ("copy_512MiB", lambda: dst.copy_(buf[: 1 << 26]), 1 << 30)):
+        c = timed_cold(fn)
+        ref[name] = {"cold_us": round(c * 1e3, 1), "cold_gbs": round(byts / c / 1e6, 1),
+                     "cold_frac": round(byts / c / 1e6 / PEAK_HBM_GBS, 4)}
+    res["stream_reference"] = ref
+    del buf, dst
 
     def record(name, fn, byts):
         c, w = timed_cold(fn), timed_warm(fn)
@@ -431,7 +448,14 @@ def cold_hbm_leg(torch, reps=5):
     record("bn_fwd_conv2x_b128", lambda: F.fp16_bn_relu(d, x, gamma, beta, r, y, st, ws), 8 * e)
     record("bn_bwd_conv2x_b128", lambda: F.fp16_bn_relu_bwd(d, x, None, dy, gamma, beta, r, st, dx,
                                                             dg, db, dr, ws), 14 * e)
-    del x, r, dy, y, dx, dr, ws
+    # the same pair with the ReLU mask kept by the forward (the network's form)
+    mk = torch.empty(F.fp16_bn_mask_bytes(d), dtype=torch.uint8, device="cuda")
+    record("bn_fwd_mask_conv2x_b128",
+           lambda: F.fp16_bn_relu_m(d, x, gamma, beta, r, y, st, mk, ws), 8 * e + e // 8)
+    record("bn_bwd_mask_conv2x_b128",
+           lambda: F.fp16_bn_relu_bwd_m(d, x, mk, dy, gamma, beta, st, dx, dg, db, dr, ws),
+           12 * e + e // 4)
+    del x, r, dy, y, dx, dr, ws, mk
     # the 1x1 64 -> 256 convolution of conv2_x at batch 128 (HBM-bound, AI 51)
     xc = torch.randn((N, H, H, 64), generator=gen, device="cuda").half()
     wc = (torch.randn((256, 1, 1, 64), generator=gen, device="cuda") * 0.17).half()
@@ -444,8 +468,10 @@ def cold_hbm_leg(torch, reps=5):
     torch.cuda.empty_cache()
     res["note"] = ("cold: one call after reading a 1 GiB buffer (evicts the 256 MB Infinity Cache), "
                    "median of 5; warm: 10 back-to-back calls; bytes are the algorithmic bytes "
-                   "(SGD 10 B/element, BN forward with statistics and shortcut 8, BN backward with "
-                   "shortcut 14, the convolution's compulsory bytes)")
+                   "(SGD 10 B/element, BN forward with statistics and shortcut 8 (+1/8 keeping the "
+                   "ReLU mask), BN backward with shortcut 14 (12.25 with the kept mask), the "
+                   "convolution's compulsory bytes); stream_reference: torch's own sum, fill and "
+                   "copy under the same cold protocol")
     return res
 
 

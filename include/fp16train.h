@@ -234,6 +234,35 @@ fp16_status fp16_bn_relu_bwd(const fp16_bn_desc* desc, const fp16_t* x, const fp
                              fp16_t* dgamma, fp16_t* dbeta, fp16_t* dresidual, void* ws,
                              size_t ws_bytes, fp16_stream_t stream);
 
+/* ---- the ReLU mask kept from the forward for the backward ----
+ * The backward of a BN whose output joins the shortcut before the ReLU (the
+ * last BN of each residual block, Section 4.1's bottleneck) needs the ReLU
+ * mask, [y > 0].  Recomputing it reads the shortcut again (2 bytes per
+ * element); the forward can keep it instead, one bit per element, and the
+ * backward read that (1/8 byte per element).  The mask is one byte per 8
+ * channels of each pixel, for NHWC with C/8 a power of two up to 256 (C = 8,
+ * 16, ..., 2048: every BN of ResNet-50 but the stem's) and ReLU on:
+ *   mask[(n*H*W + h*W + w) * (C/8) + j] bit e = [y[n,h,w,8j+e] > 0].
+ * fp16_bn_mask_bytes: its size, 0 where it is not offered (NCHW, other C, no
+ * ReLU, the BN swap); the _m calls then return
+ * FP16_ERR_UNSUPPORTED.  The mask is caller-owned, 16-byte aligned, and must
+ * not overlap any other argument.
+ * fp16_bn_relu_m / fp16_conv_bn_relu_fwd_m: fp16_bn_relu /
+ *   fp16_conv_bn_relu_fwd (bit-identical outputs) that also write the mask of
+ *   their BN output.
+ * fp16_bn_relu_bwd_m: fp16_bn_relu_bwd with the mask read from `mask`
+ *   instead of being taken from y or recomputed from the shortcut (which is
+ *   not needed: dresidual = mask ? dy : 0); bit-identical outputs. */
+size_t fp16_bn_mask_bytes(const fp16_bn_desc* desc);
+fp16_status fp16_bn_relu_m(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t* gamma,
+                           const fp16_t* beta, const fp16_t* residual, fp16_t* y, float* stats,
+                           uint8_t* mask, void* ws, size_t ws_bytes, fp16_stream_t stream);
+fp16_status fp16_bn_relu_bwd_m(const fp16_bn_desc* desc, const fp16_t* x, const uint8_t* mask,
+                               const fp16_t* dy, const fp16_t* gamma, const fp16_t* beta,
+                               const float* stats, fp16_t* dx, fp16_t* dgamma, fp16_t* dbeta,
+                               fp16_t* dresidual, void* ws, size_t ws_bytes,
+                               fp16_stream_t stream);
+
 /* Momentum SGD on FP16 weights and an FP16 momentum buffer, with no master
  * copy (Section 5.1 recipe: PyTorch SGD, dampening 0, no Nesterov;
  * Section 5.2), in place over n elements:
@@ -289,6 +318,13 @@ fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc
                                   const fp16_t* beta, const fp16_t* residual, fp16_t* y,
                                   fp16_t* z, float* stats, void* ws, size_t ws_bytes,
                                   fp16_stream_t stream);
+
+/* The same with the ReLU mask of z kept (see fp16_bn_mask_bytes). */
+fp16_status fp16_conv_bn_relu_fwd_m(const fp16_conv_desc* conv, const fp16_bn_desc* bn,
+                                    const fp16_t* x, const fp16_t* w, const fp16_t* gamma,
+                                    const fp16_t* beta, const fp16_t* residual, fp16_t* y,
+                                    fp16_t* z, float* stats, uint8_t* mask, void* ws,
+                                    size_t ws_bytes, fp16_stream_t stream);
 
 /* ---- the rest of ResNet-50 around the residual blocks (Section 5.1) ---- */
 

@@ -33,7 +33,8 @@ EXPORTS = ["fp16_conv_out_dims", "fp16_conv_workspace_bytes", "fp16_conv_fwd", "
            "fp16_avgpool_fwd", "fp16_avgpool_bwd", "fp16_softmax_ce", "fp16_status_string",
            "fp16_version", "fp16_conv_bn_workspace_bytes", "fp16_conv_bn_relu_fwd",
            "fp16_sgd_step_f16", "fp16_conv_dgrad_filter_bytes", "fp16_conv_dgrad_filter",
-           "fp16_conv_dgrad_wf", "fp16_noalloc_scratch_bytes", "fp16_conv_wgrad_noalloc"]
+           "fp16_conv_dgrad_wf", "fp16_noalloc_scratch_bytes", "fp16_conv_wgrad_noalloc",
+           "fp16_bn_mask_bytes", "fp16_bn_relu_m", "fp16_bn_relu_bwd_m", "fp16_conv_bn_relu_fwd_m"]
 
 
 class Fp16Error(RuntimeError):
@@ -78,6 +79,10 @@ _SIGS = {
     "fp16_conv_dgrad_filter": (ctypes.c_int, [_P, _P, _P, _P]),
     "fp16_conv_dgrad_wf": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_bn_workspace_bytes": (_SZ, [_P]),
+    "fp16_bn_mask_bytes": (_SZ, [_P]),
+    "fp16_bn_relu_m": (ctypes.c_int, [_P] * 9 + [_SZ, _P]),
+    "fp16_bn_relu_bwd_m": (ctypes.c_int, [_P] * 12 + [_SZ, _P]),
+    "fp16_conv_bn_relu_fwd_m": (ctypes.c_int, [_P] * 12 + [_SZ, _P]),
     "fp16_bn_relu": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_bn_relu_bwd": (ctypes.c_int, [_P] * 13 + [_SZ, _P]),
     "fp16_sgd_step": (ctypes.c_int, [_P, _P, _P, _SZ, _F, _F, _F, _P]),
@@ -243,6 +248,25 @@ def fp16_bn_relu_bwd(desc, x, y, dy, gamma, beta, residual, stats, dx, dgamma, d
         _wsb(ws, ws_bytes), _stream(stream)))
 
 
+def fp16_bn_mask_bytes(desc: BnDesc) -> int:
+    return int(lib().fp16_bn_mask_bytes(ctypes.byref(desc)))
+
+
+def fp16_bn_relu_m(desc, x, gamma, beta, residual, y, stats, mask, ws=None, ws_bytes=None,
+                   stream=None) -> None:
+    _check("fp16_bn_relu_m", lib().fp16_bn_relu_m(
+        ctypes.byref(desc), _ptr(x), _ptr(gamma), _ptr(beta), _ptr(residual), _ptr(y), _ptr(stats),
+        _ptr(mask), _ptr(ws), _wsb(ws, ws_bytes), _stream(stream)))
+
+
+def fp16_bn_relu_bwd_m(desc, x, mask, dy, gamma, beta, stats, dx, dgamma, dbeta, dresidual,
+                       ws=None, ws_bytes=None, stream=None) -> None:
+    _check("fp16_bn_relu_bwd_m", lib().fp16_bn_relu_bwd_m(
+        ctypes.byref(desc), _ptr(x), _ptr(mask), _ptr(dy), _ptr(gamma), _ptr(beta), _ptr(stats),
+        _ptr(dx), _ptr(dgamma), _ptr(dbeta), _ptr(dresidual), _ptr(ws), _wsb(ws, ws_bytes),
+        _stream(stream)))
+
+
 def fp16_sgd_step(w, g, m, n=None, lr=0.1, momentum=0.9, weight_decay=1e-4, stream=None) -> None:
     if n is None:
         n = w.numel()
@@ -308,6 +332,14 @@ def fp16_conv_bn_relu_fwd(conv, bn, x, w, gamma, beta, residual, y, z, stats, ws
     _check("fp16_conv_bn_relu_fwd", lib().fp16_conv_bn_relu_fwd(
         ctypes.byref(conv), ctypes.byref(bn), _ptr(x), _ptr(w), _ptr(gamma), _ptr(beta),
         _ptr(residual), _ptr(y), _ptr(z), _ptr(stats), _ptr(ws), _wsb(ws, ws_bytes),
+        _stream(stream)))
+
+
+def fp16_conv_bn_relu_fwd_m(conv, bn, x, w, gamma, beta, residual, y, z, stats, mask, ws=None,
+                            ws_bytes=None, stream=None) -> None:
+    _check("fp16_conv_bn_relu_fwd_m", lib().fp16_conv_bn_relu_fwd_m(
+        ctypes.byref(conv), ctypes.byref(bn), _ptr(x), _ptr(w), _ptr(gamma), _ptr(beta),
+        _ptr(residual), _ptr(y), _ptr(z), _ptr(stats), _ptr(mask), _ptr(ws), _wsb(ws, ws_bytes),
         _stream(stream)))
 
 

@@ -451,13 +451,25 @@ size_t fp16_bn_workspace_bytes(const fp16_bn_desc* desc) {
   return bn_ws_bytes(a);
 }
 
-fp16_status fp16_bn_relu(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t* gamma,
-                         const fp16_t* beta, const fp16_t* residual, fp16_t* y, float* stats,
-                         void* ws, size_t ws_bytes, fp16_stream_t stream) {
+// The ReLU mask a forward keeps: one byte per 8 channels of each pixel.
+static fp16_status check_mask(const BnArgs& a, const void* mask, size_t* bytes) {
+  if (!mask) return FP16_ERR_NULL;
+  if (!aligned16(mask)) return FP16_ERR_MISALIGNED;
+  if (a.swap) return FP16_ERR_UNSUPPORTED;
+  *bytes = bn_keep_mask_bytes(a);
+  return *bytes ? FP16_OK : FP16_ERR_UNSUPPORTED;
+}
+
+static fp16_status bn_fwd_impl(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t* gamma,
+                               const fp16_t* beta, const fp16_t* residual, fp16_t* y, float* stats,
+                               uint8_t* mask, bool want_mask, void* ws, size_t ws_bytes,
+                               fp16_stream_t stream) {
   BnArgs a;
   fp16_status s = check_bn(desc, &a);
   if (s != FP16_OK) return s;
   if (!x || !gamma || !beta || !y || !stats) return FP16_ERR_NULL;
+  size_t mb = 0;
+  if (want_mask && (s = check_mask(a, mask, &mb)) != FP16_OK) return s;
   if (a.swap && !residual) return FP16_ERR_NULL;
   if (!aligned16(x) || !aligned16(y) || (residual && !aligned16(residual)) || !aligned16(stats))
     return FP16_ERR_MISALIGNED;
@@ -474,22 +486,53 @@ fp16_status fp16_bn_relu(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t
   if (overlap(ws, need, x, eb) || overlap(ws, need, residual, eb) || overlap(ws, need, gamma, cb) ||
       overlap(ws, need, beta, cb))
     return FP16_ERR_ALIASING;
+  if (mb && (overlap(mask, mb, x, eb) || overlap(mask, mb, y, eb) ||
+             overlap(mask, mb, residual, eb) || overlap(mask, mb, gamma, cb) ||
+             overlap(mask, mb, beta, cb) || overlap(mask, mb, stats, (size_t)a.C * 8) ||
+             overlap(mask, mb, ws, need)))
+    return FP16_ERR_ALIASING;
   return hip_status(launch_bn_fwd(a, reinterpret_cast<const h16*>(x),
                                   reinterpret_cast<const h16*>(gamma),
                                   reinterpret_cast<const h16*>(beta),
                                   reinterpret_cast<const h16*>(residual), reinterpret_cast<h16*>(y),
-                                  stats, desc->use_stats, ws, static_cast<hipStream_t>(stream)));
+                                  stats, desc->use_stats, ws, mb ? mask : nullptr,
+                                  static_cast<hipStream_t>(stream)));
 }
 
-fp16_status fp16_bn_relu_bwd(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t* y,
-                             const fp16_t* dy, const fp16_t* gamma, const fp16_t* beta,
-                             const fp16_t* residual, const float* stats, fp16_t* dx,
-                             fp16_t* dgamma, fp16_t* dbeta, fp16_t* dresidual, void* ws,
-                             size_t ws_bytes, fp16_stream_t stream) {
+fp16_status fp16_bn_relu(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t* gamma,
+                         const fp16_t* beta, const fp16_t* residual, fp16_t* y, float* stats,
+                         void* ws, size_t ws_bytes, fp16_stream_t stream) {
+  return bn_fwd_impl(desc, x, gamma, beta, residual, y, stats, nullptr, false, ws, ws_bytes,
+                     stream);
+}
+
+size_t fp16_bn_mask_bytes(const fp16_bn_desc* desc) {
+  BnArgs a;
+  if (check_bn(desc, &a) != FP16_OK || a.swap) return 0;
+  return bn_keep_mask_bytes(a);
+}
+
+fp16_status fp16_bn_relu_m(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t* gamma,
+                           const fp16_t* beta, const fp16_t* residual, fp16_t* y, float* stats,
+                           uint8_t* mask, void* ws, size_t ws_bytes, fp16_stream_t stream) {
+  return bn_fwd_impl(desc, x, gamma, beta, residual, y, stats, mask, true, ws, ws_bytes, stream);
+}
+
+static fp16_status bn_bwd_impl(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t* y,
+                               const fp16_t* dy, const fp16_t* gamma, const fp16_t* beta,
+                               const fp16_t* residual, const float* stats, const uint8_t* mask,
+                               bool with_mask, fp16_t* dx, fp16_t* dgamma, fp16_t* dbeta,
+                               fp16_t* dresidual, void* ws, size_t ws_bytes,
+                               fp16_stream_t stream) {
   BnArgs a;
   fp16_status s = check_bn(desc, &a);
   if (s != FP16_OK) return s;
   if (!x || !dy || !gamma || !beta || !stats || !dx || !dgamma || !dbeta) return FP16_ERR_NULL;
+  size_t mb = 0;
+  if (with_mask) {
+    if ((s = check_mask(a, mask, &mb)) != FP16_OK) return s;
+    if (!a.relu) return FP16_ERR_UNSUPPORTED;
+  }
   if (a.swap && !residual) return FP16_ERR_NULL;
   if (!aligned16(x) || (y && !aligned16(y)) || !aligned16(dy) || !aligned16(dx) ||
       (residual && !aligned16(residual)) || (dresidual && !aligned16(dresidual)) ||
@@ -517,12 +560,35 @@ fp16_status fp16_bn_relu_bwd(const fp16_bn_desc* desc, const fp16_t* x, const fp
       overlap(ws, need, residual, eb) || overlap(ws, need, gamma, cb) ||
       overlap(ws, need, beta, cb) || overlap(ws, need, stats, (size_t)a.C * 8))
     return FP16_ERR_ALIASING;
+  if (mb && (overlap(mask, mb, dx, eb) || overlap(mask, mb, ws, need) ||
+             (dresidual && overlap(mask, mb, dresidual, eb)) || overlap(mask, mb, dgamma, cb) ||
+             overlap(mask, mb, dbeta, cb)))
+    return FP16_ERR_ALIASING;
   return hip_status(launch_bn_bwd(
       a, reinterpret_cast<const h16*>(x), reinterpret_cast<const h16*>(y),
       reinterpret_cast<const h16*>(dy), reinterpret_cast<const h16*>(gamma),
       reinterpret_cast<const h16*>(beta), reinterpret_cast<const h16*>(residual), stats,
       reinterpret_cast<h16*>(dx), reinterpret_cast<h16*>(dgamma), reinterpret_cast<h16*>(dbeta),
-      reinterpret_cast<h16*>(dresidual), ws, static_cast<hipStream_t>(stream)));
+      reinterpret_cast<h16*>(dresidual), ws, mb ? mask : nullptr,
+      static_cast<hipStream_t>(stream)));
+}
+
+fp16_status fp16_bn_relu_bwd(const fp16_bn_desc* desc, const fp16_t* x, const fp16_t* y,
+                             const fp16_t* dy, const fp16_t* gamma, const fp16_t* beta,
+                             const fp16_t* residual, const float* stats, fp16_t* dx,
+                             fp16_t* dgamma, fp16_t* dbeta, fp16_t* dresidual, void* ws,
+                             size_t ws_bytes, fp16_stream_t stream) {
+  return bn_bwd_impl(desc, x, y, dy, gamma, beta, residual, stats, nullptr, false, dx, dgamma,
+                     dbeta, dresidual, ws, ws_bytes, stream);
+}
+
+fp16_status fp16_bn_relu_bwd_m(const fp16_bn_desc* desc, const fp16_t* x, const uint8_t* mask,
+                               const fp16_t* dy, const fp16_t* gamma, const fp16_t* beta,
+                               const float* stats, fp16_t* dx, fp16_t* dgamma, fp16_t* dbeta,
+                               fp16_t* dresidual, void* ws, size_t ws_bytes,
+                               fp16_stream_t stream) {
+  return bn_bwd_impl(desc, x, nullptr, dy, gamma, beta, nullptr, stats, mask, true, dx, dgamma,
+                     dbeta, dresidual, ws, ws_bytes, stream);
 }
 
 // ---- SGD ------------------------------------------------------------------------
@@ -708,16 +774,18 @@ size_t fp16_conv_bn_workspace_bytes(const fp16_conv_desc* conv, const fp16_bn_de
   return conv_bn_band_off(d) + (rec > bnw ? rec : bnw);
 }
 
-fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc* bn,
-                                  const fp16_t* x, const fp16_t* w, const fp16_t* gamma,
-                                  const fp16_t* beta, const fp16_t* residual, fp16_t* y,
-                                  fp16_t* z, float* stats, void* ws, size_t ws_bytes,
-                                  fp16_stream_t stream) {
+static fp16_status conv_bn_impl(const fp16_conv_desc* conv, const fp16_bn_desc* bn,
+                                const fp16_t* x, const fp16_t* w, const fp16_t* gamma,
+                                const fp16_t* beta, const fp16_t* residual, fp16_t* y, fp16_t* z,
+                                float* stats, uint8_t* mask, bool want_mask, void* ws,
+                                size_t ws_bytes, fp16_stream_t stream) {
   ConvDims d;
   BnArgs b;
   fp16_status s = check_conv_bn(conv, bn, &d, &b);
   if (s != FP16_OK) return s;
   if (!x || !w || !gamma || !beta || !y || !z || !stats) return FP16_ERR_NULL;
+  size_t mb = 0;
+  if (want_mask && (s = check_mask(b, mask, &mb)) != FP16_OK) return s;
   if (b.swap && !residual) return FP16_ERR_NULL;
   if (!aligned16(x) || !aligned16(w) || !aligned16(y) || !aligned16(z) || !aligned16(stats) ||
       (residual && !aligned16(residual)))
@@ -737,6 +805,12 @@ fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc
   if (overlap(ws, need, x, xb) || overlap(ws, need, w, wb) || overlap(ws, need, gamma, cb) ||
       overlap(ws, need, beta, cb) || overlap(ws, need, residual, yb))
     return FP16_ERR_ALIASING;
+  if (mb && (overlap(mask, mb, x, xb) || overlap(mask, mb, w, wb) || overlap(mask, mb, y, yb) ||
+             overlap(mask, mb, z, yb) || overlap(mask, mb, residual, yb) ||
+             overlap(mask, mb, gamma, cb) || overlap(mask, mb, beta, cb) ||
+             overlap(mask, mb, stats, sb) || overlap(mask, mb, ws, need)))
+    return FP16_ERR_ALIASING;
+  uint8_t* mout = mb ? mask : nullptr;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const ConvWs L = conv_ws(d, FP16_PASS_FWD);
   const h16* xe = reinterpret_cast<const h16*>(x);
@@ -752,7 +826,7 @@ fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc
                                       reinterpret_cast<const h16*>(gamma),
                                       reinterpret_cast<const h16*>(beta),
                                       reinterpret_cast<const h16*>(residual),
-                                      reinterpret_cast<h16*>(z), stats, 0, part, st));
+                                      reinterpret_cast<h16*>(z), stats, 0, part, mout, st));
     }
   }
   if (d.Cp != d.C) {
@@ -777,7 +851,7 @@ fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc
     // (same results as the two calls)
     TRY(launch_igemm(a, st));
     return hip_status(launch_bn_fwd(b, reinterpret_cast<const h16*>(y), gp, bp, rp,
-                                    reinterpret_cast<h16*>(z), stats, 0, part, st));
+                                    reinterpret_cast<h16*>(z), stats, 0, part, mout, st));
   }
   a.stat = part;
   a.stat_nb = conv_bn_nb(d);
@@ -789,7 +863,25 @@ fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc
                                         reinterpret_cast<const h16*>(gamma),
                                         reinterpret_cast<const h16*>(beta),
                                         reinterpret_cast<const h16*>(residual),
-                                        reinterpret_cast<h16*>(z), stats, st));
+                                        reinterpret_cast<h16*>(z), stats, mout, st));
+}
+
+fp16_status fp16_conv_bn_relu_fwd(const fp16_conv_desc* conv, const fp16_bn_desc* bn,
+                                  const fp16_t* x, const fp16_t* w, const fp16_t* gamma,
+                                  const fp16_t* beta, const fp16_t* residual, fp16_t* y,
+                                  fp16_t* z, float* stats, void* ws, size_t ws_bytes,
+                                  fp16_stream_t stream) {
+  return conv_bn_impl(conv, bn, x, w, gamma, beta, residual, y, z, stats, nullptr, false, ws,
+                      ws_bytes, stream);
+}
+
+fp16_status fp16_conv_bn_relu_fwd_m(const fp16_conv_desc* conv, const fp16_bn_desc* bn,
+                                    const fp16_t* x, const fp16_t* w, const fp16_t* gamma,
+                                    const fp16_t* beta, const fp16_t* residual, fp16_t* y,
+                                    fp16_t* z, float* stats, uint8_t* mask, void* ws,
+                                    size_t ws_bytes, fp16_stream_t stream) {
+  return conv_bn_impl(conv, bn, x, w, gamma, beta, residual, y, z, stats, mask, true, ws,
+                      ws_bytes, stream);
 }
 
 }  // extern "C"

@@ -536,8 +536,10 @@ __global__ __launch_bounds__(64) void bn_band_combine(const float* __restrict__ 
 // the next one.
 //   kSwap: BN swap; kRelu: ReLU; kMaskY: the backward takes the ReLU mask from
 //   the stored output y; kLoadR: the shortcut r is read; kDres: the backward
-//   writes the shortcut gradient.
-constexpr int kSwap = 1, kRelu = 2, kMaskY = 4, kLoadR = 8, kDres = 16;
+//   writes the shortcut gradient; kMaskB: the backward takes the ReLU mask
+//   from the bits the forward kept; kKeepF: the forward apply keeps them (one
+//   byte per 16-byte vector of y, bit e = [y element e > 0]).
+constexpr int kSwap = 1, kRelu = 2, kMaskY = 4, kLoadR = 8, kDres = 16, kMaskB = 32, kKeepF = 64;
 
 // Each block takes runs of kApplyU * kT consecutive 16-byte vectors; a thread
 // loads its kApplyU vectors (and residual vectors) before it stores any, so
@@ -552,8 +554,10 @@ template <int MODE>
 __global__ __launch_bounds__(kT) void bn_fwd_apply_vec(const h16* x, const h16* __restrict__ gamma,
                                                        const h16* __restrict__ beta, const h16* res,
                                                        h16* y, const float* __restrict__ stats,
-                                                       Geo g, int CV, float s) {
-  constexpr bool SWAP = MODE & kSwap, RELU = MODE & kRelu, HAS_R = MODE & kLoadR;
+                                                       Geo g, int CV, float s,
+                                                       uint8_t* __restrict__ mout) {
+  constexpr bool SWAP = MODE & kSwap, RELU = MODE & kRelu, HAS_R = MODE & kLoadR,
+                 KEEP = MODE & kKeepF;
   const int t = threadIdx.x;
   const int j = t % CV;  // run starts and kT are multiples of CV
   FwdCoef k[8];
@@ -575,11 +579,17 @@ __global__ __launch_bounds__(kT) void bn_fwd_apply_vec(const h16* x, const h16* 
     for (int u = 0; u < kApplyU; ++u) {
       const int64_t v = run + t + u * kT;
       V8 out;
+      uint32_t bits = 0;
 #pragma unroll
-      for (int e = 0; e < 8; ++e)
+      for (int e = 0; e < 8; ++e) {
         out.h[e] = to_h16(fwd_value(to_f32(xv[u].h[e]), k[e], HAS_R,
                                     HAS_R ? to_f32(rv[u].h[e]) : 0.0f, RELU, SWAP));
-      if (v < nvec) store16(y + v * 8, out);
+        if (KEEP) bits |= (uint32_t)(to_f32(out.h[e]) > 0.0f) << e;
+      }
+      if (v < nvec) {
+        store16(y + v * 8, out);
+        if (KEEP) mout[v] = (uint8_t)bits;
+      }
     }
   }
 }
@@ -612,10 +622,11 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
                                                         int CV, int RB, int64_t rpb, float s,
                                                         float* ws, uint8_t* __restrict__ mbits) {
   constexpr bool SWAP = MODE & kSwap, RELU = MODE & kRelu, MASK_Y = MODE & kMaskY,
-                 LOAD_R = MODE & kLoadR;
+                 LOAD_R = MODE & kLoadR, MASK_B = MODE & kMaskB;
   // a mask recomputed from the shortcut is kept, one bit per element and one
   // byte per 16-byte vector (its index in x), so the apply reads that byte
-  // instead of the shortcut's 16 bytes
+  // instead of the shortcut's 16 bytes; with MASK_B the forward kept it and
+  // it is read here (mbits is then the caller's mask, only read)
   constexpr bool KEEP_M = LOAD_R && RELU && !MASK_Y;
   constexpr int NS = SWAP ? 3 : 2;
   __shared__ float red[8 * NS * kT];
@@ -637,6 +648,7 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
   // last is loaded clamped (in bounds) and adds exact zeros
   struct Row {
     V8 x, d, y, r;
+    uint32_t mb;
   };
   const int64_t rt = row0 + t / CV;
   const int64_t nsteps = (row1 - row0 + RB - 1) / RB;
@@ -648,6 +660,7 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
     b.d = load16(dy + off);
     if (MASK_Y) b.y = load16(y + off);
     if (LOAD_R) b.r = load16(res + off);
+    if (MASK_B) b.mb = mbits[row * CV + j];
   };
   auto sum_row = [&](const Row& b, int64_t i) {
     const bool ok = rt + i * RB < row1;
@@ -656,8 +669,9 @@ __global__ __launch_bounds__(kT) void bn_bwd_reduce_vec(const h16* __restrict__ 
     for (int e = 0; e < 8; ++e) {
       const float xf = to_f32(b.x.h[e]);
       const float rf = LOAD_R ? to_f32(b.r.h[e]) : 0.0f;
-      const bool m = relu_mask(RELU, MASK_Y, MASK_Y ? b.y.h[e] : (h16)0.0f, xf, k[e], LOAD_R, rf,
-                               SWAP);
+      const bool m = MASK_B ? ((b.mb >> e) & 1u) != 0
+                            : relu_mask(RELU, MASK_Y, MASK_Y ? b.y.h[e] : (h16)0.0f, xf, k[e],
+                                        LOAD_R, rf, SWAP);
       bits |= (uint32_t)m << e;
       const float gg = ok && m ? s * to_f32(b.d.h[e]) : 0.0f;
       const float xt = ok ? xf - k[e].mean : 0.0f;
@@ -776,9 +790,10 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_vec(const h16* x, const h16* 
                                                        h16* dres) {
   constexpr bool SWAP = MODE & kSwap, RELU = MODE & kRelu, MASK_Y = MODE & kMaskY,
                  DRES = MODE & kDres;
-  // the ReLU mask recomputed from x and the shortcut was kept by the reduce:
-  // one byte per vector instead of the shortcut's 16
-  constexpr bool NEED_R = (MODE & kLoadR) && RELU && !MASK_Y;
+  // the ReLU mask recomputed from x and the shortcut was kept by the reduce,
+  // or by the forward (kMaskB): one byte per vector instead of the
+  // shortcut's 16
+  constexpr bool NEED_R = ((MODE & kLoadR) && RELU && !MASK_Y) || (MODE & kMaskB);
   const int t = threadIdx.x;
   const int j = t % CV;  // run starts and kT are multiples of CV
   FwdCoef k[8];
@@ -865,10 +880,11 @@ unsigned apply_grid(int64_t nthreads_wanted, int CV) {
 }
 
 // Template variant of the vectorised kernels for these arguments.
-int fwd_mode(const BnArgs& a, const h16* res) {
-  return (a.swap ? kSwap : 0) | (a.relu ? kRelu : 0) | (res ? kLoadR : 0);
+int fwd_mode(const BnArgs& a, const h16* res, bool keep) {
+  return (a.swap ? kSwap : 0) | (a.relu ? kRelu : 0) | (res ? kLoadR : 0) | (keep ? kKeepF : 0);
 }
-int bwd_mode(const BnArgs& a, const h16* y, const h16* res, const h16* dres) {
+int bwd_mode(const BnArgs& a, const h16* y, const h16* res, const h16* dres, bool bits) {
+  if (bits) return kRelu | kMaskB | (dres ? kDres : 0);  // no swap: checked by the caller
   const bool relu = a.relu != 0, mask_y = relu && y != nullptr;
   const bool load_r = a.swap || (relu && !mask_y && res != nullptr);
   return (a.swap ? kSwap : 0) | (relu ? kRelu : 0) | (mask_y ? kMaskY : 0) |
@@ -876,20 +892,20 @@ int bwd_mode(const BnArgs& a, const h16* y, const h16* res, const h16* dres) {
 }
 
 // The valid variants (the BN swap always reads the shortcut).
-#define FP16K_BN_FWD_MODES(X) X(0) X(2) X(8) X(10) X(9) X(11)
-#define FP16K_BN_BWD_MODES(X) X(0) X(6) X(2) X(10) X(9) X(15) X(11)
+#define FP16K_BN_FWD_MODES(X) X(0) X(2) X(8) X(10) X(9) X(11) X(66) X(74)
+#define FP16K_BN_BWD_MODES(X) X(0) X(6) X(2) X(10) X(9) X(15) X(11) X(34)
 #define FP16K_BN_BWD_APPLY_MODES(X) \
-  FP16K_BN_BWD_MODES(X) X(16) X(22) X(18) X(26) X(25) X(31) X(27)
+  FP16K_BN_BWD_MODES(X) X(16) X(22) X(18) X(26) X(25) X(31) X(27) X(50)
 
 hipError_t launch_fwd_apply_vec(int mode, const Plan& p, const Geo& g, const h16* x,
                                 const h16* gamma, const h16* beta, const h16* res, h16* y,
-                                const float* stats, float s, hipStream_t st) {
+                                const float* stats, float s, uint8_t* mout, hipStream_t st) {
   const dim3 grid(apply_grid(g.M * p.CV / kApplyU, p.CV));
   switch (mode) {
 #define FP16K_CASE(m)                                                                          \
   case m:                                                                                      \
     hipLaunchKernelGGL(bn_fwd_apply_vec<m>, grid, dim3(kT), 0, st, x, gamma, beta, res, y,     \
-                       stats, g, p.CV, s);                                                      \
+                       stats, g, p.CV, s, mout);                                                \
     break;
     FP16K_BN_FWD_MODES(FP16K_CASE)
 #undef FP16K_CASE
@@ -932,9 +948,16 @@ size_t bn_ws_bytes(const BnArgs& a) {
   return partial_bytes(p, a.C) + coef_bytes(a.C) + mask_bytes(p, a);
 }
 
+// Bytes of a kept ReLU mask (one byte per 8 channels of each pixel), or 0
+// where the vectorised kernels do not run or there is no ReLU.
+size_t bn_keep_mask_bytes(const BnArgs& a) {
+  const Plan p = make_plan(a);
+  return p.vec && a.relu ? (size_t)((int64_t)a.N * a.H * a.W * p.CV) : 0;
+}
+
 hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const h16* beta,
                          const h16* res, h16* y, float* stats, int use_stats, void* ws,
-                         hipStream_t st) {
+                         uint8_t* mout, hipStream_t st) {
   const Plan p = make_plan(a);
   const Geo g = make_geo(a);
   float* part = reinterpret_cast<float*>(ws);
@@ -953,7 +976,8 @@ hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const 
   }
   if (p.vec) {
     const hipError_t e =
-        launch_fwd_apply_vec(fwd_mode(a, res), p, g, x, gamma, beta, res, y, stats, a.post_scale, st);
+        launch_fwd_apply_vec(fwd_mode(a, res, mout != nullptr), p, g, x, gamma, beta, res, y, stats,
+                             a.post_scale, mout, st);
     if (e != hipSuccess) return e;
   } else {
     hipLaunchKernelGGL(bn_fwd_apply_gen, dim3(apply_grid(g.M * a.C / 4, 1)), dim3(kT), 0, st, x,
@@ -969,7 +993,7 @@ size_t bn_band_ws_bytes(int C, int nb) {
 
 hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, void* band_ws,
                                const h16* x, const h16* gamma, const h16* beta, const h16* res,
-                               h16* y, float* stats, hipStream_t st) {
+                               h16* y, float* stats, uint8_t* mout, hipStream_t st) {
   const Plan p = make_plan(a);
   const Geo g = make_geo(a);
   if (nb <= kBandOne) {
@@ -984,7 +1008,8 @@ hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, void*
   }
   if (p.vec) {
     const hipError_t e =
-        launch_fwd_apply_vec(fwd_mode(a, res), p, g, x, gamma, beta, res, y, stats, a.post_scale, st);
+        launch_fwd_apply_vec(fwd_mode(a, res, mout != nullptr), p, g, x, gamma, beta, res, y, stats,
+                             a.post_scale, mout, st);
     if (e != hipSuccess) return e;
   } else {
     hipLaunchKernelGGL(bn_fwd_apply_gen, dim3(apply_grid(g.M * a.C / 4, 1)), dim3(kT), 0, st, x,
@@ -995,13 +1020,18 @@ hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, void*
 
 hipError_t launch_bn_bwd(const BnArgs& a, const h16* x, const h16* y, const h16* dy,
                          const h16* gamma, const h16* beta, const h16* res, const float* stats,
-                         h16* dx, h16* dgamma, h16* dbeta, h16* dres, void* ws, hipStream_t st) {
+                         h16* dx, h16* dgamma, h16* dbeta, h16* dres, void* ws,
+                         const uint8_t* mask, hipStream_t st) {
   const Plan p = make_plan(a);
   const Geo g = make_geo(a);
   float* part = reinterpret_cast<float*>(ws);
   float* coef = reinterpret_cast<float*>(reinterpret_cast<char*>(ws) + partial_bytes(p, a.C));
-  uint8_t* mbits = reinterpret_cast<uint8_t*>(ws) + partial_bytes(p, a.C) + coef_bytes(a.C);
-  const int mode = bwd_mode(a, y, res, dres);
+  // the forward's kept mask (only read), else the workspace's, which the
+  // reduce fills when it recomputes the mask from the shortcut
+  uint8_t* mbits = mask ? const_cast<uint8_t*>(mask)
+                        : reinterpret_cast<uint8_t*>(ws) + partial_bytes(p, a.C) + coef_bytes(a.C);
+  if (mask && (!p.vec || a.swap || !a.relu)) return hipErrorInvalidValue;
+  const int mode = bwd_mode(a, y, res, dres, mask != nullptr);
   if (p.vec) {
     switch (mode & ~kDres) {
 #define FP16K_CASE(m)                                                                          \

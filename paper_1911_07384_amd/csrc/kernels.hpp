@@ -144,19 +144,25 @@ struct BnArgs {
   int swap;  // BN swap: the shortcut joins before gamma
 };
 size_t bn_ws_bytes(const BnArgs& a);
+// mout (nullable): keep the ReLU mask of y, one byte per 16-byte vector of y
+// (bit e = [element e > 0]); needs the vectorised path and ReLU (the caller
+// checks bn_keep_mask_bytes > 0).
 hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const h16* beta,
                          const h16* res, h16* y, float* stats, int use_stats, void* ws,
-                         hipStream_t st);
+                         uint8_t* mout, hipStream_t st);
+size_t bn_keep_mask_bytes(const BnArgs& a);
 // Forward from the band records of a convolution epilogue (IgemmArgs::stat):
 // statistics, then the apply.  part: [nb][3][C] float32, 128 rows per record;
 // band_ws: bn_band_ws_bytes(C, nb) bytes of scratch for the per-slice sums.
 size_t bn_band_ws_bytes(int C, int nb);
 hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, void* band_ws,
                                const h16* x, const h16* gamma, const h16* beta, const h16* res,
-                               h16* y, float* stats, hipStream_t st);
+                               h16* y, float* stats, uint8_t* mout, hipStream_t st);
+// mask (nullable): the ReLU mask the forward kept (no BN swap)
 hipError_t launch_bn_bwd(const BnArgs& a, const h16* x, const h16* y, const h16* dy,
                          const h16* gamma, const h16* beta, const h16* res, const float* stats,
-                         h16* dx, h16* dgamma, h16* dbeta, h16* dres, void* ws, hipStream_t st);
+                         h16* dx, h16* dgamma, h16* dbeta, h16* dres, void* ws,
+                         const uint8_t* mask, hipStream_t st);
 
 // ---- pooling (pool.hip) ----------------------------------------------------
 struct PoolArgs {

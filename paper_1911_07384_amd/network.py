@@ -111,8 +111,15 @@ class ResNet50:
         y = self._buf(name + ".y", x.shape)
         self._buf(name + ".stats", (2 * c,), torch.float32)
         self._bnspecs.append((name, c))
-        self.fwd.append(Op("bn_fwd", name, {"desc": d, "x": xname, "res": res, "y": name + ".y",
-                                            "stats": name + ".stats"}))
+        a = {"desc": d, "x": xname, "res": res, "y": name + ".y", "stats": name + ".stats",
+             "mask": None}
+        # a BN whose ReLU follows the shortcut keeps its ReLU mask for the
+        # backward (one bit per element instead of reading the shortcut again)
+        mb = F.fp16_bn_mask_bytes(d) if (res is not None and relu and not swap) else 0
+        if mb:
+            self._buf(name + ".mask", (mb,), torch.uint8)
+            a["mask"] = name + ".mask"
+        self.fwd.append(Op("bn_fwd", name, a))
         return y
 
     def _plan(self, stages):
@@ -183,7 +190,7 @@ class ResNet50:
                               {"desc": op.a["desc"], "bn": nxt.a["desc"], "x": op.a["x"],
                                "w": op.a["w"], "y": op.a["y"], "z": nxt.a["y"],
                                "res": nxt.a["res"], "stats": nxt.a["stats"],
-                               "conv": op.name}))
+                               "mask": nxt.a["mask"], "conv": op.name}))
                 i += 2
             else:
                 out.append(op)
@@ -209,7 +216,7 @@ class ResNet50:
         dx = self._grad(f["x"])
         a = {"desc": f["desc"], "x": f["x"], "y": None, "dy": dy, "res": f["res"],
              "stats": f["stats"], "dx": dx, "dgamma": name + ".dgamma", "dbeta": name + ".dbeta",
-             "dres": None}
+             "dres": None, "mask": f["mask"]}
         if want_dres:
             a["dres"] = self._grad(f["res"]) if f["res"] is not None else None
         self.bwd.append(Op("bn_bwd", name, a))
@@ -344,18 +351,32 @@ class ResNet50:
             F.fp16_conv_wgrad(a["desc"], t(a["x"]), t(a["dy"]), t(a["dw"]), ws)
         elif k == "conv_bn_fwd":
             nm = op.name
-            F.fp16_conv_bn_relu_fwd(a["desc"], a["bn"], t(a["x"]), t(a["w"]), t(nm + ".gamma"),
-                                    t(nm + ".beta"), t(a["res"]), t(a["y"]), t(a["z"]),
-                                    t(a["stats"]), ws)
+            if a["mask"] is None:
+                F.fp16_conv_bn_relu_fwd(a["desc"], a["bn"], t(a["x"]), t(a["w"]),
+                                        t(nm + ".gamma"), t(nm + ".beta"), t(a["res"]), t(a["y"]),
+                                        t(a["z"]), t(a["stats"]), ws)
+            else:
+                F.fp16_conv_bn_relu_fwd_m(a["desc"], a["bn"], t(a["x"]), t(a["w"]),
+                                          t(nm + ".gamma"), t(nm + ".beta"), t(a["res"]),
+                                          t(a["y"]), t(a["z"]), t(a["stats"]), t(a["mask"]), ws)
         elif k == "bn_fwd":
             nm = op.name
-            F.fp16_bn_relu(a["desc"], t(a["x"]), t(nm + ".gamma"), t(nm + ".beta"), t(a["res"]),
-                           t(a["y"]), t(a["stats"]), ws)
+            if a["mask"] is None:
+                F.fp16_bn_relu(a["desc"], t(a["x"]), t(nm + ".gamma"), t(nm + ".beta"),
+                               t(a["res"]), t(a["y"]), t(a["stats"]), ws)
+            else:
+                F.fp16_bn_relu_m(a["desc"], t(a["x"]), t(nm + ".gamma"), t(nm + ".beta"),
+                                 t(a["res"]), t(a["y"]), t(a["stats"]), t(a["mask"]), ws)
         elif k == "bn_bwd":
             nm = op.name
-            F.fp16_bn_relu_bwd(a["desc"], t(a["x"]), t(a["y"]), t(a["dy"]), t(nm + ".gamma"),
-                               t(nm + ".beta"), t(a["res"]), t(a["stats"]), t(a["dx"]),
-                               t(a["dgamma"]), t(a["dbeta"]), t(a["dres"]), ws)
+            if a["mask"] is None:
+                F.fp16_bn_relu_bwd(a["desc"], t(a["x"]), t(a["y"]), t(a["dy"]), t(nm + ".gamma"),
+                                   t(nm + ".beta"), t(a["res"]), t(a["stats"]), t(a["dx"]),
+                                   t(a["dgamma"]), t(a["dbeta"]), t(a["dres"]), ws)
+            else:
+                F.fp16_bn_relu_bwd_m(a["desc"], t(a["x"]), t(a["mask"]), t(a["dy"]),
+                                     t(nm + ".gamma"), t(nm + ".beta"), t(a["stats"]), t(a["dx"]),
+                                     t(a["dgamma"]), t(a["dbeta"]), t(a["dres"]), ws)
         elif k == "maxpool_fwd":
             F.fp16_maxpool_fwd(a["desc"], t(a["x"]), t(a["y"]), t(a["idx"]))
         elif k == "maxpool_bwd":
@@ -376,9 +397,9 @@ class ResNet50:
     def program(self):
         return self.prep + self.fwd + self.bwd + self.upd
 
-    _OUTPUTS = {"conv_fwd": ("y",), "conv_bn_fwd": ("y", "z", "stats"), "conv_dgrad": ("dx",),
-                "conv_dgrad_add": ("dx",),
-                "conv_wgrad": ("dw",), "bn_fwd": ("y", "stats"),
+    _OUTPUTS = {"conv_fwd": ("y",), "conv_bn_fwd": ("y", "z", "stats", "mask"),
+                "conv_dgrad": ("dx",), "conv_dgrad_add": ("dx",),
+                "conv_wgrad": ("dw",), "bn_fwd": ("y", "stats", "mask"),
                 "bn_bwd": ("dx", "dgamma", "dbeta", "dres"), "maxpool_fwd": ("y", "idx"),
                 "maxpool_bwd": ("dx",), "avgpool_fwd": ("y",), "avgpool_bwd": ("dx",),
                 "softmax_ce": ("loss", "dz", "dbias"), "dgrad_filter": ("wf",)}

@@ -362,3 +362,44 @@ def test_conv_bn_validation():
     ov = list(args)
     ov[6] = D + 64  # z overlaps y without being y
     assert l.fp16_conv_bn_relu_fwd(ctypes.byref(cd), ctypes.byref(bd), *ov) == ALIASING
+
+
+def test_kept_mask_validation():
+    lib = F.lib()
+    d = F.bn_desc(2, 64, 8, 8)
+    assert F.fp16_bn_mask_bytes(d) == 2 * 8 * 8 * 64 // 8
+    # not offered: NCHW, C/8 not a power of two, no ReLU, the BN swap
+    for bad in (F.bn_desc(2, 64, 8, 8, "NCHW"), F.bn_desc(2, 20, 8, 8), F.bn_desc(2, 24, 8, 8),
+                F.bn_desc(2, 64, 8, 8, relu=False), F.bn_desc(2, 64, 8, 8, swap=True)):
+        assert F.fp16_bn_mask_bytes(bad) == 0
+    need = F.fp16_bn_workspace_bytes(d)
+    M = Cc + (8 << 20)
+    fw = [A, B, B + 256, Cc + (2 << 20), Cc, WS + (1 << 20), M, WS, need, None]
+    assert lib.fp16_bn_relu_m(ctypes.byref(d), *fw[:6], None, *fw[7:]) == NULL
+    assert lib.fp16_bn_relu_m(ctypes.byref(d), *fw[:6], M + 8, *fw[7:]) == MISALIGNED
+    nc = F.bn_desc(2, 64, 8, 8, "NCHW")
+    assert lib.fp16_bn_relu_m(ctypes.byref(nc), *fw) == UNSUPPORTED
+    sw = F.bn_desc(2, 64, 8, 8, swap=True)
+    assert lib.fp16_bn_relu_m(ctypes.byref(sw), *fw) == UNSUPPORTED
+    for at in (A, Cc, Cc + (2 << 20), WS + (1 << 20), WS):  # x, y, residual, stats, workspace
+        assert lib.fp16_bn_relu_m(ctypes.byref(d), *fw[:6], at, *fw[7:]) == ALIASING, hex(at)
+    # backward: x, mask, dy, gamma, beta, stats, dx, dgamma, dbeta, dresidual, ws
+    bw = [A, M, Cc, B, B + 256, WS + (1 << 20), Cc + (1 << 20), B + 512, B + 768, Cc + (3 << 20),
+          WS, need, None]
+    assert lib.fp16_bn_relu_bwd_m(ctypes.byref(d), bw[0], None, *bw[2:]) == NULL
+    assert lib.fp16_bn_relu_bwd_m(ctypes.byref(nc), *bw) == UNSUPPORTED
+    for i in (6, 9, 10):  # the mask under dx, dresidual or the workspace
+        bad = list(bw)
+        bad[i] = M
+        assert lib.fp16_bn_relu_bwd_m(ctypes.byref(d), *bad) == ALIASING, i
+    # the fused convolution + BN forward
+    cd = _conv()
+    bd = F.bn_desc(cd.n, cd.k, cd.h, cd.w)
+    need = F.fp16_conv_bn_workspace_bytes(cd, bd)
+    args = [A, B, B + (1 << 20), B + (1 << 20) + 256, None, Cc, Cc + (4 << 20), WS + (8 << 20)]
+    assert lib.fp16_conv_bn_relu_fwd_m(ctypes.byref(cd), ctypes.byref(bd), *args, None, WS, need,
+                                       None) == NULL
+    assert lib.fp16_conv_bn_relu_fwd_m(ctypes.byref(cd), ctypes.byref(bd), *args, Cc + 64, WS,
+                                       need, None) == ALIASING  # mask inside y
+    assert lib.fp16_conv_bn_relu_fwd_m(ctypes.byref(cd), ctypes.byref(bd), *args, Cc + (4 << 20),
+                                       WS, need, None) == ALIASING  # mask inside z

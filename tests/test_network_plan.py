@@ -38,9 +38,9 @@ def test_conv_flops_at_batch_128(net):
     assert net.step_flops() == 3 * net.conv_flops() - 2 * 112 * 112 * 64 * 3 * 49
 
 
-OUTPUTS = {"conv_fwd": ["y"], "conv_bn_fwd": ["y", "z", "stats"], "conv_dgrad": ["dx"],
+OUTPUTS = {"conv_fwd": ["y"], "conv_bn_fwd": ["y", "z", "stats", "mask"], "conv_dgrad": ["dx"],
            "conv_dgrad_add": ["dx"],
-           "conv_wgrad": ["dw"], "bn_fwd": ["y", "stats"],
+           "conv_wgrad": ["dw"], "bn_fwd": ["y", "stats", "mask"],
            "bn_bwd": ["dx", "dgamma", "dbeta", "dres"], "maxpool_fwd": ["y", "idx"],
            "maxpool_bwd": ["dx"], "avgpool_fwd": ["y"], "avgpool_bwd": ["dx"],
            "softmax_ce": ["loss", "dz", "dbias"], "dgrad_filter": ["wf"]}
@@ -78,6 +78,20 @@ def test_dataflow(net):
     for op in net.bwd:
         if op.kind in ("conv_dgrad", "conv_dgrad_add"):
             assert prep[op.a["wf"]] == op.a["w"] == op.name
+
+
+def test_block_last_bns_keep_their_relu_mask(net):
+    # the 16 BNs whose ReLU follows the shortcut write the mask in the forward
+    # and their backward reads it instead of the shortcut
+    fwd = {o.name: o for o in net.fwd if o.kind in ("bn_fwd", "conv_bn_fwd")}
+    kept = {n for n, o in fwd.items() if o.a["mask"] is not None}
+    assert kept == {n for n, o in fwd.items() if o.a["res"] is not None}
+    assert len(kept) == 16 and all(n.endswith(".bn3") for n in kept)
+    for o in net.bwd:
+        if o.kind == "bn_bwd":
+            assert o.a["mask"] == fwd[o.name].a["mask"]
+    swapped = ResNet50(n=1, image=64, device="cpu", bn_swap=True)
+    assert all(o.a["mask"] is None for o in swapped.fwd if o.kind in ("bn_fwd", "conv_bn_fwd"))
 
 
 def test_bn_swap_and_zero_gamma_options():
