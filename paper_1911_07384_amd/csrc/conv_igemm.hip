@@ -51,6 +51,7 @@
 
 #include "kernels.hpp"
 
+
 namespace fp16k {
 namespace {
 
@@ -61,6 +62,33 @@ __device__ __forceinline__ uint32_t pin_v(uint32_t x) {
 }
 // workgroup barrier without the implied memory fence; callers wait first
 __device__ __forceinline__ void bare_barrier() { __asm__ volatile("s_barrier" ::: "memory"); }
+// Tile of this workgroup, for grids of (M-tiles, N-tiles, phases).
+// Workgroups are dealt to the 8 XCDs round-robin in launch order (M fastest).
+// With gn > 0 each XCD takes a contiguous run of tiles instead, in an order
+// that walks groups of gn N-tiles (N fastest, then M), so that its run is a
+// compact block of M-tiles x N-tiles whose activation rows are read once into
+// that XCD's L2 and shared by its N-tiles.
+__device__ __forceinline__ void xcd_tile(int gn, int& z, int& mt, int& nt) {
+  if (gn <= 0) {
+    z = blockIdx.z;
+    mt = blockIdx.x;
+    nt = blockIdx.y;
+    return;
+  }
+  const int MT = gridDim.x, NT = gridDim.y, NZ = gridDim.z;
+  const int total = MT * NT * NZ;
+  const int L = (blockIdx.z * NT + blockIdx.y) * MT + blockIdx.x;
+  const int q = total >> 3, r = total & 7, xcd = L & 7;
+  const int t = xcd * q + (xcd < r ? xcd : r) + (L >> 3);
+  const int u = t / NZ;
+  z = t - u * NZ;
+  const int g = u / (gn * MT);
+  const int w = u - g * gn * MT;
+  const int gw = NT - g * gn < gn ? NT - g * gn : gn;
+  nt = g * gn + w % gw;
+  mt = w / gw;
+}
+
 template <int BM, int BN, int WM, int WN, int BK>
 struct Cfg {
   static constexpr int LDK = BK + 8;
@@ -89,12 +117,14 @@ __global__ __launch_bounds__(256) void igemm_kernel(const IgemmArgs a) {
   h16* As = reinterpret_cast<h16*>(smem);
   h16* Bs = As + 2 * BM * LDK;
 
-  const IgemmPhase ph = a.ph[blockIdx.z];
+  int tz, tm_, tn_;
+  xcd_tile(a.gn, tz, tm_, tn_);
+  const IgemmPhase ph = a.ph[tz];
   const int HoWo = ph.Ho * ph.Wo;
   const int M = a.N * HoWo;
-  const int m0 = blockIdx.x * BM;
+  const int m0 = tm_ * BM;
   if (m0 >= M) return;
-  const int n0 = blockIdx.y * BN;
+  const int n0 = tn_ * BN;
   const int Ci = a.Ci;
   const int Kg = ph.Rt * ph.St * Ci;
   const int tid = threadIdx.x;
@@ -293,12 +323,14 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
   __shared__ __attribute__((aligned(1024))) char lds2[K::BUF];
   __shared__ __attribute__((aligned(1024))) char lds3[K::BUF];
 
-  const IgemmPhase ph = a.ph[blockIdx.z];
+  int tz, tm_, tn_;
+  xcd_tile(a.gn, tz, tm_, tn_);
+  const IgemmPhase ph = a.ph[tz];
   const int HoWo = ph.Ho * ph.Wo;
   const int M = a.N * HoWo;
-  const int m0 = blockIdx.x * BM;
+  const int m0 = tm_ * BM;
   if (m0 >= M) return;
-  const int n0 = blockIdx.y * BN;
+  const int n0 = tn_ * BN;
   const int Ci = a.Ci;
   const int Kg = ph.Rt * ph.St * Ci;
   const int tid = threadIdx.x;
@@ -1005,12 +1037,14 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
   static_assert(K::Q * (S - 1) < 64, "vmcnt range");
   __shared__ __attribute__((aligned(1024))) char lds[K::LDS];
 
-  const IgemmPhase ph = a.ph[blockIdx.z];
+  int tz, tm_, tn_;
+  xcd_tile(a.gn, tz, tm_, tn_);
+  const IgemmPhase ph = a.ph[tz];
   const int HoWo = ph.Ho * ph.Wo;
   const int M = a.N * HoWo;
-  const int m0 = blockIdx.x * BM;
+  const int m0 = tm_ * BM;
   if (m0 >= M) return;
-  const int n0 = blockIdx.y * BN;
+  const int n0 = tn_ * BN;
   const int Ci = a.Ci;
   const int Kg = ph.Rt * ph.St * Ci;
   const int tid = threadIdx.x;
@@ -1338,16 +1372,30 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
   }
 }
 
+// The XCD tile order (xcd_tile) of a launch: measured on the ResNet-50
+// convolutions at batch 128, it pays for the 1x1 filters with several N-tiles
+// in one phase (1.01-1.13x: the N-tiles of an XCD share its activation rows
+// in L2; all N-tiles per group did best), and costs elsewhere -- up to 0.92x on
+// single-N-tile streams (eight distant address ranges instead of one front)
+// and 0.5-0.85x on the strided data gradients -- so those keep the launch
+// order.
+int xcd_group(const IgemmArgs& a, int NT) {
+  if (NT < 2 || a.nphase != 1 || a.ph[0].Rt * a.ph[0].St != 1) return 0;
+  return NT;
+}
+
 template <int TM, int TN, int WM, int WN, int S>
-hipError_t launch_cfg7(const IgemmArgs& a, hipStream_t st) {
+hipError_t launch_cfg7(const IgemmArgs& a0, hipStream_t st) {
   using K = Cfg7<TM, TN, WM, WN, S>;
   int maxM = 0;
-  for (int p = 0; p < a.nphase; ++p) {
-    const int m = a.N * a.ph[p].Ho * a.ph[p].Wo;
+  for (int p = 0; p < a0.nphase; ++p) {
+    const int m = a0.N * a0.ph[p].Ho * a0.ph[p].Wo;
     if (m > maxM) maxM = m;
   }
-  if (maxM == 0 || a.nphase == 0) return hipSuccess;
-  dim3 grid(ceil_div(maxM, K::BM), ceil_div(a.Co, K::BN), a.nphase);
+  if (maxM == 0 || a0.nphase == 0) return hipSuccess;
+  dim3 grid(ceil_div(maxM, K::BM), ceil_div(a0.Co, K::BN), a0.nphase);
+  IgemmArgs a = a0;
+  a.gn = xcd_group(a, grid.y);
   if (a.stat)
     hipLaunchKernelGGL((igemm7_kernel<TM, TN, WM, WN, S, true>), grid, dim3(256), 0, st, a);
   else
@@ -1356,15 +1404,17 @@ hipError_t launch_cfg7(const IgemmArgs& a, hipStream_t st) {
 }
 
 template <int TM, int TN>
-hipError_t launch_cfg4(const IgemmArgs& a, hipStream_t st) {
+hipError_t launch_cfg4(const IgemmArgs& a0, hipStream_t st) {
   using K = Cfg4<TM, TN>;
   int maxM = 0;
-  for (int p = 0; p < a.nphase; ++p) {
-    const int m = a.N * a.ph[p].Ho * a.ph[p].Wo;
+  for (int p = 0; p < a0.nphase; ++p) {
+    const int m = a0.N * a0.ph[p].Ho * a0.ph[p].Wo;
     if (m > maxM) maxM = m;
   }
-  if (maxM == 0 || a.nphase == 0) return hipSuccess;
-  dim3 grid(ceil_div(maxM, K::BM), ceil_div(a.Co, K::BN), a.nphase);
+  if (maxM == 0 || a0.nphase == 0) return hipSuccess;
+  dim3 grid(ceil_div(maxM, K::BM), ceil_div(a0.Co, K::BN), a0.nphase);
+  IgemmArgs a = a0;
+  a.gn = xcd_group(a, grid.y);
   hipLaunchKernelGGL((igemm4_kernel<TM, TN>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }
@@ -1394,14 +1444,16 @@ hipError_t launch_pw(const IgemmArgs& a, hipStream_t st) {
 }
 
 template <int BM, int BN, int WM, int WN, int BK>
-hipError_t launch_cfg(const IgemmArgs& a, hipStream_t st) {
+hipError_t launch_cfg(const IgemmArgs& a0, hipStream_t st) {
   int maxM = 0;
-  for (int p = 0; p < a.nphase; ++p) {
-    const int m = a.N * a.ph[p].Ho * a.ph[p].Wo;
+  for (int p = 0; p < a0.nphase; ++p) {
+    const int m = a0.N * a0.ph[p].Ho * a0.ph[p].Wo;
     if (m > maxM) maxM = m;
   }
-  if (maxM == 0 || a.nphase == 0) return hipSuccess;
-  dim3 grid(ceil_div(maxM, BM), ceil_div(a.Co, BN), a.nphase);
+  if (maxM == 0 || a0.nphase == 0) return hipSuccess;
+  dim3 grid(ceil_div(maxM, BM), ceil_div(a0.Co, BN), a0.nphase);
+  IgemmArgs a = a0;
+  a.gn = xcd_group(a, grid.y);
   hipLaunchKernelGGL((igemm_kernel<BM, BN, WM, WN, BK>), grid, dim3(256), 0, st, a);
   return hipGetLastError();
 }

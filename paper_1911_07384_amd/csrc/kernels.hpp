@@ -58,6 +58,9 @@ struct IgemmArgs {
   // over its rows, at stat[(b * 3 + q) * Co + c], q = 0, 1, 2.
   float* stat;
   int stat_nb;
+  // N-tiles per group of the XCD-contiguous workgroup-to-tile order, or 0
+  // for the launch order (set by the launcher)
+  int gn;
 };
 
 hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st);
