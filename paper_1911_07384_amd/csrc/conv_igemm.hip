@@ -601,9 +601,7 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
 
 // ---- pointwise (1x1) convolutions bound by the output's bytes ------------------
 // For a 1x1 filter over CI = 64 or 128 input channels with 128+ output
-// channels, writing y costs 2-4x more bytes than reading x, and staging the
-// accumulators through LDS for the stores (as the kernels above do) held these
-// layers at 2-2.5 TB/s.  Here:
+// channels, writing y costs 2-4x more bytes than reading x.  Here:
 //  - the BN x CI filter tile is loaded into LDS once (16-byte chunks XOR-
 //    swizzled by row, so fragment reads are conflict free) and each workgroup
 //    walks over 128-row tiles of the output, grid-stride; every lane loads its
@@ -613,20 +611,31 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
 //    8*(e/4) + 4*(lane/32) + e%4 of each 32-channel tile.  Swapping the upper
 //    lane half of channel group 2g with the lower lane half of group 2g+1
 //    (v_permlane32_swap, four register pairs per group pair) leaves each lane
-//    with 8 consecutive channels twice, which go out as 16-byte stores;
+//    with 8 consecutive channels twice;
+//  - those rounded 16-byte chunks go through a small per-wave LDS buffer
+//    (SW 32-channel tiles at a time, chunks XOR-swizzled by pixel) and come
+//    back so that 4*SW consecutive lanes hold one pixel's 64*SW consecutive
+//    bytes: each store instruction then writes whole 128-byte (SW = 2) or
+//    64-byte lines.  Written straight from the swapped layout, every store
+//    instruction split into 32 separate 32-byte writes, and the store path
+//    (not HBM) bounded these layers;
 //  - with BN statistics the plain product D = X x W is computed too (the
 //    MFMAs are cheap here), whose layout gives each lane one channel and 16
-//    rows: the band sums are taken in the lane, and the four waves' bands of a
-//    tile are combined into one 128-row record as in igemm4_kernel.
+//    rows: the band sums are taken in the lane and kept in registers, and the
+//    four waves' bands of a tile are combined into one 128-row record as in
+//    igemm4_kernel, through the same LDS space.
 // Each output element is the same k-ordered sum of exact products in both
 // MFMA forms, so the values equal the other kernels' bit for bit.
 template <int CI, int BN, bool STATS>
 struct CfgPw {
   static constexpr int KS = CI / 16;          // k sub-steps of 16 channels
   static constexpr int TN = BN / 32;          // 32-channel tiles
+  static constexpr int SW = CI == 64 ? 2 : 1; // 32-channel tiles per store group
   static constexpr int BBYTES = BN * CI * 2;  // resident filter tile
+  static constexpr int STG = 4 * 32 * SW * 64;            // [wave][pixel][SW*64 bytes]
   static constexpr int BST = STATS ? 4 * 3 * BN * 4 : 0;  // [wave][K, s1, s2][BN]
-  static constexpr int LDS = BBYTES + BST + 16;
+  static constexpr int SHARED = STG > BST ? STG : BST;
+  static constexpr int LDS = BBYTES + SHARED + 16;
 };
 
 __device__ __forceinline__ void lane_half_swap(float& x, float& y) {
@@ -636,16 +645,28 @@ __device__ __forceinline__ void lane_half_swap(float& x, float& y) {
   y = __builtin_bit_cast(float, (unsigned)r[1]);
 }
 
+// LDS written by this wave's lanes visible to all of them (LDS operations of
+// one wave complete in order; this keeps the compiler from moving them)
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 template <int CI, int BN, bool STATS, bool ADD>
 __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) {
   using K = CfgPw<CI, BN, STATS>;
-  constexpr int KS = K::KS, TN = K::TN;
+  constexpr int KS = K::KS, TN = K::TN, SW = K::SW;
+  constexpr int SLOTS = 4 * SW;       // 16-byte chunks per staged pixel row
+  constexpr int PPI = 64 / SLOTS;     // pixels per store instruction
   static_assert(CI == 64 || CI == 128, "input channels");
   static_assert(!(STATS && ADD), "statistics are taken without an addend");
+  static_assert(TN % SW == 0, "store groups");
   __shared__ __attribute__((aligned(1024))) char lds[K::LDS];
   char* bt = lds;
-  float* bst = reinterpret_cast<float*>(lds + K::BBYTES);
-  int* bcnt = reinterpret_cast<int*>(lds + K::BBYTES + K::BST);
+  char* shared = lds + K::BBYTES;
+  float* bst = reinterpret_cast<float*>(shared);
+  int* bcnt = reinterpret_cast<int*>(lds + K::BBYTES + K::SHARED);
 
   const IgemmPhase ph = a.ph[0];
   const int HoWo = ph.Ho * ph.Wo;
@@ -654,6 +675,7 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int lrow = lane & 31, lhi = lane >> 5;
+  char* stg = shared + wave * 32 * SLOTS * 16;
   constexpr uint32_t OOB = 0x80000000u;
   const int act_bytes = (int)((int64_t)a.N * a.Hi * a.Wi * CI * 2);
   const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
@@ -711,35 +733,37 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
         }
     }
     load_a(Anext, row_off(tile + gridDim.x));
+    float bk[STATS ? TN : 1], b1[STATS ? TN : 1], b2[STATS ? TN : 1];
 #pragma unroll
-    for (int tn = 0; tn < TN; ++tn) {
-      floatx16 at, an;
+    for (int g = 0; g < TN / SW; ++g) {
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        at[e] = 0.0f;
-        an[e] = 0.0f;
-      }
+      for (int tl = 0; tl < SW; ++tl) {
+        const int tn = g * SW + tl;
+        floatx16 at, an;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks) {
-        const int pos = ((ks * 2 + lhi) ^ swz) * 16;
-        const half8 bf = *reinterpret_cast<const half8*>(bt + (tn * 32 + lrow) * (CI * 2) + pos);
-        at = mfma32x32x16(bf, Acur[ks], at);
-        if (STATS) an = mfma32x32x16(Acur[ks], bf, an);
-      }
-      float v[16];
+        for (int e = 0; e < 16; ++e) {
+          at[e] = 0.0f;
+          an[e] = 0.0f;
+        }
 #pragma unroll
-      for (int e = 0; e < 16; ++e) v[e] = at[e];
+        for (int ks = 0; ks < KS; ++ks) {
+          const int pos = ((ks * 2 + lhi) ^ swz) * 16;
+          const half8 bf = *reinterpret_cast<const half8*>(bt + (tn * 32 + lrow) * (CI * 2) + pos);
+          at = mfma32x32x16(bf, Acur[ks], at);
+          if (STATS) an = mfma32x32x16(Acur[ks], bf, an);
+        }
+        float v[16];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        lane_half_swap(v[q], v[4 + q]);
-        lane_half_swap(v[8 + q], v[12 + q]);
-      }
-      // v[8h .. 8h+7] = channels tn*32 + 16h + 8*lhi + 0..7 of pixel mp
+        for (int e = 0; e < 16; ++e) v[e] = at[e];
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int n = n0 + tn * 32 + h * 16 + lhi * 8;
-        if (mp_ok && n < a.Co) {
-          const int64_t off = (int64_t)mp * a.ldo + n;
+        for (int q = 0; q < 4; ++q) {
+          lane_half_swap(v[q], v[4 + q]);
+          lane_half_swap(v[8 + q], v[12 + q]);
+        }
+        // v[8h .. 8h+7] = channels tn*32 + 16h + 8*lhi + 0..7 of pixel mp:
+        // chunk tl*4 + 2h + lhi of this store group's row of pixel lrow
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
           float w[8];
 #pragma unroll
           for (int e = 0; e < 8; ++e) w[e] = v[h * 8 + e];
@@ -750,34 +774,54 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
           V8 o;
 #pragma unroll
           for (int e = 0; e < 8; ++e) o.h[e] = to_h16(w[e]);
-          store16(a.out + off, o);
+          const int slot = (tl * 4 + 2 * h + lhi) ^ (lrow & (SLOTS - 1));
+          *reinterpret_cast<V8*>(stg + (lrow * SLOTS + slot) * 16) = o;
+        }
+        if (STATS) {
+          // plain layout: lane holds channel tn*32 + lane % 32 and band rows
+          // 8*(e/4) + 4*(lane/32) + e%4; the shift is the band's first row
+          float y[16];
+#pragma unroll
+          for (int e = 0; e < 16; ++e) y[e] = to_f32(to_h16(an[e]));
+          const float K0 = __shfl(y[0], lrow, 64);
+          float s1 = 0.0f, s2 = 0.0f;
+#pragma unroll
+          for (int e = 0; e < 16; ++e) {
+            const int r = 8 * (e >> 2) + 4 * lhi + (e & 3);
+            const float d = band_m0 + r < M ? y[e] - K0 : 0.0f;
+            s1 += d;
+            s2 = __builtin_fmaf(d, d, s2);
+          }
+          s1 += __shfl_xor(s1, 32, 64);
+          s2 += __shfl_xor(s2, 32, 64);
+          bk[tn] = K0;
+          b1[tn] = s1;
+          b2[tn] = s2;
         }
       }
-      if (STATS) {
-        // plain layout: lane holds channel tn*32 + lane % 32 and band rows
-        // 8*(e/4) + 4*(lane/32) + e%4; the shift is the band's first row
-        float y[16];
+      wave_lds_sync();
+      // lane: chunk lane % SLOTS of pixel lane / SLOTS (+ PPI per instruction)
+      const int c = lane % SLOTS;
+      const int n = n0 + g * SW * 32 + c * 8;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) y[e] = to_f32(to_h16(an[e]));
-        const float K0 = __shfl(y[0], lrow, 64);
-        float s1 = 0.0f, s2 = 0.0f;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int r = 8 * (e >> 2) + 4 * lhi + (e & 3);
-          const float d = band_m0 + r < M ? y[e] - K0 : 0.0f;
-          s1 += d;
-          s2 = __builtin_fmaf(d, d, s2);
-        }
-        s1 += __shfl_xor(s1, 32, 64);
-        s2 += __shfl_xor(s2, 32, 64);
-        if (lhi == 0) {
-          bst[(wave * 3 + 0) * BN + tn * 32 + lrow] = K0;
-          bst[(wave * 3 + 1) * BN + tn * 32 + lrow] = s1;
-          bst[(wave * 3 + 2) * BN + tn * 32 + lrow] = s2;
-        }
+      for (int i = 0; i < 32 / PPI; ++i) {
+        const int q = lane / SLOTS + i * PPI;
+        const V8 o = *reinterpret_cast<const V8*>(stg + (q * SLOTS + (c ^ (q & (SLOTS - 1)))) * 16);
+        const int m = band_m0 + q;
+        if (m < M && n < a.Co) store16(a.out + (int64_t)m * a.ldo + n, o);
       }
+      wave_lds_sync();
     }
     if (STATS) {
+      __syncthreads();  // every wave is done with its staging buffer
+      if (lhi == 0) {
+#pragma unroll
+        for (int tn = 0; tn < TN; ++tn) {
+          bst[(wave * 3 + 0) * BN + tn * 32 + lrow] = bk[tn];
+          bst[(wave * 3 + 1) * BN + tn * 32 + lrow] = b1[tn];
+          bst[(wave * 3 + 2) * BN + tn * 32 + lrow] = b2[tn];
+        }
+      }
       if (lane == 0) {
         const int rows = M - band_m0;
         bcnt[wave] = rows <= 0 ? 0 : (rows < 32 ? rows : 32);
