@@ -618,7 +618,9 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
 //    bytes: each store instruction then writes whole 128-byte (SW = 2) or
 //    64-byte lines.  Written straight from the swapped layout, every store
 //    instruction split into 32 separate 32-byte writes, and the store path
-//    (not HBM) bounded these layers;
+//    (not HBM) bounded these layers.  With an addend the float32 sums take
+//    that path instead (the addend joins before the one rounding), and the
+//    addend is read in the same whole-line layout;
 //  - with BN statistics the plain product D = X x W is computed too (the
 //    MFMAs are cheap here), whose layout gives each lane one channel and 16
 //    rows: the band sums are taken in the lane and kept in registers, and the
@@ -626,16 +628,18 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
 //    igemm4_kernel, through the same LDS space.
 // Each output element is the same k-ordered sum of exact products in both
 // MFMA forms, so the values equal the other kernels' bit for bit.
-template <int CI, int BN, bool STATS>
+template <int CI, int BN, bool STATS, bool ADD>
 struct CfgPw {
   static constexpr int KS = CI / 16;          // k sub-steps of 16 channels
   static constexpr int TN = BN / 32;          // 32-channel tiles
   static constexpr int SW = CI == 64 ? 2 : 1; // 32-channel tiles per store group
   static constexpr int BBYTES = BN * CI * 2;  // resident filter tile
-  static constexpr int STG = 4 * 32 * SW * 64;            // [wave][pixel][SW*64 bytes]
+  // [wave][pixel][SW*64 bytes] of rounded values, or [wave][pixel][SW*128
+  // bytes] of float32 sums where the addend joins before the rounding
+  static constexpr int STG = 4 * 32 * SW * (ADD ? 128 : 64);
   static constexpr int BST = STATS ? 4 * 3 * BN * 4 : 0;  // [wave][K, s1, s2][BN]
   static constexpr int SHARED = STG > BST ? STG : BST;
-  static constexpr int LDS = BBYTES + SHARED + 16;
+  static constexpr int LDS = BBYTES + SHARED + (STATS ? 16 : 0);  // (+ 4 band row counts)
 };
 
 __device__ __forceinline__ void lane_half_swap(float& x, float& y) {
@@ -655,7 +659,7 @@ __device__ __forceinline__ void wave_lds_sync() {
 
 template <int CI, int BN, bool STATS, bool ADD>
 __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) {
-  using K = CfgPw<CI, BN, STATS>;
+  using K = CfgPw<CI, BN, STATS, ADD>;
   constexpr int KS = K::KS, TN = K::TN, SW = K::SW;
   constexpr int SLOTS = 4 * SW;       // 16-byte chunks per staged pixel row
   constexpr int PPI = 64 / SLOTS;     // pixels per store instruction
@@ -675,7 +679,7 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
   const int tid = threadIdx.x;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int lrow = lane & 31, lhi = lane >> 5;
-  char* stg = shared + wave * 32 * SLOTS * 16;
+  char* stg = shared + wave * 32 * SLOTS * (ADD ? 32 : 16);
   constexpr uint32_t OOB = 0x80000000u;
   const int act_bytes = (int)((int64_t)a.N * a.Hi * a.Wi * CI * 2);
   const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
@@ -718,18 +722,17 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
   const int swz = lrow & 7;
   for (; tile < ntiles; tile += gridDim.x) {
     const int band_m0 = tile * 128 + wave * 32;
-    const int mp = band_m0 + lrow;  // this lane's output pixel in the transposed tile
-    const bool mp_ok = mp < M;
-    V8 adv[ADD ? TN : 1][2];
+    // the tile's addend, loaded before the MFMAs in the store layout (lane:
+    // chunk lane % SLOTS of pixel lane / SLOTS + PPI*i; clamped into range)
+    V8 adv[ADD ? TN / SW : 1][ADD ? 32 / PPI : 1];
     if (ADD) {
-      // the tile's addend, loaded before the MFMAs (pixel clamped into range)
-      const int64_t mrow = (int64_t)(mp_ok ? mp : M - 1) * a.ldo;
 #pragma unroll
-      for (int tn = 0; tn < TN; ++tn)
+      for (int g = 0; g < TN / SW; ++g)
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int n = n0 + tn * 32 + h * 16 + lhi * 8;
-          adv[tn][h] = load16(a.addend + mrow + (n < a.Co ? n : 0));
+        for (int i = 0; i < 32 / PPI; ++i) {
+          const int m = band_m0 + lane / SLOTS + i * PPI;
+          const int n = n0 + g * SW * 32 + (lane % SLOTS) * 8;
+          adv[g][i] = load16(a.addend + (int64_t)(m < M ? m : M - 1) * a.ldo + (n < a.Co ? n : 0));
         }
     }
     load_a(Anext, row_off(tile + gridDim.x));
@@ -764,18 +767,26 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
         // chunk tl*4 + 2h + lhi of this store group's row of pixel lrow
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          float w[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) w[e] = v[h * 8 + e];
+          const int k = tl * 4 + 2 * h + lhi;
           if (ADD) {
+            // float32: two 16-byte halves per chunk, swizzled over 2*SLOTS slots
 #pragma unroll
-            for (int e = 0; e < 8; ++e) w[e] += to_f32(adv[tn][h].h[e]);
+            for (int j = 0; j < 2; ++j) {
+              const int slot = (2 * k + j) ^ (lrow & (2 * SLOTS - 1));
+              float4 f;
+              f.x = v[h * 8 + 4 * j];
+              f.y = v[h * 8 + 4 * j + 1];
+              f.z = v[h * 8 + 4 * j + 2];
+              f.w = v[h * 8 + 4 * j + 3];
+              *reinterpret_cast<float4*>(stg + (lrow * 2 * SLOTS + slot) * 16) = f;
+            }
+          } else {
+            V8 o;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) o.h[e] = to_h16(v[h * 8 + e]);
+            const int slot = k ^ (lrow & (SLOTS - 1));
+            *reinterpret_cast<V8*>(stg + (lrow * SLOTS + slot) * 16) = o;
           }
-          V8 o;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) o.h[e] = to_h16(w[e]);
-          const int slot = (tl * 4 + 2 * h + lhi) ^ (lrow & (SLOTS - 1));
-          *reinterpret_cast<V8*>(stg + (lrow * SLOTS + slot) * 16) = o;
         }
         if (STATS) {
           // plain layout: lane holds channel tn*32 + lane % 32 and band rows
@@ -806,7 +817,23 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
 #pragma unroll
       for (int i = 0; i < 32 / PPI; ++i) {
         const int q = lane / SLOTS + i * PPI;
-        const V8 o = *reinterpret_cast<const V8*>(stg + (q * SLOTS + (c ^ (q & (SLOTS - 1)))) * 16);
+        V8 o;
+        if (ADD) {
+          float w[8];
+#pragma unroll
+          for (int j = 0; j < 2; ++j) {
+            const float4 f = *reinterpret_cast<const float4*>(
+                stg + (q * 2 * SLOTS + ((2 * c + j) ^ (q & (2 * SLOTS - 1)))) * 16);
+            w[4 * j] = f.x;
+            w[4 * j + 1] = f.y;
+            w[4 * j + 2] = f.z;
+            w[4 * j + 3] = f.w;
+          }
+#pragma unroll
+          for (int e = 0; e < 8; ++e) o.h[e] = to_h16(w[e] + to_f32(adv[g][i].h[e]));
+        } else {
+          o = *reinterpret_cast<const V8*>(stg + (q * SLOTS + (c ^ (q & (SLOTS - 1)))) * 16);
+        }
         const int m = band_m0 + q;
         if (m < M && n < a.Co) store16(a.out + (int64_t)m * a.ldo + n, o);
       }
