@@ -127,6 +127,8 @@ def op_work(op, net):
     if k == "dgrad_filter":
         d = a["desc"]
         return 0, 4 * d.k * d.c * d.r * d.s, "hbm"
+    if k == "dgrad_filters":
+        return 0, sum(4 * d.k * d.c * d.r * d.s for d, _, _ in a["items"]), "hbm"
     if k == "maxpool_fwd":
         d = a["desc"]
         p, q = (d.h + 2 * d.pad_h - d.r) // d.stride_h + 1, (d.w + 2 * d.pad_w - d.s) // d.stride_w + 1

@@ -158,6 +158,17 @@ fp16_status fp16_conv_dgrad_filter(const fp16_conv_desc* desc, const fp16_t* w, 
 fp16_status fp16_conv_dgrad_wf(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* wf,
                                const fp16_t* addend, fp16_t* dx, void* ws, size_t ws_bytes,
                                fp16_stream_t stream);
+/* fp16_conv_dgrad_filter for `count` convolutions at once (descs[i], w[i],
+ * wf[i]; host arrays, read during the call only): every filter of a network
+ * rearranged by one launch (or a few) instead of one launch each, with
+ * identical results.  0 <= count <= FP16_DGRAD_FILTERS_MAX (else
+ * FP16_ERR_SHAPE); every item is validated as fp16_conv_dgrad_filter does
+ * before anything is launched, and no wf[i] may overlap any w[j] or another
+ * wf[j] (FP16_ERR_ALIASING). */
+#define FP16_DGRAD_FILTERS_MAX 1024
+fp16_status fp16_conv_dgrad_filters(int32_t count, const fp16_conv_desc* descs,
+                                    const fp16_t* const* w, fp16_t* const* wf,
+                                    fp16_stream_t stream);
 
 /* Weight gradient: the gradient with respect to the filter that the
  * momentum-SGD update of Section 5.1 consumes, stored in binary16 with no

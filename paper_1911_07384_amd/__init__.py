@@ -33,6 +33,7 @@ EXPORTS = ["fp16_conv_out_dims", "fp16_conv_workspace_bytes", "fp16_conv_fwd", "
            "fp16_avgpool_fwd", "fp16_avgpool_bwd", "fp16_softmax_ce", "fp16_status_string",
            "fp16_version", "fp16_conv_bn_workspace_bytes", "fp16_conv_bn_relu_fwd",
            "fp16_sgd_step_f16", "fp16_conv_dgrad_filter_bytes", "fp16_conv_dgrad_filter",
+           "fp16_conv_dgrad_filters",
            "fp16_conv_dgrad_wf", "fp16_noalloc_scratch_bytes", "fp16_conv_wgrad_noalloc",
            "fp16_bn_mask_bytes", "fp16_bn_relu_m", "fp16_bn_relu_bwd_m", "fp16_conv_bn_relu_fwd_m"]
 
@@ -77,6 +78,7 @@ _SIGS = {
     "fp16_noalloc_scratch_bytes": (_SZ, []),
     "fp16_conv_wgrad_noalloc": (ctypes.c_int, [_P, _P, _P, _P, _P]),
     "fp16_conv_dgrad_filter": (ctypes.c_int, [_P, _P, _P, _P]),
+    "fp16_conv_dgrad_filters": (ctypes.c_int, [ctypes.c_int32, _P, _P, _P, _P]),
     "fp16_conv_dgrad_wf": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_bn_workspace_bytes": (_SZ, [_P]),
     "fp16_bn_mask_bytes": (_SZ, [_P]),
@@ -207,6 +209,17 @@ def fp16_conv_dgrad_filter_bytes(desc: ConvDesc) -> int:
 def fp16_conv_dgrad_filter(desc, w, wf, stream=None) -> None:
     _check("fp16_conv_dgrad_filter", lib().fp16_conv_dgrad_filter(ctypes.byref(desc), _ptr(w),
                                                                   _ptr(wf), _stream(stream)))
+
+
+def fp16_conv_dgrad_filters(descs, ws, wfs, stream=None) -> None:
+    """fp16_conv_dgrad_filter for every (desc, w, wf) of the three lists."""
+    n = len(descs)
+    if not (len(ws) == len(wfs) == n):
+        raise ValueError("descs, ws and wfs differ in length")
+    d = (ConvDesc * max(n, 1))(*descs)
+    w = (ctypes.c_void_p * max(n, 1))(*[_ptr(t) for t in ws])
+    f = (ctypes.c_void_p * max(n, 1))(*[_ptr(t) for t in wfs])
+    _check("fp16_conv_dgrad_filters", lib().fp16_conv_dgrad_filters(n, d, w, f, _stream(stream)))
 
 
 def fp16_conv_dgrad_wf(desc, dy, wf, addend, dx, ws=None, ws_bytes=None, stream=None) -> None:

@@ -7,6 +7,8 @@
 
 #include <stdint.h>
 
+#include <vector>
+
 using namespace fp16k;
 
 namespace {
@@ -358,6 +360,46 @@ fp16_status fp16_conv_dgrad_filter(const fp16_conv_desc* desc, const fp16_t* w, 
   return hip_status(launch_dgrad_filter(reinterpret_cast<const h16*>(w), reinterpret_cast<h16*>(wf),
                                         d.K, d.C, d.R, d.S, d.C, d.Kp, d.sh, d.sw, d.ph, d.pw,
                                         static_cast<hipStream_t>(stream)));
+}
+
+fp16_status fp16_conv_dgrad_filters(int32_t count, const fp16_conv_desc* descs,
+                                    const fp16_t* const* w, fp16_t* const* wf,
+                                    fp16_stream_t stream) {
+  if (count == 0) return FP16_OK;
+  if (count < 0 || count > FP16_DGRAD_FILTERS_MAX) return FP16_ERR_SHAPE;
+  if (!descs || !w || !wf) return FP16_ERR_NULL;
+  std::vector<DgradFiltJob> jobs((size_t)count);
+  std::vector<size_t> wb((size_t)count), fb((size_t)count);
+  for (int i = 0; i < count; ++i) {
+    ConvDims d;
+    const fp16_status s = check_conv(&descs[i], &d);
+    if (s != FP16_OK) return s;
+    if (d.layout != FP16_NHWC) return FP16_ERR_UNSUPPORTED;
+    if (!w[i] || !wf[i]) return FP16_ERR_NULL;
+    if (!aligned16(w[i]) || !aligned16(wf[i])) return FP16_ERR_MISALIGNED;
+    wb[i] = (size_t)d.w_elems * 2;
+    fb[i] = dgrad_filter_bytes(d);
+    DgradFiltJob& J = jobs[(size_t)i];
+    J.w = reinterpret_cast<const h16*>(w[i]);
+    J.dst = reinterpret_cast<h16*>(wf[i]);
+    J.K = d.K;
+    J.C = d.C;
+    J.R = d.R;
+    J.S = d.S;
+    J.Kp = d.Kp;
+    J.sh = d.sh;
+    J.sw = d.sw;
+    J.pad_h = d.ph;
+    J.pad_w = d.pw;
+    J.blk0 = 0;
+  }
+  // every output apart from every filter and every other output
+  for (int i = 0; i < count; ++i)
+    for (int j = 0; j < count; ++j) {
+      if (overlap(wf[i], fb[i], w[j], wb[j])) return FP16_ERR_ALIASING;
+      if (j != i && overlap(wf[i], fb[i], wf[j], fb[j])) return FP16_ERR_ALIASING;
+    }
+  return hip_status(launch_dgrad_filters(jobs.data(), count, static_cast<hipStream_t>(stream)));
 }
 
 fp16_status fp16_conv_dgrad_wf(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* wf,

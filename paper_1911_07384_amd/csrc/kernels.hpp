@@ -87,8 +87,8 @@ bool igemm_takes_stats(const IgemmArgs& a);
 struct DgradPhase {
   int r0, s0, ntr, nts, Hph, Wph, pad_h, pad_w;
 };
-inline DgradPhase dgrad_phase(int ph, int pw, int H, int W, int R, int S, int sh, int sw,
-                              int pad_h, int pad_w) {
+__host__ __device__ inline DgradPhase dgrad_phase(int ph, int pw, int H, int W, int R, int S,
+                                                  int sh, int sw, int pad_h, int pad_w) {
   DgradPhase d;
   d.r0 = (ph + pad_h) % sh;
   d.s0 = (pw + pad_w) % sw;
@@ -106,6 +106,15 @@ inline DgradPhase dgrad_phase(int ph, int pw, int H, int W, int R, int S, int sh
 // holding W[k][r0 + sh*(nt_r-1-t_r)][s0 + sw*(nt_s-1-t_s)][c] (zero for k >= K).
 hipError_t launch_dgrad_filter(const h16* w, h16* dst, int K, int C, int R, int S, int Cw,
                                int Kp, int sh, int sw, int pad_h, int pad_w, hipStream_t st);
+// The same rearrangement for n filters (channel stride Cw = C each), in as
+// few launches as the kernel-argument table allows.
+struct DgradFiltJob {
+  const h16* w;
+  h16* dst;
+  int K, C, R, S, Kp, sh, sw, pad_h, pad_w;
+  int blk0;  // first block of this job in its launch (set by the launcher)
+};
+hipError_t launch_dgrad_filters(const DgradFiltJob* jobs, int n, hipStream_t st);
 
 struct WgradArgs {
   const h16* x;   // NHWC [N][H][W][C], C % 8 == 0

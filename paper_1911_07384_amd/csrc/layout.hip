@@ -110,15 +110,15 @@ struct DgradTaps {
   int ntr[kMaxTaps], nts[kMaxTaps], tr[kMaxTaps], ts[kMaxTaps], r[kMaxTaps], s[kMaxTaps];
 };
 
-__global__ __launch_bounds__(256) void dgrad_filter_tiled(const h16* __restrict__ w,
-                                                          h16* __restrict__ dst, int K, int C,
-                                                          int R, int S, int Cw, int Kp,
-                                                          const DgradTaps taps) {
+// One 64 x 64 (channel x filter) tile of one tap: reads 64 rows of 64
+// consecutive channels of W at tap (r, s) and writes them transposed into the
+// phase filter at dst + off (ntr x nts taps, tap (tr, ts)).
+__device__ __forceinline__ void dgrad_tile(const h16* __restrict__ w, h16* __restrict__ dst,
+                                           int K, int C, int R, int S, int Cw, int Kp, int r,
+                                           int s, int64_t off, int ntr, int nts, int tr, int ts,
+                                           int c0, int k0) {
   __shared__ h16 tile[64][66];  // [channel][k]
-  const int q = blockIdx.z;
-  const int c0 = blockIdx.x * 64, k0 = blockIdx.y * 64;
   const int t = threadIdx.x;
-  const int r = taps.r[q], s = taps.s[q];
   if (Cw % 8 == 0) {
     // 16-byte loads, both of a thread's in flight together
     V8 v[2];
@@ -155,8 +155,7 @@ __global__ __launch_bounds__(256) void dgrad_filter_tiled(const h16* __restrict_
   const int cc = t >> 2, kq = (t & 3) * 16;
   const int c = c0 + cc;
   if (c >= C) return;
-  h16* row = dst + taps.off[q] +
-             (((int64_t)c * taps.ntr[q] + taps.tr[q]) * taps.nts[q] + taps.ts[q]) * Kp;
+  h16* row = dst + off + (((int64_t)c * ntr + tr) * nts + ts) * Kp;
 #pragma unroll
   for (int h = 0; h < 2; ++h) {
     const int k = k0 + kq + h * 8;
@@ -165,6 +164,52 @@ __global__ __launch_bounds__(256) void dgrad_filter_tiled(const h16* __restrict_
 #pragma unroll
       for (int e = 0; e < 8; ++e) v.h[e] = tile[cc][kq + h * 8 + e];
       store16(row + k, v);
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void dgrad_filter_tiled(const h16* __restrict__ w,
+                                                          h16* __restrict__ dst, int K, int C,
+                                                          int R, int S, int Cw, int Kp,
+                                                          const DgradTaps taps) {
+  const int q = blockIdx.z;
+  dgrad_tile(w, dst, K, C, R, S, Cw, Kp, taps.r[q], taps.s[q], taps.off[q], taps.ntr[q],
+             taps.nts[q], taps.tr[q], taps.ts[q], blockIdx.x * 64, blockIdx.y * 64);
+}
+
+// Many filters' rearrangements in one launch: the jobs (one filter each, all
+// its taps) are laid end to end over a 1-D grid of 64 x 64 tiles; each block
+// finds its job, then its tap by walking the stride phases in (ph, pw)
+// row-major order as the per-filter launcher does.
+constexpr int kDfBatch = 32;  // jobs per launch (kernel-argument table)
+struct DgradFiltBatch {
+  int n;
+  DgradFiltJob j[kDfBatch];
+};
+
+__global__ __launch_bounds__(256) void dgrad_filter_batched(const DgradFiltBatch b) {
+  const int bid = blockIdx.x;
+  int i = 0;
+  while (i + 1 < b.n && b.j[i + 1].blk0 <= bid) ++i;
+  const DgradFiltJob& J = b.j[i];
+  const int CT = (J.C + 63) / 64, KT = (J.Kp + 63) / 64;
+  int local = bid - J.blk0;
+  int q = local / (CT * KT);
+  local -= q * CT * KT;
+  const int ct = local / KT, kt = local - (local / KT) * KT;
+  int64_t off = 0;
+  for (int ph = 0; ph < J.sh; ++ph) {
+    for (int pw = 0; pw < J.sw; ++pw) {
+      const DgradPhase d = dgrad_phase(ph, pw, 1, 1, J.R, J.S, J.sh, J.sw, J.pad_h, J.pad_w);
+      const int nt = d.ntr * d.nts;
+      if (q < nt) {
+        const int tr = q / d.nts, ts = q - (q / d.nts) * d.nts;
+        dgrad_tile(J.w, J.dst, J.K, J.C, J.R, J.S, J.C, J.Kp, d.r0 + J.sh * (d.ntr - 1 - tr),
+                   d.s0 + J.sw * (d.nts - 1 - ts), off, d.ntr, d.nts, tr, ts, ct * 64, kt * 64);
+        return;
+      }
+      q -= nt;
+      off += (int64_t)J.C * nt * J.Kp;
     }
   }
 }
@@ -230,6 +275,45 @@ hipError_t launch_pad_channels(const h16* src, h16* dst, int64_t P, int C, int C
     hipLaunchKernelGGL(pad_channels_kernel, dim3(grid_for(P * Cp)), dim3(kThreads), 0, st, src,
                        dst, P, C, Cp);
   return hipGetLastError();
+}
+
+hipError_t launch_dgrad_filters(const DgradFiltJob* jobs, int n, hipStream_t st) {
+  DgradFiltBatch b{};
+  int blocks = 0;
+  auto flush = [&]() -> hipError_t {
+    if (b.n == 0) return hipSuccess;
+    hipLaunchKernelGGL(dgrad_filter_batched, dim3(blocks), dim3(256), 0, st, b);
+    b.n = 0;
+    blocks = 0;
+    return hipGetLastError();
+  };
+  for (int i = 0; i < n; ++i) {
+    const DgradFiltJob& J = jobs[i];
+    if (J.R * J.S > kMaxTaps || J.Kp % 8 != 0) {
+      // outside the tiled path: its own launch(es)
+      const hipError_t e = launch_dgrad_filter(J.w, J.dst, J.K, J.C, J.R, J.S, J.C, J.Kp, J.sh,
+                                               J.sw, J.pad_h, J.pad_w, st);
+      if (e != hipSuccess) return e;
+      continue;
+    }
+    int taps = 0;
+    for (int ph = 0; ph < J.sh; ++ph)
+      for (int pw = 0; pw < J.sw; ++pw) {
+        const DgradPhase d = dgrad_phase(ph, pw, 1, 1, J.R, J.S, J.sh, J.sw, J.pad_h, J.pad_w);
+        taps += d.ntr * d.nts;
+      }
+    const int nb = taps * ((J.C + 63) / 64) * ((J.Kp + 63) / 64);
+    if (nb == 0) continue;
+    if (b.n == kDfBatch) {
+      const hipError_t e = flush();
+      if (e != hipSuccess) return e;
+    }
+    b.j[b.n] = J;
+    b.j[b.n].blk0 = blocks;
+    ++b.n;
+    blocks += nb;
+  }
+  return flush();
 }
 
 hipError_t launch_dgrad_filter(const h16* w, h16* dst, int K, int C, int R, int S, int Cw, int Kp,

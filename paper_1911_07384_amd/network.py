@@ -347,6 +347,9 @@ class ResNet50:
             F.fp16_conv_dgrad_wf(a["desc"], t(a["dy"]), t(a["wf"]), t(a["addend"]), t(a["dx"]), ws)
         elif k == "dgrad_filter":
             F.fp16_conv_dgrad_filter(a["desc"], t(a["w"]), t(a["wf"]))
+        elif k == "dgrad_filters":
+            F.fp16_conv_dgrad_filters([d for d, _, _ in a["items"]], [t(w) for _, w, _ in a["items"]],
+                                      [t(f) for _, _, f in a["items"]])
         elif k == "conv_wgrad":
             F.fp16_conv_wgrad(a["desc"], t(a["x"]), t(a["dy"]), t(a["dw"]), ws)
         elif k == "conv_bn_fwd":
@@ -394,8 +397,14 @@ class ResNet50:
         else:
             raise ValueError(k)
 
+    @property
+    def prep_op(self):
+        """The rearrangements of self.prep as one batched call."""
+        return Op("dgrad_filters", "prep", {"items": [(o.a["desc"], o.a["w"], o.a["wf"])
+                                                      for o in self.prep]})
+
     def program(self):
-        return self.prep + self.fwd + self.bwd + self.upd
+        return [self.prep_op] + self.fwd + self.bwd + self.upd
 
     _OUTPUTS = {"conv_fwd": ("y",), "conv_bn_fwd": ("y", "z", "stats", "mask"),
                 "conv_dgrad": ("dx",), "conv_dgrad_add": ("dx",),
@@ -425,17 +434,17 @@ class ResNet50:
     def forward(self):
         # the data-gradient filters of this step's weights, on the side stream
         # while the forward runs (the backward waits for them)
+        # (all of them in one call: launched one filter each, they ran one
+        # after another ahead of the forward, 0.54 ms of the step)
         if self.side is None:
-            for op in self.prep:
-                self.run(op)
+            self.run(self.prep_op)
         else:
             main = torch.cuda.current_stream()
             start = torch.cuda.Event()
             start.record(main)
             self.side.wait_event(start)
             with torch.cuda.stream(self.side):
-                for op in self.prep:
-                    self.run(op, ws=self.ws_side)
+                self.run(self.prep_op, ws=self.ws_side)
             self._wf_ready = torch.cuda.Event()
             self._wf_ready.record(self.side)
         for op in self.fwd:

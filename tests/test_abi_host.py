@@ -403,3 +403,22 @@ def test_kept_mask_validation():
                                        need, None) == ALIASING  # mask inside y
     assert lib.fp16_conv_bn_relu_fwd_m(ctypes.byref(cd), ctypes.byref(bd), *args, Cc + (4 << 20),
                                        WS, need, None) == ALIASING  # mask inside z
+
+
+def test_dgrad_filters_validation():
+    lib = F.lib()
+    assert lib.fp16_conv_dgrad_filters(0, None, None, None, None) == OK  # nothing to do
+    D = (F.ConvDesc * 2)(_conv(), _conv(k=128))
+    P = lambda *a: (ctypes.c_void_p * len(a))(*a)
+    assert lib.fp16_conv_dgrad_filters(-1, D, P(A), P(B), None) == SHAPE
+    assert lib.fp16_conv_dgrad_filters(2, None, P(A, A + (1 << 20)), P(B, B + (1 << 20)), None) == NULL
+    assert lib.fp16_conv_dgrad_filters(2, D, P(A, None), P(B, B + (1 << 20)), None) == NULL
+    assert lib.fp16_conv_dgrad_filters(2, D, P(A, A + (1 << 20)), P(B, B + 8), None) == MISALIGNED
+    # an output over another item's filter, or over another output
+    assert lib.fp16_conv_dgrad_filters(2, D, P(A, A + (1 << 20)), P(B, A + (1 << 20) + 64),
+                                       None) == ALIASING
+    assert lib.fp16_conv_dgrad_filters(2, D, P(A, A + (1 << 20)), P(B, B + 256), None) == ALIASING
+    N = (F.ConvDesc * 1)(_conv(layout="NCHW"))
+    assert lib.fp16_conv_dgrad_filters(1, N, P(A), P(B), None) == UNSUPPORTED
+    bad = (F.ConvDesc * 1)(_conv(n=0))
+    assert lib.fp16_conv_dgrad_filters(1, bad, P(A), P(B), None) == SHAPE

@@ -192,3 +192,29 @@ def test_dgrad_from_rearranged_filter_is_identical(shape, with_addend):
     F.fp16_conv_dgrad_wf(case.desc, dev(case.dy), wf, addend, b, ws)
     torch.cuda.synchronize()
     assert np.array_equal(host(a).view(np.uint16), host(b).view(np.uint16))
+
+
+def test_batched_filter_rearrangement_is_identical():
+    # every ResNet-50 filter shape (and the classifier as a 1x1 convolution,
+    # K = 1000) plus ragged and strided ones: 70 filters, so the batch spans
+    # three launches; each wf must equal the one-filter call's bit for bit
+    require_gpu()
+    from paper_1911_07384_amd import resnet50, synth
+    shapes = [(L.c, L.k, L.r, L.stride) for L in resnet50.LAYERS]
+    shapes += [(2048, 1000, 1, 1), (24, 40, 3, 1), (8, 8, 5, 2), (136, 72, 3, 2), (3, 64, 7, 2)]
+    shapes = (shapes * 3)[:70]
+    descs, ws, wb, wa = [], [], [], []
+    for i, (c, k, r, st) in enumerate(shapes):
+        d = F.conv_desc(2, c, 16, 16, k, r, r, st, r // 2)
+        descs.append(d)
+        ws.append(dev(synth.normal_f16((k, r, r, c), 0.1, 11, i)))
+        nb = F.fp16_conv_dgrad_filter_bytes(d) // 2
+        wa.append(torch.full((nb,), float("nan"), dtype=torch.float16, device="cuda"))
+        wb.append(torch.full((nb,), float("nan"), dtype=torch.float16, device="cuda"))
+    note(f"[gpu] dgrad_filters x{len(descs)}")
+    F.fp16_conv_dgrad_filters(descs, ws, wb)
+    for d, w, a in zip(descs, ws, wa):
+        F.fp16_conv_dgrad_filter(d, w, a)
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(zip(wa, wb)):
+        assert np.array_equal(host(a).view(np.uint16), host(b).view(np.uint16)), shapes[i]
