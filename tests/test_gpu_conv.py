@@ -51,6 +51,12 @@ SHAPES = [
     (3, 136, 9, 9, 64, 1, 1, 1, 0, "NHWC"),     # pointwise dgrad: 64 -> 136 channels (one 8-wide chunk
                                                 # in the second channel tile)
     (5, 64, 56, 56, 256, 1, 1, 1, 0, "NHWC"),   # pointwise fwd / dgrad over many tiles per workgroup
+    # 3x3 stride 1 on the DMA-staged kernel at its edges:
+    (2, 64, 31, 31, 128, 3, 3, 1, 1, "NHWC"),   # odd row width, one 64-channel k-block per tap
+    (3, 192, 5, 9, 136, 3, 3, 1, 1, "NHWC"),    # three k-blocks per tap, ragged second N tile
+    (2, 128, 1, 13, 128, 3, 3, 1, 1, "NHWC"),   # one-row images: the outer tap rows all padding
+    (1, 256, 14, 14, 256, 3, 3, 1, 1, "NHWC"),  # the conv4_x 3x3 layer at N = 1
+    (2, 64, 8, 32, 128, 3, 3, 1, 1, "NHWC"),    # 32-pixel rows
 ]
 
 
