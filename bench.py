@@ -66,6 +66,9 @@ def parse():
     ap.add_argument("--no-block", action="store_true", help="skip the conv2_x block at batch 32")
     ap.add_argument("--no-f16-arith", action="store_true",
                     help="skip the strict binary16-arithmetic timing leg")
+    ap.add_argument("--sweep-only", action="store_true",
+                    help="only the 16 3x3 layers at batch 128 (NHWC), for counter runs: every "
+                         "timed batch of calls follows a spin kernel")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="first run three device-to-device copies of MIB MiB (a plain copy of "
                          "known size, the yardstick for the HBM byte counters)")
@@ -278,7 +281,7 @@ def calls_only(args, torch):
 
 # ---- config 3: the per-layer sweep at batch 128 -----------------------------------
 
-def conv_sweep_leg(torch, sweep_all: bool):
+def conv_sweep_leg(torch, sweep_all: bool, nchw: bool = True):
     from paper_1911_07384_amd import resnet50
     layers = resnet50.LAYERS if sweep_all else [l for l in resnet50.LAYERS if l.r == 3]
     rows = resnet50.sweep(128, layers)
@@ -312,6 +315,8 @@ def conv_sweep_leg(torch, sweep_all: bool):
     if sweep_all:
         out["conv53_b128"] = {k: round(v, 4) for k, v in summ["all_53"].items()}
     torch.cuda.empty_cache()
+    if not nchw:
+        return out, rows
     nchw = resnet50.sweep(128, [l for l in resnet50.LAYERS if l.r == 3], layout="NCHW")
     s2 = resnet50.summarize(nchw, PEAK_FP16_TFLOPS)["3x3_16"]
     out["conv3x3_b128_nchw"] = {k: round(v, 4) for k, v in s2.items()}
@@ -762,6 +767,10 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    if args.sweep_only:
+        legs, _ = conv_sweep_leg(torch, False, nchw=False)
+        print(json.dumps(legs), flush=True)
+        return
     if args.calls_only:
         calls_only(args, torch)
         return
