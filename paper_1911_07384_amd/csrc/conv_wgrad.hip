@@ -655,14 +655,61 @@ hipError_t launch_wgrad_partial(const WgradArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+// Split-K partial sums folded in place: block (b, g) adds, for the 64
+// float4 columns [64b, 64b + 64) of the split rows (row4 float4 each), the
+// splits [g*kFoldGs, (g+1)*kFoldGs) of group g and writes the sum over the
+// group's first split.  Wave w takes the group's splits w, w + 4, ... in
+// order (all of its loads in flight; a split past the last is loaded
+// clamped, in bounds, and not added), then the four wave sums are added in
+// order.  Only this block reads or writes these elements of these splits.
+constexpr int kFoldGs = 16;
+
+__global__ __launch_bounds__(256) void wgrad_fold_kernel(float* part, int splits, int64_t row4) {
+  __shared__ float4 red[3][64];
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int64_t col = (int64_t)blockIdx.x * 64 + lane;
+  const bool live = col < row4;
+  const int64_t cc = live ? col : 0;
+  const int g0 = blockIdx.y * kFoldGs;
+  float4* p = reinterpret_cast<float4*>(part);
+  constexpr int U = kFoldGs / 4;
+  float4 v[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int sp = g0 + w + 4 * u;
+    v[u] = p[(int64_t)(sp < splits ? sp : splits - 1) * row4 + cc];
+  }
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    if (g0 + w + 4 * u < splits) {
+      acc.x += v[u].x;
+      acc.y += v[u].y;
+      acc.z += v[u].z;
+      acc.w += v[u].w;
+    }
+  }
+  if (w > 0) red[w - 1][lane] = acc;
+  __syncthreads();
+  if (w != 0 || !live) return;
+#pragma unroll
+  for (int i = 0; i < 3; ++i) {
+    acc.x += red[i][lane].x;
+    acc.y += red[i][lane].y;
+    acc.z += red[i][lane].z;
+    acc.w += red[i][lane].w;
+  }
+  p[(int64_t)g0 * row4 + col] = acc;
+}
+
 // The stem's weight gradient computed as a 4x4 stride-1 convolution over the
 // 2x2 space-to-depth image (16 channels, (dh*2 + dw)*3 + c): original tap
 // (r, s, c) is s2d tap ((r+1)/2, (s+1)/2) at channel (((r+1)%2)*2 + (s+1)%2)*3
-// + c.  dw[k][r][s][c] (KRSC, 7x7x3) = rne16(sum over splits, in order, of
-// partial[split][k][(r'*4 + s')*16 + ch]).
+// + c.  dw[k][r][s][c] (KRSC, 7x7x3) = rne16(sum over the groups, in order, of
+// the folded partial[g * kFoldGs][k][(r'*4 + s')*16 + ch]).
 __global__ __launch_bounds__(256) void wgrad_reduce_s2d3_kernel(const float* __restrict__ partial,
-                                                                 int splits, int K,
-                                                                 h16* __restrict__ dw) {
+                                                                 int groups, int64_t stride,
+                                                                 int K, h16* __restrict__ dw) {
   const int i = blockIdx.x * 256 + threadIdx.x;  // enumerates k, r, s, c
   if (i >= K * 147) return;
   const int c = i % 3, rs = (i / 3) % 49, k = i / 147;
@@ -670,25 +717,28 @@ __global__ __launch_bounds__(256) void wgrad_reduce_s2d3_kernel(const float* __r
   const int rp = (r + 1) >> 1, sp = (s + 1) >> 1;
   const int ch = (((r + 1) & 1) * 2 + ((s + 1) & 1)) * 3 + c;
   const float* p = partial + (int64_t)k * 256 + (rp * 4 + sp) * 16 + ch;
-  const int64_t stride = (int64_t)K * 256;
+  constexpr int U = 8;
   float acc = 0.0f;
-  int sp2 = 0;
-  for (; sp2 + 4 <= splits; sp2 += 4) {
-    const float v0 = p[(sp2 + 0) * stride], v1 = p[(sp2 + 1) * stride];
-    const float v2 = p[(sp2 + 2) * stride], v3 = p[(sp2 + 3) * stride];
-    acc += v0;
-    acc += v1;
-    acc += v2;
-    acc += v3;
+  for (int g0 = 0; g0 < groups; g0 += U) {
+    float v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) v[u] = p[(int64_t)(g0 + u < groups ? g0 + u : groups - 1) * stride];
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+      if (g0 + u < groups) acc += v[u];
   }
-  for (; sp2 < splits; ++sp2) acc += p[sp2 * stride];
   dw[i] = to_h16(acc);
 }
 
-hipError_t launch_wgrad_reduce_s2d3(const float* partial, int splits, int K, h16* dw,
-                                    hipStream_t st) {
+hipError_t launch_wgrad_reduce_s2d3(float* partial, int splits, int K, h16* dw, hipStream_t st) {
+  const int64_t row4 = (int64_t)K * 256 / 4;
+  const int groups = (splits + kFoldGs - 1) / kFoldGs;
+  hipLaunchKernelGGL(wgrad_fold_kernel, dim3((unsigned)((row4 + 63) / 64), groups), dim3(256), 0,
+                     st, partial, splits, row4);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
   hipLaunchKernelGGL(wgrad_reduce_s2d3_kernel, dim3((K * 147 + 255) / 256), dim3(256), 0, st,
-                     partial, splits, K, dw);
+                     partial, groups, (int64_t)kFoldGs * K * 256, K, dw);
   return hipGetLastError();
 }
 

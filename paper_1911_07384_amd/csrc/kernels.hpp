@@ -131,10 +131,10 @@ hipError_t launch_wgrad_reduce(const float* partial, int splits, int K, int Kp, 
                                int C, int Cp, int layout, h16* dw, hipStream_t st);
 // The stem's weight gradient through a 2x2 space-to-depth view (layout.hip,
 // conv_wgrad.hip): the 3-channel image as 16 channels at half resolution, and
-// the 4x4 x 16 partial sums gathered back into the 7x7x3 filter.
+// the 4x4 x 16 partial sums gathered back into the 7x7x3 filter (the splits
+// folded in place in groups first, so partial holds scratch afterwards).
 hipError_t launch_s2d3(const h16* src, h16* dst, int N, int H, int W, hipStream_t st);
-hipError_t launch_wgrad_reduce_s2d3(const float* partial, int splits, int K, h16* dw,
-                                    hipStream_t st);
+hipError_t launch_wgrad_reduce_s2d3(float* partial, int splits, int K, h16* dw, hipStream_t st);
 // Split-K plan of the weight gradient.
 void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int* splits, int* pix_per_split);
 
