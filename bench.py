@@ -107,12 +107,14 @@ def op_work(op, net):
     shortcut, 4 + 2 when its statistics come from the convolution, + 1/8 for
     a kept ReLU mask; BN backward 10 B/element + 4 with the shortcut
     recomputing the mask, + 2 (the shortcut gradient) + 1/4 (the mask, read
-    twice) with a kept mask; SGD 10 B/element)."""
+    twice) with a kept mask; a data gradient's addend 2 B/element + 1/8 under
+    a mask; SGD 10 B/element)."""
     a, k = op.a, op.kind
     if k in ("conv_fwd", "conv_dgrad", "conv_dgrad_add", "conv_wgrad"):
         fl, by = conv_work(a["desc"], {"conv_fwd": "fwd", "conv_wgrad": "wgrad"}.get(k, "dgrad"))
         if k == "conv_dgrad_add":
-            by += 2 * a["desc"].n * a["desc"].c * a["desc"].h * a["desc"].w
+            ex = a["desc"].n * a["desc"].c * a["desc"].h * a["desc"].w
+            by += 2 * ex + (ex // 8 if a.get("amask") else 0)
         return fl, by, "mfma" if fl / by >= RIDGE else "hbm"
     if k == "conv_bn_fwd":
         fl, by = conv_work(a["desc"], "fwd")

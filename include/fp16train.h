@@ -158,6 +158,22 @@ fp16_status fp16_conv_dgrad_filter(const fp16_conv_desc* desc, const fp16_t* w, 
 fp16_status fp16_conv_dgrad_wf(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* wf,
                                const fp16_t* addend, fp16_t* dx, void* ws, size_t ws_bytes,
                                fp16_stream_t stream);
+/* fp16_conv_dgrad_wf with the addend taken under a ReLU mask:
+ *   dx = round_to_binary16(dgrad(dy, W) + (mask ? addend : +0))
+ * where the mask bit of element (n, h, w, c) is bit c % 8 of byte
+ * ((n*H + h)*W + w)*(C/8) + c/8 of addend_mask (the layout fp16_bn_relu_m
+ * keeps, x_elems/8 bytes).  With the addend the gradient a block-last BN
+ * received and the mask its forward kept, this is the block input gradient
+ * of Section 4.1 (branch gradient + the identity shortcut's gradient, which
+ * is the BN's incoming gradient through its ReLU) without that BN's backward
+ * writing the shortcut gradient out.  Bit-identical to fp16_conv_dgrad_wf on
+ * the masked addend.  NHWC with C % 8 == 0 only (FP16_ERR_UNSUPPORTED
+ * otherwise); addend and addend_mask non-null (FP16_ERR_NULL); the mask must
+ * not overlap dx or ws (FP16_ERR_ALIASING); other rules as
+ * fp16_conv_dgrad_wf. */
+fp16_status fp16_conv_dgrad_wf_m(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* wf,
+                                 const fp16_t* addend, const uint8_t* addend_mask, fp16_t* dx,
+                                 void* ws, size_t ws_bytes, fp16_stream_t stream);
 /* fp16_conv_dgrad_filter for `count` convolutions at once (descs[i], w[i],
  * wf[i]; host arrays, read during the call only): every filter of a network
  * rearranged by one launch (or a few) instead of one launch each, with

@@ -255,15 +255,19 @@ fp16_status fp16_conv_fwd(const fp16_conv_desc* desc, const fp16_t* x, const fp1
 static size_t dgrad_filter_bytes(const ConvDims& d) { return (size_t)d.C * d.R * d.S * d.Kp * 2; }
 
 // Data gradient; with wf_given the filter is already rearranged (w is then
-// the rearranged filter, fp16_conv_dgrad_filter_bytes long, NHWC only).
+// the rearranged filter, fp16_conv_dgrad_filter_bytes long, NHWC only); with
+// amask the addend is taken under that ReLU mask (NHWC, C % 8 == 0).
 static fp16_status conv_dgrad_impl(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* w,
                                    const fp16_t* addend, fp16_t* dx, void* ws, size_t ws_bytes,
-                                   fp16_stream_t stream, bool wf_given = false) {
+                                   fp16_stream_t stream, bool wf_given = false,
+                                   const uint8_t* amask = nullptr) {
   ConvDims d;
   fp16_status s = check_conv(desc, &d);
   if (s != FP16_OK) return s;
   if (!dy || !w || !dx) return FP16_ERR_NULL;
   if (wf_given && d.layout != FP16_NHWC) return FP16_ERR_UNSUPPORTED;
+  if (amask && (!addend || d.layout != FP16_NHWC || d.C % 8 != 0 || d.accum))
+    return addend ? FP16_ERR_UNSUPPORTED : FP16_ERR_NULL;
   // the binary16 chains: the plain data gradient from the filter only
   if (d.accum && (wf_given || addend)) return FP16_ERR_UNSUPPORTED;
   if (!aligned16(dy) || !aligned16(w) || !aligned16(dx) || (addend && !aligned16(addend)))
@@ -274,7 +278,8 @@ static fp16_status conv_dgrad_impl(const fp16_conv_desc* desc, const fp16_t* dy,
   const size_t wb = wf_given ? dgrad_filter_bytes(d) : (size_t)d.w_elems * 2;
   if (overlap(dx, xb, dy, (size_t)d.y_elems * 2) || overlap(dx, xb, w, wb) ||
       overlap(dx, xb, ws, L.total) || (addend && addend != dx && overlap(dx, xb, addend, xb)) ||
-      (addend && overlap(addend, xb, ws, L.total)))
+      (addend && overlap(addend, xb, ws, L.total)) ||
+      (amask && (overlap(amask, xb / 16, dx, xb) || overlap(amask, xb / 16, ws, L.total))))
     return FP16_ERR_ALIASING;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const h16* dye = reinterpret_cast<const h16*>(dy);
@@ -306,6 +311,7 @@ static fp16_status conv_dgrad_impl(const fp16_conv_desc* desc, const fp16_t* dy,
   a.stride_h = 1; a.stride_w = 1;
   a.Co = d.C; a.out = dxe; a.OH = d.H; a.OW = d.W; a.ldo = d.C; a.os_h = d.sh; a.os_w = d.sw;
   a.addend = addend ? (d.layout == FP16_NCHW ? dxe : reinterpret_cast<const h16*>(addend)) : nullptr;
+  a.amask = amask;
   a.nphase = 0;
   int64_t off = 0;
   for (int ph = 0; ph < d.sh; ++ph) {
@@ -406,6 +412,13 @@ fp16_status fp16_conv_dgrad_wf(const fp16_conv_desc* desc, const fp16_t* dy, con
                                const fp16_t* addend, fp16_t* dx, void* ws, size_t ws_bytes,
                                fp16_stream_t stream) {
   return conv_dgrad_impl(desc, dy, wf, addend, dx, ws, ws_bytes, stream, true);
+}
+
+fp16_status fp16_conv_dgrad_wf_m(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* wf,
+                                 const fp16_t* addend, const uint8_t* addend_mask, fp16_t* dx,
+                                 void* ws, size_t ws_bytes, fp16_stream_t stream) {
+  if (!addend || !addend_mask) return FP16_ERR_NULL;
+  return conv_dgrad_impl(desc, dy, wf, addend, dx, ws, ws_bytes, stream, true, addend_mask);
 }
 
 }  // extern "C"

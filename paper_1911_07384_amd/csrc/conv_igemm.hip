@@ -55,6 +55,24 @@
 namespace fp16k {
 namespace {
 
+// The addend of the 8 outputs at element offset off (a multiple of 8) under
+// the ReLU mask byte mb of those 8 (bit e for element off + e): an element
+// whose bit is clear adds +0.
+__device__ __forceinline__ V8 masked8(V8 v, uint32_t mb) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v.s[e] = ((mb >> e) & 1u) ? v.s[e] : (uint16_t)0;
+  return v;
+}
+__device__ __forceinline__ V8 addend8(const IgemmArgs& a, int64_t off) {
+  const V8 v = load16(a.addend + off);
+  return a.amask ? masked8(v, a.amask[off >> 3]) : v;
+}
+// one element of the addend, under the mask
+__device__ __forceinline__ float addend1(const IgemmArgs& a, int64_t i) {
+  const float v = to_f32(a.addend[i]);
+  return (a.amask && !((a.amask[i >> 3] >> (i & 7)) & 1u)) ? 0.0f : v;
+}
+
 // keep a value materialised in a VGPR (blocks branchy code motion around it)
 __device__ __forceinline__ uint32_t pin_v(uint32_t x) {
   __asm__("" : "+v"(x));
@@ -273,7 +291,7 @@ __global__ __launch_bounds__(256) void igemm_kernel(const IgemmArgs a) {
         for (int e = 0; e < 8; ++e) v[e] = src[e];
         if (vec_ok) {
           if (a.addend) {
-            const V8 ad = load16(a.addend + off);
+            const V8 ad = addend8(a, off);
 #pragma unroll
             for (int e = 0; e < 8; ++e) v[e] += to_f32(ad.h[e]);
           }
@@ -286,7 +304,7 @@ __global__ __launch_bounds__(256) void igemm_kernel(const IgemmArgs a) {
           for (int e = 0; e < 8; ++e) {
             if (n + e < a.Co) {
               float x = v[e];
-              if (a.addend) x += to_f32(a.addend[off + e]);
+              if (a.addend) x += addend1(a, off + e);
               a.out[off + e] = to_h16(x);
             }
           }
@@ -520,7 +538,7 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
           for (int e = 0; e < 8; ++e) v[e] = src[e];
           if (vec_ok) {
             if (a.addend) {
-              const V8 ad = load16(a.addend + off);
+              const V8 ad = addend8(a, off);
 #pragma unroll
               for (int e = 0; e < 8; ++e) v[e] += to_f32(ad.h[e]);
             }
@@ -541,7 +559,7 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
             for (int e = 0; e < 8; ++e) {
               if (n + e < a.Co) {
                 float x = v[e];
-                if (a.addend) x += to_f32(a.addend[off + e]);
+                if (a.addend) x += addend1(a, off + e);
                 a.out[off + e] = to_h16(x);
               }
             }
@@ -620,7 +638,8 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
 //    instruction split into 32 separate 32-byte writes, and the store path
 //    (not HBM) bounded these layers.  With an addend the float32 sums take
 //    that path instead (the addend joins before the one rounding), and the
-//    addend is read in the same whole-line layout;
+//    addend (and its ReLU mask, one byte per 16-byte chunk) is read in the
+//    same whole-line layout;
 //  - with BN statistics the plain product D = X x W is computed too (the
 //    MFMAs are cheap here), whose layout gives each lane one channel and 16
 //    rows: the band sums are taken in the lane and kept in registers, and the
@@ -657,7 +676,7 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <int CI, int BN, bool STATS, bool ADD>
+template <int CI, int BN, bool STATS, bool ADD, bool MASK>
 __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) {
   using K = CfgPw<CI, BN, STATS, ADD>;
   constexpr int KS = K::KS, TN = K::TN, SW = K::SW;
@@ -665,6 +684,7 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
   constexpr int PPI = 64 / SLOTS;     // pixels per store instruction
   static_assert(CI == 64 || CI == 128, "input channels");
   static_assert(!(STATS && ADD), "statistics are taken without an addend");
+  static_assert(ADD || !MASK, "a mask is over the addend");
   static_assert(TN % SW == 0, "store groups");
   __shared__ __attribute__((aligned(1024))) char lds[K::LDS];
   char* bt = lds;
@@ -724,7 +744,9 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
     const int band_m0 = tile * 128 + wave * 32;
     // the tile's addend, loaded before the MFMAs in the store layout (lane:
     // chunk lane % SLOTS of pixel lane / SLOTS + PPI*i; clamped into range)
+    // (and with MASK the addend's ReLU mask bytes, applied where it is added)
     V8 adv[ADD ? TN / SW : 1][ADD ? 32 / PPI : 1];
+    uint32_t amb[MASK ? TN / SW : 1][MASK ? 32 / PPI : 1];
     if (ADD) {
 #pragma unroll
       for (int g = 0; g < TN / SW; ++g)
@@ -732,7 +754,9 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
         for (int i = 0; i < 32 / PPI; ++i) {
           const int m = band_m0 + lane / SLOTS + i * PPI;
           const int n = n0 + g * SW * 32 + (lane % SLOTS) * 8;
-          adv[g][i] = load16(a.addend + (int64_t)(m < M ? m : M - 1) * a.ldo + (n < a.Co ? n : 0));
+          const int64_t off = (int64_t)(m < M ? m : M - 1) * a.ldo + (n < a.Co ? n : 0);
+          adv[g][i] = load16(a.addend + off);
+          if (MASK) amb[g][i] = a.amask[off >> 3];
         }
     }
     load_a(Anext, row_off(tile + gridDim.x));
@@ -829,8 +853,9 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
             w[4 * j + 2] = f.z;
             w[4 * j + 3] = f.w;
           }
+          const V8 ad = MASK ? masked8(adv[g][i], amb[g][i]) : adv[g][i];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) o.h[e] = to_h16(w[e] + to_f32(adv[g][i].h[e]));
+          for (int e = 0; e < 8; ++e) o.h[e] = to_h16(w[e] + to_f32(ad.h[e]));
         } else {
           o = *reinterpret_cast<const V8*>(stg + (q * SLOTS + (c ^ (q & (SLOTS - 1)))) * 16);
         }
@@ -1260,6 +1285,7 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
     // lane: output pixel m (lane % 32 of each 32-row tile) and, after the
     // swaps, channels 16h + 8*(lane/32) + 0..7 of each 32-channel tile
     V8 adv[TM][TN][2];
+    uint32_t amb[TM][TN][2];
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm) {
       const int m = m0 + wm * 32 * TM + tm * 32 + lrow;
@@ -1280,6 +1306,15 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
             const int n = n0 + wn * 32 * TN + tn * 32 + h * 16 + lhi * 8;
             if (m < M && n + 8 <= a.Co) adv[tm][tn][h] = load16(a.addend + base + n);
           }
+        if (a.amask) {
+#pragma unroll
+          for (int tn = 0; tn < TN; ++tn)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              const int n = n0 + wn * 32 * TN + tn * 32 + h * 16 + lhi * 8;
+              if (m < M && n + 8 <= a.Co) amb[tm][tn][h] = a.amask[(base + n) >> 3];
+            }
+        }
       }
 #pragma unroll
       for (int tn = 0; tn < TN; ++tn) {
@@ -1301,8 +1336,9 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
 #pragma unroll
             for (int e = 0; e < 8; ++e) w[e] = v[h * 8 + e];
             if (a.addend) {
+              const V8 ad = a.amask ? masked8(adv[tm][tn][h], amb[tm][tn][h]) : adv[tm][tn][h];
 #pragma unroll
-              for (int e = 0; e < 8; ++e) w[e] += to_f32(adv[tm][tn][h].h[e]);
+              for (int e = 0; e < 8; ++e) w[e] += to_f32(ad.h[e]);
             }
             V8 o;
 #pragma unroll
@@ -1313,7 +1349,7 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
             for (int e = 0; e < 8; ++e) {
               if (n + e < a.Co) {
                 float x = v[h * 8 + e];
-                if (a.addend) x += to_f32(a.addend[off + e]);
+                if (a.addend) x += addend1(a, off + e);
                 a.out[off + e] = to_h16(x);
               }
             }
@@ -1371,7 +1407,7 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
         for (int e = 0; e < 8; ++e) v[e] = src[e];
         if (vec_ok) {
           if (a.addend) {
-            const V8 ad = load16(a.addend + off);
+            const V8 ad = addend8(a, off);
 #pragma unroll
             for (int e = 0; e < 8; ++e) v[e] += to_f32(ad.h[e]);
           }
@@ -1384,7 +1420,7 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
           for (int e = 0; e < 8; ++e) {
             if (n + e < a.Co) {
               float x = v[e];
-              if (a.addend) x += to_f32(a.addend[off + e]);
+              if (a.addend) x += addend1(a, off + e);
               a.out[off + e] = to_h16(x);
             }
           }
@@ -1506,11 +1542,13 @@ hipError_t launch_pw(const IgemmArgs& a, hipStream_t st) {
   // two to three workgroups per CU walk the tiles
   dim3 grid(ntiles < 512 ? ntiles : 512, ceil_div(a.Co, BN));
   if (a.stat)
-    hipLaunchKernelGGL((pw_kernel<CI, BN, true, false>), grid, dim3(256), 0, st, a, ntiles);
+    hipLaunchKernelGGL((pw_kernel<CI, BN, true, false, false>), grid, dim3(256), 0, st, a, ntiles);
+  else if (a.addend && a.amask)
+    hipLaunchKernelGGL((pw_kernel<CI, BN, false, true, true>), grid, dim3(256), 0, st, a, ntiles);
   else if (a.addend)
-    hipLaunchKernelGGL((pw_kernel<CI, BN, false, true>), grid, dim3(256), 0, st, a, ntiles);
+    hipLaunchKernelGGL((pw_kernel<CI, BN, false, true, false>), grid, dim3(256), 0, st, a, ntiles);
   else
-    hipLaunchKernelGGL((pw_kernel<CI, BN, false, false>), grid, dim3(256), 0, st, a, ntiles);
+    hipLaunchKernelGGL((pw_kernel<CI, BN, false, false, false>), grid, dim3(256), 0, st, a, ntiles);
   return hipGetLastError();
 }
 

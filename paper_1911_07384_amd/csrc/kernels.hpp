@@ -47,6 +47,10 @@ struct IgemmArgs {
   int Co;          // output channels (GEMM N)
   h16* out;        // NHWC output [N][OH][OW][ldo], writes channels [0, Co)
   const h16* addend;  // nullable, laid out like out: out = rne16(acc + addend)
+  // nullable (needs addend, ldo == Co, Co % 8 == 0): a ReLU mask over the
+  // addend, bit (i % 8) of byte i / 8 for element i of out's layout; an
+  // element whose bit is clear adds +0 instead of the addend
+  const uint8_t* amask;
   int OH, OW, ldo;
   int os_h, os_w;
   int nphase;

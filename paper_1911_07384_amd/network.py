@@ -211,18 +211,27 @@ class ResNet50:
     def _bn_op(self, name):
         return next(o for o in self.fwd if o.kind == "bn_fwd" and o.name == name)
 
-    def _bn_bwd(self, name, dy, want_dres):
+    def _bn_bwd(self, name, dy, want_dres, mask_of=None):
+        """The backward of BN `name`; with mask_of, dy is the gradient the BN
+        mask_of received and this BN's output reached mask_of's ReLU through
+        the shortcut, so its incoming gradient is dy under mask_of's kept mask
+        (the call is the ReLU form with that mask)."""
         f = self._bn_op(name).a
         dx = self._grad(f["x"])
-        a = {"desc": f["desc"], "x": f["x"], "y": None, "dy": dy, "res": f["res"],
+        desc, mask = f["desc"], f["mask"]
+        if mask_of is not None:
+            d = desc
+            desc = F.bn_desc(d.n, d.c, d.h, d.w, "NHWC", d.eps, d.post_scale, True)
+            mask = self._bn_op(mask_of).a["mask"]
+        a = {"desc": desc, "x": f["x"], "y": None, "dy": dy, "res": f["res"],
              "stats": f["stats"], "dx": dx, "dgamma": name + ".dgamma", "dbeta": name + ".dbeta",
-             "dres": None, "mask": f["mask"]}
+             "dres": None, "mask": mask, "mask_of": mask_of or name}
         if want_dres:
             a["dres"] = self._grad(f["res"]) if f["res"] is not None else None
         self.bwd.append(Op("bn_bwd", name, a))
         return dx
 
-    def _conv_bwd(self, name, dy, dx_needed=True, addend=None, dx_name=None):
+    def _conv_bwd(self, name, dy, dx_needed=True, addend=None, dx_name=None, mask_of=None):
         c = self._conv_op(name)
         if dx_needed:
             dx = dx_name or self._grad(c["x"])
@@ -236,9 +245,12 @@ class ResNet50:
                 self.bwd.append(Op("conv_dgrad", name, {"desc": c["desc"], "dy": dy, "w": name,
                                                         "wf": wf, "dx": dx}))
             else:
-                self.bwd.append(Op("conv_dgrad_add", name, {"desc": c["desc"], "dy": dy,
-                                                            "w": name, "wf": wf,
-                                                            "addend": addend, "dx": dx}))
+                # with mask_of, the addend is the gradient the BN mask_of
+                # received, taken under that BN's kept ReLU mask
+                self.bwd.append(Op("conv_dgrad_add", name, {
+                    "desc": c["desc"], "dy": dy, "w": name, "wf": wf, "addend": addend,
+                    "amask": self._bn_op(mask_of).a["mask"] if mask_of else None,
+                    "mask_of": mask_of, "dx": dx}))
         self.bwd.append(Op("conv_wgrad", name, {"desc": c["desc"], "x": c["x"], "dy": dy,
                                                 "dw": "d:" + name}))
 
@@ -251,9 +263,13 @@ class ResNet50:
         dout = dlast
         for blk in reversed(self.blocks):
             nm = blk["name"]
-            dc3 = self._bn_bwd(nm + ".bn3", dout, want_dres=True)
-            dres = self._bn_op(nm + ".bn3").a["res"]
-            dres = "d:" + dres
+            # a block-last BN that kept its ReLU mask writes no shortcut
+            # gradient: it is that BN's incoming gradient under the mask, and
+            # its readers (the block input's data gradient, or the shortcut
+            # BN's backward) take it that way
+            kept = self._bn_op(nm + ".bn3").a["mask"] is not None
+            dc3 = self._bn_bwd(nm + ".bn3", dout, want_dres=not kept)
+            dres = "d:" + self._bn_op(nm + ".bn3").a["res"]
             self._conv_bwd(nm + ".c3", dc3)
             dc2 = self._bn_bwd(nm + ".bn2", "d:" + nm + ".bn2.y", want_dres=False)
             self._conv_bwd(nm + ".c2", dc2)
@@ -263,11 +279,16 @@ class ResNet50:
             self.buffers[dxb] = torch.empty(self.buffers[blk["x"]].shape, dtype=torch.float16,
                                             device=self.dev)
             if blk["ds"]:
-                dcd = self._bn_bwd(nm + ".bnd", dres, want_dres=False)
+                if kept:
+                    dcd = self._bn_bwd(nm + ".bnd", dout, want_dres=False, mask_of=nm + ".bn3")
+                else:
+                    dcd = self._bn_bwd(nm + ".bnd", dres, want_dres=False)
                 dsx = "dds:" + nm
                 self.buffers[dsx] = torch.empty_like(self.buffers[dxb])
                 self._conv_bwd(nm + ".ds", dcd, dx_name=dsx)
                 self._conv_bwd(nm + ".c1", dc1, addend=dsx, dx_name=dxb)
+            elif kept:
+                self._conv_bwd(nm + ".c1", dc1, addend=dout, dx_name=dxb, mask_of=nm + ".bn3")
             else:
                 self._conv_bwd(nm + ".c1", dc1, addend=dres, dx_name=dxb)
             dout = dxb
@@ -344,7 +365,12 @@ class ResNet50:
         elif k == "conv_dgrad":
             F.fp16_conv_dgrad_wf(a["desc"], t(a["dy"]), t(a["wf"]), None, t(a["dx"]), ws)
         elif k == "conv_dgrad_add":
-            F.fp16_conv_dgrad_wf(a["desc"], t(a["dy"]), t(a["wf"]), t(a["addend"]), t(a["dx"]), ws)
+            if a["amask"] is None:
+                F.fp16_conv_dgrad_wf(a["desc"], t(a["dy"]), t(a["wf"]), t(a["addend"]), t(a["dx"]),
+                                     ws)
+            else:
+                F.fp16_conv_dgrad_wf_m(a["desc"], t(a["dy"]), t(a["wf"]), t(a["addend"]),
+                                       t(a["amask"]), t(a["dx"]), ws)
         elif k == "dgrad_filter":
             F.fp16_conv_dgrad_filter(a["desc"], t(a["w"]), t(a["wf"]))
         elif k == "dgrad_filters":

@@ -123,6 +123,19 @@ def test_dgrad_filter_validation():
     assert g(ctypes.byref(d), A, B, None, Cc, 0, 0, None) == WORKSPACE
     # dx over the rearranged filter
     assert g(ctypes.byref(d), A, B, None, B + 64, WS, need, None) == ALIASING
+    # the addend under a ReLU mask: dy, wf, addend, mask, dx, ws
+    gm = lib.fp16_conv_dgrad_wf_m
+    M = Cc + (16 << 20)
+    ok = [A, B, Cc + (8 << 20), M, Cc, WS, need, None]
+    assert gm(ctypes.byref(d), *ok[:2], None, *ok[3:]) == NULL
+    assert gm(ctypes.byref(d), *ok[:3], None, *ok[4:]) == NULL
+    assert gm(ctypes.byref(_conv(layout="NCHW")), *ok[:6], 1 << 30, None) == UNSUPPORTED
+    assert gm(ctypes.byref(_conv(c=20)), *ok) == UNSUPPORTED  # C % 8 != 0
+    for at in (Cc, Cc + 2 * 56 * 56 * 64 * 2 - 8, WS):  # the mask under dx or the workspace
+        bad = list(ok)
+        bad[3] = at
+        assert gm(ctypes.byref(d), *bad) == ALIASING, hex(at)
+    assert gm(ctypes.byref(d), *ok[:4], B + 64, WS, need, None) == ALIASING  # dx over wf
 
 
 @pytest.mark.parametrize("hw,r,st,pad", [(56, 3, 1, 1), (56, 1, 2, 0), (224, 7, 2, 3), (7, 3, 1, 1),

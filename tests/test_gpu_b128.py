@@ -25,6 +25,7 @@ import torch
 
 import oracle
 from gpu_util import dev, host, note, require_gpu, ulp_dist
+from test_gpu_network import masked_addend
 from paper_1911_07384_amd import resnet50, synth
 import paper_1911_07384_amd as F
 
@@ -145,7 +146,7 @@ def _conv_sampled(op, H, seed):
         got = H[a["dx"]].reshape(-1)
         idx = _sample_idx(got.size, 500, seed)
         ref = oracle.conv_dgrad_at(shp, H[a["dy"]], H[a["w"]], idx) + \
-            H[a["addend"]].reshape(-1)[idx].astype(np.float64)
+            masked_addend(a, H).reshape(-1)[idx].astype(np.float64)
     else:
         got = H[a["dw"]].reshape(-1)
         idx = _sample_idx(got.size, 500, seed)

@@ -68,6 +68,17 @@ def _small_ok(got, ref16, ref64, what):
     assert ok.all(), what
 
 
+def masked_addend(a, H):
+    """The addend of a block input's data gradient: with a mask, the
+    block-last BN's incoming gradient where that BN's output is positive and
+    +0 elsewhere (the shortcut gradient of Section 4.1 through the ReLU)."""
+    ad = H[a["addend"]]
+    if a.get("amask") is None:
+        return ad
+    pos = H[a["mask_of"] + ".y"].astype(np.float32) > 0
+    return np.where(pos, ad, np.float16(0.0))
+
+
 def _check_op(net, op, H):
     a, k = op.a, op.kind
     what = f"{op.name}:{k}"
@@ -80,7 +91,7 @@ def _check_op(net, op, H):
             ref = oracle.conv_dgrad(shp, H[a["dy"]], H[a["w"]])
             _close(H[a["dx"]], ref[0], what, ref[1])
         elif k == "conv_dgrad_add":
-            ref = oracle.conv_dgrad_add(shp, H[a["dy"]], H[a["w"]], H[a["addend"]])
+            ref = oracle.conv_dgrad_add(shp, H[a["dy"]], H[a["w"]], masked_addend(a, H))
             _close(H[a["dx"]], ref[0], what, ref[1])
         else:
             ref = oracle.conv_wgrad(shp, H[a["x"]], H[a["dy"]])
@@ -109,7 +120,9 @@ def _check_op(net, op, H):
     elif k == "bn_bwd":
         d = a["desc"]
         shp = oracle.bn_shape(d.n, d.c, d.h, d.w)
-        y = H[op.name + ".y"]  # the forward output: the mask the GPU recomputed
+        # the forward output whose ReLU mask applies: this BN's, or (a
+        # downsampling shortcut's BN) the block-last BN's it joined
+        y = H[a["mask_of"] + ".y"]
         ref = oracle.bn_bwd(shp, H[a["x"]], y, H[a["dy"]], H[op.name + ".gamma"], d.eps,
                             d.post_scale, bool(d.relu), want_dres=a["dres"] is not None,
                             swap=bool(d.swap),

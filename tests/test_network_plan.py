@@ -58,7 +58,9 @@ def test_dataflow(net):
     # forward, on the side stream)
     for op in net.prep + net.fwd + net.bwd:
         outs = [k for k in OUTPUTS[op.kind] if op.a.get(k) is not None]
-        reads = [v for k, v in op.a.items() if isinstance(v, str) and k not in outs]
+        # ("mask_of" names a BN, whose kept mask the call reads)
+        reads = [v for k, v in op.a.items()
+                 if isinstance(v, str) and k not in outs and k != "mask_of"]
         if op.kind in ("bn_fwd", "bn_bwd", "conv_bn_fwd"):
             reads += [op.name + ".gamma", op.name + ".beta"]
         for v in reads:
@@ -89,7 +91,26 @@ def test_block_last_bns_keep_their_relu_mask(net):
     assert len(kept) == 16 and all(n.endswith(".bn3") for n in kept)
     for o in net.bwd:
         if o.kind == "bn_bwd":
-            assert o.a["mask"] == fwd[o.name].a["mask"]
+            assert o.a["mask"] == fwd[o.a["mask_of"]].a["mask"]
+            # no block-last BN writes its shortcut gradient: the downsampling
+            # shortcut's BN takes the block-last BN's gradient under its mask
+            assert o.a["dres"] is None
+            if o.name.endswith(".bnd"):
+                assert o.a["mask_of"] == o.name[:-4] + ".bn3" and o.a["desc"].relu == 1
+            else:
+                assert o.a["mask_of"] == o.name
+    # the identity blocks' input gradients add the block-last BN's incoming
+    # gradient under its mask
+    adds = {o.name: o for o in net.bwd if o.kind == "conv_dgrad_add"}
+    assert len(adds) == 16
+    for nm, o in adds.items():
+        blk = nm[:-3]
+        if blk.endswith(".0"):
+            assert o.a["amask"] is None and o.a["addend"] == "dds:" + blk
+        else:
+            bn3 = [b for b in net.bwd if b.kind == "bn_bwd" and b.name == blk + ".bn3"][0]
+            assert o.a["amask"] == fwd[blk + ".bn3"].a["mask"]
+            assert o.a["addend"] == bn3.a["dy"]
     swapped = ResNet50(n=1, image=64, device="cpu", bn_swap=True)
     assert all(o.a["mask"] is None for o in swapped.fwd if o.kind in ("bn_fwd", "conv_bn_fwd"))
 
