@@ -108,7 +108,8 @@ def op_work(op, net):
     a kept ReLU mask; BN backward 10 B/element + 4 with the shortcut
     recomputing the mask, + 2 (the shortcut gradient) + 1/4 (the mask, read
     twice) with a kept mask; a data gradient's addend 2 B/element + 1/8 under
-    a mask; SGD 10 B/element)."""
+    a mask; the BN fused into the max pool 4 B per input element + 3 per
+    pooled element; SGD 10 B/element)."""
     a, k = op.a, op.kind
     if k in ("conv_fwd", "conv_dgrad", "conv_dgrad_add", "conv_wgrad"):
         fl, by = conv_work(a["desc"], {"conv_fwd": "fwd", "conv_wgrad": "wgrad"}.get(k, "dgrad"))
@@ -138,6 +139,11 @@ def op_work(op, net):
         d = a["desc"]
         p, q = (d.h + 2 * d.pad_h - d.r) // d.stride_h + 1, (d.w + 2 * d.pad_w - d.s) // d.stride_w + 1
         return 0, 2 * d.n * d.c * d.h * d.w + 3 * d.n * d.c * p * q, "hbm"
+    if k == "bn_maxpool_fwd":
+        d, pd = a["desc"], a["pool"]
+        e = bn_elems(d)
+        p, q = (pd.h + 2 * pd.pad_h - pd.r) // pd.stride_h + 1, (pd.w + 2 * pd.pad_w - pd.s) // pd.stride_w + 1
+        return 0, 4 * e + 3 * pd.n * pd.c * p * q, "hbm"
     if k == "maxpool_bwd":
         d = a["desc"]
         p, q = (d.h + 2 * d.pad_h - d.r) // d.stride_h + 1, (d.w + 2 * d.pad_w - d.s) // d.stride_w + 1

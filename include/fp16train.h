@@ -389,6 +389,24 @@ fp16_status fp16_maxpool_fwd(const fp16_pool_desc* desc, const fp16_t* x, fp16_t
 fp16_status fp16_maxpool_bwd(const fp16_pool_desc* desc, const uint8_t* idx, const fp16_t* dy,
                              fp16_t* dx, fp16_stream_t stream);
 
+/* BN + ReLU whose output only feeds a max pool (ResNet-50's stem BN, Section
+ * 5.1, and the 3x3 stride-2 pool after it), in one pass that never writes the
+ * BN output: y and idx are bit for bit those of
+ *   fp16_bn_relu(bn, x, gamma, beta, NULL, z, stats, ws) then
+ *   fp16_maxpool_fwd(pool, z, y, idx)
+ * and stats is written (or read, with bn->use_stats) as fp16_bn_relu does.
+ * The backward needs only x, stats and idx: fp16_bn_relu_bwd recomputes the
+ * ReLU mask from x (y = NULL).  Taken: NHWC, bn->relu = 1, no BN swap, C a
+ * multiple of 8 with C/8 a power of two <= 256, a 3x3 pool window
+ * (FP16_ERR_UNSUPPORTED otherwise); the pool descriptor's n, c, h, w and
+ * layout equal the BN's (FP16_ERR_SHAPE otherwise).  Workspace:
+ * fp16_bn_workspace_bytes(bn).  y, idx and the workspace must not overlap x,
+ * gamma, beta, stats or each other (FP16_ERR_ALIASING). */
+fp16_status fp16_bn_relu_maxpool(const fp16_bn_desc* bn, const fp16_pool_desc* pool,
+                                 const fp16_t* x, const fp16_t* gamma, const fp16_t* beta,
+                                 float* stats, fp16_t* y, uint8_t* idx, void* ws, size_t ws_bytes,
+                                 fp16_stream_t stream);
+
 /* Global average pooling (before ResNet-50's classifier): the window must be
  * the whole image (r = h, s = w, pads 0; FP16_ERR_UNSUPPORTED otherwise).
  *   y[n,c] = (sum over the H x W grid of x[n,c,.,.]) / (H*W)

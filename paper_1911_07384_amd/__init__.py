@@ -36,7 +36,7 @@ EXPORTS = ["fp16_conv_out_dims", "fp16_conv_workspace_bytes", "fp16_conv_fwd", "
            "fp16_conv_dgrad_filters",
            "fp16_conv_dgrad_wf", "fp16_noalloc_scratch_bytes", "fp16_conv_wgrad_noalloc",
            "fp16_bn_mask_bytes", "fp16_bn_relu_m", "fp16_bn_relu_bwd_m", "fp16_conv_bn_relu_fwd_m",
-           "fp16_conv_dgrad_wf_m"]
+           "fp16_conv_dgrad_wf_m", "fp16_bn_relu_maxpool"]
 
 
 class Fp16Error(RuntimeError):
@@ -82,6 +82,7 @@ _SIGS = {
     "fp16_conv_dgrad_filters": (ctypes.c_int, [ctypes.c_int32, _P, _P, _P, _P]),
     "fp16_conv_dgrad_wf": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_conv_dgrad_wf_m": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "fp16_bn_relu_maxpool": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_bn_workspace_bytes": (_SZ, [_P]),
     "fp16_bn_mask_bytes": (_SZ, [_P]),
     "fp16_bn_relu_m": (ctypes.c_int, [_P] * 9 + [_SZ, _P]),
@@ -322,6 +323,13 @@ def fp16_pool_out_dims(desc: PoolDesc):
 def fp16_maxpool_fwd(desc, x, y, idx, stream=None) -> None:
     _check("fp16_maxpool_fwd", lib().fp16_maxpool_fwd(ctypes.byref(desc), _ptr(x), _ptr(y),
                                                       _ptr(idx), _stream(stream)))
+
+
+def fp16_bn_relu_maxpool(bn, pool, x, gamma, beta, stats, y, idx, ws=None, ws_bytes=None,
+                         stream=None) -> None:
+    _check("fp16_bn_relu_maxpool", lib().fp16_bn_relu_maxpool(
+        ctypes.byref(bn), ctypes.byref(pool), _ptr(x), _ptr(gamma), _ptr(beta), _ptr(stats),
+        _ptr(y), _ptr(idx), _ptr(ws), _wsb(ws, ws_bytes), _stream(stream)))
 
 
 def fp16_maxpool_bwd(desc, idx, dy, dx, stream=None) -> None:

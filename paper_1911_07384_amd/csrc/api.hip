@@ -735,6 +735,42 @@ fp16_status fp16_maxpool_bwd(const fp16_pool_desc* desc, const uint8_t* idx, con
                                        static_cast<hipStream_t>(stream)));
 }
 
+fp16_status fp16_bn_relu_maxpool(const fp16_bn_desc* bn, const fp16_pool_desc* pool,
+                                 const fp16_t* x, const fp16_t* gamma, const fp16_t* beta,
+                                 float* stats, fp16_t* y, uint8_t* idx, void* ws, size_t ws_bytes,
+                                 fp16_stream_t stream) {
+  BnArgs b;
+  PoolArgs pa;
+  fp16_status s = check_bn(bn, &b);
+  if (s != FP16_OK) return s;
+  if ((s = check_pool(pool, &pa)) != FP16_OK) return s;
+  if (!x || !gamma || !beta || !stats || !y || !idx) return FP16_ERR_NULL;
+  if (pa.N != b.N || pa.C != b.C || pa.H != b.H || pa.W != b.W || pa.layout != b.layout)
+    return FP16_ERR_SHAPE;
+  if (!bn_maxpool_ok(b, pa)) return FP16_ERR_UNSUPPORTED;
+  if (!aligned16(x) || !aligned16(y) || !aligned16(idx) || !aligned16(stats))
+    return FP16_ERR_MISALIGNED;
+  const size_t need = bn_ws_bytes(b);
+  if (!ws || ws_bytes < need) return FP16_ERR_WORKSPACE;
+  if (!aligned16(ws)) return FP16_ERR_MISALIGNED;
+  const size_t eb = (size_t)b.N * b.C * b.H * b.W * 2, cb = (size_t)b.C * 2,
+               sb = (size_t)b.C * 8;
+  const size_t yn = (size_t)pa.N * pa.C * pa.P * pa.Q;
+  const void* ins[4] = {x, gamma, beta, stats};
+  const size_t insz[4] = {eb, cb, cb, sb};
+  for (int i = 0; i < 4; ++i)
+    if (overlap(y, yn * 2, ins[i], insz[i]) || overlap(idx, yn, ins[i], insz[i]) ||
+        (i < 3 && overlap(ws, need, ins[i], insz[i])))
+      return FP16_ERR_ALIASING;
+  if (overlap(y, yn * 2, idx, yn) || overlap(y, yn * 2, ws, need) || overlap(idx, yn, ws, need) ||
+      overlap(stats, sb, ws, need))
+    return FP16_ERR_ALIASING;
+  return hip_status(launch_bn_fwd_maxpool(
+      b, pa, reinterpret_cast<const h16*>(x), reinterpret_cast<const h16*>(gamma),
+      reinterpret_cast<const h16*>(beta), stats, bn->use_stats, ws, reinterpret_cast<h16*>(y),
+      idx, static_cast<hipStream_t>(stream)));
+}
+
 // The global window only.  With r, s <= 15 the window holds at most 225
 // binary16 terms, so every float64 sum of them is exact (|sum| < 2^24 in
 // units of 2^-24 fits in 53 bits).

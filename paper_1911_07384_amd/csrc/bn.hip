@@ -871,6 +871,90 @@ __global__ __launch_bounds__(kT) void bn_bwd_apply_gen(const h16* x, const h16* 
   }
 }
 
+// ---- forward apply fused into the max pool that reads it ----------------------
+// The apply + ReLU (no shortcut, no swap) evaluated inside the R x S max pool
+// over its output: per pooled output vector (8 channels of one position)
+// every input of the window is normalised with the apply's float32 sequence
+// and rounded to binary16, then pooled with max pooling's comparison (the
+// first in-image tap in row-major order starts; a later one replaces it only
+// when strictly larger, or as the first NaN), so the pooled values and tap
+// indices are bit for bit those of the apply followed by the pool, and the
+// normalised tensor is never written.  All R*S loads of a vector are issued
+// before the first use (clamped into the image; a tap outside it is no
+// candidate).  Grid-stride over output vectors; kT and the stride are
+// multiples of C/8, so a thread keeps one channel chunk and its coefficients.
+template <int R, int S>
+__global__ __launch_bounds__(kT) void bn_apply_maxpool_vec(const h16* __restrict__ x,
+                                                           const h16* __restrict__ gamma,
+                                                           const h16* __restrict__ beta,
+                                                           const float* __restrict__ stats,
+                                                           float s, PoolArgs a,
+                                                           h16* __restrict__ y,
+                                                           uint8_t* __restrict__ idx) {
+  const int CV = a.C / 8;
+  const int j = threadIdx.x % CV;
+  FwdCoef k[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) k[e] = fwd_coef(stats, gamma, beta, a.C, j * 8 + e, s);
+  const int64_t total = (int64_t)a.N * a.P * a.Q * CV;
+  for (int64_t v = (int64_t)blockIdx.x * kT + threadIdx.x; v < total;
+       v += (int64_t)gridDim.x * kT) {
+    int64_t r = v / CV;
+    const int q = (int)(r % a.Q);
+    r /= a.Q;
+    const int p = (int)(r % a.P);
+    const int n = (int)(r / a.P);
+    const int h0 = p * a.sh - a.ph, w0 = q * a.sw - a.pw;
+    const h16* xb = x + (int64_t)n * a.H * a.W * a.C + j * 8;
+    V8 xv[R][S];
+#pragma unroll
+    for (int rr = 0; rr < R; ++rr)
+#pragma unroll
+      for (int ss = 0; ss < S; ++ss) {
+        const int h = h0 + rr, w = w0 + ss;
+        const int hc = h < 0 ? 0 : (h < a.H ? h : a.H - 1);
+        const int wc = w < 0 ? 0 : (w < a.W ? w : a.W - 1);
+        xv[rr][ss] = load16(xb + ((int64_t)hc * a.W + wc) * a.C);
+      }
+    __builtin_amdgcn_sched_barrier(0);  // every load issued before the first use
+    float best[8];
+    int tap[8];
+    V8 win;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      best[e] = 0.0f;
+      tap[e] = 0;
+      win.s[e] = 0;
+    }
+    bool started = false;
+#pragma unroll
+    for (int rr = 0; rr < R; ++rr)
+#pragma unroll
+      for (int ss = 0; ss < S; ++ss) {
+        const int h = h0 + rr, w = w0 + ss;
+        const bool in = h >= 0 && h < a.H && w >= 0 && w < a.W;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const h16 z = to_h16(fwd_value(to_f32(xv[rr][ss].h[e]), k[e], false, 0.0f, true, false));
+          const float f = to_f32(z);
+          const bool tk = in && (!started || pool_takes(best[e], f));
+          best[e] = tk ? f : best[e];
+          win.h[e] = tk ? z : win.h[e];
+          tap[e] = tk ? rr * S + ss : tap[e];
+        }
+        started = started || in;
+      }
+    uint32_t lo = 0, hi = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      lo |= (uint32_t)tap[e] << (8 * e);
+      hi |= (uint32_t)tap[e + 4] << (8 * e);
+    }
+    store16(y + v * 8, win);
+    *reinterpret_cast<uint2*>(idx + v * 8) = make_uint2(lo, hi);
+  }
+}
+
 unsigned apply_grid(int64_t nthreads_wanted, int CV) {
   int64_t b = (nthreads_wanted + kT - 1) / kT;
   if (b > 16384) b = 16384;
@@ -955,25 +1039,28 @@ size_t bn_keep_mask_bytes(const BnArgs& a) {
   return p.vec && a.relu ? (size_t)((int64_t)a.N * a.H * a.W * p.CV) : 0;
 }
 
+// The batch statistics of x into stats (the partial sums in ws).
+static void bn_fwd_stats(const BnArgs& a, const Plan& p, const Geo& g, const h16* x, float* stats,
+                         void* ws, hipStream_t st) {
+  float* part = reinterpret_cast<float*>(ws);
+  if (p.vec)
+    hipLaunchKernelGGL(bn_fwd_reduce_vec, dim3(p.G), dim3(kT), 0, st, x, g, p.CV, p.RB, p.rpb,
+                       part);
+  else
+    hipLaunchKernelGGL(bn_fwd_reduce_gen, dim3(p.G, a.C), dim3(kT), 0, st, x, g, p.rpb, part);
+  if (p.vec && a.C >= kBmC)
+    hipLaunchKernelGGL(bn_fwd_finalize_bm, dim3((a.C + 63) / 64), dim3(64 * kFinW), 0, st, x, g,
+                       p.G, part, a.eps, stats);
+  else
+    hipLaunchKernelGGL(bn_fwd_finalize, dim3(a.C), dim3(64), 0, st, x, g, p.G, part, a.eps, stats);
+}
+
 hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const h16* beta,
                          const h16* res, h16* y, float* stats, int use_stats, void* ws,
                          uint8_t* mout, hipStream_t st) {
   const Plan p = make_plan(a);
   const Geo g = make_geo(a);
-  float* part = reinterpret_cast<float*>(ws);
-  if (!use_stats) {
-    if (p.vec)
-      hipLaunchKernelGGL(bn_fwd_reduce_vec, dim3(p.G), dim3(kT), 0, st, x, g, p.CV, p.RB, p.rpb,
-                         part);
-    else
-      hipLaunchKernelGGL(bn_fwd_reduce_gen, dim3(p.G, a.C), dim3(kT), 0, st, x, g, p.rpb, part);
-    if (p.vec && a.C >= kBmC)
-      hipLaunchKernelGGL(bn_fwd_finalize_bm, dim3((a.C + 63) / 64), dim3(64 * kFinW), 0, st, x, g,
-                         p.G, part, a.eps, stats);
-    else
-      hipLaunchKernelGGL(bn_fwd_finalize, dim3(a.C), dim3(64), 0, st, x, g, p.G, part, a.eps,
-                         stats);
-  }
+  if (!use_stats) bn_fwd_stats(a, p, g, x, stats, ws, st);
   if (p.vec) {
     const hipError_t e =
         launch_fwd_apply_vec(fwd_mode(a, res, mout != nullptr), p, g, x, gamma, beta, res, y, stats,
@@ -983,6 +1070,23 @@ hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const 
     hipLaunchKernelGGL(bn_fwd_apply_gen, dim3(apply_grid(g.M * a.C / 4, 1)), dim3(kT), 0, st, x,
                        gamma, beta, res, y, stats, g, a.post_scale, a.relu);
   }
+  return hipGetLastError();
+}
+
+bool bn_maxpool_ok(const BnArgs& a, const PoolArgs& pa) {
+  return make_plan(a).vec && a.relu && !a.swap && pa.layout == 0 && pa.N == a.N &&
+         pa.C == a.C && pa.H == a.H && pa.W == a.W && pa.R == 3 && pa.S == 3;
+}
+
+hipError_t launch_bn_fwd_maxpool(const BnArgs& a, const PoolArgs& pa, const h16* x,
+                                 const h16* gamma, const h16* beta, float* stats, int use_stats,
+                                 void* ws, h16* y, uint8_t* idx, hipStream_t st) {
+  const Plan p = make_plan(a);
+  const Geo g = make_geo(a);
+  if (!use_stats) bn_fwd_stats(a, p, g, x, stats, ws, st);
+  const int64_t total = (int64_t)pa.N * pa.P * pa.Q * (pa.C / 8);
+  hipLaunchKernelGGL((bn_apply_maxpool_vec<3, 3>), dim3(apply_grid(total, p.CV)), dim3(kT), 0, st,
+                     x, gamma, beta, stats, a.post_scale, pa, y, idx);
   return hipGetLastError();
 }
 

@@ -62,6 +62,13 @@ __device__ __forceinline__ h16 dbl_to_h16(double d) {
   return (h16)f;
 }
 
+// Max pooling's comparison: a later element replaces the running maximum
+// only if it is strictly larger, or if it is the first NaN (NaN propagates;
+// ties keep the earliest position).
+__device__ __forceinline__ bool pool_takes(float best, float v) {
+  return !__builtin_isnan(best) && (__builtin_isnan(v) || v > best);
+}
+
 // ReLU keeping NaN and mapping -0 and negatives to +0.
 __device__ __forceinline__ float relu_keep_nan(float v) {
   return (v > 0.0f || __builtin_isnan(v)) ? v : 0.0f;

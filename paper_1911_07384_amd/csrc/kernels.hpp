@@ -188,6 +188,15 @@ hipError_t launch_maxpool_fwd(const PoolArgs& a, const h16* x, h16* y, uint8_t* 
                               hipStream_t st);
 hipError_t launch_maxpool_bwd(const PoolArgs& a, const uint8_t* idx, const h16* dy, h16* dx,
                               hipStream_t st);
+// BN forward (batch statistics unless use_stats, ReLU, no shortcut) whose
+// output goes straight into a 3x3 max pool (bn.hip): y and idx as
+// launch_maxpool_fwd on the BN output, which is not written.  bn_maxpool_ok
+// says whether the pair is taken (NHWC, the BN's vectorised path, 3x3 window
+// over the BN's tensor).
+bool bn_maxpool_ok(const BnArgs& a, const PoolArgs& pa);
+hipError_t launch_bn_fwd_maxpool(const BnArgs& a, const PoolArgs& pa, const h16* x,
+                                 const h16* gamma, const h16* beta, float* stats, int use_stats,
+                                 void* ws, h16* y, uint8_t* idx, hipStream_t st);
 hipError_t launch_avgpool_fwd(const PoolArgs& a, const h16* x, h16* y, hipStream_t st);
 hipError_t launch_avgpool_bwd(const PoolArgs& a, const h16* dy, h16* dx, hipStream_t st);
 

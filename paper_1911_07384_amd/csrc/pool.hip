@@ -18,12 +18,6 @@ namespace {
 
 constexpr int kPT = 256;
 
-// A later element replaces the running maximum only if it is strictly larger,
-// or if it is the first NaN (NaN propagates; ties keep the earliest position).
-__device__ __forceinline__ bool takes(float best, float v) {
-  return !__builtin_isnan(best) && (__builtin_isnan(v) || v > best);
-}
-
 // First tap of a window that lies inside the image (windows are never empty).
 __device__ __forceinline__ int first_tap(int o, int st, int pad) {
   const int lo = o * st - pad;
@@ -77,7 +71,7 @@ __global__ __launch_bounds__(kPT) void maxpool_fwd_vec(const h16* __restrict__ x
 #pragma unroll
         for (int e = 0; e < 8; ++e) {
           const float f = to_f32(xv.h[e]);
-          const bool tk = takes(best[e], f);
+          const bool tk = pool_takes(best[e], f);
           best[e] = tk ? f : best[e];
           win.s[e] = tk ? xv.s[e] : win.s[e];
           tap[e] = tk ? t : tap[e];
@@ -122,7 +116,7 @@ __global__ __launch_bounds__(kPT) void maxpool_fwd_gen(const h16* __restrict__ x
         if (w >= a.W) break;
         const h16 xv = x[act_at(a, n, c, h, w)];
         const float f = to_f32(xv);
-        const bool tk = takes(best, f);
+        const bool tk = pool_takes(best, f);
         best = tk ? f : best;
         win = tk ? xv : win;
         tap = tk ? rr * a.S + ss : tap;

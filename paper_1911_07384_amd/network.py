@@ -173,7 +173,38 @@ class ResNet50:
         self._last = xname
         self._plan_backward(gd, pd)
         if self.fuse:
+            self._fuse_bn_pool()
             self._fuse_conv_bn()
+
+    def _fuse_bn_pool(self):
+        """A BN + ReLU whose output only feeds the max pool that follows it
+        (the stem's) becomes one fp16_bn_relu_maxpool call: the BN output is
+        never written (its backward recomputes the ReLU mask from the BN input
+        and the statistics), so its buffer is dropped."""
+        out, i = [], 0
+        while i < len(self.fwd):
+            op = self.fwd[i]
+            nxt = self.fwd[i + 1] if i + 1 < len(self.fwd) else None
+            if (op.kind == "bn_fwd" and nxt is not None and nxt.kind == "maxpool_fwd"
+                    and nxt.a["x"] == op.a["y"] and op.a["res"] is None and op.a["mask"] is None
+                    and op.a["desc"].relu and not self._reads_elsewhere(op.a["y"], nxt)):
+                out.append(Op("bn_maxpool_fwd", op.name,
+                              {"desc": op.a["desc"], "pool": nxt.a["desc"], "x": op.a["x"],
+                               "stats": op.a["stats"], "y": nxt.a["y"], "idx": nxt.a["idx"]}))
+                del self.buffers[op.a["y"]]
+                i += 2
+            else:
+                out.append(op)
+                i += 1
+        self.fwd = out
+
+    def _reads_elsewhere(self, buf, but):
+        """Whether any call of the step other than `but` reads buffer `buf`."""
+        for op in self.fwd + self.bwd:
+            if op is not but and any(isinstance(v, str) and v == buf and
+                                     k not in self._OUTPUTS[op.kind] for k, v in op.a.items()):
+                return True
+        return False
 
     def _fuse_conv_bn(self):
         """Each conv whose next forward call is the BN of its output becomes
@@ -408,6 +439,10 @@ class ResNet50:
                                      t(a["dgamma"]), t(a["dbeta"]), t(a["dres"]), ws)
         elif k == "maxpool_fwd":
             F.fp16_maxpool_fwd(a["desc"], t(a["x"]), t(a["y"]), t(a["idx"]))
+        elif k == "bn_maxpool_fwd":
+            nm = op.name
+            F.fp16_bn_relu_maxpool(a["desc"], a["pool"], t(a["x"]), t(nm + ".gamma"),
+                                   t(nm + ".beta"), t(a["stats"]), t(a["y"]), t(a["idx"]), ws)
         elif k == "maxpool_bwd":
             F.fp16_maxpool_bwd(a["desc"], t(a["idx"]), t(a["dy"]), t(a["dx"]))
         elif k == "avgpool_fwd":
@@ -437,6 +472,7 @@ class ResNet50:
                 "conv_wgrad": ("dw",), "bn_fwd": ("y", "stats", "mask"),
                 "bn_bwd": ("dx", "dgamma", "dbeta", "dres"), "maxpool_fwd": ("y", "idx"),
                 "maxpool_bwd": ("dx",), "avgpool_fwd": ("y",), "avgpool_bwd": ("dx",),
+                "bn_maxpool_fwd": ("stats", "y", "idx"),
                 "softmax_ce": ("loss", "dz", "dbias"), "dgrad_filter": ("wf",)}
 
     def _schedule(self):

@@ -418,6 +418,39 @@ def test_kept_mask_validation():
                                        WS, need, None) == ALIASING  # mask inside z
 
 
+def test_bn_relu_maxpool_validation():
+    lib = F.lib()
+    f = lib.fp16_bn_relu_maxpool
+    bd = F.bn_desc(2, 64, 112, 112)
+    pd = F.pool_desc(2, 64, 112, 112, 3, 3, 2, 1)
+    need = F.fp16_bn_workspace_bytes(bd)
+    # x, gamma, beta, stats, y, idx, ws
+    ok = [A, B, B + 256, B + 512, Cc, Cc + (8 << 20), WS, need, None]
+    r = lambda b=bd, p=pd, args=ok: f(ctypes.byref(b), ctypes.byref(p), *args)
+    assert f(None, ctypes.byref(pd), *ok) == NULL
+    assert f(ctypes.byref(bd), None, *ok) == NULL
+    for i in range(6):
+        bad = list(ok)
+        bad[i] = None
+        assert r(args=bad) == NULL, i
+    assert r(p=F.pool_desc(2, 64, 112, 110, 3, 3, 2, 1)) == SHAPE     # not the BN's tensor
+    assert r(p=F.pool_desc(2, 64, 112, 112, 2, 2, 2, 0)) == UNSUPPORTED  # 2x2 window
+    for b in (F.bn_desc(2, 64, 112, 112, relu=False), F.bn_desc(2, 64, 112, 112, swap=True),
+              F.bn_desc(2, 24, 112, 112)):
+        assert r(b=b, p=F.pool_desc(b.n, b.c, b.h, b.w, 3, 3, 2, 1)) == UNSUPPORTED
+    nb, npd = F.bn_desc(2, 64, 112, 112, "NCHW"), F.pool_desc(2, 64, 112, 112, 3, 3, 2, 1, "NCHW")
+    assert r(b=nb, p=npd) == UNSUPPORTED
+    bad = list(ok)
+    bad[4] = Cc + 8
+    assert r(args=bad) == MISALIGNED
+    assert r(args=ok[:6] + [WS, need - 16, None]) == WORKSPACE
+    # y over x, idx over y, the workspace over stats
+    for i, at in ((4, A + 64), (5, Cc + 64), (6, B)):
+        bad = list(ok)
+        bad[i] = at
+        assert r(args=bad) == ALIASING, i
+
+
 def test_dgrad_filters_validation():
     lib = F.lib()
     assert lib.fp16_conv_dgrad_filters(0, None, None, None, None) == OK  # nothing to do

@@ -194,7 +194,7 @@ def test_resnet50_step_b128_teacher_forced(net_b128, group):
         kinds.add(op.kind)
         del H
     if group == "stem+pool+head":
-        assert {"conv_bn_fwd", "maxpool_fwd", "maxpool_bwd", "avgpool_fwd", "avgpool_bwd",
+        assert {"bn_maxpool_fwd", "maxpool_bwd", "avgpool_fwd", "avgpool_bwd",
                 "softmax_ce", "bn_bwd", "conv_wgrad", "conv_fwd", "conv_dgrad"} <= kinds, kinds
     else:
         assert {"conv_bn_fwd", "bn_bwd", "conv_wgrad", "conv_dgrad_add"} <= kinds, kinds

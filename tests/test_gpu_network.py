@@ -68,6 +68,20 @@ def _small_ok(got, ref16, ref64, what):
     assert ok.all(), what
 
 
+def bn_out(net, name, H):
+    """The forward output of BN `name`: its buffer, or, where the step never
+    writes it (the stem BN, which feeds the max pool directly), the declared
+    apply recomputed from the BN's input and the statistics it wrote."""
+    if name + ".y" in net.buffers:
+        return H[name + ".y"]
+    f = next(o for o in net.fwd if o.name == name)
+    d = f.a["desc"]
+    st = H[f.a["stats"]]
+    return oracle.bn_apply_f32(oracle.bn_shape(d.n, d.c, d.h, d.w), H[f.a["x"]],
+                               H[name + ".gamma"], H[name + ".beta"], st[:d.c], st[d.c:], None,
+                               d.post_scale, bool(d.relu))
+
+
 def masked_addend(a, H):
     """The addend of a block input's data gradient: with a mask, the
     block-last BN's incoming gradient where that BN's output is positive and
@@ -122,7 +136,7 @@ def _check_op(net, op, H):
         shp = oracle.bn_shape(d.n, d.c, d.h, d.w)
         # the forward output whose ReLU mask applies: this BN's, or (a
         # downsampling shortcut's BN) the block-last BN's it joined
-        y = H[a["mask_of"] + ".y"]
+        y = bn_out(net, a["mask_of"], H)
         ref = oracle.bn_bwd(shp, H[a["x"]], y, H[a["dy"]], H[op.name + ".gamma"], d.eps,
                             d.post_scale, bool(d.relu), want_dres=a["dres"] is not None,
                             swap=bool(d.swap),
@@ -132,14 +146,29 @@ def _check_op(net, op, H):
         _small_ok(H[a["dbeta"]], ref["dbeta"], ref["dbeta64"], what + " dbeta")
         if a["dres"] is not None:
             assert np.array_equal(H[a["dres"]].view(np.uint16), ref["dres"].view(np.uint16)), what
+    elif k == "bn_maxpool_fwd":
+        d = a["desc"]
+        shp = oracle.bn_shape(d.n, d.c, d.h, d.w)
+        g, b, st = H[op.name + ".gamma"], H[op.name + ".beta"], H[a["stats"]]
+        # bit for bit the declared apply with the statistics the call wrote,
+        # pooled; within 1 ulp of the oracle's own BN, pooled
+        z = oracle.bn_apply_f32(shp, H[a["x"]], g, b, st[:d.c], st[d.c:], None, d.post_scale,
+                                bool(d.relu))
+        y, idx = oracle.maxpool_fwd(_pool_shape(a["pool"]), z)
+        assert np.array_equal(H[a["y"]].view(np.uint16), y.view(np.uint16)), what
+        assert np.array_equal(H[a["idx"]], idx), what
+        ref = oracle.bn_fwd(shp, H[a["x"]], g, b, None, d.eps, d.post_scale, bool(d.relu))
+        y2, _ = oracle.maxpool_fwd(_pool_shape(a["pool"]), ref["y"])
+        assert ulp_dist(H[a["y"]], y2).max() <= 1, what
     elif k == "maxpool_fwd":
         y, idx = oracle.maxpool_fwd(_pool_shape(a["desc"]), H[a["x"]])
         assert np.array_equal(H[a["y"]].view(np.uint16), y.view(np.uint16)), what
         assert np.array_equal(H[a["idx"]], idx), what
     elif k == "maxpool_bwd":
         # the oracle re-derives the winners from the forward input
-        fx = next(o for o in net.fwd if o.kind == "maxpool_fwd").a["x"]
-        dx = oracle.maxpool_bwd(_pool_shape(a["desc"]), H[fx], H[a["dy"]])
+        f = next(o for o in net.fwd if o.kind in ("maxpool_fwd", "bn_maxpool_fwd"))
+        px = H[f.a["x"]] if f.kind == "maxpool_fwd" else bn_out(net, f.name, H)
+        dx = oracle.maxpool_bwd(_pool_shape(a["desc"]), px, H[a["dy"]])
         assert np.array_equal(H[a["dx"]].view(np.uint16), dx.view(np.uint16)), what
     elif k == "avgpool_fwd":
         d = a["desc"]
@@ -173,10 +202,9 @@ def test_every_call_matches_the_oracle_on_its_own_inputs(variant):
     for op in net.fwd + net.bwd:
         _check_op(net, op, H)
         kinds.add(op.kind)
-    fused = {"conv_bn_fwd"} if net.fuse else {"bn_fwd"}
+    fused = {"conv_bn_fwd", "bn_maxpool_fwd"} if net.fuse else {"bn_fwd", "maxpool_fwd"}
     assert kinds == {"conv_fwd", "conv_dgrad", "conv_dgrad_add", "conv_wgrad", "bn_bwd",
-                     "maxpool_fwd", "maxpool_bwd", "avgpool_fwd", "avgpool_bwd",
-                     "softmax_ce"} | fused
+                     "maxpool_bwd", "avgpool_fwd", "avgpool_bwd", "softmax_ce"} | fused
     assert len([o for o in net.fwd if o.kind in ("conv_fwd", "conv_bn_fwd")]) == 54
     # the update, bit-exact against the declared float32 sequence
     w0, m0 = host(net.w_arena).copy(), host(net.mw_arena).copy()

@@ -172,3 +172,67 @@ def test_softmax_ce_in_place():
     F.fp16_softmax_ce(n, k, zz, dev(b), lab, loss, zz, db)
     torch.cuda.synchronize()
     assert torch.equal(zz.view(torch.int16), out.view(torch.int16))
+
+
+# (n, c, h, w, stride, pad, use_stats, special): BN + ReLU fused into a 3x3 max
+# pool; "special" puts NaN, infinities and ties into x under given statistics
+BN_POOL = [
+    (2, 64, 112, 112, 2, 1, False, False),   # the ResNet-50 stem's BN + pool at N = 2
+    (32, 64, 112, 112, 2, 1, False, False),  # ... at batch 32
+    (3, 8, 7, 9, 2, 1, False, False),        # one chunk per pixel, odd sides, ragged windows
+    (2, 16, 10, 6, 1, 1, False, False),      # stride 1
+    (2, 128, 9, 11, 2, 0, True, False),      # no padding, given statistics
+    (2, 256, 5, 5, 3, 2, True, True),        # stride 3, pad 2; NaN, infinities and ties
+    (2, 256, 20, 64, 2, 1, False, False),    # 32 channel chunks per pixel
+]
+
+
+@pytest.mark.parametrize("case", BN_POOL, ids=[str(c) for c in BN_POOL])
+def test_bn_relu_maxpool_matches_the_two_calls(case):
+    require_gpu()
+    n, c, h, w, st, pad, given, special = case
+    bd = F.bn_desc(n, c, h, w, "NHWC", 1e-5, 1.0, True)
+    pd = F.pool_desc(n, c, h, w, 3, 3, st, pad)
+    p, q = F.fp16_pool_out_dims(pd)
+    x = synth.normal_f16((n, h, w, c), 1.0, 60 + c, 1, mean=0.3)
+    gamma = synth.normal_f16((c,), 0.3, 60 + c, 2, mean=1.0)
+    beta = synth.normal_f16((c,), 0.3, 60 + c, 3)
+    G, B = dev(gamma), dev(beta)
+    ws = F.workspace(F.fp16_bn_workspace_bytes(bd))
+    S = torch.empty(2 * c, dtype=torch.float32, device="cuda")
+    Z = torch.empty((n, h, w, c), dtype=torch.float16, device="cuda")
+    note(f"[gpu] bn statistics {case}")
+    F.fp16_bn_relu(bd, dev(x), G, B, None, Z, S, ws)
+    if special:
+        x = x.copy()
+        flat = x.reshape(-1)
+        flat[::2] = flat[1::2]  # equal neighbours: ties inside windows
+        flat[::97] = np.float16(np.nan)
+        flat[5::89] = np.float16(np.inf)
+        flat[7::83] = np.float16(-np.inf)
+    X = dev(x)
+    if given:
+        bd = F.bn_desc(n, c, h, w, "NHWC", 1e-5, 1.0, True, use_stats=True)
+    Y0 = torch.empty((n, p, q, c), dtype=torch.float16, device="cuda")
+    I0 = torch.empty((n, p, q, c), dtype=torch.uint8, device="cuda")
+    S0 = S.clone()
+    note(f"[gpu] bn + maxpool (two calls) {case}")
+    F.fp16_bn_relu(bd, X, G, B, None, Z, S0, ws)
+    F.fp16_maxpool_fwd(pd, Z, Y0, I0)
+    S1 = S.clone() if given else torch.full_like(S, float("nan"))
+    Y1 = torch.full_like(Y0, float("nan"))
+    I1 = torch.full_like(I0, 0xEE)
+    note(f"[gpu] bn_relu_maxpool {case}")
+    F.fp16_bn_relu_maxpool(bd, pd, X, G, B, S1, Y1, I1, ws)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(S1), host(S0))
+    assert np.array_equal(host(Y1).view(np.uint16), host(Y0).view(np.uint16))
+    assert np.array_equal(host(I1), host(I0))
+    if n * c * h * w <= 1 << 21:
+        # and against the oracle: the declared apply with these statistics, pooled
+        s = host(S0)
+        z = oracle.bn_apply_f32(oracle.bn_shape(n, c, h, w), x, gamma, beta, s[:c], s[c:], None,
+                                1.0, True)
+        y, idx = oracle.maxpool_fwd(oracle.pool_shape(n, c, h, w, 3, 3, st, pad), z)
+        assert np.array_equal(host(Y1).view(np.uint16), y.view(np.uint16))
+        assert np.array_equal(host(I1), idx)

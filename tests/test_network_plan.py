@@ -16,10 +16,12 @@ def net():
 
 def test_layer_and_parameter_counts(net):
     kinds = [o.kind for o in net.fwd]
-    # 53 convolutions + the classifier; 53 BNs, each fused with the conv before it
+    # 53 convolutions + the classifier; 53 BNs, each fused with the conv before
+    # it except the stem's, fused with the max pool after it
     assert kinds.count("conv_fwd") + kinds.count("conv_bn_fwd") == 54
-    assert kinds.count("bn_fwd") + kinds.count("conv_bn_fwd") == 53
-    assert kinds.count("conv_bn_fwd") == 53 and kinds.count("conv_fwd") == 1
+    assert kinds.count("bn_maxpool_fwd") + kinds.count("conv_bn_fwd") == 53
+    assert kinds.count("conv_bn_fwd") == 52 and kinds.count("conv_fwd") == 2
+    assert kinds.count("bn_fwd") == kinds.count("maxpool_fwd") == 0
     unfused = ResNet50(n=1, image=64, device="cpu", fuse_bn_stats=False)
     uk = [o.kind for o in unfused.fwd]
     assert uk.count("conv_fwd") == 54 and uk.count("bn_fwd") == 53
@@ -43,6 +45,7 @@ OUTPUTS = {"conv_fwd": ["y"], "conv_bn_fwd": ["y", "z", "stats", "mask"], "conv_
            "conv_wgrad": ["dw"], "bn_fwd": ["y", "stats", "mask"],
            "bn_bwd": ["dx", "dgamma", "dbeta", "dres"], "maxpool_fwd": ["y", "idx"],
            "maxpool_bwd": ["dx"], "avgpool_fwd": ["y"], "avgpool_bwd": ["dx"],
+           "bn_maxpool_fwd": ["stats", "y", "idx"],
            "softmax_ce": ["loss", "dz", "dbias"], "dgrad_filter": ["wf"]}
 
 
@@ -61,7 +64,7 @@ def test_dataflow(net):
         # ("mask_of" names a BN, whose kept mask the call reads)
         reads = [v for k, v in op.a.items()
                  if isinstance(v, str) and k not in outs and k != "mask_of"]
-        if op.kind in ("bn_fwd", "bn_bwd", "conv_bn_fwd"):
+        if op.kind in ("bn_fwd", "bn_bwd", "conv_bn_fwd", "bn_maxpool_fwd"):
             reads += [op.name + ".gamma", op.name + ".beta"]
         for v in reads:
             assert v in net.buffers and v in written, (op.name, op.kind, v)
@@ -85,13 +88,13 @@ def test_dataflow(net):
 def test_block_last_bns_keep_their_relu_mask(net):
     # the 16 BNs whose ReLU follows the shortcut write the mask in the forward
     # and their backward reads it instead of the shortcut
-    fwd = {o.name: o for o in net.fwd if o.kind in ("bn_fwd", "conv_bn_fwd")}
-    kept = {n for n, o in fwd.items() if o.a["mask"] is not None}
-    assert kept == {n for n, o in fwd.items() if o.a["res"] is not None}
+    fwd = {o.name: o for o in net.fwd if o.kind in ("bn_fwd", "conv_bn_fwd", "bn_maxpool_fwd")}
+    kept = {n for n, o in fwd.items() if o.a.get("mask") is not None}
+    assert kept == {n for n, o in fwd.items() if o.a.get("res") is not None}
     assert len(kept) == 16 and all(n.endswith(".bn3") for n in kept)
     for o in net.bwd:
         if o.kind == "bn_bwd":
-            assert o.a["mask"] == fwd[o.a["mask_of"]].a["mask"]
+            assert o.a["mask"] == fwd[o.a["mask_of"]].a.get("mask")
             # no block-last BN writes its shortcut gradient: the downsampling
             # shortcut's BN takes the block-last BN's gradient under its mask
             assert o.a["dres"] is None
@@ -113,6 +116,20 @@ def test_block_last_bns_keep_their_relu_mask(net):
             assert o.a["addend"] == bn3.a["dy"]
     swapped = ResNet50(n=1, image=64, device="cpu", bn_swap=True)
     assert all(o.a["mask"] is None for o in swapped.fwd if o.kind in ("bn_fwd", "conv_bn_fwd"))
+
+
+def test_stem_bn_feeds_the_pool_directly(net):
+    # the stem BN + ReLU and the max pool are one call; the BN output is not
+    # kept (its backward recomputes the mask from the conv output)
+    kinds = [o.kind for o in net.fwd[:3]]
+    assert kinds == ["conv_fwd", "bn_maxpool_fwd", "conv_bn_fwd"]
+    f = net.fwd[1].a
+    assert (f["x"], f["y"], f["idx"]) == ("stem.y", "pool.y", "pool.idx")
+    assert "stem.bn.y" not in net.buffers and "d:stem.bn.y" in net.buffers
+    b = next(o for o in net.bwd if o.kind == "bn_bwd" and o.name == "stem.bn")
+    assert b.a["y"] is None and b.a["mask"] is None and b.a["x"] == "stem.y"
+    plain = ResNet50(n=1, image=64, device="cpu", fuse_bn_stats=False)
+    assert [o.kind for o in plain.fwd[:3]] == ["conv_fwd", "bn_fwd", "maxpool_fwd"]
 
 
 def test_bn_swap_and_zero_gamma_options():
