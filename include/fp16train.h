@@ -195,6 +195,22 @@ fp16_status fp16_conv_dgrad_filters(int32_t count, const fp16_conv_desc* descs,
  * x, dy or ws. */
 fp16_status fp16_conv_wgrad(const fp16_conv_desc* desc, const fp16_t* x, const fp16_t* dy,
                             fp16_t* dw, void* ws, size_t ws_bytes, fp16_stream_t stream);
+/* fp16_conv_wgrad split over fewer pixel ranges, for a weight gradient that
+ * runs beside other work on the device (the data-parallel backward of
+ * Section 5.1 overlaps the weight gradients with the data gradients and BN
+ * backwards on a second stream): the partial products aim at `workgroups`
+ * workgroups in all, 1 <= workgroups <= 512, instead of the default 512 (two
+ * per compute unit); 0 is the default, identical to fp16_conv_wgrad.  Fewer
+ * ranges mean fewer float32 partial sums written and re-read and more of the
+ * device left to the other stream; the partial sums are added in a fixed
+ * order as always, so results are deterministic for a given count (and
+ * differ from the default's only by float32 summation order).  The workspace
+ * fp16_conv_workspace_bytes(desc, FP16_PASS_WGRAD) reports suffices for
+ * every count.  FP16_ERR_SHAPE for a count outside [0, 512]; other errors as
+ * fp16_conv_wgrad. */
+fp16_status fp16_conv_wgrad_ex(const fp16_conv_desc* desc, const fp16_t* x, const fp16_t* dy,
+                               fp16_t* dw, void* ws, size_t ws_bytes, int32_t workgroups,
+                               fp16_stream_t stream);
 
 /* For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc): the

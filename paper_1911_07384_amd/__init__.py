@@ -36,7 +36,7 @@ EXPORTS = ["fp16_conv_out_dims", "fp16_conv_workspace_bytes", "fp16_conv_fwd", "
            "fp16_conv_dgrad_filters",
            "fp16_conv_dgrad_wf", "fp16_noalloc_scratch_bytes", "fp16_conv_wgrad_noalloc",
            "fp16_bn_mask_bytes", "fp16_bn_relu_m", "fp16_bn_relu_bwd_m", "fp16_conv_bn_relu_fwd_m",
-           "fp16_conv_dgrad_wf_m", "fp16_bn_relu_maxpool"]
+           "fp16_conv_dgrad_wf_m", "fp16_bn_relu_maxpool", "fp16_conv_wgrad_ex"]
 
 
 class Fp16Error(RuntimeError):
@@ -83,6 +83,7 @@ _SIGS = {
     "fp16_conv_dgrad_wf": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_conv_dgrad_wf_m": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_bn_relu_maxpool": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
+    "fp16_conv_wgrad_ex": (ctypes.c_int, [_P, _P, _P, _P, _P, _SZ, ctypes.c_int32, _P]),
     "fp16_bn_workspace_bytes": (_SZ, [_P]),
     "fp16_bn_mask_bytes": (_SZ, [_P]),
     "fp16_bn_relu_m": (ctypes.c_int, [_P] * 9 + [_SZ, _P]),
@@ -241,6 +242,13 @@ def fp16_conv_dgrad_wf_m(desc, dy, wf, addend, mask, dx, ws=None, ws_bytes=None,
 def fp16_conv_wgrad(desc, x, dy, dw, ws=None, ws_bytes=None, stream=None) -> None:
     _check("fp16_conv_wgrad", lib().fp16_conv_wgrad(ctypes.byref(desc), _ptr(x), _ptr(dy), _ptr(dw),
                                                     _ptr(ws), _wsb(ws, ws_bytes), _stream(stream)))
+
+
+def fp16_conv_wgrad_ex(desc, x, dy, dw, ws=None, ws_bytes=None, workgroups=0,
+                       stream=None) -> None:
+    _check("fp16_conv_wgrad_ex", lib().fp16_conv_wgrad_ex(
+        ctypes.byref(desc), _ptr(x), _ptr(dy), _ptr(dw), _ptr(ws), _wsb(ws, ws_bytes),
+        int(workgroups), _stream(stream)))
 
 
 def fp16_noalloc_scratch_bytes() -> int:

@@ -78,7 +78,9 @@ struct ConvWs {
   int splits = 0, pps = 0;
 };
 
-ConvWs conv_ws(const ConvDims& d, int pass) {
+// (wg: the weight gradient's workgroup target, 0 for kWgradWorkgroups)
+ConvWs conv_ws(const ConvDims& d, int pass, int wg = 0) {
+  const int target = wg > 0 ? wg : kWgradWorkgroups;
   ConvWs L;
   if (d.accum) return L;  // the binary16 chains read and write the caller's tensors only
   size_t off = 0;
@@ -113,7 +115,7 @@ ConvWs conv_ws(const ConvDims& d, int pass) {
   } else if (stem_s2d(d)) {
     L.need_x = true;
     L.x = take((size_t)d.N * d.P * d.Q * 16 * 2);
-    wgrad_plan(d.Kp, 16, 4, 4, (int64_t)d.N * d.P * d.Q, &L.splits, &L.pps);
+    wgrad_plan(d.Kp, 16, 4, 4, (int64_t)d.N * d.P * d.Q, target, &L.splits, &L.pps);
     L.part = take((size_t)L.splits * d.Kp * 256 * 4);
   } else {
     if (nchw || d.Cp != d.C) {
@@ -124,7 +126,7 @@ ConvWs conv_ws(const ConvDims& d, int pass) {
       L.need_y = true;
       L.y = take((size_t)d.N * d.P * d.Q * d.Kp * 2);
     }
-    wgrad_plan(d.Kp, d.Cp, d.R, d.S, (int64_t)d.N * d.P * d.Q, &L.splits, &L.pps);
+    wgrad_plan(d.Kp, d.Cp, d.R, d.S, (int64_t)d.N * d.P * d.Q, target, &L.splits, &L.pps);
     L.part = take((size_t)L.splits * d.Kp * d.R * d.S * d.Cp * 4);
   }
   L.total = off;
@@ -425,14 +427,16 @@ fp16_status fp16_conv_dgrad_wf_m(const fp16_conv_desc* desc, const fp16_t* dy, c
 
 extern "C" {
 
-fp16_status fp16_conv_wgrad(const fp16_conv_desc* desc, const fp16_t* x, const fp16_t* dy,
-                            fp16_t* dw, void* ws, size_t ws_bytes, fp16_stream_t stream) {
+fp16_status fp16_conv_wgrad_ex(const fp16_conv_desc* desc, const fp16_t* x, const fp16_t* dy,
+                               fp16_t* dw, void* ws, size_t ws_bytes, int32_t workgroups,
+                               fp16_stream_t stream) {
   ConvDims d;
   fp16_status s = check_conv(desc, &d);
   if (s != FP16_OK) return s;
+  if (workgroups < 0 || workgroups > kWgradWorkgroups) return FP16_ERR_SHAPE;
   if (!x || !dy || !dw) return FP16_ERR_NULL;
   if (!aligned16(x) || !aligned16(dy) || !aligned16(dw)) return FP16_ERR_MISALIGNED;
-  const ConvWs L = conv_ws(d, FP16_PASS_WGRAD);
+  const ConvWs L = conv_ws(d, FP16_PASS_WGRAD, workgroups);
   if ((s = check_ws(L, ws, ws_bytes)) != FP16_OK) return s;
   const size_t wb = (size_t)d.w_elems * 2;
   if (overlap(dw, wb, x, (size_t)d.x_elems * 2) || overlap(dw, wb, dy, (size_t)d.y_elems * 2) ||
@@ -482,6 +486,11 @@ fp16_status fp16_conv_wgrad(const fp16_conv_desc* desc, const fp16_t* x, const f
   TRY(launch_wgrad_reduce(part, L.splits, d.K, d.Kp, d.R, d.S, d.C, d.Cp, d.layout,
                           reinterpret_cast<h16*>(dw), st));
   return FP16_OK;
+}
+
+fp16_status fp16_conv_wgrad(const fp16_conv_desc* desc, const fp16_t* x, const fp16_t* dy,
+                            fp16_t* dw, void* ws, size_t ws_bytes, fp16_stream_t stream) {
+  return fp16_conv_wgrad_ex(desc, x, dy, dw, ws, ws_bytes, 0, stream);
 }
 
 // ---- batch normalisation ----------------------------------------------------

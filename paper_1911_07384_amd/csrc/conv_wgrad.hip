@@ -611,11 +611,12 @@ void launch_wgrad7(const WCfg& cfg, dim3 grid, hipStream_t st, const WgradArgs& 
 
 }  // namespace
 
-void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int* splits, int* pix_per_split) {
+void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int target, int* splits,
+                int* pix_per_split) {
   const int Nw = R * S * Cp;
   const WCfg cfg = wgrad_choice(K, Cp, Nw, npix);
   const int64_t tiles = (int64_t)ceil_div(K, cfg.BM) * ceil_div(Nw, cfg.BN);
-  int64_t want = (512 + tiles - 1) / tiles;           // about two workgroups per CU
+  int64_t want = (target + tiles - 1) / tiles;  // about `target` workgroups
   const int64_t max_splits = (npix + 2 * BKP - 1) / (2 * BKP);  // at least two k-steps each
   if (want > max_splits) want = max_splits;
   if (want < 1) want = 1;

@@ -139,8 +139,12 @@ hipError_t launch_wgrad_reduce(const float* partial, int splits, int K, int Kp, 
 // folded in place in groups first, so partial holds scratch afterwards).
 hipError_t launch_s2d3(const h16* src, h16* dst, int N, int H, int W, hipStream_t st);
 hipError_t launch_wgrad_reduce_s2d3(float* partial, int splits, int K, h16* dw, hipStream_t st);
-// Split-K plan of the weight gradient.
-void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int* splits, int* pix_per_split);
+// Split-K plan of the weight gradient: about `target` workgroups (tiles x
+// splits; kWgradWorkgroups, two per CU, unless the caller asks for fewer),
+// each split at least two k-steps of pixels.
+constexpr int kWgradWorkgroups = 512;
+void wgrad_plan(int K, int Cp, int R, int S, int64_t npix, int target, int* splits,
+                int* pix_per_split);
 
 // Convolutions with every operation in binary16 (conv_f16chain.hip): each
 // output a chain of binary16 fmas from +0 in the declared order.  NHWC

@@ -51,6 +51,13 @@ class Op:
 class ResNet50:
     """Device state and the ABI program of one ResNet-50 training step."""
 
+    # split-K workgroups of a weight gradient on the second stream: at batch
+    # 128 the step took 12.49 ms with the default 512 (two per CU), 12.20 with
+    # 256, 12.22 with 224 and 12.37 with 320 (fewer float32 partial sums, more
+    # of the device left to the memory-bound calls beside them); 128 and 64
+    # made the weight gradients the critical path
+    SIDE_WORKGROUPS = 256
+
     def __init__(self, n: int = 128, image: int = 224, classes: int = 1000, seed: int = 0,
                  lr: float = 0.1, momentum: float = 0.9, weight_decay: float = 1e-4,
                  post_scale: float = 0.25, eps: float = 1e-5, stages=STAGES, device="cuda",
@@ -282,8 +289,12 @@ class ResNet50:
                     "desc": c["desc"], "dy": dy, "w": name, "wf": wf, "addend": addend,
                     "amask": self._bn_op(mask_of).a["mask"] if mask_of else None,
                     "mask_of": mask_of, "dx": dx}))
+        # the weight gradients beside the backward's other calls aim at about
+        # one workgroup per CU; the first layer's, the last call of the
+        # backward with nothing left to overlap, takes the default two
+        wg = self.SIDE_WORKGROUPS if dx_needed else 0
         self.bwd.append(Op("conv_wgrad", name, {"desc": c["desc"], "x": c["x"], "dy": dy,
-                                                "dw": "d:" + name}))
+                                                "dw": "d:" + name, "wg": wg}))
 
     def _plan_backward(self, gd, pd):
         # classifier: the loss kernel wrote fc.dy and the bias gradient
@@ -408,7 +419,8 @@ class ResNet50:
             F.fp16_conv_dgrad_filters([d for d, _, _ in a["items"]], [t(w) for _, w, _ in a["items"]],
                                       [t(f) for _, _, f in a["items"]])
         elif k == "conv_wgrad":
-            F.fp16_conv_wgrad(a["desc"], t(a["x"]), t(a["dy"]), t(a["dw"]), ws)
+            F.fp16_conv_wgrad_ex(a["desc"], t(a["x"]), t(a["dy"]), t(a["dw"]), ws,
+                                 workgroups=a["wg"])
         elif k == "conv_bn_fwd":
             nm = op.name
             if a["mask"] is None:

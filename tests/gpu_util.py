@@ -66,7 +66,9 @@ class ConvCase:
         assert self.x.shape == xs and self.w.shape == ws and self.dy.shape == ys
         self.label = f"conv n={n} c={c} hw={h}x{w} k={k} rs={r}x{s} st={stride} pad={pad} {layout}"
 
-    def run(self, which):
+    def run(self, which, workgroups=None):
+        """One pass on the GPU; workgroups (weight gradient only) goes through
+        fp16_conv_wgrad_ex."""
         x, w, dy = dev(self.x), dev(self.w), dev(self.dy)
         pass_ = {"fwd": F.PASS_FWD, "dgrad": F.PASS_DGRAD, "wgrad": F.PASS_WGRAD}[which]
         ws = F.workspace(F.fp16_conv_workspace_bytes(self.desc, pass_))
@@ -79,7 +81,10 @@ class ConvCase:
             F.fp16_conv_dgrad(self.desc, dy, w, out, ws)
         else:
             out = torch.empty(self.ws, dtype=torch.float16, device="cuda")
-            F.fp16_conv_wgrad(self.desc, x, dy, out, ws)
+            if workgroups is None:
+                F.fp16_conv_wgrad(self.desc, x, dy, out, ws)
+            else:
+                F.fp16_conv_wgrad_ex(self.desc, x, dy, out, ws, workgroups=workgroups)
         torch.cuda.synchronize()
         return host(out)
 

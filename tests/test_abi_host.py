@@ -79,6 +79,18 @@ def test_conv_validation(fn):
     assert _call(fn, d, A, B, Cc + 8) == MISALIGNED
 
 
+def test_wgrad_workgroup_target_validation():
+    lib = F.lib()
+    d = _conv()
+    need = F.fp16_conv_workspace_bytes(d, F.PASS_WGRAD)
+    f = lambda wg, x=A: lib.fp16_conv_wgrad_ex(ctypes.byref(d), x, B, Cc, WS, need, wg, None)
+    assert f(-1) == SHAPE and f(513) == SHAPE
+    assert f(0, None) == NULL and f(256, None) == NULL
+    # dw over the workspace, at any target
+    for wg in (0, 1, 512):
+        assert lib.fp16_conv_wgrad_ex(ctypes.byref(d), A, B, WS + 64, WS, need, wg, None) == ALIASING
+
+
 def test_conv_workspace_and_aliasing():
     d = _conv()
     # native NHWC forward with C % 8 == 0 needs no workspace ...

@@ -86,6 +86,31 @@ def test_deterministic(which):
     assert np.array_equal(a.view(np.uint16), b.view(np.uint16))
 
 
+# weight gradients split for fewer workgroups (fp16_conv_wgrad_ex): the 3x3
+# 64-channel layer, a 1x1 with many filter tiles, the stem (space-to-depth
+# path) and a strided 3x3
+WG_SHAPES = [(2, 64, 28, 28, 64, 3, 3, 1, 1, "NHWC"), (2, 512, 7, 7, 256, 1, 1, 1, 0, "NHWC"),
+             (2, 3, 32, 32, 64, 7, 7, 2, 3, "NHWC"), (2, 64, 15, 15, 128, 3, 3, 2, 1, "NHWC")]
+
+
+@pytest.mark.parametrize("shape", WG_SHAPES, ids=[_id(s) for s in WG_SHAPES])
+def test_wgrad_workgroup_targets(shape):
+    require_gpu()
+    case = ConvCase(*shape, seed=3)
+    ref64, ref16 = case.oracle("wgrad")
+    default = case.run("wgrad")
+    assert np.array_equal(case.run("wgrad", workgroups=0).view(np.uint16), default.view(np.uint16))
+    for wg in (1, 7, 64, 256, 512):
+        got = case.run("wgrad", workgroups=wg)
+        check_close(got, ref64, what=f"wgrad workgroups={wg} {case.label}")
+        assert np.mean(ulp_dist(got, ref16) <= 1) > 0.99
+        # deterministic for a given count
+        assert np.array_equal(case.run("wgrad", workgroups=wg).view(np.uint16), got.view(np.uint16))
+    # the default is 512
+    assert np.array_equal(case.run("wgrad", workgroups=512).view(np.uint16),
+                          default.view(np.uint16))
+
+
 @pytest.mark.parametrize("layout", ["NHWC", "NCHW"])
 @pytest.mark.parametrize("r,shift", [(3, (0, 0)), (3, (1, -1)), (1, (0, 0)), (7, (-2, 3))])
 def test_delta_filter_forward_is_exact(layout, r, shift):
