@@ -51,12 +51,14 @@ class Op:
 class ResNet50:
     """Device state and the ABI program of one ResNet-50 training step."""
 
-    # split-K workgroups of a weight gradient on the second stream: at batch
-    # 128 the step took 12.49 ms with the default 512 (two per CU), 12.20 with
-    # 256, 12.22 with 224 and 12.37 with 320 (fewer float32 partial sums, more
-    # of the device left to the memory-bound calls beside them); 128 and 64
-    # made the weight gradients the critical path
-    SIDE_WORKGROUPS = 256
+    # split-K workgroups of a weight gradient on the second stream, by stage
+    # (the classifier's: the last entry): at batch 128 the step took 12.49 ms
+    # with the default 512 (two per CU) everywhere, 12.20 with 256, 12.22 with
+    # 224 and 12.37 with 320 (fewer float32 partial sums, more of the device
+    # left to the memory-bound calls beside them; 128 and 64 made the weight
+    # gradients the critical path); then 192 for stage 1 and 224 for stage 2
+    # took another 0.07 ms
+    SIDE_WORKGROUPS = (192, 224, 256, 256, 256)
 
     def __init__(self, n: int = 128, image: int = 224, classes: int = 1000, seed: int = 0,
                  lr: float = 0.1, momentum: float = 0.9, weight_decay: float = 1e-4,
@@ -292,7 +294,8 @@ class ResNet50:
         # the weight gradients beside the backward's other calls aim at about
         # one workgroup per CU; the first layer's, the last call of the
         # backward with nothing left to overlap, takes the default two
-        wg = self.SIDE_WORKGROUPS if dx_needed else 0
+        stage = int(name[1]) - 1 if name[0] == "l" else -1
+        wg = self.SIDE_WORKGROUPS[stage] if dx_needed else 0
         self.bwd.append(Op("conv_wgrad", name, {"desc": c["desc"], "x": c["x"], "dy": dy,
                                                 "dw": "d:" + name, "wg": wg}))
 

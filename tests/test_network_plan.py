@@ -132,6 +132,21 @@ def test_stem_bn_feeds_the_pool_directly(net):
     assert [o.kind for o in plain.fwd[:3]] == ["conv_fwd", "bn_fwd", "maxpool_fwd"]
 
 
+def test_weight_gradient_workgroup_targets(net):
+    # the weight gradients beside the backward take the per-stage targets; the
+    # first layer's, the last call of the backward, the default
+    for op in net.bwd:
+        if op.kind != "conv_wgrad":
+            continue
+        if op.name == "stem":
+            assert op.a["wg"] == 0
+        elif op.name == "fc":
+            assert op.a["wg"] == net.SIDE_WORKGROUPS[-1]
+        else:
+            assert op.a["wg"] == net.SIDE_WORKGROUPS[int(op.name[1]) - 1]
+        assert 0 <= op.a["wg"] <= 512
+
+
 def test_bn_swap_and_zero_gamma_options():
     net = ResNet50(n=1, image=64, device="cpu", bn_swap=True, zero_gamma_last=True)
     bns = [(o, o.a["bn"] if o.kind == "conv_bn_fwd" else o.a["desc"]) for o in net.fwd
