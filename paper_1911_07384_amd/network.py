@@ -20,7 +20,9 @@ also zeroes the shortcut's contribution at the start).
 
 The step is an explicit program: a list of ``Op`` records, each one ABI call
 with named device buffers.  Running the list in order is one training step.
-The weight gradients are off the backward's critical path, so ``backward``
+A downsampling block's shortcut convolution + BN runs on a second stream
+beside the block's first two convolutions in the forward.  The weight
+gradients are off the backward's critical path, so ``backward``
 runs them on a second stream with their own workspace, each after an event
 from the call that produced its input gradient, and joins the streams before
 the update; everything else runs in order on the current stream.  The step
@@ -493,7 +495,14 @@ class ResNet50:
     def _schedule(self):
         """For each weight gradient of the backward, the index (in bwd) of the
         call that writes its input gradient, or -1 when that happens before the
-        backward starts."""
+        backward starts; and for each fused downsampling shortcut of the
+        forward, the index of its block's first call (where it can start)."""
+        self._fwd_branch = {}
+        for i, op in enumerate(self.fwd):
+            if op.kind == "conv_bn_fwd" and op.a["conv"].endswith(".ds"):
+                first = min(j for j, o in enumerate(self.fwd) if o.a.get("x") == op.a["x"])
+                self._fwd_branch[first] = i
+        self._fwd_skip = set(self._fwd_branch.values())
         writer = {}
         self._dep = {}
         self._mark = set()
@@ -524,7 +533,28 @@ class ResNet50:
                 self.run(self.prep_op, ws=self.ws_side)
             self._wf_ready = torch.cuda.Event()
             self._wf_ready.record(self.side)
-        for op in self.fwd:
+        if self.side is None:
+            for op in self.fwd:
+                self.run(op)
+            return
+        # a downsampling block's shortcut (its conv + BN, one call) runs on the
+        # side stream from the block input on, beside the block's first two
+        # convolutions; the block-last BN, which adds it, waits for it
+        done = {}
+        for i, op in enumerate(self.fwd):
+            if i in self._fwd_branch:
+                ev = torch.cuda.Event()
+                ev.record(main)
+                self.side.wait_event(ev)
+                br = self.fwd[self._fwd_branch[i]]
+                with torch.cuda.stream(self.side):
+                    self.run(br, ws=self.ws_side)
+                done[br.a["z"]] = torch.cuda.Event()
+                done[br.a["z"]].record(self.side)
+            if i in self._fwd_skip:
+                continue
+            if op.a.get("res") in done:
+                main.wait_event(done[op.a["res"]])
             self.run(op)
 
     def backward(self):

@@ -132,6 +132,19 @@ def test_stem_bn_feeds_the_pool_directly(net):
     assert [o.kind for o in plain.fwd[:3]] == ["conv_fwd", "bn_fwd", "maxpool_fwd"]
 
 
+def test_forward_shortcut_branches(net):
+    # each downsampling shortcut starts with its block's first call and is
+    # joined by the block-last BN, which adds it
+    br = {net.fwd[k].name: net.fwd[v].name for k, v in net._fwd_branch.items()}
+    assert br == {f"l{s}.0.bn1": f"l{s}.0.bnd" for s in (1, 2, 3, 4)}
+    for k, v in net._fwd_branch.items():
+        assert net.fwd[k].a["x"] == net.fwd[v].a["x"] and k < v
+        later = [o for o in net.fwd[v + 1:] if o.a.get("res") == net.fwd[v].a["z"]]
+        assert [o.name for o in later] == [net.fwd[v].name[:-4] + ".bn3"]
+        # nothing between the block's first call and the shortcut reads its output
+        assert all(net.fwd[v].a["z"] not in o.a.values() for o in net.fwd[k:v])
+
+
 def test_weight_gradient_workgroup_targets(net):
     # the weight gradients beside the backward take the per-stage targets; the
     # first layer's, the last call of the backward, the default
