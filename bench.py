@@ -114,7 +114,8 @@ def op_work(op, net):
     if k in ("conv_fwd", "conv_dgrad", "conv_dgrad_add", "conv_wgrad"):
         fl, by = conv_work(a["desc"], {"conv_fwd": "fwd", "conv_wgrad": "wgrad"}.get(k, "dgrad"))
         if k == "conv_dgrad_add":
-            ex = a["desc"].n * a["desc"].c * a["desc"].h * a["desc"].w
+            d, st = a["desc"], a.get("astride", 1)
+            ex = d.n * d.c * (-(-d.h // st)) * (-(-d.w // st))  # the addend's elements
             by += 2 * ex + (ex // 8 if a.get("amask") else 0)
         return fl, by, "mfma" if fl / by >= RIDGE else "hbm"
     if k == "conv_bn_fwd":

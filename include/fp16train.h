@@ -174,6 +174,22 @@ fp16_status fp16_conv_dgrad_wf(const fp16_conv_desc* desc, const fp16_t* dy, con
 fp16_status fp16_conv_dgrad_wf_m(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* wf,
                                  const fp16_t* addend, const uint8_t* addend_mask, fp16_t* dx,
                                  void* ws, size_t ws_bytes, fp16_stream_t stream);
+/* fp16_conv_dgrad_wf with the addend's optional parts spelled out:
+ *   dx = round_to_binary16(dgrad(dy, W) + a),   a = +0 where addend is NULL;
+ * with addend_stride s > 1 the addend holds only the pixels whose row and
+ * column are multiples of s, laid out NHWC as [N][ceil(H/s)][ceil(W/s)][C]
+ * (every other pixel takes a = +0): the gradient a strided 1x1 shortcut
+ * (Section 5.1's downsampling blocks) sends to the block input, computed on
+ * its own grid instead of written out with three zeros in four; with
+ * addend_mask (over the addend's own layout, as in fp16_conv_dgrad_wf_m) a =
+ * +0 where the bit is clear.  s = 1 and no mask is fp16_conv_dgrad_wf.
+ * 1 <= addend_stride <= 16 (FP16_ERR_SHAPE); a stride or a mask needs the
+ * addend (FP16_ERR_NULL) and NHWC (FP16_ERR_UNSUPPORTED), a mask C % 8 == 0;
+ * a strided addend may not be dx or overlap it (FP16_ERR_ALIASING). */
+fp16_status fp16_conv_dgrad_wf_ex(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* wf,
+                                  const fp16_t* addend, const uint8_t* addend_mask,
+                                  int32_t addend_stride, fp16_t* dx, void* ws, size_t ws_bytes,
+                                  fp16_stream_t stream);
 /* fp16_conv_dgrad_filter for `count` convolutions at once (descs[i], w[i],
  * wf[i]; host arrays, read during the call only): every filter of a network
  * rearranged by one launch (or a few) instead of one launch each, with

@@ -36,7 +36,8 @@ EXPORTS = ["fp16_conv_out_dims", "fp16_conv_workspace_bytes", "fp16_conv_fwd", "
            "fp16_conv_dgrad_filters",
            "fp16_conv_dgrad_wf", "fp16_noalloc_scratch_bytes", "fp16_conv_wgrad_noalloc",
            "fp16_bn_mask_bytes", "fp16_bn_relu_m", "fp16_bn_relu_bwd_m", "fp16_conv_bn_relu_fwd_m",
-           "fp16_conv_dgrad_wf_m", "fp16_bn_relu_maxpool", "fp16_conv_wgrad_ex"]
+           "fp16_conv_dgrad_wf_m", "fp16_bn_relu_maxpool", "fp16_conv_wgrad_ex",
+           "fp16_conv_dgrad_wf_ex"]
 
 
 class Fp16Error(RuntimeError):
@@ -84,6 +85,7 @@ _SIGS = {
     "fp16_conv_dgrad_wf_m": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_bn_relu_maxpool": (ctypes.c_int, [_P, _P, _P, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "fp16_conv_wgrad_ex": (ctypes.c_int, [_P, _P, _P, _P, _P, _SZ, ctypes.c_int32, _P]),
+    "fp16_conv_dgrad_wf_ex": (ctypes.c_int, [_P, _P, _P, _P, _P, ctypes.c_int32, _P, _P, _SZ, _P]),
     "fp16_bn_workspace_bytes": (_SZ, [_P]),
     "fp16_bn_mask_bytes": (_SZ, [_P]),
     "fp16_bn_relu_m": (ctypes.c_int, [_P] * 9 + [_SZ, _P]),
@@ -237,6 +239,13 @@ def fp16_conv_dgrad_wf_m(desc, dy, wf, addend, mask, dx, ws=None, ws_bytes=None,
     _check("fp16_conv_dgrad_wf_m", lib().fp16_conv_dgrad_wf_m(
         ctypes.byref(desc), _ptr(dy), _ptr(wf), _ptr(addend), _ptr(mask), _ptr(dx), _ptr(ws),
         _wsb(ws, ws_bytes), _stream(stream)))
+
+
+def fp16_conv_dgrad_wf_ex(desc, dy, wf, addend, mask, addend_stride, dx, ws=None, ws_bytes=None,
+                          stream=None) -> None:
+    _check("fp16_conv_dgrad_wf_ex", lib().fp16_conv_dgrad_wf_ex(
+        ctypes.byref(desc), _ptr(dy), _ptr(wf), _ptr(addend), _ptr(mask), int(addend_stride),
+        _ptr(dx), _ptr(ws), _wsb(ws, ws_bytes), _stream(stream)))
 
 
 def fp16_conv_wgrad(desc, x, dy, dw, ws=None, ws_bytes=None, stream=None) -> None:

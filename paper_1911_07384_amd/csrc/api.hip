@@ -258,18 +258,21 @@ static size_t dgrad_filter_bytes(const ConvDims& d) { return (size_t)d.C * d.R *
 
 // Data gradient; with wf_given the filter is already rearranged (w is then
 // the rearranged filter, fp16_conv_dgrad_filter_bytes long, NHWC only); with
-// amask the addend is taken under that ReLU mask (NHWC, C % 8 == 0).
+// amask the addend is taken under that ReLU mask (NHWC, C % 8 == 0); with
+// astride > 1 the addend holds every astride-th row and column only (NHWC).
 static fp16_status conv_dgrad_impl(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* w,
                                    const fp16_t* addend, fp16_t* dx, void* ws, size_t ws_bytes,
                                    fp16_stream_t stream, bool wf_given = false,
-                                   const uint8_t* amask = nullptr) {
+                                   const uint8_t* amask = nullptr, int astride = 1) {
   ConvDims d;
   fp16_status s = check_conv(desc, &d);
   if (s != FP16_OK) return s;
   if (!dy || !w || !dx) return FP16_ERR_NULL;
+  if (astride < 1 || astride > 16) return FP16_ERR_SHAPE;
   if (wf_given && d.layout != FP16_NHWC) return FP16_ERR_UNSUPPORTED;
-  if (amask && (!addend || d.layout != FP16_NHWC || d.C % 8 != 0 || d.accum))
-    return addend ? FP16_ERR_UNSUPPORTED : FP16_ERR_NULL;
+  if ((amask || astride > 1) && !addend) return FP16_ERR_NULL;
+  if ((amask || astride > 1) && (d.layout != FP16_NHWC || d.accum)) return FP16_ERR_UNSUPPORTED;
+  if (amask && d.C % 8 != 0) return FP16_ERR_UNSUPPORTED;
   // the binary16 chains: the plain data gradient from the filter only
   if (d.accum && (wf_given || addend)) return FP16_ERR_UNSUPPORTED;
   if (!aligned16(dy) || !aligned16(w) || !aligned16(dx) || (addend && !aligned16(addend)))
@@ -278,10 +281,15 @@ static fp16_status conv_dgrad_impl(const fp16_conv_desc* desc, const fp16_t* dy,
   if ((s = check_ws(L, ws, ws_bytes)) != FP16_OK) return s;
   const size_t xb = (size_t)d.x_elems * 2;
   const size_t wb = wf_given ? dgrad_filter_bytes(d) : (size_t)d.w_elems * 2;
+  // the addend's bytes: dx's, or those of the subsampled grid
+  const size_t ab = astride > 1 ? (size_t)d.N * ((d.H + astride - 1) / astride) *
+                                      ((d.W + astride - 1) / astride) * d.C * 2
+                                : xb;
+  if (astride > 1 && addend == dx) return FP16_ERR_ALIASING;
   if (overlap(dx, xb, dy, (size_t)d.y_elems * 2) || overlap(dx, xb, w, wb) ||
-      overlap(dx, xb, ws, L.total) || (addend && addend != dx && overlap(dx, xb, addend, xb)) ||
-      (addend && overlap(addend, xb, ws, L.total)) ||
-      (amask && (overlap(amask, xb / 16, dx, xb) || overlap(amask, xb / 16, ws, L.total))))
+      overlap(dx, xb, ws, L.total) || (addend && addend != dx && overlap(dx, xb, addend, ab)) ||
+      (addend && overlap(addend, ab, ws, L.total)) ||
+      (amask && (overlap(amask, ab / 16, dx, xb) || overlap(amask, ab / 16, ws, L.total))))
     return FP16_ERR_ALIASING;
   hipStream_t st = static_cast<hipStream_t>(stream);
   const h16* dye = reinterpret_cast<const h16*>(dy);
@@ -314,6 +322,7 @@ static fp16_status conv_dgrad_impl(const fp16_conv_desc* desc, const fp16_t* dy,
   a.Co = d.C; a.out = dxe; a.OH = d.H; a.OW = d.W; a.ldo = d.C; a.os_h = d.sh; a.os_w = d.sw;
   a.addend = addend ? (d.layout == FP16_NCHW ? dxe : reinterpret_cast<const h16*>(addend)) : nullptr;
   a.amask = amask;
+  a.astride = astride;
   a.nphase = 0;
   int64_t off = 0;
   for (int ph = 0; ph < d.sh; ++ph) {
@@ -421,6 +430,14 @@ fp16_status fp16_conv_dgrad_wf_m(const fp16_conv_desc* desc, const fp16_t* dy, c
                                  void* ws, size_t ws_bytes, fp16_stream_t stream) {
   if (!addend || !addend_mask) return FP16_ERR_NULL;
   return conv_dgrad_impl(desc, dy, wf, addend, dx, ws, ws_bytes, stream, true, addend_mask);
+}
+
+fp16_status fp16_conv_dgrad_wf_ex(const fp16_conv_desc* desc, const fp16_t* dy, const fp16_t* wf,
+                                  const fp16_t* addend, const uint8_t* addend_mask,
+                                  int32_t addend_stride, fp16_t* dx, void* ws, size_t ws_bytes,
+                                  fp16_stream_t stream) {
+  return conv_dgrad_impl(desc, dy, wf, addend, dx, ws, ws_bytes, stream, true, addend_mask,
+                         addend_stride);
 }
 
 }  // extern "C"

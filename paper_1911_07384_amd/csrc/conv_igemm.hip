@@ -67,6 +67,14 @@ __device__ __forceinline__ V8 addend8(const IgemmArgs& a, int64_t off) {
   const V8 v = load16(a.addend + off);
   return a.amask ? masked8(v, a.amask[off >> 3]) : v;
 }
+// Element offset in the addend of output pixel (img, oh, ow), or -1 where a
+// strided addend (IgemmArgs::astride) has no element (the pixel adds +0).
+__device__ __forceinline__ int64_t addend_row(const IgemmArgs& a, int img, int oh, int ow) {
+  if (a.astride <= 1) return ((int64_t)(img * a.OH + oh) * a.OW + ow) * a.ldo;
+  if (oh % a.astride != 0 || ow % a.astride != 0) return -1;
+  const int AH = (a.OH + a.astride - 1) / a.astride, AW = (a.OW + a.astride - 1) / a.astride;
+  return ((int64_t)(img * AH + oh / a.astride) * AW + ow / a.astride) * a.ldo;
+}
 // one element of the addend, under the mask
 __device__ __forceinline__ float addend1(const IgemmArgs& a, int64_t i) {
   const float v = to_f32(a.addend[i]);
@@ -291,7 +299,8 @@ __global__ __launch_bounds__(256) void igemm_kernel(const IgemmArgs a) {
         for (int e = 0; e < 8; ++e) v[e] = src[e];
         if (vec_ok) {
           if (a.addend) {
-            const V8 ad = addend8(a, off);
+            const int64_t ar = addend_row(a, img, oh, ow);
+            const V8 ad = ar >= 0 ? addend8(a, ar + n) : zero8();
 #pragma unroll
             for (int e = 0; e < 8; ++e) v[e] += to_f32(ad.h[e]);
           }
@@ -304,7 +313,10 @@ __global__ __launch_bounds__(256) void igemm_kernel(const IgemmArgs a) {
           for (int e = 0; e < 8; ++e) {
             if (n + e < a.Co) {
               float x = v[e];
-              if (a.addend) x += addend1(a, off + e);
+              if (a.addend) {
+                const int64_t ar = addend_row(a, img, oh, ow);
+                x += ar >= 0 ? addend1(a, ar + n + e) : 0.0f;
+              }
               a.out[off + e] = to_h16(x);
             }
           }
@@ -538,7 +550,8 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
           for (int e = 0; e < 8; ++e) v[e] = src[e];
           if (vec_ok) {
             if (a.addend) {
-              const V8 ad = addend8(a, off);
+              const int64_t ar = addend_row(a, img, oh, ow);
+            const V8 ad = ar >= 0 ? addend8(a, ar + n) : zero8();
 #pragma unroll
               for (int e = 0; e < 8; ++e) v[e] += to_f32(ad.h[e]);
             }
@@ -559,7 +572,10 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
             for (int e = 0; e < 8; ++e) {
               if (n + e < a.Co) {
                 float x = v[e];
-                if (a.addend) x += addend1(a, off + e);
+                if (a.addend) {
+                  const int64_t ar = addend_row(a, img, oh, ow);
+                  x += ar >= 0 ? addend1(a, ar + n + e) : 0.0f;
+                }
                 a.out[off + e] = to_h16(x);
               }
             }
@@ -745,16 +761,33 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
     // the tile's addend, loaded before the MFMAs in the store layout (lane:
     // chunk lane % SLOTS of pixel lane / SLOTS + PPI*i; clamped into range)
     // (and with MASK the addend's ReLU mask bytes, applied where it is added)
+    // (a strided addend: the row of each of the lane's pixels, or +0)
     V8 adv[ADD ? TN / SW : 1][ADD ? 32 / PPI : 1];
     uint32_t amb[MASK ? TN / SW : 1][MASK ? 32 / PPI : 1];
+    bool aok[ADD ? 32 / PPI : 1];
     if (ADD) {
+      int64_t arow[32 / PPI];
+#pragma unroll
+      for (int i = 0; i < 32 / PPI; ++i) {
+        const int m = band_m0 + lane / SLOTS + i * PPI;
+        const int mc = m < M ? m : M - 1;
+        arow[i] = (int64_t)mc * a.ldo;
+        aok[i] = true;
+        if (a.astride > 1) {
+          const int img = mc / HoWo;
+          const int rem = mc - img * HoWo;
+          const int oh = rem / ph.Wo;
+          const int64_t r = addend_row(a, img, oh, rem - oh * ph.Wo);
+          aok[i] = r >= 0;
+          arow[i] = r >= 0 ? r : 0;
+        }
+      }
 #pragma unroll
       for (int g = 0; g < TN / SW; ++g)
 #pragma unroll
         for (int i = 0; i < 32 / PPI; ++i) {
-          const int m = band_m0 + lane / SLOTS + i * PPI;
           const int n = n0 + g * SW * 32 + (lane % SLOTS) * 8;
-          const int64_t off = (int64_t)(m < M ? m : M - 1) * a.ldo + (n < a.Co ? n : 0);
+          const int64_t off = arow[i] + (n < a.Co ? n : 0);
           adv[g][i] = load16(a.addend + off);
           if (MASK) amb[g][i] = a.amask[off >> 3];
         }
@@ -853,7 +886,8 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
             w[4 * j + 2] = f.z;
             w[4 * j + 3] = f.w;
           }
-          const V8 ad = MASK ? masked8(adv[g][i], amb[g][i]) : adv[g][i];
+          V8 ad = MASK ? masked8(adv[g][i], amb[g][i]) : adv[g][i];
+          if (!aok[i]) ad = zero8();
 #pragma unroll
           for (int e = 0; e < 8; ++e) o.h[e] = to_h16(w[e] + to_f32(ad.h[e]));
         } else {
@@ -1289,13 +1323,15 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
 #pragma unroll
     for (int tm = 0; tm < TM; ++tm) {
       const int m = m0 + wm * 32 * TM + tm * 32 + lrow;
-      int64_t base = 0;
+      int64_t base = 0, abase = -1;  // abase: the addend's row, -1 for +0
       if (m < M) {
         const int img = m / HoWo;
         const int rem = m - img * HoWo;
         const int i = rem / ph.Wo;
         const int j = rem - i * ph.Wo;
-        base = ((int64_t)(img * a.OH + i * a.os_h + ph.oph) * a.OW + j * a.os_w + ph.opw) * a.ldo;
+        const int oh = i * a.os_h + ph.oph, ow = j * a.os_w + ph.opw;
+        base = ((int64_t)(img * a.OH + oh) * a.OW + ow) * a.ldo;
+        if (a.addend) abase = addend_row(a, img, oh, ow);
       }
       if (a.addend && (a.ldo % 8) == 0) {
         // the addend first, so its loads overlap the swaps and conversions
@@ -1304,7 +1340,7 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
 #pragma unroll
           for (int h = 0; h < 2; ++h) {
             const int n = n0 + wn * 32 * TN + tn * 32 + h * 16 + lhi * 8;
-            if (m < M && n + 8 <= a.Co) adv[tm][tn][h] = load16(a.addend + base + n);
+            if (abase >= 0 && n + 8 <= a.Co) adv[tm][tn][h] = load16(a.addend + abase + n);
           }
         if (a.amask) {
 #pragma unroll
@@ -1312,7 +1348,7 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
               const int n = n0 + wn * 32 * TN + tn * 32 + h * 16 + lhi * 8;
-              if (m < M && n + 8 <= a.Co) amb[tm][tn][h] = a.amask[(base + n) >> 3];
+              if (abase >= 0 && n + 8 <= a.Co) amb[tm][tn][h] = a.amask[(abase + n) >> 3];
             }
         }
       }
@@ -1336,7 +1372,8 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
 #pragma unroll
             for (int e = 0; e < 8; ++e) w[e] = v[h * 8 + e];
             if (a.addend) {
-              const V8 ad = a.amask ? masked8(adv[tm][tn][h], amb[tm][tn][h]) : adv[tm][tn][h];
+              V8 ad = a.amask ? masked8(adv[tm][tn][h], amb[tm][tn][h]) : adv[tm][tn][h];
+              if (abase < 0) ad = zero8();
 #pragma unroll
               for (int e = 0; e < 8; ++e) w[e] += to_f32(ad.h[e]);
             }
@@ -1349,7 +1386,9 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
             for (int e = 0; e < 8; ++e) {
               if (n + e < a.Co) {
                 float x = v[h * 8 + e];
-                if (a.addend) x += addend1(a, off + e);
+                if (a.addend) {
+                  x += abase >= 0 ? addend1(a, abase + n + e) : 0.0f;
+                }
                 a.out[off + e] = to_h16(x);
               }
             }
@@ -1407,7 +1446,8 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
         for (int e = 0; e < 8; ++e) v[e] = src[e];
         if (vec_ok) {
           if (a.addend) {
-            const V8 ad = addend8(a, off);
+            const int64_t ar = addend_row(a, img, oh, ow);
+            const V8 ad = ar >= 0 ? addend8(a, ar + n) : zero8();
 #pragma unroll
             for (int e = 0; e < 8; ++e) v[e] += to_f32(ad.h[e]);
           }
@@ -1420,7 +1460,10 @@ __global__ __launch_bounds__(256) void igemm7_kernel(const IgemmArgs a) {
           for (int e = 0; e < 8; ++e) {
             if (n + e < a.Co) {
               float x = v[e];
-              if (a.addend) x += addend1(a, off + e);
+              if (a.addend) {
+                const int64_t ar = addend_row(a, img, oh, ow);
+                x += ar >= 0 ? addend1(a, ar + n + e) : 0.0f;
+              }
               a.out[off + e] = to_h16(x);
             }
           }

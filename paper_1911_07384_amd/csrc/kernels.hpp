@@ -48,9 +48,13 @@ struct IgemmArgs {
   h16* out;        // NHWC output [N][OH][OW][ldo], writes channels [0, Co)
   const h16* addend;  // nullable, laid out like out: out = rne16(acc + addend)
   // nullable (needs addend, ldo == Co, Co % 8 == 0): a ReLU mask over the
-  // addend, bit (i % 8) of byte i / 8 for element i of out's layout; an
-  // element whose bit is clear adds +0 instead of the addend
+  // addend, bit (i % 8) of byte i / 8 for element i of the addend's layout;
+  // an element whose bit is clear adds +0 instead of the addend
   const uint8_t* amask;
+  // 0 or 1: the addend is laid out like out; s > 1: it holds only the output
+  // pixels whose row and column are multiples of s, as [N][ceil(OH/s)]
+  // [ceil(OW/s)][ldo], and every other pixel adds +0
+  int astride;
   int OH, OW, ldo;
   int os_h, os_w;
   int nphase;

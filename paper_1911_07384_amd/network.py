@@ -273,26 +273,32 @@ class ResNet50:
         self.bwd.append(Op("bn_bwd", name, a))
         return dx
 
-    def _conv_bwd(self, name, dy, dx_needed=True, addend=None, dx_name=None, mask_of=None):
+    def _conv_bwd(self, name, dy, dx_needed=True, addend=None, dx_name=None, mask_of=None,
+                  dgrad_desc=None, addend_stride=1):
+        """The data gradient (with dgrad_desc: computed as that problem instead,
+        e.g. a strided 1x1 convolution's on its own output grid) and the weight
+        gradient of convolution `name`."""
         c = self._conv_op(name)
         if dx_needed:
             dx = dx_name or self._grad(c["x"])
+            dd = dgrad_desc or c["desc"]
             # the filter is rearranged for the data gradient during the forward
             # (on the side stream, off the critical path); the data gradient
             # reads the rearranged copy
             wf = name + ".wf"
-            self._buf(wf, (F.fp16_conv_dgrad_filter_bytes(c["desc"]) // 2,))
-            self.prep.append(Op("dgrad_filter", name, {"desc": c["desc"], "w": name, "wf": wf}))
+            self._buf(wf, (F.fp16_conv_dgrad_filter_bytes(dd) // 2,))
+            self.prep.append(Op("dgrad_filter", name, {"desc": dd, "w": name, "wf": wf}))
             if addend is None:
-                self.bwd.append(Op("conv_dgrad", name, {"desc": c["desc"], "dy": dy, "w": name,
+                self.bwd.append(Op("conv_dgrad", name, {"desc": dd, "dy": dy, "w": name,
                                                         "wf": wf, "dx": dx}))
             else:
                 # with mask_of, the addend is the gradient the BN mask_of
-                # received, taken under that BN's kept ReLU mask
+                # received, taken under that BN's kept ReLU mask; with
+                # addend_stride s, it holds every s-th row and column only
                 self.bwd.append(Op("conv_dgrad_add", name, {
-                    "desc": c["desc"], "dy": dy, "w": name, "wf": wf, "addend": addend,
+                    "desc": dd, "dy": dy, "w": name, "wf": wf, "addend": addend,
                     "amask": self._bn_op(mask_of).a["mask"] if mask_of else None,
-                    "mask_of": mask_of, "dx": dx}))
+                    "mask_of": mask_of, "astride": addend_stride, "dx": dx}))
         # the weight gradients beside the backward's other calls aim at about
         # one workgroup per CU; the first layer's, the last call of the
         # backward with nothing left to overlap, takes the default two
@@ -331,9 +337,24 @@ class ResNet50:
                 else:
                     dcd = self._bn_bwd(nm + ".bnd", dres, want_dres=False)
                 dsx = "dds:" + nm
-                self.buffers[dsx] = torch.empty_like(self.buffers[dxb])
-                self._conv_bwd(nm + ".ds", dcd, dx_name=dsx)
-                self._conv_bwd(nm + ".c1", dc1, addend=dsx, dx_name=dxb)
+                d = self._conv_op(nm + ".ds")["desc"]
+                if d.stride_h > 1:
+                    # a strided 1x1 shortcut's data gradient is nonzero on its
+                    # own grid only: computed there (a 1x1 stride-1 problem)
+                    # and added by the block input's data gradient as a
+                    # strided addend, instead of written out three zeros in four
+                    p, q = F.fp16_conv_out_dims(d)
+                    dc = F.conv_desc(d.n, d.c, p, q, d.k, 1, 1, 1, 0)
+                    self.buffers[dsx] = torch.empty((d.n, p, q, d.c), dtype=torch.float16,
+                                                    device=self.dev)
+                    self._ws_need = max(self._ws_need, F.fp16_conv_workspace_bytes(dc, F.PASS_DGRAD))
+                    self._conv_bwd(nm + ".ds", dcd, dx_name=dsx, dgrad_desc=dc)
+                    self._conv_bwd(nm + ".c1", dc1, addend=dsx, dx_name=dxb,
+                                   addend_stride=d.stride_h)
+                else:
+                    self.buffers[dsx] = torch.empty_like(self.buffers[dxb])
+                    self._conv_bwd(nm + ".ds", dcd, dx_name=dsx)
+                    self._conv_bwd(nm + ".c1", dc1, addend=dsx, dx_name=dxb)
             elif kept:
                 self._conv_bwd(nm + ".c1", dc1, addend=dout, dx_name=dxb, mask_of=nm + ".bn3")
             else:
@@ -412,12 +433,15 @@ class ResNet50:
         elif k == "conv_dgrad":
             F.fp16_conv_dgrad_wf(a["desc"], t(a["dy"]), t(a["wf"]), None, t(a["dx"]), ws)
         elif k == "conv_dgrad_add":
-            if a["amask"] is None:
+            if a["amask"] is None and a["astride"] == 1:
                 F.fp16_conv_dgrad_wf(a["desc"], t(a["dy"]), t(a["wf"]), t(a["addend"]), t(a["dx"]),
                                      ws)
-            else:
+            elif a["astride"] == 1:
                 F.fp16_conv_dgrad_wf_m(a["desc"], t(a["dy"]), t(a["wf"]), t(a["addend"]),
                                        t(a["amask"]), t(a["dx"]), ws)
+            else:
+                F.fp16_conv_dgrad_wf_ex(a["desc"], t(a["dy"]), t(a["wf"]), t(a["addend"]),
+                                        t(a["amask"]), a["astride"], t(a["dx"]), ws)
         elif k == "dgrad_filter":
             F.fp16_conv_dgrad_filter(a["desc"], t(a["w"]), t(a["wf"]))
         elif k == "dgrad_filters":

@@ -148,6 +148,16 @@ def test_dgrad_filter_validation():
         bad[3] = at
         assert gm(ctypes.byref(d), *bad) == ALIASING, hex(at)
     assert gm(ctypes.byref(d), *ok[:4], B + 64, WS, need, None) == ALIASING  # dx over wf
+    # the strided addend: dy, wf, addend, mask, stride, dx, ws
+    ge = lib.fp16_conv_dgrad_wf_ex
+    ex = [A, B, Cc + (8 << 20), None, 2, Cc, WS, need, None]
+    for bad_s in (0, -1, 17):
+        assert ge(ctypes.byref(d), *ex[:4], bad_s, *ex[5:]) == SHAPE
+    assert ge(ctypes.byref(d), *ex[:2], None, None, 2, *ex[5:]) == NULL
+    assert ge(ctypes.byref(_conv(layout="NCHW")), *ex[:7], 1 << 30, None) == UNSUPPORTED
+    assert ge(ctypes.byref(d), *ex[:2], Cc, None, 2, Cc, *ex[6:]) == ALIASING  # addend is dx
+    # the addend's own extent (a quarter of dx's at stride 2) over dx's tail
+    assert ge(ctypes.byref(d), *ex[:2], Cc + 2 * 56 * 56 * 64 * 2 - 64, None, 2, *ex[5:]) == ALIASING
 
 
 @pytest.mark.parametrize("hw,r,st,pad", [(56, 3, 1, 1), (56, 1, 2, 0), (224, 7, 2, 3), (7, 3, 1, 1),

@@ -74,3 +74,52 @@ def test_masked_addend(case, in_place):
         shp = oracle.conv_shape(n, c, h, w, k, r, r, st, pad)
         want64, _ = oracle.conv_dgrad_add(shp, dy, wt, adm)
         check_close(got, want64, what=f"dgrad_wf_m {case}")
+
+
+# (n, c, h, w, k, r, stride, pad, addend stride, with mask): fp16_conv_dgrad_wf_ex
+# with the addend on every s-th row and column
+STRIDED = [
+    (2, 256, 14, 14, 128, 1, 1, 0, 2, False),   # pointwise kernel (the conv3_x block input)
+    (2, 256, 15, 13, 64, 1, 1, 0, 2, False),    # pointwise, odd sides (ceil grid)
+    (2, 512, 14, 14, 256, 1, 1, 0, 2, False),   # register-direct kernel (the conv4_x block input)
+    (2, 1024, 7, 7, 512, 1, 1, 0, 2, False),    # DMA-staged kernel (the conv5_x block input)
+    (2, 16, 9, 9, 24, 3, 1, 1, 3, False),       # LDS-staged kernel, stride 3
+    (2, 64, 14, 14, 64, 3, 2, 1, 2, False),     # stride phases of the data gradient itself
+    (2, 256, 14, 14, 128, 1, 1, 0, 2, True),    # with a mask over the strided addend
+    (2, 512, 10, 10, 256, 1, 1, 0, 2, True),
+    (32, 256, 56, 56, 128, 1, 1, 0, 2, False),  # the conv3_x block input gradient at batch 32
+]
+
+
+@pytest.mark.parametrize("case", STRIDED, ids=[str(c) for c in STRIDED])
+def test_strided_addend(case):
+    require_gpu()
+    n, c, h, w, k, r, st, pad, s, with_mask = case
+    d = F.conv_desc(n, c, h, w, k, r, r, st, pad)
+    p, q = F.fp16_conv_out_dims(d)
+    ah, aw = -(-h // s), -(-w // s)
+    seed = 190 + c + k + s
+    dy = synth.normal_f16((n, p, q, k), 1e-2, seed, 1)
+    wt = synth.normal_f16((k, r, r, c), synth.he_std(c * r * r), seed, 2)
+    ad = synth.normal_f16((n, ah, aw, c), 1e-2, seed, 3)
+    mask = np.random.default_rng(seed).integers(0, 256, size=ad.size // 8, dtype=np.uint8)
+    adm = np.where(_bits(mask, ad.size).reshape(ad.shape), ad, np.float16(0.0)) if with_mask else ad
+    full = np.zeros((n, h, w, c), np.float16)
+    full[:, ::s, ::s, :] = adm
+    DY, W, AD, FULL = dev(dy), dev(wt), dev(ad), dev(full)
+    M = torch.from_numpy(mask).to("cuda") if with_mask else None
+    WF = torch.empty(F.fp16_conv_dgrad_filter_bytes(d) // 2, dtype=torch.float16, device="cuda")
+    ws = F.workspace(F.fp16_conv_workspace_bytes(d, F.PASS_DGRAD))
+    note(f"[gpu] dgrad_wf_ex {case}")
+    F.fp16_conv_dgrad_filter(d, W, WF)
+    ref = torch.empty_like(FULL)
+    F.fp16_conv_dgrad_wf(d, DY, WF, FULL, ref, ws)
+    DX = torch.full_like(FULL, float("nan"))
+    F.fp16_conv_dgrad_wf_ex(d, DY, WF, AD, M, s, DX, ws)
+    torch.cuda.synchronize()
+    got = host(DX)
+    assert np.array_equal(got.view(np.uint16), host(ref).view(np.uint16))
+    if n * h * w * c <= 1 << 20:
+        shp = oracle.conv_shape(n, c, h, w, k, r, r, st, pad)
+        want64, _ = oracle.conv_dgrad_add(shp, dy, wt, full)
+        check_close(got, want64, what=f"dgrad_wf_ex {case}")

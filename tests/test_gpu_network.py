@@ -83,14 +83,22 @@ def bn_out(net, name, H):
 
 
 def masked_addend(a, H):
-    """The addend of a block input's data gradient: with a mask, the
-    block-last BN's incoming gradient where that BN's output is positive and
-    +0 elsewhere (the shortcut gradient of Section 4.1 through the ReLU)."""
+    """The addend of a block input's data gradient as a full-size tensor: with
+    a mask, the block-last BN's incoming gradient where that BN's output is
+    positive and +0 elsewhere (the shortcut gradient of Section 4.1 through
+    the ReLU); with a stride s, the strided shortcut's gradient placed on every
+    s-th row and column, +0 elsewhere."""
     ad = H[a["addend"]]
-    if a.get("amask") is None:
-        return ad
-    pos = H[a["mask_of"] + ".y"].astype(np.float32) > 0
-    return np.where(pos, ad, np.float16(0.0))
+    if a.get("amask") is not None:
+        pos = H[a["mask_of"] + ".y"].astype(np.float32) > 0
+        ad = np.where(pos, ad, np.float16(0.0))
+    s = a.get("astride", 1)
+    if s > 1:
+        d = a["desc"]
+        full = np.zeros((d.n, d.h, d.w, d.c), np.float16)
+        full[:, ::s, ::s, :] = ad
+        ad = full
+    return ad
 
 
 def _check_op(net, op, H):

@@ -4,6 +4,8 @@ buffer a call reads is written earlier in the step, and no buffer is written
 twice."""
 
 import numpy as np
+
+import paper_1911_07384_amd as F
 import pytest
 
 from paper_1911_07384_amd.network import ResNet50
@@ -130,6 +132,26 @@ def test_stem_bn_feeds_the_pool_directly(net):
     assert b.a["y"] is None and b.a["mask"] is None and b.a["x"] == "stem.y"
     plain = ResNet50(n=1, image=64, device="cpu", fuse_bn_stats=False)
     assert [o.kind for o in plain.fwd[:3]] == ["conv_fwd", "bn_fwd", "maxpool_fwd"]
+
+
+def test_strided_shortcut_gradient_on_its_own_grid(net):
+    # a stride-2 1x1 shortcut's data gradient is a 1x1 stride-1 problem on the
+    # shortcut's output grid, added by the block input's data gradient at stride 2
+    for st in (2, 3, 4):
+        blk = f"l{st}.0"
+        ds = next(o for o in net.bwd if o.name == blk + ".ds" and o.kind == "conv_dgrad")
+        add = next(o for o in net.bwd if o.name == blk + ".c1" and o.kind == "conv_dgrad_add")
+        fwd = next(c for c in net.convs if c["name"] == blk + ".ds")["desc"]
+        d = ds.a["desc"]
+        p, q = F.fp16_conv_out_dims(fwd)
+        assert (d.n, d.c, d.h, d.w, d.k, d.r, d.s, d.stride_h, d.pad_h) == \
+            (fwd.n, fwd.c, p, q, fwd.k, 1, 1, 1, 0)
+        assert tuple(net.buffers[ds.a["dx"]].shape) == (fwd.n, p, q, fwd.c)
+        assert add.a["addend"] == ds.a["dx"] and add.a["astride"] == 2
+        wgrad = next(o for o in net.bwd if o.name == blk + ".ds" and o.kind == "conv_wgrad")
+        assert wgrad.a["desc"] is fwd
+    l1 = next(o for o in net.bwd if o.name == "l1.0.c1" and o.kind == "conv_dgrad_add")
+    assert l1.a["astride"] == 1
 
 
 def test_forward_shortcut_branches(net):
