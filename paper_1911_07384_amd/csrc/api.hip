@@ -971,7 +971,7 @@ static fp16_status conv_bn_impl(const fp16_conv_desc* conv, const fp16_bn_desc* 
                                     reinterpret_cast<h16*>(z), stats, 0, part, mout, st));
   }
   a.stat = part;
-  a.stat_nb = conv_bn_nb(d);
+  a.stat_nb = igemm_stat_records(a);  // at most conv_bn_nb(d), which sizes the space
   TRY(launch_igemm(a, st));
   void* band_ws = reinterpret_cast<char*>(part) +
                   align256((size_t)3 * d.K * a.stat_nb * sizeof(float));

@@ -381,8 +381,10 @@ __global__ __launch_bounds__(64 * kFinW) void bn_fwd_finalize_bm(const h16* __re
 }
 
 // Statistics from the records a convolution's epilogue wrote ([nb][3][C]:
-// per 128-row tile b and channel c a shift K_b (its first value) and the sums
-// of (y - K_b) and (y - K_b)^2 over its n_b rows).  About K_0:
+// record b covers the 128-row tiles b, b + nb, b + 2nb, ... (one tile each
+// where nb is the tile count) and holds per channel c a shift K_b (one of its
+// values) and the sums of (y - K_b) and (y - K_b)^2 over its n_b rows).
+// About K_0:
 //   S1 = sum_b s1_b + n_b d_b,  S2 = sum_b s2_b + 2 d_b s1_b + n_b d_b^2,
 // d_b = K_b - K_0, in float64.  Up to kBandOne records: bn_band_finalize, one
 // 256-thread block per channel; thread t takes records t, t + 256, ... in
@@ -399,11 +401,21 @@ __global__ __launch_bounds__(64 * kFinW) void bn_fwd_finalize_bm(const h16* __re
 constexpr int kBandOne = 2048;
 constexpr int kBandRps = 32;  // records per slice: 8 per wave
 
+// Rows of record j of nb over M rows: 128 per tile it covers, less the
+// last tile's missing rows where that tile is its.
+__device__ __forceinline__ int64_t band_rows(int64_t M, int nb, int j) {
+  const int64_t nt = (M + 127) / 128;
+  if (j >= nt) return 0;
+  int64_t r = 128 * ((nt - 1 - j) / nb + 1);
+  if (j == (nt - 1) % nb) r -= 128 * nt - M;
+  return r;
+}
+
 // One record's terms; a record past the last adds exact zeros, so that its
 // (clamped, in-bounds) loads stay unconditional and in flight together.
 __device__ __forceinline__ void band_term_if(bool ok, int64_t rows, float k, double K0, float s1,
                                              float s2, double& a, double& b) {
-  const double n = ok ? (double)(rows < 128 ? rows : 128) : 0.0;
+  const double n = ok ? (double)rows : 0.0;
   const double d = ok ? (double)k - K0 : 0.0;
   const double t1 = ok ? (double)s1 : 0.0, t2 = ok ? (double)s2 : 0.0;
   a += t1 + n * d;
@@ -441,7 +453,7 @@ __global__ __launch_bounds__(256) void bn_band_finalize(const float* __restrict_
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int j = j0 + 256 * u;
-      band_term_if(j < nb, g.M - (int64_t)j * 128, k[u], K0, s1[u], s2[u], a, b);
+      band_term_if(j < nb, band_rows(g.M, nb, j), k[u], K0, s1[u], s2[u], a, b);
     }
   }
 #pragma unroll
@@ -482,7 +494,7 @@ __global__ __launch_bounds__(256) void bn_band_slices(const float* __restrict__ 
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int j = s * kBandRps + w + 4 * u;
-      band_term_if(j < nb, g.M - (int64_t)j * 128, k[u], K0, s1[u], s2[u], a, b);
+      band_term_if(j < nb, band_rows(g.M, nb, j), k[u], K0, s1[u], s2[u], a, b);
     }
   }
   red[0][w][lane] = a;

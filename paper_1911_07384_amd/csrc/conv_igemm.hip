@@ -656,11 +656,16 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
 //    that path instead (the addend joins before the one rounding), and the
 //    addend (and its ReLU mask, one byte per 16-byte chunk) is read in the
 //    same whole-line layout;
-//  - with BN statistics the plain product D = X x W is computed too (the
-//    MFMAs are cheap here), whose layout gives each lane one channel and 16
-//    rows: the band sums are taken in the lane and kept in registers, and the
-//    four waves' bands of a tile are combined into one 128-row record as in
-//    igemm4_kernel, through the same LDS space.
+//  - BN statistics are taken from the rounded values each lane reads back
+//    for its stores (8 channels of a few pixels per store group): per
+//    channel, (y - K) and its square are added into the lane's float32 sums,
+//    kept in registers over every tile the wave walks, about a shift K per
+//    channel (the value in the wave's first row, kept in LDS); after the last
+//    tile the lanes holding the same channels are added up, and the four
+//    waves are combined once into one record covering the tiles blockIdx.x,
+//    blockIdx.x + gridDim.x, ... (no barrier per tile).  A lane holds
+//    BN / 8 channels over 64 input channels and BN / 4 over 128: at most 32
+//    (64 would leave one wave per SIMD).
 // Each output element is the same k-ordered sum of exact products in both
 // MFMA forms, so the values equal the other kernels' bit for bit.
 template <int CI, int BN, bool STATS, bool ADD>
@@ -674,7 +679,8 @@ struct CfgPw {
   static constexpr int STG = 4 * 32 * SW * (ADD ? 128 : 64);
   static constexpr int BST = STATS ? 4 * 3 * BN * 4 : 0;  // [wave][K, s1, s2][BN]
   static constexpr int SHARED = STG > BST ? STG : BST;
-  static constexpr int LDS = BBYTES + SHARED + (STATS ? 16 : 0);  // (+ 4 band row counts)
+  // (+ 4 wave row counts and the waves' shifts, [wave][BN] binary16)
+  static constexpr int LDS = BBYTES + SHARED + (STATS ? 16 + 4 * BN * 2 : 0);
 };
 
 __device__ __forceinline__ void lane_half_swap(float& x, float& y) {
@@ -702,6 +708,8 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
   static_assert(!(STATS && ADD), "statistics are taken without an addend");
   static_assert(ADD || !MASK, "a mask is over the addend");
   static_assert(TN % SW == 0, "store groups");
+  constexpr int NG = TN / SW;         // store groups
+  static_assert(!STATS || NG * 8 <= 32, "statistics: at most 32 channels per lane");
   __shared__ __attribute__((aligned(1024))) char lds[K::LDS];
   char* bt = lds;
   char* shared = lds + K::BBYTES;
@@ -716,6 +724,8 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int lrow = lane & 31, lhi = lane >> 5;
   char* stg = shared + wave * 32 * SLOTS * (ADD ? 32 : 16);
+  // the wave's shifts: channel n0 + i at kst[i]
+  h16* kst = reinterpret_cast<h16*>(lds + K::BBYTES + K::SHARED + 16) + wave * BN;
   constexpr uint32_t OOB = 0x80000000u;
   const int act_bytes = (int)((int64_t)a.N * a.Hi * a.Wi * CI * 2);
   const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
@@ -752,6 +762,19 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
                                             rs_a, o == OOB ? OOB : o + ks * 32, 0, 0));
   };
   half8 Acur[KS], Anext[KS];
+  // the lane's running sums of (y - K) and (y - K)^2 for channel e of its
+  // chunk in store group g, over the pixels it stored; nrows: the wave's rows
+  float s1[STATS ? NG : 1][8], s2[STATS ? NG : 1][8];
+#pragma unroll
+  for (int g = 0; g < (STATS ? NG : 1); ++g)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      s1[g][e] = 0.0f;
+      s2[g][e] = 0.0f;
+    }
+  int nrows = 0;
+  h16 one = (h16)1.0f;
+  asm("" : "+v"(one));  // kept opaque, so that y * one is not folded into y
   int tile = blockIdx.x;
   load_a(Acur, row_off(tile));
   __syncthreads();
@@ -793,24 +816,24 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
         }
     }
     load_a(Anext, row_off(tile + gridDim.x));
-    float bk[STATS ? TN : 1], b1[STATS ? TN : 1], b2[STATS ? TN : 1];
+    const bool first = tile == (int)blockIdx.x;
+    if (STATS) {
+      const int rows = M - band_m0;
+      nrows += rows <= 0 ? 0 : (rows < 32 ? rows : 32);
+    }
 #pragma unroll
     for (int g = 0; g < TN / SW; ++g) {
 #pragma unroll
       for (int tl = 0; tl < SW; ++tl) {
         const int tn = g * SW + tl;
-        floatx16 at, an;
+        floatx16 at;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          at[e] = 0.0f;
-          an[e] = 0.0f;
-        }
+        for (int e = 0; e < 16; ++e) at[e] = 0.0f;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           const int pos = ((ks * 2 + lhi) ^ swz) * 16;
           const half8 bf = *reinterpret_cast<const half8*>(bt + (tn * 32 + lrow) * (CI * 2) + pos);
           at = mfma32x32x16(bf, Acur[ks], at);
-          if (STATS) an = mfma32x32x16(Acur[ks], bf, an);
         }
         float v[16];
 #pragma unroll
@@ -845,32 +868,22 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
             *reinterpret_cast<V8*>(stg + (lrow * SLOTS + slot) * 16) = o;
           }
         }
-        if (STATS) {
-          // plain layout: lane holds channel tn*32 + lane % 32 and band rows
-          // 8*(e/4) + 4*(lane/32) + e%4; the shift is the band's first row
-          float y[16];
-#pragma unroll
-          for (int e = 0; e < 16; ++e) y[e] = to_f32(to_h16(an[e]));
-          const float K0 = __shfl(y[0], lrow, 64);
-          float s1 = 0.0f, s2 = 0.0f;
-#pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int r = 8 * (e >> 2) + 4 * lhi + (e & 3);
-            const float d = band_m0 + r < M ? y[e] - K0 : 0.0f;
-            s1 += d;
-            s2 = __builtin_fmaf(d, d, s2);
-          }
-          s1 += __shfl_xor(s1, 32, 64);
-          s2 += __shfl_xor(s2, 32, 64);
-          bk[tn] = K0;
-          b1[tn] = s1;
-          b2[tn] = s2;
-        }
       }
       wave_lds_sync();
       // lane: chunk lane % SLOTS of pixel lane / SLOTS (+ PPI per instruction)
       const int c = lane % SLOTS;
       const int n = n0 + g * SW * 32 + c * 8;
+      V8 kv;
+      if (STATS) {
+        if (first) {
+          // the shifts: the values of the wave's first row (staged pixel 0)
+          if (lane < SLOTS)
+            *reinterpret_cast<V8*>(kst + g * SW * 32 + lane * 8) =
+                *reinterpret_cast<const V8*>(stg + lane * 16);
+          wave_lds_sync();
+        }
+        kv = *reinterpret_cast<const V8*>(kst + g * SW * 32 + c * 8);
+      }
 #pragma unroll
       for (int i = 0; i < 32 / PPI; ++i) {
         const int q = lane / SLOTS + i * PPI;
@@ -895,50 +908,73 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
         }
         const int m = band_m0 + q;
         if (m < M && n < a.Co) store16(a.out + (int64_t)m * a.ldo + n, o);
+        if (STATS && m < M) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            // y * 1 - K, exact operands and one rounding: the same value as
+            // the difference of the two widened values, in one mixed-precision
+            // FMA that reads y's binary16 half directly
+            const float d = __builtin_fmaf(to_f32(o.h[e]), to_f32(one), -to_f32(kv.h[e]));
+            s1[g][e] += d;
+            s2[g][e] = __builtin_fmaf(d, d, s2[g][e]);
+          }
+        }
       }
       wave_lds_sync();
     }
-    if (STATS) {
-      __syncthreads();  // every wave is done with its staging buffer
-      if (lhi == 0) {
-#pragma unroll
-        for (int tn = 0; tn < TN; ++tn) {
-          bst[(wave * 3 + 0) * BN + tn * 32 + lrow] = bk[tn];
-          bst[(wave * 3 + 1) * BN + tn * 32 + lrow] = b1[tn];
-          bst[(wave * 3 + 2) * BN + tn * 32 + lrow] = b2[tn];
-        }
-      }
-      if (lane == 0) {
-        const int rows = M - band_m0;
-        bcnt[wave] = rows <= 0 ? 0 : (rows < 32 ? rows : 32);
-      }
-      __syncthreads();
-      // one record per 128-row tile: the bands re-based on the first band's
-      // shift, in wave order
-      for (int c = tid; c < BN; c += 256) {
-        if (bcnt[0] > 0 && n0 + c < a.Co) {
-          const float K0 = bst[c];
-          float S1 = 0.0f, S2 = 0.0f;
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            const float nw = (float)bcnt[w];
-            if (bcnt[w] == 0) break;
-            const float d = bst[(w * 3) * BN + c] - K0;
-            const float t1 = bst[(w * 3 + 1) * BN + c];
-            S1 += __builtin_fmaf(nw, d, t1);
-            S2 += __builtin_fmaf(nw * d, d,
-                                 __builtin_fmaf(2.0f * d, t1, bst[(w * 3 + 2) * BN + c]));
-          }
-          float* rec = a.stat + (int64_t)tile * 3 * a.Co + n0 + c;
-          rec[0] = K0;
-          rec[a.Co] = S1;
-          rec[2 * a.Co] = S2;
-        }
-      }
-      __syncthreads();
-    }
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) Acur[ks] = Anext[ks];
+  }
+  if (STATS) {
+    // lanes l, l + SLOTS, l + 2*SLOTS, ... hold the same channels: add them
+    // up (fixed order), then lane l < SLOTS writes its chunks' band sums
+#pragma unroll
+    for (int off = SLOTS; off < 64; off *= 2)
+#pragma unroll
+      for (int g = 0; g < NG; ++g)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          s1[g][e] += __shfl_xor(s1[g][e], off, 64);
+          s2[g][e] += __shfl_xor(s2[g][e], off, 64);
+        }
+    __syncthreads();  // every wave is done with its staging buffer
+    if (lane < SLOTS) {
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        const V8 kv = *reinterpret_cast<const V8*>(kst + g * SW * 32 + lane * 8);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const int ch = g * SW * 32 + lane * 8 + e;
+          bst[(wave * 3 + 0) * BN + ch] = to_f32(kv.h[e]);
+          bst[(wave * 3 + 1) * BN + ch] = s1[g][e];
+          bst[(wave * 3 + 2) * BN + ch] = s2[g][e];
+        }
+      }
+    }
+    if (lane == 0) bcnt[wave] = nrows;
+    __syncthreads();
+    // the workgroup's record: the waves re-based on wave 0's shift, in wave
+    // order (wave 0 always has rows: the first tile starts inside M)
+    for (int c = tid; c < BN; c += 256) {
+      if (n0 + c < a.Co) {
+        const float K0 = bst[c];
+        float S1 = 0.0f, S2 = 0.0f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          const float nw = (float)bcnt[w];
+          if (bcnt[w] == 0) break;
+          const float d = bst[(w * 3) * BN + c] - K0;
+          const float t1 = bst[(w * 3 + 1) * BN + c];
+          S1 += __builtin_fmaf(nw, d, t1);
+          S2 += __builtin_fmaf(nw * d, d,
+                               __builtin_fmaf(2.0f * d, t1, bst[(w * 3 + 2) * BN + c]));
+        }
+        float* rec = a.stat + (int64_t)blockIdx.x * 3 * a.Co + n0 + c;
+        rec[0] = K0;
+        rec[a.Co] = S1;
+        rec[2 * a.Co] = S2;
+      }
+    }
   }
 }
 
@@ -1577,16 +1613,30 @@ hipError_t launch_c3(const IgemmArgs& a, int tpi, hipStream_t st) {
   return hipGetLastError();
 }
 
+// workgroups along the rows of the pointwise kernel, which walk the 128-row
+// tiles: about six tiles each at ResNet-50's sizes, where the filter tile's
+// load into LDS is paid once per workgroup (batch 128, with statistics: the
+// conv2_x layer 56 us at 512 groups, 64-66 us at 256 or 1024; the conv3_x
+// layer on 128-channel tiles 51 us at 128 groups, 54-58 at 64 or 96, 64 at
+// 192 and 74 at 512)
+static int pw_row_groups(int ntiles, int ci, bool stats) {
+  const int cap = ci == 128 && stats ? 128 : 512;
+  return ntiles < cap ? ntiles : cap;
+}
+
 template <int CI, int BN>
 hipError_t launch_pw(const IgemmArgs& a, hipStream_t st) {
   const int M = a.N * a.ph[0].Ho * a.ph[0].Wo;
   if (M == 0) return hipSuccess;
   const int ntiles = ceil_div(M, 128);
-  // two to three workgroups per CU walk the tiles
-  dim3 grid(ntiles < 512 ? ntiles : 512, ceil_div(a.Co, BN));
-  if (a.stat)
-    hipLaunchKernelGGL((pw_kernel<CI, BN, true, false, false>), grid, dim3(256), 0, st, a, ntiles);
-  else if (a.addend && a.amask)
+  dim3 grid(pw_row_groups(ntiles, CI, a.stat != nullptr), ceil_div(a.Co, BN));
+  if (a.stat) {
+    if constexpr (BN / (CI == 64 ? 8 : 4) <= 32)  // the lane's channels: see pw_kernel
+      hipLaunchKernelGGL((pw_kernel<CI, BN, true, false, false>), grid, dim3(256), 0, st, a,
+                         ntiles);
+    else
+      return hipErrorInvalidValue;
+  } else if (a.addend && a.amask)
     hipLaunchKernelGGL((pw_kernel<CI, BN, false, true, true>), grid, dim3(256), 0, st, a, ntiles);
   else if (a.addend)
     hipLaunchKernelGGL((pw_kernel<CI, BN, false, true, false>), grid, dim3(256), 0, st, a, ntiles);
@@ -1846,6 +1896,11 @@ bool igemm_stats_pay(const IgemmArgs& a) {
   return !(igemm_kind(b) == IgemmKind::kDma && (int64_t)a.N * a.OH * a.OW >= 100352);
 }
 
+int igemm_stat_records(const IgemmArgs& a) {
+  const int ntiles = ceil_div(a.N * a.ph[0].Ho * a.ph[0].Wo, 128);
+  return igemm_kind(a) == IgemmKind::kPointwise ? pw_row_groups(ntiles, a.Ci, true) : ntiles;
+}
+
 bool igemm_takes_stats(const IgemmArgs& a) {
   // the kernel that would run with statistics requested (the 3x3 kernel
   // leaves them to the DMA-staged one)
@@ -1878,7 +1933,10 @@ hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st) {
         const bool narrow = a.stat && (int64_t)a.N * a.OH * a.OW <= 131072;
         return a.Co >= 256 && !narrow ? launch_pw<64, 256>(a, st) : launch_pw<64, 128>(a, st);
       }
-      return launch_pw<128, 256>(a, st);
+      // (statistics over 128 input channels: 128-channel tiles, 32 channels
+      // per lane and two waves per SIMD; 256-channel tiles with 64 per lane
+      // ran at one wave per SIMD, 59-61 us against 51)
+      return a.stat ? launch_pw<128, 128>(a, st) : launch_pw<128, 256>(a, st);
     default:
       return a.Co <= 64 ? launch_cfg<128, 64, 4, 1, 64>(a, st) : launch_cfg<128, 128, 2, 2, 64>(a, st);
   }

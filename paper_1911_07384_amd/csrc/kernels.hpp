@@ -61,9 +61,10 @@ struct IgemmArgs {
   IgemmPhase ph[4];
   // Optional statistics of the rounded output for a following BN (single
   // phase, Co % 8 == 0, no addend, and a kernel that takes them, see
-  // igemm_takes_stats): per 128-row tile b of the output rows and channel c, a
-  // shift K (the tile's first value) and the sums of (y - K) and (y - K)^2
-  // over its rows, at stat[(b * 3 + q) * Co + c], q = 0, 1, 2.
+  // igemm_takes_stats): nb = igemm_stat_records records; record j covers the
+  // 128-row tiles j, j + nb, j + 2nb, ... of the output rows and holds, per
+  // channel c, a shift K (one of its values) and the sums of (y - K) and
+  // (y - K)^2 over its rows, at stat[(j * 3 + q) * Co + c], q = 0, 1, 2.
   float* stat;
   int stat_nb;
   // N-tiles per group of the XCD-contiguous workgroup-to-tile order, or 0
@@ -85,6 +86,10 @@ hipError_t launch_stem(const IgemmArgs& a, hipStream_t st);
 // Whether the kernel launch_igemm picks for this problem can take the BN
 // statistics (IgemmArgs::stat) in its epilogue.
 bool igemm_takes_stats(const IgemmArgs& a);
+// The number of statistics records the kernel picked for this problem writes
+// (one per 128-row tile, or fewer where a workgroup sums several tiles);
+// never more than the tiles.
+int igemm_stat_records(const IgemmArgs& a);
 
 // Geometry of one stride phase (ph, pw) of the data gradient.  Output rows
 // h = ph + sh*i (i < Hph) receive exactly the taps r = r0 + sh*t (t < ntr)
@@ -176,7 +181,8 @@ hipError_t launch_bn_fwd(const BnArgs& a, const h16* x, const h16* gamma, const 
                          uint8_t* mout, hipStream_t st);
 size_t bn_keep_mask_bytes(const BnArgs& a);
 // Forward from the band records of a convolution epilogue (IgemmArgs::stat):
-// statistics, then the apply.  part: [nb][3][C] float32, 128 rows per record;
+// statistics, then the apply.  part: [nb][3][C] float32, record j over the
+// 128-row tiles j, j + nb, ...;
 // band_ws: bn_band_ws_bytes(C, nb) bytes of scratch for the per-slice sums.
 size_t bn_band_ws_bytes(int C, int nb);
 hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, void* band_ws,

@@ -40,6 +40,10 @@ CASES = [
     (5, 64, 56, 256, 1, 1, 0, 0.25, True, True, False),    # pointwise, many tiles per workgroup
     (6, 64, 212, 64, 1, 1, 0, 0.25, False, True, False),   # 2,107 tile records (ragged): the
                                                            # statistics take the sliced two-kernel path
+    (21, 64, 56, 256, 1, 1, 0, 0.25, True, True, False),   # pointwise: 515 tiles over 512 workgroup
+                                                           # records, the ragged last tile in record 2
+    (21, 128, 28, 512, 1, 1, 0, 0.25, True, True, False),  # pointwise over 128 channels: 129 tiles
+                                                           # over 128 records (tiles 0 and 128 in one)
 ]
 
 

@@ -149,7 +149,10 @@ def _check_op(net, op, H):
                             d.post_scale, bool(d.relu), want_dres=a["dres"] is not None,
                             swap=bool(d.swap),
                             residual=None if a["res"] is None else H[a["res"]])
-        _close(H[a["dx"]], ref["dx64"], what)
+        # binary16 output: entries within 1 ulp of the oracle's rounding pass
+        # where the largest (the max pool routes the stem's gradient to one
+        # input in four) sit far above the RMS
+        _close(H[a["dx"]], ref["dx64"], what, ref["dx"])
         _small_ok(H[a["dgamma"]], ref["dgamma"], ref["dgamma64"], what + " dgamma")
         _small_ok(H[a["dbeta"]], ref["dbeta"], ref["dbeta64"], what + " dbeta")
         if a["dres"] is not None:
