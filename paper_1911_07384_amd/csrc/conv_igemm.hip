@@ -704,7 +704,7 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
   constexpr int KS = K::KS, TN = K::TN, SW = K::SW;
   constexpr int SLOTS = 4 * SW;       // 16-byte chunks per staged pixel row
   constexpr int PPI = 64 / SLOTS;     // pixels per store instruction
-  static_assert(CI == 64 || CI == 128, "input channels");
+  static_assert(CI == 64 || CI == 128 || CI == 256, "input channels");
   static_assert(!(STATS && ADD), "statistics are taken without an addend");
   static_assert(ADD || !MASK, "a mask is over the addend");
   static_assert(TN % SW == 0, "store groups");
@@ -1613,15 +1613,36 @@ hipError_t launch_c3(const IgemmArgs& a, int tpi, hipStream_t st) {
   return hipGetLastError();
 }
 
-// workgroups along the rows of the pointwise kernel, which walk the 128-row
-// tiles: about six tiles each at ResNet-50's sizes, where the filter tile's
-// load into LDS is paid once per workgroup (batch 128, with statistics: the
-// conv2_x layer 56 us at 512 groups, 64-66 us at 256 or 1024; the conv3_x
-// layer on 128-channel tiles 51 us at 128 groups, 54-58 at 64 or 96, 64 at
-// 192 and 74 at 512)
-static int pw_row_groups(int ntiles, int ci, bool stats) {
-  const int cap = ci == 128 && stats ? 128 : 512;
+// workgroups along the rows of the pointwise kernel (nblk channel tiles),
+// which walk the 128-row tiles, the filter tile's load into LDS paid once per
+// workgroup.  Measured at batch 128: over 64 input channels 512 groups (the
+// conv2_x conv3 + bn3 56 us, 64-66 at 256 or 1024); over 128 with statistics
+// 128 groups on 4 channel tiles (51 us, 54-58 at 64 or 96, 64 at 192, 74 at
+// 512); over 256 about 256 workgroups in all, one per CU (the conv4_x conv3 +
+// bn3 on 8 channel tiles 75-78 us with 32 groups, 92-95 with 64, 117-123 with
+// 128; the strided conv3_x shortcut on 4 tiles 114 us with 64 groups, 131
+// with 128, 160 with 32)
+static int pw_row_groups(int ntiles, int ci, bool stats, int nblk) {
+  const int cap = ci == 256 ? (nblk > 1 ? (256 + nblk - 1) / nblk : 256)
+                            : ci == 128 && stats ? 128 : 512;
   return ntiles < cap ? ntiles : cap;
+}
+
+// channel tile of the pointwise kernel for this problem:
+//  - 64 input channels: 256, or 128 for the statistics variant on small grids
+//    (the conv2_x block's conv3 + bn3 at batch 32: 58.3 -> 56.5 us); at batch
+//    128, and without statistics, 256-channel tiles are faster;
+//  - 128: 256, and 128 with statistics (32 channels per lane and two waves
+//    per SIMD; 256-channel tiles with 64 per lane ran at one wave per SIMD,
+//    59-61 us against 51);
+//  - 256: 128 (a 64 KB filter tile).
+static int pw_tile_n(const IgemmArgs& a) {
+  if (a.Ci == 64) {
+    const bool narrow = a.stat && (int64_t)a.N * a.OH * a.OW <= 131072;
+    return a.Co >= 256 && !narrow ? 256 : 128;
+  }
+  if (a.Ci == 128) return a.stat ? 128 : 256;
+  return 128;
 }
 
 template <int CI, int BN>
@@ -1629,18 +1650,24 @@ hipError_t launch_pw(const IgemmArgs& a, hipStream_t st) {
   const int M = a.N * a.ph[0].Ho * a.ph[0].Wo;
   if (M == 0) return hipSuccess;
   const int ntiles = ceil_div(M, 128);
-  dim3 grid(pw_row_groups(ntiles, CI, a.stat != nullptr), ceil_div(a.Co, BN));
+  dim3 grid(pw_row_groups(ntiles, CI, a.stat != nullptr, ceil_div(a.Co, BN)), ceil_div(a.Co, BN));
   if (a.stat) {
     if constexpr (BN / (CI == 64 ? 8 : 4) <= 32)  // the lane's channels: see pw_kernel
       hipLaunchKernelGGL((pw_kernel<CI, BN, true, false, false>), grid, dim3(256), 0, st, a,
                          ntiles);
     else
       return hipErrorInvalidValue;
-  } else if (a.addend && a.amask)
-    hipLaunchKernelGGL((pw_kernel<CI, BN, false, true, true>), grid, dim3(256), 0, st, a, ntiles);
-  else if (a.addend)
-    hipLaunchKernelGGL((pw_kernel<CI, BN, false, true, false>), grid, dim3(256), 0, st, a, ntiles);
-  else
+  } else if (a.addend) {
+    if constexpr (CI < 256) {  // (igemm_kind takes no addend over 256 channels)
+      if (a.amask)
+        hipLaunchKernelGGL((pw_kernel<CI, BN, false, true, true>), grid, dim3(256), 0, st, a, ntiles);
+      else
+        hipLaunchKernelGGL((pw_kernel<CI, BN, false, true, false>), grid, dim3(256), 0, st, a,
+                           ntiles);
+    } else {
+      return hipErrorInvalidValue;
+    }
+  } else
     hipLaunchKernelGGL((pw_kernel<CI, BN, false, false, false>), grid, dim3(256), 0, st, a, ntiles);
   return hipGetLastError();
 }
@@ -1847,13 +1874,19 @@ enum class IgemmKind { kLds, kDirect, kDma, kPointwise, k3x3 };
 IgemmKind igemm_kind(const IgemmArgs& a) {
   if (c3_tiles_per_image(a) > 0) return IgemmKind::k3x3;
   {
-    // a 1x1 filter over 64 or 128 channels with a dense output of 128+
-    // channels: the pointwise kernel
+    // a 1x1 filter over 64 or 128 channels (or 256 without an addend) with a
+    // dense output of 128+ channels: the pointwise kernel.  (Over 256 channels
+    // its workgroups, one per CU walking a fixed share of the tiles, ran the
+    // conv4_x block inputs' data gradients 48 us against 58 alone, but 82-89
+    // against 66 in the training step, beside the weight gradients on the
+    // second stream: the register-direct kernel's one-tile workgroups share
+    // the CUs better.)
     const IgemmPhase& p = a.ph[0];
     const int64_t act = (int64_t)a.N * a.Hi * a.Wi * a.Ci * 2;
+    const bool ci_ok = a.Ci == 64 || a.Ci == 128 || (a.Ci == 256 && !a.addend);
     if (a.nphase == 1 && p.Rt == 1 && p.St == 1 && p.pad_h == 0 && p.pad_w == 0 &&
         p.oph == 0 && p.opw == 0 && a.os_h == 1 && a.os_w == 1 && a.OH == p.Ho &&
-        a.OW == p.Wo && (a.Ci == 64 || a.Ci == 128) && p.ldb == a.Ci && a.Co >= 128 &&
+        a.OW == p.Wo && ci_ok && p.ldb == a.Ci && a.Co >= 128 &&
         a.Co % 8 == 0 && a.ldo % 8 == 0 && act < ((int64_t)1 << 31))
       return IgemmKind::kPointwise;
   }
@@ -1898,7 +1931,9 @@ bool igemm_stats_pay(const IgemmArgs& a) {
 
 int igemm_stat_records(const IgemmArgs& a) {
   const int ntiles = ceil_div(a.N * a.ph[0].Ho * a.ph[0].Wo, 128);
-  return igemm_kind(a) == IgemmKind::kPointwise ? pw_row_groups(ntiles, a.Ci, true) : ntiles;
+  return igemm_kind(a) == IgemmKind::kPointwise
+             ? pw_row_groups(ntiles, a.Ci, true, ceil_div(a.Co, pw_tile_n(a)))
+             : ntiles;
 }
 
 bool igemm_takes_stats(const IgemmArgs& a) {
@@ -1925,18 +1960,12 @@ hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st) {
       return a.Co <= 64 ? launch_cfg4<1, 2>(a, st) : launch_cfg4<1, 4>(a, st);
     case IgemmKind::k3x3:
       return launch_c3(a, c3_tiles_per_image(a), st);
-    case IgemmKind::kPointwise:
-      if (a.Ci == 64) {
-        // 128-channel tiles for the statistics variant on small grids (the
-        // conv2_x block's conv3 + bn3 at batch 32: 58.3 -> 56.5 us); at batch
-        // 128, and without statistics, 256-channel tiles are faster
-        const bool narrow = a.stat && (int64_t)a.N * a.OH * a.OW <= 131072;
-        return a.Co >= 256 && !narrow ? launch_pw<64, 256>(a, st) : launch_pw<64, 128>(a, st);
-      }
-      // (statistics over 128 input channels: 128-channel tiles, 32 channels
-      // per lane and two waves per SIMD; 256-channel tiles with 64 per lane
-      // ran at one wave per SIMD, 59-61 us against 51)
-      return a.stat ? launch_pw<128, 128>(a, st) : launch_pw<128, 256>(a, st);
+    case IgemmKind::kPointwise: {
+      const bool wide = pw_tile_n(a) == 256;
+      if (a.Ci == 64) return wide ? launch_pw<64, 256>(a, st) : launch_pw<64, 128>(a, st);
+      if (a.Ci == 128) return wide ? launch_pw<128, 256>(a, st) : launch_pw<128, 128>(a, st);
+      return launch_pw<256, 128>(a, st);
+    }
     default:
       return a.Co <= 64 ? launch_cfg<128, 64, 4, 1, 64>(a, st) : launch_cfg<128, 128, 2, 2, 64>(a, st);
   }

@@ -51,6 +51,10 @@ SHAPES = [
     (3, 136, 9, 9, 64, 1, 1, 1, 0, "NHWC"),     # pointwise dgrad: 64 -> 136 channels (one 8-wide chunk
                                                 # in the second channel tile)
     (5, 64, 56, 56, 256, 1, 1, 1, 0, "NHWC"),   # pointwise fwd / dgrad over many tiles per workgroup
+    (2, 256, 14, 14, 384, 1, 1, 1, 0, "NHWC"),  # pointwise fwd over 256 channels, 3 channel tiles
+    (2, 136, 9, 9, 256, 1, 1, 1, 0, "NHWC"),    # pointwise dgrad over 256: 136 outputs (ragged tile)
+    (3, 256, 40, 40, 1024, 1, 1, 1, 0, "NHWC"), # pointwise over 256, 38 tiles on 32 row groups
+    (5, 256, 28, 28, 200, 1, 1, 2, 0, "NHWC"),  # strided pointwise fwd over 256, ragged channels
     # 3x3 stride 1 on the DMA-staged kernel at its edges:
     (2, 64, 31, 31, 128, 3, 3, 1, 1, "NHWC"),   # odd row width, one 64-channel k-block per tap
     (3, 192, 5, 9, 136, 3, 3, 1, 1, "NHWC"),    # three k-blocks per tap, ragged second N tile
@@ -168,7 +172,8 @@ def test_parity_full_size_sampled(shape, which):
 
 # (n, c, h, k): 1x1 stride-1 data gradients plus an addend (the bottleneck's
 # first convolution, whose input gradient joins the shortcut's)
-ADD_SHAPES = [(2, 256, 14, 64), (3, 136, 9, 64), (2, 64, 28, 64), (4, 256, 56, 64)]
+ADD_SHAPES = [(2, 256, 14, 64), (3, 136, 9, 64), (2, 64, 28, 64), (4, 256, 56, 64),
+              (2, 512, 14, 256), (3, 200, 20, 256), (3, 1024, 40, 256)]  # (256-long reductions)
 
 
 @pytest.mark.parametrize("shape", ADD_SHAPES, ids=["n{}c{}h{}k{}".format(*s) for s in ADD_SHAPES])

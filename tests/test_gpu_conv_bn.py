@@ -44,6 +44,10 @@ CASES = [
                                                            # records, the ragged last tile in record 2
     (21, 128, 28, 512, 1, 1, 0, 0.25, True, True, False),  # pointwise over 128 channels: 129 tiles
                                                            # over 128 records (tiles 0 and 128 in one)
+    (3, 256, 40, 1024, 1, 1, 0, 0.25, True, True, False),  # pointwise over 256: 38 tiles on 32 records
+    (2, 256, 14, 136, 1, 1, 0, 0.25, False, True, False),  # pointwise over 256, ragged channel tile
+    (4, 256, 28, 512, 1, 2, 0, 0.25, False, True, False),  # strided pointwise over 256 (the conv3_x
+                                                           # shortcut's shape)
 ]
 
 

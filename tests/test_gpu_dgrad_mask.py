@@ -30,6 +30,8 @@ CASES = [
     (2, 128, 14, 14, 256, 3, 2, 1),   # four stride phases, DMA-staged
     (2, 16, 9, 9, 24, 3, 1, 1),       # LDS-staged kernel (24 channels)
     (32, 256, 56, 56, 64, 1, 1, 0),   # the conv2_x block input gradient at batch 32
+    (2, 512, 14, 14, 256, 1, 1, 0),   # register-direct kernel, 256-long reduction
+    (3, 1024, 40, 40, 256, 1, 1, 0),  # ... over many tiles
 ]
 
 
@@ -87,6 +89,7 @@ STRIDED = [
     (2, 64, 14, 14, 64, 3, 2, 1, 2, False),     # stride phases of the data gradient itself
     (2, 256, 14, 14, 128, 1, 1, 0, 2, True),    # with a mask over the strided addend
     (2, 512, 10, 10, 256, 1, 1, 0, 2, True),
+    (3, 1024, 40, 40, 256, 1, 1, 0, 2, False),  # register-direct kernel over many tiles
     (32, 256, 56, 56, 128, 1, 1, 0, 2, False),  # the conv3_x block input gradient at batch 32
 ]
 
