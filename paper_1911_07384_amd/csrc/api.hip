@@ -90,6 +90,17 @@ ConvWs conv_ws(const ConvDims& d, int pass, int wg = 0) {
     return at;
   };
   const bool nchw = d.layout == FP16_NCHW;
+  // a 1x1 filter over 1x1 images (a classifier) is a dense GEMM; with few
+  // rows its reduction is split (float32 partials)
+  const bool dense = !nchw && d.H == 1 && d.W == 1 && d.R == 1 && d.S == 1 && d.ph == 0 &&
+                     d.pw == 0 && d.P == 1 && d.Q == 1;
+  if (pass == FP16_PASS_FWD && dense && d.Cp == d.C) {
+    L.splits = dense_gemm_splits(d.N, d.Cp, d.K);
+    if (L.splits > 1) L.part = take((size_t)L.splits * d.N * d.K * 4);
+  } else if (pass == FP16_PASS_DGRAD && dense && d.Kp == d.K) {
+    L.splits = dense_gemm_splits(d.N, d.Kp, d.C);
+    if (L.splits > 1) L.part = take((size_t)L.splits * d.N * d.C * 4);
+  }
   if (pass == FP16_PASS_FWD) {
     if (nchw || d.Cp != d.C) {
       L.need_x = L.need_w = true;
@@ -244,6 +255,10 @@ fp16_status fp16_conv_fwd(const fp16_conv_desc* desc, const fp16_t* x, const fp1
   a.Co = d.K; a.out = ye; a.OH = d.P; a.OW = d.Q; a.ldo = d.K; a.os_h = 1; a.os_w = 1;
   a.nphase = 1;
   a.ph[0] = IgemmPhase{we, d.R * d.S * d.Cp, d.R, d.S, d.ph, d.pw, d.P, d.Q, 0, 0};
+  if (L.splits > 1) {  // a dense GEMM with its reduction split
+    a.part = reinterpret_cast<float*>(static_cast<char*>(ws) + L.part);
+    a.splits = L.splits;
+  }
   TRY(launch_igemm(a, st));
   if (d.layout == FP16_NCHW) TRY(launch_nhwc_to_nchw(ye, reinterpret_cast<h16*>(y), d.N, d.K,
                                                      d.P * d.Q, d.K, st));
@@ -323,6 +338,10 @@ static fp16_status conv_dgrad_impl(const fp16_conv_desc* desc, const fp16_t* dy,
   a.addend = addend ? (d.layout == FP16_NCHW ? dxe : reinterpret_cast<const h16*>(addend)) : nullptr;
   a.amask = amask;
   a.astride = astride;
+  if (L.splits > 1 && !amask && astride == 1) {  // a dense GEMM with its reduction split
+    a.part = reinterpret_cast<float*>(static_cast<char*>(ws) + L.part);
+    a.splits = L.splits;
+  }
   a.nphase = 0;
   int64_t off = 0;
   for (int ph = 0; ph < d.sh; ++ph) {

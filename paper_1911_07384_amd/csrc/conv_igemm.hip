@@ -1944,7 +1944,100 @@ bool igemm_takes_stats(const IgemmArgs& a) {
   return igemm_kind(b) != IgemmKind::kLds;
 }
 
+// ---- dense GEMM with a split reduction ------------------------------------------
+// A 1x1 filter over 1x1 images is the plain GEMM out[m][n] = sum_k act[m][k]
+// filt[n][k] (m an image).  With few rows (a classifier's batch) its tiles are
+// too few for the CUs and each walks the whole reduction, so the reduction is
+// split: workgroup (M tile of 32, N tile of 128, split z) has four waves, one
+// 32 x 32 block each, which load both operands' MFMA fragments for k in
+// [z*kc, (z+1)*kc) straight from global memory (16 bytes per lane, all of
+// them in flight together) and store the float32 block to part[z].  A second kernel
+// adds the splits in order (then the addend) and rounds once.
+constexpr int kDenseKc = 256;  // reduction elements per split
+
+int dense_gemm_splits(int64_t M, int K, int Co) {
+  const int64_t tiles = ((M + 31) / 32) * ((Co + 127) / 128);
+  if (M > 512 || K < 2 * kDenseKc || tiles >= 128) return 0;
+  return (K + kDenseKc - 1) / kDenseKc;
+}
+
+__global__ __launch_bounds__(256) void dense_splitk_kernel(const IgemmArgs a) {
+  const int M = a.N, K = a.Ci;
+  const int tid = threadIdx.x;
+  const int wave = tid >> 6, lane = tid & 63;
+  const int lrow = lane & 31, lhi = lane >> 5;
+  const int m = blockIdx.x * 32 + lrow;
+  const int n = blockIdx.y * 128 + wave * 32 + lrow;
+  const int k0 = blockIdx.z * kDenseKc;
+  const int k1 = k0 + kDenseKc < K ? k0 + kDenseKc : K;
+  // range-checked buffer loads: a row past M or Co, or k past k1, reads
+  // zeros (K % 8 == 0: a lane's 8 elements are all inside or all past k1)
+  constexpr uint32_t OOB = 0x80000000u;
+  const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<h16*>(a.act), (short)0, (int)((int64_t)M * K * 2), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rs_b = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<h16*>(a.ph[0].filt), (short)0, (int)((int64_t)a.Co * a.ph[0].ldb * 2), 0x00020000);
+  const uint32_t a_row = m < M ? (uint32_t)m * (uint32_t)K * 2u : OOB;
+  const uint32_t b_row = n < a.Co ? (uint32_t)n * (uint32_t)a.ph[0].ldb * 2u : OOB;
+  // all of the split's operand fragments in flight at once, then its MFMAs
+  constexpr int KSTEPS = kDenseKc / 16;
+  half8 af[KSTEPS], bf[KSTEPS];
+#pragma unroll
+  for (int u = 0; u < KSTEPS; ++u) {
+    const int kk = k0 + 16 * u + 8 * lhi;
+    const uint32_t ko = (uint32_t)kk * 2u;
+    const bool ok = kk < k1;
+    af[u] = __builtin_bit_cast(half8, __builtin_amdgcn_raw_buffer_load_b128(
+                                          rs_a, ok && a_row != OOB ? a_row + ko : OOB, 0, 0));
+    bf[u] = __builtin_bit_cast(half8, __builtin_amdgcn_raw_buffer_load_b128(
+                                          rs_b, ok && b_row != OOB ? b_row + ko : OOB, 0, 0));
+  }
+  floatx16 acc;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) acc[e] = 0.0f;
+#pragma unroll
+  for (int u = 0; u < KSTEPS; ++u) acc = mfma32x32x16(af[u], bf[u], acc);
+  // lane: column n; rows 8*(e/4) + 4*lhi + e%4 of the M tile
+  if (n >= a.Co) return;
+  float* dst = a.part + (int64_t)blockIdx.z * M * a.Co + n;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) {
+    const int mr = blockIdx.x * 32 + 8 * (e >> 2) + 4 * lhi + (e & 3);
+    if (mr < M) dst[(int64_t)mr * a.Co] = acc[e];
+  }
+}
+
+__global__ __launch_bounds__(256) void dense_splitk_reduce(const IgemmArgs a) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t total = (int64_t)a.N * a.Co;
+  if (i >= total) return;
+  float v = 0.0f;
+  for (int z = 0; z < a.splits; ++z) v += a.part[z * total + i];
+  const int64_t m = i / a.Co, n = i - m * a.Co;
+  const int64_t off = m * a.ldo + n;
+  if (a.addend) v += to_f32(a.addend[off]);
+  a.out[off] = to_h16(v);
+}
+
+// whether launch_igemm runs this problem as a dense GEMM with a split
+// reduction (the caller provided part for a.splits splits)
+static bool dense_split_ok(const IgemmArgs& a) {
+  const IgemmPhase& p = a.ph[0];
+  return a.part && a.splits > 1 && !a.stat && !a.amask && a.astride <= 1 && a.nphase == 1 &&
+         a.Hi == 1 && a.Wi == 1 && p.Rt == 1 && p.St == 1 && p.pad_h == 0 && p.pad_w == 0 &&
+         p.Ho == 1 && p.Wo == 1 && a.OH == 1 && a.OW == 1 && p.oph == 0 && p.opw == 0 &&
+         a.Ci % 8 == 0 && p.ldb % 8 == 0 && a.splits == dense_gemm_splits(a.N, a.Ci, a.Co);
+}
+
 hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st) {
+  if (dense_split_ok(a)) {
+    const dim3 grid(ceil_div(a.N, 32), ceil_div(a.Co, 128), a.splits);
+    hipLaunchKernelGGL(dense_splitk_kernel, grid, dim3(256), 0, st, a);
+    const int64_t total = (int64_t)a.N * a.Co;
+    hipLaunchKernelGGL(dense_splitk_reduce, dim3((unsigned)((total + 255) / 256)), dim3(256), 0,
+                       st, a);
+    return hipGetLastError();
+  }
   switch (igemm_kind(a)) {
     case IgemmKind::kDma: {
       // two stages (two workgroups per CU) unless the grid fits the 256 CUs

@@ -70,7 +70,19 @@ struct IgemmArgs {
   // N-tiles per group of the XCD-contiguous workgroup-to-tile order, or 0
   // for the launch order (set by the launcher)
   int gn;
+  // Optional split of the reduction for a dense GEMM (a 1x1 filter over 1x1
+  // images, no statistics, no masked or strided addend; see
+  // dense_gemm_splits): float32 partial sums [splits][N][Co], summed in
+  // split order, the addend added, and rounded once by a second kernel.
+  float* part;
+  int splits;
 };
+
+// Reduction splits for a dense GEMM of M rows, a K-long reduction and Co
+// outputs (the classifier at batch 128: fc forward 128 x 2048 -> 1000, data
+// gradient 128 x 1000 -> 2048), or 0 where the GEMM runs whole: on tiles of
+// 32 x 128 the unsplit problem has too few workgroups to fill the CUs.
+int dense_gemm_splits(int64_t M, int K, int Co);
 
 hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st);
 // Whether taking the BN statistics in the convolution's epilogue is faster

@@ -33,6 +33,11 @@ SHAPES = [
     (2, 24, 9, 11, 40, 3, 3, 1, 1, "NHWC"),     # channels not a tile multiple
     (3, 16, 6, 5, 3, 3, 3, 1, 2, "NHWC"),       # 3 output channels, pad > R/2
     (4, 512, 1, 1, 200, 1, 1, 1, 0, "NHWC"),    # fully connected as a 1x1 on 1x1 images
+                                                # (forward: the reduction in two splits)
+    (128, 2048, 1, 1, 1000, 1, 1, 1, 0, "NHWC"),  # the ResNet-50 classifier: 8 splits forward,
+                                                  # 4 in the data gradient
+    (3, 1000, 1, 1, 600, 1, 1, 1, 0, "NHWC"),   # split reductions with a ragged last split,
+                                                # ragged row and channel tiles
     (1, 8, 1, 1, 8, 1, 1, 1, 0, "NHWC"),        # smallest case
     (2, 128, 7, 7, 128, 3, 3, 1, 1, "NHWC"),    # wide channels, tiny image
     (1, 16, 9, 9, 16, 3, 3, 3, 0, "NHWC"),      # stride 3 (9 dgrad phases)
@@ -173,7 +178,8 @@ def test_parity_full_size_sampled(shape, which):
 # (n, c, h, k): 1x1 stride-1 data gradients plus an addend (the bottleneck's
 # first convolution, whose input gradient joins the shortcut's)
 ADD_SHAPES = [(2, 256, 14, 64), (3, 136, 9, 64), (2, 64, 28, 64), (4, 256, 56, 64),
-              (2, 512, 14, 256), (3, 200, 20, 256), (3, 1024, 40, 256)]  # (256-long reductions)
+              (2, 512, 14, 256), (3, 200, 20, 256), (3, 1024, 40, 256),  # (256-long reductions)
+              (128, 2048, 1, 1000)]  # the classifier's data gradient, split reduction + addend
 
 
 @pytest.mark.parametrize("shape", ADD_SHAPES, ids=["n{}c{}h{}k{}".format(*s) for s in ADD_SHAPES])
