@@ -949,7 +949,7 @@ __global__ __launch_bounds__(kT) void bn_apply_maxpool_vec(const h16* __restrict
         for (int e = 0; e < 8; ++e) {
           const h16 z = to_h16(fwd_value(to_f32(xv[rr][ss].h[e]), k[e], false, 0.0f, true, false));
           const float f = to_f32(z);
-          const bool tk = in && (!started || pool_takes(best[e], f));
+          const bool tk = in & (!started | pool_takes(best[e], f));
           best[e] = tk ? f : best[e];
           win.h[e] = tk ? z : win.h[e];
           tap[e] = tk ? rr * S + ss : tap[e];

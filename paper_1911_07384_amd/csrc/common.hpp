@@ -66,7 +66,8 @@ __device__ __forceinline__ h16 dbl_to_h16(double d) {
 // only if it is strictly larger, or if it is the first NaN (NaN propagates;
 // ties keep the earliest position).
 __device__ __forceinline__ bool pool_takes(float best, float v) {
-  return !__builtin_isnan(best) && (__builtin_isnan(v) || v > best);
+  // (non-short-circuit: compare-and-select, no branch per element)
+  return !__builtin_isnan(best) & (__builtin_isnan(v) | (v > best));
 }
 
 // ReLU keeping NaN and mapping -0 and negatives to +0.

@@ -184,6 +184,8 @@ BN_POOL = [
     (2, 128, 9, 11, 2, 0, True, False),      # no padding, given statistics
     (2, 256, 5, 5, 3, 2, True, True),        # stride 3, pad 2; NaN, infinities and ties
     (2, 256, 20, 64, 2, 1, False, False),    # 32 channel chunks per pixel
+    (2, 256, 9, 7, 2, 1, True, True),        # the stride-2 column strips: NaN, infinities, ties
+    (2, 64, 35, 21, 2, 1, False, False),     # ragged last row strip (18 rows) and column strip
 ]
 
 
