@@ -994,6 +994,24 @@ static fp16_status conv_bn_impl(const fp16_conv_desc* conv, const fp16_bn_desc* 
   TRY(launch_igemm(a, st));
   void* band_ws = reinterpret_cast<char*>(part) +
                   align256((size_t)3 * d.K * a.stat_nb * sizeof(float));
+  IgemmArgs z2 = a;
+  z2.stat = nullptr;
+  if (b.layout == FP16_NHWC && igemm_takes_apply(z2)) {
+    // the statistics, then a second pass of the convolution that recomputes
+    // y bit for bit from x and writes z = the BN apply of it (with the
+    // shortcut and the kept ReLU mask) instead of reading y back
+    TRY(launch_bn_band_stats(b, part, a.stat_nb, band_ws, stats, st));
+    z2.out = reinterpret_cast<h16*>(z);
+    z2.bn_stats = stats;
+    z2.bn_gamma = gp;
+    z2.bn_beta = bp;
+    z2.bn_res = rp;
+    z2.bn_mask = mout;
+    z2.bn_scale = b.post_scale;
+    z2.bn_relu = b.relu;
+    z2.bn_swap = b.swap;
+    return hip_status(launch_igemm(z2, st));
+  }
   return hip_status(launch_bn_fwd_bands(b, part, a.stat_nb, band_ws,
                                         reinterpret_cast<const h16*>(y),
                                         reinterpret_cast<const h16*>(gamma),

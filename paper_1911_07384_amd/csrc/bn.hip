@@ -86,36 +86,6 @@ Plan make_plan(const BnArgs& a) {
   return p;
 }
 
-// Per-channel forward coefficients of the declared float32 apply sequence.
-struct FwdCoef {
-  float mean, a, b, sg;
-};
-__device__ __forceinline__ FwdCoef fwd_coef(const float* stats, const h16* gamma, const h16* beta,
-                                            int C, int c, float s) {
-  FwdCoef k;
-  k.mean = stats[c];
-  const float rstd = stats[C + c];
-  const float sg = s * to_f32(gamma[c]);
-  k.a = sg * rstd;
-  k.b = s * to_f32(beta[c]);
-  k.sg = sg;
-  return k;
-}
-
-__device__ __forceinline__ float fwd_value(float x, const FwdCoef& k, bool has_r, float r,
-                                           bool relu, bool swap) {
-  const float t = x - k.mean;
-  float v;
-  if (swap) {
-    v = __builtin_fmaf(t, k.a, __builtin_fmaf(k.sg, r, k.b));
-  } else {
-    v = __builtin_fmaf(t, k.a, k.b);
-    if (has_r) v = v + r;
-  }
-  if (relu) v = relu_keep_nan(v);
-  return v;
-}
-
 // Mask of the ReLU: from the stored output when given, else recomputed bit
 // for bit with the forward sequence.  The stored rne16(relu(v)) is positive
 // exactly when v > 2^-25 (smaller positive values round to +0, 2^-25 itself
@@ -1107,10 +1077,8 @@ size_t bn_band_ws_bytes(int C, int nb) {
   return align256((size_t)2 * C * ns * sizeof(double));
 }
 
-hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, void* band_ws,
-                               const h16* x, const h16* gamma, const h16* beta, const h16* res,
-                               h16* y, float* stats, uint8_t* mout, hipStream_t st) {
-  const Plan p = make_plan(a);
+hipError_t launch_bn_band_stats(const BnArgs& a, const float* part, int nb, void* band_ws,
+                                float* stats, hipStream_t st) {
   const Geo g = make_geo(a);
   if (nb <= kBandOne) {
     hipLaunchKernelGGL(bn_band_finalize, dim3(a.C), dim3(256), 0, st, part, nb, g, a.eps, stats);
@@ -1122,6 +1090,16 @@ hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, void*
     hipLaunchKernelGGL(bn_band_combine, dim3(a.C), dim3(64), 0, st, part, sl, ns, g, a.eps,
                        stats);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, void* band_ws,
+                               const h16* x, const h16* gamma, const h16* beta, const h16* res,
+                               h16* y, float* stats, uint8_t* mout, hipStream_t st) {
+  const Plan p = make_plan(a);
+  const Geo g = make_geo(a);
+  const hipError_t es = launch_bn_band_stats(a, part, nb, band_ws, stats, st);
+  if (es != hipSuccess) return es;
   if (p.vec) {
     const hipError_t e =
         launch_fwd_apply_vec(fwd_mode(a, res, mout != nullptr), p, g, x, gamma, beta, res, y, stats,

@@ -67,12 +67,45 @@ __device__ __forceinline__ h16 dbl_to_h16(double d) {
 // ties keep the earliest position).
 __device__ __forceinline__ bool pool_takes(float best, float v) {
   // (non-short-circuit: compare-and-select, no branch per element)
-  return !__builtin_isnan(best) & (__builtin_isnan(v) | (v > best));
+  return ((int)!__builtin_isnan(best) & ((int)__builtin_isnan(v) | (int)(v > best))) != 0;
 }
 
 // ReLU keeping NaN and mapping -0 and negatives to +0.
 __device__ __forceinline__ float relu_keep_nan(float v) {
   return (v > 0.0f || __builtin_isnan(v)) ? v : 0.0f;
+}
+
+// Per-channel forward coefficients of the BN apply's declared float32 sequence
+// (Section 4.1: normalise, scale by gamma and the post scale, add beta, then
+// the shortcut and the ReLU); shared by the BN kernels and the convolution
+// epilogue that applies the BN, so both give the same bits.
+struct FwdCoef {
+  float mean, a, b, sg;
+};
+__device__ __forceinline__ FwdCoef fwd_coef(const float* stats, const h16* gamma, const h16* beta,
+                                            int C, int c, float s) {
+  FwdCoef k;
+  k.mean = stats[c];
+  const float rstd = stats[C + c];
+  const float sg = s * to_f32(gamma[c]);
+  k.a = sg * rstd;
+  k.b = s * to_f32(beta[c]);
+  k.sg = sg;
+  return k;
+}
+
+__device__ __forceinline__ float fwd_value(float x, const FwdCoef& k, bool has_r, float r,
+                                           bool relu, bool swap) {
+  const float t = x - k.mean;
+  float v;
+  if (swap) {
+    v = __builtin_fmaf(t, k.a, __builtin_fmaf(k.sg, r, k.b));
+  } else {
+    v = __builtin_fmaf(t, k.a, k.b);
+    if (has_r) v = v + r;
+  }
+  if (relu) v = relu_keep_nan(v);
+  return v;
 }
 
 // Transpose an 8x8 block of binary16 values held as eight 16-byte rows:

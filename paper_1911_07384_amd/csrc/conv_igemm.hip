@@ -668,7 +668,7 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
 //    (64 would leave one wave per SIMD).
 // Each output element is the same k-ordered sum of exact products in both
 // MFMA forms, so the values equal the other kernels' bit for bit.
-template <int CI, int BN, bool STATS, bool ADD>
+template <int CI, int BN, bool STATS, bool ADD, bool APPLY = false>
 struct CfgPw {
   static constexpr int KS = CI / 16;          // k sub-steps of 16 channels
   static constexpr int TN = BN / 32;          // 32-channel tiles
@@ -680,7 +680,9 @@ struct CfgPw {
   static constexpr int BST = STATS ? 4 * 3 * BN * 4 : 0;  // [wave][K, s1, s2][BN]
   static constexpr int SHARED = STG > BST ? STG : BST;
   // (+ 4 wave row counts and the waves' shifts, [wave][BN] binary16)
-  static constexpr int LDS = BBYTES + SHARED + (STATS ? 16 + 4 * BN * 2 : 0);
+  static constexpr int XTRA = STATS ? 16 + 4 * BN * 2 : 0;
+  // (+ the BN apply's coefficients: [BN] x {mean, a, b, sg})
+  static constexpr int LDS = BBYTES + SHARED + XTRA + (APPLY ? BN * 16 : 0);
 };
 
 __device__ __forceinline__ void lane_half_swap(float& x, float& y) {
@@ -698,15 +700,19 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-template <int CI, int BN, bool STATS, bool ADD, bool MASK>
+template <int CI, int BN, bool STATS, bool ADD, bool MASK, bool APPLY = false, bool RES = false>
 __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) {
-  using K = CfgPw<CI, BN, STATS, ADD>;
+  using K = CfgPw<CI, BN, STATS, ADD, APPLY>;
   constexpr int KS = K::KS, TN = K::TN, SW = K::SW;
   constexpr int SLOTS = 4 * SW;       // 16-byte chunks per staged pixel row
   constexpr int PPI = 64 / SLOTS;     // pixels per store instruction
   static_assert(CI == 64 || CI == 128 || CI == 256, "input channels");
   static_assert(!(STATS && ADD), "statistics are taken without an addend");
   static_assert(ADD || !MASK, "a mask is over the addend");
+  static_assert(!APPLY || (!STATS && !ADD), "the BN apply follows the statistics pass");
+  static_assert(APPLY || !RES, "the shortcut joins in the BN apply");
+  // the early loads in the store layout: the addend, or the apply's shortcut
+  constexpr bool EARLY = ADD || RES;
   static_assert(TN % SW == 0, "store groups");
   constexpr int NG = TN / SW;         // store groups
   static_assert(!STATS || NG * 8 <= 32, "statistics: at most 32 channels per lane");
@@ -726,6 +732,19 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
   char* stg = shared + wave * 32 * SLOTS * (ADD ? 32 : 16);
   // the wave's shifts: channel n0 + i at kst[i]
   h16* kst = reinterpret_cast<h16*>(lds + K::BBYTES + K::SHARED + 16) + wave * BN;
+  // the BN apply's coefficients of channel n0 + i at cof[i]
+  float4* cof = reinterpret_cast<float4*>(lds + K::BBYTES + K::SHARED + K::XTRA);
+  const h16* early = ADD ? a.addend : a.bn_res;
+  if (APPLY) {
+    for (int i = tid; i < BN; i += 256) {
+      float4 q = make_float4(0.0f, 0.0f, 0.0f, 0.0f);
+      if (n0 + i < a.Co) {
+        const FwdCoef k = fwd_coef(a.bn_stats, a.bn_gamma, a.bn_beta, a.Co, n0 + i, a.bn_scale);
+        q = make_float4(k.mean, k.a, k.b, k.sg);
+      }
+      cof[i] = q;
+    }
+  }
   constexpr uint32_t OOB = 0x80000000u;
   const int act_bytes = (int)((int64_t)a.N * a.Hi * a.Wi * CI * 2);
   const __amdgpu_buffer_rsrc_t rs_a = __builtin_amdgcn_make_buffer_rsrc(
@@ -785,10 +804,10 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
     // chunk lane % SLOTS of pixel lane / SLOTS + PPI*i; clamped into range)
     // (and with MASK the addend's ReLU mask bytes, applied where it is added)
     // (a strided addend: the row of each of the lane's pixels, or +0)
-    V8 adv[ADD ? TN / SW : 1][ADD ? 32 / PPI : 1];
+    V8 adv[EARLY ? TN / SW : 1][EARLY ? 32 / PPI : 1];
     uint32_t amb[MASK ? TN / SW : 1][MASK ? 32 / PPI : 1];
-    bool aok[ADD ? 32 / PPI : 1];
-    if (ADD) {
+    bool aok[EARLY ? 32 / PPI : 1];
+    if (EARLY) {
       int64_t arow[32 / PPI];
 #pragma unroll
       for (int i = 0; i < 32 / PPI; ++i) {
@@ -796,7 +815,7 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
         const int mc = m < M ? m : M - 1;
         arow[i] = (int64_t)mc * a.ldo;
         aok[i] = true;
-        if (a.astride > 1) {
+        if (ADD && a.astride > 1) {
           const int img = mc / HoWo;
           const int rem = mc - img * HoWo;
           const int oh = rem / ph.Wo;
@@ -811,7 +830,7 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
         for (int i = 0; i < 32 / PPI; ++i) {
           const int n = n0 + g * SW * 32 + (lane % SLOTS) * 8;
           const int64_t off = arow[i] + (n < a.Co ? n : 0);
-          adv[g][i] = load16(a.addend + off);
+          adv[g][i] = load16(early + off);
           if (MASK) amb[g][i] = a.amask[off >> 3];
         }
     }
@@ -874,6 +893,11 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
       const int c = lane % SLOTS;
       const int n = n0 + g * SW * 32 + c * 8;
       V8 kv;
+      float4 cf[APPLY ? 8 : 1];
+      if (APPLY) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) cf[e] = cof[g * SW * 32 + c * 8 + e];
+      }
       if (STATS) {
         if (first) {
           // the shifts: the values of the wave's first row (staged pixel 0)
@@ -907,7 +931,23 @@ __global__ __launch_bounds__(256) void pw_kernel(const IgemmArgs a, int ntiles) 
           o = *reinterpret_cast<const V8*>(stg + (q * SLOTS + (c ^ (q & (SLOTS - 1)))) * 16);
         }
         const int m = band_m0 + q;
-        if (m < M && n < a.Co) store16(a.out + (int64_t)m * a.ldo + n, o);
+        uint32_t zbits = 0;
+        if (APPLY) {
+          // z from the rounded y with the BN apply's float32 sequence (the
+          // shortcut and ReLU per the flags), and its ReLU mask bits
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float4 q4 = cf[e];
+            const FwdCoef k{q4.x, q4.y, q4.z, q4.w};
+            o.h[e] = to_h16(fwd_value(to_f32(o.h[e]), k, RES, RES ? to_f32(adv[g][i].h[e]) : 0.0f,
+                                      a.bn_relu != 0, a.bn_swap != 0));
+            zbits |= (uint32_t)(to_f32(o.h[e]) > 0.0f) << e;
+          }
+        }
+        if (m < M && n < a.Co) {
+          store16(a.out + (int64_t)m * a.ldo + n, o);
+          if (APPLY && a.bn_mask) a.bn_mask[((int64_t)m * a.ldo + n) >> 3] = (uint8_t)zbits;
+        }
         if (STATS && m < M) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
@@ -1651,7 +1691,14 @@ hipError_t launch_pw(const IgemmArgs& a, hipStream_t st) {
   if (M == 0) return hipSuccess;
   const int ntiles = ceil_div(M, 128);
   dim3 grid(pw_row_groups(ntiles, CI, a.stat != nullptr, ceil_div(a.Co, BN)), ceil_div(a.Co, BN));
-  if (a.stat) {
+  if (a.bn_stats) {
+    if (a.bn_res)
+      hipLaunchKernelGGL((pw_kernel<CI, BN, false, false, false, true, true>), grid, dim3(256), 0,
+                         st, a, ntiles);
+    else
+      hipLaunchKernelGGL((pw_kernel<CI, BN, false, false, false, true, false>), grid, dim3(256), 0,
+                         st, a, ntiles);
+  } else if (a.stat) {
     if constexpr (BN / (CI == 64 ? 8 : 4) <= 32)  // the lane's channels: see pw_kernel
       hipLaunchKernelGGL((pw_kernel<CI, BN, true, false, false>), grid, dim3(256), 0, st, a,
                          ntiles);
@@ -1929,6 +1976,15 @@ bool igemm_stats_pay(const IgemmArgs& a) {
   return !(igemm_kind(b) == IgemmKind::kDma && (int64_t)a.N * a.OH * a.OW >= 100352);
 }
 
+bool igemm_takes_apply(const IgemmArgs& a) {
+  // the pointwise kernel over 64 input channels: a second pass that
+  // recomputes y from x (a quarter of y's bytes) and writes z in place of the
+  // BN apply's read of y
+  IgemmArgs b = a;
+  b.stat = nullptr;
+  return !a.addend && !a.amask && a.Ci == 64 && igemm_kind(b) == IgemmKind::kPointwise;
+}
+
 int igemm_stat_records(const IgemmArgs& a) {
   const int ntiles = ceil_div(a.N * a.ph[0].Ho * a.ph[0].Wo, 128);
   return igemm_kind(a) == IgemmKind::kPointwise
@@ -2023,13 +2079,15 @@ __global__ __launch_bounds__(256) void dense_splitk_reduce(const IgemmArgs a) {
 // reduction (the caller provided part for a.splits splits)
 static bool dense_split_ok(const IgemmArgs& a) {
   const IgemmPhase& p = a.ph[0];
-  return a.part && a.splits > 1 && !a.stat && !a.amask && a.astride <= 1 && a.nphase == 1 &&
+  return a.part && a.splits > 1 && !a.stat && !a.bn_stats && !a.amask && a.astride <= 1 &&
+         a.nphase == 1 &&
          a.Hi == 1 && a.Wi == 1 && p.Rt == 1 && p.St == 1 && p.pad_h == 0 && p.pad_w == 0 &&
          p.Ho == 1 && p.Wo == 1 && a.OH == 1 && a.OW == 1 && p.oph == 0 && p.opw == 0 &&
          a.Ci % 8 == 0 && p.ldb % 8 == 0 && a.splits == dense_gemm_splits(a.N, a.Ci, a.Co);
 }
 
 hipError_t launch_igemm(const IgemmArgs& a, hipStream_t st) {
+  if (a.bn_stats && (a.stat || !igemm_takes_apply(a))) return hipErrorInvalidValue;
   if (dense_split_ok(a)) {
     const dim3 grid(ceil_div(a.N, 32), ceil_div(a.Co, 128), a.splits);
     hipLaunchKernelGGL(dense_splitk_kernel, grid, dim3(256), 0, st, a);

@@ -76,6 +76,19 @@ struct IgemmArgs {
   // split order, the addend added, and rounded once by a second kernel.
   float* part;
   int splits;
+  // Optional BN apply in the epilogue (the pointwise kernel; see
+  // igemm_takes_apply): out receives z, the declared float32 apply of the
+  // rounded convolution output y with the statistics bn_stats (mean [Co],
+  // 1/sqrt(var + eps) [Co]), bn_gamma, bn_beta, bn_scale, the shortcut bn_res
+  // (nullable), the BN swap and the ReLU, instead of y; bn_mask (nullable)
+  // keeps z's ReLU mask, one byte per 8 channels (bit e = [z element e > 0]).
+  const float* bn_stats;
+  const h16* bn_gamma;
+  const h16* bn_beta;
+  const h16* bn_res;
+  uint8_t* bn_mask;
+  float bn_scale;
+  int bn_relu, bn_swap;
 };
 
 // Reduction splits for a dense GEMM of M rows, a K-long reduction and Co
@@ -98,6 +111,9 @@ hipError_t launch_stem(const IgemmArgs& a, hipStream_t st);
 // Whether the kernel launch_igemm picks for this problem can take the BN
 // statistics (IgemmArgs::stat) in its epilogue.
 bool igemm_takes_stats(const IgemmArgs& a);
+// Whether launch_igemm can apply a following BN in the epilogue of this
+// problem (IgemmArgs::bn_stats; the problem without stats, addend or mask).
+bool igemm_takes_apply(const IgemmArgs& a);
 // The number of statistics records the kernel picked for this problem writes
 // (one per 128-row tile, or fewer where a workgroup sums several tiles);
 // never more than the tiles.
@@ -197,6 +213,9 @@ size_t bn_keep_mask_bytes(const BnArgs& a);
 // 128-row tiles j, j + nb, ...;
 // band_ws: bn_band_ws_bytes(C, nb) bytes of scratch for the per-slice sums.
 size_t bn_band_ws_bytes(int C, int nb);
+// The statistics alone from such records (mean [C], 1/sqrt(var + eps) [C]).
+hipError_t launch_bn_band_stats(const BnArgs& a, const float* part, int nb, void* band_ws,
+                                float* stats, hipStream_t st);
 hipError_t launch_bn_fwd_bands(const BnArgs& a, const float* part, int nb, void* band_ws,
                                const h16* x, const h16* gamma, const h16* beta, const h16* res,
                                h16* y, float* stats, uint8_t* mout, hipStream_t st);

@@ -44,6 +44,9 @@ CASES = [
                                                            # records, the ragged last tile in record 2
     (21, 128, 28, 512, 1, 1, 0, 0.25, True, True, False),  # pointwise over 128 channels: 129 tiles
                                                            # over 128 records (tiles 0 and 128 in one)
+    (2, 64, 20, 192, 1, 1, 0, 0.25, True, False, False),  # pointwise over 64, its second pass
+                                                           # applying the BN: no ReLU, ragged tile
+    (3, 64, 9, 256, 1, 1, 0, 0.25, False, True, False),    # ... no shortcut, ragged rows
     (3, 256, 40, 1024, 1, 1, 0, 0.25, True, True, False),  # pointwise over 256: 38 tiles on 32 records
     (2, 256, 14, 136, 1, 1, 0, 0.25, False, True, False),  # pointwise over 256, ragged channel tile
     (4, 256, 28, 512, 1, 2, 0, 0.25, False, True, False),  # strided pointwise over 256 (the conv3_x
@@ -111,3 +114,35 @@ def test_conv_bn_in_place_output():
     F.fp16_conv_bn_relu_fwd(cd, bd, dev(x), dev(w), dev(g), dev(b), None, Y2, Y2, S, ws)
     torch.cuda.synchronize()
     assert torch.equal(Y2.view(torch.int16), Z.view(torch.int16))
+
+
+@pytest.mark.parametrize("alias", ["z_is_y", "z_is_residual"])
+def test_conv_bn_pointwise_in_place(alias):
+    # the pointwise kernel over 64 channels applies the BN in a second pass
+    # that recomputes y from x: z may still be y, or the shortcut it reads
+    require_gpu()
+    n, c, h, k = 2, 64, 28, 256
+    cd = F.conv_desc(n, c, h, h, k, 1, 1, 1, 0)
+    bd = F.bn_desc(n, k, h, h, "NHWC", EPS, 0.25, True)
+    x = synth.normal_f16((n, h, h, c), 1.0, 71, 1)
+    w = synth.normal_f16((k, 1, 1, c), synth.he_std(c), 71, 2)
+    g = synth.normal_f16((k,), 0.3, 71, 3, mean=1.0)
+    b = synth.normal_f16((k,), 0.3, 71, 4)
+    r = synth.normal_f16((n, h, h, k), 1.0, 71, 5)
+    ws = F.workspace(F.fp16_conv_bn_workspace_bytes(cd, bd))
+    Y = torch.empty((n, h, h, k), dtype=torch.float16, device="cuda")
+    Z = torch.empty_like(Y)
+    S = torch.empty(2 * k, dtype=torch.float32, device="cuda")
+    note(f"[gpu] conv_bn pointwise in place {alias}")
+    F.fp16_conv_bn_relu_fwd(cd, bd, dev(x), dev(w), dev(g), dev(b), dev(r), Y, Z, S, ws)
+    Y2 = torch.empty_like(Y)
+    R2 = dev(r)
+    if alias == "z_is_y":
+        F.fp16_conv_bn_relu_fwd(cd, bd, dev(x), dev(w), dev(g), dev(b), R2, Y2, Y2, S, ws)
+        out = Y2
+    else:
+        F.fp16_conv_bn_relu_fwd(cd, bd, dev(x), dev(w), dev(g), dev(b), R2, Y2, R2, S, ws)
+        out = R2
+        assert torch.equal(Y2.view(torch.int16), Y.view(torch.int16))
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), Z.view(torch.int16))
