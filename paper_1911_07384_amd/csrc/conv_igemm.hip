@@ -32,14 +32,16 @@
 //                    MFMA operands read one k sub-step ahead.  Needs
 //                    Ci % 64 == 0; wins on the long reductions (every 3x3
 //                    layer).
-//   pw_kernel     -- 1x1 filters with 64 or 128 input channels and a dense
-//                    output of 128+ channels (bound by the output's bytes):
-//                    the filter tile stays in LDS, each workgroup walks over
-//                    128-row tiles, and the MFMA operands are swapped so that
-//                    the accumulators hold the transposed tile; lane-pair
-//                    swaps (v_permlane32_swap) then give each lane 8
-//                    consecutive channels of one output pixel, written
-//                    straight from registers.
+//   pw_kernel     -- 1x1 filters with 64 or 128 input channels (or 256
+//                    without an addend) and a dense output of 128+ channels
+//                    (bound by the output's bytes): the filter tile stays in
+//                    LDS, each workgroup walks over 128-row tiles, and the
+//                    MFMA operands are swapped so that the accumulators hold
+//                    the transposed tile; lane-pair swaps (v_permlane32_swap)
+//                    then give each lane 8 consecutive channels of one output
+//                    pixel, staged through LDS into whole-line stores.  Its
+//                    epilogue can take the following BN's statistics, or
+//                    (a second pass) apply that BN to the recomputed output.
 //
 // Epilogue (the first three): each wave stages a 32-row band of its float32
 // tile in LDS and writes whole output rows with 16-byte stores.  Every value is rounded
@@ -664,8 +666,8 @@ __global__ __launch_bounds__(256) void igemm4_kernel(const IgemmArgs a) {
 //    tile the lanes holding the same channels are added up, and the four
 //    waves are combined once into one record covering the tiles blockIdx.x,
 //    blockIdx.x + gridDim.x, ... (no barrier per tile).  A lane holds
-//    BN / 8 channels over 64 input channels and BN / 4 over 128: at most 32
-//    (64 would leave one wave per SIMD).
+//    BN / 8 channels over 64 input channels and BN / 4 over 128 or 256: at
+//    most 32 (64 would leave one wave per SIMD).
 // Each output element is the same k-ordered sum of exact products in both
 // MFMA forms, so the values equal the other kernels' bit for bit.
 template <int CI, int BN, bool STATS, bool ADD, bool APPLY = false>
