@@ -1660,13 +1660,26 @@ hipError_t launch_c3(const IgemmArgs& a, int tpi, hipStream_t st) {
 // workgroup.  Measured at batch 128: over 64 input channels 512 groups (the
 // conv2_x conv3 + bn3 56 us, 64-66 at 256 or 1024); over 128 with statistics
 // 128 groups on 4 channel tiles (51 us, 54-58 at 64 or 96, 64 at 192, 74 at
-// 512); over 256 about 256 workgroups in all, one per CU (the conv4_x conv3 +
+// 512), without them about six tiles per group (the conv3_x block inputs'
+// data gradients with the masked addend: 784 tiles, 128 groups on 2 channel
+// tiles 64-67 us against 75 at 512; the conv3_x block's own, 3,136 tiles on
+// one channel tile: 85 us at 512 groups, 91 at 256, 145 at 128); over 256
+// about 256 workgroups in all, one per CU (the conv4_x conv3 +
 // bn3 on 8 channel tiles 75-78 us with 32 groups, 92-95 with 64, 117-123 with
 // 128; the strided conv3_x shortcut on 4 tiles 114 us with 64 groups, 131
 // with 128, 160 with 32)
 static int pw_row_groups(int ntiles, int ci, bool stats, int nblk) {
-  const int cap = ci == 256 ? (nblk > 1 ? (256 + nblk - 1) / nblk : 256)
-                            : ci == 128 && stats ? 128 : 512;
+  int cap = ci == 256 ? (nblk > 1 ? (256 + nblk - 1) / nblk : 256)
+                      : ci == 128 && stats ? 128 : 512;
+  // over 128 channels without statistics: about six tiles per workgroup, the
+  // workgroups in all a whole multiple of the 256 CUs (each walks its tiles
+  // to the end: 262 of them left six CUs with a second, 90 us against 66)
+  if (ci == 128 && !stats) {
+    const int want = (ntiles + 5) / 6 < cap ? (ntiles + 5) / 6 : cap;
+    const int total = want * nblk;
+    cap = total >= 256 ? (total / 256) * 256 / nblk : want;
+    if (cap < 1) cap = 1;
+  }
   return ntiles < cap ? ntiles : cap;
 }
 
